@@ -1,0 +1,186 @@
+/*
+ * libspyke.h -- C ABI of the MI355X (gfx950) hot path for convolutional
+ * spiking networks with at most one spike per neuron (Mozafari et al.,
+ * "SpykeTorch", Frontiers in Neuroscience 2019).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensor arguments are DEVICE pointers owned by the caller, contiguous,
+ *   row-major and batch-major.  The library never allocates or frees caller
+ *   memory; scratch space comes from a caller-provided device `workspace`
+ *   whose size the matching *_workspace_size() function returns (a NULL
+ *   workspace is accepted when that size is 0).
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   All work is enqueued asynchronously on it; no call synchronises the host.
+ * - Spike waves are u8 [B][T][C][H][W] holding 0/1, cumulative in t
+ *   (the paper's Eq.1: S[t] = 1 from the first-spike step on).  First-spike
+ *   maps are u8 [B][C][H][W] with the value T meaning "never spiked" (the
+ *   paper's infinity).  Hence T <= 255.
+ * - A neuron's linear index inside one image is c*H*W + y*W + x.
+ * - Every function returns an int status.  Arguments are validated on the
+ *   host before anything is enqueued; on an error nothing is launched,
+ *   outputs are untouched, and spk_last_error() (thread-local) describes it.
+ *   An asynchronous device fault surfaces at the caller's next synchronisation.
+ * - Entry points are stateless and re-entrant; calls on different streams
+ *   may run concurrently as long as their buffers do not overlap.
+ */
+#ifndef LIBSPYKE_H
+#define LIBSPYKE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define SPK_API __attribute__((visibility("default")))
+#else
+#define SPK_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    SPK_OK = 0,
+    SPK_E_ARG = 1,        /* NULL where a buffer is required, or a bad flag  */
+    SPK_E_SHAPE = 2,      /* non-positive or inconsistent sizes              */
+    SPK_E_RANGE = 3,      /* a size beyond a documented limit (T > 255, ...) */
+    SPK_E_WORKSPACE = 4,  /* workspace smaller than *_workspace_size()       */
+    SPK_E_INPUT = 5,      /* bad values in a host-side argument              */
+    SPK_E_HIP = 6         /* a HIP launch or runtime call failed             */
+};
+
+/* Library version, (major << 16) | (minor << 8) | patch. */
+SPK_API int spk_version(void);
+
+/* Message of the last failing call on this thread ("" if none). */
+SPK_API const char *spk_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Intensity-to-latency encoding (paper, section "utils Module": Filter,
+ * DoGKernel/GaborKernel and Intensity2Latency; threshold as in the
+ * "functional Module").
+ *   image       u8  [B][H][W], pixel values 0..255.
+ *   filters     f32 [C][KF][KF], KF odd, KF <= 31; same-size
+ *               cross-correlation (no kernel flip), zero outside the image.
+ *   intensities f32 [B][C][H][W] or NULL: filter response, with values
+ *               below filter_threshold set to 0.  Accumulated in double and
+ *               rounded once to float.
+ *   t_first     u8  [B][C][H][W] or NULL: rank-order latency.  Per image,
+ *               the n positive intensities of all channels are ranked from
+ *               largest to smallest (equal values by ascending linear index)
+ *               and the entry of rank rho spikes at floor(rho*T/n); other
+ *               entries never spike (value T).
+ *   wave        u8  [B][T][C][H][W] or NULL: Eq.1 wave of t_first.
+ * Limits: 1 <= T <= 255, C*H*W < 2^31, (8 + KF - 1) * W <= 65536.
+ * Workspace: spk_encode_latency_workspace_size(B, C, H, W, T) bytes.      */
+SPK_API size_t spk_encode_latency_workspace_size(int B, int C, int H, int W, int T);
+SPK_API int spk_encode_latency(const uint8_t *image, int B, int H, int W,
+                       const float *filters, int C, int KF, float filter_threshold, int T,
+                       uint8_t *wave, uint8_t *t_first, float *intensities,
+                       void *workspace, size_t ws_bytes, void *stream);
+
+/* Eq.1: wave u8 [B][T][C][H][W] from first-spike times u8 [B][C][H][W]
+ * (values >= T never spike).  1 <= T <= 255.                               */
+SPK_API int spk_expand_wave(const uint8_t *t_first, int B, int T, int C, int H, int W,
+                    uint8_t *wave, void *stream);
+
+/* Checks Eq.1's structure: writes to *bad_count (device i32) the number of
+ * neurons whose entries are not 0/1 or decrease in t.                      */
+SPK_API int spk_validate_wave(const uint8_t *wave, int B, int T, int C, int H, int W,
+                      int32_t *bad_count, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Convolution + firing (section "snn Module", Eq.2; firing from the
+ * "functional Module"; infinite-threshold in-place firing, Eq.5).
+ *   wave       u8  [B][T][Cin][H][W], a valid cumulative spike wave
+ *              (the result is defined through its first-spike times).
+ *   weight     f32 [Cout][Cin][K][K], finite, |w| < 65504.
+ *   pad        zero padding of the input (padded neurons never spike);
+ *              Ho = H + 2*pad - K + 1, Wo = W + 2*pad - K + 1 (stride 1).
+ *   threshold  finite: spike at step t iff P[t] >= threshold;
+ *              +INFINITY: Eq.5 -- P[t] = 0 for t < T-1, spike only at
+ *              t = T-1 and only where P[T-1] > 0.
+ *   potentials f32 [B][T][Cout][Ho][Wo] or NULL:
+ *              P[t,f,y,x] = sum over (ci,ky,kx) of W[f,ci,ky,kx] * S[t,ci,y+ky-pad,x+kx-pad].
+ *              Computed on fp16 matrix cores from an exact two-term split of
+ *              each weight (relative weight error <= 2^-22) with float
+ *              accumulation.
+ *   spikes     u8  [B][T][Cout][Ho][Wo] or NULL: 1 where the neuron fires.
+ *   t_first    u8  [B][Cout][Ho][Wo]: first firing step, T if silent.
+ *   v_first    f32 [B][Cout][Ho][Wo]: potential at t_first, 0 if silent.
+ * Limits: 1 <= T <= 255, Ho, Wo >= 1, Cin*K*K <= 65536.
+ * Workspace: spk_conv_fire_workspace_size(...) bytes.                      */
+SPK_API size_t spk_conv_fire_workspace_size(int B, int T, int Cin, int H, int W, int Cout, int K, int pad);
+SPK_API int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, int W,
+                  const float *weight, int Cout, int K, int pad, float threshold,
+                  float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
+                  void *workspace, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Spike max-pooling (section "snn Module", Eq.3): on a spike wave each
+ * window yields its earliest spike.  Window `kernel`, stride `stride`,
+ * zero padding `pad`; Ho = floor((H + 2*pad - kernel)/stride) + 1.
+ *   out_wave    u8 [B][T][C][Ho][Wo]
+ *   out_t_first u8 [B][C][Ho][Wo] or NULL (T where the window never spikes). */
+SPK_API int spk_pool(const uint8_t *wave, int B, int T, int C, int H, int W,
+             int kernel, int stride, int pad,
+             uint8_t *out_wave, uint8_t *out_t_first, void *stream);
+
+/* ------------------------------------------------------------------------
+ * k winners-take-all with feature-wise and lateral inhibition (sections
+ * "snn Module" and "functional Module": get_k_winners).  Eligible neurons
+ * have t_first < T.  Up to k times: the eligible, uninhibited neuron with
+ * the earliest t_first, then the largest v_first, then the lowest linear
+ * index wins; its whole feature map is inhibited, and so is every position
+ * within Chebyshev distance `radius` of it in all maps.
+ *   winners   i32 [B][k][4] = (feature, t, y, x) in selection order,
+ *             rows beyond the count filled with -1.
+ *   n_winners i32 [B].
+ * Limits: C*H*W <= 2^24, H*W <= 65536, 1 <= k, 0 <= radius, T <= 255.
+ * Workspace: spk_kwta_workspace_size(B, C, H, W) bytes.                    */
+SPK_API size_t spk_kwta_workspace_size(int B, int C, int H, int W);
+SPK_API int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int T, int C, int H, int W,
+             int k, int radius, int32_t *winners, int32_t *n_winners,
+             void *workspace, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * STDP (Eq.4) on the winners' weights, in place.  For winner
+ * (f, t_i, y, x) of image b and synapse (ci, ky, kx), the pre-synaptic
+ * neuron is (ci, y+ky-pad, x+kx-pad) of the layer input; it counts as
+ * T_j <= T_i when pre_wave[b][t_i] is 1 there (padding never spikes).
+ *   dW = A * (W - lb) * (ub - W), A = a_plus if T_j <= T_i else a_minus;
+ * with stabilizer == 0 the product term is 1.  W is clamped to [lb, ub].
+ * Batches use frozen-forward, ordered replay: the winners of image 0 are
+ * applied first, then image 1, and so on; one image's winners use distinct
+ * features, so their order does not matter.  The update of each weight is
+ * evaluated in double precision as d = (w-lb)*(ub-w); u = a*d; w = w+u;
+ * clamp; and stored as float.
+ *   weight    f32 [Cout][Cin][K][K] (updated in place)
+ *   pre_wave  u8  [B][T][Cin][H][W]: the layer's (unpadded) input wave
+ *   winners / n_winners as produced by spk_kwta with the same k.           */
+SPK_API int spk_stdp(float *weight, int Cout, int Cin, int K, int pad,
+             const uint8_t *pre_wave, int B, int T, int H, int W,
+             const int32_t *winners, const int32_t *n_winners, int k,
+             float a_plus, float a_minus, float lb, float ub, int stabilizer, void *stream);
+
+/* R-STDP (section "snn Module": two STDP objects; tutorial: anti-STDP
+ * negates the learning rates): as spk_stdp, with reward i8 [B] per image:
+ * +1 applies (a_plus, a_minus), -1 applies (-a_plus, -a_minus), 0 skips.   */
+SPK_API int spk_rstdp(float *weight, int Cout, int Cin, int K, int pad,
+              const uint8_t *pre_wave, int B, int T, int H, int W,
+              const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward,
+              float a_plus, float a_minus, float lb, float ub, int stabilizer, void *stream);
+
+/* Decision and reward (tutorial: the first winner's feature maps to a
+ * class; reward when it equals the label, punish otherwise, nothing for a
+ * silent sample).  decision i32 [B] = winners[b][0].feature % n_classes or
+ * -1 when n_winners[b] == 0; reward i8 [B] in {+1, -1, 0}.                 */
+SPK_API int spk_decide(const int32_t *winners, const int32_t *n_winners, int B, int k,
+               const int32_t *labels, int n_classes, int32_t *decision, int8_t *reward,
+               void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LIBSPYKE_H */

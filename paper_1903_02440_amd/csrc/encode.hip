@@ -1,0 +1,377 @@
+// Intensity-to-latency encoding and spike-wave utilities (gfx950).
+//
+// Paper: section "utils Module" (multi-channel DoG/Gabor Filter applied to the
+// image, Intensity2Latency = rank-order coding), the threshold semantics of
+// the "functional Module", and Eq.1 (cumulative spike wave).
+//
+// spk_encode_latency runs three kernels on the caller's stream:
+//   1. k_filter: same-size cross-correlation of each u8 image with the C
+//      filters (double accumulation over the non-zero taps, one rounding to
+//      float, then values below the threshold set to 0).  One workgroup per
+//      (image, band of 8 rows) stages the band plus its halo in LDS.
+//   2. k_rank_select: one workgroup per image finds the T-1 bin boundaries of
+//      the rank-order code by an MSD radix select (8 passes of 8 bits) on the
+//      unique 64-bit keys  (float bits of I) << 32 | ~index  of the positive
+//      intensities; all boundaries share each pass's digit histograms.
+//   3. k_expand_latency: every entry counts the boundaries its key does not
+//      exceed -- that count is its bin floor(rho*T/n) -- and writes t_first
+//      and the T planes of the wave (4 entries per thread, u32 stores).
+#include <algorithm>
+
+#include "common.hpp"
+
+namespace {
+
+constexpr int ROWS = 8;          // filter rows per workgroup
+constexpr int MAX_KF = 31;
+constexpr int SEL_THREADS = 1024;
+constexpr int MAX_GROUPS = 32;   // bin boundaries resolved per select batch
+constexpr int LDS_KEYS = 12288;  // intensities cached in LDS when N fits
+
+// ------------------------------------------------------------------ filter
+__global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img, int B, int H, int W,
+                                                const float *__restrict__ filt, int C, int KF, float thr,
+                                                float *__restrict__ out) {
+    extern __shared__ unsigned char smem[];
+    const int nb = (H + ROWS - 1) / ROWS;
+    const int b = blockIdx.x / nb, band = blockIdx.x % nb;
+    const int y0 = band * ROWS, p = (KF - 1) / 2;
+    const int rows = min(ROWS, H - y0);
+    const int srows = rows + KF - 1;
+    float *sf = reinterpret_cast<float *>(smem);                 // C*KF*KF taps
+    int *bbox = reinterpret_cast<int *>(sf + C * KF * KF);        // C x (y0,y1,x0,x1)
+    uint8_t *sim = reinterpret_cast<uint8_t *>(bbox + 4 * C);     // srows x W pixels
+
+    for (int i = threadIdx.x; i < C * KF * KF; i += blockDim.x) sf[i] = filt[i];
+    for (int i = threadIdx.x; i < srows * W; i += blockDim.x) {
+        const int r = i / W, x = i % W, y = y0 - p + r;
+        sim[i] = (y >= 0 && y < H) ? img[((int64_t)b * H + y) * W + x] : 0;
+    }
+    __syncthreads();
+    // bounding box of the non-zero taps of each channel (zero taps add nothing)
+    for (int c = threadIdx.x; c < C; c += blockDim.x) {
+        int ya = KF, yb = -1, xa = KF, xb = -1;
+        for (int ky = 0; ky < KF; ++ky)
+            for (int kx = 0; kx < KF; ++kx)
+                if (sf[(c * KF + ky) * KF + kx] != 0.0f) {
+                    ya = min(ya, ky); yb = max(yb, ky); xa = min(xa, kx); xb = max(xb, kx);
+                }
+        bbox[4 * c] = ya; bbox[4 * c + 1] = yb; bbox[4 * c + 2] = xa; bbox[4 * c + 3] = xb;
+    }
+    __syncthreads();
+    const int per = rows * W;
+    for (int i = threadIdx.x; i < C * per; i += blockDim.x) {
+        const int c = i / per, r = (i % per) / W, x = i % W;
+        const int ya = bbox[4 * c], yb = bbox[4 * c + 1], xa = bbox[4 * c + 2], xb = bbox[4 * c + 3];
+        double s = 0.0;
+        for (int ky = ya; ky <= yb; ++ky) {
+            const uint8_t *row = sim + (r + ky) * W;
+            const float *frow = sf + (c * KF + ky) * KF;
+            for (int kx = xa; kx <= xb; ++kx) {
+                const int ix = x + kx - p;
+                if (ix >= 0 && ix < W) s += (double)frow[kx] * (double)row[ix];
+            }
+        }
+        const float v = (float)s;
+        out[(((int64_t)b * C + c) * H + y0 + r) * W + x] = (v < thr) ? 0.0f : v;
+    }
+}
+
+// ------------------------------------------------------------------ rank select
+__device__ __forceinline__ uint64_t make_key(float v, uint32_t idx) {
+    return ((uint64_t)__float_as_uint(v) << 32) | (uint64_t)(0xFFFFFFFFu - idx);
+}
+
+// Output per image: bounds[b][j] (j = 0..T-2) = key at rank ceil((j+1)*n/T)
+// in descending order, 0 when that rank is >= n; count[b] = n.
+__global__ __launch_bounds__(SEL_THREADS) void k_rank_select(const float *__restrict__ inten, int64_t N, int T,
+                                                             uint64_t *__restrict__ bounds,
+                                                             uint32_t *__restrict__ count) {
+    __shared__ uint32_t hist[MAX_GROUPS][256];
+    __shared__ uint64_t gprefix[MAX_GROUPS];
+    __shared__ uint64_t tprefix[MAX_GROUPS];
+    __shared__ uint32_t trank[MAX_GROUPS];
+    __shared__ int tgroup[MAX_GROUPS];
+    __shared__ int ngroups, ntarg;
+    __shared__ int red[SEL_THREADS / 64];
+    __shared__ float cache[LDS_KEYS];
+
+    const int b = blockIdx.x;
+    const float *I = inten + (int64_t)b * N;
+    const bool cached = N <= LDS_KEYS;
+    const int tid = threadIdx.x;
+
+    int cnt = 0;
+    for (int64_t i = tid; i < N; i += SEL_THREADS) {
+        const float v = I[i];
+        if (cached) cache[i] = v;
+        cnt += v > 0.0f;
+    }
+    cnt = spk::wave_sum_i32(cnt);
+    if ((tid & 63) == 0) red[tid >> 6] = cnt;
+    __syncthreads();
+    uint32_t n = 0;
+    for (int w = 0; w < SEL_THREADS / 64; ++w) n += (uint32_t)red[w];
+    if (tid == 0) count[b] = n;
+
+    for (int j0 = 0; j0 < T - 1; j0 += MAX_GROUPS) {
+        const int jn = min(MAX_GROUPS, T - 1 - j0);
+        if (tid < jn) {
+            const uint64_t r = ((uint64_t)(j0 + tid + 1) * n + T - 1) / T;  // ceil((j+1) n / T)
+            trank[tid] = (uint32_t)r;
+            tprefix[tid] = 0;
+            bounds[(int64_t)b * (T - 1) + j0 + tid] = 0;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            int m = 0;
+            for (int j = 0; j < jn; ++j) m += trank[j] < n;
+            ntarg = m;  // active targets are a prefix (ranks grow with j)
+        }
+        __syncthreads();
+        const int m = ntarg;
+        if (m == 0) continue;
+        for (int pass = 0; pass < 8; ++pass) {
+            const int shift = 56 - 8 * pass;
+            // group the active targets by their current prefix (non-increasing in j)
+            if (tid == 0) {
+                int g = -1;
+                for (int j = 0; j < m; ++j) {
+                    if (g < 0 || tprefix[j] != gprefix[g]) gprefix[++g] = tprefix[j];
+                    tgroup[j] = g;
+                }
+                ngroups = g + 1;
+            }
+            __syncthreads();
+            const int ng = ngroups;
+            for (int i = tid; i < ng * 256; i += SEL_THREADS) (&hist[0][0])[i] = 0;
+            __syncthreads();
+            for (int64_t i = tid; i < N; i += SEL_THREADS) {
+                const float v = cached ? cache[i] : I[i];
+                if (!(v > 0.0f)) continue;
+                const uint64_t key = make_key(v, (uint32_t)i);
+                const uint64_t pre = pass == 0 ? 0 : (key >> (shift + 8));
+                // binary search among the group prefixes (sorted descending)
+                int lo = 0, hi = ng - 1, g = -1;
+                while (lo <= hi) {
+                    const int mid = (lo + hi) >> 1;
+                    const uint64_t gp = gprefix[mid];
+                    if (gp == pre) { g = mid; break; }
+                    if (gp > pre) lo = mid + 1; else hi = mid - 1;
+                }
+                if (g >= 0) atomicAdd(&hist[g][(key >> shift) & 255u], 1u);
+            }
+            __syncthreads();
+            if (tid < m) {
+                const int g = tgroup[tid];
+                uint32_t r = trank[tid];
+                int d = 255;
+                for (; d > 0; --d) {
+                    const uint32_t h = hist[g][d];
+                    if (r < h) break;
+                    r -= h;
+                }
+                trank[tid] = r;
+                tprefix[tid] = (tprefix[tid] << 8) | (uint64_t)d;
+            }
+            __syncthreads();
+        }
+        if (tid < m) bounds[(int64_t)b * (T - 1) + j0 + tid] = tprefix[tid];
+        __syncthreads();
+    }
+}
+
+// t_first = number of boundaries K_j with key <= K_j (the K_j are non-increasing).
+__device__ __forceinline__ int bin_of(uint64_t key, const uint64_t *kb, int nb) {
+    int lo = 0, hi = nb;  // first j with kb[j] < key
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (kb[mid] >= key) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(256) void k_expand_latency(const float *__restrict__ inten, int64_t N, int T,
+                                                        const uint64_t *__restrict__ bounds,
+                                                        uint8_t *__restrict__ tf_out, uint8_t *__restrict__ wave,
+                                                        int chunks) {
+    __shared__ uint64_t kb[256];
+    const int b = blockIdx.x / chunks, ch = blockIdx.x % chunks;
+    const int nbnd = T - 1;
+    for (int j = threadIdx.x; j < nbnd; j += blockDim.x) kb[j] = bounds[(int64_t)b * nbnd + j];
+    __syncthreads();
+    const float *I = inten + (int64_t)b * N;
+    const bool vec = (N % 4) == 0;
+    const int64_t groups = (N + 3) / 4;
+    for (int64_t q = (int64_t)ch * blockDim.x + threadIdx.x; q < groups; q += (int64_t)chunks * blockDim.x) {
+        uint32_t tv = 0;
+        int t4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t i = q * 4 + j;
+            int t = T;
+            if (i < N) {
+                const float v = I[i];
+                if (v > 0.0f) t = bin_of(make_key(v, (uint32_t)i), kb, nbnd);
+            }
+            t4[j] = t;
+            tv |= (uint32_t)t << (8 * j);
+        }
+        if (vec) {
+            if (tf_out) *reinterpret_cast<uint32_t *>(tf_out + (int64_t)b * N + q * 4) = tv;
+            if (wave)
+                for (int t = 0; t < T; ++t) {
+                    uint32_t w = 0;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) w |= (uint32_t)(t >= t4[j]) << (8 * j);
+                    *reinterpret_cast<uint32_t *>(wave + ((int64_t)b * T + t) * N + q * 4) = w;
+                }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t i = q * 4 + j;
+                if (i >= N) break;
+                if (tf_out) tf_out[(int64_t)b * N + i] = (uint8_t)t4[j];
+                if (wave)
+                    for (int t = 0; t < T; ++t) wave[((int64_t)b * T + t) * N + i] = (uint8_t)(t >= t4[j]);
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------ Eq.1 utilities
+__global__ __launch_bounds__(256) void k_expand_wave(const uint8_t *__restrict__ tf, int64_t N, int T,
+                                                     uint8_t *__restrict__ wave, int64_t total_groups,
+                                                     int64_t groups_per_img) {
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= total_groups) return;
+    const int64_t b = q / groups_per_img, g = q % groups_per_img;
+    if ((N % 4) == 0) {
+        const uint32_t t4 = *reinterpret_cast<const uint32_t *>(tf + b * N + g * 4);
+        for (int t = 0; t < T; ++t) {
+            uint32_t w = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) w |= (uint32_t)(t >= (int)((t4 >> (8 * j)) & 255u)) << (8 * j);
+            *reinterpret_cast<uint32_t *>(wave + (b * T + t) * N + g * 4) = w;
+        }
+    } else {
+        for (int j = 0; j < 4; ++j) {
+            const int64_t i = g * 4 + j;
+            if (i >= N) break;
+            const int tv = tf[b * N + i];
+            for (int t = 0; t < T; ++t) wave[(b * T + t) * N + i] = (uint8_t)(t >= tv);
+        }
+    }
+}
+
+__global__ void k_zero_i32(int32_t *p) { *p = 0; }
+
+__global__ __launch_bounds__(256) void k_validate_wave(const uint8_t *__restrict__ wave, int64_t B, int64_t N, int T,
+                                                       int32_t *__restrict__ bad) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int my = 0;
+    if (i < B * N) {
+        const int64_t b = i / N, e = i % N;
+        int prev = 0;
+        for (int t = 0; t < T; ++t) {
+            const int v = wave[(b * T + t) * N + e];
+            if (v > 1 || v < prev) { my = 1; break; }
+            prev = v;
+        }
+    }
+    my = spk::wave_sum_i32(my);
+    if ((threadIdx.x & 63) == 0 && my) atomicAdd(bad, my);
+}
+
+struct EncPlan {
+    int64_t N;
+    size_t inten_bytes, bound_bytes, count_bytes;
+};
+
+int enc_plan(int B, int C, int H, int W, int T, EncPlan &p) {
+    SPK_REQUIRE(B >= 0 && C >= 1 && H >= 1 && W >= 1 && T >= 1, SPK_E_SHAPE,
+                "spk_encode_latency: bad sizes B=%d C=%d H=%d W=%d T=%d", B, C, H, W, T);
+    SPK_REQUIRE(T <= 255, SPK_E_RANGE, "spk_encode_latency: T=%d > 255", T);
+    p.N = (int64_t)C * H * W;
+    SPK_REQUIRE(p.N < (1LL << 31), SPK_E_RANGE, "spk_encode_latency: C*H*W too large");
+    p.inten_bytes = (size_t)B * p.N * sizeof(float);
+    p.bound_bytes = (size_t)B * (T > 1 ? T - 1 : 1) * sizeof(uint64_t);
+    p.count_bytes = (size_t)B * sizeof(uint32_t);
+    return SPK_OK;
+}
+
+}  // namespace
+
+extern "C" size_t spk_encode_latency_workspace_size(int B, int C, int H, int W, int T) {
+    EncPlan p;
+    if (enc_plan(B, C, H, W, T, p) != SPK_OK) return 0;
+    spk::Carver c(nullptr);
+    c.take<float>(p.inten_bytes / sizeof(float));
+    c.take<uint64_t>(p.bound_bytes / sizeof(uint64_t));
+    c.take<uint32_t>(p.count_bytes / sizeof(uint32_t));
+    return spk::align_up(c.off, 256);
+}
+
+extern "C" int spk_encode_latency(const uint8_t *image, int B, int H, int W, const float *filters, int C, int KF,
+                                  float filter_threshold, int T, uint8_t *wave, uint8_t *t_first,
+                                  float *intensities, void *workspace, size_t ws_bytes, void *stream) {
+    EncPlan p;
+    int rc = enc_plan(B, C, H, W, T, p);
+    if (rc != SPK_OK) return rc;
+    SPK_REQUIRE(KF >= 1 && (KF % 2) == 1 && KF <= MAX_KF, SPK_E_RANGE,
+                "spk_encode_latency: filter size %d must be odd and <= %d", KF, MAX_KF);
+    SPK_REQUIRE((int64_t)(ROWS + KF - 1) * W <= 65536, SPK_E_RANGE, "spk_encode_latency: image width %d too large",
+                W);
+    SPK_REQUIRE(!std::isnan(filter_threshold), SPK_E_ARG, "spk_encode_latency: threshold is NaN");
+    if (B == 0) return spk::ok();
+    SPK_REQUIRE(image && filters, SPK_E_ARG, "spk_encode_latency: image and filters are required");
+    const size_t need = spk_encode_latency_workspace_size(B, C, H, W, T);
+    SPK_REQUIRE(workspace && ws_bytes >= need, SPK_E_WORKSPACE,
+                "spk_encode_latency: workspace of %zu bytes < %zu required", ws_bytes, need);
+    hipStream_t st = spk::as_stream(stream);
+    spk::Carver cv(workspace);
+    float *ws_int = cv.take<float>(p.inten_bytes / sizeof(float));
+    uint64_t *bounds = cv.take<uint64_t>(p.bound_bytes / sizeof(uint64_t));
+    uint32_t *count = cv.take<uint32_t>(p.count_bytes / sizeof(uint32_t));
+    float *I = intensities ? intensities : ws_int;
+
+    const int nb = (H + ROWS - 1) / ROWS;
+    const size_t lds = (size_t)C * KF * KF * sizeof(float) + 4 * C * sizeof(int) + (size_t)(ROWS + KF - 1) * W;
+    SPK_REQUIRE(lds <= 65536, SPK_E_RANGE, "spk_encode_latency: %d filters of %dx%d do not fit", C, KF, KF);
+    hipLaunchKernelGGL(k_filter, dim3((unsigned)(B * nb)), dim3(256), lds, st, image, B, H, W, filters, C, KF,
+                       filter_threshold, I);
+    if (!t_first && !wave) return spk::check_launch("spk_encode_latency");
+    if (T > 1)
+        hipLaunchKernelGGL(k_rank_select, dim3(B), dim3(SEL_THREADS), 0, st, I, p.N, T, bounds, count);
+    const int64_t groups = (p.N + 3) / 4;
+    const int chunks = (int)std::max<int64_t>(1, std::min<int64_t>(64, spk::ceil_div(groups, 256)));
+    hipLaunchKernelGGL(k_expand_latency, dim3((unsigned)(B * chunks)), dim3(256), 0, st, I, p.N, T, bounds,
+                       t_first, wave, chunks);
+    return spk::check_launch("spk_encode_latency");
+}
+
+extern "C" int spk_expand_wave(const uint8_t *t_first, int B, int T, int C, int H, int W, uint8_t *wave,
+                               void *stream) {
+    SPK_REQUIRE(B >= 0 && C >= 1 && H >= 1 && W >= 1 && T >= 1, SPK_E_SHAPE, "spk_expand_wave: bad sizes");
+    SPK_REQUIRE(T <= 255, SPK_E_RANGE, "spk_expand_wave: T=%d > 255", T);
+    if (B == 0) return spk::ok();
+    SPK_REQUIRE(t_first && wave, SPK_E_ARG, "spk_expand_wave: t_first and wave are required");
+    const int64_t N = (int64_t)C * H * W;
+    const int64_t gpi = (N + 3) / 4, total = gpi * B;
+    hipLaunchKernelGGL(k_expand_wave, dim3((unsigned)spk::ceil_div(total, 256)), dim3(256), 0, spk::as_stream(stream),
+                       t_first, N, T, wave, total, gpi);
+    return spk::check_launch("spk_expand_wave");
+}
+
+extern "C" int spk_validate_wave(const uint8_t *wave, int B, int T, int C, int H, int W, int32_t *bad_count,
+                                 void *stream) {
+    SPK_REQUIRE(B >= 0 && C >= 1 && H >= 1 && W >= 1 && T >= 1, SPK_E_SHAPE, "spk_validate_wave: bad sizes");
+    SPK_REQUIRE(bad_count && (wave || B == 0), SPK_E_ARG, "spk_validate_wave: wave and bad_count are required");
+    hipStream_t st = spk::as_stream(stream);
+    hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(1), 0, st, bad_count);
+    const int64_t N = (int64_t)C * H * W, total = N * B;
+    if (total > 0)
+        hipLaunchKernelGGL(k_validate_wave, dim3((unsigned)spk::ceil_div(total, 256)), dim3(256), 0, st, wave,
+                           (int64_t)B, N, T, bad_count);
+    return spk::check_launch("spk_validate_wave");
+}

@@ -1,0 +1,218 @@
+// k winners-take-all with feature-wise and lateral inhibition (gfx950).
+//
+// Paper: section "snn Module" (winners chosen first by the earliest spike,
+// then by the largest potential; lateral inhibition of the winner's
+// surroundings in all feature maps) and "functional Module" (get_k_winners
+// returning (feature, row, column) triplets; here with the spike step t).
+//
+// Every spiking neuron gets a unique 64-bit key whose unsigned order is the
+// winner order:
+//     bits 63..56  255 - t_first          (earlier spike wins)
+//     bits 55..24  v_first, order-mapped  (larger potential wins)
+//     bits 23..0   2^24 - 1 - index       (lower linear index wins ties)
+// Silent neurons get key 0.  Each feature map is cut into tiles of RB rows.
+//   1. k_kwta_tiles: the maximum key of every tile (a group of G lanes per
+//      tile, shuffle reduction), written to the workspace.
+//   2. k_kwta_select: one workgroup per image keeps its tile keys in LDS and
+//      runs the k rounds: block argmax (wave shuffles, then across waves),
+//      emit the winner, set the lateral window in an LDS bitmap of inhibited
+//      positions, clear the winner's feature tiles, and recompute only the
+//      tiles whose current maximum fell inside the window -- every other
+//      tile keeps its maximum, since inhibition only removes candidates.
+#include "common.hpp"
+
+namespace {
+
+constexpr int SEL_THREADS = 1024;
+constexpr int MAX_TILES = 4096;
+
+struct KwtaGeom {
+    int B, T, C, H, W, k, r;
+    int RB, nbands, ntiles, G;  // rows per tile, tiles per map, tiles per image, lanes per tile
+};
+
+__device__ __forceinline__ uint64_t kwta_key(int t, float v, uint32_t idx) {
+    uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);  // -0 and +0 are equal potentials
+    u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ((uint64_t)(255 - t) << 56) | ((uint64_t)u << 24) | (uint64_t)(0xFFFFFFu - idx);
+}
+
+__device__ __forceinline__ uint64_t group_max(uint64_t v, int G) {
+    for (int s = G >> 1; s >= 1; s >>= 1) {
+        const uint64_t o = __shfl_xor(v, s, 64);
+        v = o > v ? o : v;
+    }
+    return v;
+}
+
+// Maximum key of one tile over its non-inhibited neurons; all G lanes of the
+// group return it.  `inh` is the LDS bitmap of laterally inhibited positions
+// (nullptr before any winner exists).
+__device__ __forceinline__ uint64_t tile_max(const uint8_t *tf, const float *vf, const KwtaGeom &g, int tile,
+                                             int sub, const uint32_t *inh) {
+    const int f = tile / g.nbands, band = tile % g.nbands;
+    const int y0 = band * g.RB;
+    const int rows = min(g.RB, g.H - y0);
+    const int nn = rows * g.W;
+    const int64_t base = ((int64_t)f * g.H + y0) * g.W;
+    uint64_t m = 0;
+    for (int j = sub; j < nn; j += g.G) {
+        const int pos = y0 * g.W + j;
+        if (inh && ((inh[pos >> 5] >> (pos & 31)) & 1u)) continue;
+        const int t = tf[base + j];
+        if (t < g.T) {
+            const uint64_t key = kwta_key(t, vf[base + j], (uint32_t)(base + j));
+            m = key > m ? key : m;
+        }
+    }
+    return group_max(m, g.G);
+}
+
+__global__ __launch_bounds__(256) void k_kwta_tiles(const uint8_t *__restrict__ tf, const float *__restrict__ vf,
+                                                    KwtaGeom g, uint64_t *__restrict__ tilekey) {
+    const int64_t gid = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / g.G;
+    const int sub = threadIdx.x % g.G;
+    const int64_t total = (int64_t)g.B * g.ntiles;
+    const bool live = gid < total;
+    const int64_t b = live ? gid / g.ntiles : 0;
+    const int tile = live ? (int)(gid % g.ntiles) : 0;
+    const int64_t N = (int64_t)g.C * g.H * g.W;
+    // every lane takes part in the shuffles; lanes past the end read tile 0 of image 0
+    const uint64_t m = tile_max(tf + b * N, vf + b * N, g, tile, sub, nullptr);
+    if (live && sub == 0) tilekey[gid] = m;
+}
+
+__global__ __launch_bounds__(SEL_THREADS) void k_kwta_select(const uint8_t *__restrict__ tf_all,
+                                                             const float *__restrict__ vf_all, KwtaGeom g,
+                                                             const uint64_t *__restrict__ tilekey,
+                                                             int32_t *__restrict__ winners,
+                                                             int32_t *__restrict__ n_winners) {
+    extern __shared__ uint64_t smem64[];
+    uint64_t *keys = smem64;                                          // ntiles
+    int *list = reinterpret_cast<int *>(keys + g.ntiles);             // ntiles
+    const int nwords = (g.H * g.W + 31) / 32;
+    uint32_t *inh = reinterpret_cast<uint32_t *>(list + g.ntiles);    // nwords
+    __shared__ uint64_t red[SEL_THREADS / 64];
+    __shared__ int nlist;
+
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int64_t N = (int64_t)g.C * g.H * g.W;
+    const uint8_t *tf = tf_all + (int64_t)b * N;
+    const float *vf = vf_all + (int64_t)b * N;
+    int32_t *win = winners + (int64_t)b * g.k * 4;
+
+    for (int i = tid; i < g.ntiles; i += SEL_THREADS) keys[i] = tilekey[(int64_t)b * g.ntiles + i];
+    for (int i = tid; i < nwords; i += SEL_THREADS) inh[i] = 0u;
+    for (int i = tid; i < 4 * g.k; i += SEL_THREADS) win[i] = -1;
+    if (tid == 0) nlist = 0;
+    __syncthreads();
+
+    int found = 0;
+    for (int round = 0; round < g.k; ++round) {
+        uint64_t m = 0;
+        for (int i = tid; i < g.ntiles; i += SEL_THREADS) m = keys[i] > m ? keys[i] : m;
+        m = spk::wave_max_u64(m);
+        if (lane == 0) red[wv] = m;
+        __syncthreads();
+        uint64_t best = 0;
+        for (int w = 0; w < SEL_THREADS / 64; ++w) best = red[w] > best ? red[w] : best;
+        if (best == 0) break;  // uniform: every thread read the same red[]
+        const int idx = (int)(0xFFFFFFu - (uint32_t)(best & 0xFFFFFFu));
+        const int t = 255 - (int)(best >> 56);
+        const int f = idx / (g.H * g.W), y = (idx / g.W) % g.H, x = idx % g.W;
+        if (tid == 0) {
+            win[4 * round + 0] = f;
+            win[4 * round + 1] = t;
+            win[4 * round + 2] = y;
+            win[4 * round + 3] = x;
+        }
+        ++found;
+        // lateral window, clipped at the borders
+        const int ya = max(0, y - g.r), yb = min(g.H - 1, y + g.r);
+        const int xa = max(0, x - g.r), xb = min(g.W - 1, x + g.r);
+        const int wh = yb - ya + 1, ww = xb - xa + 1;
+        for (int i = tid; i < wh * ww; i += SEL_THREADS) {
+            const int pos = (ya + i / ww) * g.W + xa + i % ww;
+            atomicOr(&inh[pos >> 5], 1u << (pos & 31));
+        }
+        // retire the winner's feature map; list tiles whose maximum is now inhibited
+        for (int i = tid; i < g.ntiles; i += SEL_THREADS) {
+            const uint64_t kk = keys[i];
+            if (kk == 0) continue;
+            if (i / g.nbands == f) {
+                keys[i] = 0;
+                continue;
+            }
+            const int ti = (int)(0xFFFFFFu - (uint32_t)(kk & 0xFFFFFFu));
+            const int ty = (ti / g.W) % g.H, tx = ti % g.W;
+            if (ty >= ya && ty <= yb && tx >= xa && tx <= xb) list[atomicAdd(&nlist, 1)] = i;
+        }
+        __syncthreads();
+        const int nl = nlist;
+        const int groups = SEL_THREADS / g.G, grp = tid / g.G, sub = tid % g.G;
+        const int passes = (nl + groups - 1) / groups;  // identical trip count for all lanes
+        for (int p = 0; p < passes; ++p) {
+            const int e = p * groups + grp;
+            const int tile = e < nl ? list[e] : list[0];
+            const uint64_t mm = tile_max(tf, vf, g, tile, sub, inh);
+            if (e < nl && sub == 0) keys[tile] = mm;
+        }
+        __syncthreads();
+        if (tid == 0) nlist = 0;
+        __syncthreads();
+    }
+    if (tid == 0) n_winners[b] = found;
+}
+
+int kwta_geom(int B, int T, int C, int H, int W, int k, int r, KwtaGeom &g) {
+    SPK_REQUIRE(B >= 0 && T >= 1 && C >= 1 && H >= 1 && W >= 1, SPK_E_SHAPE, "spk_kwta: bad sizes");
+    SPK_REQUIRE(T <= 255, SPK_E_RANGE, "spk_kwta: T=%d > 255", T);
+    SPK_REQUIRE((int64_t)C * H * W <= (1LL << 24), SPK_E_RANGE, "spk_kwta: C*H*W > 2^24");
+    SPK_REQUIRE((int64_t)H * W <= 65536, SPK_E_RANGE, "spk_kwta: H*W > 65536");
+    SPK_REQUIRE(k >= 1 && r >= 0, SPK_E_ARG, "spk_kwta: k=%d must be >= 1 and radius=%d >= 0", k, r);
+    g.B = B; g.T = T; g.C = C; g.H = H; g.W = W; g.k = k; g.r = r;
+    int RB = 1;
+    while (RB < H && (int64_t)C * ((H + RB - 1) / RB) > MAX_TILES) RB *= 2;
+    RB = RB > H ? H : RB;
+    g.RB = RB;
+    g.nbands = (H + RB - 1) / RB;
+    SPK_REQUIRE((int64_t)C * g.nbands <= MAX_TILES, SPK_E_RANGE, "spk_kwta: %d feature maps exceed %d tiles", C,
+                MAX_TILES);
+    g.ntiles = C * g.nbands;
+    const int nn = RB * W;
+    int G = 1;
+    while (G < nn && G < 64) G <<= 1;
+    g.G = G;
+    return SPK_OK;
+}
+
+}  // namespace
+
+extern "C" size_t spk_kwta_workspace_size(int B, int C, int H, int W) {
+    KwtaGeom g;
+    if (kwta_geom(B, 1, C, H, W, 1, 0, g) != SPK_OK) return 0;
+    return spk::align_up((size_t)B * g.ntiles * sizeof(uint64_t), 256);
+}
+
+extern "C" int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int T, int C, int H, int W, int k,
+                        int radius, int32_t *winners, int32_t *n_winners, void *workspace, size_t ws_bytes,
+                        void *stream) {
+    KwtaGeom g;
+    int rc = kwta_geom(B, T, C, H, W, k, radius, g);
+    if (rc != SPK_OK) return rc;
+    if (B == 0) return spk::ok();
+    SPK_REQUIRE(t_first && v_first && winners && n_winners, SPK_E_ARG,
+                "spk_kwta: t_first, v_first, winners and n_winners are required");
+    const size_t need = spk_kwta_workspace_size(B, C, H, W);
+    SPK_REQUIRE(workspace && ws_bytes >= need, SPK_E_WORKSPACE, "spk_kwta: workspace of %zu bytes < %zu required",
+                ws_bytes, need);
+    hipStream_t st = spk::as_stream(stream);
+    uint64_t *tilekey = static_cast<uint64_t *>(workspace);
+    const int64_t threads = (int64_t)B * g.ntiles * g.G;
+    hipLaunchKernelGGL(k_kwta_tiles, dim3((unsigned)spk::ceil_div(threads, 256)), dim3(256), 0, st, t_first, v_first,
+                       g, tilekey);
+    const size_t lds = (size_t)g.ntiles * (sizeof(uint64_t) + sizeof(int)) + ((size_t)H * W + 31) / 32 * 4;
+    hipLaunchKernelGGL(k_kwta_select, dim3(B), dim3(SEL_THREADS), lds, st, t_first, v_first, g, tilekey, winners,
+                       n_winners);
+    return spk::check_launch("spk_kwta");
+}

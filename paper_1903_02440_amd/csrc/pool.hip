@@ -1,0 +1,63 @@
+// Spike max-pooling (gfx950).
+//
+// Paper: section "snn Module" (snn.Pooling / sf.pooling on spike waves: the
+// output holds the earliest spike of each window; stride defaults to the
+// window; zero padding) and Eq.3 for the output size, read as
+// floor((H + 2D - P)/R) + 1 (equal to the printed form whenever P == R).
+//
+// One thread per output neuron (b, c, yo, xo): for every step t it ORs the
+// window's bytes of plane t and stores one byte, so a wave reads and writes
+// consecutive x positions of one plane; the first-spike map is T minus the
+// number of steps at which the pooled neuron is on.
+#include "common.hpp"
+
+namespace {
+
+__global__ __launch_bounds__(256) void k_pool(const uint8_t *__restrict__ in, int64_t B, int T, int C, int H, int W,
+                                              int P, int R, int D, int Ho, int Wo, uint8_t *__restrict__ out,
+                                              uint8_t *__restrict__ out_tf) {
+    const int64_t total = B * C * (int64_t)Ho * Wo;
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const int xo = (int)(i % Wo);
+    int64_t r = i / Wo;
+    const int yo = (int)(r % Ho);
+    r /= Ho;
+    const int c = (int)(r % C);
+    const int64_t b = r / C;
+    const int y0 = yo * R - D, x0 = xo * R - D;
+    const int ya = max(y0, 0), yb = min(y0 + P, H), xa = max(x0, 0), xb = min(x0 + P, W);
+    const int64_t in_plane = (int64_t)C * H * W, out_plane = (int64_t)C * Ho * Wo;
+    const uint8_t *src = in + b * T * in_plane + (int64_t)c * H * W;
+    uint8_t *dst = out + b * T * out_plane + ((int64_t)c * Ho + yo) * Wo + xo;
+    int on = 0;
+    for (int t = 0; t < T; ++t) {
+        const uint8_t *pl = src + t * in_plane;
+        int m = 0;
+        for (int y = ya; y < yb; ++y)
+            for (int x = xa; x < xb; ++x) m |= pl[(int64_t)y * W + x];
+        m = m != 0;
+        dst[t * out_plane] = (uint8_t)m;
+        on += m;
+    }
+    if (out_tf) out_tf[(b * C + c) * (int64_t)Ho * Wo + (int64_t)yo * Wo + xo] = (uint8_t)(T - on);
+}
+
+}  // namespace
+
+extern "C" int spk_pool(const uint8_t *wave, int B, int T, int C, int H, int W, int kernel, int stride, int pad,
+                        uint8_t *out_wave, uint8_t *out_t_first, void *stream) {
+    SPK_REQUIRE(B >= 0 && T >= 1 && C >= 1 && H >= 1 && W >= 1, SPK_E_SHAPE, "spk_pool: bad sizes");
+    SPK_REQUIRE(T <= 255, SPK_E_RANGE, "spk_pool: T=%d > 255", T);
+    SPK_REQUIRE(kernel >= 1 && stride >= 1 && pad >= 0, SPK_E_SHAPE,
+                "spk_pool: bad window %d / stride %d / pad %d", kernel, stride, pad);
+    const int Ho = (H + 2 * pad - kernel) / stride + 1, Wo = (W + 2 * pad - kernel) / stride + 1;
+    SPK_REQUIRE(H + 2 * pad >= kernel && W + 2 * pad >= kernel && Ho >= 1 && Wo >= 1, SPK_E_SHAPE,
+                "spk_pool: window %d larger than the padded input", kernel);
+    if (B == 0) return spk::ok();
+    SPK_REQUIRE(wave && out_wave, SPK_E_ARG, "spk_pool: wave and out_wave are required");
+    const int64_t total = (int64_t)B * C * Ho * Wo;
+    hipLaunchKernelGGL(k_pool, dim3((unsigned)spk::ceil_div(total, 256)), dim3(256), 0, spk::as_stream(stream), wave,
+                       (int64_t)B, T, C, H, W, kernel, stride, pad, Ho, Wo, out_wave, out_t_first);
+    return spk::check_launch("spk_pool");
+}

@@ -1,0 +1,102 @@
+"""The C ABI: the library loads, exports every symbol the header declares,
+and rejects bad arguments on the host before any HIP call -- CPU only."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "libspyke.h")
+
+spk = pytest.importorskip("paper_1903_02440_amd")
+
+DUMMY = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
+
+
+def declared():
+    return re.findall(r"^SPK_API\s+[\w\s\*]*?\b(spk_\w+)\s*\(", open(HEADER).read(), flags=re.M)
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared()
+    assert len(names) == 14
+    lib = spk.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(names) == sorted(spk.exported_symbols())
+
+
+def test_version_and_empty_error():
+    assert spk.spk_version() == 0x000100
+    assert spk.lib().spk_last_error() in (b"",) or isinstance(spk.lib().spk_last_error(), bytes)
+
+
+def test_workspace_sizes_are_host_only_and_consistent():
+    a = spk.spk_conv_fire_workspace_size(1000, 15, 30, 14, 14, 250, 3, 1)
+    b = spk.spk_conv_fire_workspace_size(2000, 15, 30, 14, 14, 250, 3, 1)
+    assert 0 < a < b
+    assert spk.spk_conv_fire_workspace_size(1, 300, 30, 14, 14, 250, 3, 1) == 0  # T out of range
+    assert spk.spk_encode_latency_workspace_size(1000, 6, 28, 28, 15) >= 1000 * 6 * 28 * 28 * 4
+    assert spk.spk_kwta_workspace_size(16, 256, 256, 256) == 16 * 4096 * 8
+    assert spk.spk_kwta_workspace_size(1, 1, 512, 512) == 0  # H*W above the limit
+
+
+def _status(fn, *args):
+    return fn(*args)
+
+
+def test_conv_fire_validation_errors():
+    lib = spk.lib()
+    f = lib.spk_conv_fire
+    ok = dict(B=1, T=15, Cin=6, H=28, W=28, Cout=30, K=5, pad=2)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        thr = kw.pop("thr", 15.0) if "thr" in kw else 15.0
+        return f(DUMMY, a["B"], a["T"], a["Cin"], a["H"], a["W"], DUMMY, a["Cout"], a["K"], a["pad"],
+                 a.get("thr", thr), DUMMY, DUMMY, DUMMY, DUMMY, kw.get("ws", DUMMY), kw.get("n", 0), None)
+
+    assert call(T=256) == spk.SPK_E_RANGE
+    assert call(T=0) == spk.SPK_E_SHAPE
+    assert call(K=40) == spk.SPK_E_SHAPE
+    assert call(Cin=3000, K=5) == spk.SPK_E_RANGE
+    assert call(n=16) == spk.SPK_E_WORKSPACE
+    assert call(thr=float("nan")) == spk.SPK_E_ARG
+    assert call(thr=-math.inf) == spk.SPK_E_ARG
+    assert b"workspace" in lib.spk_last_error() or b"threshold" in lib.spk_last_error()
+    # NULL required outputs
+    r = f(DUMMY, 1, 15, 6, 28, 28, DUMMY, 30, 5, 2, 15.0, None, None, None, DUMMY, DUMMY, 1 << 30, None)
+    assert r == spk.SPK_E_ARG and b"required" in lib.spk_last_error()
+
+
+def test_other_validation_errors():
+    lib = spk.lib()
+    assert lib.spk_pool(DUMMY, 1, 300, 1, 4, 4, 2, 2, 0, DUMMY, None, None) == spk.SPK_E_RANGE
+    assert lib.spk_pool(DUMMY, 1, 4, 1, 4, 4, 9, 2, 0, DUMMY, None, None) == spk.SPK_E_SHAPE
+    assert lib.spk_pool(None, 1, 4, 1, 4, 4, 2, 2, 0, DUMMY, None, None) == spk.SPK_E_ARG
+    assert lib.spk_kwta(DUMMY, DUMMY, 1, 15, 1, 4, 4, 0, 1, DUMMY, DUMMY, DUMMY, 1 << 20, None) == spk.SPK_E_ARG
+    assert lib.spk_kwta(DUMMY, DUMMY, 1, 15, 1, 512, 512, 1, 1, DUMMY, DUMMY, DUMMY, 1 << 20, None) == spk.SPK_E_RANGE
+    assert lib.spk_kwta(DUMMY, DUMMY, 2, 15, 1, 4, 4, 1, 1, DUMMY, DUMMY, DUMMY, 8, None) == spk.SPK_E_WORKSPACE
+    assert lib.spk_stdp(DUMMY, 4, 2, 3, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, 0.004, -0.003, 0.9, 0.1, 1,
+                        None) == spk.SPK_E_ARG  # lb > ub
+    assert lib.spk_stdp(DUMMY, 4, 2, 3, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, float("inf"), -0.003, 0.0, 1.0, 1,
+                        None) == spk.SPK_E_ARG
+    assert lib.spk_rstdp(DUMMY, 4, 2, 3, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, None, 0.004, -0.003, 0.0, 1.0, 1,
+                         None) == spk.SPK_E_ARG
+    assert lib.spk_encode_latency(DUMMY, 1, 28, 28, DUMMY, 6, 12, 0.0, 15, DUMMY, DUMMY, None, DUMMY, 1 << 30,
+                                  None) == spk.SPK_E_RANGE  # even filter size
+    assert lib.spk_encode_latency(DUMMY, 1, 28, 28, DUMMY, 6, 13, 0.0, 15, DUMMY, DUMMY, None, DUMMY, 4,
+                                  None) == spk.SPK_E_WORKSPACE
+    assert lib.spk_expand_wave(DUMMY, 1, 256, 1, 2, 2, DUMMY, None) == spk.SPK_E_RANGE
+    assert lib.spk_decide(DUMMY, DUMMY, 4, 0, DUMMY, 10, DUMMY, DUMMY, None) == spk.SPK_E_SHAPE
+
+
+def test_zero_batch_is_a_no_op():
+    lib = spk.lib()
+    # B = 0 returns before any launch or pointer use
+    assert lib.spk_conv_fire(None, 0, 15, 6, 28, 28, None, 30, 5, 2, 15.0, None, None, None, None, None, 0,
+                             None) == spk.SPK_OK
+    assert lib.spk_pool(None, 0, 15, 6, 28, 28, 2, 2, 0, None, None, None) == spk.SPK_OK
+    assert lib.spk_kwta(None, None, 0, 15, 6, 28, 28, 5, 3, None, None, None, 0, None) == spk.SPK_OK
