@@ -180,6 +180,15 @@ SPK_API int spk_decide(const int32_t *winners, const int32_t *n_winners, int B, 
                const int32_t *labels, int n_classes, int32_t *decision, int8_t *reward,
                void *stream);
 
+/* Synaptic events of a convolution (the throughput unit of the hot path):
+ * the number of (spiking pre-synaptic neuron, post-synaptic neuron) pairs,
+ * each counted once -- for every output position, Cout times the number of
+ * in-bounds receptive-field taps whose input neuron spikes at some step of
+ * the wave (u8 [B][T][Cin][H][W]; its last step is 1 exactly there).
+ * *count is a device u64, overwritten.  Same size rules as spk_conv_fire.  */
+SPK_API int spk_count_events(const uint8_t *wave, int B, int T, int Cin, int H, int W,
+                             int Cout, int K, int pad, uint64_t *count, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

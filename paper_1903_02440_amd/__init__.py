@@ -48,6 +48,7 @@ _SIGS = {
     "spk_stdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _F, _F, _F, _F, _I, _P]),
     "spk_rstdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _P, _F, _F, _F, _F, _I, _P]),
     "spk_decide": (_I, [_P, _P, _I, _I, _P, _I, _P, _P, _P]),
+    "spk_count_events": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -277,6 +278,15 @@ def spk_decide(winners, n_winners, labels, n_classes=10, decision=None, reward=N
     _check(_lib.spk_decide(_ptr(winners), _ptr(n_winners), B, k, _ptr(labels), n_classes, _ptr(decision),
                            _ptr(reward), _stream(stream)))
     return decision, reward
+
+
+def spk_count_events(wave, Cout, K, pad, count=None, stream=None):
+    """Synaptic events (spiking pre, post pairs) of a conv over wave u8 [B,T,Cin,H,W] -> device int64 [1]."""
+    B, T, Cin, H, W = wave.shape
+    _need(wave, torch.uint8, (B, T, Cin, H, W), "wave")
+    count = _out(count, (1,), torch.int64, wave.device, "count")
+    _check(_lib.spk_count_events(_ptr(wave), B, T, Cin, H, W, Cout, K, pad, _ptr(count), _stream(stream)))
+    return count
 
 
 INF = math.inf

@@ -1,6 +1,7 @@
 """Builds libspyke.so (all HIP sources of csrc/) for gfx950 with hipcc.
 
-Run as ``python -m paper_1903_02440_amd.build``; the library is written next
+Run as ``python paper_1903_02440_amd/build.py`` (a plain script, so that it works
+before the library exists); the library is written next
 to this file, where the binding loads it.
 """
 from __future__ import annotations

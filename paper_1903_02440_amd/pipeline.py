@@ -1,0 +1,171 @@
+"""Batched layer chains over the libspyke entry points.
+
+A :class:`Chain` owns every device buffer of one batch (allocated once, at
+construction) and runs a workload's stages as a fixed sequence of C-ABI
+calls on one stream, with no host synchronisation and no allocation inside
+:meth:`Chain.forward` / :meth:`Chain.learn`:
+
+* source: ``spk_encode_latency`` (images + filter bank) or a given wave;
+* each conv stage: ``spk_conv_fire`` then ``spk_kwta`` (the winners feed
+  plasticity and, for the last layer, the decision);
+* each pool stage: ``spk_pool``;
+* after a reward-modulated last layer: ``spk_decide``;
+* learning: ``spk_stdp`` / ``spk_rstdp`` per conv stage, all after the
+  forward (frozen-forward, ordered replay within the batch).
+
+A stage list is any sequence of objects with the attributes of
+``Conv(cin, cout, K, pad, thr, k, r, learn, a_plus, a_minus, lb, ub,
+stabilizer)`` and ``Pool(P, R, D)``.
+"""
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import (pool_out_size, conv_out_size, spk_conv_fire, spk_conv_fire_workspace_size, spk_decide,
+               spk_encode_latency, spk_encode_latency_workspace_size, spk_kwta, spk_kwta_workspace_size,
+               spk_pool, spk_rstdp, spk_stdp)
+
+
+def _is_conv(st):
+    return hasattr(st, "cout")
+
+
+class Chain:
+    def __init__(self, stages, B, T, H, W, cin, source="image", filter_bank=None, filter_threshold=0.0,
+                 n_classes=10, device="cuda", want_potentials=True, want_spikes_all=True):
+        self.stages = list(stages)
+        self.B, self.T, self.source = B, T, source
+        self.n_classes = n_classes
+        self.filter_threshold = filter_threshold
+        dev = torch.device(device)
+        u8, f32, i32 = torch.uint8, torch.float32, torch.int32
+        ws_bytes = 0
+        if source == "image":
+            self.bank = filter_bank.to(dev).contiguous()
+            C = self.bank.shape[0]
+            self.image = torch.zeros((B, H, W), dtype=u8, device=dev)
+            ws_bytes = max(ws_bytes, spk_encode_latency_workspace_size(B, C, H, W, T))
+        else:
+            C = cin
+            self.image = None
+        self.input_wave = torch.zeros((B, T, C, H, W), dtype=u8, device=dev)
+        self.bufs = []
+        c, h, w = C, H, W
+        for st in self.stages:
+            b = {}
+            if _is_conv(st):
+                assert st.cin == c, "stage input channels do not match"
+                ho, wo = conv_out_size(h, st.K, st.pad), conv_out_size(w, st.K, st.pad)
+                b["P"] = torch.empty((B, T, st.cout, ho, wo), dtype=f32, device=dev) if want_potentials else False
+                b["S"] = torch.empty((B, T, st.cout, ho, wo), dtype=u8, device=dev)
+                b["tf"] = torch.empty((B, st.cout, ho, wo), dtype=u8, device=dev)
+                b["vf"] = torch.empty((B, st.cout, ho, wo), dtype=f32, device=dev)
+                b["win"] = torch.empty((B, st.k, 4), dtype=i32, device=dev)
+                b["nw"] = torch.empty((B,), dtype=i32, device=dev)
+                b["weight"] = torch.empty((st.cout, st.cin, st.K, st.K), dtype=f32, device=dev)
+                ws_bytes = max(ws_bytes, spk_conv_fire_workspace_size(B, T, st.cin, h, w, st.cout, st.K, st.pad),
+                               spk_kwta_workspace_size(B, st.cout, ho, wo))
+                c, h, w = st.cout, ho, wo
+            else:
+                ho, wo = pool_out_size(h, st.P, st.R, st.D), pool_out_size(w, st.P, st.R, st.D)
+                b["out"] = torch.empty((B, T, c, ho, wo), dtype=u8, device=dev)
+                h, w = ho, wo
+            b["shape_in"] = None
+            self.bufs.append(b)
+        self.workspace = torch.empty(max(ws_bytes, 256), dtype=u8, device=dev)
+        self.labels = torch.zeros((B,), dtype=i32, device=dev)
+        self.decision = torch.empty((B,), dtype=i32, device=dev)
+        self.reward = torch.zeros((B,), dtype=torch.int8, device=dev)
+        self.pre_waves = [None] * len(self.stages)
+
+    # ---------------------------------------------------------------- setup
+    def conv_stages(self):
+        return [i for i, st in enumerate(self.stages) if _is_conv(st)]
+
+    def set_weights(self, weights):
+        for i, wt in zip(self.conv_stages(), weights):
+            self.bufs[i]["weight"].copy_(wt)
+
+    def weights(self):
+        return [self.bufs[i]["weight"] for i in self.conv_stages()]
+
+    def set_input(self, image=None, wave=None, labels=None):
+        if image is not None:
+            self.image.copy_(image)
+        if wave is not None:
+            self.input_wave.copy_(wave)
+        if labels is not None:
+            self.labels.copy_(labels)
+
+    # ---------------------------------------------------------------- run
+    def forward(self, stream=None, hook=None):
+        """Enqueue the forward of the batch.  hook(name, phase), if given, is
+        called right before (phase 0) and after (phase 1) each C-ABI call;
+        names are "encode", "conv<i>", "kwta<i>", "pool<i>", "decide"."""
+        mark = hook or (lambda name, phase: None)
+        if self.source == "image":
+            mark("encode", 0)
+            spk_encode_latency(self.image, self.bank, self.T, self.filter_threshold, wave=self.input_wave,
+                               t_first=False, intensities=False, workspace=self.workspace, stream=stream)
+            mark("encode", 1)
+        x = self.input_wave
+        last_conv = None
+        for i, (st, b) in enumerate(zip(self.stages, self.bufs)):
+            self.pre_waves[i] = x
+            if _is_conv(st):
+                mark(f"conv{i}", 0)
+                spk_conv_fire(x, b["weight"], st.pad, st.thr, potentials=b["P"], spikes=b["S"], t_first=b["tf"],
+                              v_first=b["vf"], workspace=self.workspace, stream=stream)
+                mark(f"conv{i}", 1)
+                mark(f"kwta{i}", 0)
+                spk_kwta(b["tf"], b["vf"], self.T, st.k, st.r, winners=b["win"], n_winners=b["nw"],
+                         workspace=self.workspace, stream=stream)
+                mark(f"kwta{i}", 1)
+                x = b["S"]
+                last_conv = i
+            else:
+                mark(f"pool{i}", 0)
+                spk_pool(x, st.P, st.R, st.D, out_wave=b["out"], out_t_first=False, stream=stream)
+                mark(f"pool{i}", 1)
+                x = b["out"]
+        if last_conv is not None and self.stages[last_conv].learn == "rstdp":
+            b = self.bufs[last_conv]
+            mark("decide", 0)
+            spk_decide(b["win"], b["nw"], self.labels, self.n_classes, decision=self.decision, reward=self.reward,
+                       stream=stream)
+            mark("decide", 1)
+
+    def learn(self, stream=None, hook=None):
+        """Enqueue the plasticity of every learning conv stage (names "stdp<i>")."""
+        mark = hook or (lambda name, phase: None)
+        for i, (st, b) in enumerate(zip(self.stages, self.bufs)):
+            if not _is_conv(st) or st.learn is None:
+                continue
+            mark(f"stdp{i}", 0)
+            if st.learn == "rstdp":
+                spk_rstdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], self.reward, st.a_plus,
+                          st.a_minus, st.lb, st.ub, st.stabilizer, stream=stream)
+            else:
+                spk_stdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], st.a_plus, st.a_minus, st.lb,
+                         st.ub, st.stabilizer, stream=stream)
+            mark(f"stdp{i}", 1)
+
+    def step(self, stream=None, hook=None):
+        """One pass of the whole hot path over the batch: forward, then plasticity."""
+        self.forward(stream, hook)
+        self.learn(stream, hook)
+
+
+def chain_for(workload, filter_bank=None, device="cuda", **kw):
+    """A Chain for a workload description (stages, sizes, source); filter_bank
+    is the [C,KF,KF] float tensor of an image source."""
+    bank = filter_bank
+    if bank is not None and not isinstance(bank, torch.Tensor):
+        bank = torch.from_numpy(bank)
+    return Chain(workload.stages, workload.B, workload.T, workload.H, workload.W, workload.cin,
+                 source=workload.source, filter_bank=bank, n_classes=workload.n_classes, device=device, **kw)
+
+
+INF = math.inf

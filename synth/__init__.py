@@ -154,15 +154,28 @@ def times_geometric(g: np.random.Generator, shape, T: int, p: float) -> np.ndarr
 
 # ---------------------------------------------------------------- workloads
 @dataclass
-class Layer:
+class Conv:
+    """A convolutional spiking layer: conv -> fire -> kWTA, then its plasticity rule."""
     cin: int
     cout: int
     K: int
     pad: int
     thr: float
-    k: int = 1
-    r: int = 0
-    pool: tuple | None = None  # (P, R, D) applied after this layer's spikes
+    k: int
+    r: int
+    learn: str | None = "stdp"  # "stdp", "rstdp" or None
+    a_plus: float = 0.004
+    a_minus: float = -0.003
+    lb: float = 0.0
+    ub: float = 1.0
+    stabilizer: bool = True
+
+
+@dataclass
+class Pool:
+    P: int
+    R: int
+    D: int = 0
 
 
 @dataclass
@@ -171,50 +184,79 @@ class Workload:
     name: str
     B: int
     T: int
-    layers: list = field(default_factory=list)
+    H: int
+    W: int
+    stages: list = field(default_factory=list)
+    source: str = "image"   # "image": u8 images encoded with `bank`; "wave": first-spike times given
+    bank: str | None = None
+    cin: int = 1            # input channels of a "wave" source
+    n_classes: int = 10
 
 
-# The five workloads the benchmark and parity tests use (sizes from the
-# paper's tutorial network and its natural-image / stress variants).
+# The five workloads: the paper's tutorial network on MNIST-sized inputs
+# (single layer and full 3-layer), a natural-image-sized layer, and two
+# stress layers.
 def mnist_single(B: int = 1) -> Workload:
-    return Workload(1, "mnist-S1", B, 15, [Layer(6, 30, 5, 2, 15.0, k=5, r=3)])
+    return Workload(1, "mnist-S1", B, 15, 28, 28, [Conv(6, 30, 5, 2, 15.0, 5, 3)], bank="dog")
 
 
 def mnist_3layer(B: int = 1000) -> Workload:
-    return Workload(2, "mnist-3layer", B, 15, [
-        Layer(6, 30, 5, 2, 15.0, k=5, r=3, pool=(2, 2, 0)),
-        Layer(30, 250, 3, 1, 10.0, k=8, r=1, pool=(3, 3, 0)),
-        Layer(250, 200, 5, 2, math.inf, k=1, r=0),
-    ])
+    return Workload(2, "mnist-3layer", B, 15, 28, 28, [
+        Conv(6, 30, 5, 2, 15.0, 5, 3), Pool(2, 2),
+        Conv(30, 250, 3, 1, 10.0, 8, 1), Pool(3, 3),
+        Conv(250, 200, 5, 2, math.inf, 1, 0, learn="rstdp"),
+    ], bank="dog")
 
 
 def natural_single(B: int = 64) -> Workload:
-    return Workload(3, "natural-S2", B, 30, [Layer(4, 20, 17, 0, 36.0, k=1, r=5)])
+    return Workload(3, "natural-S2", B, 30, 160, 250, [Pool(7, 6), Conv(4, 20, 17, 0, 36.0, 1, 5)], bank="gabor")
 
 
 def stress_forward(B: int = 256) -> Workload:
-    return Workload(4, "stress-fwd", B, 15, [Layer(30, 250, 3, 1, 10.0, k=8, r=1)])
+    return Workload(4, "stress-fwd", B, 15, 14, 14, [Conv(30, 250, 3, 1, 10.0, 8, 1, learn=None)],
+                    source="wave", cin=30)
 
 
 def stress_large(B: int = 16) -> Workload:
-    return Workload(5, "stress-large", B, 64, [Layer(64, 256, 5, 2, 40.0, k=32, r=4)])
+    return Workload(5, "stress-large", B, 64, 256, 256, [Conv(64, 256, 5, 2, 40.0, 32, 4)], source="wave", cin=64)
 
 
-def mnist_inputs(wid: int, B: int):
-    """Stroke images, the DoG bank, labels and per-layer weights for workloads 1/2."""
-    img = stroke_images(rng(wid, 0), B)
-    bank = dog_bank()
-    lab = labels(rng(wid, 20), B)
-    return img, bank, lab
+WORKLOADS = {1: mnist_single, 2: mnist_3layer, 3: natural_single, 4: stress_forward, 5: stress_large}
 
 
-def layer_weights(wid: int, li: int, L: Layer, kind: str = "normal") -> np.ndarray:
-    g = rng(wid, 10 + li)
-    shape = (L.cout, L.cin, L.K, L.K)
-    if kind == "dyadic":
-        return dyadic_weights(g, shape, L.cin * L.K * L.K)
-    if wid == 4:
-        return uniform_weights(g, shape)
-    if wid == 5:
-        return normal_weights(g, shape, 0.5, 0.1)
-    return normal_weights(g, shape, 0.8, 0.05)
+def make_inputs(wl: Workload, weights: str = "paper") -> dict:
+    """Seeded inputs of a workload: source data, filter bank, labels and one
+    weight tensor per conv stage.  weights="dyadic" draws exactly summable
+    weights instead (same shapes) for bit-exact checks."""
+    out = {}
+    g0 = rng(wl.wid, 0)
+    if wl.source == "image":
+        if wl.bank == "dog":
+            out["image"] = stroke_images(g0, wl.B, wl.H, wl.W)
+            out["bank"] = dog_bank()
+        else:
+            out["image"] = pink_noise_images(g0, wl.B, wl.H, wl.W)
+            out["bank"] = gabor_bank()
+    elif wl.wid == 5:
+        out["t_first"] = times_geometric(g0, (wl.B, wl.cin, wl.H, wl.W), wl.T, 0.05)
+    else:
+        out["t_first"] = times_uniform_or_silent(g0, (wl.B, wl.cin, wl.H, wl.W), wl.T, 0.6)
+    out["labels"] = labels(rng(wl.wid, 20), wl.B, wl.n_classes)
+    ws = []
+    li = 0
+    for st in wl.stages:
+        if not isinstance(st, Conv):
+            continue
+        li += 1
+        g = rng(wl.wid, 10 + li)
+        shape = (st.cout, st.cin, st.K, st.K)
+        if weights == "dyadic":
+            ws.append(dyadic_weights(g, shape, st.cin * st.K * st.K))
+        elif wl.wid == 4:
+            ws.append(uniform_weights(g, shape))
+        elif wl.wid == 5:
+            ws.append(normal_weights(g, shape, 0.5, 0.1))
+        else:
+            ws.append(normal_weights(g, shape, 0.8, 0.05))
+    out["weights"] = ws
+    return out
