@@ -109,7 +109,7 @@ SPK_API int spk_validate_wave(const uint8_t *wave, int B, int T, int C, int H, i
  *   spikes     u8  [B][T][Cout][Ho][Wo] or NULL: 1 where the neuron fires.
  *   t_first    u8  [B][Cout][Ho][Wo]: first firing step, T if silent.
  *   v_first    f32 [B][Cout][Ho][Wo]: potential at t_first, 0 if silent.
- * Limits: 1 <= T <= 255, Ho, Wo >= 1, Cin*K*K <= 65536.
+ * Limits: 1 <= T <= 255, Ho, Wo >= 1, Cin*K*K <= 16384, Cout <= 4096.
  * Workspace: spk_conv_fire_workspace_size(...) bytes.                      */
 SPK_API size_t spk_conv_fire_workspace_size(int B, int T, int Cin, int H, int W, int Cout, int K, int pad);
 SPK_API int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, int W,

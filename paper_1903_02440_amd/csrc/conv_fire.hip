@@ -12,8 +12,9 @@
 // t, with a binary A_t generated on the fly from the u8 first-spike map.
 // It runs on the fp16 matrix cores (v_mfma_f32_16x16x32_f16): A_t is exact
 // in fp16 (we use the value 2.0 for a spike, a single bit, and halve the
-// result), and every fp32 weight is split into hi = fp16(w), lo = fp16(w-hi),
-// so each product pair carries 22 significant bits of w; accumulation is fp32.
+// weights instead), and every fp32 weight w/2 is split into hi = fp16(w/2),
+// lo = fp16(w/2 - hi), so each product pair carries 22 significant bits of w;
+// accumulation is fp32.
 //
 // Pipeline of one call (all on the caller's stream):
 //   1. k_pad_first_spike: wave [B,T,Cin,H,W] -> zero-padded first-spike map
@@ -35,14 +36,14 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
 constexpr int WAVES = 4;  // waves per workgroup
-constexpr int NW = 2;     // 16-feature N tiles per wave (all kernels)
+constexpr int NW_MAX = 4;  // N tiles per wave never exceed this; ntiles is padded to a multiple
 
 struct ConvGeom {
     int B, T, Cin, H, W, Cout, K, pad;
     int Hp, Wp, Ho, Wo, HoWo;
     int Kc;          // Cin*K*K
     int ksteps;      // ceil(Kc/32)
-    int ntiles;      // ceil(Cout/16) rounded up to a multiple of NW
+    int ntiles;      // ceil(Cout/16) rounded up to a multiple of NW_MAX
     int mt_per_img;  // ceil(HoWo/16)
     int64_t total_mtiles;
     float thr;
@@ -50,18 +51,17 @@ struct ConvGeom {
     int vec4;        // HoWo % 4 == 0: 16-byte potential / 4-byte spike stores
 };
 
-// 1. first-spike times of the padded input.
+// 1. first-spike times of the padded input.  Grid (image, chunk of 256 of
+// the image's Cin*Hp*Wp padded cells); 32-bit index arithmetic.
 __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restrict__ wave, ConvGeom g,
                                                          uint8_t *__restrict__ tpad) {
-    const int64_t total = (int64_t)g.B * g.Cin * g.Hp * g.Wp;
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= total) return;
-    const int px = (int)(i % g.Wp);
-    int64_t r = i / g.Wp;
-    const int py = (int)(r % g.Hp);
-    r /= g.Hp;
-    const int ci = (int)(r % g.Cin);
-    const int64_t b = r / g.Cin;
+    const int per_img = g.Cin * g.Hp * g.Wp;
+    const int i = blockIdx.y * 256 + threadIdx.x;
+    if (i >= per_img) return;
+    const int64_t b = blockIdx.x;
+    const int hw = g.Hp * g.Wp;
+    const int ci = i / hw, pix = i - ci * hw;
+    const int py = pix / g.Wp, px = pix - py * g.Wp;
     const int y = py - g.pad, x = px - g.pad;
     int t = g.T;
     if (y >= 0 && y < g.H && x >= 0 && x < g.W) {
@@ -71,7 +71,7 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
         for (int tt = 0; tt < g.T; ++tt) s += p[tt * plane] != 0;
         t = g.T - s;  // a cumulative wave has exactly T - t_first ones
     }
-    tpad[i] = (uint8_t)t;
+    tpad[b * per_img + i] = (uint8_t)t;
 }
 
 // 2. weight fragments.  Fragment (nt, ks, lane) holds, for feature
@@ -91,7 +91,8 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int k = ks * 32 + (lane >> 4) * 8 + j;
-            const float v = (n < g.Cout && k < g.Kc) ? w[(int64_t)n * g.Kc + k] : 0.0f;
+            // halved (exactly): the spike operand is 2.0, so the products are w * spike
+            const float v = (n < g.Cout && k < g.Kc) ? 0.5f * w[(int64_t)n * g.Kc + k] : 0.0f;
             const _Float16 hv = (_Float16)v;
             const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
             h[j] = hv;
@@ -113,38 +114,108 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
 }
 
 // 3. the fused GEMM + fire.  A wave owns MW consecutive 16-position M tiles
-// (across the whole batch) and NW 16-feature N tiles, for all time steps.
-// Lane l feeds A row l%16 / B column l%16 with the 8 taps 8*(l/16)..+7 and
-// receives C[4*(l/16) + j][l%16], j = 0..3: four consecutive positions of
-// one feature.
-template <int MW, int TB>
-__global__ __launch_bounds__(256, 2) void k_conv_fire(const uint8_t *__restrict__ tpad,
-                                                   const half8 *__restrict__ whi,
-                                                   const half8 *__restrict__ wlo,
-                                                   const int *__restrict__ koff, ConvGeom g,
-                                                   int n_mgroups, int n_mblocks,
-                                                   float *__restrict__ P, uint8_t *__restrict__ S,
-                                                   uint8_t *__restrict__ TF, float *__restrict__ VF) {
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int gq = lane >> 4, c = lane & 15;
-    const int ng = blockIdx.x / n_mblocks;
-    const int mg = (blockIdx.x % n_mblocks) * WAVES + wv;
-    if (mg >= n_mgroups) return;
+// (across the whole batch) and NW 16-feature N tiles, for all time steps,
+// processed TB steps at a time.  Lane l feeds A row l%16 / B column l%16
+// with the 8 taps 8*(l/16)..+7 and receives C[4*(l/16) + j][l%16], j = 0..3:
+// four consecutive positions of one feature.
+//
+// The four waves of a workgroup share their NW feature tiles, so the weight
+// fragments are staged once per workgroup in LDS, KC K-steps at a time; the
+// spike-time gathers of K-step ks+1 are in flight while step ks computes.
+// Steps past T in the last time block are computed but never stored.
+//
+// Block order is XCD-aware: hardware hands consecutive workgroups to the 8
+// XCDs in turn, so block i is remapped to logical block
+// (i % 8) * ceil(nblk / 8) + i / 8.  Each XCD then sweeps a contiguous range
+// of positions, and the partial 128-byte lines at the edges of one block's
+// output runs are completed by its neighbour in the same L2 before they are
+// written back.
+constexpr int KC = 8;                 // K-steps of weight fragments per LDS chunk, at most
+constexpr size_t LDS_BUDGET = 79872;  // per workgroup: two workgroups fit one CU's 160 KiB
 
-    int64_t abase[MW], img[MW];
+template <int MW>
+__device__ __forceinline__ void gather_tp(uint32_t (&tp)[MW][8], int ks, const uint8_t *__restrict__ tpad,
+                                          const uint32_t (&abase)[MW], const int *koff_lds, int gq) {
+    const int *ko = koff_lds + ks * 32 + gq * 8;
+    int o[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = ko[j];
+#pragma unroll
+    for (int i = 0; i < MW; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) tp[i][j] = tpad[abase[i] + (uint32_t)o[j]];
+}
+
+template <int MW, int NW, int TB>
+__device__ __forceinline__ void mfma_kstep(const uint32_t (&tp)[MW][8], const uint4 *fr, int lane,
+                                           f4 (&acc)[MW][NW][TB], int tb0) {
+    half8 bh[NW], bl[NW];
+#pragma unroll
+    for (int n = 0; n < NW; ++n) {
+        bh[n] = __builtin_bit_cast(half8, fr[(2 * n) * 64 + lane]);
+        bl[n] = __builtin_bit_cast(half8, fr[(2 * n + 1) * 64 + lane]);
+    }
+#pragma unroll
+    for (int i = 0; i < MW; ++i) {
+        // 16-bit lanes: (0x4000 + t - tp) has bit 14 set iff tp <= t (no borrow
+        // crosses the halves since 0x4000 > 255); 0x4000 is fp16 2.0
+        uint32_t d[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) d[q] = (0x4000u + (uint32_t)tb0) * 0x10001u - (tp[i][2 * q] | (tp[i][2 * q + 1] << 16));
+#pragma unroll
+        for (int t = 0; t < TB; ++t) {
+            u4 a;
+            a.x = d[0] & 0x40004000u;
+            a.y = d[1] & 0x40004000u;
+            a.z = d[2] & 0x40004000u;
+            a.w = d[3] & 0x40004000u;
+            const half8 ah = __builtin_bit_cast(half8, a);
+#pragma unroll
+            for (int n = 0; n < NW; ++n)
+                acc[i][n][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh[n], acc[i][n][t], 0, 0, 0);
+#pragma unroll
+            for (int n = 0; n < NW; ++n)
+                acc[i][n][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[n], acc[i][n][t], 0, 0, 0);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) d[q] += 0x10001u;
+        }
+    }
+}
+
+template <int MW, int NW, int TB, bool INF>
+__device__ __forceinline__ void conv_tile(const uint8_t *__restrict__ tpad, const uint4 *frl_all, const int *koff_lds,
+                                          const half8 *__restrict__ wfh, const half8 *__restrict__ wfl, uint4 *frl_chunk,
+                                          bool resident, int kc, const ConvGeom &g, int ng, int mg, bool active,
+                                          int tid, int lane, int gq, int c, float *__restrict__ P,
+                                          uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF) {
+    uint32_t abase[MW];
+    int64_t img[MW];
     int mpos0[MW];
 #pragma unroll
     for (int i = 0; i < MW; ++i) {
         const int64_t gm = (int64_t)mg * MW + i;
-        const bool v = gm < g.total_mtiles;
+        const bool v = active && gm < g.total_mtiles;
         const int64_t b = v ? gm / g.mt_per_img : 0;
         const int mt = v ? (int)(gm % g.mt_per_img) : 0;
         const int pos = min(mt * 16 + c, g.HoWo - 1);  // rows past the image are computed, not stored
         const int y = pos / g.Wo, x = pos % g.Wo;
-        abase[i] = ((int64_t)b * g.Cin * g.Hp + y) * g.Wp + x;
+        abase[i] = (uint32_t)(((int64_t)b * g.Cin * g.Hp + y) * g.Wp + x);
         img[i] = v ? b : -1;
         mpos0[i] = mt * 16 + gq * 4;
     }
+    // per (tile, feature) store offsets at step 0; a step adds Cout*HoWo
+    const int64_t tstride = (int64_t)g.Cout * g.HoWo;
+    int64_t obase[MW][NW];
+    bool ost[MW][NW];
+#pragma unroll
+    for (int i = 0; i < MW; ++i)
+#pragma unroll
+        for (int n = 0; n < NW; ++n) {
+            const int f = (ng * NW + n) * 16 + c;
+            ost[i][n] = img[i] >= 0 && f < g.Cout && mpos0[i] < g.HoWo;
+            obase[i][n] = ost[i][n] ? (img[i] * g.T * tstride + (int64_t)f * g.HoWo + mpos0[i]) : 0;
+        }
+    const bool full4 = g.vec4 != 0;
 
     int tfirst[MW][NW][4];
     float vfirst[MW][NW][4];
@@ -158,10 +229,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_fire(const uint8_t *__restrict_
                 vfirst[i][n][j] = 0.0f;
             }
 
-    const int4 *ko4 = reinterpret_cast<const int4 *>(koff);
-    const int64_t HoWo = g.HoWo;
-    const int t_begin = g.inf_mode ? g.T - 1 : 0;
-
+    const int t_begin = INF ? g.T - 1 : 0;
     for (int tb0 = t_begin; tb0 < g.T; tb0 += TB) {
         f4 acc[MW][NW][TB];
 #pragma unroll
@@ -171,150 +239,181 @@ __global__ __launch_bounds__(256, 2) void k_conv_fire(const uint8_t *__restrict_
 #pragma unroll
                 for (int t = 0; t < TB; ++t) acc[i][n][t] = f4{0.f, 0.f, 0.f, 0.f};
 
-        for (int ks = 0; ks < g.ksteps; ++ks) {
-            const int4 k0 = ko4[ks * 8 + gq * 2], k1 = ko4[ks * 8 + gq * 2 + 1];
-            uint32_t tpp[MW][4];
-#pragma unroll
-            for (int i = 0; i < MW; ++i) {
-                const uint8_t *p = tpad + abase[i];
-                tpp[i][0] = (uint32_t)p[k0.x] | ((uint32_t)p[k0.y] << 16);
-                tpp[i][1] = (uint32_t)p[k0.z] | ((uint32_t)p[k0.w] << 16);
-                tpp[i][2] = (uint32_t)p[k1.x] | ((uint32_t)p[k1.y] << 16);
-                tpp[i][3] = (uint32_t)p[k1.z] | ((uint32_t)p[k1.w] << 16);
+        for (int k0 = 0; k0 < g.ksteps; k0 += kc) {
+            const int nk = min(kc, g.ksteps - k0);
+            const uint4 *fr = frl_all + (size_t)k0 * NW * 2 * 64;
+            if (!resident) {  // stream this chunk of fragments through LDS (uniform branch)
+                __syncthreads();
+                for (int idx = tid; idx < nk * NW * 2 * 64; idx += 256) {
+                    const int ln = idx & 63, r = idx >> 6;  // r = (ksl*NW + n)*2 + h
+                    const int h = r & 1, n = (r >> 1) % NW, ksl = (r >> 1) / NW;
+                    const half8 *src = h ? wfl : wfh;
+                    frl_chunk[idx] = __builtin_bit_cast(uint4, src[(n * g.ksteps + k0 + ksl) * 64 + ln]);
+                }
+                __syncthreads();
+                fr = frl_chunk;
             }
-            half8 bh[NW], bl[NW];
-#pragma unroll
-            for (int n = 0; n < NW; ++n) {
-                const int64_t fi = ((int64_t)(ng * NW + n) * g.ksteps + ks) * 64 + lane;
-                bh[n] = whi[fi];
-                bl[n] = wlo[fi];
-            }
-#pragma unroll
-            for (int t = 0; t < TB; ++t) {
-                if (tb0 + t < g.T) {
-                    // 16-bit lanes: (0x4000 + t - tp) has bit 14 set iff tp <= t
-                    // (no borrow crosses the halves since 0x4000 > 255).
-                    const uint32_t cst = (0x4000u + (uint32_t)(tb0 + t)) * 0x10001u;
-#pragma unroll
-                    for (int i = 0; i < MW; ++i) {
-                        u4 a;
-                        a.x = (cst - tpp[i][0]) & 0x40004000u;
-                        a.y = (cst - tpp[i][1]) & 0x40004000u;
-                        a.z = (cst - tpp[i][2]) & 0x40004000u;
-                        a.w = (cst - tpp[i][3]) & 0x40004000u;
-                        const half8 ah = __builtin_bit_cast(half8, a);
-#pragma unroll
-                        for (int n = 0; n < NW; ++n) {
-                            acc[i][n][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh[n], acc[i][n][t], 0, 0, 0);
-                            acc[i][n][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[n], acc[i][n][t], 0, 0, 0);
-                        }
-                    }
+            if (active) {
+                uint32_t ta[MW][8], tb[MW][8];
+                gather_tp<MW>(ta, k0, tpad, abase, koff_lds, gq);
+                for (int kl = 0; kl < nk; kl += 2) {
+                    if (kl + 1 < nk) gather_tp<MW>(tb, k0 + kl + 1, tpad, abase, koff_lds, gq);
+                    mfma_kstep<MW, NW, TB>(ta, fr + kl * NW * 2 * 64, lane, acc, tb0);
+                    if (kl + 1 >= nk) break;
+                    if (kl + 2 < nk) gather_tp<MW>(ta, k0 + kl + 2, tpad, abase, koff_lds, gq);
+                    mfma_kstep<MW, NW, TB>(tb, fr + (kl + 1) * NW * 2 * 64, lane, acc, tb0);
                 }
             }
         }
+        if (!active) continue;
 
-        // epilogue: potentials, spikes, first-spike tracking for this time block
+        // epilogue: potentials, spikes and first-spike tracking of this time block
 #pragma unroll
         for (int t = 0; t < TB; ++t) {
             const int tt = tb0 + t;
-            if (tt >= g.T) continue;
+            if (tt >= g.T) break;  // uniform
 #pragma unroll
-            for (int i = 0; i < MW; ++i) {
-                if (img[i] < 0) continue;
-                const int p0 = mpos0[i];
+            for (int i = 0; i < MW; ++i)
 #pragma unroll
                 for (int n = 0; n < NW; ++n) {
-                    const int f = (ng * NW + n) * 16 + c;
-                    const f4 v = acc[i][n][t] * 0.5f;  // spikes entered as 2.0
+                    const f4 v = acc[i][n][t];  // the weights were halved: spikes entered as 2.0
                     uint32_t sp = 0;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        const bool s = g.inf_mode ? (v[j] > 0.0f) : (v[j] >= g.thr);
-                        sp |= (uint32_t)s << (8 * j);
-                        if (s && tfirst[i][n][j] == g.T) {
-                            tfirst[i][n][j] = tt;
-                            vfirst[i][n][j] = v[j];
-                        }
+                        const bool s = INF ? (v[j] > 0.0f) : (v[j] >= g.thr);
+                        const bool first = s && tfirst[i][n][j] == g.T;
+                        tfirst[i][n][j] = first ? tt : tfirst[i][n][j];
+                        vfirst[i][n][j] = first ? v[j] : vfirst[i][n][j];
+                        sp |= s ? (1u << (8 * j)) : 0u;
                     }
-                    if (f >= g.Cout) continue;
-                    const int64_t o = ((img[i] * g.T + tt) * (int64_t)g.Cout + f) * HoWo + p0;
-                    if (g.vec4) {
-                        if (p0 < g.HoWo) {
-                            if (P) *reinterpret_cast<f4 *>(P + o) = v;
-                            if (S) *reinterpret_cast<uint32_t *>(S + o) = sp;
-                        }
+                    if (!ost[i][n]) continue;
+                    const int64_t o = obase[i][n] + (int64_t)tt * tstride;
+                    if (full4) {
+                        if (P) *reinterpret_cast<f4 *>(P + o) = v;
+                        if (S) *reinterpret_cast<uint32_t *>(S + o) = sp;
                     } else {
+                        const int lim = g.HoWo - mpos0[i];
 #pragma unroll
                         for (int j = 0; j < 4; ++j)
-                            if (p0 + j < g.HoWo) {
+                            if (j < lim) {
                                 if (P) P[o + j] = v[j];
                                 if (S) S[o + j] = (uint8_t)(sp >> (8 * j));
                             }
                     }
                 }
-            }
         }
     }
+    if (!active) return;
 
     // Eq.5 mode: every step before the last holds zero potential and no spike.
-    if (g.inf_mode) {
+    if (INF) {
         for (int tt = 0; tt < g.T - 1; ++tt) {
 #pragma unroll
-            for (int i = 0; i < MW; ++i) {
-                if (img[i] < 0) continue;
-                const int p0 = mpos0[i];
+            for (int i = 0; i < MW; ++i)
 #pragma unroll
                 for (int n = 0; n < NW; ++n) {
-                    const int f = (ng * NW + n) * 16 + c;
-                    if (f >= g.Cout) continue;
-                    const int64_t o = ((img[i] * g.T + tt) * (int64_t)g.Cout + f) * HoWo + p0;
-                    if (g.vec4) {
-                        if (p0 < g.HoWo) {
-                            if (P) *reinterpret_cast<f4 *>(P + o) = f4{0.f, 0.f, 0.f, 0.f};
-                            if (S) *reinterpret_cast<uint32_t *>(S + o) = 0u;
-                        }
+                    if (!ost[i][n]) continue;
+                    const int64_t o = obase[i][n] + (int64_t)tt * tstride;
+                    if (full4) {
+                        if (P) *reinterpret_cast<f4 *>(P + o) = f4{0.f, 0.f, 0.f, 0.f};
+                        if (S) *reinterpret_cast<uint32_t *>(S + o) = 0u;
                     } else {
-                        for (int j = 0; j < 4; ++j)
-                            if (p0 + j < g.HoWo) {
-                                if (P) P[o + j] = 0.0f;
-                                if (S) S[o + j] = 0;
-                            }
+                        const int lim = g.HoWo - mpos0[i];
+                        for (int j = 0; j < 4 && j < lim; ++j) {
+                            if (P) P[o + j] = 0.0f;
+                            if (S) S[o + j] = 0;
+                        }
                     }
                 }
-            }
         }
     }
 
     // first-spike time and the potential there
 #pragma unroll
-    for (int i = 0; i < MW; ++i) {
-        if (img[i] < 0) continue;
-        const int p0 = mpos0[i];
+    for (int i = 0; i < MW; ++i)
 #pragma unroll
         for (int n = 0; n < NW; ++n) {
+            if (!ost[i][n]) continue;
             const int f = (ng * NW + n) * 16 + c;
-            if (f >= g.Cout) continue;
-            const int64_t o = (img[i] * (int64_t)g.Cout + f) * HoWo + p0;
-            if (g.vec4) {
-                if (p0 < g.HoWo) {
-                    uint32_t tv = 0;
+            const int64_t o = (img[i] * (int64_t)g.Cout + f) * g.HoWo + mpos0[i];
+            if (full4) {
+                uint32_t tv = 0;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) tv |= (uint32_t)tfirst[i][n][j] << (8 * j);
-                    *reinterpret_cast<uint32_t *>(TF + o) = tv;
-                    *reinterpret_cast<f4 *>(VF + o) =
-                        f4{vfirst[i][n][0], vfirst[i][n][1], vfirst[i][n][2], vfirst[i][n][3]};
-                }
+                for (int j = 0; j < 4; ++j) tv |= (uint32_t)tfirst[i][n][j] << (8 * j);
+                *reinterpret_cast<uint32_t *>(TF + o) = tv;
+                *reinterpret_cast<f4 *>(VF + o) = f4{vfirst[i][n][0], vfirst[i][n][1], vfirst[i][n][2], vfirst[i][n][3]};
             } else {
+                const int lim = g.HoWo - mpos0[i];
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    if (p0 + j < g.HoWo) {
+                    if (j < lim) {
                         TF[o + j] = (uint8_t)tfirst[i][n][j];
                         VF[o + j] = vfirst[i][n][j];
                     }
             }
         }
+}
+
+// Persistent workgroups.  Workgroup w runs on XCD x = w % 8; the XCDs split
+// the M blocks (4 waves x MW tiles of 16 positions) into 8 contiguous slices.
+// Each workgroup serves one feature group: it loads that group's weight
+// fragments into LDS once (or streams them in chunks when they do not fit)
+// and then takes the next M block of its XCD's slice from a counter shared by
+// the workgroups of the same (XCD, feature group).  The workgroups of an XCD
+// therefore always work on neighbouring positions, so the 128-byte lines
+// shared by neighbouring output runs are completed in that XCD's L2 before
+// they are written back.  Every workgroup stops when the slice is exhausted.
+template <int MW, int NW, int TB, bool INF>
+__global__ __launch_bounds__(256, 2) void k_conv_fire(const uint8_t *__restrict__ tpad,
+                                                      const half8 *__restrict__ whi,
+                                                      const half8 *__restrict__ wlo,
+                                                      const int *__restrict__ koff, ConvGeom g,
+                                                      int n_mgroups, int n_mblocks, int n_ngroups, int kc,
+                                                      int resident, unsigned *__restrict__ counters,
+                                                      float *__restrict__ P, uint8_t *__restrict__ S,
+                                                      uint8_t *__restrict__ TF, float *__restrict__ VF) {
+    extern __shared__ uint4 lds[];
+    __shared__ int next_mb;
+    int *koff_lds = reinterpret_cast<int *>(lds);      // ksteps*32 offsets
+    uint4 *frl = lds + (g.ksteps * 32 * 4 + 15) / 16;  // fragments: all K-steps, or a chunk of kc
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int gq = lane >> 4, c = lane & 15;
+    const int x = blockIdx.x % 8, j = blockIdx.x / 8;
+    const int ng = j % n_ngroups;
+    const int per_x = (n_mblocks + 7) / 8;
+    const int mb_lo = x * per_x, mb_hi = min(n_mblocks, mb_lo + per_x);
+    if (mb_lo >= mb_hi) return;  // whole workgroup: this XCD's slice is empty
+    unsigned *ctr = counters + x * n_ngroups + ng;
+
+    const half8 *wfh = whi + (int64_t)ng * NW * g.ksteps * 64;
+    const half8 *wfl = wlo + (int64_t)ng * NW * g.ksteps * 64;
+    for (int i = tid; i < g.ksteps * 32; i += 256) koff_lds[i] = koff[i];
+    if (resident) {
+        for (int idx = tid; idx < g.ksteps * NW * 2 * 64; idx += 256) {
+            const int ln = idx & 63, r = idx >> 6;  // r = (ks*NW + n)*2 + h
+            const int h = r & 1, n = (r >> 1) % NW, ks = (r >> 1) / NW;
+            const half8 *src = h ? wfl : wfh;
+            frl[idx] = __builtin_bit_cast(uint4, src[(n * g.ksteps + ks) * 64 + ln]);
+        }
+    }
+    for (;;) {
+        __syncthreads();  // LDS fills are visible; everyone has read the previous next_mb
+        if (tid == 0) next_mb = mb_lo + (int)atomicAdd(ctr, 1u);
+        __syncthreads();
+        const int mb = next_mb;
+        if (mb >= mb_hi) break;  // uniform
+        const int mg = mb * WAVES + wv;
+        conv_tile<MW, NW, TB, INF>(tpad, frl, koff_lds, wfh, wfl, frl, resident != 0, resident ? g.ksteps : kc, g,
+                                   ng, mg, mg < n_mgroups, tid, lane, gq, c, P, S, TF, VF);
     }
 }
+
+__global__ void k_zero_u32(unsigned *p, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
+constexpr int MAX_NGROUPS_COUNT = 8 * 64;  // (XCD, feature group) counters reserved in the workspace
 
 struct ConvPlan {
     ConvGeom g;
@@ -334,14 +433,18 @@ int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, Con
     g.Wo = g.Wp - K + 1;
     SPK_REQUIRE(g.Ho >= 1 && g.Wo >= 1, SPK_E_SHAPE, "spk_conv_fire: kernel %d larger than padded input %dx%d",
                 K, g.Hp, g.Wp);
-    SPK_REQUIRE((int64_t)Cin * K * K <= 65536, SPK_E_RANGE, "spk_conv_fire: Cin*K*K=%lld > 65536",
+    SPK_REQUIRE((int64_t)Cin * K * K <= 16384, SPK_E_RANGE, "spk_conv_fire: Cin*K*K=%lld > 16384",
                 (long long)Cin * K * K);
-    SPK_REQUIRE((int64_t)g.Ho * g.Wo < (1LL << 31) && (int64_t)Cin * g.Hp * g.Wp < (1LL << 31),
+    SPK_REQUIRE(Cout <= 4096, SPK_E_RANGE, "spk_conv_fire: Cout=%d > 4096", Cout);
+    SPK_REQUIRE((int64_t)g.Ho * g.Wo < (1LL << 31) && (int64_t)Cin * g.Hp * g.Wp <= 65535LL * 256,
                 SPK_E_RANGE, "spk_conv_fire: image too large");
+    // the MFMA kernel addresses the padded first-spike map with 32-bit offsets
+    SPK_REQUIRE((int64_t)B * Cin * g.Hp * g.Wp < (1LL << 32), SPK_E_RANGE,
+                "spk_conv_fire: padded input of %lld bytes exceeds 4 GiB", (long long)B * Cin * g.Hp * g.Wp);
     g.HoWo = g.Ho * g.Wo;
     g.Kc = Cin * K * K;
     g.ksteps = (g.Kc + 31) / 32;
-    g.ntiles = (int)spk::ceil_div(spk::ceil_div(Cout, 16), NW) * NW;
+    g.ntiles = (int)spk::ceil_div(spk::ceil_div(Cout, 16), NW_MAX) * NW_MAX;
     g.mt_per_img = (g.HoWo + 15) / 16;
     g.total_mtiles = (int64_t)B * g.mt_per_img;
     g.vec4 = (g.HoWo % 4) == 0;
@@ -357,18 +460,31 @@ size_t plan_workspace(const ConvPlan &pl) {
     c.take<half8>(pl.frag_count);
     c.take<half8>(pl.frag_count);
     c.take<int>(pl.koff_count);
+    c.take<unsigned>(MAX_NGROUPS_COUNT);
     return spk::align_up(c.off, 256);
 }
 
-template <int MW, int TB>
-void launch_conv(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int *koff, const ConvGeom &g,
-                 float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
+template <int MW, int NW, int TB, bool INF>
+void launch_conv(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int *koff, unsigned *counters,
+                 const ConvGeom &g, float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
     const int64_t n_mgroups = spk::ceil_div(g.total_mtiles, MW);
     const int64_t n_mblocks = spk::ceil_div(n_mgroups, WAVES);
-    const int64_t n_ngroups = g.ntiles / NW;
-    const int64_t grid = n_mblocks * n_ngroups;
-    hipLaunchKernelGGL((k_conv_fire<MW, TB>), dim3((unsigned)grid), dim3(256), 0, st, tpad, whi, wlo, koff, g,
-                       (int)n_mgroups, (int)n_mblocks, P, S, TF, VF);
+    const int n_ngroups = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), NW);
+    const size_t koff_bytes = spk::align_up((size_t)g.ksteps * 32 * sizeof(int), 16);
+    const size_t step = (size_t)NW * 2 * 64 * 16;  // one K-step of fragments
+    const int resident = koff_bytes + (size_t)g.ksteps * step <= LDS_BUDGET;
+    const int kc = resident ? g.ksteps
+                            : (int)std::max<size_t>(1, std::min<size_t>(KC, (LDS_BUDGET - koff_bytes) / step));
+    const size_t lds = koff_bytes + (size_t)kc * step;
+    // about two workgroups per CU (256 CUs, 32 per XCD), a multiple of the feature groups per XCD
+    const int64_t want = spk::ceil_div(n_mblocks * n_ngroups, 8);
+    const int64_t per_xcd = std::min<int64_t>(spk::ceil_div(std::max<int64_t>(64, n_ngroups), n_ngroups) * n_ngroups,
+                                              spk::ceil_div(want, n_ngroups) * n_ngroups);
+    const int nctr = 8 * n_ngroups;  // <= MAX_NGROUPS_COUNT: n_ngroups <= ceil(4096/16/2)
+    hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)spk::ceil_div(nctr, 256)), dim3(256), 0, st, counters, nctr);
+    hipLaunchKernelGGL((k_conv_fire<MW, NW, TB, INF>), dim3((unsigned)(per_xcd * 8)), dim3(256), lds, st, tpad, whi,
+                       wlo, koff, g, (int)n_mgroups, (int)n_mblocks, n_ngroups, kc, resident, counters, P, S, TF,
+                       VF);
 }
 
 }  // namespace
@@ -402,18 +518,27 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     half8 *whi = cv.take<half8>(pl.frag_count);
     half8 *wlo = cv.take<half8>(pl.frag_count);
     int *koff = cv.take<int>(pl.koff_count);
+    unsigned *counters = cv.take<unsigned>(MAX_NGROUPS_COUNT);
     hipStream_t st = spk::as_stream(stream);
 
-    const int64_t n1 = (int64_t)pl.tpad_bytes;
-    hipLaunchKernelGGL(k_pad_first_spike, dim3((unsigned)spk::ceil_div(n1, 256)), dim3(256), 0, st, wave, g, tpad);
+    const int64_t per_img = (int64_t)Cin * g.Hp * g.Wp;
+    hipLaunchKernelGGL(k_pad_first_spike, dim3((unsigned)B, (unsigned)spk::ceil_div(per_img, 256)), dim3(256), 0, st,
+                       wave, g, tpad);
     const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
     hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, whi,
                        wlo, koff);
-    if (g.inf_mode)
-        launch_conv<4, 1>(tpad, whi, wlo, koff, g, potentials, spikes, t_first, v_first, st);
-    else if (spk::ceil_div(T, 16) * 16 - T < spk::ceil_div(T, 15) * 15 - T)
-        launch_conv<1, 16>(tpad, whi, wlo, koff, g, potentials, spikes, t_first, v_first, st);
-    else
-        launch_conv<1, 15>(tpad, whi, wlo, koff, g, potentials, spikes, t_first, v_first, st);
+    // tile shape: one 16-position tile by two or four 16-feature tiles per wave
+    // (two when the layer has at most 32 features), 2 waves per SIMD
+    const bool wide = (Cout + 15) / 16 > 2;
+    if (g.inf_mode) {
+        if (wide) launch_conv<2, 4, 1, true>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
+        else launch_conv<2, 2, 1, true>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
+    } else if (wide) {
+        launch_conv<1, 4, 8, false>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
+    } else if (T % 15 == 0) {
+        launch_conv<1, 2, 15, false>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
+    } else {
+        launch_conv<1, 2, 16, false>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
+    }
     return spk::check_launch("spk_conv_fire");
 }

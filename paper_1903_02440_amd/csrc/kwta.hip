@@ -28,7 +28,9 @@ constexpr int MAX_TILES = 4096;
 
 struct KwtaGeom {
     int B, T, C, H, W, k, r;
-    int RB, nbands, ntiles, G;  // rows per tile, tiles per map, tiles per image, lanes per tile
+    int RB, nbands, ntiles;  // rows per tile, tiles per map, tiles per image
+    int G;                   // lanes per tile when computing all tile maxima
+    int G2;                  // lanes per tile when recomputing inhibited tiles
 };
 
 __device__ __forceinline__ uint64_t kwta_key(int t, float v, uint32_t idx) {
@@ -49,14 +51,14 @@ __device__ __forceinline__ uint64_t group_max(uint64_t v, int G) {
 // group return it.  `inh` is the LDS bitmap of laterally inhibited positions
 // (nullptr before any winner exists).
 __device__ __forceinline__ uint64_t tile_max(const uint8_t *tf, const float *vf, const KwtaGeom &g, int tile,
-                                             int sub, const uint32_t *inh) {
+                                             int sub, int G, const uint32_t *inh) {
     const int f = tile / g.nbands, band = tile % g.nbands;
     const int y0 = band * g.RB;
     const int rows = min(g.RB, g.H - y0);
     const int nn = rows * g.W;
     const int64_t base = ((int64_t)f * g.H + y0) * g.W;
     uint64_t m = 0;
-    for (int j = sub; j < nn; j += g.G) {
+    for (int j = sub; j < nn; j += G) {
         const int pos = y0 * g.W + j;
         if (inh && ((inh[pos >> 5] >> (pos & 31)) & 1u)) continue;
         const int t = tf[base + j];
@@ -65,20 +67,20 @@ __device__ __forceinline__ uint64_t tile_max(const uint8_t *tf, const float *vf,
             m = key > m ? key : m;
         }
     }
-    return group_max(m, g.G);
+    return group_max(m, G);
 }
 
 __global__ __launch_bounds__(256) void k_kwta_tiles(const uint8_t *__restrict__ tf, const float *__restrict__ vf,
                                                     KwtaGeom g, uint64_t *__restrict__ tilekey) {
-    const int64_t gid = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / g.G;
+    const uint32_t gid = (blockIdx.x * blockDim.x + threadIdx.x) / (uint32_t)g.G;  // < 2^31, checked on the host
     const int sub = threadIdx.x % g.G;
-    const int64_t total = (int64_t)g.B * g.ntiles;
+    const uint32_t total = (uint32_t)g.B * (uint32_t)g.ntiles;
     const bool live = gid < total;
-    const int64_t b = live ? gid / g.ntiles : 0;
-    const int tile = live ? (int)(gid % g.ntiles) : 0;
+    const uint32_t b = live ? gid / (uint32_t)g.ntiles : 0;
+    const int tile = live ? (int)(gid - b * (uint32_t)g.ntiles) : 0;
     const int64_t N = (int64_t)g.C * g.H * g.W;
     // every lane takes part in the shuffles; lanes past the end read tile 0 of image 0
-    const uint64_t m = tile_max(tf + b * N, vf + b * N, g, tile, sub, nullptr);
+    const uint64_t m = tile_max(tf + b * N, vf + b * N, g, tile, sub, g.G, nullptr);
     if (live && sub == 0) tilekey[gid] = m;
 }
 
@@ -149,12 +151,12 @@ __global__ __launch_bounds__(SEL_THREADS) void k_kwta_select(const uint8_t *__re
         }
         __syncthreads();
         const int nl = nlist;
-        const int groups = SEL_THREADS / g.G, grp = tid / g.G, sub = tid % g.G;
+        const int groups = SEL_THREADS / g.G2, grp = tid / g.G2, sub = tid % g.G2;
         const int passes = (nl + groups - 1) / groups;  // identical trip count for all lanes
         for (int p = 0; p < passes; ++p) {
             const int e = p * groups + grp;
             const int tile = e < nl ? list[e] : list[0];
-            const uint64_t mm = tile_max(tf, vf, g, tile, sub, inh);
+            const uint64_t mm = tile_max(tf, vf, g, tile, sub, g.G2, inh);
             if (e < nl && sub == 0) keys[tile] = mm;
         }
         __syncthreads();
@@ -183,6 +185,10 @@ int kwta_geom(int B, int T, int C, int H, int W, int k, int r, KwtaGeom &g) {
     int G = 1;
     while (G < nn && G < 64) G <<= 1;
     g.G = G;
+    // small tiles are recomputed one per thread: their loads then overlap
+    // instead of waiting on each other group after group
+    g.G2 = nn <= 32 ? 1 : G;
+    SPK_REQUIRE((int64_t)B * g.ntiles * G < (1LL << 31), SPK_E_RANGE, "spk_kwta: batch too large");
     return SPK_OK;
 }
 

@@ -13,34 +13,33 @@
 
 namespace {
 
-__global__ __launch_bounds__(256) void k_pool(const uint8_t *__restrict__ in, int64_t B, int T, int C, int H, int W,
-                                              int P, int R, int D, int Ho, int Wo, uint8_t *__restrict__ out,
+// Grid: (image, chunk of 256 of the image's C*Ho*Wo outputs).
+__global__ __launch_bounds__(256) void k_pool(const uint8_t *__restrict__ in, int T, int C, int H, int W, int P, int R,
+                                              int D, int Ho, int Wo, uint8_t *__restrict__ out,
                                               uint8_t *__restrict__ out_tf) {
-    const int64_t total = B * C * (int64_t)Ho * Wo;
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= total) return;
-    const int xo = (int)(i % Wo);
-    int64_t r = i / Wo;
-    const int yo = (int)(r % Ho);
-    r /= Ho;
-    const int c = (int)(r % C);
-    const int64_t b = r / C;
+    const int per_img = C * Ho * Wo;
+    const int i = blockIdx.y * 256 + threadIdx.x;
+    if (i >= per_img) return;
+    const int64_t b = blockIdx.x;
+    const int hw = Ho * Wo;
+    const int c = i / hw, pix = i - c * hw;
+    const int yo = pix / Wo, xo = pix - yo * Wo;
     const int y0 = yo * R - D, x0 = xo * R - D;
     const int ya = max(y0, 0), yb = min(y0 + P, H), xa = max(x0, 0), xb = min(x0 + P, W);
-    const int64_t in_plane = (int64_t)C * H * W, out_plane = (int64_t)C * Ho * Wo;
+    const int64_t in_plane = (int64_t)C * H * W, out_plane = (int64_t)per_img;
     const uint8_t *src = in + b * T * in_plane + (int64_t)c * H * W;
-    uint8_t *dst = out + b * T * out_plane + ((int64_t)c * Ho + yo) * Wo + xo;
+    uint8_t *dst = out + b * T * out_plane + i;
     int on = 0;
     for (int t = 0; t < T; ++t) {
         const uint8_t *pl = src + t * in_plane;
         int m = 0;
         for (int y = ya; y < yb; ++y)
-            for (int x = xa; x < xb; ++x) m |= pl[(int64_t)y * W + x];
+            for (int x = xa; x < xb; ++x) m |= pl[y * W + x];
         m = m != 0;
         dst[t * out_plane] = (uint8_t)m;
         on += m;
     }
-    if (out_tf) out_tf[(b * C + c) * (int64_t)Ho * Wo + (int64_t)yo * Wo + xo] = (uint8_t)(T - on);
+    if (out_tf) out_tf[b * per_img + i] = (uint8_t)(T - on);
 }
 
 }  // namespace
@@ -56,8 +55,9 @@ extern "C" int spk_pool(const uint8_t *wave, int B, int T, int C, int H, int W, 
                 "spk_pool: window %d larger than the padded input", kernel);
     if (B == 0) return spk::ok();
     SPK_REQUIRE(wave && out_wave, SPK_E_ARG, "spk_pool: wave and out_wave are required");
-    const int64_t total = (int64_t)B * C * Ho * Wo;
-    hipLaunchKernelGGL(k_pool, dim3((unsigned)spk::ceil_div(total, 256)), dim3(256), 0, spk::as_stream(stream), wave,
-                       (int64_t)B, T, C, H, W, kernel, stride, pad, Ho, Wo, out_wave, out_t_first);
+    const int64_t per_img = (int64_t)C * Ho * Wo;
+    SPK_REQUIRE(per_img <= 65535LL * 256 && (int64_t)C * H * W < (1LL << 31), SPK_E_RANGE, "spk_pool: image too large");
+    hipLaunchKernelGGL(k_pool, dim3((unsigned)B, (unsigned)spk::ceil_div(per_img, 256)), dim3(256), 0,
+                       spk::as_stream(stream), wave, T, C, H, W, kernel, stride, pad, Ho, Wo, out_wave, out_t_first);
     return spk::check_launch("spk_pool");
 }

@@ -7,12 +7,13 @@
 // the label, punish otherwise, nothing for a silent sample).
 //
 // Batch semantics (the paper leaves batch plasticity open): frozen forward,
-// ordered replay.  One workgroup owns one output feature f, so no two
-// workgroups touch the same weight.  It gathers, in image order, the images
-// whose winners include f (one image has at most one winner per feature),
-// then every thread replays that list on the weights it owns.  The
-// pre-synaptic condition T_j <= T_i is one byte of the cumulative input
-// wave at step t_i.  The arithmetic is double precision in the order
+// ordered replay.  A workgroup owns one output feature f and 256 of its
+// weights, so no two threads touch the same weight.  It gathers, in image
+// order, the images whose winners include f (one image has at most one
+// winner per feature), then every thread replays that list on its weight,
+// fetching the pre-synaptic bytes of the next PF updates while it applies
+// the current ones.  The pre-synaptic condition T_j <= T_i is one byte of
+// the cumulative input wave at step t_i.  The arithmetic is double precision in the order
 //     d = (w-lb)*(ub-w); u = a*d; w = w+u; clamp; round to float
 // so that every update is the exactly rounded value of that expression.
 #include "common.hpp"
@@ -20,39 +21,50 @@
 namespace {
 
 constexpr int CHUNK = 1024;  // images scanned per pass (4 per thread)
+constexpr int PF = 16;       // updates whose pre-synaptic bytes are fetched together
 
-__global__ __launch_bounds__(256) void k_stdp(float *__restrict__ weight, int Cout, int Cin, int K, int pad,
-                                              const uint8_t *__restrict__ pre, int B, int T, int H, int W,
+struct StdpArgs {
+    int Cout, Cin, K, pad, B, T, H, W, k, stabilizer;
+    float a_plus, a_minus, lb, ub;
+};
+
+// Grid: (feature f, chunk of 256 of its Cin*K*K weights).  Each thread owns
+// one weight and replays the feature's update list on it in image order.
+__global__ __launch_bounds__(256) void k_stdp(float *__restrict__ weight, const uint8_t *__restrict__ pre,
                                               const int32_t *__restrict__ winners, const int32_t *__restrict__ n_win,
-                                              int k, const int8_t *__restrict__ reward, float a_plus, float a_minus,
-                                              float lb, float ub, int stabilizer) {
+                                              const int8_t *__restrict__ reward, StdpArgs a) {
 #pragma clang fp contract(off)
     __shared__ int4 upd[CHUNK];   // (image, t, y, x)
     __shared__ int usg[CHUNK];    // +1 / -1
     __shared__ int scan[256];
     __shared__ int total;
     const int f = blockIdx.x, tid = threadIdx.x;
-    const int KK = K * K, Kc = Cin * KK;
-    const int64_t plane = (int64_t)Cin * H * W;
-    const double dlb = lb, dub = ub, dap = a_plus, dam = a_minus;
+    const int KK = a.K * a.K, Kc = a.Cin * KK;
+    const int e = blockIdx.y * 256 + tid;
+    const bool own = e < Kc;
+    const int ci = own ? e / KK : 0, ky = own ? (e % KK) / a.K : 0, kx = own ? e % a.K : 0;
+    const int64_t plane = (int64_t)a.Cin * a.H * a.W;
+    const int64_t cioff = (int64_t)ci * a.H * a.W;
+    const double dlb = a.lb, dub = a.ub, dap = a.a_plus, dam = a.a_minus;
+    float wf = own ? weight[(int64_t)f * Kc + e] : 0.0f;
 
-    for (int b0 = 0; b0 < B; b0 += CHUNK) {
+    for (int b0 = 0; b0 < a.B; b0 += CHUNK) {
         int slot[4], sg[4], mine = 0;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             slot[j] = -1;
             sg[j] = 1;
             const int b = b0 + tid * 4 + j;
-            if (b >= B) continue;
+            if (b >= a.B) continue;
             if (reward) {
                 if (reward[b] == 0) continue;
                 sg[j] = reward[b] > 0 ? 1 : -1;
             }
-            const int nw = min(n_win[b], k);
+            const int nw = min(n_win[b], a.k);
             for (int w = 0; w < nw; ++w)
-                if (winners[((int64_t)b * k + w) * 4] == f) {
-                    const int t = winners[((int64_t)b * k + w) * 4 + 1];
-                    if (t >= 0 && t < T) slot[j] = w;
+                if (winners[((int64_t)b * a.k + w) * 4] == f) {
+                    const int t = winners[((int64_t)b * a.k + w) * 4 + 1];
+                    if (t >= 0 && t < a.T) slot[j] = w;
                     break;
                 }
             mine += slot[j] >= 0;
@@ -72,36 +84,48 @@ __global__ __launch_bounds__(256) void k_stdp(float *__restrict__ weight, int Co
         for (int j = 0; j < 4; ++j)
             if (slot[j] >= 0) {
                 const int b = b0 + tid * 4 + j;
-                const int32_t *o = winners + ((int64_t)b * k + slot[j]) * 4;
+                const int32_t *o = winners + ((int64_t)b * a.k + slot[j]) * 4;
                 upd[off] = make_int4(b, o[1], o[2], o[3]);
                 usg[off] = sg[j];
                 ++off;
             }
         __syncthreads();
         const int n = total;
-        for (int e = tid; e < Kc && n > 0; e += 256) {
-            const int ci = e / KK, ky = (e % KK) / K, kx = e % K;
-            float *wp = weight + (int64_t)f * Kc + e;
-            float wf = *wp;
-            for (int u = 0; u < n; ++u) {
+        if (own && n > 0) {
+            // pre-synaptic bit of update u: the input wave at the winner's step, 0 in the padding
+            auto fetch = [&](int u) -> uint32_t {
+                if (u >= n) return 0u;
                 const int4 q = upd[u];
-                const int iy = q.z + ky - pad, ix = q.w + kx - pad;
-                bool on = false;
-                if (iy >= 0 && iy < H && ix >= 0 && ix < W)
-                    on = pre[((int64_t)q.x * T + q.y) * plane + ((int64_t)ci * H + iy) * W + ix] != 0;
-                const double a = (double)usg[u] * (on ? dap : dam);
-                const double w = (double)wf;
-                const double d = stabilizer ? (w - dlb) * (dub - w) : 1.0;
-                const double du = a * d;
-                double nw = w + du;
-                if (nw < dlb) nw = dlb;
-                if (nw > dub) nw = dub;
-                wf = (float)nw;
+                const int iy = q.z + ky - a.pad, ix = q.w + kx - a.pad;
+                if (iy < 0 || iy >= a.H || ix < 0 || ix >= a.W) return 0u;
+                return pre[((int64_t)q.x * a.T + q.y) * plane + cioff + (int64_t)iy * a.W + ix] != 0;
+            };
+            uint32_t cur[PF], nxt[PF];
+#pragma unroll
+            for (int q = 0; q < PF; ++q) cur[q] = fetch(q);
+            for (int u0 = 0; u0 < n; u0 += PF) {
+#pragma unroll
+                for (int q = 0; q < PF; ++q) nxt[q] = fetch(u0 + PF + q);
+#pragma unroll
+                for (int q = 0; q < PF; ++q) {
+                    if (u0 + q < n) {
+                        const double r = (double)usg[u0 + q] * (cur[q] ? dap : dam);
+                        const double w = (double)wf;
+                        const double d = a.stabilizer ? (w - dlb) * (dub - w) : 1.0;
+                        const double du = r * d;
+                        double nw = w + du;
+                        if (nw < dlb) nw = dlb;
+                        if (nw > dub) nw = dub;
+                        wf = (float)nw;
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < PF; ++q) cur[q] = nxt[q];
             }
-            *wp = wf;
         }
         __syncthreads();
     }
+    if (own) weight[(int64_t)f * Kc + e] = wf;
 }
 
 __global__ __launch_bounds__(256) void k_decide(const int32_t *__restrict__ winners, const int32_t *__restrict__ n_win,
@@ -132,8 +156,11 @@ int stdp_common(float *weight, int Cout, int Cin, int K, int pad, const uint8_t 
     if (B == 0) return spk::ok();
     SPK_REQUIRE(weight && pre_wave && winners && n_winners, SPK_E_ARG,
                 "%s: weight, pre_wave, winners and n_winners are required", name);
-    hipLaunchKernelGGL(k_stdp, dim3(Cout), dim3(256), 0, spk::as_stream(stream), weight, Cout, Cin, K, pad, pre_wave,
-                       B, T, H, W, winners, n_winners, k, reward, a_plus, a_minus, lb, ub, stabilizer);
+    StdpArgs a{Cout, Cin, K, pad, B, T, H, W, k, stabilizer, a_plus, a_minus, lb, ub};
+    const int64_t chunks = spk::ceil_div((int64_t)Cin * K * K, 256);
+    SPK_REQUIRE(chunks <= 65535, SPK_E_RANGE, "%s: kernel too large", name);
+    hipLaunchKernelGGL(k_stdp, dim3(Cout, (unsigned)chunks), dim3(256), 0, spk::as_stream(stream), weight, pre_wave,
+                       winners, n_winners, reward, a);
     return spk::check_launch(name);
 }
 
