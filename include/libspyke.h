@@ -72,7 +72,9 @@ SPK_API const char *spk_last_error(void);
  *               and the entry of rank rho spikes at floor(rho*T/n); other
  *               entries never spike (value T).
  *   wave        u8  [B][T][C][H][W] or NULL: Eq.1 wave of t_first.
- * Limits: 1 <= T <= 255, C*H*W < 2^31, (8 + KF - 1) * W <= 65536.
+ * Limits: 1 <= T <= 255, C*H*W < 2^31, KF <= 31, and the filters plus an
+ * 8-row band of the zero-padded image, as doubles, must fit 64 KiB:
+ * 8*(C*KF*KF + (7+KF)*(W+KF-1)) + 16*C <= 65536 (W <= 346 for 6 filters of 13x13).
  * Workspace: spk_encode_latency_workspace_size(B, C, H, W, T) bytes.      */
 SPK_API size_t spk_encode_latency_workspace_size(int B, int C, int H, int W, int T);
 SPK_API int spk_encode_latency(const uint8_t *image, int B, int H, int W,
@@ -95,7 +97,7 @@ SPK_API int spk_validate_wave(const uint8_t *wave, int B, int T, int C, int H, i
  * "functional Module"; infinite-threshold in-place firing, Eq.5).
  *   wave       u8  [B][T][Cin][H][W], a valid cumulative spike wave
  *              (the result is defined through its first-spike times).
- *   weight     f32 [Cout][Cin][K][K], finite, |w| < 65504.
+ *   weight     f32 [Cout][Cin][K][K], finite.
  *   pad        zero padding of the input (padded neurons never spike);
  *              Ho = H + 2*pad - K + 1, Wo = W + 2*pad - K + 1 (stride 1).
  *   threshold  finite: spike at step t iff P[t] >= threshold;
@@ -103,9 +105,11 @@ SPK_API int spk_validate_wave(const uint8_t *wave, int B, int T, int C, int H, i
  *              t = T-1 and only where P[T-1] > 0.
  *   potentials f32 [B][T][Cout][Ho][Wo] or NULL:
  *              P[t,f,y,x] = sum over (ci,ky,kx) of W[f,ci,ky,kx] * S[t,ci,y+ky-pad,x+kx-pad].
- *              Computed on fp16 matrix cores from an exact two-term split of
- *              each weight (relative weight error <= 2^-22) with float
- *              accumulation.
+ *              Computed on fp16 matrix cores: each weight, scaled by a power
+ *              of two fixed by the layer's largest |w|, is split into two
+ *              fp16 terms (relative weight error <= 2^-22 for every weight
+ *              down to 2^-17 times the largest); float accumulation; the
+ *              scaling is undone exactly.
  *   spikes     u8  [B][T][Cout][Ho][Wo] or NULL: 1 where the neuron fires.
  *   t_first    u8  [B][Cout][Ho][Wo]: first firing step, T if silent.
  *   v_first    f32 [B][Cout][Ho][Wo]: potential at t_first, 0 if silent.
@@ -126,6 +130,16 @@ SPK_API int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, int
 SPK_API int spk_pool(const uint8_t *wave, int B, int T, int C, int H, int W,
              int kernel, int stride, int pad,
              uint8_t *out_wave, uint8_t *out_t_first, void *stream);
+
+/* The same pooling computed from first-spike times: t_first u8 [B][C][H][W]
+ * (values >= T never spike) -> out_t_first u8 [B][C][Ho][Wo] = minimum over
+ * the window (T where nothing spikes), and out_wave (or NULL) its Eq.1 wave
+ * u8 [B][T][C][Ho][Wo].  For a valid cumulative wave this equals spk_pool on
+ * that wave (the earliest spike of a window is the minimum first-spike
+ * time), while reading one byte per input neuron instead of T.            */
+SPK_API int spk_pool_first_spike(const uint8_t *t_first, int B, int T, int C, int H, int W,
+                                 int kernel, int stride, int pad,
+                                 uint8_t *out_wave, uint8_t *out_t_first, void *stream);
 
 /* ------------------------------------------------------------------------
  * k winners-take-all with feature-wise and lateral inhibition (sections

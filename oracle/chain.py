@@ -55,29 +55,30 @@ def forward(wl, inputs, weights, images=None):
 
 
 def _fwd_chunk(args):
-    wl, inputs, weights, idx = args
+    wl, inputs, weights, idx, keys = args
     res, _, dec = forward(wl, inputs, weights, idx)
     keep = []
-    for r in res:  # only what plasticity needs, to keep the pipes small
-        keep.append({k: v for k, v in r.items() if k in ("pre_wave", "win", "nw")})
+    for r in res:  # only what is asked for, to keep the pipes small
+        keep.append({k: v for k, v in r.items() if k in keys})
     return keep, dec
 
 
-def forward_for_learning(wl, inputs, weights, workers=1):
-    """Pre-waves, winners and rewards of all images, forward run split over
-    `workers` forked processes (the oracle itself stays single-threaded)."""
+def forward_for_learning(wl, inputs, weights, workers=1, keep=("pre_wave", "win", "nw")):
+    """Per-stage results named in `keep` (default: what plasticity needs) and
+    the decision/reward of all images, the forward run split over `workers`
+    forked processes (the oracle itself stays single-threaded)."""
     chunks = np.array_split(np.arange(wl.B), max(1, workers))
     chunks = [c for c in chunks if len(c)]
     if workers > 1 and len(chunks) > 1:
         import multiprocessing as mp
         with mp.get_context("fork").Pool(len(chunks)) as pool_:
-            parts = pool_.map(_fwd_chunk, [(wl, inputs, weights, c) for c in chunks])
+            parts = pool_.map(_fwd_chunk, [(wl, inputs, weights, c, keep) for c in chunks])
     else:
-        parts = [_fwd_chunk((wl, inputs, weights, c)) for c in chunks]
+        parts = [_fwd_chunk((wl, inputs, weights, c, keep)) for c in chunks]
     res = []
     for si in range(len(wl.stages)):
         d = {}
-        for k in ("pre_wave", "win", "nw"):
+        for k in keep:
             vals = [p[0][si][k] for p in parts if k in p[0][si]]
             if vals:
                 d[k] = np.concatenate(vals)

@@ -43,6 +43,7 @@ _SIGS = {
     "spk_conv_fire_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I]),
     "spk_conv_fire": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z, _P]),
     "spk_pool": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
+    "spk_pool_first_spike": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
     "spk_kwta_workspace_size": (_Z, [_I, _I, _I, _I]),
     "spk_kwta": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _Z, _P]),
     "spk_stdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _F, _F, _F, _F, _I, _P]),
@@ -211,6 +212,19 @@ def spk_pool(wave, kernel, stride=None, pad=0, out_wave=None, out_t_first=False,
     out_t_first = _out(out_t_first, (B, C, Ho, Wo), torch.uint8, wave.device, "out_t_first")
     _check(_lib.spk_pool(_ptr(wave), B, T, C, H, W, kernel, stride, pad, _ptr(out_wave), _ptr(out_t_first),
                          _stream(stream)))
+    return out_wave, out_t_first
+
+
+def spk_pool_first_spike(t_first, T, kernel, stride=None, pad=0, out_wave=None, out_t_first=None, stream=None):
+    """Pooling of first-spike times u8 [B,C,H,W] -> (out_wave u8 [B,T,C,Ho,Wo], out_t_first u8 [B,C,Ho,Wo])."""
+    stride = kernel if stride is None else stride
+    B, C, H, W = t_first.shape
+    _need(t_first, torch.uint8, (B, C, H, W), "t_first")
+    Ho, Wo = pool_out_size(H, kernel, stride, pad), pool_out_size(W, kernel, stride, pad)
+    out_wave = _out(out_wave, (B, T, C, Ho, Wo), torch.uint8, t_first.device, "out_wave")
+    out_t_first = _out(out_t_first, (B, C, Ho, Wo), torch.uint8, t_first.device, "out_t_first")
+    _check(_lib.spk_pool_first_spike(_ptr(t_first), B, T, C, H, W, kernel, stride, pad, _ptr(out_wave),
+                                     _ptr(out_t_first), _stream(stream)))
     return out_wave, out_t_first
 
 

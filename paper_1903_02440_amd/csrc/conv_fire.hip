@@ -11,16 +11,18 @@
 // Per image this is a GEMM  P_t[pos, f] = A_t[pos, k] * W^T[k, f]  for every
 // t, with a binary A_t generated on the fly from the u8 first-spike map.
 // It runs on the fp16 matrix cores (v_mfma_f32_16x16x32_f16): A_t is exact
-// in fp16 (we use the value 2.0 for a spike, a single bit, and halve the
-// weights instead), and every fp32 weight w/2 is split into hi = fp16(w/2),
-// lo = fp16(w/2 - hi), so each product pair carries 22 significant bits of w;
-// accumulation is fp32.
+// in fp16 (we use the value 2.0 for a spike, a single bit), and every fp32
+// weight, scaled by a power of two so that the layer's largest weight lies in
+// [2^12, 2^13) and halved, is split into hi = fp16(v), lo = fp16(v - hi):
+// each product pair carries 22 significant bits of w for every weight down to
+// 2^-17 times the largest; accumulation is fp32 and the result is scaled back
+// exactly.
 //
 // Pipeline of one call (all on the caller's stream):
 //   1. k_pad_first_spike: wave [B,T,Cin,H,W] -> zero-padded first-spike map
 //      tpad [B,Cin,H+2p,W+2p] (border = T: padding never spikes).
-//   2. k_split_weights: W -> hi/lo fp16 B-operand fragments + the receptive
-//      field offset table koff[k] = (ci*Hp + ky)*Wp + kx.
+//   2. k_weight_absmax + k_split_weights: W -> scaled hi/lo fp16 B-operand
+//      fragments + the receptive field offset table koff[k] = (ci*Hp + ky)*Wp + kx.
 //   3. k_conv_fire: the GEMM for all steps of a block of TB time steps, with
 //      threshold, spike, first-spike time and potential-at-first-spike in the
 //      epilogue; potentials and spikes are stored straight from registers.
@@ -74,13 +76,36 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
     tpad[b * per_img + i] = (uint8_t)t;
 }
 
-// 2. weight fragments.  Fragment (nt, ks, lane) holds, for feature
-// n = nt*16 + lane%16, the 8 taps k = ks*32 + 8*(lane/16) + j.
+// 2. weight fragments.  Every weight is scaled by a power of two
+// s = 2^(12 - E), E = the exponent of max|w|, so the largest scaled weight lies
+// in [2^12, 2^13): then both terms of the split are normal fp16 for every
+// weight down to max|w| * 2^-17, i.e. w*s = hi + lo + e with |e| <= 2^-22 |w*s|.
+// The GEMM result is multiplied back by 1/s (exact).  The factor also carries
+// the 1/2 that compensates the spike operand 2.0.  Fragment (nt, ks, lane)
+// holds, for feature n = nt*16 + lane%16, the 8 taps k = ks*32 + 8*(lane/16) + j.
+__global__ __launch_bounds__(256) void k_weight_absmax(const float *__restrict__ w, int64_t n,
+                                                       unsigned *__restrict__ maxbits) {
+    unsigned m = 0;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+        m = max(m, __float_as_uint(fabsf(w[i])));
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, s, 64));
+    if ((threadIdx.x & 63) == 0 && m) atomicMax(maxbits, m);
+}
+
+__device__ __forceinline__ int weight_scale_exp(unsigned maxbits) {
+    const int E = maxbits ? (int)((maxbits >> 23) & 255u) - 127 : 0;  // subnormal maxima count as 2^-127
+    return 12 - max(-100, min(100, E));
+}
+
 __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__ w, ConvGeom g,
+                                                       const unsigned *__restrict__ maxbits,
                                                        half8 *__restrict__ whi, half8 *__restrict__ wlo,
-                                                       int *__restrict__ koff) {
+                                                       int *__restrict__ koff, float *__restrict__ inv_scale) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t total = (int64_t)g.ntiles * g.ksteps * 64;
+    const int e = weight_scale_exp(*maxbits);
+    if (i == 0) *inv_scale = ldexpf(1.0f, -e);
     if (i < total) {
         const int lane = (int)(i & 63);
         const int64_t r = i >> 6;
@@ -91,8 +116,8 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int k = ks * 32 + (lane >> 4) * 8 + j;
-            // halved (exactly): the spike operand is 2.0, so the products are w * spike
-            const float v = (n < g.Cout && k < g.Kc) ? 0.5f * w[(int64_t)n * g.Kc + k] : 0.0f;
+            // scaled by 2^(e-1): the spike operand is 2.0, so the products are w * 2^e
+            const float v = (n < g.Cout && k < g.Kc) ? ldexpf(w[(int64_t)n * g.Kc + k], e - 1) : 0.0f;
             const _Float16 hv = (_Float16)v;
             const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
             h[j] = hv;
@@ -183,7 +208,8 @@ __device__ __forceinline__ void mfma_kstep(const uint32_t (&tp)[MW][8], const ui
 }
 
 template <int MW, int NW, int TB, bool INF>
-__device__ __forceinline__ void conv_tile(const uint8_t *__restrict__ tpad, const uint4 *frl_all, const int *koff_lds,
+__device__ __forceinline__ void conv_tile(float inv_s, const uint8_t *__restrict__ tpad, const uint4 *frl_all,
+                                          const int *koff_lds,
                                           const half8 *__restrict__ wfh, const half8 *__restrict__ wfl, uint4 *frl_chunk,
                                           bool resident, int kc, const ConvGeom &g, int ng, int mg, bool active,
                                           int tid, int lane, int gq, int c, float *__restrict__ P,
@@ -276,7 +302,7 @@ __device__ __forceinline__ void conv_tile(const uint8_t *__restrict__ tpad, cons
             for (int i = 0; i < MW; ++i)
 #pragma unroll
                 for (int n = 0; n < NW; ++n) {
-                    const f4 v = acc[i][n][t];  // the weights were halved: spikes entered as 2.0
+                    const f4 v = acc[i][n][t] * inv_s;  // undo the weight scaling (a power of two)
                     uint32_t sp = 0;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
@@ -370,10 +396,12 @@ __global__ __launch_bounds__(256, 2) void k_conv_fire(const uint8_t *__restrict_
                                                       const int *__restrict__ koff, ConvGeom g,
                                                       int n_mgroups, int n_mblocks, int n_ngroups, int kc,
                                                       int resident, unsigned *__restrict__ counters,
+                                                      const float *__restrict__ inv_scale,
                                                       float *__restrict__ P, uint8_t *__restrict__ S,
                                                       uint8_t *__restrict__ TF, float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     __shared__ int next_mb;
+    const float inv_s = *inv_scale;
     int *koff_lds = reinterpret_cast<int *>(lds);      // ksteps*32 offsets
     uint4 *frl = lds + (g.ksteps * 32 * 4 + 15) / 16;  // fragments: all K-steps, or a chunk of kc
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -403,7 +431,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_fire(const uint8_t *__restrict_
         const int mb = next_mb;
         if (mb >= mb_hi) break;  // uniform
         const int mg = mb * WAVES + wv;
-        conv_tile<MW, NW, TB, INF>(tpad, frl, koff_lds, wfh, wfl, frl, resident != 0, resident ? g.ksteps : kc, g,
+        conv_tile<MW, NW, TB, INF>(inv_s, tpad, frl, koff_lds, wfh, wfl, frl, resident != 0, resident ? g.ksteps : kc, g,
                                    ng, mg, mg < n_mgroups, tid, lane, gq, c, P, S, TF, VF);
     }
 }
@@ -460,13 +488,14 @@ size_t plan_workspace(const ConvPlan &pl) {
     c.take<half8>(pl.frag_count);
     c.take<half8>(pl.frag_count);
     c.take<int>(pl.koff_count);
-    c.take<unsigned>(MAX_NGROUPS_COUNT);
+    c.take<unsigned>(MAX_NGROUPS_COUNT + 2);  // work counters, max|w| bits, 1/scale
     return spk::align_up(c.off, 256);
 }
 
 template <int MW, int NW, int TB, bool INF>
 void launch_conv(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int *koff, unsigned *counters,
-                 const ConvGeom &g, float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
+                 const float *inv_scale, const ConvGeom &g, float *P, uint8_t *S, uint8_t *TF, float *VF,
+                 hipStream_t st) {
     const int64_t n_mgroups = spk::ceil_div(g.total_mtiles, MW);
     const int64_t n_mblocks = spk::ceil_div(n_mgroups, WAVES);
     const int n_ngroups = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), NW);
@@ -480,11 +509,10 @@ void launch_conv(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const 
     const int64_t want = spk::ceil_div(n_mblocks * n_ngroups, 8);
     const int64_t per_xcd = std::min<int64_t>(spk::ceil_div(std::max<int64_t>(64, n_ngroups), n_ngroups) * n_ngroups,
                                               spk::ceil_div(want, n_ngroups) * n_ngroups);
-    const int nctr = 8 * n_ngroups;  // <= MAX_NGROUPS_COUNT: n_ngroups <= ceil(4096/16/2)
-    hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)spk::ceil_div(nctr, 256)), dim3(256), 0, st, counters, nctr);
+    // the 8 * n_ngroups counters (<= MAX_NGROUPS_COUNT since Cout <= 4096) were zeroed by the caller
     hipLaunchKernelGGL((k_conv_fire<MW, NW, TB, INF>), dim3((unsigned)(per_xcd * 8)), dim3(256), lds, st, tpad, whi,
-                       wlo, koff, g, (int)n_mgroups, (int)n_mblocks, n_ngroups, kc, resident, counters, P, S, TF,
-                       VF);
+                       wlo, koff, g, (int)n_mgroups, (int)n_mblocks, n_ngroups, kc, resident, counters, inv_scale, P,
+                       S, TF, VF);
 }
 
 }  // namespace
@@ -518,27 +546,34 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     half8 *whi = cv.take<half8>(pl.frag_count);
     half8 *wlo = cv.take<half8>(pl.frag_count);
     int *koff = cv.take<int>(pl.koff_count);
-    unsigned *counters = cv.take<unsigned>(MAX_NGROUPS_COUNT);
+    unsigned *counters = cv.take<unsigned>(MAX_NGROUPS_COUNT + 2);
+    unsigned *maxbits = counters + MAX_NGROUPS_COUNT;
+    float *inv_scale = reinterpret_cast<float *>(counters + MAX_NGROUPS_COUNT + 1);
     hipStream_t st = spk::as_stream(stream);
 
     const int64_t per_img = (int64_t)Cin * g.Hp * g.Wp;
     hipLaunchKernelGGL(k_pad_first_spike, dim3((unsigned)B, (unsigned)spk::ceil_div(per_img, 256)), dim3(256), 0, st,
                        wave, g, tpad);
+    hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)spk::ceil_div(MAX_NGROUPS_COUNT + 2, 256)), dim3(256), 0, st,
+                       counters, MAX_NGROUPS_COUNT + 2);
+    const int64_t nw = (int64_t)Cout * g.Kc;
+    hipLaunchKernelGGL(k_weight_absmax, dim3((unsigned)std::min<int64_t>(256, spk::ceil_div(nw, 256))), dim3(256), 0,
+                       st, weight, nw, maxbits);
     const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
-    hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, whi,
-                       wlo, koff);
+    hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, maxbits,
+                       whi, wlo, koff, inv_scale);
     // tile shape: one 16-position tile by two or four 16-feature tiles per wave
     // (two when the layer has at most 32 features), 2 waves per SIMD
     const bool wide = (Cout + 15) / 16 > 2;
     if (g.inf_mode) {
-        if (wide) launch_conv<2, 4, 1, true>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
-        else launch_conv<2, 2, 1, true>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
+        if (wide) launch_conv<2, 4, 1, true>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
+        else launch_conv<2, 2, 1, true>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
     } else if (wide) {
-        launch_conv<1, 4, 8, false>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
+        launch_conv<1, 4, 8, false>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
     } else if (T % 15 == 0) {
-        launch_conv<1, 2, 15, false>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
+        launch_conv<1, 2, 15, false>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
     } else {
-        launch_conv<1, 2, 16, false>(tpad, whi, wlo, koff, counters, g, potentials, spikes, t_first, v_first, st);
+        launch_conv<1, 2, 16, false>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
     }
     return spk::check_launch("spk_conv_fire");
 }

@@ -8,7 +8,7 @@
 //   1. k_filter: same-size cross-correlation of each u8 image with the C
 //      filters (double accumulation over the non-zero taps, one rounding to
 //      float, then values below the threshold set to 0).  One workgroup per
-//      (image, band of 8 rows) stages the band plus its halo in LDS.
+//      (image, band of 8 rows) stages the zero-padded band in LDS.
 //   2. k_rank_select: one workgroup per image finds the T-1 bin boundaries of
 //      the rank-order code by an MSD radix select (8 passes of 8 bits) on the
 //      unique 64-bit keys  (float bits of I) << 32 | ~index  of the positive
@@ -29,23 +29,28 @@ constexpr int MAX_GROUPS = 32;   // bin boundaries resolved per select batch
 constexpr int LDS_KEYS = 12288;  // intensities cached in LDS when N fits
 
 // ------------------------------------------------------------------ filter
+// LDS holds the taps and the zero-padded band of the image as doubles, so the
+// tap loop has no bounds checks; padded pixels contribute +0 terms, which
+// leave every partial sum unchanged (the sums are never -0), so the result
+// equals the sum over the in-image taps in the same ky-then-kx order.
 __global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img, int B, int H, int W,
                                                 const float *__restrict__ filt, int C, int KF, float thr,
                                                 float *__restrict__ out) {
-    extern __shared__ unsigned char smem[];
+    extern __shared__ double smem_d[];
     const int nb = (H + ROWS - 1) / ROWS;
     const int b = blockIdx.x / nb, band = blockIdx.x % nb;
     const int y0 = band * ROWS, p = (KF - 1) / 2;
     const int rows = min(ROWS, H - y0);
-    const int srows = rows + KF - 1;
-    float *sf = reinterpret_cast<float *>(smem);                 // C*KF*KF taps
-    int *bbox = reinterpret_cast<int *>(sf + C * KF * KF);        // C x (y0,y1,x0,x1)
-    uint8_t *sim = reinterpret_cast<uint8_t *>(bbox + 4 * C);     // srows x W pixels
+    const int srows = rows + KF - 1, Wp = W + 2 * p;
+    double *fd = smem_d;                                       // C*KF*KF taps
+    double *sim = fd + C * KF * KF;                            // srows x Wp pixels
+    int *bbox = reinterpret_cast<int *>(sim + srows * Wp);     // C x (y0,y1,x0,x1)
 
-    for (int i = threadIdx.x; i < C * KF * KF; i += blockDim.x) sf[i] = filt[i];
-    for (int i = threadIdx.x; i < srows * W; i += blockDim.x) {
-        const int r = i / W, x = i % W, y = y0 - p + r;
-        sim[i] = (y >= 0 && y < H) ? img[((int64_t)b * H + y) * W + x] : 0;
+    for (int i = threadIdx.x; i < C * KF * KF; i += blockDim.x) fd[i] = (double)filt[i];
+    for (int i = threadIdx.x; i < srows * Wp; i += blockDim.x) {
+        const int r = i / Wp, xp = i - r * Wp;
+        const int y = y0 - p + r, x = xp - p;
+        sim[i] = (y >= 0 && y < H && x >= 0 && x < W) ? (double)img[((int64_t)b * H + y) * W + x] : 0.0;
     }
     __syncthreads();
     // bounding box of the non-zero taps of each channel (zero taps add nothing)
@@ -53,27 +58,27 @@ __global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img,
         int ya = KF, yb = -1, xa = KF, xb = -1;
         for (int ky = 0; ky < KF; ++ky)
             for (int kx = 0; kx < KF; ++kx)
-                if (sf[(c * KF + ky) * KF + kx] != 0.0f) {
+                if (fd[(c * KF + ky) * KF + kx] != 0.0) {
                     ya = min(ya, ky); yb = max(yb, ky); xa = min(xa, kx); xb = max(xb, kx);
                 }
         bbox[4 * c] = ya; bbox[4 * c + 1] = yb; bbox[4 * c + 2] = xa; bbox[4 * c + 3] = xb;
     }
     __syncthreads();
     const int per = rows * W;
-    for (int i = threadIdx.x; i < C * per; i += blockDim.x) {
-        const int c = i / per, r = (i % per) / W, x = i % W;
+    for (int c = 0; c < C; ++c) {
         const int ya = bbox[4 * c], yb = bbox[4 * c + 1], xa = bbox[4 * c + 2], xb = bbox[4 * c + 3];
-        double s = 0.0;
-        for (int ky = ya; ky <= yb; ++ky) {
-            const uint8_t *row = sim + (r + ky) * W;
-            const float *frow = sf + (c * KF + ky) * KF;
-            for (int kx = xa; kx <= xb; ++kx) {
-                const int ix = x + kx - p;
-                if (ix >= 0 && ix < W) s += (double)frow[kx] * (double)row[ix];
+        const double *fc = fd + c * KF * KF;
+        for (int i = threadIdx.x; i < per; i += blockDim.x) {
+            const int r = i / W, x = i - r * W;
+            double s = 0.0;
+            for (int ky = ya; ky <= yb; ++ky) {
+                const double *row = sim + (r + ky) * Wp + x;
+                const double *frow = fc + ky * KF;
+                for (int kx = xa; kx <= xb; ++kx) s += frow[kx] * row[kx];
             }
+            const float v = (float)s;
+            out[(((int64_t)b * C + c) * H + y0 + r) * W + x] = (v < thr) ? 0.0f : v;
         }
-        const float v = (float)s;
-        out[(((int64_t)b * C + c) * H + y0 + r) * W + x] = (v < thr) ? 0.0f : v;
     }
 }
 
@@ -162,16 +167,40 @@ __global__ __launch_bounds__(SEL_THREADS) void k_rank_select(const float *__rest
                 if (g >= 0) atomicAdd(&hist[g][(key >> shift) & 255u], 1u);
             }
             __syncthreads();
-            if (tid < m) {
-                const int g = tgroup[tid];
-                uint32_t r = trank[tid];
-                int d = 255;
-                for (; d > 0; --d) {
-                    const uint32_t h = hist[g][d];
-                    if (r < h) break;
-                    r -= h;
+            // per group, suffix sums over the digits (digit 255 first): one wave per group
+            for (int g = tid >> 6; g < ng; g += SEL_THREADS / 64) {
+                const int lane = tid & 63;
+                uint32_t h[4], loc = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    h[q] = hist[g][4 * lane + q];
+                    loc += h[q];
                 }
-                trank[tid] = r;
+                uint32_t suf = loc;  // sum over lanes >= lane
+#pragma unroll
+                for (int d = 1; d < 64; d <<= 1) {
+                    const uint32_t o = __shfl_down(suf, d, 64);
+                    if (lane + d < 64) suf += o;
+                }
+                uint32_t above = suf - loc;  // digits held by higher lanes
+                for (int q = 3; q >= 0; --q) {
+                    above += h[q];
+                    hist[g][4 * lane + q] = above;  // now: entries with digit >= 4*lane+q
+                }
+            }
+            __syncthreads();
+            if (tid < m) {
+                // the digit d with S[d+1] <= r < S[d], where S[d] = entries with digit >= d
+                const int g = tgroup[tid];
+                const uint32_t r = trank[tid];
+                int lo = 0, hi = 255;  // S[0] > r holds: the rank exists in this group
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (hist[g][mid] > r) lo = mid; else hi = mid - 1;
+                }
+                const int d = lo;
+                const uint32_t above = d < 255 ? hist[g][d + 1] : 0u;
+                trank[tid] = r - above;
                 tprefix[tid] = (tprefix[tid] << 8) | (uint64_t)d;
             }
             __syncthreads();
@@ -320,8 +349,7 @@ extern "C" int spk_encode_latency(const uint8_t *image, int B, int H, int W, con
     if (rc != SPK_OK) return rc;
     SPK_REQUIRE(KF >= 1 && (KF % 2) == 1 && KF <= MAX_KF, SPK_E_RANGE,
                 "spk_encode_latency: filter size %d must be odd and <= %d", KF, MAX_KF);
-    SPK_REQUIRE((int64_t)(ROWS + KF - 1) * W <= 65536, SPK_E_RANGE, "spk_encode_latency: image width %d too large",
-                W);
+
     SPK_REQUIRE(!std::isnan(filter_threshold), SPK_E_ARG, "spk_encode_latency: threshold is NaN");
     if (B == 0) return spk::ok();
     SPK_REQUIRE(image && filters, SPK_E_ARG, "spk_encode_latency: image and filters are required");
@@ -336,8 +364,10 @@ extern "C" int spk_encode_latency(const uint8_t *image, int B, int H, int W, con
     float *I = intensities ? intensities : ws_int;
 
     const int nb = (H + ROWS - 1) / ROWS;
-    const size_t lds = (size_t)C * KF * KF * sizeof(float) + 4 * C * sizeof(int) + (size_t)(ROWS + KF - 1) * W;
-    SPK_REQUIRE(lds <= 65536, SPK_E_RANGE, "spk_encode_latency: %d filters of %dx%d do not fit", C, KF, KF);
+    const size_t lds = ((size_t)C * KF * KF + (size_t)(ROWS + KF - 1) * (W + KF - 1)) * sizeof(double) +
+                       4 * C * sizeof(int);
+    SPK_REQUIRE(lds <= 65536, SPK_E_RANGE, "spk_encode_latency: %d filters of %dx%d on width %d do not fit", C, KF,
+                KF, W);
     hipLaunchKernelGGL(k_filter, dim3((unsigned)(B * nb)), dim3(256), lds, st, image, B, H, W, filters, C, KF,
                        filter_threshold, I);
     if (!t_first && !wave) return spk::check_launch("spk_encode_latency");

@@ -42,7 +42,53 @@ __global__ __launch_bounds__(256) void k_pool(const uint8_t *__restrict__ in, in
     if (out_tf) out_tf[b * per_img + i] = (uint8_t)(T - on);
 }
 
+// Pooling of first-spike maps: grid (image, chunk of 256 of the image's
+// C*Ho*Wo outputs); the minimum over the window, then its T wave bytes.
+__global__ __launch_bounds__(256) void k_pool_first_spike(const uint8_t *__restrict__ tf, int T, int C, int H, int W,
+                                                          int P, int R, int D, int Ho, int Wo,
+                                                          uint8_t *__restrict__ out, uint8_t *__restrict__ out_tf) {
+    const int per_img = C * Ho * Wo;
+    const int i = blockIdx.y * 256 + threadIdx.x;
+    if (i >= per_img) return;
+    const int64_t b = blockIdx.x;
+    const int hw = Ho * Wo;
+    const int c = i / hw, pix = i - c * hw;
+    const int yo = pix / Wo, xo = pix - yo * Wo;
+    const int y0 = yo * R - D, x0 = xo * R - D;
+    const int ya = max(y0, 0), yb = min(y0 + P, H), xa = max(x0, 0), xb = min(x0 + P, W);
+    const uint8_t *src = tf + (b * C + c) * (int64_t)H * W;
+    int m = T;
+    for (int y = ya; y < yb; ++y)
+        for (int x = xa; x < xb; ++x) m = min(m, (int)src[y * W + x]);
+    if (out_tf) out_tf[b * per_img + i] = (uint8_t)m;
+    if (out) {
+        uint8_t *dst = out + b * T * (int64_t)per_img + i;
+        for (int t = 0; t < T; ++t) dst[(int64_t)t * per_img] = (uint8_t)(t >= m);
+    }
+}
+
 }  // namespace
+
+extern "C" int spk_pool_first_spike(const uint8_t *t_first, int B, int T, int C, int H, int W, int kernel,
+                                    int stride, int pad, uint8_t *out_wave, uint8_t *out_t_first, void *stream) {
+    SPK_REQUIRE(B >= 0 && T >= 1 && C >= 1 && H >= 1 && W >= 1, SPK_E_SHAPE, "spk_pool_first_spike: bad sizes");
+    SPK_REQUIRE(T <= 255, SPK_E_RANGE, "spk_pool_first_spike: T=%d > 255", T);
+    SPK_REQUIRE(kernel >= 1 && stride >= 1 && pad >= 0, SPK_E_SHAPE,
+                "spk_pool_first_spike: bad window %d / stride %d / pad %d", kernel, stride, pad);
+    const int Ho = (H + 2 * pad - kernel) / stride + 1, Wo = (W + 2 * pad - kernel) / stride + 1;
+    SPK_REQUIRE(H + 2 * pad >= kernel && W + 2 * pad >= kernel && Ho >= 1 && Wo >= 1, SPK_E_SHAPE,
+                "spk_pool_first_spike: window %d larger than the padded input", kernel);
+    if (B == 0) return spk::ok();
+    SPK_REQUIRE(t_first && (out_wave || out_t_first), SPK_E_ARG,
+                "spk_pool_first_spike: t_first and an output are required");
+    const int64_t per_img = (int64_t)C * Ho * Wo;
+    SPK_REQUIRE(per_img <= 65535LL * 256 && (int64_t)C * H * W < (1LL << 31), SPK_E_RANGE,
+                "spk_pool_first_spike: image too large");
+    hipLaunchKernelGGL(k_pool_first_spike, dim3((unsigned)B, (unsigned)spk::ceil_div(per_img, 256)), dim3(256), 0,
+                       spk::as_stream(stream), t_first, T, C, H, W, kernel, stride, pad, Ho, Wo, out_wave,
+                       out_t_first);
+    return spk::check_launch("spk_pool_first_spike");
+}
 
 extern "C" int spk_pool(const uint8_t *wave, int B, int T, int C, int H, int W, int kernel, int stride, int pad,
                         uint8_t *out_wave, uint8_t *out_t_first, void *stream) {

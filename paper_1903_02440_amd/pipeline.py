@@ -8,7 +8,10 @@ calls on one stream, with no host synchronisation and no allocation inside
 * source: ``spk_encode_latency`` (images + filter bank) or a given wave;
 * each conv stage: ``spk_conv_fire`` then ``spk_kwta`` (the winners feed
   plasticity and, for the last layer, the decision);
-* each pool stage: ``spk_pool``;
+* each pool stage: ``spk_pool_first_spike`` on the first-spike map of the
+  stage below (which equals ``spk_pool`` on its wave whenever that wave is
+  cumulative -- always the case for non-negative weights), or ``spk_pool``
+  on the wave when constructed with ``pool_from_first_spike=False``;
 * after a reward-modulated last layer: ``spk_decide``;
 * learning: ``spk_stdp`` / ``spk_rstdp`` per conv stage, all after the
   forward (frozen-forward, ordered replay within the batch).
@@ -25,7 +28,7 @@ import torch
 
 from . import (pool_out_size, conv_out_size, spk_conv_fire, spk_conv_fire_workspace_size, spk_decide,
                spk_encode_latency, spk_encode_latency_workspace_size, spk_kwta, spk_kwta_workspace_size,
-               spk_pool, spk_rstdp, spk_stdp)
+               spk_pool, spk_pool_first_spike, spk_rstdp, spk_stdp)
 
 
 def _is_conv(st):
@@ -34,8 +37,9 @@ def _is_conv(st):
 
 class Chain:
     def __init__(self, stages, B, T, H, W, cin, source="image", filter_bank=None, filter_threshold=0.0,
-                 n_classes=10, device="cuda", want_potentials=True, want_spikes_all=True):
+                 n_classes=10, device="cuda", want_potentials=True, pool_from_first_spike=True):
         self.stages = list(stages)
+        self.pool_from_first_spike = pool_from_first_spike
         self.B, self.T, self.source = B, T, source
         self.n_classes = n_classes
         self.filter_threshold = filter_threshold
@@ -51,6 +55,7 @@ class Chain:
             C = cin
             self.image = None
         self.input_wave = torch.zeros((B, T, C, H, W), dtype=u8, device=dev)
+        self.input_tf = torch.zeros((B, C, H, W), dtype=u8, device=dev) if source == "image" else None
         self.bufs = []
         c, h, w = C, H, W
         for st in self.stages:
@@ -71,6 +76,7 @@ class Chain:
             else:
                 ho, wo = pool_out_size(h, st.P, st.R, st.D), pool_out_size(w, st.P, st.R, st.D)
                 b["out"] = torch.empty((B, T, c, ho, wo), dtype=u8, device=dev)
+                b["out_tf"] = torch.empty((B, c, ho, wo), dtype=u8, device=dev)
                 h, w = ho, wo
             b["shape_in"] = None
             self.bufs.append(b)
@@ -108,9 +114,9 @@ class Chain:
         if self.source == "image":
             mark("encode", 0)
             spk_encode_latency(self.image, self.bank, self.T, self.filter_threshold, wave=self.input_wave,
-                               t_first=False, intensities=False, workspace=self.workspace, stream=stream)
+                               t_first=self.input_tf, intensities=False, workspace=self.workspace, stream=stream)
             mark("encode", 1)
-        x = self.input_wave
+        x, x_tf = self.input_wave, self.input_tf
         last_conv = None
         for i, (st, b) in enumerate(zip(self.stages, self.bufs)):
             self.pre_waves[i] = x
@@ -123,13 +129,17 @@ class Chain:
                 spk_kwta(b["tf"], b["vf"], self.T, st.k, st.r, winners=b["win"], n_winners=b["nw"],
                          workspace=self.workspace, stream=stream)
                 mark(f"kwta{i}", 1)
-                x = b["S"]
+                x, x_tf = b["S"], b["tf"]
                 last_conv = i
             else:
                 mark(f"pool{i}", 0)
-                spk_pool(x, st.P, st.R, st.D, out_wave=b["out"], out_t_first=False, stream=stream)
+                if self.pool_from_first_spike and x_tf is not None:
+                    spk_pool_first_spike(x_tf, self.T, st.P, st.R, st.D, out_wave=b["out"], out_t_first=b["out_tf"],
+                                         stream=stream)
+                else:
+                    spk_pool(x, st.P, st.R, st.D, out_wave=b["out"], out_t_first=b["out_tf"], stream=stream)
                 mark(f"pool{i}", 1)
-                x = b["out"]
+                x, x_tf = b["out"], b["out_tf"]
         if last_conv is not None and self.stages[last_conv].learn == "rstdp":
             b = self.bufs[last_conv]
             mark("decide", 0)

@@ -125,6 +125,18 @@ def test_pool_parity(case):
     assert_equal(host(otf), orc.first_spike(ref), "pooled t_first")
 
 
+@pytest.mark.parametrize("case", POOL_CASES)
+def test_pool_first_spike_parity(case):
+    B, T, C, H, W, P, R, D = case
+    g = synth.rng(250 + H, 0)
+    tf = synth.times_uniform_or_silent(g, (B, C, H, W), T, 0.7)
+    out, otf = spk.spk_pool_first_spike(dev(tf), T, P, R, D)
+    sync()
+    ref = orc.pool(wave_of(tf, T), P, R, D)
+    assert_equal(host(out), ref, "pooled wave")
+    assert_equal(host(otf), orc.first_spike(ref), "pooled t_first")
+
+
 def test_pool_toy_t2(golden):
     g = golden("t2_pool.txt")
     T = int(g["T"][0])
