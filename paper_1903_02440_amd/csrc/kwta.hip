@@ -10,7 +10,9 @@
 //     bits 63..56  255 - t_first          (earlier spike wins)
 //     bits 55..24  v_first, order-mapped  (larger potential wins)
 //     bits 23..0   2^24 - 1 - index       (lower linear index wins ties)
-// Silent neurons get key 0.  Each feature map is cut into tiles of RB rows.
+// Silent neurons get key 0.  Small maps use tiles of 16 consecutive positions
+// and one wave per image (see "small maps" below); large maps cut each
+// feature map into tiles of RB rows:
 //   1. k_kwta_tiles: the maximum key of every tile (a group of G lanes per
 //      tile, shuffle reduction), written to the workspace.
 //   2. k_kwta_select: one workgroup per image keeps its tile keys in LDS and
@@ -166,6 +168,170 @@ __global__ __launch_bounds__(SEL_THREADS) void k_kwta_select(const uint8_t *__re
     if (tid == 0) n_winners[b] = found;
 }
 
+// ------------------------------------------------------------------ small maps
+// When every image has at most SMALL_TILES tiles of 16 consecutive positions
+// of one feature map, one wave per image does the selection, so all images
+// are in flight at once and no round needs a workgroup barrier.  Each round's
+// argmax scan also retires the previous winner lazily: a tile of its feature
+// is cleared, a tile whose maximum lies in its window is listed (ballot
+// compaction) and then recomputed from global memory, one listed tile per
+// lane with its 16 loads issued together, against the LDS bitmap of all
+// inhibited positions.  Quotients come from magic multipliers
+// (q = umulhi(n, ceil(2^32/d)), exact for the sizes the host admits here).
+constexpr int SMALL_TILES = 4096;  // keeps keys, list and bitmap within 64 KB of LDS
+
+struct KwtaSmall {
+    int B, T, C, HW, W, k, r, tpm, ntiles;  // tpm: 16-position tiles per feature map
+    unsigned mHW, mW;                        // magic multipliers for /HW and /W
+};
+
+__device__ __forceinline__ unsigned qdiv(unsigned n, unsigned m) { return __umulhi(n, m); }
+
+__global__ __launch_bounds__(256) void k_kwta_tiles16(const uint8_t *__restrict__ tf, const float *__restrict__ vf,
+                                                      KwtaSmall g, uint64_t *__restrict__ tilekey) {
+    const uint32_t gt = blockIdx.x * 256u + threadIdx.x;  // < 2^31, checked on the host
+    const uint32_t gid = gt >> 4;
+    const int j = (int)(gt & 15u);
+    const uint32_t total = (uint32_t)g.B * (uint32_t)g.ntiles;
+    const bool live = gid < total;
+    const uint32_t b = live ? gid / (uint32_t)g.ntiles : 0;
+    const int tile = live ? (int)(gid - b * (uint32_t)g.ntiles) : 0;
+    const int f = tile / g.tpm, pos = (tile - f * g.tpm) * 16 + j;
+    uint64_t key = 0;
+    if (live && pos < g.HW) {
+        const int64_t base = (int64_t)b * g.C * g.HW;
+        const int idx = f * g.HW + pos;
+        const int t = tf[base + idx];
+        if (t < g.T) key = kwta_key(t, vf[base + idx], (uint32_t)idx);
+    }
+    key = group_max(key, 16);
+    if (live && j == 0) tilekey[gid] = key;
+}
+
+__device__ __forceinline__ uint64_t recompute16(const uint8_t *__restrict__ tf, const float *__restrict__ vf,
+                                                const KwtaSmall &g, int tile, const uint32_t *inh) {
+    const int f = tile / g.tpm, pos0 = (tile - f * g.tpm) * 16;
+    int tv[16];
+    float vv[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const bool ok = pos0 + j < g.HW;
+        tv[j] = ok ? (int)tf[f * g.HW + pos0 + j] : g.T;
+        vv[j] = ok ? vf[f * g.HW + pos0 + j] : 0.0f;
+    }
+    uint64_t m = 0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const int pos = pos0 + j;
+        if (tv[j] < g.T && !((inh[pos >> 5] >> (pos & 31)) & 1u)) {
+            const uint64_t key = kwta_key(tv[j], vv[j], (uint32_t)(f * g.HW + pos));
+            m = key > m ? key : m;
+        }
+    }
+    return m;
+}
+
+__global__ __launch_bounds__(64) void k_kwta_select_wave(const uint8_t *__restrict__ tf_all,
+                                                         const float *__restrict__ vf_all, KwtaSmall g,
+                                                         const uint64_t *__restrict__ tilekey,
+                                                         int32_t *__restrict__ winners,
+                                                         int32_t *__restrict__ n_winners) {
+    extern __shared__ uint64_t keys[];  // ntiles keys, ntiles list entries, the inhibition bitmap
+    int *list = reinterpret_cast<int *>(keys + g.ntiles);
+    uint32_t *inh = reinterpret_cast<uint32_t *>(list + g.ntiles);
+    const int nwords = (g.HW + 31) / 32;
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int64_t N = (int64_t)g.C * g.HW;
+    const uint8_t *tf = tf_all + (int64_t)b * N;
+    const float *vf = vf_all + (int64_t)b * N;
+    int32_t *win = winners + (int64_t)b * g.k * 4;
+    for (int i = lane; i < g.ntiles; i += 64) keys[i] = tilekey[(int64_t)b * g.ntiles + i];
+    for (int i = lane; i < nwords; i += 64) inh[i] = 0u;
+    for (int i = lane; i < 4 * g.k; i += 64) win[i] = -1;
+    __syncthreads();
+    const uint64_t below = (1ULL << lane) - 1ULL;  // lanes under this one
+    int fw = -1, yw = 0, xw = 0, found = 0;
+    for (int round = 0; round < g.k; ++round) {
+        // scan: retire the previous winner's feature, list the tiles whose
+        // maximum fell in its window, and take the maximum of the rest
+        uint64_t m = 0;
+        int nl = 0;  // wave-uniform
+        for (int i0 = 0; i0 < g.ntiles; i0 += 64) {
+            const int i = i0 + lane;
+            uint64_t key = i < g.ntiles ? keys[i] : 0;
+            bool redo = false;
+            if (key != 0 && fw >= 0) {
+                const unsigned idx = 0xFFFFFFu - (unsigned)(key & 0xFFFFFFu);
+                const unsigned f = qdiv(idx, g.mHW), pos = idx - f * (unsigned)g.HW;
+                const int y = (int)qdiv(pos, g.mW), x = (int)pos - y * g.W;
+                if ((int)f == fw) {
+                    key = 0;
+                    keys[i] = 0;
+                } else if (abs(y - yw) <= g.r && abs(x - xw) <= g.r) {
+                    redo = true;
+                    key = 0;
+                }
+            }
+            const uint64_t mask = __ballot(redo);
+            if (redo) list[nl + __popcll(mask & below)] = i;
+            nl += __popcll(mask);
+            m = key > m ? key : m;
+        }
+        __syncthreads();
+        // recompute the listed tiles, one per lane, their loads in flight together
+        for (int e0 = 0; e0 < nl; e0 += 64) {
+            const int e = e0 + lane;
+            if (e < nl) {
+                const int tile = list[e];
+                const uint64_t key = recompute16(tf, vf, g, tile, inh);
+                keys[tile] = key;
+                m = key > m ? key : m;
+            }
+        }
+        m = spk::wave_max_u64(m);
+        if (m == 0) break;  // uniform
+        const int idx = (int)(0xFFFFFFu - (unsigned)(m & 0xFFFFFFu));
+        const int t = 255 - (int)(m >> 56);
+        fw = (int)qdiv((unsigned)idx, g.mHW);
+        const int pos = idx - fw * g.HW;
+        yw = (int)qdiv((unsigned)pos, g.mW);
+        xw = pos - yw * g.W;
+        if (lane == 0) {
+            win[4 * round + 0] = fw;
+            win[4 * round + 1] = t;
+            win[4 * round + 2] = yw;
+            win[4 * round + 3] = xw;
+        }
+        ++found;
+        const int H = g.HW / g.W;
+        const int ya = max(0, yw - g.r), yb = min(H - 1, yw + g.r);
+        const int xa = max(0, xw - g.r), xb = min(g.W - 1, xw + g.r);
+        const int wh = yb - ya + 1, ww = xb - xa + 1;
+        for (int i = lane; i < wh * ww; i += 64) {
+            const int p = (ya + i / ww) * g.W + xa + i % ww;
+            atomicOr(&inh[p >> 5], 1u << (p & 31));
+        }
+        __syncthreads();
+    }
+    if (lane == 0) n_winners[b] = found;
+}
+
+bool kwta_small(int B, int T, int C, int H, int W, int k, int r, KwtaSmall &s) {
+    const int64_t HW = (int64_t)H * W;
+    const int64_t tpm = (HW + 15) / 16;
+    if (HW > 65536 || C * tpm > SMALL_TILES) return false;
+    auto magic = [](int64_t d) { return (unsigned)(((1ULL << 32) + (uint64_t)d - 1) / (uint64_t)d); };
+    auto exact = [](int64_t d, int64_t n) {  // umulhi(x, ceil(2^32/d)) == x/d for all x < n
+        const uint64_t m = ((1ULL << 32) + (uint64_t)d - 1) / (uint64_t)d;
+        const uint64_t e = m * (uint64_t)d - (1ULL << 32);
+        return (uint64_t)n * e < (1ULL << 32);
+    };
+    if (!exact(HW, (int64_t)C * HW) || !exact(W, HW)) return false;
+    if ((int64_t)B * C * tpm * 16 >= (1LL << 31)) return false;
+    s = KwtaSmall{B, T, C, (int)HW, W, k, r, (int)tpm, (int)(C * tpm), magic(HW), magic(W)};
+    return true;
+}
+
 int kwta_geom(int B, int T, int C, int H, int W, int k, int r, KwtaGeom &g) {
     SPK_REQUIRE(B >= 0 && T >= 1 && C >= 1 && H >= 1 && W >= 1, SPK_E_SHAPE, "spk_kwta: bad sizes");
     SPK_REQUIRE(T <= 255, SPK_E_RANGE, "spk_kwta: T=%d > 255", T);
@@ -197,7 +363,9 @@ int kwta_geom(int B, int T, int C, int H, int W, int k, int r, KwtaGeom &g) {
 extern "C" size_t spk_kwta_workspace_size(int B, int C, int H, int W) {
     KwtaGeom g;
     if (kwta_geom(B, 1, C, H, W, 1, 0, g) != SPK_OK) return 0;
-    return spk::align_up((size_t)B * g.ntiles * sizeof(uint64_t), 256);
+    KwtaSmall sm;
+    const int ntiles = kwta_small(B, 1, C, H, W, 1, 0, sm) ? sm.ntiles : g.ntiles;
+    return spk::align_up((size_t)B * ntiles * sizeof(uint64_t), 256);
 }
 
 extern "C" int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int T, int C, int H, int W, int k,
@@ -214,6 +382,16 @@ extern "C" int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int
                 ws_bytes, need);
     hipStream_t st = spk::as_stream(stream);
     uint64_t *tilekey = static_cast<uint64_t *>(workspace);
+    KwtaSmall sm;
+    if (kwta_small(B, T, C, H, W, k, radius, sm)) {
+        const int64_t threads = (int64_t)B * sm.ntiles * 16;
+        hipLaunchKernelGGL(k_kwta_tiles16, dim3((unsigned)spk::ceil_div(threads, 256)), dim3(256), 0, st, t_first,
+                           v_first, sm, tilekey);
+        const size_t lds = (size_t)sm.ntiles * (sizeof(uint64_t) + sizeof(int)) + (size_t)(sm.HW + 31) / 32 * 4;
+        hipLaunchKernelGGL(k_kwta_select_wave, dim3(B), dim3(64), lds, st, t_first, v_first, sm, tilekey, winners,
+                           n_winners);
+        return spk::check_launch("spk_kwta");
+    }
     const int64_t threads = (int64_t)B * g.ntiles * g.G;
     hipLaunchKernelGGL(k_kwta_tiles, dim3((unsigned)spk::ceil_div(threads, 256)), dim3(256), 0, st, t_first, v_first,
                        g, tilekey);

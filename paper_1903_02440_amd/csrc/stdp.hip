@@ -10,10 +10,10 @@
 // ordered replay.  A workgroup owns one output feature f and 256 of its
 // weights, so no two threads touch the same weight.  It gathers, in image
 // order, the images whose winners include f (one image has at most one
-// winner per feature), then every thread replays that list on its weight,
-// fetching the pre-synaptic bytes of the next PF updates while it applies
-// the current ones.  The pre-synaptic condition T_j <= T_i is one byte of
-// the cumulative input wave at step t_i.  The arithmetic is double precision in the order
+// winner per feature).  Every thread then first fetches, with independent
+// loads, the pre-synaptic bit of each update for its weight (T_j <= T_i is
+// one byte of the cumulative input wave at step t_i) into its column of an
+// LDS bit array, and only then replays the chain of updates on its weight.  The arithmetic is double precision in the order
 //     d = (w-lb)*(ub-w); u = a*d; w = w+u; clamp; round to float
 // so that every update is the exactly rounded value of that expression.
 #include "common.hpp"
@@ -21,7 +21,6 @@
 namespace {
 
 constexpr int CHUNK = 1024;  // images scanned per pass (4 per thread)
-constexpr int PF = 16;       // updates whose pre-synaptic bytes are fetched together
 
 struct StdpArgs {
     int Cout, Cin, K, pad, B, T, H, W, k, stabilizer;
@@ -36,6 +35,7 @@ __global__ __launch_bounds__(256) void k_stdp(float *__restrict__ weight, const 
 #pragma clang fp contract(off)
     __shared__ int4 upd[CHUNK];   // (image, t, y, x)
     __shared__ int usg[CHUNK];    // +1 / -1
+    __shared__ uint32_t bits[CHUNK / 32][256];  // pre-synaptic bits: word u/32 of thread tid
     __shared__ int scan[256];
     __shared__ int total;
     const int f = blockIdx.x, tid = threadIdx.x;
@@ -92,35 +92,37 @@ __global__ __launch_bounds__(256) void k_stdp(float *__restrict__ weight, const 
         __syncthreads();
         const int n = total;
         if (own && n > 0) {
-            // pre-synaptic bit of update u: the input wave at the winner's step, 0 in the padding
-            auto fetch = [&](int u) -> uint32_t {
-                if (u >= n) return 0u;
-                const int4 q = upd[u];
-                const int iy = q.z + ky - a.pad, ix = q.w + kx - a.pad;
-                if (iy < 0 || iy >= a.H || ix < 0 || ix >= a.W) return 0u;
-                return pre[((int64_t)q.x * a.T + q.y) * plane + cioff + (int64_t)iy * a.W + ix] != 0;
-            };
-            uint32_t cur[PF], nxt[PF];
+            // phase 1: the pre-synaptic bit of every update (the input wave at
+            // the winner's step, 0 in the padding), 32 independent loads per word
+            for (int u0 = 0; u0 < n; u0 += 32) {
+                uint32_t word = 0;
 #pragma unroll
-            for (int q = 0; q < PF; ++q) cur[q] = fetch(q);
-            for (int u0 = 0; u0 < n; u0 += PF) {
-#pragma unroll
-                for (int q = 0; q < PF; ++q) nxt[q] = fetch(u0 + PF + q);
-#pragma unroll
-                for (int q = 0; q < PF; ++q) {
-                    if (u0 + q < n) {
-                        const double r = (double)usg[u0 + q] * (cur[q] ? dap : dam);
-                        const double w = (double)wf;
-                        const double d = a.stabilizer ? (w - dlb) * (dub - w) : 1.0;
-                        const double du = r * d;
-                        double nw = w + du;
-                        if (nw < dlb) nw = dlb;
-                        if (nw > dub) nw = dub;
-                        wf = (float)nw;
+                for (int q = 0; q < 32; ++q) {
+                    const int u = u0 + q;
+                    if (u < n) {
+                        const int4 qq = upd[u];
+                        const int iy = qq.z + ky - a.pad, ix = qq.w + kx - a.pad;
+                        if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
+                            word |= (uint32_t)(pre[((int64_t)qq.x * a.T + qq.y) * plane + cioff + (int64_t)iy * a.W +
+                                                   ix] != 0) << q;
                     }
                 }
-#pragma unroll
-                for (int q = 0; q < PF; ++q) cur[q] = nxt[q];
+                bits[u0 >> 5][tid] = word;
+            }
+            // phase 2: the ordered chain of updates on this weight
+            for (int u0 = 0; u0 < n; u0 += 32) {
+                const uint32_t word = bits[u0 >> 5][tid];
+                const int cnt = min(32, n - u0);
+                for (int q = 0; q < cnt; ++q) {
+                    const double r = (double)usg[u0 + q] * (((word >> q) & 1u) ? dap : dam);
+                    const double w = (double)wf;
+                    const double d = a.stabilizer ? (w - dlb) * (dub - w) : 1.0;
+                    const double du = r * d;
+                    double nw = w + du;
+                    if (nw < dlb) nw = dlb;
+                    if (nw > dub) nw = dub;
+                    wf = (float)nw;
+                }
             }
         }
         __syncthreads();

@@ -14,7 +14,10 @@ calls on one stream, with no host synchronisation and no allocation inside
   on the wave when constructed with ``pool_from_first_spike=False``;
 * after a reward-modulated last layer: ``spk_decide``;
 * learning: ``spk_stdp`` / ``spk_rstdp`` per conv stage, all after the
-  forward (frozen-forward, ordered replay within the batch).
+  forward (frozen-forward, ordered replay within the batch).  The layers'
+  updates touch disjoint weights, so with ``concurrent_learn`` they run on
+  side streams (default priority) that fork from and join back into the
+  caller's stream.
 
 A stage list is any sequence of objects with the attributes of
 ``Conv(cin, cout, K, pad, thr, k, r, learn, a_plus, a_minus, lb, ub,
@@ -37,7 +40,8 @@ def _is_conv(st):
 
 class Chain:
     def __init__(self, stages, B, T, H, W, cin, source="image", filter_bank=None, filter_threshold=0.0,
-                 n_classes=10, device="cuda", want_potentials=True, pool_from_first_spike=True):
+                 n_classes=10, device="cuda", want_potentials=True, pool_from_first_spike=True,
+                 concurrent_learn=True):
         self.stages = list(stages)
         self.pool_from_first_spike = pool_from_first_spike
         self.B, self.T, self.source = B, T, source
@@ -85,6 +89,12 @@ class Chain:
         self.decision = torch.empty((B,), dtype=i32, device=dev)
         self.reward = torch.zeros((B,), dtype=torch.int8, device=dev)
         self.pre_waves = [None] * len(self.stages)
+        n_learn = sum(1 for st in self.stages if _is_conv(st) and st.learn is not None)
+        self.concurrent_learn = concurrent_learn and n_learn > 1
+        if self.concurrent_learn:
+            self._side = [torch.cuda.Stream(device=dev) for _ in range(n_learn)]
+            self._fork = torch.cuda.Event()
+            self._joins = [torch.cuda.Event() for _ in range(n_learn)]
 
     # ---------------------------------------------------------------- setup
     def conv_stages(self):
@@ -148,19 +158,35 @@ class Chain:
             mark("decide", 1)
 
     def learn(self, stream=None, hook=None):
-        """Enqueue the plasticity of every learning conv stage (names "stdp<i>")."""
+        """Enqueue the plasticity of every learning conv stage (names "stdp<i>",
+        or one "learn" span when the layers run concurrently)."""
         mark = hook or (lambda name, phase: None)
-        for i, (st, b) in enumerate(zip(self.stages, self.bufs)):
-            if not _is_conv(st) or st.learn is None:
-                continue
-            mark(f"stdp{i}", 0)
+        main = stream if stream is not None else torch.cuda.current_stream()
+        learners = [(i, st, b) for i, (st, b) in enumerate(zip(self.stages, self.bufs))
+                    if _is_conv(st) and st.learn is not None]
+        if self.concurrent_learn:
+            mark("learn", 0)
+            self._fork.record(main)
+        for j, (i, st, b) in enumerate(learners):
+            s = main
+            if self.concurrent_learn:
+                s = self._side[j]
+                s.wait_event(self._fork)
+            else:
+                mark(f"stdp{i}", 0)
             if st.learn == "rstdp":
                 spk_rstdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], self.reward, st.a_plus,
-                          st.a_minus, st.lb, st.ub, st.stabilizer, stream=stream)
+                          st.a_minus, st.lb, st.ub, st.stabilizer, stream=s)
             else:
                 spk_stdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], st.a_plus, st.a_minus, st.lb,
-                         st.ub, st.stabilizer, stream=stream)
-            mark(f"stdp{i}", 1)
+                         st.ub, st.stabilizer, stream=s)
+            if self.concurrent_learn:
+                self._joins[j].record(s)
+                main.wait_event(self._joins[j])
+            else:
+                mark(f"stdp{i}", 1)
+        if self.concurrent_learn:
+            mark("learn", 1)
 
     def step(self, stream=None, hook=None):
         """One pass of the whole hot path over the batch: forward, then plasticity."""
