@@ -53,27 +53,79 @@ struct ConvGeom {
     int vec4;        // HoWo % 4 == 0: 16-byte potential / 4-byte spike stores
 };
 
-// 1. first-spike times of the padded input.  Grid (image, chunk of 256 of
-// the image's Cin*Hp*Wp padded cells); 32-bit index arithmetic.
+// 1. first-spike times of the padded input.  Grid (chunk of padded rows,
+// images).  A chunk is up to PAD_LDS bytes of whole padded rows of one image;
+// its interior cells come from one contiguous range of the input plane.  The
+// workgroup fills an LDS copy of the chunk with T (padding never spikes),
+// counts the ones of every interior cell over the T steps (4 cells per 4-byte
+// load when the wave pointer and the plane size are multiples of 4), drops
+// t_first = T - count into LDS, then writes the chunk out with 16-byte stores.
+// The LDS copy is shifted by the chunk's address mod 16, so LDS and global
+// 16-byte boundaries coincide.  32-bit index arithmetic within an image.
+constexpr int PAD_LDS = 32768;
+
+__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t w) {  // 1 in every nonzero byte
+    return ((((w & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | w) & 0x80808080u) >> 7;
+}
+
 __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restrict__ wave, ConvGeom g,
-                                                         uint8_t *__restrict__ tpad) {
-    const int per_img = g.Cin * g.Hp * g.Wp;
-    const int i = blockIdx.y * 256 + threadIdx.x;
-    if (i >= per_img) return;
-    const int64_t b = blockIdx.x;
-    const int hw = g.Hp * g.Wp;
-    const int ci = i / hw, pix = i - ci * hw;
-    const int py = pix / g.Wp, px = pix - py * g.Wp;
-    const int y = py - g.pad, x = px - g.pad;
-    int t = g.T;
-    if (y >= 0 && y < g.H && x >= 0 && x < g.W) {
-        const int64_t plane = (int64_t)g.Cin * g.H * g.W;
-        const uint8_t *p = wave + b * g.T * plane + ((int64_t)ci * g.H + y) * g.W + x;
-        int s = 0;
-        for (int tt = 0; tt < g.T; ++tt) s += p[tt * plane] != 0;
-        t = g.T - s;  // a cumulative wave has exactly T - t_first ones
+                                                         int rows_per_chunk, int words, uint8_t *__restrict__ tpad) {
+    __shared__ __attribute__((aligned(16))) uint8_t buf[PAD_LDS + 16];
+    const int tid = threadIdx.x;
+    const int plane = g.Cin * g.H * g.W, hw = g.H * g.W;
+    const int rows_img = g.Cin * g.Hp;
+    const int r0 = blockIdx.x * rows_per_chunk;
+    const int nr = min(rows_per_chunk, rows_img - r0);
+    const int nbytes = nr * g.Wp;
+    // the input range [i_begin, i_end) of the chunk's interior rows
+    int ci = r0 / g.Hp, py = r0 - ci * g.Hp;
+    if (py < g.pad) py = g.pad;
+    else if (py >= g.pad + g.H) { ++ci; py = g.pad; }
+    const int i_begin = ci * hw + (py - g.pad) * g.W;
+    ci = (r0 + nr - 1) / g.Hp;
+    py = r0 + nr - 1 - ci * g.Hp;
+    if (py >= g.pad + g.H) py = g.pad + g.H - 1;
+    else if (py < g.pad) { --ci; py = g.pad + g.H - 1; }
+    const int i_end = ci * hw + (py - g.pad + 1) * g.W;
+    const uint32_t tfill = (uint32_t)g.T * 0x01010101u;
+    for (int64_t b = blockIdx.y; b < g.B; b += gridDim.y) {
+        uint8_t *out = tpad + (b * rows_img + r0) * g.Wp;
+        const int shift = (int)((uintptr_t)out & 15);
+        for (int i = tid * 4; i < shift + nbytes; i += 1024) *reinterpret_cast<uint32_t *>(buf + i) = tfill;
+        __syncthreads();
+        const uint8_t *src = wave + b * g.T * plane;
+        for (int w = (i_begin & ~3) + tid * 4; w < i_end; w += 1024) {
+            uint32_t cnt = 0;  // four byte counters (T <= 255)
+            const uint8_t *p = src + w;
+            if (words) {
+#pragma unroll 8
+                for (int tt = 0; tt < g.T; ++tt, p += plane) cnt += nonzero_bytes(*reinterpret_cast<const uint32_t *>(p));
+            } else {
+                for (int tt = 0; tt < g.T; ++tt, p += plane)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        if (w + q >= i_begin && w + q < i_end) cnt += (uint32_t)(p[q] != 0) << (8 * q);
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int i = w + q;
+                if (i < i_begin || i >= i_end) continue;
+                const int c = i / hw, pix = i - c * hw;
+                const int y = pix / g.W, x = pix - y * g.W;
+                // a cumulative wave has exactly T - t_first ones
+                buf[shift + (c * g.Hp + y + g.pad - r0) * g.Wp + x + g.pad] =
+                    (uint8_t)(g.T - (int)((cnt >> (8 * q)) & 0xFFu));
+            }
+        }
+        __syncthreads();
+        const int head = min(nbytes, (16 - shift) & 15);
+        const int body = (nbytes - head) & ~15;
+        for (int i = tid; i < head; i += 256) out[i] = buf[shift + i];
+        for (int i = head + tid * 16; i < head + body; i += 4096)
+            *reinterpret_cast<uint4 *>(out + i) = *reinterpret_cast<const uint4 *>(buf + shift + i);
+        for (int i = head + body + tid; i < nbytes; i += 256) out[i] = buf[shift + i];
+        __syncthreads();
     }
-    tpad[b * per_img + i] = (uint8_t)t;
 }
 
 // 2. weight fragments.  Every weight is scaled by a power of two
@@ -464,7 +516,8 @@ int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, Con
     SPK_REQUIRE((int64_t)Cin * K * K <= 16384, SPK_E_RANGE, "spk_conv_fire: Cin*K*K=%lld > 16384",
                 (long long)Cin * K * K);
     SPK_REQUIRE(Cout <= 4096, SPK_E_RANGE, "spk_conv_fire: Cout=%d > 4096", Cout);
-    SPK_REQUIRE((int64_t)g.Ho * g.Wo < (1LL << 31) && (int64_t)Cin * g.Hp * g.Wp <= 65535LL * 256,
+    SPK_REQUIRE((int64_t)g.Ho * g.Wo < (1LL << 31) && (int64_t)Cin * g.Hp * g.Wp <= 65535LL * 256 &&
+                    g.Wp <= PAD_LDS,
                 SPK_E_RANGE, "spk_conv_fire: image too large");
     // the MFMA kernel addresses the padded first-spike map with 32-bit offsets
     SPK_REQUIRE((int64_t)B * Cin * g.Hp * g.Wp < (1LL << 32), SPK_E_RANGE,
@@ -551,9 +604,12 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     float *inv_scale = reinterpret_cast<float *>(counters + MAX_NGROUPS_COUNT + 1);
     hipStream_t st = spk::as_stream(stream);
 
-    const int64_t per_img = (int64_t)Cin * g.Hp * g.Wp;
-    hipLaunchKernelGGL(k_pad_first_spike, dim3((unsigned)B, (unsigned)spk::ceil_div(per_img, 256)), dim3(256), 0, st,
-                       wave, g, tpad);
+    const int rows_img = Cin * g.Hp;
+    const int rows_per_chunk = std::min(rows_img, PAD_LDS / g.Wp);
+    const int words = ((Cin * H * W) & 3) == 0 && ((uintptr_t)wave & 3) == 0;
+    hipLaunchKernelGGL(k_pad_first_spike, dim3((unsigned)spk::ceil_div(rows_img, rows_per_chunk),
+                                               (unsigned)std::min(B, 65535)),
+                       dim3(256), 0, st, wave, g, rows_per_chunk, words, tpad);
     hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)spk::ceil_div(MAX_NGROUPS_COUNT + 2, 256)), dim3(256), 0, st,
                        counters, MAX_NGROUPS_COUNT + 2);
     const int64_t nw = (int64_t)Cout * g.Kc;

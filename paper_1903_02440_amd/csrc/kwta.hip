@@ -11,7 +11,7 @@
 //     bits 55..24  v_first, order-mapped  (larger potential wins)
 //     bits 23..0   2^24 - 1 - index       (lower linear index wins ties)
 // Silent neurons get key 0.  Small maps use tiles of 16 consecutive positions
-// and one wave per image (see "small maps" below); large maps cut each
+// and one 256-thread workgroup per image (see "small maps" below); large maps cut each
 // feature map into tiles of RB rows:
 //   1. k_kwta_tiles: the maximum key of every tile (a group of G lanes per
 //      tile, shuffle reduction), written to the workspace.
@@ -21,6 +21,8 @@
 //      positions, clear the winner's feature tiles, and recompute only the
 //      tiles whose current maximum fell inside the window -- every other
 //      tile keeps its maximum, since inhibition only removes candidates.
+#include <algorithm>
+
 #include "common.hpp"
 
 namespace {
@@ -170,15 +172,15 @@ __global__ __launch_bounds__(SEL_THREADS) void k_kwta_select(const uint8_t *__re
 
 // ------------------------------------------------------------------ small maps
 // When every image has at most SMALL_TILES tiles of 16 consecutive positions
-// of one feature map, one wave per image does the selection, so all images
-// are in flight at once and no round needs a workgroup barrier.  Each round's
-// argmax scan also retires the previous winner lazily: a tile of its feature
-// is cleared, a tile whose maximum lies in its window is listed (ballot
-// compaction) and then recomputed from global memory, one listed tile per
-// lane with its 16 loads issued together, against the LDS bitmap of all
-// inhibited positions.  Quotients come from magic multipliers
+// of one feature map, one 256-thread workgroup per image keeps all its tile
+// keys in LDS.  Each round's argmax scan also retires the previous winner
+// lazily: a tile of its feature is cleared, a tile whose maximum lies in its
+// window is listed (ballot compaction) and then recomputed from global memory,
+// one listed tile per thread with its loads issued together, against the LDS
+// bitmap of all inhibited positions.  Quotients come from magic multipliers
 // (q = umulhi(n, ceil(2^32/d)), exact for the sizes the host admits here).
-constexpr int SMALL_TILES = 4096;  // keeps keys, list and bitmap within 64 KB of LDS
+constexpr int SMALL_TILES = 4096;  // keys, list and bitmap stay within 64 KB of LDS
+constexpr int SMALL_THREADS = 256;
 
 struct KwtaSmall {
     int B, T, C, HW, W, k, r, tpm, ntiles;  // tpm: 16-position tiles per feature map
@@ -187,77 +189,125 @@ struct KwtaSmall {
 
 __device__ __forceinline__ unsigned qdiv(unsigned n, unsigned m) { return __umulhi(n, m); }
 
-__global__ __launch_bounds__(256) void k_kwta_tiles16(const uint8_t *__restrict__ tf, const float *__restrict__ vf,
-                                                      KwtaSmall g, uint64_t *__restrict__ tilekey) {
-    const uint32_t gt = blockIdx.x * 256u + threadIdx.x;  // < 2^31, checked on the host
-    const uint32_t gid = gt >> 4;
-    const int j = (int)(gt & 15u);
-    const uint32_t total = (uint32_t)g.B * (uint32_t)g.ntiles;
-    const bool live = gid < total;
-    const uint32_t b = live ? gid / (uint32_t)g.ntiles : 0;
-    const int tile = live ? (int)(gid - b * (uint32_t)g.ntiles) : 0;
-    const int f = tile / g.tpm, pos = (tile - f * g.tpm) * 16 + j;
-    uint64_t key = 0;
-    if (live && pos < g.HW) {
-        const int64_t base = (int64_t)b * g.C * g.HW;
-        const int idx = f * g.HW + pos;
-        const int t = tf[base + idx];
-        if (t < g.T) key = kwta_key(t, vf[base + idx], (uint32_t)idx);
+// The 16 first-spike times and potentials of one tile: as four 4-byte and four
+// 16-byte loads when `vec` (map size a multiple of 4 and aligned bases: then
+// every full tile is aligned), else as single loads.
+__device__ __forceinline__ void load_tile16(const uint8_t *__restrict__ tf, const float *__restrict__ vf, int64_t base,
+                                            int n, int T, int vec, int (&tv)[16], float (&vv)[16]) {
+    if (vec && n == 16) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t w = *reinterpret_cast<const uint32_t *>(tf + base + 4 * q);
+            const float4 v = *reinterpret_cast<const float4 *>(vf + base + 4 * q);
+            tv[4 * q + 0] = w & 0xFF; tv[4 * q + 1] = (w >> 8) & 0xFF;
+            tv[4 * q + 2] = (w >> 16) & 0xFF; tv[4 * q + 3] = w >> 24;
+            vv[4 * q + 0] = v.x; vv[4 * q + 1] = v.y; vv[4 * q + 2] = v.z; vv[4 * q + 3] = v.w;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            tv[j] = j < n ? (int)tf[base + j] : T;
+            vv[j] = j < n ? vf[base + j] : 0.0f;
+        }
     }
-    key = group_max(key, 16);
-    if (live && j == 0) tilekey[gid] = key;
+}
+
+// Four lanes per tile, each with 4 consecutive positions, so a wave's loads
+// are contiguous; two shuffle steps combine the quarter maxima.  Grid-stride
+// over the batch's tiles (the stride is a multiple of 4 lanes).
+__global__ __launch_bounds__(256) void k_kwta_tiles16(const uint8_t *__restrict__ tf, const float *__restrict__ vf,
+                                                      KwtaSmall g, int vec, uint64_t *__restrict__ tilekey) {
+    const uint32_t total = (uint32_t)g.B * (uint32_t)g.ntiles * 4u;  // < 2^31, checked on the host
+    const uint32_t stride = gridDim.x * 256u;
+    for (uint32_t g0 = blockIdx.x * 256u; g0 < total; g0 += stride) {  // uniform per workgroup
+        const uint32_t gt = g0 + threadIdx.x;
+        const uint32_t gid = gt >> 2;
+        const int sub = (int)(gt & 3u);
+        const bool live = gt < total;
+        uint64_t m = 0;
+        if (live) {
+            const uint32_t b = gid / (uint32_t)g.ntiles;
+            const int tile = (int)(gid - b * (uint32_t)g.ntiles);
+            const int f = tile / g.tpm, pos0 = (tile - f * g.tpm) * 16 + 4 * sub;
+            const int64_t base = (int64_t)b * g.C * g.HW + (int64_t)f * g.HW + pos0;
+            int tv[4];
+            float vv[4];
+            if (vec && pos0 + 4 <= g.HW) {
+                const uint32_t w = *reinterpret_cast<const uint32_t *>(tf + base);
+                const float4 v = *reinterpret_cast<const float4 *>(vf + base);
+                tv[0] = w & 0xFF; tv[1] = (w >> 8) & 0xFF; tv[2] = (w >> 16) & 0xFF; tv[3] = w >> 24;
+                vv[0] = v.x; vv[1] = v.y; vv[2] = v.z; vv[3] = v.w;
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const bool ok = pos0 + j < g.HW;
+                    tv[j] = ok ? (int)tf[base + j] : g.T;
+                    vv[j] = ok ? vf[base + j] : 0.0f;
+                }
+            }
+            const uint32_t idx0 = (uint32_t)(f * g.HW + pos0);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (tv[j] < g.T) {
+                    const uint64_t key = kwta_key(tv[j], vv[j], idx0 + j);
+                    m = key > m ? key : m;
+                }
+        }
+        m = group_max(m, 4);
+        if (live && sub == 0) tilekey[gid] = m;
+    }
 }
 
 __device__ __forceinline__ uint64_t recompute16(const uint8_t *__restrict__ tf, const float *__restrict__ vf,
-                                                const KwtaSmall &g, int tile, const uint32_t *inh) {
+                                                const KwtaSmall &g, int vec, int tile, const uint32_t *inh) {
     const int f = tile / g.tpm, pos0 = (tile - f * g.tpm) * 16;
+    const int base = f * g.HW + pos0;
     int tv[16];
     float vv[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-        const bool ok = pos0 + j < g.HW;
-        tv[j] = ok ? (int)tf[f * g.HW + pos0 + j] : g.T;
-        vv[j] = ok ? vf[f * g.HW + pos0 + j] : 0.0f;
-    }
+    load_tile16(tf, vf, base, min(16, g.HW - pos0), g.T, vec, tv, vv);
     uint64_t m = 0;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
         const int pos = pos0 + j;
         if (tv[j] < g.T && !((inh[pos >> 5] >> (pos & 31)) & 1u)) {
-            const uint64_t key = kwta_key(tv[j], vv[j], (uint32_t)(f * g.HW + pos));
+            const uint64_t key = kwta_key(tv[j], vv[j], (uint32_t)(base + j));
             m = key > m ? key : m;
         }
     }
     return m;
 }
 
-__global__ __launch_bounds__(64) void k_kwta_select_wave(const uint8_t *__restrict__ tf_all,
-                                                         const float *__restrict__ vf_all, KwtaSmall g,
-                                                         const uint64_t *__restrict__ tilekey,
-                                                         int32_t *__restrict__ winners,
-                                                         int32_t *__restrict__ n_winners) {
-    extern __shared__ uint64_t keys[];  // ntiles keys, ntiles list entries, the inhibition bitmap
-    int *list = reinterpret_cast<int *>(keys + g.ntiles);
-    uint32_t *inh = reinterpret_cast<uint32_t *>(list + g.ntiles);
+__global__ __launch_bounds__(SMALL_THREADS) void k_kwta_select_small(const uint8_t *__restrict__ tf_all,
+                                                                     const float *__restrict__ vf_all, KwtaSmall g,
+                                                                     int vec, const uint64_t *__restrict__ tilekey,
+                                                                     int32_t *__restrict__ winners,
+                                                                     int32_t *__restrict__ n_winners) {
+    extern __shared__ uint64_t keys[];  // ntiles keys, the inhibition bitmap, ntiles list entries
     const int nwords = (g.HW + 31) / 32;
-    const int b = blockIdx.x, lane = threadIdx.x;
+    uint32_t *inh = reinterpret_cast<uint32_t *>(keys + g.ntiles);
+    uint16_t *list = reinterpret_cast<uint16_t *>(inh + nwords);
+    __shared__ uint64_t red[SMALL_THREADS / 64];
+    __shared__ int nlist[2];
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int64_t N = (int64_t)g.C * g.HW;
     const uint8_t *tf = tf_all + (int64_t)b * N;
     const float *vf = vf_all + (int64_t)b * N;
     int32_t *win = winners + (int64_t)b * g.k * 4;
-    for (int i = lane; i < g.ntiles; i += 64) keys[i] = tilekey[(int64_t)b * g.ntiles + i];
-    for (int i = lane; i < nwords; i += 64) inh[i] = 0u;
-    for (int i = lane; i < 4 * g.k; i += 64) win[i] = -1;
+    for (int i = tid; i < g.ntiles; i += SMALL_THREADS) keys[i] = tilekey[(int64_t)b * g.ntiles + i];
+    for (int i = tid; i < nwords; i += SMALL_THREADS) inh[i] = 0u;
+    for (int i = tid; i < 4 * g.k; i += SMALL_THREADS) win[i] = -1;
+    if (tid < 2) nlist[tid] = 0;
     __syncthreads();
     const uint64_t below = (1ULL << lane) - 1ULL;  // lanes under this one
+    const int H = g.HW / g.W;
     int fw = -1, yw = 0, xw = 0, found = 0;
     for (int round = 0; round < g.k; ++round) {
+        int *cnt = &nlist[round & 1];
         // scan: retire the previous winner's feature, list the tiles whose
         // maximum fell in its window, and take the maximum of the rest
         uint64_t m = 0;
-        int nl = 0;  // wave-uniform
-        for (int i0 = 0; i0 < g.ntiles; i0 += 64) {
-            const int i = i0 + lane;
+        for (int i0 = 0; i0 < g.ntiles; i0 += SMALL_THREADS) {
+            const int i = i0 + tid;
             uint64_t key = i < g.ntiles ? keys[i] : 0;
             bool redo = false;
             if (key != 0 && fw >= 0) {
@@ -273,47 +323,54 @@ __global__ __launch_bounds__(64) void k_kwta_select_wave(const uint8_t *__restri
                 }
             }
             const uint64_t mask = __ballot(redo);
-            if (redo) list[nl + __popcll(mask & below)] = i;
-            nl += __popcll(mask);
+            if (mask) {
+                int at = 0;
+                if (lane == 0) at = atomicAdd(cnt, __popcll(mask));
+                at = __shfl(at, 0, 64);
+                if (redo) list[at + __popcll(mask & below)] = (uint16_t)i;
+            }
             m = key > m ? key : m;
         }
         __syncthreads();
-        // recompute the listed tiles, one per lane, their loads in flight together
-        for (int e0 = 0; e0 < nl; e0 += 64) {
-            const int e = e0 + lane;
-            if (e < nl) {
-                const int tile = list[e];
-                const uint64_t key = recompute16(tf, vf, g, tile, inh);
-                keys[tile] = key;
-                m = key > m ? key : m;
-            }
+        // recompute the listed tiles, one per thread
+        const int nl = *cnt;
+        for (int e = tid; e < nl; e += SMALL_THREADS) {
+            const int tile = list[e];
+            const uint64_t key = recompute16(tf, vf, g, vec, tile, inh);
+            keys[tile] = key;
+            m = key > m ? key : m;
         }
         m = spk::wave_max_u64(m);
-        if (m == 0) break;  // uniform
-        const int idx = (int)(0xFFFFFFu - (unsigned)(m & 0xFFFFFFu));
-        const int t = 255 - (int)(m >> 56);
+        if (lane == 0) red[wv] = m;
+        __syncthreads();
+        uint64_t best = 0;
+#pragma unroll
+        for (int w = 0; w < SMALL_THREADS / 64; ++w) best = red[w] > best ? red[w] : best;
+        if (tid == 0) nlist[(round + 1) & 1] = 0;  // the other counter: last read before the previous barrier
+        if (best == 0) break;  // uniform: every thread read the same red[]
+        const int idx = (int)(0xFFFFFFu - (unsigned)(best & 0xFFFFFFu));
+        const int t = 255 - (int)(best >> 56);
         fw = (int)qdiv((unsigned)idx, g.mHW);
         const int pos = idx - fw * g.HW;
         yw = (int)qdiv((unsigned)pos, g.mW);
         xw = pos - yw * g.W;
-        if (lane == 0) {
+        if (tid == 0) {
             win[4 * round + 0] = fw;
             win[4 * round + 1] = t;
             win[4 * round + 2] = yw;
             win[4 * round + 3] = xw;
         }
         ++found;
-        const int H = g.HW / g.W;
         const int ya = max(0, yw - g.r), yb = min(H - 1, yw + g.r);
         const int xa = max(0, xw - g.r), xb = min(g.W - 1, xw + g.r);
         const int wh = yb - ya + 1, ww = xb - xa + 1;
-        for (int i = lane; i < wh * ww; i += 64) {
+        for (int i = tid; i < wh * ww; i += SMALL_THREADS) {
             const int p = (ya + i / ww) * g.W + xa + i % ww;
             atomicOr(&inh[p >> 5], 1u << (p & 31));
         }
         __syncthreads();
     }
-    if (lane == 0) n_winners[b] = found;
+    if (tid == 0) n_winners[b] = found;
 }
 
 bool kwta_small(int B, int T, int C, int H, int W, int k, int r, KwtaSmall &s) {
@@ -384,12 +441,14 @@ extern "C" int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int
     uint64_t *tilekey = static_cast<uint64_t *>(workspace);
     KwtaSmall sm;
     if (kwta_small(B, T, C, H, W, k, radius, sm)) {
-        const int64_t threads = (int64_t)B * sm.ntiles * 16;
-        hipLaunchKernelGGL(k_kwta_tiles16, dim3((unsigned)spk::ceil_div(threads, 256)), dim3(256), 0, st, t_first,
-                           v_first, sm, tilekey);
-        const size_t lds = (size_t)sm.ntiles * (sizeof(uint64_t) + sizeof(int)) + (size_t)(sm.HW + 31) / 32 * 4;
-        hipLaunchKernelGGL(k_kwta_select_wave, dim3(B), dim3(64), lds, st, t_first, v_first, sm, tilekey, winners,
-                           n_winners);
+        const int64_t threads = (int64_t)B * sm.ntiles * 4;
+        const int vec = (sm.HW % 4) == 0 && ((uintptr_t)t_first & 3) == 0 && ((uintptr_t)v_first & 15) == 0;
+        hipLaunchKernelGGL(k_kwta_tiles16, dim3((unsigned)std::min<int64_t>(spk::ceil_div(threads, 256), 8192)),
+                           dim3(256), 0, st, t_first,
+                           v_first, sm, vec, tilekey);
+        const size_t lds = (size_t)sm.ntiles * (sizeof(uint64_t) + sizeof(uint16_t)) + (size_t)(sm.HW + 31) / 32 * 4;
+        hipLaunchKernelGGL(k_kwta_select_small, dim3(B), dim3(SMALL_THREADS), lds, st, t_first, v_first, sm, vec,
+                           tilekey, winners, n_winners);
         return spk::check_launch("spk_kwta");
     }
     const int64_t threads = (int64_t)B * g.ntiles * g.G;

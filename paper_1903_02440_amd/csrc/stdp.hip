@@ -61,12 +61,12 @@ __global__ __launch_bounds__(256) void k_stdp(float *__restrict__ weight, const 
                 sg[j] = reward[b] > 0 ? 1 : -1;
             }
             const int nw = min(n_win[b], a.k);
-            for (int w = 0; w < nw; ++w)
-                if (winners[((int64_t)b * a.k + w) * 4] == f) {
-                    const int t = winners[((int64_t)b * a.k + w) * 4 + 1];
-                    if (t >= 0 && t < a.T) slot[j] = w;
-                    break;
-                }
+            const int32_t *wb = winners + (int64_t)b * a.k * 4;
+            // every record is read (no early exit), so the loads overlap
+            for (int w = 0; w < a.k; ++w) {
+                const int fw = wb[4 * w], t = wb[4 * w + 1];
+                if (w < nw && fw == f && slot[j] < 0 && t >= 0 && t < a.T) slot[j] = w;
+            }
             mine += slot[j] >= 0;
         }
         // block exclusive scan of the per-thread counts keeps image order
@@ -93,21 +93,25 @@ __global__ __launch_bounds__(256) void k_stdp(float *__restrict__ weight, const 
         const int n = total;
         if (own && n > 0) {
             // phase 1: the pre-synaptic bit of every update (the input wave at
-            // the winner's step, 0 in the padding), 32 independent loads per word
+            // the winner's step, 0 in the padding).  The 32 loads of a word are
+            // unconditional (a masked-off one reads the wave's first byte), so
+            // they are all in flight before the first is used.
             for (int u0 = 0; u0 < n; u0 += 32) {
-                uint32_t word = 0;
+                uint8_t v[32];
+                uint32_t ok = 0;
 #pragma unroll
                 for (int q = 0; q < 32; ++q) {
-                    const int u = u0 + q;
-                    if (u < n) {
-                        const int4 qq = upd[u];
-                        const int iy = qq.z + ky - a.pad, ix = qq.w + kx - a.pad;
-                        if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
-                            word |= (uint32_t)(pre[((int64_t)qq.x * a.T + qq.y) * plane + cioff + (int64_t)iy * a.W +
-                                                   ix] != 0) << q;
-                    }
+                    const int4 qq = upd[min(u0 + q, n - 1)];
+                    const int iy = qq.z + ky - a.pad, ix = qq.w + kx - a.pad;
+                    const bool in = u0 + q < n && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
+                    const int64_t at = ((int64_t)qq.x * a.T + qq.y) * plane + cioff + (int64_t)iy * a.W + ix;
+                    v[q] = pre[in ? at : 0];
+                    ok |= (uint32_t)in << q;
                 }
-                bits[u0 >> 5][tid] = word;
+                uint32_t word = 0;
+#pragma unroll
+                for (int q = 0; q < 32; ++q) word |= (uint32_t)(v[q] != 0) << q;
+                bits[u0 >> 5][tid] = word & ok;
             }
             // phase 2: the ordered chain of updates on this weight
             for (int u0 = 0; u0 < n; u0 += 32) {

@@ -24,6 +24,17 @@ def host(t):
     return t.cpu().numpy()
 
 
+def dev_shifted(a, shift=1):
+    """A device copy of `a` that starts `shift` elements into its allocation,
+    so that its address is not aligned to the element group the kernels'
+    wide loads use."""
+    a = np.ascontiguousarray(a)
+    flat = torch.empty(a.size + shift, dtype=torch.from_numpy(a[:0].reshape(-1)).dtype, device="cuda")
+    view = flat[shift:].view(a.shape)
+    view.copy_(torch.from_numpy(a))
+    return view
+
+
 def sync():
     torch.cuda.synchronize()
 
@@ -107,6 +118,18 @@ def test_conv_fire_deterministic_and_optional_outputs():
     assert torch.equal(tf, a[2]) and torch.equal(vf, a[3])
 
 
+def test_conv_fire_unaligned_wave():
+    B, T, Cin, H, W, Cout, K, pad = 2, 15, 6, 28, 28, 30, 5, 2
+    g = synth.rng(8, 1)
+    wave = wave_of(synth.times_uniform_or_silent(g, (B, Cin, H, W), T, 0.5), T)
+    Wt = synth.dyadic_weights(g, (Cout, Cin, K, K), Cin * K * K)
+    out = spk.spk_conv_fire(dev_shifted(wave), dev(Wt), pad, 15.0)
+    sync()
+    ref = orc.conv_fire(wave, Wt, pad, 15.0)
+    for x, r, name in zip(out, ref, ("P", "S", "t_first", "v_first")):
+        assert_equal(host(x), r, name)
+
+
 # ---------------------------------------------------------------- pool
 POOL_CASES = [(3, 15, 30, 28, 28, 2, 2, 0), (2, 15, 250, 14, 14, 3, 3, 0), (2, 30, 4, 160, 250, 7, 6, 0),
               (2, 7, 3, 9, 10, 3, 2, 1), (1, 5, 2, 5, 5, 5, 1, 2), (2, 3, 1, 1, 1, 1, 1, 0)]
@@ -167,6 +190,17 @@ def test_kwta_parity(case, ties):
     B, T, C, H, W, k, r = case
     tf, vf = kwta_inputs(C + H, B, T, C, H, W, ties)
     win, nw = spk.spk_kwta(dev(tf), dev(vf), T, k, r)
+    sync()
+    rw, rn = orc.kwta(tf, vf, T, k, r)
+    assert_equal(host(nw), rn, "n_winners")
+    assert_equal(host(win), rw, "winners")
+
+
+@pytest.mark.parametrize("case", KWTA_CASES[:2])
+def test_kwta_unaligned_inputs(case):
+    B, T, C, H, W, k, r = case
+    tf, vf = kwta_inputs(C + H + 1, B, T, C, H, W, False)
+    win, nw = spk.spk_kwta(dev_shifted(tf), dev_shifted(vf), T, k, r)
     sync()
     rw, rn = orc.kwta(tf, vf, T, k, r)
     assert_equal(host(nw), rn, "n_winners")
