@@ -42,7 +42,7 @@ def step_bytes(wl):
     out = {}
     c, h, w = (6 if wl.bank == "dog" else 4) if wl.source == "image" else wl.cin, wl.H, wl.W
     if wl.source == "image":
-        out["encode"] = B * h * w + B * T * c * h * w
+        out["encode"] = B * h * w + B * T * c * h * w + B * c * h * w
     for i, st in enumerate(wl.stages):
         if hasattr(st, "cout"):
             nb, ho, wo = conv_call_bytes(B, T, c, h, w, st)
@@ -53,16 +53,31 @@ def step_bytes(wl):
             c, h, w = st.cout, ho, wo
         else:
             ho, wo = (h + 2 * st.D - st.P) // st.R + 1, (w + 2 * st.D - st.P) // st.R + 1
-            out[f"pool{i}"] = B * T * c * h * w + B * T * c * ho * wo
+            # first-spike pooling: one byte per input neuron in, the wave and first-spike map out
+            out[f"pool{i}"] = B * c * h * w + B * T * c * ho * wo + B * c * ho * wo
             h, w = ho, wo
     return out
 
 
-def source_hash(paths):
-    h = hashlib.sha256()
-    for p in paths:
-        h.update(open(os.path.join(ROOT, p), "rb").read())
-    return h.hexdigest()[:16]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_fire_S2_mnist3layer_traffic.md")
+CONV_SRC = os.path.join(ROOT, "paper_1903_02440_amd", "csrc", "conv_fire.hip")
+
+
+def read_traffic(workload, call):
+    """HBM bytes per call measured with rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by
+    a plain copy's counts), or None when they were taken on another workload or
+    call, or before the kernel source last changed."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and line.startswith("    "):
+            k, v = line.strip().split(":", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(CONV_SRC, "rb").read()).hexdigest()[:16]
+    if kv.get("conv_fire_source_sha256_16") != sha or kv.get("workload") != workload or kv.get("call") != call:
+        return None
+    return int(kv["traffic_bytes_per_call"])
 
 
 def cpu_baseline(wl, inp, budget_s):
@@ -102,6 +117,18 @@ def cpu_baseline(wl, inp, budget_s):
                       f"single-threaded C oracle, {t_used:.1f} s"}
 
 
+def copy_probe(nbytes):
+    """A plain copy kernel of known size: reads and writes nbytes per launch."""
+    import torch
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes, "launches": 5}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -110,7 +137,13 @@ def main():
     ap.add_argument("--workload", type=int, default=2, help="1..5 (2 = the 3-layer network, the headline)")
     ap.add_argument("--batch", type=int, default=None, help="override the workload's batch")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle baseline budget (0 = skip)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES bytes 5 times (the reference "
+                         "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures a single GPU (asked for {args.gpus} GPUs, WORLD_SIZE={world}); "
@@ -183,13 +216,7 @@ def main():
 
     ms_per_step = 1000.0 * elapsed / args.steps
     achieved = nbytes[dominant] / (dom_avg_ms * 1e-3) / 1e9
-    traffic = None
-    tfile = os.path.join(ROOT, "profiles", "traffic.json")
-    kernel_src = ["paper_1903_02440_amd/csrc/conv_fire.hip"]
-    if os.path.exists(tfile):
-        t = json.load(open(tfile))
-        if t.get("source_sha") == source_hash(kernel_src) and t.get("workload") == wl.name and t.get("call") == dominant:
-            traffic = t.get("bytes")
+    traffic = read_traffic(wl.name, dominant)
     total_bytes = sum(nbytes.values())
     rec = {
         "metric": "images/sec and synaptic events/sec (conv_fire+kWTA+STDP) on 1 MI355X",
