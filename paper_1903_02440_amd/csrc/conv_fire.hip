@@ -6,26 +6,28 @@
 //
 // Formulation.  For output neuron (f, y, x) and step t
 //     P[t,f,y,x] = sum_k W[f,k] * [tp_k <= t]
-// where k = (ci, ky, kx) runs over the receptive field and tp_k is the
-// first-spike step of that input neuron (Eq.1 makes S[t] = [tp <= t]).
-// Per image this is a GEMM  P_t[pos, f] = A_t[pos, k] * W^T[k, f]  for every
-// t, with a binary A_t generated on the fly from the u8 first-spike map.
-// It runs on the fp16 matrix cores (v_mfma_f32_16x16x32_f16): A_t is exact
-// in fp16 (we use the value 2.0 for a spike, a single bit), and every fp32
-// weight, scaled by a power of two so that the layer's largest weight lies in
-// [2^12, 2^13) and halved, is split into hi = fp16(v), lo = fp16(v - hi):
-// each product pair carries 22 significant bits of w for every weight down to
-// 2^-17 times the largest; accumulation is fp32 and the result is scaled back
-// exactly.
+// where k runs over the receptive field and tp_k is the first-spike step of
+// that input neuron (Eq.1 makes S[t] = [tp <= t]).  Per image this is a GEMM
+// P_t[pos, f] = A_t[pos, k] * W^T[k, f] for every t, with a binary A_t made on
+// the fly from the u8 first-spike map.  It runs on the fp16 matrix cores
+// (v_mfma_f32_16x16x32_f16): a spike is fp16 1.0, produced for two taps at
+// once by one packed add with clamping, clamp((1025 + t) - (1024 + tp)), which
+// is 1 exactly when tp <= t and 0 otherwise; every fp32 weight, scaled by a
+// power of two so that the layer's largest |w| lies in [2^12, 2^13), is split
+// into hi = fp16(v), lo = fp16(v - hi), so each product pair carries 22
+// significant bits of w for every weight down to 2^-17 times the largest;
+// accumulation is fp32 and the scale is undone exactly.
 //
 // Pipeline of one call (all on the caller's stream):
-//   1. k_pad_first_spike: wave [B,T,Cin,H,W] -> zero-padded first-spike map
-//      tpad [B,Cin,H+2p,W+2p] (border = T: padding never spikes).
+//   1. k_pad_first_spike: wave [B,T,Cin,H,W] -> zero-padded first-spike map in
+//      channel-last order, tpad [B][H+2p][W+2p][CP] (CP = Cin rounded up to 4
+//      or to a multiple of 8; padding and padded channels hold T = never).
+//      Taps are ordered k = (ky*K + kx)*CP + ci, so the 8 taps a lane feeds to
+//      one MFMA are two 4-byte words of tpad.
 //   2. k_weight_absmax + k_split_weights: W -> scaled hi/lo fp16 B-operand
-//      fragments + the receptive field offset table koff[k] = (ci*Hp + ky)*Wp + kx.
-//   3. k_conv_fire: the GEMM for all steps of a block of TB time steps, with
-//      threshold, spike, first-spike time and potential-at-first-spike in the
-//      epilogue; potentials and spikes are stored straight from registers.
+//      fragments and the per-lane word offsets of every 8-tap group.
+//   3. finite threshold: k_conv_fire_fin (below); threshold = +inf (Eq.5):
+//      k_conv_fire_inf, which computes only the last step.
 #include <algorithm>
 #include <cmath>
 
@@ -37,85 +39,58 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-constexpr int WAVES = 4;  // waves per workgroup
-constexpr int NW_MAX = 4;  // N tiles per wave never exceed this; ntiles is padded to a multiple
+constexpr int NTILE_ALIGN = 4;  // the N tiles (16 features) are padded to a multiple of this
 
 struct ConvGeom {
     int B, T, Cin, H, W, Cout, K, pad;
+    int CP;          // channels per tpad cell (Cin rounded up)
     int Hp, Wp, Ho, Wo, HoWo;
-    int Kc;          // Cin*K*K
-    int ksteps;      // ceil(Kc/32)
-    int ntiles;      // ceil(Cout/16) rounded up to a multiple of NW_MAX
+    int ksteps;      // ceil(K*K*CP / 32)
+    int ntiles;      // ceil(Cout/16) rounded up to NTILE_ALIGN
     int mt_per_img;  // ceil(HoWo/16)
     int64_t total_mtiles;
     float thr;
-    int inf_mode;
-    int vec4;        // HoWo % 4 == 0: 16-byte potential / 4-byte spike stores
 };
 
-// 1. first-spike times of the padded input.  Grid (chunk of padded rows,
-// images).  A chunk is up to PAD_LDS bytes of whole padded rows of one image;
-// its interior cells come from one contiguous range of the input plane.  The
-// workgroup fills an LDS copy of the chunk with T (padding never spikes),
-// counts the ones of every interior cell over the T steps (4 cells per 4-byte
-// load when the wave pointer and the plane size are multiples of 4), drops
-// t_first = T - count into LDS, then writes the chunk out with 16-byte stores.
-// The LDS copy is shifted by the chunk's address mod 16, so LDS and global
-// 16-byte boundaries coincide.  32-bit index arithmetic within an image.
+// ------------------------------------------------------------------ 1. padded first-spike map
+// Grid (chunk of padded rows, images).  A chunk is up to PAD_LDS bytes of
+// whole padded rows (Wp*CP bytes each) of one image, contiguous in tpad.  The
+// workgroup fills an LDS copy with T, writes T - (number of ones over the T
+// steps) for every interior (ci, y, x) of the chunk (byte loads, consecutive
+// threads on consecutive x), then stores the chunk with 16-byte stores; the
+// LDS copy is shifted by the chunk's address mod 16 so that LDS and global
+// 16-byte boundaries coincide.
 constexpr int PAD_LDS = 32768;
 
-__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t w) {  // 1 in every nonzero byte
-    return ((((w & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | w) & 0x80808080u) >> 7;
-}
-
 __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restrict__ wave, ConvGeom g,
-                                                         int rows_per_chunk, int words, uint8_t *__restrict__ tpad) {
+                                                         int rows_per_chunk, uint8_t *__restrict__ tpad) {
     __shared__ __attribute__((aligned(16))) uint8_t buf[PAD_LDS + 16];
     const int tid = threadIdx.x;
-    const int plane = g.Cin * g.H * g.W, hw = g.H * g.W;
-    const int rows_img = g.Cin * g.Hp;
+    const int row_bytes = g.Wp * g.CP;
     const int r0 = blockIdx.x * rows_per_chunk;
-    const int nr = min(rows_per_chunk, rows_img - r0);
-    const int nbytes = nr * g.Wp;
-    // the input range [i_begin, i_end) of the chunk's interior rows
-    int ci = r0 / g.Hp, py = r0 - ci * g.Hp;
-    if (py < g.pad) py = g.pad;
-    else if (py >= g.pad + g.H) { ++ci; py = g.pad; }
-    const int i_begin = ci * hw + (py - g.pad) * g.W;
-    ci = (r0 + nr - 1) / g.Hp;
-    py = r0 + nr - 1 - ci * g.Hp;
-    if (py >= g.pad + g.H) py = g.pad + g.H - 1;
-    else if (py < g.pad) { --ci; py = g.pad + g.H - 1; }
-    const int i_end = ci * hw + (py - g.pad + 1) * g.W;
+    const int nr = min(rows_per_chunk, g.Hp - r0);
+    const int nbytes = nr * row_bytes;
+    const int hw = g.H * g.W;
+    // interior input rows of the chunk
+    const int y_lo = max(r0 - g.pad, 0), y_hi = min(r0 + nr - g.pad, g.H);
+    const int ncell = y_hi > y_lo ? g.Cin * (y_hi - y_lo) * g.W : 0;
     const uint32_t tfill = (uint32_t)g.T * 0x01010101u;
     for (int64_t b = blockIdx.y; b < g.B; b += gridDim.y) {
-        uint8_t *out = tpad + (b * rows_img + r0) * g.Wp;
+        uint8_t *out = tpad + (b * g.Hp + r0) * (int64_t)row_bytes;
         const int shift = (int)((uintptr_t)out & 15);
         for (int i = tid * 4; i < shift + nbytes; i += 1024) *reinterpret_cast<uint32_t *>(buf + i) = tfill;
         __syncthreads();
-        const uint8_t *src = wave + b * g.T * plane;
-        for (int w = (i_begin & ~3) + tid * 4; w < i_end; w += 1024) {
-            uint32_t cnt = 0;  // four byte counters (T <= 255)
-            const uint8_t *p = src + w;
-            if (words) {
-#pragma unroll 8
-                for (int tt = 0; tt < g.T; ++tt, p += plane) cnt += nonzero_bytes(*reinterpret_cast<const uint32_t *>(p));
-            } else {
-                for (int tt = 0; tt < g.T; ++tt, p += plane)
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        if (w + q >= i_begin && w + q < i_end) cnt += (uint32_t)(p[q] != 0) << (8 * q);
-            }
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int i = w + q;
-                if (i < i_begin || i >= i_end) continue;
-                const int c = i / hw, pix = i - c * hw;
-                const int y = pix / g.W, x = pix - y * g.W;
-                // a cumulative wave has exactly T - t_first ones
-                buf[shift + (c * g.Hp + y + g.pad - r0) * g.Wp + x + g.pad] =
-                    (uint8_t)(g.T - (int)((cnt >> (8 * q)) & 0xFFu));
-            }
+        const uint8_t *src = wave + b * g.T * (int64_t)g.Cin * hw;
+        for (int i = tid; i < ncell; i += 256) {
+            const int x = i % g.W, rest = i / g.W;
+            const int yy = rest % (y_hi - y_lo), ci = rest / (y_hi - y_lo);
+            const int y = y_lo + yy;
+            const uint8_t *p = src + ci * hw + y * g.W + x;
+            int cnt = 0;
+#pragma unroll 5
+            for (int t = 0; t < g.T; ++t) cnt += p[(int64_t)t * g.Cin * hw] != 0;
+            // a cumulative wave has exactly T - t_first ones
+            buf[shift + ((y + g.pad - r0) * g.Wp + x + g.pad) * g.CP + ci] = (uint8_t)(g.T - cnt);
         }
         __syncthreads();
         const int head = min(nbytes, (16 - shift) & 15);
@@ -128,13 +103,13 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
     }
 }
 
-// 2. weight fragments.  Every weight is scaled by a power of two
-// s = 2^(12 - E), E = the exponent of max|w|, so the largest scaled weight lies
-// in [2^12, 2^13): then both terms of the split are normal fp16 for every
-// weight down to max|w| * 2^-17, i.e. w*s = hi + lo + e with |e| <= 2^-22 |w*s|.
-// The GEMM result is multiplied back by 1/s (exact).  The factor also carries
-// the 1/2 that compensates the spike operand 2.0.  Fragment (nt, ks, lane)
-// holds, for feature n = nt*16 + lane%16, the 8 taps k = ks*32 + 8*(lane/16) + j.
+// ------------------------------------------------------------------ 2. weight fragments
+// Every weight is scaled by s = 2^e, e = 12 - E with E the exponent of max|w|,
+// so the largest scaled weight lies in [2^12, 2^13): both terms of the split
+// are then normal fp16 for every weight down to max|w| * 2^-17, i.e.
+// w*s = hi + lo + err with |err| <= 2^-22 |w*s|.  The GEMM result is
+// multiplied back by 1/s (exact).  Fragment (nt, ks, lane) holds, for feature
+// n = nt*16 + lane%16, the 8 taps k = ks*32 + 8*(lane/16) + j, j = 0..7.
 __global__ __launch_bounds__(256) void k_weight_absmax(const float *__restrict__ w, int64_t n,
                                                        unsigned *__restrict__ maxbits) {
     unsigned m = 0;
@@ -150,13 +125,19 @@ __device__ __forceinline__ int weight_scale_exp(unsigned maxbits) {
     return 12 - max(-100, min(100, E));
 }
 
+// Tap k of the padded receptive field: cell kyx = k / CP, channel ci = k % CP.
+// koff2[q] holds, for the 8-tap group q = k/8, the tpad byte offsets (relative
+// to the output position's top-left input cell) of its two 4-byte words; with
+// CP >= 8 they are adjacent, with CP == 4 they are the cells 2q and 2q+1.
+// Groups past the receptive field point at offset 0 (their weights are 0).
 __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__ w, ConvGeom g,
                                                        const unsigned *__restrict__ maxbits,
                                                        half8 *__restrict__ whi, half8 *__restrict__ wlo,
-                                                       int *__restrict__ koff, float *__restrict__ inv_scale) {
+                                                       int2 *__restrict__ koff2, float *__restrict__ inv_scale) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t total = (int64_t)g.ntiles * g.ksteps * 64;
     const int e = weight_scale_exp(*maxbits);
+    const int KK = g.K * g.K;
     if (i == 0) *inv_scale = ldexpf(1.0f, -e);
     if (i < total) {
         const int lane = (int)(i & 63);
@@ -168,8 +149,9 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int k = ks * 32 + (lane >> 4) * 8 + j;
-            // scaled by 2^(e-1): the spike operand is 2.0, so the products are w * 2^e
-            const float v = (n < g.Cout && k < g.Kc) ? ldexpf(w[(int64_t)n * g.Kc + k], e - 1) : 0.0f;
+            const int kyx = k / g.CP, ci = k % g.CP;
+            float v = 0.0f;
+            if (n < g.Cout && kyx < KK && ci < g.Cin) v = ldexpf(w[((int64_t)n * g.Cin + ci) * KK + kyx], e);
             const _Float16 hv = (_Float16)v;
             const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
             h[j] = hv;
@@ -178,284 +160,407 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
         whi[i] = h;
         wlo[i] = l;
     }
-    if (i < (int64_t)g.ksteps * 32) {
-        const int k = (int)i;
-        int off = 0;
-        if (k < g.Kc) {
-            const int ci = k / (g.K * g.K), rem = k % (g.K * g.K);
-            const int ky = rem / g.K, kx = rem % g.K;
-            off = (ci * g.Hp + ky) * g.Wp + kx;
+    if (i < (int64_t)g.ksteps * 4) {
+        const int q = (int)i;
+        int2 o{0, 0};
+        auto cell = [&](int kyx) { return kyx < KK ? ((kyx / g.K) * g.Wp + kyx % g.K) * g.CP : 0; };
+        if (g.CP >= 8) {
+            const int k0 = q * 8, kyx = k0 / g.CP;
+            o.x = kyx < KK ? cell(kyx) + k0 % g.CP : 0;
+            o.y = kyx < KK ? o.x + 4 : 0;
+        } else {
+            o.x = cell(2 * q);
+            o.y = cell(2 * q + 1);
         }
-        koff[k] = off;
+        koff2[q] = o;
     }
 }
 
-// 3. the fused GEMM + fire.  A wave owns MW consecutive 16-position M tiles
-// (across the whole batch) and NW 16-feature N tiles, for all time steps,
-// processed TB steps at a time.  Lane l feeds A row l%16 / B column l%16
-// with the 8 taps 8*(l/16)..+7 and receives C[4*(l/16) + j][l%16], j = 0..3:
-// four consecutive positions of one feature.
-//
-// The four waves of a workgroup share their NW feature tiles, so the weight
-// fragments are staged once per workgroup in LDS, KC K-steps at a time; the
-// spike-time gathers of K-step ks+1 are in flight while step ks computes.
-// Steps past T in the last time block are computed but never stored.
-//
-// Block order is XCD-aware: hardware hands consecutive workgroups to the 8
-// XCDs in turn, so block i is remapped to logical block
-// (i % 8) * ceil(nblk / 8) + i / 8.  Each XCD then sweeps a contiguous range
-// of positions, and the partial 128-byte lines at the edges of one block's
-// output runs are completed by its neighbour in the same L2 before they are
-// written back.
-constexpr int KC = 8;                 // K-steps of weight fragments per LDS chunk, at most
-constexpr size_t LDS_BUDGET = 79872;  // per workgroup: two workgroups fit one CU's 160 KiB
-
-template <int MW>
-__device__ __forceinline__ void gather_tp(uint32_t (&tp)[MW][8], int ks, const uint8_t *__restrict__ tpad,
-                                          const uint32_t (&abase)[MW], const int *koff_lds, int gq) {
-    const int *ko = koff_lds + ks * 32 + gq * 8;
-    int o[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) o[j] = ko[j];
-#pragma unroll
-    for (int i = 0; i < MW; ++i)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) tp[i][j] = tpad[abase[i] + (uint32_t)o[j]];
+// ------------------------------------------------------------------ shared MFMA helpers
+// fp16 -(1024 + tp) for the four tap bytes of a word, as two packed pairs.
+__device__ __forceinline__ void neg_times(uint32_t w, uint32_t &lo, uint32_t &hi) {
+    lo = __builtin_amdgcn_perm(0xE4E4E4E4u, w, 0x05010400u);
+    hi = __builtin_amdgcn_perm(0xE4E4E4E4u, w, 0x05030402u);
 }
 
-template <int MW, int NW, int TB>
-__device__ __forceinline__ void mfma_kstep(const uint32_t (&tp)[MW][8], const uint4 *fr, int lane,
-                                           f4 (&acc)[MW][NW][TB], int tb0) {
-    half8 bh[NW], bl[NW];
-#pragma unroll
-    for (int n = 0; n < NW; ++n) {
-        bh[n] = __builtin_bit_cast(half8, fr[(2 * n) * 64 + lane]);
-        bl[n] = __builtin_bit_cast(half8, fr[(2 * n + 1) * 64 + lane]);
-    }
-#pragma unroll
-    for (int i = 0; i < MW; ++i) {
-        // 16-bit lanes: (0x4000 + t - tp) has bit 14 set iff tp <= t (no borrow
-        // crosses the halves since 0x4000 > 255); 0x4000 is fp16 2.0
-        uint32_t d[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) d[q] = (0x4000u + (uint32_t)tb0) * 0x10001u - (tp[i][2 * q] | (tp[i][2 * q + 1] << 16));
-#pragma unroll
-        for (int t = 0; t < TB; ++t) {
-            u4 a;
-            a.x = d[0] & 0x40004000u;
-            a.y = d[1] & 0x40004000u;
-            a.z = d[2] & 0x40004000u;
-            a.w = d[3] & 0x40004000u;
-            const half8 ah = __builtin_bit_cast(half8, a);
-#pragma unroll
-            for (int n = 0; n < NW; ++n)
-                acc[i][n][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh[n], acc[i][n][t], 0, 0, 0);
-#pragma unroll
-            for (int n = 0; n < NW; ++n)
-                acc[i][n][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[n], acc[i][n][t], 0, 0, 0);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) d[q] += 0x10001u;
-        }
-    }
+// Spike operand of 8 taps at step t: clamp((1025 + t) - (1024 + tp)) per tap.
+__device__ __forceinline__ half8 spike_operand(const uint32_t (&xn)[4], uint32_t ct) {
+    u4 a;
+    asm("v_pk_add_f16 %0, %1, %2 clamp" : "=v"(a.x) : "v"(ct), "v"(xn[0]));
+    asm("v_pk_add_f16 %0, %1, %2 clamp" : "=v"(a.y) : "v"(ct), "v"(xn[1]));
+    asm("v_pk_add_f16 %0, %1, %2 clamp" : "=v"(a.z) : "v"(ct), "v"(xn[2]));
+    asm("v_pk_add_f16 %0, %1, %2 clamp" : "=v"(a.w) : "v"(ct), "v"(xn[3]));
+    return __builtin_bit_cast(half8, a);
 }
 
-template <int MW, int NW, int TB, bool INF>
-__device__ __forceinline__ void conv_tile(float inv_s, const uint8_t *__restrict__ tpad, const uint4 *frl_all,
-                                          const int *koff_lds,
-                                          const half8 *__restrict__ wfh, const half8 *__restrict__ wfl, uint4 *frl_chunk,
-                                          bool resident, int kc, const ConvGeom &g, int ng, int mg, bool active,
-                                          int tid, int lane, int gq, int c, float *__restrict__ P,
-                                          uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF) {
-    uint32_t abase[MW];
-    int64_t img[MW];
-    int mpos0[MW];
+// fp16 (1025 + t) in both halves (t <= 1022)
+__device__ __forceinline__ uint32_t step_const(int t) { return (0x6401u + (uint32_t)t) * 0x10001u; }
+
+__device__ __forceinline__ f4 mfma(half8 a, half8 b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// ------------------------------------------------------------------ 3a. finite threshold
+// One workgroup = 4 MFMA waves + 4 store waves, persistent, serving one pair
+// of 16-feature tiles (32 features).  Its tasks are (image, chunk of up to 16
+// position tiles) of one XCD's slice of the task list.  For every block of TB
+// time steps:
+//   * each MFMA wave computes the GEMM of its tiles (local tiles w, w+4, ...)
+//     for the 32 features and TB steps -- spike words read straight from
+//     tpad (L2), weight fragments from LDS (or L2 when they do not fit) --
+//     and writes the scaled potentials into the LDS staging area
+//     [TB][32 features][chunk positions];
+//   * the store waves then fire the staged potentials (threshold, first spike,
+//     potential at the first spike, kept in their registers for the whole
+//     task) and write potentials and spikes of each step as contiguous runs
+//     (one run per feature row; a whole-image chunk is one region), while the
+//     MFMA waves go on with the next block.
+// Keeping every global store in the store waves keeps the MFMA waves' own
+// memory counter free of store acknowledgements, so their operand loads never
+// wait behind the output stream.  Two barriers per block: "staging free"
+// (the store waves are done with the previous block) and "staging full".
+constexpr int FIN_TB = 3;
+constexpr int FIN_CW = 8;          // MFMA waves (waves 0-7)
+constexpr int FIN_MT = 2;          // position tiles per MFMA wave
+constexpr int FIN_SW = 4;          // store waves (waves 8-11)
+constexpr int FIN_THREADS = (FIN_CW + FIN_SW) * 64;
+// position tiles per task at most: 16 with 4-element store groups, 8 with single elements
+__host__ __device__ constexpr int chunk_tiles_max(int G) { return G == 4 ? 16 : 8; }
+
+constexpr int FIN_AW = 16384 / 4 / (FIN_CW * 64);  // words of the staged spike region per MFMA-wave thread (16 KiB)
+
+template <int G, bool BLDS, bool ALDS>
+__global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
+    const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
+    const int2 *__restrict__ koff2, ConvGeom g, int n_pairs, int n_chunks, int chunk_tiles, int np_max,
+    int a_words, const float *__restrict__ inv_scale, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
+    float *__restrict__ VF) {
+    extern __shared__ uint4 lds[];
+    const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
+    const int gq = lane >> 4, c = lane & 15;
+    int2 *koff_l = reinterpret_cast<int2 *>(lds);
+    uint4 *frag_l = lds + (g.ksteps * 4 * 8 + 15) / 16;                  // [ks][n(2)][hi/lo][64] (BLDS)
+    float *stage = reinterpret_cast<float *>(frag_l + (BLDS ? g.ksteps * 4 * 64 : 0));  // [TB][32*np_max]
+    const int stage_t = 32 * np_max;
+    uint32_t *abuf = reinterpret_cast<uint32_t *>(stage + FIN_TB * stage_t);  // 2 buffers x a_words (ALDS)
+    const int row_bytes = g.Wp * g.CP;
+
+    const int x = blockIdx.x % 8, j = blockIdx.x / 8;
+    const int pair = j % n_pairs, r = j / n_pairs, R = (int)(gridDim.x / 8) / n_pairs;
+    const int ntask = g.B * n_chunks;
+    const int per_x = (ntask + 7) / 8;
+    const int t_lo = x * per_x, t_hi = min(ntask, t_lo + per_x);
+    const int f0 = pair * 32;
+    const int nf = min(32, g.Cout - f0);
+
+    // The padded first-spike rows a task reads: rows y_first .. y_last+K-1 of
+    // its image, one contiguous range of tpad (a multiple of 4 bytes).
+    auto region = [&](int task, int &yf, int &w0, int &nw) {
+        const int b = task / n_chunks, ch = task % n_chunks;
+        const int p0 = ch * chunk_tiles * 16;
+        const int np = min(chunk_tiles * 16, g.HoWo - p0);
+        yf = p0 / g.Wo;
+        const int rows = (p0 + np - 1) / g.Wo + g.K - yf;
+        w0 = (int)((((int64_t)b * g.Hp + yf) * row_bytes) >> 2);
+        nw = rows * row_bytes / 4;
+    };
+    auto fetch_region = [&](int task, uint32_t (&v)[FIN_AW]) {
+        int yf, w0, nw;
+        region(task, yf, w0, nw);
+        const uint32_t *src = reinterpret_cast<const uint32_t *>(tpad) + (uint32_t)w0;
 #pragma unroll
-    for (int i = 0; i < MW; ++i) {
-        const int64_t gm = (int64_t)mg * MW + i;
-        const bool v = active && gm < g.total_mtiles;
-        const int64_t b = v ? gm / g.mt_per_img : 0;
-        const int mt = v ? (int)(gm % g.mt_per_img) : 0;
-        const int pos = min(mt * 16 + c, g.HoWo - 1);  // rows past the image are computed, not stored
-        const int y = pos / g.Wo, x = pos % g.Wo;
-        abase[i] = (uint32_t)(((int64_t)b * g.Cin * g.Hp + y) * g.Wp + x);
-        img[i] = v ? b : -1;
-        mpos0[i] = mt * 16 + gq * 4;
+        for (int k = 0; k < FIN_AW; ++k) {
+            const int w = tid + FIN_CW * 64 * k;
+            v[k] = w < nw ? src[w] : 0u;
+        }
+    };
+    auto store_region = [&](const uint32_t (&v)[FIN_AW], uint32_t *dst) {
+#pragma unroll
+        for (int k = 0; k < FIN_AW; ++k) {
+            const int w = tid + FIN_CW * 64 * k;
+            if (w < a_words) dst[w] = v[k];
+        }
+    };
+    if (ALDS && wv < FIN_CW && t_lo + r < t_hi) {
+        uint32_t v[FIN_AW];
+        fetch_region(t_lo + r, v);
+        store_region(v, abuf);
     }
-    // per (tile, feature) store offsets at step 0; a step adds Cout*HoWo
-    const int64_t tstride = (int64_t)g.Cout * g.HoWo;
-    int64_t obase[MW][NW];
-    bool ost[MW][NW];
-#pragma unroll
-    for (int i = 0; i < MW; ++i)
-#pragma unroll
-        for (int n = 0; n < NW; ++n) {
-            const int f = (ng * NW + n) * 16 + c;
-            ost[i][n] = img[i] >= 0 && f < g.Cout && mpos0[i] < g.HoWo;
-            obase[i][n] = ost[i][n] ? (img[i] * g.T * tstride + (int64_t)f * g.HoWo + mpos0[i]) : 0;
+    for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) koff_l[i] = koff2[i];
+    if (BLDS) {
+        for (int i = tid; i < g.ksteps * 4 * 64; i += FIN_THREADS) {
+            const int ln = i & 63, rr = i >> 6;  // rr = (ks*2 + n)*2 + h
+            const int h = rr & 1, n = (rr >> 1) & 1, ks = rr >> 2;
+            const half8 *src = h ? wlo : whi;
+            frag_l[i] = __builtin_bit_cast(uint4, src[((int64_t)(pair * 2 + n) * g.ksteps + ks) * 64 + ln]);
         }
-    const bool full4 = g.vec4 != 0;
+    }
+    __syncthreads();
+    const float inv_s = *inv_scale;
+    const int64_t tplane = (int64_t)g.Cout * g.HoWo;
 
-    int tfirst[MW][NW][4];
-    float vfirst[MW][NW][4];
+    if (wv < FIN_CW) {
+        // ------------------------------------------------ MFMA waves
+        // Every wave computes 4 tiles (local tiles wv, wv+4, wv+8, wv+12); tiles
+        // past the chunk repeat its last position and are never stored, which
+        // keeps the MFMA stream free of branches.
+        const half8 *gh = whi + (int64_t)(pair * 2) * g.ksteps * 64 + lane;
+        const half8 *gl = wlo + (int64_t)(pair * 2) * g.ksteps * 64 + lane;
+        int abuf_sel = 0;
+        for (int task = t_lo + r; task < t_hi; task += R) {
+            const int b = task / n_chunks, ch = task % n_chunks;
+            const int tile0 = ch * chunk_tiles;
+            const int ntl = min(chunk_tiles, g.mt_per_img - tile0);
+            const int pos0 = tile0 * 16;
+            const int np = min(ntl * 16, g.HoWo - pos0);
+            const uint8_t *abase[FIN_MT];
+            uint32_t alds[FIN_MT];
+            int yf_t, w0_t, nw_t;
+            region(task, yf_t, w0_t, nw_t);
+            const uint8_t *abuf_t = reinterpret_cast<const uint8_t *>(abuf + abuf_sel * a_words);
 #pragma unroll
-    for (int i = 0; i < MW; ++i)
-#pragma unroll
-        for (int n = 0; n < NW; ++n)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                tfirst[i][n][j] = g.T;
-                vfirst[i][n][j] = 0.0f;
+            for (int i = 0; i < FIN_MT; ++i) {
+                const int pos = min(pos0 + (wv + FIN_CW * i) * 16 + c, pos0 + np - 1);
+                const int y = pos / g.Wo, xx = pos - y * g.Wo;
+                abase[i] = tpad + (uint32_t)((((int64_t)b * g.Hp + y) * g.Wp + xx) * g.CP);
+                alds[i] = (uint32_t)((y - yf_t) * row_bytes + xx * g.CP);
             }
-
-    const int t_begin = INF ? g.T - 1 : 0;
-    for (int tb0 = t_begin; tb0 < g.T; tb0 += TB) {
-        f4 acc[MW][NW][TB];
+            const bool has_next = ALDS && task + R < t_hi;
+            uint32_t nxt[FIN_AW];
+            if (has_next) fetch_region(task + R, nxt);  // consumed at the end of the task
+            for (int tb0 = 0; tb0 < g.T; tb0 += FIN_TB) {
+                const bool last_block = tb0 + FIN_TB >= g.T;
+                f4 acc[FIN_MT][2][FIN_TB];
 #pragma unroll
-        for (int i = 0; i < MW; ++i)
+                for (int i = 0; i < FIN_MT; ++i)
 #pragma unroll
-            for (int n = 0; n < NW; ++n)
+                    for (int n = 0; n < 2; ++n)
 #pragma unroll
-                for (int t = 0; t < TB; ++t) acc[i][n][t] = f4{0.f, 0.f, 0.f, 0.f};
-
-        for (int k0 = 0; k0 < g.ksteps; k0 += kc) {
-            const int nk = min(kc, g.ksteps - k0);
-            const uint4 *fr = frl_all + (size_t)k0 * NW * 2 * 64;
-            if (!resident) {  // stream this chunk of fragments through LDS (uniform branch)
-                __syncthreads();
-                for (int idx = tid; idx < nk * NW * 2 * 64; idx += 256) {
-                    const int ln = idx & 63, r = idx >> 6;  // r = (ksl*NW + n)*2 + h
-                    const int h = r & 1, n = (r >> 1) % NW, ksl = (r >> 1) / NW;
-                    const half8 *src = h ? wfl : wfh;
-                    frl_chunk[idx] = __builtin_bit_cast(uint4, src[(n * g.ksteps + k0 + ksl) * 64 + ln]);
-                }
-                __syncthreads();
-                fr = frl_chunk;
-            }
-            if (active) {
-                uint32_t ta[MW][8], tb[MW][8];
-                gather_tp<MW>(ta, k0, tpad, abase, koff_lds, gq);
-                for (int kl = 0; kl < nk; kl += 2) {
-                    if (kl + 1 < nk) gather_tp<MW>(tb, k0 + kl + 1, tpad, abase, koff_lds, gq);
-                    mfma_kstep<MW, NW, TB>(ta, fr + kl * NW * 2 * 64, lane, acc, tb0);
-                    if (kl + 1 >= nk) break;
-                    if (kl + 2 < nk) gather_tp<MW>(ta, k0 + kl + 2, tpad, abase, koff_lds, gq);
-                    mfma_kstep<MW, NW, TB>(tb, fr + (kl + 1) * NW * 2 * 64, lane, acc, tb0);
-                }
-            }
-        }
-        if (!active) continue;
-
-        // epilogue: potentials, spikes and first-spike tracking of this time block
+                        for (int t = 0; t < FIN_TB; ++t) acc[i][n][t] = f4{0.f, 0.f, 0.f, 0.f};
+                // Software pipeline, unrolled by two K-steps with two register sets:
+                // while K-step ks runs on the matrix cores, the spike words and weight
+                // fragments of ks+1 are in flight and the tap offsets of ks+2 are read.
+                auto koff_at = [&](int ks) { return koff_l[min(ks, g.ksteps - 1) * 4 + gq]; };
+                auto load_a = [&](uint32_t (&an)[FIN_MT][2], int2 o) {
 #pragma unroll
-        for (int t = 0; t < TB; ++t) {
-            const int tt = tb0 + t;
-            if (tt >= g.T) break;  // uniform
-#pragma unroll
-            for (int i = 0; i < MW; ++i)
-#pragma unroll
-                for (int n = 0; n < NW; ++n) {
-                    const f4 v = acc[i][n][t] * inv_s;  // undo the weight scaling (a power of two)
-                    uint32_t sp = 0;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const bool s = INF ? (v[j] > 0.0f) : (v[j] >= g.thr);
-                        const bool first = s && tfirst[i][n][j] == g.T;
-                        tfirst[i][n][j] = first ? tt : tfirst[i][n][j];
-                        vfirst[i][n][j] = first ? v[j] : vfirst[i][n][j];
-                        sp |= s ? (1u << (8 * j)) : 0u;
+                    for (int i = 0; i < FIN_MT; ++i) {
+                        if (ALDS) {
+                            an[i][0] = *reinterpret_cast<const uint32_t *>(abuf_t + alds[i] + (uint32_t)o.x);
+                            an[i][1] = *reinterpret_cast<const uint32_t *>(abuf_t + alds[i] + (uint32_t)o.y);
+                        } else {
+                            an[i][0] = *reinterpret_cast<const uint32_t *>(abase[i] + (uint32_t)o.x);
+                            an[i][1] = *reinterpret_cast<const uint32_t *>(abase[i] + (uint32_t)o.y);
+                        }
                     }
-                    if (!ost[i][n]) continue;
-                    const int64_t o = obase[i][n] + (int64_t)tt * tstride;
-                    if (full4) {
-                        if (P) *reinterpret_cast<f4 *>(P + o) = v;
-                        if (S) *reinterpret_cast<uint32_t *>(S + o) = sp;
+                };
+                auto load_b = [&](half8 (&bn)[4], int ks) {
+                    if (BLDS) {
+                        const uint4 *fr = frag_l + ks * 256 + lane;
+                        bn[0] = __builtin_bit_cast(half8, fr[0]);
+                        bn[1] = __builtin_bit_cast(half8, fr[64]);
+                        bn[2] = __builtin_bit_cast(half8, fr[128]);
+                        bn[3] = __builtin_bit_cast(half8, fr[192]);
                     } else {
-                        const int lim = g.HoWo - mpos0[i];
-#pragma unroll
-                        for (int j = 0; j < 4; ++j)
-                            if (j < lim) {
-                                if (P) P[o + j] = v[j];
-                                if (S) S[o + j] = (uint8_t)(sp >> (8 * j));
-                            }
+                        bn[0] = gh[ks * 64];
+                        bn[1] = gl[ks * 64];
+                        bn[2] = gh[(g.ksteps + ks) * 64];
+                        bn[3] = gl[(g.ksteps + ks) * 64];
                     }
-                }
-        }
-    }
-    if (!active) return;
-
-    // Eq.5 mode: every step before the last holds zero potential and no spike.
-    if (INF) {
-        for (int tt = 0; tt < g.T - 1; ++tt) {
+                };
+                // one K-step: spike operands from the words, then TB x 4 tiles x 2 features x hi/lo
+                auto kstep = [&](const uint32_t (&an)[FIN_MT][2], const half8 (&bc)[4]) {
+                    uint32_t xn[FIN_MT][4];
 #pragma unroll
-            for (int i = 0; i < MW; ++i)
+                    for (int i = 0; i < FIN_MT; ++i) {
+                        neg_times(an[i][0], xn[i][0], xn[i][1]);
+                        neg_times(an[i][1], xn[i][2], xn[i][3]);
+                    }
 #pragma unroll
-                for (int n = 0; n < NW; ++n) {
-                    if (!ost[i][n]) continue;
-                    const int64_t o = obase[i][n] + (int64_t)tt * tstride;
-                    if (full4) {
-                        if (P) *reinterpret_cast<f4 *>(P + o) = f4{0.f, 0.f, 0.f, 0.f};
-                        if (S) *reinterpret_cast<uint32_t *>(S + o) = 0u;
-                    } else {
-                        const int lim = g.HoWo - mpos0[i];
-                        for (int j = 0; j < 4 && j < lim; ++j) {
-                            if (P) P[o + j] = 0.0f;
-                            if (S) S[o + j] = 0;
+                    for (int t = 0; t < FIN_TB; ++t) {
+                        const uint32_t ct = step_const(tb0 + t);
+                        half8 a[FIN_MT];
+#pragma unroll
+                        for (int i = 0; i < FIN_MT; ++i) a[i] = spike_operand(xn[i], ct);
+                        // all hi products first, then the lo ones: dependent MFMAs are 8 apart
+#pragma unroll
+                        for (int i = 0; i < FIN_MT; ++i)
+#pragma unroll
+                            for (int n = 0; n < 2; ++n) acc[i][n][t] = mfma(a[i], bc[2 * n], acc[i][n][t]);
+#pragma unroll
+                        for (int i = 0; i < FIN_MT; ++i)
+#pragma unroll
+                            for (int n = 0; n < 2; ++n) acc[i][n][t] = mfma(a[i], bc[2 * n + 1], acc[i][n][t]);
+                    }
+                };
+                uint32_t a0[FIN_MT][2], a1[FIN_MT][2];
+                half8 b0[4], b1[4];
+                int2 o2 = koff_at(0);
+                load_a(a0, o2);
+                load_b(b0, 0);
+                o2 = koff_at(1);
+                load_a(a1, o2);
+                load_b(b1, min(1, g.ksteps - 1));
+                o2 = koff_at(2);
+                for (int ks = 0; ks < g.ksteps; ks += 2) {
+                    kstep(a0, b0);
+                    const int2 o3 = koff_at(ks + 3);
+                    if (ks + 2 < g.ksteps) {
+                        load_a(a0, o2);
+                        load_b(b0, ks + 2);
+                    }
+                    if (ks + 1 < g.ksteps) {
+                        kstep(a1, b1);
+                        o2 = koff_at(ks + 4);
+                        if (ks + 3 < g.ksteps) {
+                            load_a(a1, o3);
+                            load_b(b1, ks + 3);
                         }
                     }
                 }
-        }
-    }
-
-    // first-spike time and the potential there
+                __syncthreads();  // staging free: the store waves are done with the previous block
 #pragma unroll
-    for (int i = 0; i < MW; ++i)
+                for (int t = 0; t < FIN_TB; ++t) {
+                    if (tb0 + t >= g.T) break;
+                    float *st = stage + t * stage_t;
 #pragma unroll
-        for (int n = 0; n < NW; ++n) {
-            if (!ost[i][n]) continue;
-            const int f = (ng * NW + n) * 16 + c;
-            const int64_t o = (img[i] * (int64_t)g.Cout + f) * g.HoWo + mpos0[i];
-            if (full4) {
-                uint32_t tv = 0;
+                    for (int i = 0; i < FIN_MT; ++i) {
+                        const int pl = (wv + FIN_CW * i) * 16 + gq * 4;  // first of this lane's 4 positions
 #pragma unroll
-                for (int j = 0; j < 4; ++j) tv |= (uint32_t)tfirst[i][n][j] << (8 * j);
-                *reinterpret_cast<uint32_t *>(TF + o) = tv;
-                *reinterpret_cast<f4 *>(VF + o) = f4{vfirst[i][n][0], vfirst[i][n][1], vfirst[i][n][2], vfirst[i][n][3]};
-            } else {
-                const int lim = g.HoWo - mpos0[i];
+                        for (int n = 0; n < 2; ++n) {
+                            const int fl = n * 16 + c;
+                            const f4 v = acc[i][n][t] * inv_s;  // undo the weight scaling (a power of two)
+                            if (G == 4) {
+                                if (pl < np) *reinterpret_cast<f4 *>(st + fl * np + pl) = v;
+                            } else {
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (j < lim) {
-                        TF[o + j] = (uint8_t)tfirst[i][n][j];
-                        VF[o + j] = vfirst[i][n][j];
+                                for (int q = 0; q < 4; ++q)
+                                    if (pl + q < np) st[fl * np + pl + q] = v[q];
+                            }
+                        }
                     }
+                }
+                if (has_next && last_block) store_region(nxt, abuf + (abuf_sel ^ 1) * a_words);
+                __syncthreads();  // staging full
+            }
+            abuf_sel ^= 1;
+        }
+    } else {
+        // ------------------------------------------------ store waves
+        const int s = tid - FIN_CW * 64;
+        for (int task = t_lo + r; task < t_hi; task += R) {
+            const int b = task / n_chunks, ch = task % n_chunks;
+            const int tile0 = ch * chunk_tiles;
+            const int ntl = min(chunk_tiles, g.mt_per_img - tile0);
+            const int pos0 = tile0 * 16;
+            const int np = min(ntl * 16, g.HoWo - pos0);
+            const int nel = nf * np;  // staged elements of the task
+            constexpr int NSLOT = 32 * chunk_tiles_max(G) * 16 / (FIN_SW * 64) / G;  // staged groups per thread
+            // per slot: its output offset within a step's plane (feature row fl, position pl), or -1;
+            // slots past the task read element 0 and are never stored
+            int off[NSLOT], src[NSLOT];
+#pragma unroll
+            for (int m = 0; m < NSLOT; ++m) {
+                const int e = (s + FIN_SW * 64 * m) * G;  // first staged element of the slot
+                const int fl = e / np, pl = e - fl * np;
+                off[m] = e < nel ? fl * g.HoWo + pl : -1;
+                src[m] = e < nel ? e : 0;
+            }
+            int tfirst[NSLOT][G];
+            float vfirst[NSLOT][G];
+#pragma unroll
+            for (int m = 0; m < NSLOT; ++m)
+#pragma unroll
+                for (int q = 0; q < G; ++q) {
+                    tfirst[m][q] = g.T;
+                    vfirst[m][q] = 0.0f;
+                }
+            for (int tb0 = 0; tb0 < g.T; tb0 += FIN_TB) {
+                __syncthreads();  // staging free
+                __syncthreads();  // staging full
+                for (int t = 0; t < FIN_TB && tb0 + t < g.T; ++t) {
+                    const int tt = tb0 + t;
+                    const float *st = stage + t * stage_t;
+                    float *Pt = P ? P + ((int64_t)b * g.T + tt) * tplane + (int64_t)f0 * g.HoWo + pos0 : nullptr;
+                    uint8_t *St = S ? S + ((int64_t)b * g.T + tt) * tplane + (int64_t)f0 * g.HoWo + pos0 : nullptr;
+#pragma unroll
+                    for (int m = 0; m < NSLOT; ++m) {
+                        if (off[m] < 0) continue;
+                        const uint32_t o = (uint32_t)off[m];
+                        float v[G];
+                        if (G == 4) {
+                            const f4 x4 = *reinterpret_cast<const f4 *>(st + src[m]);
+#pragma unroll
+                            for (int q = 0; q < G; ++q) v[q] = x4[q];
+                        } else {
+                            v[0] = st[src[m]];
+                        }
+                        uint32_t sp = 0;
+#pragma unroll
+                        for (int q = 0; q < G; ++q) {
+                            const bool fire = v[q] >= g.thr;
+                            const bool first = fire && tfirst[m][q] == g.T;
+                            tfirst[m][q] = first ? tt : tfirst[m][q];
+                            vfirst[m][q] = first ? v[q] : vfirst[m][q];
+                            sp |= fire ? (1u << (8 * q)) : 0u;
+                        }
+                        if (G == 4) {
+                            if (Pt) *reinterpret_cast<f4 *>(Pt + o) = f4{v[0], v[1], v[2], v[3]};
+                            if (St) *reinterpret_cast<uint32_t *>(St + o) = sp;
+                        } else {
+                            if (Pt) Pt[o] = v[0];
+                            if (St) St[o] = (uint8_t)sp;
+                        }
+                    }
+                }
+            }
+            // first-spike time and the potential there
+            uint8_t *TFt = TF + ((int64_t)b * g.Cout + f0) * g.HoWo + pos0;
+            float *VFt = VF + ((int64_t)b * g.Cout + f0) * g.HoWo + pos0;
+#pragma unroll
+            for (int m = 0; m < NSLOT; ++m) {
+                if (off[m] < 0) continue;
+                const uint32_t o = (uint32_t)off[m];
+                if (G == 4) {
+                    uint32_t tv = 0;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) tv |= (uint32_t)tfirst[m][q] << (8 * q);
+                    *reinterpret_cast<uint32_t *>(TFt + o) = tv;
+                    *reinterpret_cast<f4 *>(VFt + o) = f4{vfirst[m][0], vfirst[m][1], vfirst[m][2], vfirst[m][3]};
+                } else {
+                    TFt[o] = (uint8_t)tfirst[m][0];
+                    VFt[o] = vfirst[m][0];
+                }
             }
         }
+    }
 }
 
-// Persistent workgroups.  Workgroup w runs on XCD x = w % 8; the XCDs split
-// the M blocks (4 waves x MW tiles of 16 positions) into 8 contiguous slices.
-// Each workgroup serves one feature group: it loads that group's weight
-// fragments into LDS once (or streams them in chunks when they do not fit)
-// and then takes the next M block of its XCD's slice from a counter shared by
-// the workgroups of the same (XCD, feature group).  The workgroups of an XCD
-// therefore always work on neighbouring positions, so the 128-byte lines
-// shared by neighbouring output runs are completed in that XCD's L2 before
-// they are written back.  Every workgroup stops when the slice is exhausted.
-template <int MW, int NW, int TB, bool INF>
-__global__ __launch_bounds__(256, 2) void k_conv_fire(const uint8_t *__restrict__ tpad,
-                                                      const half8 *__restrict__ whi,
-                                                      const half8 *__restrict__ wlo,
-                                                      const int *__restrict__ koff, ConvGeom g,
-                                                      int n_mgroups, int n_mblocks, int n_ngroups, int kc,
-                                                      int resident, unsigned *__restrict__ counters,
-                                                      const float *__restrict__ inv_scale,
-                                                      float *__restrict__ P, uint8_t *__restrict__ S,
-                                                      uint8_t *__restrict__ TF, float *__restrict__ VF) {
+// ------------------------------------------------------------------ 3b. infinite threshold (Eq.5)
+// Only the last step is computed: P[T-1] = sum_k W[f,k] [tp_k <= T-1],
+// spike where P[T-1] > 0; every earlier step holds zero potential and no
+// spike.  Persistent workgroups of 4 waves, each serving one group of NW
+// 16-feature tiles; a wave owns MW position tiles.  The weight fragments of
+// the group stay in LDS when they fit, else they stream through LDS KC
+// K-steps at a time.  Blocks of positions are handed out from per-(XCD,
+// feature group) counters, so the workgroups of an XCD work on neighbouring
+// positions (workgroup w runs on XCD w % 8).
+constexpr int INF_KC = 8;
+constexpr size_t INF_LDS_BUDGET = 79872;
+
+template <int MW, int NW, bool VEC>
+__global__ __launch_bounds__(256, 2) void k_conv_fire_inf(const uint8_t *__restrict__ tpad,
+                                                          const half8 *__restrict__ whi,
+                                                          const half8 *__restrict__ wlo,
+                                                          const int2 *__restrict__ koff2, ConvGeom g,
+                                                          int n_mgroups, int n_mblocks, int n_ngroups, int kc,
+                                                          int resident, unsigned *__restrict__ counters,
+                                                          const float *__restrict__ inv_scale,
+                                                          float *__restrict__ P, uint8_t *__restrict__ S,
+                                                          uint8_t *__restrict__ TF, float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     __shared__ int next_mb;
-    const float inv_s = *inv_scale;
-    int *koff_lds = reinterpret_cast<int *>(lds);      // ksteps*32 offsets
-    uint4 *frl = lds + (g.ksteps * 32 * 4 + 15) / 16;  // fragments: all K-steps, or a chunk of kc
+    int2 *koff_l = reinterpret_cast<int2 *>(lds);
+    uint4 *frl = lds + (g.ksteps * 4 * 8 + 15) / 16;  // fragments: all K-steps, or a chunk of kc
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int gq = lane >> 4, c = lane & 15;
     const int x = blockIdx.x % 8, j = blockIdx.x / 8;
@@ -464,27 +569,130 @@ __global__ __launch_bounds__(256, 2) void k_conv_fire(const uint8_t *__restrict_
     const int mb_lo = x * per_x, mb_hi = min(n_mblocks, mb_lo + per_x);
     if (mb_lo >= mb_hi) return;  // whole workgroup: this XCD's slice is empty
     unsigned *ctr = counters + x * n_ngroups + ng;
-
+    const float inv_s = *inv_scale;
     const half8 *wfh = whi + (int64_t)ng * NW * g.ksteps * 64;
     const half8 *wfl = wlo + (int64_t)ng * NW * g.ksteps * 64;
-    for (int i = tid; i < g.ksteps * 32; i += 256) koff_lds[i] = koff[i];
-    if (resident) {
-        for (int idx = tid; idx < g.ksteps * NW * 2 * 64; idx += 256) {
-            const int ln = idx & 63, r = idx >> 6;  // r = (ks*NW + n)*2 + h
-            const int h = r & 1, n = (r >> 1) % NW, ks = (r >> 1) / NW;
+    auto fill = [&](int k0, int nk) {
+        for (int idx = tid; idx < nk * NW * 2 * 64; idx += 256) {
+            const int ln = idx & 63, rr = idx >> 6;  // rr = (ksl*NW + n)*2 + h
+            const int h = rr & 1, n = (rr >> 1) % NW, ksl = (rr >> 1) / NW;
             const half8 *src = h ? wfl : wfh;
-            frl[idx] = __builtin_bit_cast(uint4, src[(n * g.ksteps + ks) * 64 + ln]);
+            frl[idx] = __builtin_bit_cast(uint4, src[(n * g.ksteps + k0 + ksl) * 64 + ln]);
         }
-    }
+    };
+    for (int i = tid; i < g.ksteps * 4; i += 256) koff_l[i] = koff2[i];
+    if (resident) fill(0, g.ksteps);
+    const uint32_t ct = step_const(g.T - 1);
+    const int64_t tstride = (int64_t)g.Cout * g.HoWo;
+
     for (;;) {
         __syncthreads();  // LDS fills are visible; everyone has read the previous next_mb
         if (tid == 0) next_mb = mb_lo + (int)atomicAdd(ctr, 1u);
         __syncthreads();
         const int mb = next_mb;
         if (mb >= mb_hi) break;  // uniform
-        const int mg = mb * WAVES + wv;
-        conv_tile<MW, NW, TB, INF>(inv_s, tpad, frl, koff_lds, wfh, wfl, frl, resident != 0, resident ? g.ksteps : kc, g,
-                                   ng, mg, mg < n_mgroups, tid, lane, gq, c, P, S, TF, VF);
+        const int mg = mb * 4 + wv;
+        const bool active = mg < n_mgroups;
+        uint32_t abase[MW];
+        int64_t img[MW];
+        int mpos0[MW];
+#pragma unroll
+        for (int i = 0; i < MW; ++i) {
+            const int64_t gm = (int64_t)mg * MW + i;
+            const bool v = active && gm < g.total_mtiles;
+            const int64_t b = v ? gm / g.mt_per_img : 0;
+            const int mt = v ? (int)(gm % g.mt_per_img) : 0;
+            const int pos = min(mt * 16 + c, g.HoWo - 1);  // rows past the image are computed, not stored
+            const int y = pos / g.Wo, xx = pos % g.Wo;
+            abase[i] = (uint32_t)(((b * g.Hp + y) * g.Wp + xx) * g.CP);
+            img[i] = v ? b : -1;
+            mpos0[i] = mt * 16 + gq * 4;
+        }
+        f4 acc[MW][NW];
+#pragma unroll
+        for (int i = 0; i < MW; ++i)
+#pragma unroll
+            for (int n = 0; n < NW; ++n) acc[i][n] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int k0 = 0; k0 < g.ksteps; k0 += kc) {
+            const int nk = min(kc, g.ksteps - k0);
+            if (!resident) {  // stream this chunk of fragments through LDS (uniform branch)
+                __syncthreads();
+                fill(k0, nk);
+                __syncthreads();
+            }
+            const uint4 *fr = frl + (resident ? (size_t)k0 * NW * 2 * 64 : 0);
+            if (!active) continue;
+            for (int kl = 0; kl < nk; ++kl) {
+                const int2 o = koff_l[(k0 + kl) * 4 + gq];
+                half8 bh[NW], bl[NW];
+#pragma unroll
+                for (int n = 0; n < NW; ++n) {
+                    bh[n] = __builtin_bit_cast(half8, fr[(kl * NW + n) * 128 + lane]);
+                    bl[n] = __builtin_bit_cast(half8, fr[(kl * NW + n) * 128 + 64 + lane]);
+                }
+#pragma unroll
+                for (int i = 0; i < MW; ++i) {
+                    const uint32_t w0 = *reinterpret_cast<const uint32_t *>(tpad + abase[i] + (uint32_t)o.x);
+                    const uint32_t w1 = *reinterpret_cast<const uint32_t *>(tpad + abase[i] + (uint32_t)o.y);
+                    uint32_t xn[4];
+                    neg_times(w0, xn[0], xn[1]);
+                    neg_times(w1, xn[2], xn[3]);
+                    const half8 a = spike_operand(xn, ct);
+#pragma unroll
+                    for (int n = 0; n < NW; ++n) {
+                        acc[i][n] = mfma(a, bh[n], acc[i][n]);
+                        acc[i][n] = mfma(a, bl[n], acc[i][n]);
+                    }
+                }
+            }
+        }
+        if (!active) continue;
+#pragma unroll
+        for (int i = 0; i < MW; ++i)
+#pragma unroll
+            for (int n = 0; n < NW; ++n) {
+                const int f = (ng * NW + n) * 16 + c;
+                if (img[i] < 0 || f >= g.Cout || mpos0[i] >= g.HoWo) continue;
+                const f4 v = acc[i][n] * inv_s;
+                const int lim = g.HoWo - mpos0[i];
+                const int64_t ob = img[i] * g.T * tstride + (int64_t)f * g.HoWo + mpos0[i];
+                uint32_t sp = 0, tv = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    sp |= (uint32_t)(v[q] > 0.0f) << (8 * q);
+                    tv |= (uint32_t)(v[q] > 0.0f ? g.T - 1 : g.T) << (8 * q);
+                }
+                const int64_t of = (img[i] * (int64_t)g.Cout + f) * g.HoWo + mpos0[i];
+                if (VEC) {  // HoWo % 4 == 0: the 4 positions are in the image and aligned
+                    for (int tt = 0; tt < g.T - 1; ++tt) {
+                        const int64_t o = ob + (int64_t)tt * tstride;
+                        if (P) *reinterpret_cast<f4 *>(P + o) = f4{0.f, 0.f, 0.f, 0.f};
+                        if (S) *reinterpret_cast<uint32_t *>(S + o) = 0u;
+                    }
+                    const int64_t o = ob + (int64_t)(g.T - 1) * tstride;
+                    if (P) *reinterpret_cast<f4 *>(P + o) = v;
+                    if (S) *reinterpret_cast<uint32_t *>(S + o) = sp;
+                    *reinterpret_cast<uint32_t *>(TF + of) = tv;
+                    *reinterpret_cast<f4 *>(VF + of) = v;
+                } else {
+                    for (int tt = 0; tt < g.T; ++tt) {
+                        const int64_t o = ob + (int64_t)tt * tstride;
+                        const bool last = tt == g.T - 1;
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            if (q < lim) {
+                                if (P) P[o + q] = last ? v[q] : 0.0f;
+                                if (S) S[o + q] = last ? (uint8_t)(sp >> (8 * q)) : (uint8_t)0;
+                            }
+                    }
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        if (q < lim) {
+                            TF[of + q] = (uint8_t)(tv >> (8 * q));
+                            VF[of + q] = v[q];
+                        }
+                }
+            }
     }
 }
 
@@ -505,33 +713,37 @@ int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, Con
                 SPK_E_SHAPE, "spk_conv_fire: bad sizes B=%d T=%d Cin=%d H=%d W=%d Cout=%d K=%d pad=%d",
                 B, T, Cin, H, W, Cout, K, pad);
     SPK_REQUIRE(T <= 255, SPK_E_RANGE, "spk_conv_fire: T=%d > 255", T);
+    SPK_REQUIRE(Cin <= 4096 && K <= 64 && pad <= 64 && H <= 65536 && W <= 65536, SPK_E_RANGE,
+                "spk_conv_fire: Cin, K, pad or the image too large");
     ConvGeom &g = pl.g;
     g.B = B; g.T = T; g.Cin = Cin; g.H = H; g.W = W; g.Cout = Cout; g.K = K; g.pad = pad;
+    g.CP = Cin <= 4 ? 4 : (Cin + 7) / 8 * 8;
     g.Hp = H + 2 * pad;
     g.Wp = W + 2 * pad;
     g.Ho = g.Hp - K + 1;
     g.Wo = g.Wp - K + 1;
     SPK_REQUIRE(g.Ho >= 1 && g.Wo >= 1, SPK_E_SHAPE, "spk_conv_fire: kernel %d larger than padded input %dx%d",
                 K, g.Hp, g.Wp);
-    SPK_REQUIRE((int64_t)Cin * K * K <= 16384, SPK_E_RANGE, "spk_conv_fire: Cin*K*K=%lld > 16384",
-                (long long)Cin * K * K);
+    SPK_REQUIRE((int64_t)K * K * g.CP <= 16384, SPK_E_RANGE,
+                "spk_conv_fire: K*K*Cin (Cin rounded up to %d) = %lld > 16384", g.CP, (long long)K * K * g.CP);
     SPK_REQUIRE(Cout <= 4096, SPK_E_RANGE, "spk_conv_fire: Cout=%d > 4096", Cout);
-    SPK_REQUIRE((int64_t)g.Ho * g.Wo < (1LL << 31) && (int64_t)Cin * g.Hp * g.Wp <= 65535LL * 256 &&
-                    g.Wp <= PAD_LDS,
-                SPK_E_RANGE, "spk_conv_fire: image too large");
-    // the MFMA kernel addresses the padded first-spike map with 32-bit offsets
-    SPK_REQUIRE((int64_t)B * Cin * g.Hp * g.Wp < (1LL << 32), SPK_E_RANGE,
-                "spk_conv_fire: padded input of %lld bytes exceeds 4 GiB", (long long)B * Cin * g.Hp * g.Wp);
+    SPK_REQUIRE((int64_t)g.Ho * g.Wo <= (1LL << 26), SPK_E_RANGE, "spk_conv_fire: %lld output positions > 2^26",
+                (long long)g.Ho * g.Wo);
+    SPK_REQUIRE((int64_t)g.Wp * g.CP <= PAD_LDS, SPK_E_RANGE,
+                "spk_conv_fire: padded input row of %lld bytes exceeds %d", (long long)g.Wp * g.CP, PAD_LDS);
+    // the MFMA kernels address the padded first-spike map with 32-bit offsets
+    SPK_REQUIRE((int64_t)B * g.Hp * g.Wp * g.CP < (1LL << 32), SPK_E_RANGE,
+                "spk_conv_fire: padded input of %lld bytes exceeds 4 GiB", (long long)B * g.Hp * g.Wp * g.CP);
+    SPK_REQUIRE((int64_t)B * ((g.Ho * (int64_t)g.Wo + 15) / 16) < (1LL << 31), SPK_E_RANGE,
+                "spk_conv_fire: too many output positions");
     g.HoWo = g.Ho * g.Wo;
-    g.Kc = Cin * K * K;
-    g.ksteps = (g.Kc + 31) / 32;
-    g.ntiles = (int)spk::ceil_div(spk::ceil_div(Cout, 16), NW_MAX) * NW_MAX;
+    g.ksteps = (K * K * g.CP + 31) / 32;
+    g.ntiles = (int)spk::ceil_div(spk::ceil_div(Cout, 16), NTILE_ALIGN) * NTILE_ALIGN;
     g.mt_per_img = (g.HoWo + 15) / 16;
     g.total_mtiles = (int64_t)B * g.mt_per_img;
-    g.vec4 = (g.HoWo % 4) == 0;
-    pl.tpad_bytes = (size_t)B * Cin * g.Hp * g.Wp;
+    pl.tpad_bytes = (size_t)B * g.Hp * g.Wp * g.CP;
     pl.frag_count = (size_t)g.ntiles * g.ksteps * 64;
-    pl.koff_count = (size_t)g.ksteps * 32;
+    pl.koff_count = (size_t)g.ksteps * 4;
     return SPK_OK;
 }
 
@@ -540,32 +752,50 @@ size_t plan_workspace(const ConvPlan &pl) {
     c.take<uint8_t>(pl.tpad_bytes);
     c.take<half8>(pl.frag_count);
     c.take<half8>(pl.frag_count);
-    c.take<int>(pl.koff_count);
+    c.take<int2>(pl.koff_count);
     c.take<unsigned>(MAX_NGROUPS_COUNT + 2);  // work counters, max|w| bits, 1/scale
     return spk::align_up(c.off, 256);
 }
 
-template <int MW, int NW, int TB, bool INF>
-void launch_conv(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int *koff, unsigned *counters,
-                 const float *inv_scale, const ConvGeom &g, float *P, uint8_t *S, uint8_t *TF, float *VF,
-                 hipStream_t st) {
+int max_lds_per_block() {
+    int dev = 0, v = 65536;
+    if (hipGetDevice(&dev) != hipSuccess) return 65536;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) return 65536;
+    return v;
+}
+
+template <int G, bool BLDS, bool ALDS>
+void launch_fin(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, const float *inv_scale,
+                const ConvGeom &g, int n_pairs, int n_chunks, int chunk_tiles, int np_max, int a_words, size_t lds,
+                float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
+    // one workgroup per CU: a multiple of the feature pairs on every XCD
+    const int per_xcd = (int)spk::ceil_div(std::max(32, n_pairs), n_pairs) * n_pairs;
+    hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
+                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, chunk_tiles, np_max, a_words, inv_scale, P, S, TF,
+                       VF);
+}
+
+template <int MW, int NW, bool VEC>
+void launch_inf(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, unsigned *counters,
+                const float *inv_scale, const ConvGeom &g, float *P, uint8_t *S, uint8_t *TF, float *VF,
+                hipStream_t st) {
     const int64_t n_mgroups = spk::ceil_div(g.total_mtiles, MW);
-    const int64_t n_mblocks = spk::ceil_div(n_mgroups, WAVES);
+    const int64_t n_mblocks = spk::ceil_div(n_mgroups, 4);
     const int n_ngroups = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), NW);
-    const size_t koff_bytes = spk::align_up((size_t)g.ksteps * 32 * sizeof(int), 16);
+    const size_t koff_bytes = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16);
     const size_t step = (size_t)NW * 2 * 64 * 16;  // one K-step of fragments
-    const int resident = koff_bytes + (size_t)g.ksteps * step <= LDS_BUDGET;
+    const int resident = koff_bytes + (size_t)g.ksteps * step <= INF_LDS_BUDGET;
     const int kc = resident ? g.ksteps
-                            : (int)std::max<size_t>(1, std::min<size_t>(KC, (LDS_BUDGET - koff_bytes) / step));
+                            : (int)std::max<size_t>(1, std::min<size_t>(INF_KC, (INF_LDS_BUDGET - koff_bytes) / step));
     const size_t lds = koff_bytes + (size_t)kc * step;
     // about two workgroups per CU (256 CUs, 32 per XCD), a multiple of the feature groups per XCD
     const int64_t want = spk::ceil_div(n_mblocks * n_ngroups, 8);
     const int64_t per_xcd = std::min<int64_t>(spk::ceil_div(std::max<int64_t>(64, n_ngroups), n_ngroups) * n_ngroups,
                                               spk::ceil_div(want, n_ngroups) * n_ngroups);
     // the 8 * n_ngroups counters (<= MAX_NGROUPS_COUNT since Cout <= 4096) were zeroed by the caller
-    hipLaunchKernelGGL((k_conv_fire<MW, NW, TB, INF>), dim3((unsigned)(per_xcd * 8)), dim3(256), lds, st, tpad, whi,
-                       wlo, koff, g, (int)n_mgroups, (int)n_mblocks, n_ngroups, kc, resident, counters, inv_scale, P,
-                       S, TF, VF);
+    hipLaunchKernelGGL((k_conv_fire_inf<MW, NW, VEC>), dim3((unsigned)(per_xcd * 8)), dim3(256), lds, st, tpad, whi, wlo,
+                       koff2, g, (int)n_mgroups, (int)n_mblocks, n_ngroups, kc, resident, counters, inv_scale, P, S,
+                       TF, VF);
 }
 
 }  // namespace
@@ -591,45 +821,81 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     SPK_REQUIRE(workspace && ws_bytes >= need, SPK_E_WORKSPACE,
                 "spk_conv_fire: workspace of %zu bytes < %zu required", ws_bytes, need);
     ConvGeom g = pl.g;
-    g.inf_mode = std::isinf(threshold) ? 1 : 0;
-    g.thr = g.inf_mode ? 0.0f : threshold;
+    const bool inf_mode = std::isinf(threshold);
+    g.thr = inf_mode ? 0.0f : threshold;
 
     spk::Carver cv(workspace);
     uint8_t *tpad = cv.take<uint8_t>(pl.tpad_bytes);
     half8 *whi = cv.take<half8>(pl.frag_count);
     half8 *wlo = cv.take<half8>(pl.frag_count);
-    int *koff = cv.take<int>(pl.koff_count);
+    int2 *koff2 = cv.take<int2>(pl.koff_count);
     unsigned *counters = cv.take<unsigned>(MAX_NGROUPS_COUNT + 2);
     unsigned *maxbits = counters + MAX_NGROUPS_COUNT;
     float *inv_scale = reinterpret_cast<float *>(counters + MAX_NGROUPS_COUNT + 1);
     hipStream_t st = spk::as_stream(stream);
 
-    const int rows_img = Cin * g.Hp;
-    const int rows_per_chunk = std::min(rows_img, PAD_LDS / g.Wp);
-    const int words = ((Cin * H * W) & 3) == 0 && ((uintptr_t)wave & 3) == 0;
-    hipLaunchKernelGGL(k_pad_first_spike, dim3((unsigned)spk::ceil_div(rows_img, rows_per_chunk),
+    // finite-threshold launch configuration (validated before anything is enqueued)
+    const bool vec = (g.HoWo % 4) == 0 && ((uintptr_t)potentials & 15) == 0 && ((uintptr_t)v_first & 15) == 0 &&
+                     ((uintptr_t)spikes & 3) == 0 && ((uintptr_t)t_first & 3) == 0;
+    const int mt = g.mt_per_img;
+    const int ct_max = chunk_tiles_max(vec ? 4 : 1);
+    const int n_chunks = (mt + ct_max - 1) / ct_max;
+    const int chunk_tiles = (mt + n_chunks - 1) / n_chunks;
+    const int np_max = chunk_tiles * 16;
+    const int n_pairs = (int)spk::ceil_div(spk::ceil_div(Cout, 16), 2);
+    const size_t koff_lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16);
+    const size_t stage_lds = (size_t)FIN_TB * 32 * np_max * sizeof(float);
+    const size_t frag_lds = (size_t)g.ksteps * 4 * 64 * 16;
+    const size_t lds_limit = (size_t)max_lds_per_block();
+    // spike rows of the largest task, staged in LDS (double-buffered) when small enough
+    int a_rows = 0;
+    for (int ch = 0; ch < n_chunks; ++ch) {
+        const int p0 = ch * chunk_tiles * 16, np = std::min(chunk_tiles * 16, g.HoWo - p0);
+        a_rows = std::max(a_rows, (p0 + np - 1) / g.Wo + K - p0 / g.Wo);
+    }
+    const int a_words = a_rows * g.Wp * g.CP / 4;
+    const size_t a_lds = 2 * (size_t)a_words * 4;
+    const bool alds = a_words <= FIN_CW * 64 * FIN_AW && koff_lds + stage_lds + a_lds <= lds_limit;
+    const bool blds = koff_lds + frag_lds + stage_lds + (alds ? a_lds : 0) <= lds_limit;
+    const size_t fin_lds = koff_lds + (blds ? frag_lds : 0) + stage_lds + (alds ? a_lds : 0);
+    SPK_REQUIRE(inf_mode || fin_lds <= lds_limit, SPK_E_RANGE,
+                "spk_conv_fire: needs %zu bytes of LDS per workgroup, the device has %zu", fin_lds, lds_limit);
+
+    const int row_bytes = g.Wp * g.CP;
+    const int rows_per_chunk = std::min(g.Hp, PAD_LDS / row_bytes);
+    hipLaunchKernelGGL(k_pad_first_spike, dim3((unsigned)spk::ceil_div(g.Hp, rows_per_chunk),
                                                (unsigned)std::min(B, 65535)),
-                       dim3(256), 0, st, wave, g, rows_per_chunk, words, tpad);
+                       dim3(256), 0, st, wave, g, rows_per_chunk, tpad);
     hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)spk::ceil_div(MAX_NGROUPS_COUNT + 2, 256)), dim3(256), 0, st,
                        counters, MAX_NGROUPS_COUNT + 2);
-    const int64_t nw = (int64_t)Cout * g.Kc;
+    const int64_t nw = (int64_t)Cout * Cin * K * K;
     hipLaunchKernelGGL(k_weight_absmax, dim3((unsigned)std::min<int64_t>(256, spk::ceil_div(nw, 256))), dim3(256), 0,
                        st, weight, nw, maxbits);
     const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
     hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, maxbits,
-                       whi, wlo, koff, inv_scale);
-    // tile shape: one 16-position tile by two or four 16-feature tiles per wave
-    // (two when the layer has at most 32 features), 2 waves per SIMD
-    const bool wide = (Cout + 15) / 16 > 2;
-    if (g.inf_mode) {
-        if (wide) launch_conv<2, 4, 1, true>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
-        else launch_conv<2, 2, 1, true>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
-    } else if (wide) {
-        launch_conv<1, 4, 8, false>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
-    } else if (T % 15 == 0) {
-        launch_conv<1, 2, 15, false>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
+                       whi, wlo, koff2, inv_scale);
+    if (inf_mode) {
+        if (vec)
+            launch_inf<2, 4, true>(tpad, whi, wlo, koff2, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
+        else
+            launch_inf<2, 4, false>(tpad, whi, wlo, koff2, counters, inv_scale, g, potentials, spikes, t_first, v_first,
+                                    st);
     } else {
-        launch_conv<1, 2, 16, false>(tpad, whi, wlo, koff, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
+#define SPK_FIN(G, BL, AL)                                                                                    \
+    launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, g, n_pairs, n_chunks, chunk_tiles, np_max, a_words, \
+                          fin_lds, potentials, spikes, t_first, v_first, st)
+        const int sel = (vec ? 4 : 0) + (blds ? 2 : 0) + (alds ? 1 : 0);
+        switch (sel) {
+            case 0: SPK_FIN(1, false, false); break;
+            case 1: SPK_FIN(1, false, true); break;
+            case 2: SPK_FIN(1, true, false); break;
+            case 3: SPK_FIN(1, true, true); break;
+            case 4: SPK_FIN(4, false, false); break;
+            case 5: SPK_FIN(4, false, true); break;
+            case 6: SPK_FIN(4, true, false); break;
+            default: SPK_FIN(4, true, true); break;
+        }
+#undef SPK_FIN
     }
     return spk::check_launch("spk_conv_fire");
 }
