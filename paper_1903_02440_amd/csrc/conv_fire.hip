@@ -125,8 +125,26 @@ __device__ __forceinline__ int weight_scale_exp(unsigned maxbits) {
     return 12 - max(-100, min(100, E));
 }
 
-// Tap k of the padded receptive field: cell kyx = k / CP, channel ci = k % CP.
-// koff2[q] holds, for the 8-tap group q = k/8, the tpad byte offsets (relative
+// Tap (K-step ks, lane group gq, j) of the padded receptive field -> (cell kyx,
+// channel ci).  In general k = ks*32 + 8*gq + j is cell k / CP, channel k % CP.
+// When CP is a multiple of 32 the CP/32 K-steps of a cell are laid out so that
+// a lane group's channels are contiguous over the whole cell: channel
+// gq*CP/4 + 8*(ks mod CP/32) + j, i.e. a lane reads CP/4 consecutive bytes of
+// tpad per cell (the same order as the general one when CP == 32).
+__device__ __forceinline__ void tap_of(const ConvGeom &g, int ks, int gq, int j, int &kyx, int &ci) {
+    if (g.CP % 32 == 0) {
+        const int kpc = g.CP / 32;
+        kyx = ks / kpc;
+        ci = gq * (g.CP / 4) + (ks % kpc) * 8 + j;
+    } else {
+        const int k = ks * 32 + gq * 8 + j;
+        kyx = k / g.CP;
+        ci = k % g.CP;
+    }
+}
+
+// Tap k of the padded receptive field: cell kyx, channel ci (tap_of).
+// koff2[q] holds, for the 8-tap group q = 4*ks + gq, the tpad byte offsets (relative
 // to the output position's top-left input cell) of its two 4-byte words; with
 // CP >= 8 they are adjacent, with CP == 4 they are the cells 2q and 2q+1.
 // Groups past the receptive field point at offset 0 (their weights are 0).
@@ -148,8 +166,8 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
         half8 h, l;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const int k = ks * 32 + (lane >> 4) * 8 + j;
-            const int kyx = k / g.CP, ci = k % g.CP;
+            int kyx, ci;
+            tap_of(g, ks, lane >> 4, j, kyx, ci);
             float v = 0.0f;
             if (n < g.Cout && kyx < KK && ci < g.Cin) v = ldexpf(w[((int64_t)n * g.Cin + ci) * KK + kyx], e);
             const _Float16 hv = (_Float16)v;
@@ -165,8 +183,9 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
         int2 o{0, 0};
         auto cell = [&](int kyx) { return kyx < KK ? ((kyx / g.K) * g.Wp + kyx % g.K) * g.CP : 0; };
         if (g.CP >= 8) {
-            const int k0 = q * 8, kyx = k0 / g.CP;
-            o.x = kyx < KK ? cell(kyx) + k0 % g.CP : 0;
+            int kyx, ci0;
+            tap_of(g, q / 4, q % 4, 0, kyx, ci0);
+            o.x = kyx < KK ? cell(kyx) + ci0 : 0;
             o.y = kyx < KK ? o.x + 4 : 0;
         } else {
             o.x = cell(2 * q);
@@ -536,158 +555,185 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 }
 
 // ------------------------------------------------------------------ 3b. infinite threshold (Eq.5)
-// Only the last step is computed: P[T-1] = sum_k W[f,k] [tp_k <= T-1],
-// spike where P[T-1] > 0; every earlier step holds zero potential and no
-// spike.  Persistent workgroups of 4 waves, each serving one group of NW
-// 16-feature tiles; a wave owns MW position tiles.  The weight fragments of
-// the group stay in LDS when they fit, else they stream through LDS KC
-// K-steps at a time.  Blocks of positions are handed out from per-(XCD,
-// feature group) counters, so the workgroups of an XCD work on neighbouring
-// positions (workgroup w runs on XCD w % 8).
-constexpr int INF_KC = 8;
-constexpr size_t INF_LDS_BUDGET = 79872;
+// Only the last step is computed: P[T-1] = sum_k W[f,k] [tp_k <= T-1], spike
+// where P[T-1] > 0.  Every earlier step holds zero potential and no spike;
+// those planes are contiguous per image and written by k_zero_planes.
+// Persistent workgroups of 8 waves; a task is (group of 4 16-feature tiles,
+// block of 16 position tiles), tasks ordered feature-group major and split
+// into 8 contiguous XCD slices, so an XCD's L2 holds the fragments of about
+// one feature group.  The fragments stream through two LDS buffers of KC
+// K-steps, filled with direct global-to-LDS loads one chunk ahead; the spike
+// words of a chunk are fetched before the next chunk's fill is issued, so
+// the MFMA loop never waits behind it.
+constexpr int INF_WAVES = 8;
+constexpr int INF_MW = 2;   // position tiles per wave
+constexpr int INF_NW = 4;   // 16-feature tiles per workgroup
+constexpr int INF_KC = 8;   // K-steps per LDS chunk
+constexpr int INF_CHUNK_U4 = INF_KC * INF_NW * 2 * 64;  // uint4 per chunk buffer
 
-template <int MW, int NW, bool VEC>
-__global__ __launch_bounds__(256, 2) void k_conv_fire_inf(const uint8_t *__restrict__ tpad,
-                                                          const half8 *__restrict__ whi,
-                                                          const half8 *__restrict__ wlo,
-                                                          const int2 *__restrict__ koff2, ConvGeom g,
-                                                          int n_mgroups, int n_mblocks, int n_ngroups, int kc,
-                                                          int resident, unsigned *__restrict__ counters,
-                                                          const float *__restrict__ inv_scale,
-                                                          float *__restrict__ P, uint8_t *__restrict__ S,
-                                                          uint8_t *__restrict__ TF, float *__restrict__ VF) {
+template <bool VEC>
+__global__ __launch_bounds__(INF_WAVES * 64, 1) void k_conv_fire_inf(
+    const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
+    const int2 *__restrict__ koff2, ConvGeom g, int n_mb, int n_ng, const float *__restrict__ inv_scale,
+    float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
-    __shared__ int next_mb;
     int2 *koff_l = reinterpret_cast<int2 *>(lds);
-    uint4 *frl = lds + (g.ksteps * 4 * 8 + 15) / 16;  // fragments: all K-steps, or a chunk of kc
+    uint4 *cbuf = lds + (g.ksteps * 4 * 8 + 15) / 16;  // 2 chunk buffers [ksl][n][hi/lo][64]
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int gq = lane >> 4, c = lane & 15;
-    const int x = blockIdx.x % 8, j = blockIdx.x / 8;
-    const int ng = j % n_ngroups;
-    const int per_x = (n_mblocks + 7) / 8;
-    const int mb_lo = x * per_x, mb_hi = min(n_mblocks, mb_lo + per_x);
-    if (mb_lo >= mb_hi) return;  // whole workgroup: this XCD's slice is empty
-    unsigned *ctr = counters + x * n_ngroups + ng;
+    for (int i = tid; i < g.ksteps * 4; i += INF_WAVES * 64) koff_l[i] = koff2[i];
     const float inv_s = *inv_scale;
-    const half8 *wfh = whi + (int64_t)ng * NW * g.ksteps * 64;
-    const half8 *wfl = wlo + (int64_t)ng * NW * g.ksteps * 64;
-    auto fill = [&](int k0, int nk) {
-        for (int idx = tid; idx < nk * NW * 2 * 64; idx += 256) {
-            const int ln = idx & 63, rr = idx >> 6;  // rr = (ksl*NW + n)*2 + h
-            const int h = rr & 1, n = (rr >> 1) % NW, ksl = (rr >> 1) / NW;
-            const half8 *src = h ? wfl : wfh;
-            frl[idx] = __builtin_bit_cast(uint4, src[(n * g.ksteps + k0 + ksl) * 64 + ln]);
-        }
-    };
-    for (int i = tid; i < g.ksteps * 4; i += 256) koff_l[i] = koff2[i];
-    if (resident) fill(0, g.ksteps);
     const uint32_t ct = step_const(g.T - 1);
+    const int nchunks = (g.ksteps + INF_KC - 1) / INF_KC;
+    const int x = blockIdx.x % 8, j = blockIdx.x / 8, per_xcd = (int)gridDim.x / 8;
+    const int ntask = n_mb * n_ng, per_x = (ntask + 7) / 8;
+    const int t_lo = x * per_x, t_hi = min(ntask, t_lo + per_x);
     const int64_t tstride = (int64_t)g.Cout * g.HoWo;
 
-    for (;;) {
-        __syncthreads();  // LDS fills are visible; everyone has read the previous next_mb
-        if (tid == 0) next_mb = mb_lo + (int)atomicAdd(ctr, 1u);
-        __syncthreads();
-        const int mb = next_mb;
-        if (mb >= mb_hi) break;  // uniform
-        const int mg = mb * 4 + wv;
-        const bool active = mg < n_mgroups;
-        uint32_t abase[MW];
-        int64_t img[MW];
-        int mpos0[MW];
+    for (int task = t_lo + j; task < t_hi; task += per_xcd) {
+        const int ng = task / n_mb, mb = task % n_mb;
+        const half8 *fh = whi + (int64_t)ng * INF_NW * g.ksteps * 64;
+        const half8 *fl = wlo + (int64_t)ng * INF_NW * g.ksteps * 64;
+        // chunk ch -> buffer: wave w issues the 64-lane groups w, w+8, ... (16 bytes per lane)
+        auto fill = [&](int ch) {
+            uint4 *dst = cbuf + (ch & 1) * INF_CHUNK_U4;
+            const int k0 = ch * INF_KC, nk = min(INF_KC, g.ksteps - k0);
+            for (int grp = wv; grp < nk * INF_NW * 2; grp += INF_WAVES) {
+                const int h = grp & 1, n = (grp >> 1) % INF_NW, ksl = (grp >> 1) / INF_NW;
+                const half8 *src = (h ? fl : fh) + ((int64_t)n * g.ksteps + k0 + ksl) * 64 + lane;
+                __builtin_amdgcn_global_load_lds(src, dst + grp * 64, 16, 0, 0);
+            }
+        };
+        const uint8_t *abase[INF_MW];
+        int64_t img[INF_MW];
+        int mpos0[INF_MW];
 #pragma unroll
-        for (int i = 0; i < MW; ++i) {
-            const int64_t gm = (int64_t)mg * MW + i;
-            const bool v = active && gm < g.total_mtiles;
+        for (int i = 0; i < INF_MW; ++i) {
+            const int64_t gm = ((int64_t)mb * INF_WAVES + wv) * INF_MW + i;
+            const bool v = gm < g.total_mtiles;
             const int64_t b = v ? gm / g.mt_per_img : 0;
             const int mt = v ? (int)(gm % g.mt_per_img) : 0;
             const int pos = min(mt * 16 + c, g.HoWo - 1);  // rows past the image are computed, not stored
             const int y = pos / g.Wo, xx = pos % g.Wo;
-            abase[i] = (uint32_t)(((b * g.Hp + y) * g.Wp + xx) * g.CP);
+            abase[i] = tpad + (uint32_t)(((b * g.Hp + y) * g.Wp + xx) * g.CP);
             img[i] = v ? b : -1;
             mpos0[i] = mt * 16 + gq * 4;
         }
-        f4 acc[MW][NW];
+        f4 acc[INF_MW][INF_NW];
 #pragma unroll
-        for (int i = 0; i < MW; ++i)
+        for (int i = 0; i < INF_MW; ++i)
 #pragma unroll
-            for (int n = 0; n < NW; ++n) acc[i][n] = f4{0.f, 0.f, 0.f, 0.f};
-        for (int k0 = 0; k0 < g.ksteps; k0 += kc) {
-            const int nk = min(kc, g.ksteps - k0);
-            if (!resident) {  // stream this chunk of fragments through LDS (uniform branch)
-                __syncthreads();
-                fill(k0, nk);
-                __syncthreads();
-            }
-            const uint4 *fr = frl + (resident ? (size_t)k0 * NW * 2 * 64 : 0);
-            if (!active) continue;
-            for (int kl = 0; kl < nk; ++kl) {
-                const int2 o = koff_l[(k0 + kl) * 4 + gq];
-                half8 bh[NW], bl[NW];
+            for (int n = 0; n < INF_NW; ++n) acc[i][n] = f4{0.f, 0.f, 0.f, 0.f};
+        // the spike words of a chunk are loaded with its fill, one chunk ahead; two
+        // register sets, the loop unrolled by two chunks so that both are static
+        uint32_t aw0[INF_KC][INF_MW][2], aw1[INF_KC][INF_MW][2];
+        // With CP a multiple of 64 a cell has an even number of K-steps and K-steps
+        // 2m, 2m+1 of it are 16 consecutive, aligned bytes of a lane's run; with
+        // CP >= 8 a K-step's two words are adjacent; with CP == 4 separate cells.
+        const int wide = g.CP % 64 == 0 ? 2 : (g.CP >= 8 ? 1 : 0);
+        auto load_aw = [&](int ch, uint32_t (&dst)[INF_KC][INF_MW][2]) {
+            if (wide == 2) {
 #pragma unroll
-                for (int n = 0; n < NW; ++n) {
-                    bh[n] = __builtin_bit_cast(half8, fr[(kl * NW + n) * 128 + lane]);
-                    bl[n] = __builtin_bit_cast(half8, fr[(kl * NW + n) * 128 + 64 + lane]);
+                for (int kl = 0; kl < INF_KC; kl += 2) {
+                    const int2 o = koff_l[min(ch * INF_KC + kl, g.ksteps - 2) * 4 + gq];
+#pragma unroll
+                    for (int i = 0; i < INF_MW; ++i) {
+                        const uint4 v = *reinterpret_cast<const uint4 *>(abase[i] + (uint32_t)o.x);
+                        dst[kl][i][0] = v.x;
+                        dst[kl][i][1] = v.y;
+                        dst[kl + 1][i][0] = v.z;
+                        dst[kl + 1][i][1] = v.w;
+                    }
                 }
+            } else {
 #pragma unroll
-                for (int i = 0; i < MW; ++i) {
-                    const uint32_t w0 = *reinterpret_cast<const uint32_t *>(tpad + abase[i] + (uint32_t)o.x);
-                    const uint32_t w1 = *reinterpret_cast<const uint32_t *>(tpad + abase[i] + (uint32_t)o.y);
-                    uint32_t xn[4];
-                    neg_times(w0, xn[0], xn[1]);
-                    neg_times(w1, xn[2], xn[3]);
-                    const half8 a = spike_operand(xn, ct);
+                for (int kl = 0; kl < INF_KC; ++kl) {
+                    const int2 o = koff_l[min(ch * INF_KC + kl, g.ksteps - 1) * 4 + gq];
 #pragma unroll
-                    for (int n = 0; n < NW; ++n) {
-                        acc[i][n] = mfma(a, bh[n], acc[i][n]);
-                        acc[i][n] = mfma(a, bl[n], acc[i][n]);
+                    for (int i = 0; i < INF_MW; ++i) {
+                        if (wide == 1) {
+                            const uint2 v = *reinterpret_cast<const uint2 *>(abase[i] + (uint32_t)o.x);
+                            dst[kl][i][0] = v.x;
+                            dst[kl][i][1] = v.y;
+                        } else {
+                            dst[kl][i][0] = *reinterpret_cast<const uint32_t *>(abase[i] + (uint32_t)o.x);
+                            dst[kl][i][1] = *reinterpret_cast<const uint32_t *>(abase[i] + (uint32_t)o.y);
+                        }
                     }
                 }
             }
+        };
+        auto chunk = [&](int ch, const uint32_t (&awc)[INF_KC][INF_MW][2], uint32_t (&awn)[INF_KC][INF_MW][2]) {
+            const int nk = min(INF_KC, g.ksteps - ch * INF_KC);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's words and fill of chunk ch landed
+            __syncthreads();  // every wave's part of chunk ch is in LDS; chunk ch-1's buffer is free
+            if (ch + 1 < nchunks) {
+                load_aw(ch + 1, awn);
+                fill(ch + 1);
+            }
+            const uint4 *fr = cbuf + (ch & 1) * INF_CHUNK_U4 + lane;
+#pragma unroll
+            for (int kl = 0; kl < INF_KC; ++kl) {
+                if (kl >= nk) break;  // uniform
+                half8 bh[INF_NW], bl[INF_NW];
+#pragma unroll
+                for (int n = 0; n < INF_NW; ++n) {
+                    bh[n] = __builtin_bit_cast(half8, fr[((kl * INF_NW + n) * 2) * 64]);
+                    bl[n] = __builtin_bit_cast(half8, fr[((kl * INF_NW + n) * 2 + 1) * 64]);
+                }
+                half8 a[INF_MW];
+#pragma unroll
+                for (int i = 0; i < INF_MW; ++i) {
+                    uint32_t xn[4];
+                    neg_times(awc[kl][i][0], xn[0], xn[1]);
+                    neg_times(awc[kl][i][1], xn[2], xn[3]);
+                    a[i] = spike_operand(xn, ct);
+                }
+#pragma unroll
+                for (int i = 0; i < INF_MW; ++i)
+#pragma unroll
+                    for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma(a[i], bh[n], acc[i][n]);
+#pragma unroll
+                for (int i = 0; i < INF_MW; ++i)
+#pragma unroll
+                    for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma(a[i], bl[n], acc[i][n]);
+            }
+        };
+        __syncthreads();  // the buffers are free (previous task done), koff is visible
+        load_aw(0, aw0);
+        fill(0);
+        for (int ch = 0; ch < nchunks; ch += 2) {
+            chunk(ch, aw0, aw1);
+            if (ch + 1 < nchunks) chunk(ch + 1, aw1, aw0);
         }
-        if (!active) continue;
+        // the last step's potentials and spikes, the first-spike time and potential
 #pragma unroll
-        for (int i = 0; i < MW; ++i)
+        for (int i = 0; i < INF_MW; ++i)
 #pragma unroll
-            for (int n = 0; n < NW; ++n) {
-                const int f = (ng * NW + n) * 16 + c;
+            for (int n = 0; n < INF_NW; ++n) {
+                const int f = (ng * INF_NW + n) * 16 + c;
                 if (img[i] < 0 || f >= g.Cout || mpos0[i] >= g.HoWo) continue;
                 const f4 v = acc[i][n] * inv_s;
                 const int lim = g.HoWo - mpos0[i];
-                const int64_t ob = img[i] * g.T * tstride + (int64_t)f * g.HoWo + mpos0[i];
+                const int64_t o = (img[i] * g.T + g.T - 1) * tstride + (int64_t)f * g.HoWo + mpos0[i];
+                const int64_t of = (img[i] * (int64_t)g.Cout + f) * g.HoWo + mpos0[i];
                 uint32_t sp = 0, tv = 0;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     sp |= (uint32_t)(v[q] > 0.0f) << (8 * q);
                     tv |= (uint32_t)(v[q] > 0.0f ? g.T - 1 : g.T) << (8 * q);
                 }
-                const int64_t of = (img[i] * (int64_t)g.Cout + f) * g.HoWo + mpos0[i];
                 if (VEC) {  // HoWo % 4 == 0: the 4 positions are in the image and aligned
-                    for (int tt = 0; tt < g.T - 1; ++tt) {
-                        const int64_t o = ob + (int64_t)tt * tstride;
-                        if (P) *reinterpret_cast<f4 *>(P + o) = f4{0.f, 0.f, 0.f, 0.f};
-                        if (S) *reinterpret_cast<uint32_t *>(S + o) = 0u;
-                    }
-                    const int64_t o = ob + (int64_t)(g.T - 1) * tstride;
                     if (P) *reinterpret_cast<f4 *>(P + o) = v;
                     if (S) *reinterpret_cast<uint32_t *>(S + o) = sp;
                     *reinterpret_cast<uint32_t *>(TF + of) = tv;
                     *reinterpret_cast<f4 *>(VF + of) = v;
                 } else {
-                    for (int tt = 0; tt < g.T; ++tt) {
-                        const int64_t o = ob + (int64_t)tt * tstride;
-                        const bool last = tt == g.T - 1;
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            if (q < lim) {
-                                if (P) P[o + q] = last ? v[q] : 0.0f;
-                                if (S) S[o + q] = last ? (uint8_t)(sp >> (8 * q)) : (uint8_t)0;
-                            }
-                    }
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
                         if (q < lim) {
+                            if (P) P[o + q] = v[q];
+                            if (S) S[o + q] = (uint8_t)(sp >> (8 * q));
                             TF[of + q] = (uint8_t)(tv >> (8 * q));
                             VF[of + q] = v[q];
                         }
@@ -696,12 +742,40 @@ __global__ __launch_bounds__(256, 2) void k_conv_fire_inf(const uint8_t *__restr
     }
 }
 
+// Zero potentials (f32) and spikes (u8) of steps 0..T-2 of every image: per
+// image one contiguous run of (T-1)*Cout*Ho*Wo elements.  Grid (chunk, image).
+__global__ __launch_bounds__(256) void k_zero_planes(ConvGeom g, float *__restrict__ P, uint8_t *__restrict__ S) {
+    const int64_t plane = (int64_t)g.Cout * g.HoWo;
+    const int64_t n = (int64_t)(g.T - 1) * plane;
+    for (int64_t b = blockIdx.y; b < g.B; b += gridDim.y) {
+        if (P) {
+            float *p = P + b * g.T * plane;
+            const int64_t head = min<int64_t>(n, (int64_t)((16 - ((uintptr_t)p & 15)) & 15) / 4);
+            const int64_t body = (n - head) & ~(int64_t)3;
+            for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < head; i += (int64_t)gridDim.x * 256) p[i] = 0.0f;
+            for (int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4; i < body; i += (int64_t)gridDim.x * 1024)
+                *reinterpret_cast<f4 *>(p + head + i) = f4{0.f, 0.f, 0.f, 0.f};
+            for (int64_t i = head + body + (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+                p[i] = 0.0f;
+        }
+        if (S) {
+            uint8_t *q = S + b * g.T * plane;
+            const int64_t head = min<int64_t>(n, (int64_t)((16 - ((uintptr_t)q & 15)) & 15));
+            const int64_t body = (n - head) & ~(int64_t)15;
+            for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < head; i += (int64_t)gridDim.x * 256) q[i] = 0;
+            for (int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 16; i < body; i += (int64_t)gridDim.x * 4096)
+                *reinterpret_cast<uint4 *>(q + head + i) = uint4{0u, 0u, 0u, 0u};
+            for (int64_t i = head + body + (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+                q[i] = 0;
+        }
+    }
+}
+
 __global__ void k_zero_u32(unsigned *p, int n) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) p[i] = 0u;
 }
 
-constexpr int MAX_NGROUPS_COUNT = 8 * 64;  // (XCD, feature group) counters reserved in the workspace
 
 struct ConvPlan {
     ConvGeom g;
@@ -753,7 +827,7 @@ size_t plan_workspace(const ConvPlan &pl) {
     c.take<half8>(pl.frag_count);
     c.take<half8>(pl.frag_count);
     c.take<int2>(pl.koff_count);
-    c.take<unsigned>(MAX_NGROUPS_COUNT + 2);  // work counters, max|w| bits, 1/scale
+    c.take<unsigned>(2);  // max|w| bits, 1/scale
     return spk::align_up(c.off, 256);
 }
 
@@ -775,27 +849,19 @@ void launch_fin(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const i
                        VF);
 }
 
-template <int MW, int NW, bool VEC>
-void launch_inf(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, unsigned *counters,
-                const float *inv_scale, const ConvGeom &g, float *P, uint8_t *S, uint8_t *TF, float *VF,
-                hipStream_t st) {
-    const int64_t n_mgroups = spk::ceil_div(g.total_mtiles, MW);
-    const int64_t n_mblocks = spk::ceil_div(n_mgroups, 4);
-    const int n_ngroups = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), NW);
-    const size_t koff_bytes = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16);
-    const size_t step = (size_t)NW * 2 * 64 * 16;  // one K-step of fragments
-    const int resident = koff_bytes + (size_t)g.ksteps * step <= INF_LDS_BUDGET;
-    const int kc = resident ? g.ksteps
-                            : (int)std::max<size_t>(1, std::min<size_t>(INF_KC, (INF_LDS_BUDGET - koff_bytes) / step));
-    const size_t lds = koff_bytes + (size_t)kc * step;
-    // about two workgroups per CU (256 CUs, 32 per XCD), a multiple of the feature groups per XCD
-    const int64_t want = spk::ceil_div(n_mblocks * n_ngroups, 8);
-    const int64_t per_xcd = std::min<int64_t>(spk::ceil_div(std::max<int64_t>(64, n_ngroups), n_ngroups) * n_ngroups,
-                                              spk::ceil_div(want, n_ngroups) * n_ngroups);
-    // the 8 * n_ngroups counters (<= MAX_NGROUPS_COUNT since Cout <= 4096) were zeroed by the caller
-    hipLaunchKernelGGL((k_conv_fire_inf<MW, NW, VEC>), dim3((unsigned)(per_xcd * 8)), dim3(256), lds, st, tpad, whi, wlo,
-                       koff2, g, (int)n_mgroups, (int)n_mblocks, n_ngroups, kc, resident, counters, inv_scale, P, S,
-                       TF, VF);
+template <bool VEC>
+void launch_inf(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, const float *inv_scale,
+                const ConvGeom &g, float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
+    const int n_mb = (int)spk::ceil_div(g.total_mtiles, INF_WAVES * INF_MW);
+    const int n_ng = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), INF_NW);
+    const size_t lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16) + 2 * (size_t)INF_CHUNK_U4 * 16;
+    if (g.T > 1 && (P || S)) {
+        const int64_t n = (int64_t)(g.T - 1) * g.Cout * g.HoWo;
+        const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>(64, spk::ceil_div(n, 256 * 16)));
+        hipLaunchKernelGGL(k_zero_planes, dim3(gx, (unsigned)std::min(g.B, 65535)), dim3(256), 0, st, g, P, S);
+    }
+    hipLaunchKernelGGL((k_conv_fire_inf<VEC>), dim3(256), dim3(INF_WAVES * 64), lds, st, tpad, whi, wlo, koff2, g, n_mb,
+                       n_ng, inv_scale, P, S, TF, VF);
 }
 
 }  // namespace
@@ -829,9 +895,8 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     half8 *whi = cv.take<half8>(pl.frag_count);
     half8 *wlo = cv.take<half8>(pl.frag_count);
     int2 *koff2 = cv.take<int2>(pl.koff_count);
-    unsigned *counters = cv.take<unsigned>(MAX_NGROUPS_COUNT + 2);
-    unsigned *maxbits = counters + MAX_NGROUPS_COUNT;
-    float *inv_scale = reinterpret_cast<float *>(counters + MAX_NGROUPS_COUNT + 1);
+    unsigned *maxbits = cv.take<unsigned>(2);
+    float *inv_scale = reinterpret_cast<float *>(maxbits + 1);
     hipStream_t st = spk::as_stream(stream);
 
     // finite-threshold launch configuration (validated before anything is enqueued)
@@ -858,6 +923,9 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     const bool alds = a_words <= FIN_CW * 64 * FIN_AW && koff_lds + stage_lds + a_lds <= lds_limit;
     const bool blds = koff_lds + frag_lds + stage_lds + (alds ? a_lds : 0) <= lds_limit;
     const size_t fin_lds = koff_lds + (blds ? frag_lds : 0) + stage_lds + (alds ? a_lds : 0);
+    const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4 * 16;
+    SPK_REQUIRE(!inf_mode || inf_lds <= lds_limit, SPK_E_RANGE,
+                "spk_conv_fire: needs %zu bytes of LDS per workgroup, the device has %zu", inf_lds, lds_limit);
     SPK_REQUIRE(inf_mode || fin_lds <= lds_limit, SPK_E_RANGE,
                 "spk_conv_fire: needs %zu bytes of LDS per workgroup, the device has %zu", fin_lds, lds_limit);
 
@@ -866,8 +934,7 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     hipLaunchKernelGGL(k_pad_first_spike, dim3((unsigned)spk::ceil_div(g.Hp, rows_per_chunk),
                                                (unsigned)std::min(B, 65535)),
                        dim3(256), 0, st, wave, g, rows_per_chunk, tpad);
-    hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)spk::ceil_div(MAX_NGROUPS_COUNT + 2, 256)), dim3(256), 0, st,
-                       counters, MAX_NGROUPS_COUNT + 2);
+    hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(64), 0, st, maxbits, 1);
     const int64_t nw = (int64_t)Cout * Cin * K * K;
     hipLaunchKernelGGL(k_weight_absmax, dim3((unsigned)std::min<int64_t>(256, spk::ceil_div(nw, 256))), dim3(256), 0,
                        st, weight, nw, maxbits);
@@ -876,10 +943,9 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
                        whi, wlo, koff2, inv_scale);
     if (inf_mode) {
         if (vec)
-            launch_inf<2, 4, true>(tpad, whi, wlo, koff2, counters, inv_scale, g, potentials, spikes, t_first, v_first, st);
+            launch_inf<true>(tpad, whi, wlo, koff2, inv_scale, g, potentials, spikes, t_first, v_first, st);
         else
-            launch_inf<2, 4, false>(tpad, whi, wlo, koff2, counters, inv_scale, g, potentials, spikes, t_first, v_first,
-                                    st);
+            launch_inf<false>(tpad, whi, wlo, koff2, inv_scale, g, potentials, spikes, t_first, v_first, st);
     } else {
 #define SPK_FIN(G, BL, AL)                                                                                    \
     launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, g, n_pairs, n_chunks, chunk_tiles, np_max, a_words, \
