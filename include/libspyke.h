@@ -113,7 +113,9 @@ SPK_API int spk_validate_wave(const uint8_t *wave, int B, int T, int C, int H, i
  *   spikes     u8  [B][T][Cout][Ho][Wo] or NULL: 1 where the neuron fires.
  *   t_first    u8  [B][Cout][Ho][Wo]: first firing step, T if silent.
  *   v_first    f32 [B][Cout][Ho][Wo]: potential at t_first, 0 if silent.
- * Limits: 1 <= T <= 255, Ho, Wo >= 1, Cin*K*K <= 16384, Cout <= 4096.
+ * Limits: 1 <= T <= 255, Ho, Wo >= 1, Ho*Wo <= 2^26, Cout <= 4096,
+ * K*K*CP <= 16384 and (W+2*pad)*CP <= 32768 where CP is Cin rounded up to 4
+ * (Cin <= 4) or to a multiple of 8, and B*(H+2*pad)*(W+2*pad)*CP < 2^32.
  * Workspace: spk_conv_fire_workspace_size(...) bytes.                      */
 SPK_API size_t spk_conv_fire_workspace_size(int B, int T, int Cin, int H, int W, int Cout, int K, int pad);
 SPK_API int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, int W,
@@ -172,19 +174,28 @@ SPK_API int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int T,
  * clamp; and stored as float.
  *   weight    f32 [Cout][Cin][K][K] (updated in place)
  *   pre_wave  u8  [B][T][Cin][H][W]: the layer's (unpadded) input wave
- *   winners / n_winners as produced by spk_kwta with the same k.           */
+ *   winners / n_winners as produced by spk_kwta with the same k.
+ * Limits: T <= 255, Cout*B < 2^31, Cin*K*K <= 65535*256, and
+ * ceil(B*min(k,Cout)/32) + Cout <= 65535.
+ * Workspace: spk_stdp_workspace_size(Cout, Cin, K, B, k) bytes (per-feature
+ * update lists and the packed pre-synaptic bits); calls that run
+ * concurrently need separate workspaces.                                  */
+SPK_API size_t spk_stdp_workspace_size(int Cout, int Cin, int K, int B, int k);
 SPK_API int spk_stdp(float *weight, int Cout, int Cin, int K, int pad,
              const uint8_t *pre_wave, int B, int T, int H, int W,
              const int32_t *winners, const int32_t *n_winners, int k,
-             float a_plus, float a_minus, float lb, float ub, int stabilizer, void *stream);
+             float a_plus, float a_minus, float lb, float ub, int stabilizer,
+             void *workspace, size_t ws_bytes, void *stream);
 
 /* R-STDP (section "snn Module": two STDP objects; tutorial: anti-STDP
  * negates the learning rates): as spk_stdp, with reward i8 [B] per image:
- * +1 applies (a_plus, a_minus), -1 applies (-a_plus, -a_minus), 0 skips.   */
+ * +1 applies (a_plus, a_minus), -1 applies (-a_plus, -a_minus), 0 skips.
+ * Same workspace as spk_stdp.                                              */
 SPK_API int spk_rstdp(float *weight, int Cout, int Cin, int K, int pad,
               const uint8_t *pre_wave, int B, int T, int H, int W,
               const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward,
-              float a_plus, float a_minus, float lb, float ub, int stabilizer, void *stream);
+              float a_plus, float a_minus, float lb, float ub, int stabilizer,
+              void *workspace, size_t ws_bytes, void *stream);
 
 /* Decision and reward (tutorial: the first winner's feature maps to a
  * class; reward when it equals the label, punish otherwise, nothing for a

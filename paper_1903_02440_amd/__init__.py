@@ -46,8 +46,9 @@ _SIGS = {
     "spk_pool_first_spike": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
     "spk_kwta_workspace_size": (_Z, [_I, _I, _I, _I]),
     "spk_kwta": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _Z, _P]),
-    "spk_stdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _F, _F, _F, _F, _I, _P]),
-    "spk_rstdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _P, _F, _F, _F, _F, _I, _P]),
+    "spk_stdp_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
+    "spk_stdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _F, _F, _F, _F, _I, _P, _Z, _P]),
+    "spk_rstdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _P, _F, _F, _F, _F, _I, _P, _Z, _P]),
     "spk_decide": (_I, [_P, _P, _I, _I, _P, _I, _P, _P, _P]),
     "spk_count_events": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
 }
@@ -260,24 +261,32 @@ def _stdp_args(weight, pre_wave, winners, n_winners):
     return Cout, Cin, K, B, T, H, W, k
 
 
+def spk_stdp_workspace_size(Cout, Cin, K, B, k) -> int:
+    return int(_lib.spk_stdp_workspace_size(Cout, Cin, K, B, k))
+
+
 def spk_stdp(weight, pad, pre_wave, winners, n_winners, a_plus, a_minus, lb=0.0, ub=1.0, stabilizer=True,
-             stream=None):
+             workspace=None, stream=None):
     """Eq.4 on the winners' weights (in place on `weight`), ordered replay over images."""
     Cout, Cin, K, B, T, H, W, k = _stdp_args(weight, pre_wave, winners, n_winners)
+    n = spk_stdp_workspace_size(Cout, Cin, K, B, k)
+    ws = _ws(workspace, n, weight.device)
     _check(_lib.spk_stdp(_ptr(weight), Cout, Cin, K, pad, _ptr(pre_wave), B, T, H, W, _ptr(winners),
                          _ptr(n_winners), k, float(a_plus), float(a_minus), float(lb), float(ub), int(bool(stabilizer)),
-                         _stream(stream)))
+                         _ptr(ws), n, _stream(stream)))
     return weight
 
 
 def spk_rstdp(weight, pad, pre_wave, winners, n_winners, reward, a_plus, a_minus, lb=0.0, ub=1.0, stabilizer=True,
-              stream=None):
+              workspace=None, stream=None):
     """R-STDP: reward i8 [B] in {+1,-1,0} selects STDP, anti-STDP or nothing per image."""
     Cout, Cin, K, B, T, H, W, k = _stdp_args(weight, pre_wave, winners, n_winners)
     _need(reward, torch.int8, (B,), "reward")
+    n = spk_stdp_workspace_size(Cout, Cin, K, B, k)
+    ws = _ws(workspace, n, weight.device)
     _check(_lib.spk_rstdp(_ptr(weight), Cout, Cin, K, pad, _ptr(pre_wave), B, T, H, W, _ptr(winners),
                           _ptr(n_winners), k, _ptr(reward), float(a_plus), float(a_minus), float(lb), float(ub),
-                          int(bool(stabilizer)), _stream(stream)))
+                          int(bool(stabilizer)), _ptr(ws), n, _stream(stream)))
     return weight
 
 

@@ -7,131 +7,202 @@
 // the label, punish otherwise, nothing for a silent sample).
 //
 // Batch semantics (the paper leaves batch plasticity open): frozen forward,
-// ordered replay.  A workgroup owns one output feature f and 256 of its
-// weights, so no two threads touch the same weight.  It gathers, in image
-// order, the images whose winners include f (one image has at most one
-// winner per feature).  Every thread then first fetches, with independent
-// loads, the pre-synaptic bit of each update for its weight (T_j <= T_i is
-// one byte of the cumulative input wave at step t_i) into its column of an
-// LDS bit array, and only then replays the chain of updates on its weight.  The arithmetic is double precision in the order
+// ordered replay.  Each feature f gets the list, in image order, of the
+// images whose winners include f (one image has at most one winner per
+// feature).  The pre-synaptic bit of every (update, weight) pair (T_j <= T_i
+// is one byte of the cumulative input wave at step t_i) is gathered by a
+// fully parallel pass and packed 32 updates to a word, so the serial part --
+// one thread per weight replaying its feature's chain of updates in image
+// order -- only reads coalesced bit words.  A feature that wins many images
+// has a long chain, but its chains run on as many threads as it has weights.
+// The arithmetic is double precision in the order
 //     d = (w-lb)*(ub-w); u = a*d; w = w+u; clamp; round to float
 // so that every update is the exactly rounded value of that expression.
+#include <algorithm>
+#include <cmath>
+
 #include "common.hpp"
 
 namespace {
 
-constexpr int CHUNK = 1024;  // images scanned per pass (4 per thread)
+constexpr int LIST_THREADS = 1024;  // images scanned per pass of the list kernel
 
 struct StdpArgs {
     int Cout, Cin, K, pad, B, T, H, W, k, stabilizer;
     float a_plus, a_minus, lb, ub;
 };
 
-// Grid: (feature f, chunk of 256 of its Cin*K*K weights).  Each thread owns
-// one weight and replays the feature's update list on it in image order.
-__global__ __launch_bounds__(256) void k_stdp(float *__restrict__ weight, const uint8_t *__restrict__ pre,
-                                              const int32_t *__restrict__ winners, const int32_t *__restrict__ n_win,
-                                              const int8_t *__restrict__ reward, StdpArgs a) {
-#pragma clang fp contract(off)
-    __shared__ int4 upd[CHUNK];   // (image, t, y, x)
-    __shared__ int usg[CHUNK];    // +1 / -1
-    __shared__ uint32_t bits[CHUNK / 32][256];  // pre-synaptic bits: word u/32 of thread tid
-    __shared__ int scan[256];
-    __shared__ int total;
-    const int f = blockIdx.x, tid = threadIdx.x;
-    const int KK = a.K * a.K, Kc = a.Cin * KK;
-    const int e = blockIdx.y * 256 + tid;
-    const bool own = e < Kc;
-    const int ci = own ? e / KK : 0, ky = own ? (e % KK) / a.K : 0, kx = own ? e % a.K : 0;
-    const int64_t plane = (int64_t)a.Cin * a.H * a.W;
-    const int64_t cioff = (int64_t)ci * a.H * a.W;
-    const double dlb = a.lb, dub = a.ub, dap = a.a_plus, dam = a.a_minus;
-    float wf = own ? weight[(int64_t)f * Kc + e] : 0.0f;
+// Workspace of one call (sizes in spk_stdp_workspace_size):
+//   count [Cout]           updates of each feature
+//   woff  [Cout+1]         first bit row of each feature (exclusive prefix of ceil(count/32))
+//   list  [Cout][B] int4   the feature's updates in image order: (image, t, y, x)
+//   lsign [Cout][B] i8     +1 / -1 (STDP / anti-STDP)
+//   bits  [rows][Kc] u32   bit q of row woff[f]+i, column e: pre-synaptic bit of update 32i+q on weight e
+struct StdpWork {
+    int *count, *woff;
+    int4 *list;
+    int8_t *lsign;
+    uint32_t *bits;
+    int64_t rows;  // capacity of bits in rows of Kc words
+};
 
-    for (int b0 = 0; b0 < a.B; b0 += CHUNK) {
-        int slot[4], sg[4], mine = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            slot[j] = -1;
-            sg[j] = 1;
-            const int b = b0 + tid * 4 + j;
-            if (b >= a.B) continue;
-            if (reward) {
-                if (reward[b] == 0) continue;
-                sg[j] = reward[b] > 0 ? 1 : -1;
-            }
+int64_t bit_rows(int Cout, int B, int k) { return ((int64_t)B * std::min(k, Cout) + 31) / 32 + Cout; }
+
+StdpWork carve(void *ws, int Cout, int Cin, int K, int B, int k, size_t *bytes) {
+    spk::Carver c(ws);
+    StdpWork w;
+    w.count = c.take<int>(Cout);
+    w.woff = c.take<int>(Cout + 1);
+    w.list = c.take<int4>((size_t)Cout * B);
+    w.lsign = c.take<int8_t>((size_t)Cout * B);
+    w.rows = bit_rows(Cout, B, k);
+    w.bits = c.take<uint32_t>((size_t)w.rows * Cin * K * K);
+    if (bytes) *bytes = spk::align_up(c.off, 256);
+    return w;
+}
+
+// 1. Grid: one workgroup per feature f.  For each pass over up to 1024 images
+// (one per thread) it finds the image's winner of feature f (one image has at
+// most one), then a wave ballot and a scan of the 16 wave counts place the
+// updates in image order.
+__global__ __launch_bounds__(LIST_THREADS) void k_stdp_list(const int32_t *__restrict__ winners,
+                                                            const int32_t *__restrict__ n_win,
+                                                            const int8_t *__restrict__ reward, StdpArgs a, StdpWork w) {
+    __shared__ int wave_cnt[LIST_THREADS / 64];
+    const int f = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    int base = 0;
+    for (int b0 = 0; b0 < a.B; b0 += LIST_THREADS) {
+        const int b = b0 + tid;
+        int slot = -1, sg = 1;
+        if (b < a.B && (!reward || reward[b] != 0)) {
+            if (reward) sg = reward[b] > 0 ? 1 : -1;
             const int nw = min(n_win[b], a.k);
             const int32_t *wb = winners + (int64_t)b * a.k * 4;
-            // every record is read (no early exit), so the loads overlap
-            for (int w = 0; w < a.k; ++w) {
-                const int fw = wb[4 * w], t = wb[4 * w + 1];
-                if (w < nw && fw == f && slot[j] < 0 && t >= 0 && t < a.T) slot[j] = w;
+            for (int q = 0; q < a.k; ++q) {  // every record is read, so the loads overlap
+                const int fw = wb[4 * q], t = wb[4 * q + 1];
+                if (q < nw && fw == f && slot < 0 && t >= 0 && t < a.T) slot = q;
             }
-            mine += slot[j] >= 0;
         }
-        // block exclusive scan of the per-thread counts keeps image order
-        scan[tid] = mine;
+        const uint64_t mask = __ballot(slot >= 0);
+        if (lane == 0) wave_cnt[wv] = __popcll(mask);
         __syncthreads();
-        for (int s = 1; s < 256; s <<= 1) {
-            const int v = tid >= s ? scan[tid - s] : 0;
-            __syncthreads();
-            scan[tid] += v;
-            __syncthreads();
+        int off = base + __popcll(mask & ((1ull << lane) - 1ull)), n = 0;
+        for (int q = 0; q < LIST_THREADS / 64; ++q) {
+            off += q < wv ? wave_cnt[q] : 0;
+            n += wave_cnt[q];
         }
-        int off = scan[tid] - mine;
-        if (tid == 255) total = scan[255];
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if (slot[j] >= 0) {
-                const int b = b0 + tid * 4 + j;
-                const int32_t *o = winners + ((int64_t)b * a.k + slot[j]) * 4;
-                upd[off] = make_int4(b, o[1], o[2], o[3]);
-                usg[off] = sg[j];
-                ++off;
-            }
+        if (slot >= 0) {
+            const int32_t *o = winners + ((int64_t)b * a.k + slot) * 4;
+            w.list[(int64_t)f * a.B + off] = make_int4(b, o[1], o[2], o[3]);
+            w.lsign[(int64_t)f * a.B + off] = (int8_t)sg;
+        }
+        base += n;
+        __syncthreads();  // wave_cnt is rewritten by the next pass
+    }
+    if (tid == 0) w.count[f] = base;
+}
+
+// 2. One workgroup: woff[f] = sum over f' < f of ceil(count[f'] / 32).
+__global__ __launch_bounds__(1024) void k_stdp_offsets(int Cout, StdpWork w) {
+    __shared__ int part[1024];
+    const int tid = threadIdx.x;
+    const int per = (Cout + 1023) / 1024, f0 = tid * per;
+    int sum = 0;
+    for (int f = f0; f < min(Cout, f0 + per); ++f) sum += (w.count[f] + 31) / 32;
+    part[tid] = sum;
+    __syncthreads();
+    for (int s = 1; s < 1024; s <<= 1) {
+        const int v = tid >= s ? part[tid - s] : 0;
         __syncthreads();
-        const int n = total;
-        if (own && n > 0) {
-            // phase 1: the pre-synaptic bit of every update (the input wave at
-            // the winner's step, 0 in the padding).  The 32 loads of a word are
-            // unconditional (a masked-off one reads the wave's first byte), so
-            // they are all in flight before the first is used.
-            for (int u0 = 0; u0 < n; u0 += 32) {
-                uint8_t v[32];
-                uint32_t ok = 0;
-#pragma unroll
-                for (int q = 0; q < 32; ++q) {
-                    const int4 qq = upd[min(u0 + q, n - 1)];
-                    const int iy = qq.z + ky - a.pad, ix = qq.w + kx - a.pad;
-                    const bool in = u0 + q < n && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
-                    const int64_t at = ((int64_t)qq.x * a.T + qq.y) * plane + cioff + (int64_t)iy * a.W + ix;
-                    v[q] = pre[in ? at : 0];
-                    ok |= (uint32_t)in << q;
-                }
-                uint32_t word = 0;
-#pragma unroll
-                for (int q = 0; q < 32; ++q) word |= (uint32_t)(v[q] != 0) << q;
-                bits[u0 >> 5][tid] = word & ok;
-            }
-            // phase 2: the ordered chain of updates on this weight
-            for (int u0 = 0; u0 < n; u0 += 32) {
-                const uint32_t word = bits[u0 >> 5][tid];
-                const int cnt = min(32, n - u0);
-                for (int q = 0; q < cnt; ++q) {
-                    const double r = (double)usg[u0 + q] * (((word >> q) & 1u) ? dap : dam);
-                    const double w = (double)wf;
-                    const double d = a.stabilizer ? (w - dlb) * (dub - w) : 1.0;
-                    const double du = r * d;
-                    double nw = w + du;
-                    if (nw < dlb) nw = dlb;
-                    if (nw > dub) nw = dub;
-                    wf = (float)nw;
-                }
-            }
-        }
+        part[tid] += v;
         __syncthreads();
     }
-    if (own) weight[(int64_t)f * Kc + e] = wf;
+    int run = part[tid] - sum;
+    for (int f = f0; f < min(Cout, f0 + per); ++f) {
+        w.woff[f] = run;
+        run += (w.count[f] + 31) / 32;
+    }
+    if (tid == 1023) w.woff[Cout] = part[1023];
+}
+
+// 3. Grid (chunk of 256 weights, bit row).  Row r belongs to the feature f
+// with woff[f] <= r < woff[f+1] (binary search); its thread for weight
+// e = (ci, ky, kx) loads the pre-synaptic byte of each of the row's up to 32
+// updates -- the layer input at (image, winner step, ci, y+ky-pad, x+kx-pad),
+// 0 in the padding -- with independent loads and packs the 32 bits.
+__global__ __launch_bounds__(256) void k_stdp_bits(const uint8_t *__restrict__ pre, StdpArgs a, StdpWork w) {
+    const int r = blockIdx.y;
+    if (r >= w.woff[a.Cout]) return;  // uniform
+    int lo = 0, hi = a.Cout - 1;      // the largest f with woff[f] <= r
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (w.woff[mid] <= r) lo = mid;
+        else hi = mid - 1;
+    }
+    const int f = lo, u0 = (r - w.woff[f]) * 32, cnt = min(32, w.count[f] - u0);
+    const int KK = a.K * a.K, Kc = a.Cin * KK;
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e >= Kc) return;
+    const int ci = e / KK, ky = (e % KK) / a.K, kx = e % a.K;
+    const int64_t plane = (int64_t)a.Cin * a.H * a.W, cioff = (int64_t)ci * a.H * a.W;
+    const int4 *lst = w.list + (int64_t)f * a.B + u0;
+    uint8_t v[32];
+#pragma unroll
+    for (int q = 0; q < 32; ++q) {
+        v[q] = 0;
+        if (q < cnt) {
+            const int4 u = lst[q];
+            const int iy = u.z + ky - a.pad, ix = u.w + kx - a.pad;
+            if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
+                v[q] = pre[((int64_t)u.x * a.T + u.y) * plane + cioff + (int64_t)iy * a.W + ix];
+        }
+    }
+    uint32_t word = 0;
+#pragma unroll
+    for (int q = 0; q < 32; ++q) word |= (uint32_t)(v[q] != 0) << q;
+    w.bits[(int64_t)r * Kc + e] = word;
+}
+
+// 4. Grid (chunk of 256 weights, feature): each thread replays its weight's
+// chain of updates in image order, 32 per bit word (the next word is loaded
+// while the current one is replayed); the signs of 1024 updates at a time sit
+// in LDS.
+__global__ __launch_bounds__(256) void k_stdp_apply(float *__restrict__ weight, StdpArgs a, StdpWork w) {
+#pragma clang fp contract(off)
+    __shared__ int8_t sgn[1024];
+    const int f = blockIdx.y, tid = threadIdx.x;
+    const int n = w.count[f];
+    if (n == 0) return;  // uniform
+    const int KK = a.K * a.K, Kc = a.Cin * KK;
+    const int e = blockIdx.x * 256 + tid;
+    const bool own = e < Kc;
+    const double dlb = a.lb, dub = a.ub, dap = a.a_plus, dam = a.a_minus;
+    float *wp = weight + (int64_t)f * Kc + e;
+    float wf = own ? *wp : 0.0f;
+    const uint32_t *brow = w.bits + (int64_t)w.woff[f] * Kc + e;
+    for (int c0 = 0; c0 < n; c0 += 1024) {
+        for (int i = tid; i < min(1024, n - c0); i += 256) sgn[i] = w.lsign[(int64_t)f * a.B + c0 + i];
+        __syncthreads();
+        const int words = (min(1024, n - c0) + 31) / 32;
+        uint32_t nxt = own ? brow[(int64_t)(c0 / 32) * Kc] : 0u;
+        for (int wi = 0; wi < words; ++wi) {
+            const uint32_t word = nxt;
+            if (own && wi + 1 < words) nxt = brow[(int64_t)(c0 / 32 + wi + 1) * Kc];
+            const int cnt = min(32, n - c0 - 32 * wi);
+            for (int q = 0; q < cnt; ++q) {
+                const double r = (double)sgn[32 * wi + q] * (((word >> q) & 1u) ? dap : dam);
+                const double x = (double)wf;
+                const double d = a.stabilizer ? (x - dlb) * (dub - x) : 1.0;
+                const double du = r * d;
+                double nw = x + du;
+                if (nw < dlb) nw = dlb;
+                if (nw > dub) nw = dub;
+                wf = (float)nw;
+            }
+        }
+        __syncthreads();  // sgn is rewritten by the next pass
+    }
+    if (own) *wp = wf;
 }
 
 __global__ __launch_bounds__(256) void k_decide(const int32_t *__restrict__ winners, const int32_t *__restrict__ n_win,
@@ -151,40 +222,60 @@ __global__ __launch_bounds__(256) void k_decide(const int32_t *__restrict__ winn
 
 int stdp_common(float *weight, int Cout, int Cin, int K, int pad, const uint8_t *pre_wave, int B, int T, int H,
                 int W, const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward, float a_plus,
-                float a_minus, float lb, float ub, int stabilizer, void *stream, const char *name) {
+                float a_minus, float lb, float ub, int stabilizer, void *workspace, size_t ws_bytes, void *stream,
+                const char *name) {
     SPK_REQUIRE(Cout >= 1 && Cin >= 1 && K >= 1 && pad >= 0 && B >= 0 && T >= 1 && H >= 1 && W >= 1 && k >= 1,
                 SPK_E_SHAPE, "%s: bad sizes", name);
     SPK_REQUIRE(T <= 255, SPK_E_RANGE, "%s: T=%d > 255", name, T);
-    SPK_REQUIRE((int64_t)Cin * K * K < (1LL << 31), SPK_E_RANGE, "%s: kernel too large", name);
+    SPK_REQUIRE(Cout <= 65535 && (int64_t)Cout * B < (1LL << 31), SPK_E_RANGE, "%s: Cout*B too large", name);
+    SPK_REQUIRE((int64_t)Cin * K * K <= 65535LL * 256 && bit_rows(Cout, B, k) <= 65535 &&
+                    bit_rows(Cout, B, k) * Cin * K * K < (1LL << 31),
+                SPK_E_RANGE, "%s: kernel or batch too large", name);
     SPK_REQUIRE(std::isfinite(a_plus) && std::isfinite(a_minus) && std::isfinite(lb) && std::isfinite(ub) && lb <= ub,
                 SPK_E_ARG, "%s: rates and bounds must be finite with lb <= ub", name);
     SPK_REQUIRE(stabilizer == 0 || stabilizer == 1, SPK_E_ARG, "%s: stabilizer must be 0 or 1", name);
     if (B == 0) return spk::ok();
     SPK_REQUIRE(weight && pre_wave && winners && n_winners, SPK_E_ARG,
                 "%s: weight, pre_wave, winners and n_winners are required", name);
+    size_t need = 0;
+    carve(nullptr, Cout, Cin, K, B, k, &need);
+    SPK_REQUIRE(workspace && ws_bytes >= need, SPK_E_WORKSPACE, "%s: workspace of %zu bytes < %zu required", name,
+                ws_bytes, need);
+    StdpWork wk = carve(workspace, Cout, Cin, K, B, k, nullptr);
     StdpArgs a{Cout, Cin, K, pad, B, T, H, W, k, stabilizer, a_plus, a_minus, lb, ub};
-    const int64_t chunks = spk::ceil_div((int64_t)Cin * K * K, 256);
-    SPK_REQUIRE(chunks <= 65535, SPK_E_RANGE, "%s: kernel too large", name);
-    hipLaunchKernelGGL(k_stdp, dim3(Cout, (unsigned)chunks), dim3(256), 0, spk::as_stream(stream), weight, pre_wave,
-                       winners, n_winners, reward, a);
+    hipStream_t st = spk::as_stream(stream);
+    const unsigned wchunks = (unsigned)spk::ceil_div((int64_t)Cin * K * K, 256);
+    hipLaunchKernelGGL(k_stdp_list, dim3(Cout), dim3(LIST_THREADS), 0, st, winners, n_winners, reward, a, wk);
+    hipLaunchKernelGGL(k_stdp_offsets, dim3(1), dim3(1024), 0, st, Cout, wk);
+    hipLaunchKernelGGL(k_stdp_bits, dim3(wchunks, (unsigned)wk.rows), dim3(256), 0, st, pre_wave, a, wk);
+    hipLaunchKernelGGL(k_stdp_apply, dim3(wchunks, Cout), dim3(256), 0, st, weight, a, wk);
     return spk::check_launch(name);
 }
 
 }  // namespace
 
+extern "C" size_t spk_stdp_workspace_size(int Cout, int Cin, int K, int B, int k) {
+    if (Cout < 1 || Cin < 1 || K < 1 || B < 0 || k < 1) return 0;
+    size_t need = 0;
+    carve(nullptr, Cout, Cin, K, B, k, &need);
+    return need;
+}
+
 extern "C" int spk_stdp(float *weight, int Cout, int Cin, int K, int pad, const uint8_t *pre_wave, int B, int T,
                         int H, int W, const int32_t *winners, const int32_t *n_winners, int k, float a_plus,
-                        float a_minus, float lb, float ub, int stabilizer, void *stream) {
+                        float a_minus, float lb, float ub, int stabilizer, void *workspace, size_t ws_bytes,
+                        void *stream) {
     return stdp_common(weight, Cout, Cin, K, pad, pre_wave, B, T, H, W, winners, n_winners, k, nullptr, a_plus,
-                       a_minus, lb, ub, stabilizer, stream, "spk_stdp");
+                       a_minus, lb, ub, stabilizer, workspace, ws_bytes, stream, "spk_stdp");
 }
 
 extern "C" int spk_rstdp(float *weight, int Cout, int Cin, int K, int pad, const uint8_t *pre_wave, int B, int T,
                          int H, int W, const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward,
-                         float a_plus, float a_minus, float lb, float ub, int stabilizer, void *stream) {
+                         float a_plus, float a_minus, float lb, float ub, int stabilizer, void *workspace,
+                         size_t ws_bytes, void *stream) {
     SPK_REQUIRE(reward || B == 0, SPK_E_ARG, "spk_rstdp: reward is required");
     return stdp_common(weight, Cout, Cin, K, pad, pre_wave, B, T, H, W, winners, n_winners, k, reward, a_plus,
-                       a_minus, lb, ub, stabilizer, stream, "spk_rstdp");
+                       a_minus, lb, ub, stabilizer, workspace, ws_bytes, stream, "spk_rstdp");
 }
 
 extern "C" int spk_decide(const int32_t *winners, const int32_t *n_winners, int B, int k, const int32_t *labels,

@@ -31,7 +31,7 @@ import torch
 
 from . import (pool_out_size, conv_out_size, spk_conv_fire, spk_conv_fire_workspace_size, spk_decide,
                spk_encode_latency, spk_encode_latency_workspace_size, spk_kwta, spk_kwta_workspace_size,
-               spk_pool, spk_pool_first_spike, spk_rstdp, spk_stdp)
+               spk_pool, spk_pool_first_spike, spk_rstdp, spk_stdp, spk_stdp_workspace_size)
 
 
 def _is_conv(st):
@@ -74,6 +74,9 @@ class Chain:
                 b["win"] = torch.empty((B, st.k, 4), dtype=i32, device=dev)
                 b["nw"] = torch.empty((B,), dtype=i32, device=dev)
                 b["weight"] = torch.empty((st.cout, st.cin, st.K, st.K), dtype=f32, device=dev)
+                # each learning layer has its own plasticity workspace (the layers update concurrently)
+                b["ws_learn"] = (torch.empty(max(256, spk_stdp_workspace_size(st.cout, st.cin, st.K, B, st.k)),
+                                             dtype=u8, device=dev) if st.learn is not None else None)
                 ws_bytes = max(ws_bytes, spk_conv_fire_workspace_size(B, T, st.cin, h, w, st.cout, st.K, st.pad),
                                spk_kwta_workspace_size(B, st.cout, ho, wo))
                 c, h, w = st.cout, ho, wo
@@ -176,10 +179,10 @@ class Chain:
                 mark(f"stdp{i}", 0)
             if st.learn == "rstdp":
                 spk_rstdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], self.reward, st.a_plus,
-                          st.a_minus, st.lb, st.ub, st.stabilizer, stream=s)
+                          st.a_minus, st.lb, st.ub, st.stabilizer, workspace=b["ws_learn"], stream=s)
             else:
                 spk_stdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], st.a_plus, st.a_minus, st.lb,
-                         st.ub, st.stabilizer, stream=s)
+                         st.ub, st.stabilizer, workspace=b["ws_learn"], stream=s)
             if self.concurrent_learn:
                 self._joins[j].record(s)
                 main.wait_event(self._joins[j])

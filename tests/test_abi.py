@@ -21,7 +21,7 @@ def declared():
 
 def test_every_declared_symbol_is_exported():
     names = declared()
-    assert len(names) == 16
+    assert len(names) == 17
     lib = spk.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -79,12 +79,16 @@ def test_other_validation_errors():
     assert lib.spk_kwta(DUMMY, DUMMY, 1, 15, 1, 4, 4, 0, 1, DUMMY, DUMMY, DUMMY, 1 << 20, None) == spk.SPK_E_ARG
     assert lib.spk_kwta(DUMMY, DUMMY, 1, 15, 1, 512, 512, 1, 1, DUMMY, DUMMY, DUMMY, 1 << 20, None) == spk.SPK_E_RANGE
     assert lib.spk_kwta(DUMMY, DUMMY, 2, 15, 1, 4, 4, 1, 1, DUMMY, DUMMY, DUMMY, 8, None) == spk.SPK_E_WORKSPACE
+    ws = spk.spk_stdp_workspace_size(4, 2, 3, 1, 1)
+    assert ws > 0
     assert lib.spk_stdp(DUMMY, 4, 2, 3, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, 0.004, -0.003, 0.9, 0.1, 1,
-                        None) == spk.SPK_E_ARG  # lb > ub
+                        DUMMY, ws, None) == spk.SPK_E_ARG  # lb > ub
     assert lib.spk_stdp(DUMMY, 4, 2, 3, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, float("inf"), -0.003, 0.0, 1.0, 1,
-                        None) == spk.SPK_E_ARG
+                        DUMMY, ws, None) == spk.SPK_E_ARG
+    assert lib.spk_stdp(DUMMY, 4, 2, 3, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, 0.004, -0.003, 0.0, 1.0, 1,
+                        DUMMY, ws - 1, None) == spk.SPK_E_WORKSPACE
     assert lib.spk_rstdp(DUMMY, 4, 2, 3, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, None, 0.004, -0.003, 0.0, 1.0, 1,
-                         None) == spk.SPK_E_ARG
+                         DUMMY, ws, None) == spk.SPK_E_ARG
     assert lib.spk_encode_latency(DUMMY, 1, 28, 28, DUMMY, 6, 12, 0.0, 15, DUMMY, DUMMY, None, DUMMY, 1 << 30,
                                   None) == spk.SPK_E_RANGE  # even filter size
     assert lib.spk_encode_latency(DUMMY, 1, 28, 28, DUMMY, 6, 13, 0.0, 15, DUMMY, DUMMY, None, DUMMY, 4,
