@@ -16,6 +16,11 @@
 //   3. k_expand_latency: every entry counts the boundaries its key does not
 //      exceed -- that count is its bin floor(rho*T/n) -- and writes t_first
 //      and the T planes of the wave (4 entries per thread, u32 stores).
+// When C*H*W <= SORT_MAX, steps 2 and 3 are one kernel instead,
+// k_rank_sort: one workgroup per image gathers the keys of the positive
+// intensities into LDS, sorts them (bitonic network over the next power of two
+// of their count), gives the entry at rank rho the bin floor(rho*T/n) in an
+// LDS map of t_first, and writes t_first and the wave from that map.
 #include <algorithm>
 
 #include "common.hpp"
@@ -27,6 +32,8 @@ constexpr int MAX_KF = 31;
 constexpr int SEL_THREADS = 1024;
 constexpr int MAX_GROUPS = 32;   // bin boundaries resolved per select batch
 constexpr int LDS_KEYS = 12288;  // intensities cached in LDS when N fits
+constexpr int SORT_MAX = 8192;   // entries per image sorted in LDS
+constexpr int SORT_THREADS = 1024;
 
 // ------------------------------------------------------------------ filter
 // LDS holds the taps and the zero-padded band of the image as doubles, so the
@@ -268,6 +275,80 @@ __global__ __launch_bounds__(256) void k_expand_latency(const float *__restrict_
     }
 }
 
+// ------------------------------------------------------------------ rank by sorting (small images)
+__global__ __launch_bounds__(SORT_THREADS) void k_rank_sort(const float *__restrict__ inten, int N, int T,
+                                                            uint8_t *__restrict__ tf_out, uint8_t *__restrict__ wave) {
+    __shared__ uint64_t key[SORT_MAX];
+    __shared__ uint8_t tmap[SORT_MAX];
+    __shared__ int npos;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const float *I = inten + (int64_t)b * N;
+    if (tid == 0) npos = 0;
+    for (int i = tid; i < N; i += SORT_THREADS) tmap[i] = (uint8_t)T;
+    __syncthreads();
+    // gather the positive entries' keys (their order in LDS does not matter: keys are unique)
+    for (int i0 = 0; i0 < N; i0 += SORT_THREADS) {
+        const int i = i0 + tid;
+        const float v = i < N ? I[i] : 0.0f;
+        const bool pos = v > 0.0f;
+        const uint64_t m = __ballot(pos);
+        int base = 0;
+        if ((tid & 63) == 0 && m) base = atomicAdd(&npos, __popcll(m));
+        base = __shfl(base, 0, 64);
+        if (pos) key[base + __popcll(m & ((1ull << (tid & 63)) - 1ull))] = make_key(v, (uint32_t)i);
+    }
+    __syncthreads();
+    const int n = npos;
+    int m = 1;
+    while (m < n) m <<= 1;
+    for (int i = n + tid; i < m; i += SORT_THREADS) key[i] = 0;  // below every positive key
+    __syncthreads();
+    // bitonic network, descending overall
+    for (int k = 2; k <= m; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = tid; i < m / 2; i += SORT_THREADS) {
+                const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1)), hi = lo + j;
+                const uint64_t x = key[lo], y = key[hi];
+                const bool desc = (lo & k) == 0;
+                if ((x < y) == desc) {
+                    key[lo] = y;
+                    key[hi] = x;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int p = tid; p < n; p += SORT_THREADS)
+        tmap[0xFFFFFFFFu - (uint32_t)key[p]] = (uint8_t)(((int64_t)p * T) / n);
+    __syncthreads();
+    uint8_t *tf = tf_out ? tf_out + (int64_t)b * N : nullptr;
+    uint8_t *wv = wave ? wave + (int64_t)b * T * N : nullptr;
+    if ((N & 3) == 0) {
+        const int nq = N / 4;
+        for (int q = tid; q < nq; q += SORT_THREADS) {
+            const uint32_t t4 = *reinterpret_cast<const uint32_t *>(tmap + 4 * q);
+            if (tf) *reinterpret_cast<uint32_t *>(tf + 4 * q) = t4;
+        }
+        if (wv)
+            for (int e = tid; e < T * nq; e += SORT_THREADS) {
+                const int t = e / nq, q = e - t * nq;
+                const uint32_t t4 = *reinterpret_cast<const uint32_t *>(tmap + 4 * q);
+                uint32_t w = 0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) w |= (uint32_t)(t >= (int)((t4 >> (8 * j)) & 255u)) << (8 * j);
+                *reinterpret_cast<uint32_t *>(wv + (int64_t)t * N + 4 * q) = w;
+            }
+    } else {
+        for (int i = tid; i < N; i += SORT_THREADS)
+            if (tf) tf[i] = tmap[i];
+        if (wv)
+            for (int e = tid; e < T * N; e += SORT_THREADS) {
+                const int t = e / N, i = e - t * N;
+                wv[(int64_t)t * N + i] = (uint8_t)(t >= (int)tmap[i]);
+            }
+    }
+}
+
 // ------------------------------------------------------------------ Eq.1 utilities
 __global__ __launch_bounds__(256) void k_expand_wave(const uint8_t *__restrict__ tf, int64_t N, int T,
                                                      uint8_t *__restrict__ wave, int64_t total_groups,
@@ -371,6 +452,10 @@ extern "C" int spk_encode_latency(const uint8_t *image, int B, int H, int W, con
     hipLaunchKernelGGL(k_filter, dim3((unsigned)(B * nb)), dim3(256), lds, st, image, B, H, W, filters, C, KF,
                        filter_threshold, I);
     if (!t_first && !wave) return spk::check_launch("spk_encode_latency");
+    if (p.N <= SORT_MAX) {
+        hipLaunchKernelGGL(k_rank_sort, dim3(B), dim3(SORT_THREADS), 0, st, I, (int)p.N, T, t_first, wave);
+        return spk::check_launch("spk_encode_latency");
+    }
     if (T > 1)
         hipLaunchKernelGGL(k_rank_select, dim3(B), dim3(SEL_THREADS), 0, st, I, p.N, T, bounds, count);
     const int64_t groups = (p.N + 3) / 4;

@@ -38,11 +38,12 @@ struct StdpArgs {
 //   list  [Cout][B] int4   the feature's updates in image order: (image, t, y, x)
 //   lsign [Cout][B] i8     +1 / -1 (STDP / anti-STDP)
 //   bits  [rows][Kc] u32   bit q of row woff[f]+i, column e: pre-synaptic bit of update 32i+q on weight e
+//   sbits [rows] u32       bit q of row woff[f]+i: update 32i+q is an anti-STDP one (negated rates)
 struct StdpWork {
     int *count, *woff;
     int4 *list;
     int8_t *lsign;
-    uint32_t *bits;
+    uint32_t *bits, *sbits;
     int64_t rows;  // capacity of bits in rows of Kc words
 };
 
@@ -57,6 +58,7 @@ StdpWork carve(void *ws, int Cout, int Cin, int K, int B, int k, size_t *bytes) 
     w.lsign = c.take<int8_t>((size_t)Cout * B);
     w.rows = bit_rows(Cout, B, k);
     w.bits = c.take<uint32_t>((size_t)w.rows * Cin * K * K);
+    w.sbits = c.take<uint32_t>((size_t)w.rows);
     if (bytes) *bytes = spk::align_up(c.off, 256);
     return w;
 }
@@ -140,6 +142,11 @@ __global__ __launch_bounds__(256) void k_stdp_bits(const uint8_t *__restrict__ p
         else hi = mid - 1;
     }
     const int f = lo, u0 = (r - w.woff[f]) * 32, cnt = min(32, w.count[f] - u0);
+    if (blockIdx.x == 0 && threadIdx.x < 64) {  // the row's sign word
+        const bool neg = (int)threadIdx.x < cnt && w.lsign[(int64_t)f * a.B + u0 + threadIdx.x] < 0;
+        const uint64_t m = __ballot(neg);
+        if (threadIdx.x == 0) w.sbits[r] = (uint32_t)m;
+    }
     const int KK = a.K * a.K, Kc = a.Cin * KK;
     const int e = blockIdx.x * 256 + threadIdx.x;
     if (e >= Kc) return;
@@ -165,42 +172,61 @@ __global__ __launch_bounds__(256) void k_stdp_bits(const uint8_t *__restrict__ p
 
 // 4. Grid (chunk of 256 weights, feature): each thread replays its weight's
 // chain of updates in image order, 32 per bit word (the next word is loaded
-// while the current one is replayed); the signs of 1024 updates at a time sit
-// in LDS.
+// while the current one is replayed).  The rates of a word's updates come from
+// its pre-synaptic and sign bits, off the dependency chain, which is then
+//     x = w; d = (x-lb)*(ub-x); u = r*d; w = clamp(x+u); w = float(w)
+// With FAST (stabilizer on and max|rate| * (ub-lb) <= 1/2, checked by the
+// host) the clamp is applied to the first update of the chain only: from then
+// on lb <= x <= ub, so u >= 0 stays below 0.51*(ub-x) and u < 0 above
+// -0.51*(x-lb) even after the roundings of d and u, and x+u rounds into
+// [lb, ub] without it.  Clamping in double and then rounding, or rounding
+// first, give the same float, since lb and ub are floats.
+template <bool FAST>
+__device__ __forceinline__ float stdp_one(float wf, double r, double dlb, double dub, bool stab, bool clamp) {
+#pragma clang fp contract(off)
+    const double x = (double)wf;
+    const double d = stab ? (x - dlb) * (dub - x) : 1.0;
+    const double du = r * d;
+    double nw = x + du;
+    if (!FAST || clamp) {
+        nw = nw < dlb ? dlb : nw;
+        nw = nw > dub ? dub : nw;
+    }
+    return (float)nw;
+}
+
+template <bool FAST>
 __global__ __launch_bounds__(256) void k_stdp_apply(float *__restrict__ weight, StdpArgs a, StdpWork w) {
 #pragma clang fp contract(off)
-    __shared__ int8_t sgn[1024];
     const int f = blockIdx.y, tid = threadIdx.x;
     const int n = w.count[f];
     if (n == 0) return;  // uniform
     const int KK = a.K * a.K, Kc = a.Cin * KK;
     const int e = blockIdx.x * 256 + tid;
     const bool own = e < Kc;
+    const bool stab = FAST || a.stabilizer;
     const double dlb = a.lb, dub = a.ub, dap = a.a_plus, dam = a.a_minus;
     float *wp = weight + (int64_t)f * Kc + e;
     float wf = own ? *wp : 0.0f;
-    const uint32_t *brow = w.bits + (int64_t)w.woff[f] * Kc + e;
-    for (int c0 = 0; c0 < n; c0 += 1024) {
-        for (int i = tid; i < min(1024, n - c0); i += 256) sgn[i] = w.lsign[(int64_t)f * a.B + c0 + i];
-        __syncthreads();
-        const int words = (min(1024, n - c0) + 31) / 32;
-        uint32_t nxt = own ? brow[(int64_t)(c0 / 32) * Kc] : 0u;
-        for (int wi = 0; wi < words; ++wi) {
-            const uint32_t word = nxt;
-            if (own && wi + 1 < words) nxt = brow[(int64_t)(c0 / 32 + wi + 1) * Kc];
-            const int cnt = min(32, n - c0 - 32 * wi);
-            for (int q = 0; q < cnt; ++q) {
-                const double r = (double)sgn[32 * wi + q] * (((word >> q) & 1u) ? dap : dam);
-                const double x = (double)wf;
-                const double d = a.stabilizer ? (x - dlb) * (dub - x) : 1.0;
-                const double du = r * d;
-                double nw = x + du;
-                if (nw < dlb) nw = dlb;
-                if (nw > dub) nw = dub;
-                wf = (float)nw;
-            }
+    const int row0 = w.woff[f];
+    const uint32_t *brow = w.bits + (int64_t)row0 * Kc + e;
+    const int words = (n + 31) / 32;
+    uint32_t nxt = own ? brow[0] : 0u;
+    for (int wi = 0; wi < words; ++wi) {
+        const uint32_t word = nxt, sw = w.sbits[row0 + wi];
+        if (own && wi + 1 < words) nxt = brow[(int64_t)(wi + 1) * Kc];
+        const int cnt = min(32, n - 32 * wi);
+        if (FAST && wi == 0) {  // the clamped first update
+            const double r0 = (word & 1u) ? dap : dam;
+            wf = stdp_one<FAST>(wf, (sw & 1u) ? -r0 : r0, dlb, dub, stab, true);
         }
-        __syncthreads();  // sgn is rewritten by the next pass
+#pragma unroll
+        for (int q = 0; q < 32; ++q) {
+            if (FAST && q == 0 && wi == 0) continue;
+            if (q >= cnt) break;  // uniform
+            const double rq = ((word >> q) & 1u) ? dap : dam;
+            wf = stdp_one<FAST>(wf, ((sw >> q) & 1u) ? -rq : rq, dlb, dub, stab, false);
+        }
     }
     if (own) *wp = wf;
 }
@@ -248,7 +274,12 @@ int stdp_common(float *weight, int Cout, int Cin, int K, int pad, const uint8_t 
     hipLaunchKernelGGL(k_stdp_list, dim3(Cout), dim3(LIST_THREADS), 0, st, winners, n_winners, reward, a, wk);
     hipLaunchKernelGGL(k_stdp_offsets, dim3(1), dim3(1024), 0, st, Cout, wk);
     hipLaunchKernelGGL(k_stdp_bits, dim3(wchunks, (unsigned)wk.rows), dim3(256), 0, st, pre_wave, a, wk);
-    hipLaunchKernelGGL(k_stdp_apply, dim3(wchunks, Cout), dim3(256), 0, st, weight, a, wk);
+    // the clamp can be dropped after the first update (see k_stdp_apply)
+    const double rmax = std::max(std::fabs((double)a_plus), std::fabs((double)a_minus));
+    if (stabilizer && rmax * ((double)ub - (double)lb) <= 0.5)
+        hipLaunchKernelGGL(k_stdp_apply<true>, dim3(wchunks, Cout), dim3(256), 0, st, weight, a, wk);
+    else
+        hipLaunchKernelGGL(k_stdp_apply<false>, dim3(wchunks, Cout), dim3(256), 0, st, weight, a, wk);
     return spk::check_launch(name);
 }
 

@@ -252,7 +252,8 @@ def test_encode_toy_t4(golden):
 
 
 ENC_CASES = [("dog", 3, 28, 28, 15, 0.0), ("gabor", 2, 160, 250, 30, 0.0), ("dog", 2, 28, 28, 1, 0.0),
-             ("dog", 2, 28, 28, 64, 0.0), ("dog", 1, 28, 28, 255, 0.0), ("rand", 2, 19, 23, 15, 3.0)]
+             ("dog", 2, 28, 28, 64, 0.0), ("dog", 1, 28, 28, 255, 0.0), ("rand", 2, 19, 23, 15, 3.0),
+             ("pos", 2, 40, 50, 15, 0.0), ("pos", 1, 41, 50, 15, 0.0), ("pos", 3, 1, 1, 15, 0.0)]
 
 
 @pytest.mark.parametrize("case", ENC_CASES)
@@ -263,6 +264,9 @@ def test_encode_parity(case):
         img, bank = synth.stroke_images(g, B, H, W), synth.dog_bank()
     elif kind == "gabor":
         img, bank = synth.pink_noise_images(g, B, H, W), synth.gabor_bank()
+    elif kind == "pos":  # 4 positive filters on a noise image: every entry is ranked
+        img = g.integers(1, 256, (B, H, W)).astype(np.uint8)
+        bank = (g.integers(1, 65, (4, 3, 3)) / 64.0).astype(np.float32)
     else:
         img = g.integers(0, 256, (B, H, W)).astype(np.uint8)
         bank = (g.integers(-64, 65, (5, 7, 7)) / 64.0).astype(np.float32)
@@ -335,6 +339,22 @@ def test_rstdp_and_bounds_variant():
     sync()
     ref = orc.stdp(Wt, wave, 2, win, nw, 0.05, -0.04, 0.2, 0.8, stabilizer=False, reward=reward)
     assert_equal(host(Wg), ref, "R-STDP clamp")
+
+
+@pytest.mark.parametrize("rates", [(0.004, -0.003), (0.7, -0.6)])
+def test_stdp_weights_outside_bounds(rates):
+    # the first update of a chain starts from a weight outside [lb, ub]; with small
+    # rates the later updates skip the clamp, with large ones they keep it
+    wave, Wt, win, nw = layer_case(*STDP_CASES[0])
+    Wt = Wt.copy()
+    g = synth.rng(650, 0)
+    flat = Wt.reshape(-1)
+    idx = g.choice(flat.size, flat.size // 4, replace=False)
+    flat[idx] = g.choice(np.array([-0.25, 1.5, 0.0, 1.0, -0.0], np.float32), idx.size)
+    Wg = dev(Wt)
+    spk.spk_stdp(Wg, 2, dev(wave), dev(win), dev(nw), *rates)
+    sync()
+    assert_equal(host(Wg), orc.stdp(Wt, wave, 2, win, nw, *rates), "weights")
 
 
 def test_stdp_ordered_replay_many_images():
