@@ -30,6 +30,7 @@
 //      k_conv_fire_inf, which computes only the last step.
 #include <algorithm>
 #include <cmath>
+#include <numeric>
 
 #include "common.hpp"
 
@@ -251,7 +252,7 @@ constexpr int FIN_AW = 16384 / 4 / (FIN_CW * 64);  // words of the staged spike 
 template <int G, bool BLDS, bool ALDS>
 __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
-    const int2 *__restrict__ koff2, ConvGeom g, int n_pairs, int n_chunks, int chunk_tiles, int np_max,
+    const int2 *__restrict__ koff2, ConvGeom g, int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max,
     int a_words, const float *__restrict__ inv_scale, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
     float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
@@ -266,22 +267,38 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 
     const int x = blockIdx.x % 8, j = blockIdx.x / 8;
     const int pair = j % n_pairs, r = j / n_pairs, R = (int)(gridDim.x / 8) / n_pairs;
-    const int ntask = g.B * n_chunks;
+    const int ntask = n_chunks;
     const int per_x = (ntask + 7) / 8;
     const int t_lo = x * per_x, t_hi = min(ntask, t_lo + per_x);
     const int f0 = pair * 32;
     const int nf = min(32, g.Cout - f0);
+    const int npos = g.B * g.HoWo;  // flattened (image, position) index space
 
-    // The padded first-spike rows a task reads: rows y_first .. y_last+K-1 of
-    // its image, one contiguous range of tpad (a multiple of 4 bytes).
-    auto region = [&](int task, int &yf, int &w0, int &nw) {
-        const int b = task / n_chunks, ch = task % n_chunks;
-        const int p0 = ch * chunk_tiles * 16;
-        const int np = min(chunk_tiles * 16, g.HoWo - p0);
-        yf = p0 / g.Wo;
-        const int rows = (p0 + np - 1) / g.Wo + g.K - yf;
-        w0 = (int)((((int64_t)b * g.Hp + yf) * row_bytes) >> 2);
-        nw = rows * row_bytes / 4;
+    // A task is the flattened positions [p0, p0 + np): with cpi > 0, chunk
+    // task % cpi of image task / cpi; with cpi == 0, chunk `task` of the
+    // flattened space, which may span two images.
+    auto task_range = [&](int task, int &p0, int &np) {
+        if (cpi > 0) {
+            const int b = task / cpi, q0 = (task - b * cpi) * chunk_tiles * 16;
+            p0 = b * g.HoWo + q0;
+            np = min(chunk_tiles * 16, g.HoWo - q0);
+        } else {
+            p0 = task * chunk_tiles * 16;
+            np = min(chunk_tiles * 16, npos - p0);
+        }
+    };
+    // The padded first-spike rows it reads: from row y_first of its first image
+    // to row y_last+K-1 of its last one, one contiguous range of tpad (rows of
+    // consecutive images follow each other; a multiple of 4 bytes).
+    auto region = [&](int task, int &row0, int &w0, int &nw) {
+        int p0, np;
+        task_range(task, p0, np);
+        const int pa = p0, pb = p0 + np - 1;
+        const int ba = pa / g.HoWo, bb = pb / g.HoWo;
+        row0 = ba * g.Hp + (pa - ba * g.HoWo) / g.Wo;
+        const int row1 = bb * g.Hp + (pb - bb * g.HoWo) / g.Wo + g.K - 1;
+        w0 = (int)(((int64_t)row0 * row_bytes) >> 2);
+        nw = (row1 - row0 + 1) * row_bytes / 4;
     };
     auto fetch_region = [&](int task, uint32_t (&v)[FIN_AW]) {
         int yf, w0, nw;
@@ -327,22 +344,21 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         const half8 *gl = wlo + (int64_t)(pair * 2) * g.ksteps * 64 + lane;
         int abuf_sel = 0;
         for (int task = t_lo + r; task < t_hi; task += R) {
-            const int b = task / n_chunks, ch = task % n_chunks;
-            const int tile0 = ch * chunk_tiles;
-            const int ntl = min(chunk_tiles, g.mt_per_img - tile0);
-            const int pos0 = tile0 * 16;
-            const int np = min(ntl * 16, g.HoWo - pos0);
+            int pos0, np;
+            task_range(task, pos0, np);
             const uint8_t *abase[FIN_MT];
             uint32_t alds[FIN_MT];
-            int yf_t, w0_t, nw_t;
-            region(task, yf_t, w0_t, nw_t);
+            int row0_t, w0_t, nw_t;
+            region(task, row0_t, w0_t, nw_t);
             const uint8_t *abuf_t = reinterpret_cast<const uint8_t *>(abuf + abuf_sel * a_words);
 #pragma unroll
             for (int i = 0; i < FIN_MT; ++i) {
-                const int pos = min(pos0 + (wv + FIN_CW * i) * 16 + c, pos0 + np - 1);
+                const int gp = min(pos0 + (wv + FIN_CW * i) * 16 + c, pos0 + np - 1);
+                const int b = gp / g.HoWo, pos = gp - b * g.HoWo;
                 const int y = pos / g.Wo, xx = pos - y * g.Wo;
-                abase[i] = tpad + (uint32_t)((((int64_t)b * g.Hp + y) * g.Wp + xx) * g.CP);
-                alds[i] = (uint32_t)((y - yf_t) * row_bytes + xx * g.CP);
+                const int row = b * g.Hp + y;
+                abase[i] = tpad + (uint32_t)(((int64_t)row * g.Wp + xx) * g.CP);
+                alds[i] = (uint32_t)((row - row0_t) * row_bytes + xx * g.CP);
             }
             const bool has_next = ALDS && task + R < t_hi;
             uint32_t nxt[FIN_AW];
@@ -420,22 +436,20 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 load_a(a1, o2);
                 load_b(b1, min(1, g.ksteps - 1));
                 o2 = koff_at(2);
-                for (int ks = 0; ks < g.ksteps; ks += 2) {
+                // pairs of K-steps without branches (the loads past the last K-step
+                // re-read it), so the LDS waits count exactly; an odd last one after
+                int ks = 0;
+                for (; ks + 1 < g.ksteps; ks += 2) {
                     kstep(a0, b0);
                     const int2 o3 = koff_at(ks + 3);
-                    if (ks + 2 < g.ksteps) {
-                        load_a(a0, o2);
-                        load_b(b0, ks + 2);
-                    }
-                    if (ks + 1 < g.ksteps) {
-                        kstep(a1, b1);
-                        o2 = koff_at(ks + 4);
-                        if (ks + 3 < g.ksteps) {
-                            load_a(a1, o3);
-                            load_b(b1, ks + 3);
-                        }
-                    }
+                    load_a(a0, o2);
+                    load_b(b0, min(ks + 2, g.ksteps - 1));
+                    kstep(a1, b1);
+                    o2 = koff_at(ks + 4);
+                    load_a(a1, o3);
+                    load_b(b1, min(ks + 3, g.ksteps - 1));
                 }
+                if (ks < g.ksteps) kstep(a0, b0);
                 __syncthreads();  // staging free: the store waves are done with the previous block
 #pragma unroll
                 for (int t = 0; t < FIN_TB; ++t) {
@@ -467,21 +481,22 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         // ------------------------------------------------ store waves
         const int s = tid - FIN_CW * 64;
         for (int task = t_lo + r; task < t_hi; task += R) {
-            const int b = task / n_chunks, ch = task % n_chunks;
-            const int tile0 = ch * chunk_tiles;
-            const int ntl = min(chunk_tiles, g.mt_per_img - tile0);
-            const int pos0 = tile0 * 16;
-            const int np = min(ntl * 16, g.HoWo - pos0);
+            int pos0, np;
+            task_range(task, pos0, np);
             const int nel = nf * np;  // staged elements of the task
             constexpr int NSLOT = 32 * chunk_tiles_max(G) * 16 / (FIN_SW * 64) / G;  // staged groups per thread
-            // per slot: its output offset within a step's plane (feature row fl, position pl), or -1;
-            // slots past the task read element 0 and are never stored
+            // per slot: the output element (feature f0+fl of flattened position pos0+pl) at step 0
+            // relative to (image b0, feature f0), or -1; slots past the task read element 0 and are
+            // never stored.  A group of G never straddles two images (G = 4 needs HoWo % 4 == 0).
+            const int b0 = pos0 / g.HoWo;
+            const int64_t base0 = (int64_t)b0 * g.T * tplane + (int64_t)f0 * g.HoWo;
             int off[NSLOT], src[NSLOT];
 #pragma unroll
             for (int m = 0; m < NSLOT; ++m) {
                 const int e = (s + FIN_SW * 64 * m) * G;  // first staged element of the slot
                 const int fl = e / np, pl = e - fl * np;
-                off[m] = e < nel ? fl * g.HoWo + pl : -1;
+                const int gp = pos0 + pl, b = gp / g.HoWo, pos = gp - b * g.HoWo;
+                off[m] = e < nel ? (b - b0) * g.T * (int)tplane + fl * g.HoWo + pos : -1;
                 src[m] = e < nel ? e : 0;
             }
             int tfirst[NSLOT][G];
@@ -499,8 +514,8 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 for (int t = 0; t < FIN_TB && tb0 + t < g.T; ++t) {
                     const int tt = tb0 + t;
                     const float *st = stage + t * stage_t;
-                    float *Pt = P ? P + ((int64_t)b * g.T + tt) * tplane + (int64_t)f0 * g.HoWo + pos0 : nullptr;
-                    uint8_t *St = S ? S + ((int64_t)b * g.T + tt) * tplane + (int64_t)f0 * g.HoWo + pos0 : nullptr;
+                    float *Pt = P ? P + base0 + (int64_t)tt * tplane : nullptr;
+                    uint8_t *St = S ? S + base0 + (int64_t)tt * tplane : nullptr;
 #pragma unroll
                     for (int m = 0; m < NSLOT; ++m) {
                         if (off[m] < 0) continue;
@@ -533,12 +548,15 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 }
             }
             // first-spike time and the potential there
-            uint8_t *TFt = TF + ((int64_t)b * g.Cout + f0) * g.HoWo + pos0;
-            float *VFt = VF + ((int64_t)b * g.Cout + f0) * g.HoWo + pos0;
 #pragma unroll
             for (int m = 0; m < NSLOT; ++m) {
                 if (off[m] < 0) continue;
-                const uint32_t o = (uint32_t)off[m];
+                const int e = (s + FIN_SW * 64 * m) * G;
+                const int fl = e / np, pl = e - fl * np;
+                const int gp = pos0 + pl, b = gp / g.HoWo, pos = gp - b * g.HoWo;
+                const int64_t o = ((int64_t)b * g.Cout + f0 + fl) * g.HoWo + pos;
+                uint8_t *TFt = TF;
+                float *VFt = VF;
                 if (G == 4) {
                     uint32_t tv = 0;
 #pragma unroll
@@ -808,8 +826,8 @@ int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, Con
     // the MFMA kernels address the padded first-spike map with 32-bit offsets
     SPK_REQUIRE((int64_t)B * g.Hp * g.Wp * g.CP < (1LL << 32), SPK_E_RANGE,
                 "spk_conv_fire: padded input of %lld bytes exceeds 4 GiB", (long long)B * g.Hp * g.Wp * g.CP);
-    SPK_REQUIRE((int64_t)B * ((g.Ho * (int64_t)g.Wo + 15) / 16) < (1LL << 31), SPK_E_RANGE,
-                "spk_conv_fire: too many output positions");
+    SPK_REQUIRE((int64_t)B * ((g.Ho * (int64_t)g.Wo + 15) / 16) * 16 + 256 < (1LL << 31), SPK_E_RANGE,
+                "spk_conv_fire: B * Ho * Wo too large");
     g.HoWo = g.Ho * g.Wo;
     g.ksteps = (K * K * g.CP + 31) / 32;
     g.ntiles = (int)spk::ceil_div(spk::ceil_div(Cout, 16), NTILE_ALIGN) * NTILE_ALIGN;
@@ -840,12 +858,14 @@ int max_lds_per_block() {
 
 template <int G, bool BLDS, bool ALDS>
 void launch_fin(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, const float *inv_scale,
-                const ConvGeom &g, int n_pairs, int n_chunks, int chunk_tiles, int np_max, int a_words, size_t lds,
+                const ConvGeom &g, int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words,
+                size_t lds,
                 float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
     // one workgroup per CU: a multiple of the feature pairs on every XCD
     const int per_xcd = (int)spk::ceil_div(std::max(32, n_pairs), n_pairs) * n_pairs;
     hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
-                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, chunk_tiles, np_max, a_words, inv_scale, P, S, TF,
+                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, P, S,
+                       TF,
                        VF);
 }
 
@@ -902,10 +922,24 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     // finite-threshold launch configuration (validated before anything is enqueued)
     const bool vec = (g.HoWo % 4) == 0 && ((uintptr_t)potentials & 15) == 0 && ((uintptr_t)v_first & 15) == 0 &&
                      ((uintptr_t)spikes & 3) == 0 && ((uintptr_t)t_first & 3) == 0;
-    const int mt = g.mt_per_img;
+    // Tasks: chunks of up to ct_max position tiles.  An image of at most ct_max
+    // tiles is one task (each step's outputs of a feature pair are then one
+    // contiguous region); larger images are cut into chunks of the flattened
+    // (image, position) space, which may span two images, so that no tile slot
+    // is padding (store offsets relative to the chunk's first image fit 32 bits).
     const int ct_max = chunk_tiles_max(vec ? 4 : 1);
-    const int n_chunks = (mt + ct_max - 1) / ct_max;
-    const int chunk_tiles = (mt + n_chunks - 1) / n_chunks;
+    const int64_t npos = (int64_t)B * g.HoWo;
+    const bool flat = g.mt_per_img > ct_max && ((int64_t)T * Cout + 32) * g.HoWo < (1LL << 31);
+    int cpi, chunk_tiles, n_chunks;
+    if (flat) {
+        cpi = 0;
+        chunk_tiles = ct_max;
+        n_chunks = (int)spk::ceil_div(npos, ct_max * 16);
+    } else {
+        cpi = (g.mt_per_img + ct_max - 1) / ct_max;
+        chunk_tiles = (g.mt_per_img + cpi - 1) / cpi;
+        n_chunks = B * cpi;
+    }
     const int np_max = chunk_tiles * 16;
     const int n_pairs = (int)spk::ceil_div(spk::ceil_div(Cout, 16), 2);
     const size_t koff_lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16);
@@ -913,10 +947,25 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     const size_t frag_lds = (size_t)g.ksteps * 4 * 64 * 16;
     const size_t lds_limit = (size_t)max_lds_per_block();
     // spike rows of the largest task, staged in LDS (double-buffered) when small enough
+    // (the row count of a chunk depends on its first position modulo HoWo, which repeats
+    // every HoWo / gcd(HoWo, np_max) chunks; past 65536 of them a bound is used)
+    auto chunk_rows = [&](int64_t p0) {
+        const int64_t pb = std::min(p0 + np_max, npos) - 1;
+        const int64_t ba = p0 / g.HoWo, bb = pb / g.HoWo;
+        return (int)((bb * g.Hp + (pb - bb * g.HoWo) / g.Wo + K) - (ba * g.Hp + (p0 - ba * g.HoWo) / g.Wo));
+    };
+    const int64_t period = g.HoWo / std::gcd((int64_t)g.HoWo, (int64_t)np_max);
     int a_rows = 0;
-    for (int ch = 0; ch < n_chunks; ++ch) {
-        const int p0 = ch * chunk_tiles * 16, np = std::min(chunk_tiles * 16, g.HoWo - p0);
-        a_rows = std::max(a_rows, (p0 + np - 1) / g.Wo + K - p0 / g.Wo);
+    if (!flat) {
+        for (int ch = 0; ch < cpi; ++ch) {
+            const int p0 = ch * np_max, np = std::min(np_max, g.HoWo - p0);
+            a_rows = std::max(a_rows, (p0 + np - 1) / g.Wo + K - p0 / g.Wo);
+        }
+    } else if (period <= 65536) {
+        for (int64_t ch = 0; ch < std::min<int64_t>(n_chunks, period); ++ch)
+            a_rows = std::max(a_rows, chunk_rows(ch * np_max));
+    } else {  // HoWo > 65536 > np_max: a chunk touches at most two images
+        a_rows = (np_max + g.Wo - 1) / g.Wo + 2 * g.Hp;
     }
     const int a_words = a_rows * g.Wp * g.CP / 4;
     const size_t a_lds = 2 * (size_t)a_words * 4;
@@ -948,7 +997,7 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
             launch_inf<false>(tpad, whi, wlo, koff2, inv_scale, g, potentials, spikes, t_first, v_first, st);
     } else {
 #define SPK_FIN(G, BL, AL)                                                                                    \
-    launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, g, n_pairs, n_chunks, chunk_tiles, np_max, a_words, \
+    launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, \
                           fin_lds, potentials, spikes, t_first, v_first, st)
         const int sel = (vec ? 4 : 0) + (blds ? 2 : 0) + (alds ? 1 : 0);
         switch (sel) {
