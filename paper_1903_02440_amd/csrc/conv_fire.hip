@@ -246,6 +246,10 @@ constexpr int FIN_SW = 4;          // store waves (waves 8-11)
 constexpr int FIN_THREADS = (FIN_CW + FIN_SW) * 64;
 // position tiles per task at most: 16 with 4-element store groups, 8 with single elements
 __host__ __device__ constexpr int chunk_tiles_max(int G) { return G == 4 ? 16 : 8; }
+// Row stride (floats) of a feature's positions in the staging area: at least np,
+// a multiple of 4 with an odd quotient, so that the 16 feature lanes of an
+// epilogue 16-byte write fall in distinct LDS bank groups.
+__host__ __device__ constexpr int stage_stride(int np) { return (((np + 3) / 4) | 1) * 4; }
 
 constexpr int FIN_AW = 16384 / 4 / (FIN_CW * 64);  // words of the staged spike region per MFMA-wave thread (16 KiB)
 
@@ -253,7 +257,7 @@ template <int G, bool BLDS, bool ALDS>
 __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
     const int2 *__restrict__ koff2, ConvGeom g, int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max,
-    int a_words, const float *__restrict__ inv_scale, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
+    int a_words, int a_lwords, int apad_shift, const float *__restrict__ inv_scale, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
     float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
@@ -261,8 +265,12 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     int2 *koff_l = reinterpret_cast<int2 *>(lds);
     uint4 *frag_l = lds + (g.ksteps * 4 * 8 + 15) / 16;                  // [ks][n(2)][hi/lo][64] (BLDS)
     float *stage = reinterpret_cast<float *>(frag_l + (BLDS ? g.ksteps * 4 * 64 : 0));  // [TB][32*np_max]
-    const int stage_t = 32 * np_max;
-    uint32_t *abuf = reinterpret_cast<uint32_t *>(stage + FIN_TB * stage_t);  // 2 buffers x a_words (ALDS)
+    const int stage_t = 32 * stage_stride(np_max);
+    // ALDS: 2 buffers of a_lwords words.  With apad_shift >= 0 every position's
+    // cell of CP = 4 << apad_shift bytes takes CP + 8 bytes in LDS, so that the
+    // 16 positions of an A read fall in distinct bank pairs.
+    uint32_t *abuf = reinterpret_cast<uint32_t *>(stage + FIN_TB * stage_t);
+    const int cell_l = apad_shift >= 0 ? g.CP + 8 : g.CP;  // LDS bytes per position cell
     const int row_bytes = g.Wp * g.CP;
 
     const int x = blockIdx.x % 8, j = blockIdx.x / 8;
@@ -314,7 +322,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 #pragma unroll
         for (int k = 0; k < FIN_AW; ++k) {
             const int w = tid + FIN_CW * 64 * k;
-            if (w < a_words) dst[w] = v[k];
+            if (w < a_words) dst[apad_shift >= 0 ? w + 2 * (w >> apad_shift) : w] = v[k];
         }
     };
     if (ALDS && wv < FIN_CW && t_lo + r < t_hi) {
@@ -322,7 +330,17 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         fetch_region(t_lo + r, v);
         store_region(v, abuf);
     }
-    for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) koff_l[i] = koff2[i];
+    if (ALDS && apad_shift >= 0) {  // tap offsets in the padded LDS copy (8 channels of one cell per lane)
+        const int KK = g.K * g.K;
+        for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) {
+            int kyx, ci0;
+            tap_of(g, i >> 2, i & 3, 0, kyx, ci0);
+            const int ox = kyx < KK ? ((kyx / g.K) * g.Wp + kyx % g.K) * cell_l + ci0 : 0;
+            koff_l[i] = int2{ox, ox + 4};
+        }
+    } else {
+        for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) koff_l[i] = koff2[i];
+    }
     if (BLDS) {
         for (int i = tid; i < g.ksteps * 4 * 64; i += FIN_THREADS) {
             const int ln = i & 63, rr = i >> 6;  // rr = (ks*2 + n)*2 + h
@@ -350,7 +368,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             uint32_t alds[FIN_MT];
             int row0_t, w0_t, nw_t;
             region(task, row0_t, w0_t, nw_t);
-            const uint8_t *abuf_t = reinterpret_cast<const uint8_t *>(abuf + abuf_sel * a_words);
+            const uint8_t *abuf_t = reinterpret_cast<const uint8_t *>(abuf + abuf_sel * a_lwords);
 #pragma unroll
             for (int i = 0; i < FIN_MT; ++i) {
                 const int gp = min(pos0 + (wv + FIN_CW * i) * 16 + c, pos0 + np - 1);
@@ -358,7 +376,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 const int y = pos / g.Wo, xx = pos - y * g.Wo;
                 const int row = b * g.Hp + y;
                 abase[i] = tpad + (uint32_t)(((int64_t)row * g.Wp + xx) * g.CP);
-                alds[i] = (uint32_t)((row - row0_t) * row_bytes + xx * g.CP);
+                alds[i] = (uint32_t)(((row - row0_t) * g.Wp + xx) * cell_l);
             }
             const bool has_next = ALDS && task + R < t_hi;
             uint32_t nxt[FIN_AW];
@@ -455,6 +473,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 for (int t = 0; t < FIN_TB; ++t) {
                     if (tb0 + t >= g.T) break;
                     float *st = stage + t * stage_t;
+                    const int sp = stage_stride(np);
 #pragma unroll
                     for (int i = 0; i < FIN_MT; ++i) {
                         const int pl = (wv + FIN_CW * i) * 16 + gq * 4;  // first of this lane's 4 positions
@@ -463,16 +482,16 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                             const int fl = n * 16 + c;
                             const f4 v = acc[i][n][t] * inv_s;  // undo the weight scaling (a power of two)
                             if (G == 4) {
-                                if (pl < np) *reinterpret_cast<f4 *>(st + fl * np + pl) = v;
+                                if (pl < np) *reinterpret_cast<f4 *>(st + fl * sp + pl) = v;
                             } else {
 #pragma unroll
                                 for (int q = 0; q < 4; ++q)
-                                    if (pl + q < np) st[fl * np + pl + q] = v[q];
+                                    if (pl + q < np) st[fl * sp + pl + q] = v[q];
                             }
                         }
                     }
                 }
-                if (has_next && last_block) store_region(nxt, abuf + (abuf_sel ^ 1) * a_words);
+                if (has_next && last_block) store_region(nxt, abuf + (abuf_sel ^ 1) * a_lwords);
                 __syncthreads();  // staging full
             }
             abuf_sel ^= 1;
@@ -497,7 +516,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 const int fl = e / np, pl = e - fl * np;
                 const int gp = pos0 + pl, b = gp / g.HoWo, pos = gp - b * g.HoWo;
                 off[m] = e < nel ? (b - b0) * g.T * (int)tplane + fl * g.HoWo + pos : -1;
-                src[m] = e < nel ? e : 0;
+                src[m] = e < nel ? fl * stage_stride(np) + pl : 0;
             }
             int tfirst[NSLOT][G];
             float vfirst[NSLOT][G];
@@ -859,12 +878,13 @@ int max_lds_per_block() {
 template <int G, bool BLDS, bool ALDS>
 void launch_fin(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, const float *inv_scale,
                 const ConvGeom &g, int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words,
-                size_t lds,
+                int a_lwords, int apad_shift, size_t lds,
                 float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
     // one workgroup per CU: a multiple of the feature pairs on every XCD
     const int per_xcd = (int)spk::ceil_div(std::max(32, n_pairs), n_pairs) * n_pairs;
     hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
-                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, P, S,
+                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, a_lwords,
+                       apad_shift, inv_scale, P, S,
                        TF,
                        VF);
 }
@@ -943,7 +963,7 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     const int np_max = chunk_tiles * 16;
     const int n_pairs = (int)spk::ceil_div(spk::ceil_div(Cout, 16), 2);
     const size_t koff_lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16);
-    const size_t stage_lds = (size_t)FIN_TB * 32 * np_max * sizeof(float);
+    const size_t stage_lds = (size_t)FIN_TB * 32 * stage_stride(np_max) * sizeof(float);
     const size_t frag_lds = (size_t)g.ksteps * 4 * 64 * 16;
     const size_t lds_limit = (size_t)max_lds_per_block();
     // spike rows of the largest task, staged in LDS (double-buffered) when small enough
@@ -968,9 +988,25 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
         a_rows = (np_max + g.Wo - 1) / g.Wo + 2 * g.Hp;
     }
     const int a_words = a_rows * g.Wp * g.CP / 4;
-    const size_t a_lds = 2 * (size_t)a_words * 4;
-    const bool alds = a_words <= FIN_CW * 64 * FIN_AW && koff_lds + stage_lds + a_lds <= lds_limit;
-    const bool blds = koff_lds + frag_lds + stage_lds + (alds ? a_lds : 0) <= lds_limit;
+    // staged spike rows: padded cells when CP is a power of two >= 16 and everything fits
+    auto fits = [&](bool al, bool bl, int lw) {
+        return koff_lds + stage_lds + (al ? 2 * (size_t)lw * 4 : 0) + (bl ? frag_lds : 0) <= lds_limit;
+    };
+    const bool a_small = a_words <= FIN_CW * 64 * FIN_AW;
+    const bool pad_ok = g.CP >= 16 && (g.CP & (g.CP - 1)) == 0;
+    const int padded_words = pad_ok ? a_words + 2 * (a_words / (g.CP / 4)) : a_words;
+    bool alds, blds;
+    int a_lwords = a_words, apad_shift = -1;
+    if (a_small && pad_ok && fits(true, true, padded_words)) {
+        alds = blds = true;
+        a_lwords = padded_words;
+        for (apad_shift = 0; (4 << apad_shift) < g.CP; ++apad_shift) {
+        }
+    } else {
+        alds = a_small && fits(true, false, a_words);
+        blds = fits(alds, true, a_words);
+    }
+    const size_t a_lds = 2 * (size_t)a_lwords * 4;
     const size_t fin_lds = koff_lds + (blds ? frag_lds : 0) + stage_lds + (alds ? a_lds : 0);
     const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4 * 16;
     SPK_REQUIRE(!inf_mode || inf_lds <= lds_limit, SPK_E_RANGE,
@@ -998,6 +1034,7 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     } else {
 #define SPK_FIN(G, BL, AL)                                                                                    \
     launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, \
+                          a_lwords, apad_shift,                                                                    \
                           fin_lds, potentials, spikes, t_first, v_first, st)
         const int sel = (vec ? 4 : 0) + (blds ? 2 : 0) + (alds ? 1 : 0);
         switch (sel) {
