@@ -397,9 +397,10 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 auto load_a = [&](uint32_t (&an)[FIN_MT][2], int2 o) {
 #pragma unroll
                     for (int i = 0; i < FIN_MT; ++i) {
-                        if (ALDS) {
-                            an[i][0] = *reinterpret_cast<const uint32_t *>(abuf_t + alds[i] + (uint32_t)o.x);
-                            an[i][1] = *reinterpret_cast<const uint32_t *>(abuf_t + alds[i] + (uint32_t)o.y);
+                        if (ALDS) {  // CP >= 8: the lane's 8 taps are 8 contiguous bytes (o.y == o.x + 4)
+                            const uint2 w2 = *reinterpret_cast<const uint2 *>(abuf_t + alds[i] + (uint32_t)o.x);
+                            an[i][0] = w2.x;
+                            an[i][1] = w2.y;
                         } else {
                             an[i][0] = *reinterpret_cast<const uint32_t *>(abase[i] + (uint32_t)o.x);
                             an[i][1] = *reinterpret_cast<const uint32_t *>(abase[i] + (uint32_t)o.y);
@@ -992,7 +993,7 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     auto fits = [&](bool al, bool bl, int lw) {
         return koff_lds + stage_lds + (al ? 2 * (size_t)lw * 4 : 0) + (bl ? frag_lds : 0) <= lds_limit;
     };
-    const bool a_small = a_words <= FIN_CW * 64 * FIN_AW;
+    const bool a_small = a_words <= FIN_CW * 64 * FIN_AW && g.CP >= 8;  // (8-byte LDS reads)
     const bool pad_ok = g.CP >= 16 && (g.CP & (g.CP - 1)) == 0;
     const int padded_words = pad_ok ? a_words + 2 * (a_words / (g.CP / 4)) : a_words;
     bool alds, blds;
