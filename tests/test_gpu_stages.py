@@ -170,7 +170,8 @@ def test_pool_toy_t2(golden):
 
 # ---------------------------------------------------------------- kWTA
 KWTA_CASES = [(4, 15, 30, 28, 28, 5, 3), (3, 15, 250, 14, 14, 8, 1), (6, 15, 200, 4, 4, 1, 0),
-              (2, 30, 20, 10, 25, 1, 5), (3, 4, 3, 5, 7, 12, 1), (2, 15, 5, 40, 300, 6, 2)]
+              (2, 30, 20, 10, 25, 1, 5), (3, 4, 3, 5, 7, 12, 1), (2, 15, 5, 40, 300, 6, 2),
+              (3, 15, 40, 1, 1, 4, 0), (2, 15, 7, 1, 9, 3, 1)]
 
 
 def kwta_inputs(seed, B, T, C, H, W, ties=True):
