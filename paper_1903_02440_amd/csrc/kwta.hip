@@ -187,7 +187,8 @@ struct KwtaSmall {
     unsigned mHW, mW;                        // magic multipliers for /HW and /W
 };
 
-__device__ __forceinline__ unsigned qdiv(unsigned n, unsigned m) { return __umulhi(n, m); }
+// n / d as umulhi(n, m) with m = ceil(2^32 / d); m == 0 stands for d == 1 (2^32 does not fit)
+__device__ __forceinline__ unsigned qdiv(unsigned n, unsigned m) { return m ? __umulhi(n, m) : n; }
 
 // The 16 first-spike times and potentials of one tile: as four 4-byte and four
 // 16-byte loads when `vec` (map size a multiple of 4 and aligned bases: then
@@ -377,7 +378,9 @@ bool kwta_small(int B, int T, int C, int H, int W, int k, int r, KwtaSmall &s) {
     const int64_t HW = (int64_t)H * W;
     const int64_t tpm = (HW + 15) / 16;
     if (HW > 65536 || C * tpm > SMALL_TILES) return false;
-    auto magic = [](int64_t d) { return (unsigned)(((1ULL << 32) + (uint64_t)d - 1) / (uint64_t)d); };
+    auto magic = [](int64_t d) {  // 0 for d == 1 (see qdiv)
+        return d == 1 ? 0u : (unsigned)(((1ULL << 32) + (uint64_t)d - 1) / (uint64_t)d);
+    };
     auto exact = [](int64_t d, int64_t n) {  // umulhi(x, ceil(2^32/d)) == x/d for all x < n
         const uint64_t m = ((1ULL << 32) + (uint64_t)d - 1) / (uint64_t)d;
         const uint64_t e = m * (uint64_t)d - (1ULL << 32);
