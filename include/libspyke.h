@@ -171,7 +171,7 @@ SPK_API int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int T,
  * applied first, then image 1, and so on; one image's winners use distinct
  * features, so their order does not matter.  The update of each weight is
  * evaluated in double precision as d = (w-lb)*(ub-w); u = a*d; w = w+u;
- * clamp; and stored as float.
+ * clamp; and stored as float.  Weights are expected to be finite.
  *   weight    f32 [Cout][Cin][K][K] (updated in place)
  *   pre_wave  u8  [B][T][Cin][H][W]: the layer's (unpadded) input wave
  *   winners / n_winners as produced by spk_kwta with the same k.

@@ -221,24 +221,29 @@ __device__ __forceinline__ f4 mfma(half8 a, half8 b, f4 c) {
 }
 
 // ------------------------------------------------------------------ 3a. finite threshold
-// One workgroup = 4 MFMA waves + 4 store waves, persistent, serving one pair
-// of 16-feature tiles (32 features).  Its tasks are (image, chunk of up to 16
-// position tiles) of one XCD's slice of the task list.  For every block of TB
-// time steps:
-//   * each MFMA wave computes the GEMM of its tiles (local tiles w, w+4, ...)
-//     for the 32 features and TB steps -- spike words read straight from
-//     tpad (L2), weight fragments from LDS (or L2 when they do not fit) --
-//     and writes the scaled potentials into the LDS staging area
-//     [TB][32 features][chunk positions];
+// One workgroup = 8 MFMA waves + 4 store waves, persistent, serving one pair
+// of 16-feature tiles (32 features).  A task is a run of up to 16 position
+// tiles: a whole image when it has at most 16 tiles, else a chunk of the
+// flattened (image, position) space that may span two images (no padded
+// tiles); the workgroup takes its tasks from its XCD's slice of the list.
+// For every block of TB time steps:
+//   * each MFMA wave computes the GEMM of its tiles (local tiles w and w+8)
+//     for the 32 features and TB steps -- spike words from the task's rows,
+//     staged in LDS one task ahead (or straight from tpad), weight fragments
+//     from LDS (or L2 when they do not fit) -- and writes the scaled
+//     potentials into the LDS staging area [TB][32 features][row stride];
 //   * the store waves then fire the staged potentials (threshold, first spike,
 //     potential at the first spike, kept in their registers for the whole
 //     task) and write potentials and spikes of each step as contiguous runs
-//     (one run per feature row; a whole-image chunk is one region), while the
+//     (one run per feature row; a whole-image task is one region), while the
 //     MFMA waves go on with the next block.
 // Keeping every global store in the store waves keeps the MFMA waves' own
 // memory counter free of store acknowledgements, so their operand loads never
 // wait behind the output stream.  Two barriers per block: "staging free"
 // (the store waves are done with the previous block) and "staging full".
+// LDS bank conflicts are avoided on both sides of the LDS traffic: the
+// staging rows have a stride whose quotient by 4 is odd, and each staged
+// spike position takes CP + 8 bytes when CP is a power of two >= 16.
 constexpr int FIN_TB = 3;
 constexpr int FIN_CW = 8;          // MFMA waves (waves 0-7)
 constexpr int FIN_MT = 2;          // position tiles per MFMA wave
