@@ -221,7 +221,7 @@ __device__ __forceinline__ f4 mfma(half8 a, half8 b, f4 c) {
 }
 
 // ------------------------------------------------------------------ 3a. finite threshold
-// One workgroup = 8 MFMA waves + 4 store waves, persistent, serving one pair
+// One workgroup = 8 MFMA waves + 8 store waves, persistent, serving one pair
 // of 16-feature tiles (32 features).  A task is a run of up to 16 position
 // tiles: a whole image when it has at most 16 tiles, else a chunk of the
 // flattened (image, position) space that may span two images (no padded
@@ -242,12 +242,14 @@ __device__ __forceinline__ f4 mfma(half8 a, half8 b, f4 c) {
 // wait behind the output stream.  Two barriers per block: "staging free"
 // (the store waves are done with the previous block) and "staging full".
 // LDS bank conflicts are avoided on both sides of the LDS traffic: the
-// staging rows have a stride whose quotient by 4 is odd, and each staged
-// spike position takes CP + 8 bytes when CP is a power of two >= 16.
+// staging rows have a stride whose quotient by 4 is odd, and the staged spike
+// rows are stored channel-group major (see k_conv_fire_fin's ALDS buffers).
+// Two waves per SIMD do the firing and storing: their VALU work and LDS
+// waits overlap each other's.
 constexpr int FIN_TB = 3;
 constexpr int FIN_CW = 8;          // MFMA waves (waves 0-7)
 constexpr int FIN_MT = 2;          // position tiles per MFMA wave
-constexpr int FIN_SW = 4;          // store waves (waves 8-11)
+constexpr int FIN_SW = 8;          // store waves (waves 8-15)
 constexpr int FIN_THREADS = (FIN_CW + FIN_SW) * 64;
 // position tiles per task at most: 16 with 4-element store groups, 8 with single elements
 __host__ __device__ constexpr int chunk_tiles_max(int G) { return G == 4 ? 16 : 8; }
@@ -256,14 +258,12 @@ __host__ __device__ constexpr int chunk_tiles_max(int G) { return G == 4 ? 16 : 
 // epilogue 16-byte write fall in distinct LDS bank groups.
 __host__ __device__ constexpr int stage_stride(int np) { return (((np + 3) / 4) | 1) * 4; }
 
-constexpr int FIN_AW = 16384 / 4 / (FIN_CW * 64);  // words of the staged spike region per MFMA-wave thread (16 KiB)
-
 template <int G, bool BLDS, bool ALDS>
 __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
     const int2 *__restrict__ koff2, ConvGeom g, int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max,
-    int a_words, int a_lwords, int apad_shift, const float *__restrict__ inv_scale, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
-    float *__restrict__ VF) {
+    int a_words, const float *__restrict__ inv_scale, float *__restrict__ P, uint8_t *__restrict__ S,
+    uint8_t *__restrict__ TF, float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
     const int gq = lane >> 4, c = lane & 15;
@@ -271,11 +271,10 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     uint4 *frag_l = lds + (g.ksteps * 4 * 8 + 15) / 16;                  // [ks][n(2)][hi/lo][64] (BLDS)
     float *stage = reinterpret_cast<float *>(frag_l + (BLDS ? g.ksteps * 4 * 64 : 0));  // [TB][32*np_max]
     const int stage_t = 32 * stage_stride(np_max);
-    // ALDS: 2 buffers of a_lwords words.  With apad_shift >= 0 every position's
-    // cell of CP = 4 << apad_shift bytes takes CP + 8 bytes in LDS, so that the
-    // 16 positions of an A read fall in distinct bank pairs.
+    // ALDS: 2 buffers of a_words words (a multiple of 64) holding a task's
+    // padded rows channel-group major, [row][CP/8][Wp][8 bytes], so that the 16
+    // consecutive positions of an 8-byte A read are 128 contiguous bytes.
     uint32_t *abuf = reinterpret_cast<uint32_t *>(stage + FIN_TB * stage_t);
-    const int cell_l = apad_shift >= 0 ? g.CP + 8 : g.CP;  // LDS bytes per position cell
     const int row_bytes = g.Wp * g.CP;
 
     const int x = blockIdx.x % 8, j = blockIdx.x / 8;
@@ -313,34 +312,29 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         w0 = (int)(((int64_t)row0 * row_bytes) >> 2);
         nw = (row1 - row0 + 1) * row_bytes / 4;
     };
-    auto fetch_region = [&](int task, uint32_t (&v)[FIN_AW]) {
-        int yf, w0, nw;
-        region(task, yf, w0, nw);
+    // Direct global-to-LDS loads of a task's rows into `dst` by the MFMA waves
+    // (lane i of a load writes word d0 + i); they complete before the barrier
+    // that precedes the buffer's first use (s_waitcnt vmcnt(0) ahead of it).
+    auto fill_region = [&](int task, uint32_t *dst) {
+        int row0, w0, nw;
+        region(task, row0, w0, nw);
         const uint32_t *src = reinterpret_cast<const uint32_t *>(tpad) + (uint32_t)w0;
-#pragma unroll
-        for (int k = 0; k < FIN_AW; ++k) {
-            const int w = tid + FIN_CW * 64 * k;
-            v[k] = w < nw ? src[w] : 0u;
+        const int rw = row_bytes / 4, gw = 2 * g.Wp, cw = g.CP / 4;
+        for (int d0 = wv * 64; d0 < nw; d0 += FIN_CW * 64) {
+            const int d = min(d0 + lane, nw - 1);  // lanes past the region repeat its last word
+            const int rr = d / rw, rem = d - rr * rw;
+            const int cg = rem / gw, rem2 = rem - cg * gw;
+            __builtin_amdgcn_global_load_lds(src + rr * rw + (rem2 >> 1) * cw + cg * 2 + (rem2 & 1), dst + d0, 4, 0,
+                                             0);
         }
     };
-    auto store_region = [&](const uint32_t (&v)[FIN_AW], uint32_t *dst) {
-#pragma unroll
-        for (int k = 0; k < FIN_AW; ++k) {
-            const int w = tid + FIN_CW * 64 * k;
-            if (w < a_words) dst[apad_shift >= 0 ? w + 2 * (w >> apad_shift) : w] = v[k];
-        }
-    };
-    if (ALDS && wv < FIN_CW && t_lo + r < t_hi) {
-        uint32_t v[FIN_AW];
-        fetch_region(t_lo + r, v);
-        store_region(v, abuf);
-    }
-    if (ALDS && apad_shift >= 0) {  // tap offsets in the padded LDS copy (8 channels of one cell per lane)
+    if (ALDS && wv < FIN_CW && t_lo + r < t_hi) fill_region(t_lo + r, abuf);
+    if (ALDS) {  // tap offsets in the LDS copy: 8 channels (one channel group of a cell) per lane
         const int KK = g.K * g.K;
         for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) {
             int kyx, ci0;
             tap_of(g, i >> 2, i & 3, 0, kyx, ci0);
-            const int ox = kyx < KK ? ((kyx / g.K) * g.Wp + kyx % g.K) * cell_l + ci0 : 0;
+            const int ox = kyx < KK ? (kyx / g.K) * row_bytes + (ci0 >> 3) * g.Wp * 8 + (kyx % g.K) * 8 : 0;
             koff_l[i] = int2{ox, ox + 4};
         }
     } else {
@@ -354,6 +348,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             frag_l[i] = __builtin_bit_cast(uint4, src[((int64_t)(pair * 2 + n) * g.ksteps + ks) * 64 + ln]);
         }
     }
+    if (ALDS) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     const float inv_s = *inv_scale;
     const int64_t tplane = (int64_t)g.Cout * g.HoWo;
@@ -373,7 +368,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             uint32_t alds[FIN_MT];
             int row0_t, w0_t, nw_t;
             region(task, row0_t, w0_t, nw_t);
-            const uint8_t *abuf_t = reinterpret_cast<const uint8_t *>(abuf + abuf_sel * a_lwords);
+            const uint8_t *abuf_t = reinterpret_cast<const uint8_t *>(abuf + abuf_sel * a_words);
 #pragma unroll
             for (int i = 0; i < FIN_MT; ++i) {
                 const int gp = min(pos0 + (wv + FIN_CW * i) * 16 + c, pos0 + np - 1);
@@ -381,11 +376,10 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 const int y = pos / g.Wo, xx = pos - y * g.Wo;
                 const int row = b * g.Hp + y;
                 abase[i] = tpad + (uint32_t)(((int64_t)row * g.Wp + xx) * g.CP);
-                alds[i] = (uint32_t)(((row - row0_t) * g.Wp + xx) * cell_l);
+                alds[i] = (uint32_t)((row - row0_t) * row_bytes + xx * 8);
             }
             const bool has_next = ALDS && task + R < t_hi;
-            uint32_t nxt[FIN_AW];
-            if (has_next) fetch_region(task + R, nxt);  // consumed at the end of the task
+            if (has_next) fill_region(task + R, abuf + (abuf_sel ^ 1) * a_words);  // read from the next task on
             for (int tb0 = 0; tb0 < g.T; tb0 += FIN_TB) {
                 const bool last_block = tb0 + FIN_TB >= g.T;
                 f4 acc[FIN_MT][2][FIN_TB];
@@ -497,7 +491,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                         }
                     }
                 }
-                if (has_next && last_block) store_region(nxt, abuf + (abuf_sel ^ 1) * a_lwords);
+                if (has_next && last_block) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                 __syncthreads();  // staging full
             }
             abuf_sel ^= 1;
@@ -884,13 +878,12 @@ int max_lds_per_block() {
 template <int G, bool BLDS, bool ALDS>
 void launch_fin(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, const float *inv_scale,
                 const ConvGeom &g, int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words,
-                int a_lwords, int apad_shift, size_t lds,
+                size_t lds,
                 float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
     // one workgroup per CU: a multiple of the feature pairs on every XCD
     const int per_xcd = (int)spk::ceil_div(std::max(32, n_pairs), n_pairs) * n_pairs;
     hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
-                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, a_lwords,
-                       apad_shift, inv_scale, P, S,
+                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, P, S,
                        TF,
                        VF);
 }
@@ -993,26 +986,11 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     } else {  // HoWo > 65536 > np_max: a chunk touches at most two images
         a_rows = (np_max + g.Wo - 1) / g.Wo + 2 * g.Hp;
     }
-    const int a_words = a_rows * g.Wp * g.CP / 4;
-    // staged spike rows: padded cells when CP is a power of two >= 16 and everything fits
-    auto fits = [&](bool al, bool bl, int lw) {
-        return koff_lds + stage_lds + (al ? 2 * (size_t)lw * 4 : 0) + (bl ? frag_lds : 0) <= lds_limit;
-    };
-    const bool a_small = a_words <= FIN_CW * 64 * FIN_AW && g.CP >= 8;  // (8-byte LDS reads)
-    const bool pad_ok = g.CP >= 16 && (g.CP & (g.CP - 1)) == 0;
-    const int padded_words = pad_ok ? a_words + 2 * (a_words / (g.CP / 4)) : a_words;
-    bool alds, blds;
-    int a_lwords = a_words, apad_shift = -1;
-    if (a_small && pad_ok && fits(true, true, padded_words)) {
-        alds = blds = true;
-        a_lwords = padded_words;
-        for (apad_shift = 0; (4 << apad_shift) < g.CP; ++apad_shift) {
-        }
-    } else {
-        alds = a_small && fits(true, false, a_words);
-        blds = fits(alds, true, a_words);
-    }
-    const size_t a_lds = 2 * (size_t)a_lwords * 4;
+    // staged spike rows: CP >= 8 (8-byte reads of one channel group), buffers rounded to 64 words
+    const int a_words = (int)spk::align_up((size_t)a_rows * g.Wp * g.CP / 4, 64);
+    const size_t a_lds = 2 * (size_t)a_words * 4;
+    const bool alds = g.CP >= 8 && koff_lds + stage_lds + a_lds <= lds_limit;
+    const bool blds = koff_lds + frag_lds + stage_lds + (alds ? a_lds : 0) <= lds_limit;
     const size_t fin_lds = koff_lds + (blds ? frag_lds : 0) + stage_lds + (alds ? a_lds : 0);
     const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4 * 16;
     SPK_REQUIRE(!inf_mode || inf_lds <= lds_limit, SPK_E_RANGE,
@@ -1040,7 +1018,6 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
     } else {
 #define SPK_FIN(G, BL, AL)                                                                                    \
     launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, \
-                          a_lwords, apad_shift,                                                                    \
                           fin_lds, potentials, spikes, t_first, v_first, st)
         const int sel = (vec ? 4 : 0) + (blds ? 2 : 0) + (alds ? 1 : 0);
         switch (sel) {
