@@ -27,12 +27,13 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 
 
-def conv_call_bytes(B, T, cin, h, w, st):
-    """Algorithmic bytes of one spk_conv_fire call: read the input wave and
-    the weights once, write potentials + spikes for every step and the
-    first-spike time + potential once."""
+def conv_call_bytes(B, T, cin, h, w, st, from_times):
+    """Algorithmic bytes of one conv call: read the input (its first-spike map
+    when the call takes that, spk_conv_fire_first_spike, else the T planes of
+    the wave) and the weights once, write potentials + spikes for every step
+    and the first-spike time + potential once."""
     ho, wo = h + 2 * st.pad - st.K + 1, w + 2 * st.pad - st.K + 1
-    return (B * T * cin * h * w + st.cout * cin * st.K * st.K * 4
+    return ((1 if from_times else T) * B * cin * h * w + st.cout * cin * st.K * st.K * 4
             + B * T * st.cout * ho * wo * 5 + B * st.cout * ho * wo * 5), ho, wo
 
 
@@ -43,9 +44,11 @@ def step_bytes(wl):
     c, h, w = (6 if wl.bank == "dog" else 4) if wl.source == "image" else wl.cin, wl.H, wl.W
     if wl.source == "image":
         out["encode"] = B * h * w + B * T * c * h * w + B * c * h * w
+    exact = wl.source == "image"  # the chain feeds a conv the first-spike map of an Eq.1 wave
     for i, st in enumerate(wl.stages):
         if hasattr(st, "cout"):
-            nb, ho, wo = conv_call_bytes(B, T, c, h, w, st)
+            nb, ho, wo = conv_call_bytes(B, T, c, h, w, st, exact)
+            exact = False
             out[f"conv{i}"] = nb
             out[f"kwta{i}"] = B * st.cout * ho * wo * 5 + B * st.k * 16
             if st.learn:
@@ -56,6 +59,7 @@ def step_bytes(wl):
             # first-spike pooling: one byte per input neuron in, the wave and first-spike map out
             out[f"pool{i}"] = B * c * h * w + B * T * c * ho * wo + B * c * ho * wo
             h, w = ho, wo
+            exact = True
     return out
 
 

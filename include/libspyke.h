@@ -123,6 +123,17 @@ SPK_API int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, int
                   float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
                   void *workspace, size_t ws_bytes, void *stream);
 
+/* The same call with the input given by its first-spike map (Eq.1: the
+ * wave is 1 at step t exactly where t >= t_first), which is what the
+ * contraction consumes; it saves reading the T planes of the wave.
+ *   in_t_first u8 [B][Cin][H][W], values in [0, T] (T = never; larger
+ *   values count as T).  Outputs, limits, workspace and errors as
+ *   spk_conv_fire.                                                          */
+SPK_API int spk_conv_fire_first_spike(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+             const float *weight, int Cout, int K, int pad, float threshold,
+             float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
+             void *workspace, size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------------------
  * Spike max-pooling (section "snn Module", Eq.3): on a spike wave each
  * window yields its earliest spike.  Window `kernel`, stride `stride`,

@@ -63,6 +63,8 @@ struct ConvGeom {
 // 16-byte boundaries coincide.
 constexpr int PAD_LDS = 32768;
 
+// TIMES: the input is the first-spike map t_first [B][Cin][H][W] itself (T = never).
+template <bool TIMES>
 __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restrict__ wave, ConvGeom g,
                                                          int rows_per_chunk, uint8_t *__restrict__ tpad) {
     __shared__ __attribute__((aligned(16))) uint8_t buf[PAD_LDS + 16];
@@ -81,17 +83,22 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
         const int shift = (int)((uintptr_t)out & 15);
         for (int i = tid * 4; i < shift + nbytes; i += 1024) *reinterpret_cast<uint32_t *>(buf + i) = tfill;
         __syncthreads();
-        const uint8_t *src = wave + b * g.T * (int64_t)g.Cin * hw;
+        const uint8_t *src = wave + b * (TIMES ? 1 : g.T) * (int64_t)g.Cin * hw;
         for (int i = tid; i < ncell; i += 256) {
             const int x = i % g.W, rest = i / g.W;
             const int yy = rest % (y_hi - y_lo), ci = rest / (y_hi - y_lo);
             const int y = y_lo + yy;
             const uint8_t *p = src + ci * hw + y * g.W + x;
-            int cnt = 0;
+            int tp;
+            if (TIMES) {
+                tp = min((int)*p, g.T);
+            } else {
+                int cnt = 0;
 #pragma unroll 5
-            for (int t = 0; t < g.T; ++t) cnt += p[(int64_t)t * g.Cin * hw] != 0;
-            // a cumulative wave has exactly T - t_first ones
-            buf[shift + ((y + g.pad - r0) * g.Wp + x + g.pad) * g.CP + ci] = (uint8_t)(g.T - cnt);
+                for (int t = 0; t < g.T; ++t) cnt += p[(int64_t)t * g.Cin * hw] != 0;
+                tp = g.T - cnt;  // a cumulative wave has exactly T - t_first ones
+            }
+            buf[shift + ((y + g.pad - r0) * g.Wp + x + g.pad) * g.CP + ci] = (uint8_t)tp;
         }
         __syncthreads();
         const int head = min(nbytes, (16 - shift) & 15);
@@ -113,12 +120,24 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
 // n = nt*16 + lane%16, the 8 taps k = ks*32 + 8*(lane/16) + j, j = 0..7.
 __global__ __launch_bounds__(256) void k_weight_absmax(const float *__restrict__ w, int64_t n,
                                                        unsigned *__restrict__ maxbits) {
+    __shared__ unsigned red[4];
     unsigned m = 0;
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
-        m = max(m, __float_as_uint(fabsf(w[i])));
+    // four independent loads per thread and pass, then one atomic per workgroup
+    for (int64_t i0 = (int64_t)blockIdx.x * 1024 + threadIdx.x; i0 < n; i0 += (int64_t)gridDim.x * 1024) {
+        float v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = i0 + 256 * j < n ? w[i0 + 256 * j] : 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) m = max(m, __float_as_uint(fabsf(v[j])));
+    }
 #pragma unroll
     for (int s = 32; s >= 1; s >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, s, 64));
-    if ((threadIdx.x & 63) == 0 && m) atomicMax(maxbits, m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        m = max(max(red[0], red[1]), max(red[2], red[3]));
+        if (m) atomicMax(maxbits, m);
+    }
 }
 
 __device__ __forceinline__ int weight_scale_exp(unsigned maxbits) {
@@ -911,9 +930,11 @@ extern "C" size_t spk_conv_fire_workspace_size(int B, int T, int Cin, int H, int
     return plan_workspace(pl);
 }
 
-extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, int W, const float *weight,
-                             int Cout, int K, int pad, float threshold, float *potentials, uint8_t *spikes,
-                             uint8_t *t_first, float *v_first, void *workspace, size_t ws_bytes, void *stream) {
+namespace {
+// The conv call on either input form (times: in = first-spike map, else the wave).
+int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int W, const float *weight, int Cout,
+              int K, int pad, float threshold, float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
+              void *workspace, size_t ws_bytes, void *stream) {
     ConvPlan pl;
     int rc = make_plan(B, T, Cin, H, W, Cout, K, pad, pl);
     if (rc != SPK_OK) return rc;
@@ -921,7 +942,7 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
                 "spk_conv_fire: threshold must be a number or +INFINITY");
     if (B == 0) return spk::ok();
     SPK_REQUIRE(wave && weight && t_first && v_first, SPK_E_ARG,
-                "spk_conv_fire: wave, weight, t_first and v_first are required");
+                "spk_conv_fire: the input, weight, t_first and v_first are required");
     const size_t need = plan_workspace(pl);
     SPK_REQUIRE(workspace && ws_bytes >= need, SPK_E_WORKSPACE,
                 "spk_conv_fire: workspace of %zu bytes < %zu required", ws_bytes, need);
@@ -1000,13 +1021,15 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
 
     const int row_bytes = g.Wp * g.CP;
     const int rows_per_chunk = std::min(g.Hp, PAD_LDS / row_bytes);
-    hipLaunchKernelGGL(k_pad_first_spike, dim3((unsigned)spk::ceil_div(g.Hp, rows_per_chunk),
-                                               (unsigned)std::min(B, 65535)),
-                       dim3(256), 0, st, wave, g, rows_per_chunk, tpad);
+    const dim3 pad_grid((unsigned)spk::ceil_div(g.Hp, rows_per_chunk), (unsigned)std::min(B, 65535));
+    if (times)
+        hipLaunchKernelGGL(k_pad_first_spike<true>, pad_grid, dim3(256), 0, st, wave, g, rows_per_chunk, tpad);
+    else
+        hipLaunchKernelGGL(k_pad_first_spike<false>, pad_grid, dim3(256), 0, st, wave, g, rows_per_chunk, tpad);
     hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(64), 0, st, maxbits, 1);
     const int64_t nw = (int64_t)Cout * Cin * K * K;
-    hipLaunchKernelGGL(k_weight_absmax, dim3((unsigned)std::min<int64_t>(256, spk::ceil_div(nw, 256))), dim3(256), 0,
-                       st, weight, nw, maxbits);
+    hipLaunchKernelGGL(k_weight_absmax, dim3((unsigned)std::min<int64_t>(2048, spk::ceil_div(nw, 1024))), dim3(256),
+                       0, st, weight, nw, maxbits);
     const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
     hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, maxbits,
                        whi, wlo, koff2, inv_scale);
@@ -1033,4 +1056,20 @@ extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, 
 #undef SPK_FIN
     }
     return spk::check_launch("spk_conv_fire");
+}
+}  // namespace
+
+extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, int W, const float *weight,
+                             int Cout, int K, int pad, float threshold, float *potentials, uint8_t *spikes,
+                             uint8_t *t_first, float *v_first, void *workspace, size_t ws_bytes, void *stream) {
+    return conv_fire(wave, false, B, T, Cin, H, W, weight, Cout, K, pad, threshold, potentials, spikes, t_first,
+                     v_first, workspace, ws_bytes, stream);
+}
+
+extern "C" int spk_conv_fire_first_spike(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+                                         const float *weight, int Cout, int K, int pad, float threshold,
+                                         float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
+                                         void *workspace, size_t ws_bytes, void *stream) {
+    return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, pad, threshold, potentials, spikes,
+                     t_first, v_first, workspace, ws_bytes, stream);
 }

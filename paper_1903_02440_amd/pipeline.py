@@ -7,7 +7,10 @@ calls on one stream, with no host synchronisation and no allocation inside
 
 * source: ``spk_encode_latency`` (images + filter bank) or a given wave;
 * each conv stage: ``spk_conv_fire`` then ``spk_kwta`` (the winners feed
-  plasticity and, for the last layer, the decision);
+  plasticity and, for the last layer, the decision); when its input is the
+  encoder's or a pool's output, whose wave is Eq.1 of its first-spike map by
+  construction, ``spk_conv_fire_first_spike`` reads that map instead of the
+  T planes of the wave;
 * each pool stage: ``spk_pool_first_spike`` on the first-spike map of the
   stage below (which equals ``spk_pool`` on its wave whenever that wave is
   cumulative -- always the case for non-negative weights), or ``spk_pool``
@@ -29,7 +32,8 @@ import math
 
 import torch
 
-from . import (pool_out_size, conv_out_size, spk_conv_fire, spk_conv_fire_workspace_size, spk_decide,
+from . import (pool_out_size, conv_out_size, spk_conv_fire, spk_conv_fire_first_spike, spk_conv_fire_workspace_size,
+               spk_decide,
                spk_encode_latency, spk_encode_latency_workspace_size, spk_kwta, spk_kwta_workspace_size,
                spk_pool, spk_pool_first_spike, spk_rstdp, spk_stdp, spk_stdp_workspace_size)
 
@@ -130,27 +134,35 @@ class Chain:
                                t_first=self.input_tf, intensities=False, workspace=self.workspace, stream=stream)
             mark("encode", 1)
         x, x_tf = self.input_wave, self.input_tf
+        x_exact = x_tf is not None  # x is Eq.1 of x_tf
         last_conv = None
         for i, (st, b) in enumerate(zip(self.stages, self.bufs)):
             self.pre_waves[i] = x
             if _is_conv(st):
                 mark(f"conv{i}", 0)
-                spk_conv_fire(x, b["weight"], st.pad, st.thr, potentials=b["P"], spikes=b["S"], t_first=b["tf"],
-                              v_first=b["vf"], workspace=self.workspace, stream=stream)
+                if x_exact:
+                    spk_conv_fire_first_spike(x_tf, self.T, b["weight"], st.pad, st.thr, potentials=b["P"],
+                                              spikes=b["S"], t_first=b["tf"], v_first=b["vf"],
+                                              workspace=self.workspace, stream=stream)
+                else:
+                    spk_conv_fire(x, b["weight"], st.pad, st.thr, potentials=b["P"], spikes=b["S"], t_first=b["tf"],
+                                  v_first=b["vf"], workspace=self.workspace, stream=stream)
                 mark(f"conv{i}", 1)
                 mark(f"kwta{i}", 0)
                 spk_kwta(b["tf"], b["vf"], self.T, st.k, st.r, winners=b["win"], n_winners=b["nw"],
                          workspace=self.workspace, stream=stream)
                 mark(f"kwta{i}", 1)
-                x, x_tf = b["S"], b["tf"]
+                x, x_tf, x_exact = b["S"], b["tf"], False
                 last_conv = i
             else:
                 mark(f"pool{i}", 0)
                 if self.pool_from_first_spike and x_tf is not None:
                     spk_pool_first_spike(x_tf, self.T, st.P, st.R, st.D, out_wave=b["out"], out_t_first=b["out_tf"],
                                          stream=stream)
+                    x_exact = True  # the pooled wave is written as Eq.1 of the pooled map
                 else:
                     spk_pool(x, st.P, st.R, st.D, out_wave=b["out"], out_t_first=b["out_tf"], stream=stream)
+                    # (pooling an Eq.1 wave gives the Eq.1 wave of the pooled map)
                 mark(f"pool{i}", 1)
                 x, x_tf = b["out"], b["out_tf"]
         if last_conv is not None and self.stages[last_conv].learn == "rstdp":

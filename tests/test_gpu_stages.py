@@ -104,6 +104,23 @@ def test_conv_fire_parity(case, kind):
         assert_equal(gpu[1], ref[1], "spikes (exact)")
 
 
+@pytest.mark.parametrize("case", CONV_CASES, ids=[c[0] for c in CONV_CASES])
+def test_conv_fire_first_spike_input(case):
+    # the first-spike-map entry on the map of an Eq.1 wave: oracle parity on the wave, and
+    # bitwise the same outputs as the wave entry
+    name, B, T, Cin, H, W, Cout, K, pad, thr, ps = case
+    g = synth.rng(150 + len(name), 1)
+    tf = synth.times_uniform_or_silent(g, (B, Cin, H, W), T, ps)
+    wave = wave_of(tf, T)
+    Wt = synth.normal_weights(g, (Cout, Cin, K, K), 0.8, 0.05)
+    got = spk.spk_conv_fire_first_spike(dev(tf), T, dev(Wt), pad, thr)
+    via_wave = spk.spk_conv_fire(dev(wave), dev(Wt), pad, thr)
+    sync()
+    for a, b in zip(got, via_wave):
+        assert torch.equal(a, b)
+    compare_conv_fire(tuple(host(x) for x in got), orc.conv_fire(wave, Wt, pad, thr), thr, exact_potentials=False)
+
+
 def test_conv_fire_deterministic_and_optional_outputs():
     B, T, Cin, H, W, Cout, K, pad = 2, 15, 30, 14, 14, 250, 3, 1
     g = synth.rng(7, 1)
