@@ -215,47 +215,62 @@ __device__ __forceinline__ void load_tile16(const uint8_t *__restrict__ tf, cons
 
 // Four lanes per tile, each with 4 consecutive positions, so a wave's loads
 // are contiguous; two shuffle steps combine the quarter maxima.  Grid-stride
-// over the batch's tiles (the stride is a multiple of 4 lanes).
+// over the batch's tiles (the stride is a multiple of 4 lanes), four strides
+// per pass with all their loads issued before any is used.
 __global__ __launch_bounds__(256) void k_kwta_tiles16(const uint8_t *__restrict__ tf, const float *__restrict__ vf,
                                                       KwtaSmall g, int vec, uint64_t *__restrict__ tilekey) {
+    constexpr int U = 4;
     const uint32_t total = (uint32_t)g.B * (uint32_t)g.ntiles * 4u;  // < 2^31, checked on the host
     const uint32_t stride = gridDim.x * 256u;
-    for (uint32_t g0 = blockIdx.x * 256u; g0 < total; g0 += stride) {  // uniform per workgroup
-        const uint32_t gt = g0 + threadIdx.x;
-        const uint32_t gid = gt >> 2;
-        const int sub = (int)(gt & 3u);
-        const bool live = gt < total;
-        uint64_t m = 0;
-        if (live) {
-            const uint32_t b = gid / (uint32_t)g.ntiles;
-            const int tile = (int)(gid - b * (uint32_t)g.ntiles);
-            const int f = tile / g.tpm, pos0 = (tile - f * g.tpm) * 16 + 4 * sub;
-            const int64_t base = (int64_t)b * g.C * g.HW + (int64_t)f * g.HW + pos0;
-            int tv[4];
-            float vv[4];
-            if (vec && pos0 + 4 <= g.HW) {
-                const uint32_t w = *reinterpret_cast<const uint32_t *>(tf + base);
-                const float4 v = *reinterpret_cast<const float4 *>(vf + base);
-                tv[0] = w & 0xFF; tv[1] = (w >> 8) & 0xFF; tv[2] = (w >> 16) & 0xFF; tv[3] = w >> 24;
-                vv[0] = v.x; vv[1] = v.y; vv[2] = v.z; vv[3] = v.w;
-            } else {
+    for (uint32_t g0 = blockIdx.x * 256u; g0 < total; g0 += U * stride) {  // uniform per workgroup
+        int tv[U][4];
+        float vv[U][4];
+        uint32_t idx0[U];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const bool ok = pos0 + j < g.HW;
-                    tv[j] = ok ? (int)tf[base + j] : g.T;
-                    vv[j] = ok ? vf[base + j] : 0.0f;
+        for (int u = 0; u < U; ++u) {
+            const uint32_t gt = g0 + u * stride + threadIdx.x;
+            const uint32_t gid = gt >> 2;
+            const int sub = (int)(gt & 3u);
+            idx0[u] = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                tv[u][j] = g.T;
+                vv[u][j] = 0.0f;
+            }
+            if (gt < total) {
+                const uint32_t b = gid / (uint32_t)g.ntiles;
+                const int tile = (int)(gid - b * (uint32_t)g.ntiles);
+                const int f = tile / g.tpm, pos0 = (tile - f * g.tpm) * 16 + 4 * sub;
+                const int64_t base = (int64_t)b * g.C * g.HW + (int64_t)f * g.HW + pos0;
+                idx0[u] = (uint32_t)(f * g.HW + pos0);
+                if (vec && pos0 + 4 <= g.HW) {
+                    const uint32_t w = *reinterpret_cast<const uint32_t *>(tf + base);
+                    const float4 v = *reinterpret_cast<const float4 *>(vf + base);
+                    tv[u][0] = w & 0xFF; tv[u][1] = (w >> 8) & 0xFF; tv[u][2] = (w >> 16) & 0xFF; tv[u][3] = w >> 24;
+                    vv[u][0] = v.x; vv[u][1] = v.y; vv[u][2] = v.z; vv[u][3] = v.w;
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const bool ok = pos0 + j < g.HW;
+                        tv[u][j] = ok ? (int)tf[base + j] : g.T;
+                        vv[u][j] = ok ? vf[base + j] : 0.0f;
+                    }
                 }
             }
-            const uint32_t idx0 = (uint32_t)(f * g.HW + pos0);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t gt = g0 + u * stride + threadIdx.x;
+            uint64_t m = 0;
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                if (tv[j] < g.T) {
-                    const uint64_t key = kwta_key(tv[j], vv[j], idx0 + j);
+                if (tv[u][j] < g.T) {
+                    const uint64_t key = kwta_key(tv[u][j], vv[u][j], idx0[u] + j);
                     m = key > m ? key : m;
                 }
+            m = group_max(m, 4);
+            if (gt < total && (gt & 3u) == 0) tilekey[gt >> 2] = m;
         }
-        m = group_max(m, 4);
-        if (live && sub == 0) tilekey[gid] = m;
     }
 }
 

@@ -5,10 +5,12 @@
 // window; zero padding) and Eq.3 for the output size, read as
 // floor((H + 2D - P)/R) + 1 (equal to the printed form whenever P == R).
 //
-// One thread per output neuron (b, c, yo, xo): for every step t it ORs the
-// window's bytes of plane t and stores one byte, so a wave reads and writes
-// consecutive x positions of one plane; the first-spike map is T minus the
-// number of steps at which the pooled neuron is on.
+// One thread per output neuron (b, c, yo, xo) of the wave form: for every
+// step t it ORs the window's bytes of plane t and stores one byte, so a wave
+// reads and writes consecutive x positions of one plane; the first-spike map
+// is T minus the number of steps at which the pooled neuron is on.
+#include <cstdint>
+
 #include "common.hpp"
 
 namespace {
@@ -42,28 +44,65 @@ __global__ __launch_bounds__(256) void k_pool(const uint8_t *__restrict__ in, in
     if (out_tf) out_tf[b * per_img + i] = (uint8_t)(T - on);
 }
 
-// Pooling of first-spike maps: grid (image, chunk of 256 of the image's
-// C*Ho*Wo outputs); the minimum over the window, then its T wave bytes.
+// Pooling of first-spike maps: the minimum over the window, then its T wave
+// bytes.  Grid (image, chunk of the image's C*Ho*Wo outputs); with VEC (C*Ho*Wo
+// a multiple of 4, 4-byte aligned outputs) each thread makes 4 consecutive
+// outputs and stores them as one word per plane, else one output per thread.
+// PW > 0 is the window size known at compile time: every window load is then
+// issued before any is used.
+template <bool VEC, int PW>
 __global__ __launch_bounds__(256) void k_pool_first_spike(const uint8_t *__restrict__ tf, int T, int C, int H, int W,
                                                           int P, int R, int D, int Ho, int Wo,
                                                           uint8_t *__restrict__ out, uint8_t *__restrict__ out_tf) {
+    constexpr int NQ = VEC ? 4 : 1;
     const int per_img = C * Ho * Wo;
-    const int i = blockIdx.y * 256 + threadIdx.x;
-    if (i >= per_img) return;
+    const int i0 = (blockIdx.y * 256 + threadIdx.x) * NQ;
+    if (i0 >= per_img) return;
     const int64_t b = blockIdx.x;
     const int hw = Ho * Wo;
-    const int c = i / hw, pix = i - c * hw;
-    const int yo = pix / Wo, xo = pix - yo * Wo;
-    const int y0 = yo * R - D, x0 = xo * R - D;
-    const int ya = max(y0, 0), yb = min(y0 + P, H), xa = max(x0, 0), xb = min(x0 + P, W);
-    const uint8_t *src = tf + (b * C + c) * (int64_t)H * W;
-    int m = T;
-    for (int y = ya; y < yb; ++y)
-        for (int x = xa; x < xb; ++x) m = min(m, (int)src[y * W + x]);
-    if (out_tf) out_tf[b * per_img + i] = (uint8_t)m;
-    if (out) {
-        uint8_t *dst = out + b * T * (int64_t)per_img + i;
-        for (int t = 0; t < T; ++t) dst[(int64_t)t * per_img] = (uint8_t)(t >= m);
+    uint32_t m4 = 0;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const int i = i0 + q;
+        const int c = i / hw, pix = i - c * hw;
+        const int yo = pix / Wo, xo = pix - yo * Wo;
+        const int y0 = yo * R - D, x0 = xo * R - D;
+        const int ya = max(y0, 0), yb = min(y0 + P, H), xa = max(x0, 0), xb = min(x0 + P, W);
+        const uint8_t *src = tf + (b * C + c) * (int64_t)H * W;
+        int m = T;
+        if (PW > 0) {
+#pragma unroll
+            for (int dy = 0; dy < PW; ++dy)
+#pragma unroll
+                for (int dx = 0; dx < PW; ++dx) {
+                    const int y = y0 + dy, x = x0 + dx;
+                    const bool in = y >= 0 && y < H && x >= 0 && x < W;
+                    m = min(m, in ? (int)src[y * W + x] : T);
+                }
+        } else {
+            for (int y = ya; y < yb; ++y)
+                for (int x = xa; x < xb; ++x) m = min(m, (int)src[y * W + x]);
+        }
+        m4 |= (uint32_t)m << (8 * q);
+    }
+    if (VEC) {
+        if (out_tf) *reinterpret_cast<uint32_t *>(out_tf + b * per_img + i0) = m4;
+        if (out) {
+            uint8_t *dst = out + b * T * (int64_t)per_img + i0;
+            for (int t = 0; t < T; ++t) {
+                uint32_t w = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) w |= (uint32_t)(t >= (int)((m4 >> (8 * q)) & 255u)) << (8 * q);
+                *reinterpret_cast<uint32_t *>(dst + (int64_t)t * per_img) = w;
+            }
+        }
+    } else {
+        const int m = (int)m4;
+        if (out_tf) out_tf[b * per_img + i0] = (uint8_t)m;
+        if (out) {
+            uint8_t *dst = out + b * T * (int64_t)per_img + i0;
+            for (int t = 0; t < T; ++t) dst[(int64_t)t * per_img] = (uint8_t)(t >= m);
+        }
     }
 }
 
@@ -84,9 +123,17 @@ extern "C" int spk_pool_first_spike(const uint8_t *t_first, int B, int T, int C,
     const int64_t per_img = (int64_t)C * Ho * Wo;
     SPK_REQUIRE(per_img <= 65535LL * 256 && (int64_t)C * H * W < (1LL << 31), SPK_E_RANGE,
                 "spk_pool_first_spike: image too large");
-    hipLaunchKernelGGL(k_pool_first_spike, dim3((unsigned)B, (unsigned)spk::ceil_div(per_img, 256)), dim3(256), 0,
-                       spk::as_stream(stream), t_first, T, C, H, W, kernel, stride, pad, Ho, Wo, out_wave,
-                       out_t_first);
+    const bool vec = per_img % 4 == 0 && ((uintptr_t)out_wave & 3) == 0 && ((uintptr_t)out_t_first & 3) == 0;
+    const dim3 grid((unsigned)B, (unsigned)spk::ceil_div(per_img, vec ? 1024 : 256));
+    hipStream_t st = spk::as_stream(stream);
+#define SPK_POOL(V, PW)                                                                                            \
+    hipLaunchKernelGGL((k_pool_first_spike<V, PW>), grid, dim3(256), 0, st, t_first, T, C, H, W, kernel, stride, pad, \
+                       Ho, Wo, out_wave, out_t_first)
+    if (vec && kernel == 2) SPK_POOL(true, 2);
+    else if (vec && kernel == 3) SPK_POOL(true, 3);
+    else if (vec) SPK_POOL(true, 0);
+    else SPK_POOL(false, 0);
+#undef SPK_POOL
     return spk::check_launch("spk_pool_first_spike");
 }
 
