@@ -39,7 +39,10 @@ constexpr int SORT_THREADS = 1024;
 // LDS holds the taps and the zero-padded band of the image as doubles, so the
 // tap loop has no bounds checks; padded pixels contribute +0 terms, which
 // leave every partial sum unchanged (the sums are never -0), so the result
-// equals the sum over the in-image taps in the same ky-then-kx order.
+// equals the sum over the in-image taps in the same ky-then-kx order.  A
+// thread makes 4 consecutive outputs of a row: along kx it keeps the 4 pixels
+// under the taps in registers and reads one new pixel per tap (3 zero columns
+// pad the band on the right for the last group).
 __global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img, int B, int H, int W,
                                                 const float *__restrict__ filt, int C, int KF, float thr,
                                                 float *__restrict__ out) {
@@ -48,7 +51,7 @@ __global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img,
     const int b = blockIdx.x / nb, band = blockIdx.x % nb;
     const int y0 = band * ROWS, p = (KF - 1) / 2;
     const int rows = min(ROWS, H - y0);
-    const int srows = rows + KF - 1, Wp = W + 2 * p;
+    const int srows = rows + KF - 1, Wp = W + 2 * p + 3;
     double *fd = smem_d;                                       // C*KF*KF taps
     double *sim = fd + C * KF * KF;                            // srows x Wp pixels
     int *bbox = reinterpret_cast<int *>(sim + srows * Wp);     // C x (y0,y1,x0,x1)
@@ -71,20 +74,37 @@ __global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img,
         bbox[4 * c] = ya; bbox[4 * c + 1] = yb; bbox[4 * c + 2] = xa; bbox[4 * c + 3] = xb;
     }
     __syncthreads();
-    const int per = rows * W;
+    const int xg = (W + 3) / 4, per = rows * xg;
     for (int c = 0; c < C; ++c) {
         const int ya = bbox[4 * c], yb = bbox[4 * c + 1], xa = bbox[4 * c + 2], xb = bbox[4 * c + 3];
         const double *fc = fd + c * KF * KF;
         for (int i = threadIdx.x; i < per; i += blockDim.x) {
-            const int r = i / W, x = i - r * W;
-            double s = 0.0;
+            const int r = i / xg, x = (i - r * xg) * 4;
+            double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
             for (int ky = ya; ky <= yb; ++ky) {
                 const double *row = sim + (r + ky) * Wp + x;
                 const double *frow = fc + ky * KF;
-                for (int kx = xa; kx <= xb; ++kx) s += frow[kx] * row[kx];
+                double w0 = row[xa], w1 = row[xa + 1], w2 = row[xa + 2];
+#pragma unroll 4
+                for (int kx = xa; kx <= xb; ++kx) {
+                    const double w3 = row[kx + 3], f = frow[kx];
+                    s0 += f * w0;
+                    s1 += f * w1;
+                    s2 += f * w2;
+                    s3 += f * w3;
+                    w0 = w1;
+                    w1 = w2;
+                    w2 = w3;
+                }
             }
-            const float v = (float)s;
-            out[(((int64_t)b * C + c) * H + y0 + r) * W + x] = (v < thr) ? 0.0f : v;
+            float *o = out + (((int64_t)b * C + c) * H + y0 + r) * W + x;
+            const double sv[4] = {s0, s1, s2, s3};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (x + j < W) {
+                    const float v = (float)sv[j];
+                    o[j] = (v < thr) ? 0.0f : v;
+                }
         }
     }
 }
@@ -445,7 +465,7 @@ extern "C" int spk_encode_latency(const uint8_t *image, int B, int H, int W, con
     float *I = intensities ? intensities : ws_int;
 
     const int nb = (H + ROWS - 1) / ROWS;
-    const size_t lds = ((size_t)C * KF * KF + (size_t)(ROWS + KF - 1) * (W + KF - 1)) * sizeof(double) +
+    const size_t lds = ((size_t)C * KF * KF + (size_t)(ROWS + KF - 1) * (W + KF - 1 + 3)) * sizeof(double) +
                        4 * C * sizeof(int);
     SPK_REQUIRE(lds <= 65536, SPK_E_RANGE, "spk_encode_latency: %d filters of %dx%d on width %d do not fit", C, KF,
                 KF, W);
