@@ -16,11 +16,12 @@ calls on one stream, with no host synchronisation and no allocation inside
   cumulative -- always the case for non-negative weights), or ``spk_pool``
   on the wave when constructed with ``pool_from_first_spike=False``;
 * after a reward-modulated last layer: ``spk_decide``;
-* learning: ``spk_stdp`` / ``spk_rstdp`` per conv stage, all after the
-  forward (frozen-forward, ordered replay within the batch).  The layers'
-  updates touch disjoint weights, so with ``concurrent_learn`` they run on
-  side streams (default priority) that fork from and join back into the
-  caller's stream.
+* learning: ``spk_stdp`` / ``spk_rstdp`` per conv stage (frozen forward,
+  ordered replay within the batch).  The layers' updates touch disjoint
+  weights, so with ``concurrent_learn`` they run on side streams (default
+  priority) that fork from and join back into the caller's stream; in
+  :meth:`Chain.step` the layers up to the second-to-last conv stage fork right
+  after that stage's kWTA, overlapping the rest of the forward.
 
 A stage list is any sequence of objects with the attributes of
 ``Conv(cin, cout, K, pad, thr, k, r, learn, a_plus, a_minus, lb, ub,
@@ -100,8 +101,15 @@ class Chain:
         self.concurrent_learn = concurrent_learn and n_learn > 1
         if self.concurrent_learn:
             self._side = [torch.cuda.Stream(device=dev) for _ in range(n_learn)]
-            self._fork = torch.cuda.Event()
+            self._forks = [torch.cuda.Event(), torch.cuda.Event()]
             self._joins = [torch.cuda.Event() for _ in range(n_learn)]
+        # With concurrent learning, the layers up to the second-to-last conv stage
+        # start their plasticity right after that stage's kWTA (their inputs and
+        # winners are final then, and no later stage reads their weights), so it
+        # overlaps the rest of the forward; the last conv stage's follows it.
+        convs = [i for i, st in enumerate(self.stages) if _is_conv(st)]
+        self._early_at = convs[-2] if self.concurrent_learn and len(convs) >= 2 else None
+        self._launched = set()
 
     # ---------------------------------------------------------------- setup
     def conv_stages(self):
@@ -123,7 +131,7 @@ class Chain:
             self.labels.copy_(labels)
 
     # ---------------------------------------------------------------- run
-    def forward(self, stream=None, hook=None):
+    def forward(self, stream=None, hook=None, early_learn=False):
         """Enqueue the forward of the batch.  hook(name, phase), if given, is
         called right before (phase 0) and after (phase 1) each C-ABI call;
         names are "encode", "conv<i>", "kwta<i>", "pool<i>", "decide"."""
@@ -152,6 +160,8 @@ class Chain:
                 spk_kwta(b["tf"], b["vf"], self.T, st.k, st.r, winners=b["win"], n_winners=b["nw"],
                          workspace=self.workspace, stream=stream)
                 mark(f"kwta{i}", 1)
+                if early_learn and i == self._early_at:
+                    self._launch_learners(lambda ii: ii <= i, self._forks[0], stream)
                 x, x_tf, x_exact = b["S"], b["tf"], False
                 last_conv = i
             else:
@@ -172,40 +182,55 @@ class Chain:
                        stream=stream)
             mark("decide", 1)
 
+    def _learners(self):
+        return [(i, st, b) for i, (st, b) in enumerate(zip(self.stages, self.bufs))
+                if _is_conv(st) and st.learn is not None]
+
+    def _apply(self, i, st, b, s):
+        if st.learn == "rstdp":
+            spk_rstdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], self.reward, st.a_plus,
+                      st.a_minus, st.lb, st.ub, st.stabilizer, workspace=b["ws_learn"], stream=s)
+        else:
+            spk_stdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], st.a_plus, st.a_minus, st.lb,
+                     st.ub, st.stabilizer, workspace=b["ws_learn"], stream=s)
+
+    def _launch_learners(self, which, fork, stream):
+        """Enqueue, each on its side stream forked from the caller's stream at
+        this point, the plasticity of the not yet launched learners i with which(i)."""
+        main = stream if stream is not None else torch.cuda.current_stream()
+        fork.record(main)
+        for j, (i, st, b) in enumerate(self._learners()):
+            if i in self._launched or not which(i):
+                continue
+            s = self._side[j]
+            s.wait_event(fork)
+            self._apply(i, st, b, s)
+            self._joins[j].record(s)
+            self._launched.add(i)
+
     def learn(self, stream=None, hook=None):
-        """Enqueue the plasticity of every learning conv stage (names "stdp<i>",
-        or one "learn" span when the layers run concurrently)."""
+        """Enqueue the plasticity of every learning conv stage not yet started by
+        forward(early_learn=True) (names "stdp<i>", or one "learn" span -- the
+        part not hidden behind the forward -- when the layers run concurrently)."""
         mark = hook or (lambda name, phase: None)
         main = stream if stream is not None else torch.cuda.current_stream()
-        learners = [(i, st, b) for i, (st, b) in enumerate(zip(self.stages, self.bufs))
-                    if _is_conv(st) and st.learn is not None]
         if self.concurrent_learn:
             mark("learn", 0)
-            self._fork.record(main)
-        for j, (i, st, b) in enumerate(learners):
-            s = main
-            if self.concurrent_learn:
-                s = self._side[j]
-                s.wait_event(self._fork)
-            else:
-                mark(f"stdp{i}", 0)
-            if st.learn == "rstdp":
-                spk_rstdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], self.reward, st.a_plus,
-                          st.a_minus, st.lb, st.ub, st.stabilizer, workspace=b["ws_learn"], stream=s)
-            else:
-                spk_stdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], st.a_plus, st.a_minus, st.lb,
-                         st.ub, st.stabilizer, workspace=b["ws_learn"], stream=s)
-            if self.concurrent_learn:
-                self._joins[j].record(s)
+            self._launch_learners(lambda i: True, self._forks[1], stream)
+            for j in range(len(self._learners())):
                 main.wait_event(self._joins[j])
-            else:
-                mark(f"stdp{i}", 1)
-        if self.concurrent_learn:
+            self._launched.clear()
             mark("learn", 1)
+            return
+        for i, st, b in self._learners():
+            mark(f"stdp{i}", 0)
+            self._apply(i, st, b, main)
+            mark(f"stdp{i}", 1)
 
     def step(self, stream=None, hook=None):
-        """One pass of the whole hot path over the batch: forward, then plasticity."""
-        self.forward(stream, hook)
+        """One pass of the whole hot path over the batch: forward, then plasticity
+        (the earlier layers' plasticity overlaps the end of the forward)."""
+        self.forward(stream, hook, early_learn=self.concurrent_learn)
         self.learn(stream, hook)
 
 
