@@ -110,6 +110,9 @@ class Chain:
         convs = [i for i, st in enumerate(self.stages) if _is_conv(st)]
         self._early_at = convs[-2] if self.concurrent_learn and len(convs) >= 2 else None
         self._launched = set()
+        # step(defer_learn=True): learner stage -> its join event, waited for by the next
+        # forward right before the stage that rewrites the learner's input
+        self._pending = {}
 
     # ---------------------------------------------------------------- setup
     def conv_stages(self):
@@ -136,6 +139,8 @@ class Chain:
         called right before (phase 0) and after (phase 1) each C-ABI call;
         names are "encode", "conv<i>", "kwta<i>", "pool<i>", "decide"."""
         mark = hook or (lambda name, phase: None)
+        main = stream if stream is not None else torch.cuda.current_stream()
+        self._wait_pending(-1, main)
         if self.source == "image":
             mark("encode", 0)
             spk_encode_latency(self.image, self.bank, self.T, self.filter_threshold, wave=self.input_wave,
@@ -145,6 +150,7 @@ class Chain:
         x_exact = x_tf is not None  # x is Eq.1 of x_tf
         last_conv = None
         for i, (st, b) in enumerate(zip(self.stages, self.bufs)):
+            self._wait_pending(i, main)
             self.pre_waves[i] = x
             if _is_conv(st):
                 mark(f"conv{i}", 0)
@@ -208,6 +214,17 @@ class Chain:
             self._joins[j].record(s)
             self._launched.add(i)
 
+    def _wait_pending(self, stage, main):
+        """Make `main` wait for the deferred learners of conv stages <= stage + 1
+        (stage i writes the input of conv stage i + 1; -1 stands for the source)."""
+        for i in [i for i in self._pending if i - 1 <= stage]:
+            main.wait_event(self._joins[self._pending.pop(i)])
+
+    def finish(self, stream=None):
+        """Join any plasticity left running by step(defer_learn=True) into the stream."""
+        main = stream if stream is not None else torch.cuda.current_stream()
+        self._wait_pending(len(self.stages), main)
+
     def learn(self, stream=None, hook=None):
         """Enqueue the plasticity of every learning conv stage not yet started by
         forward(early_learn=True) (names "stdp<i>", or one "learn" span -- the
@@ -227,11 +244,23 @@ class Chain:
             self._apply(i, st, b, main)
             mark(f"stdp{i}", 1)
 
-    def step(self, stream=None, hook=None):
+    def step(self, stream=None, hook=None, defer_learn=False):
         """One pass of the whole hot path over the batch: forward, then plasticity
-        (the earlier layers' plasticity overlaps the end of the forward)."""
+        (the earlier layers' plasticity overlaps the end of the forward).  With
+        defer_learn (and concurrent learning) the plasticity is not joined at the
+        end of the step: the next forward waits for each layer's update right
+        before the stage that rewrites that layer's input (and so before the
+        layer's conv), so the last layer's update overlaps the next batch's first
+        layers; call finish() (or synchronize the device) before reading weights.
+        The results are those of joined steps."""
         self.forward(stream, hook, early_learn=self.concurrent_learn)
-        self.learn(stream, hook)
+        if not (defer_learn and self.concurrent_learn):
+            self.learn(stream, hook)
+            return
+        self._launch_learners(lambda i: True, self._forks[1], stream)
+        for j, (i, st, b) in enumerate(self._learners()):
+            self._pending[i] = j
+        self._launched.clear()
 
 
 def chain_for(workload, filter_bank=None, device="cuda", **kw):

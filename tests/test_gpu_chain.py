@@ -237,3 +237,29 @@ def test_full_size_stress_large_sampled():
         if f not in used:
             assert np.array_equal(Wn[f], W0[f])
     assert Wn.min() >= 0 and Wn.max() <= 1
+
+
+@pytest.mark.parametrize("defer", [False, True])
+def test_steps_in_a_row_match_joined_steps(defer):
+    # three steps of the 3-layer chain with the plasticity joined at every step end, and
+    # with it deferred into the next step (joined before the stage that rewrites each
+    # layer's input): identical weights and winners, bit for bit
+    wl = synth.WORKLOADS[2](48)
+    inp = synth.make_inputs(wl)
+
+    def run(defer_learn):
+        ch = chain_for(wl, inp["bank"])
+        ch.set_weights([torch.from_numpy(w) for w in inp["weights"]])
+        ch.set_input(image=torch.from_numpy(inp["image"]), labels=torch.from_numpy(inp["labels"]))
+        for _ in range(3):
+            ch.step(defer_learn=defer_learn)
+        ch.finish()
+        torch.cuda.synchronize()
+        return [w.cpu() for w in ch.weights()], [ch.bufs[i]["win"].cpu() for i in ch.conv_stages()]
+
+    w_ref, win_ref = run(False)
+    w_got, win_got = run(defer)
+    for a, b in zip(w_got, w_ref):
+        assert torch.equal(a, b)
+    for a, b in zip(win_got, win_ref):
+        assert torch.equal(a, b)
