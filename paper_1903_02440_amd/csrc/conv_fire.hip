@@ -399,8 +399,8 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             }
             const bool has_next = ALDS && task + R < t_hi;
             if (has_next) fill_region(task + R, abuf + (abuf_sel ^ 1) * a_words);  // read from the next task on
-            for (int tb0 = 0; tb0 < g.T; tb0 += FIN_TB) {
-                const bool last_block = tb0 + FIN_TB >= g.T;
+            for (int tb0 = (g.T - 1) / FIN_TB * FIN_TB; tb0 >= 0; tb0 -= FIN_TB) {  // latest steps first
+                const bool last_block = tb0 == 0;
                 f4 acc[FIN_MT][2][FIN_TB];
 #pragma unroll
                 for (int i = 0; i < FIN_MT; ++i)
@@ -537,19 +537,20 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 off[m] = e < nel ? (b - b0) * g.T * (int)tplane + fl * g.HoWo + pos : -1;
                 src[m] = e < nel ? fl * stage_stride(np) + pl : 0;
             }
-            int tfirst[NSLOT][G];
+            // The steps arrive latest first, so the first spike is the last firing
+            // seen: tf (4 bytes per slot) and vf are overwritten on every firing.
+            uint32_t tf4[NSLOT];
             float vfirst[NSLOT][G];
 #pragma unroll
-            for (int m = 0; m < NSLOT; ++m)
+            for (int m = 0; m < NSLOT; ++m) {
+                tf4[m] = (uint32_t)g.T * 0x01010101u;
 #pragma unroll
-                for (int q = 0; q < G; ++q) {
-                    tfirst[m][q] = g.T;
-                    vfirst[m][q] = 0.0f;
-                }
-            for (int tb0 = 0; tb0 < g.T; tb0 += FIN_TB) {
+                for (int q = 0; q < G; ++q) vfirst[m][q] = 0.0f;
+            }
+            for (int tb0 = (g.T - 1) / FIN_TB * FIN_TB; tb0 >= 0; tb0 -= FIN_TB) {
                 __syncthreads();  // staging free
                 __syncthreads();  // staging full
-                for (int t = 0; t < FIN_TB && tb0 + t < g.T; ++t) {
+                for (int t = min(FIN_TB, g.T - tb0) - 1; t >= 0; --t) {
                     const int tt = tb0 + t;
                     const float *st = stage + t * stage_t;
                     float *Pt = P ? P + base0 + (int64_t)tt * tplane : nullptr;
@@ -566,15 +567,15 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                         } else {
                             v[0] = st[src[m]];
                         }
-                        uint32_t sp = 0;
+                        uint32_t bm = 0;  // 0xFF in the bytes that fire
 #pragma unroll
                         for (int q = 0; q < G; ++q) {
                             const bool fire = v[q] >= g.thr;
-                            const bool first = fire && tfirst[m][q] == g.T;
-                            tfirst[m][q] = first ? tt : tfirst[m][q];
-                            vfirst[m][q] = first ? v[q] : vfirst[m][q];
-                            sp |= fire ? (1u << (8 * q)) : 0u;
+                            vfirst[m][q] = fire ? v[q] : vfirst[m][q];
+                            bm |= fire ? (0xFFu << (8 * q)) : 0u;
                         }
+                        const uint32_t sp = bm & 0x01010101u;
+                        tf4[m] = (tf4[m] & ~bm) | ((uint32_t)tt * 0x01010101u & bm);
                         if (G == 4) {
                             if (Pt) *reinterpret_cast<f4 *>(Pt + o) = f4{v[0], v[1], v[2], v[3]};
                             if (St) *reinterpret_cast<uint32_t *>(St + o) = sp;
@@ -596,13 +597,10 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 uint8_t *TFt = TF;
                 float *VFt = VF;
                 if (G == 4) {
-                    uint32_t tv = 0;
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) tv |= (uint32_t)tfirst[m][q] << (8 * q);
-                    *reinterpret_cast<uint32_t *>(TFt + o) = tv;
+                    *reinterpret_cast<uint32_t *>(TFt + o) = tf4[m];
                     *reinterpret_cast<f4 *>(VFt + o) = f4{vfirst[m][0], vfirst[m][1], vfirst[m][2], vfirst[m][3]};
                 } else {
-                    TFt[o] = (uint8_t)tfirst[m][0];
+                    TFt[o] = (uint8_t)tf4[m];
                     VFt[o] = vfirst[m][0];
                 }
             }
