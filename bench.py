@@ -27,18 +27,19 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 
 
-def conv_call_bytes(B, T, cin, h, w, st, from_times):
+def conv_call_bytes(B, T, cin, h, w, st, from_times, write_p=True, write_s=True):
     """Algorithmic bytes of one conv call: read the input (its first-spike map
     when the call takes that, spk_conv_fire_first_spike, else the T planes of
     the wave) and the weights once, write potentials + spikes for every step
     and the first-spike time + potential once."""
     ho, wo = h + 2 * st.pad - st.K + 1, w + 2 * st.pad - st.K + 1
     return ((1 if from_times else T) * B * cin * h * w + st.cout * cin * st.K * st.K * 4
-            + B * T * st.cout * ho * wo * 5 + B * st.cout * ho * wo * 5), ho, wo
+            + B * T * st.cout * ho * wo * (4 * write_p + write_s) + B * st.cout * ho * wo * 5), ho, wo
 
 
-def step_bytes(wl):
-    """Algorithmic bytes of every call of one step, by call name."""
+def step_bytes(wl, compact=False):
+    """Algorithmic bytes of every call of one step, by call name (compact: the
+    chain writes no potentials, and per-step spikes only where a stage reads them)."""
     B, T = wl.B, wl.T
     out = {}
     c, h, w = (6 if wl.bank == "dog" else 4) if wl.source == "image" else wl.cin, wl.H, wl.W
@@ -47,7 +48,9 @@ def step_bytes(wl):
     exact = wl.source == "image"  # the chain feeds a conv the first-spike map of an Eq.1 wave
     for i, st in enumerate(wl.stages):
         if hasattr(st, "cout"):
-            nb, ho, wo = conv_call_bytes(B, T, c, h, w, st, exact)
+            nxt = wl.stages[i + 1] if i + 1 < len(wl.stages) else None
+            spikes_read = nxt is not None and hasattr(nxt, "cout")
+            nb, ho, wo = conv_call_bytes(B, T, c, h, w, st, exact, not compact, not compact or spikes_read)
             exact = False
             out[f"conv{i}"] = nb
             out[f"kwta{i}"] = B * st.cout * ho * wo * 5 + B * st.k * 16
@@ -141,6 +144,9 @@ def main():
     ap.add_argument("--workload", type=int, default=2, help="1..5 (2 = the 3-layer network, the headline)")
     ap.add_argument("--batch", type=int, default=None, help="override the workload's batch")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle baseline budget (0 = skip)")
+    ap.add_argument("--compact", action="store_true",
+                    help="the compact inter-layer form: no per-step potentials and no unread per-step spikes "
+                         "(a separate figure, not the contract number)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 5 times (the reference "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -165,7 +171,8 @@ def main():
     inp = synth.make_inputs(wl)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    ch = chain_for(wl, inp.get("bank"), device=dev)
+    ch = chain_for(wl, inp.get("bank"), device=dev, want_potentials=not args.compact,
+                   want_spikes=not args.compact)
     ch.set_weights([torch.from_numpy(w) for w in inp["weights"]])
     labels = torch.from_numpy(inp["labels"])
     if wl.source == "image":
@@ -174,7 +181,7 @@ def main():
         ch.set_input(wave=spk.spk_expand_wave(torch.from_numpy(inp["t_first"]).to(dev), wl.T), labels=labels)
     torch.cuda.synchronize()
 
-    nbytes = step_bytes(wl)
+    nbytes = step_bytes(wl, args.compact)
     convs = [k for k in nbytes if k.startswith("conv")]
     dominant = max(convs, key=lambda k: nbytes[k])
 
@@ -221,7 +228,7 @@ def main():
 
     ms_per_step = 1000.0 * elapsed / args.steps
     achieved = nbytes[dominant] / (dom_avg_ms * 1e-3) / 1e9
-    traffic = read_traffic(wl.name, dominant)
+    traffic = None if args.compact else read_traffic(wl.name, dominant)
     total_bytes = sum(nbytes.values())
     rec = {
         "metric": "images/sec and synaptic events/sec (conv_fire+kWTA+STDP) on 1 MI355X",
@@ -239,7 +246,10 @@ def main():
         "config": {"workload": wl.name, "global_batch": wl.B, "T": wl.T,
                    "layers": [f"conv {s.cin}->{s.cout} k{s.K} p{s.pad} thr {s.thr} kwta {s.k}/{s.r} {s.learn}"
                               if hasattr(s, "cout") else f"pool {s.P}/{s.R}" for s in wl.stages],
-                   "source": wl.source + (f" ({wl.bank})" if wl.bank else ""), "parallelism": "none (1 GPU)"},
+                   "source": wl.source + (f" ({wl.bank})" if wl.bank else ""), "parallelism": "none (1 GPU)",
+                   "form": ("compact: conv layers write first-spike maps only (no per-step potentials; "
+                            "per-step spikes only where a stage reads them)" if args.compact
+                            else "contract: every call writes its full outputs")},
         "synaptic_events_per_s": round(ev * args.steps / elapsed, 1),
         "synaptic_events_per_step": ev,
         "roofline": {"bound": "hbm", "kernel": f"spk_conv_fire ({dominant}: pad-first-spike + weight split + "

@@ -46,7 +46,7 @@ def _is_conv(st):
 class Chain:
     def __init__(self, stages, B, T, H, W, cin, source="image", filter_bank=None, filter_threshold=0.0,
                  n_classes=10, device="cuda", want_potentials=True, pool_from_first_spike=True,
-                 concurrent_learn=True):
+                 concurrent_learn=True, want_spikes=True):
         self.stages = list(stages)
         self.pool_from_first_spike = pool_from_first_spike
         self.B, self.T, self.source = B, T, source
@@ -67,13 +67,18 @@ class Chain:
         self.input_tf = torch.zeros((B, C, H, W), dtype=u8, device=dev) if source == "image" else None
         self.bufs = []
         c, h, w = C, H, W
-        for st in self.stages:
+        for si, st in enumerate(self.stages):
             b = {}
             if _is_conv(st):
                 assert st.cin == c, "stage input channels do not match"
                 ho, wo = conv_out_size(h, st.K, st.pad), conv_out_size(w, st.K, st.pad)
                 b["P"] = torch.empty((B, T, st.cout, ho, wo), dtype=f32, device=dev) if want_potentials else False
-                b["S"] = torch.empty((B, T, st.cout, ho, wo), dtype=u8, device=dev)
+                # without want_spikes a conv stage's per-step spikes are written only when the next
+                # stage reads them (a conv, or a pool on waves); the first-spike map always is
+                nxt = self.stages[si + 1] if si + 1 < len(self.stages) else None
+                spikes_read = nxt is not None and (_is_conv(nxt) or not pool_from_first_spike)
+                b["S"] = (torch.empty((B, T, st.cout, ho, wo), dtype=u8, device=dev) if want_spikes or spikes_read
+                          else False)
                 b["tf"] = torch.empty((B, st.cout, ho, wo), dtype=u8, device=dev)
                 b["vf"] = torch.empty((B, st.cout, ho, wo), dtype=f32, device=dev)
                 b["win"] = torch.empty((B, st.k, 4), dtype=i32, device=dev)

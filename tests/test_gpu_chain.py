@@ -263,3 +263,23 @@ def test_steps_in_a_row_match_joined_steps(defer):
         assert torch.equal(a, b)
     for a, b in zip(win_got, win_ref):
         assert torch.equal(a, b)
+
+
+def test_compact_chain_matches_full_chain():
+    # the compact inter-layer form (no per-step potentials, per-step spikes only where a
+    # stage reads them) gives the full chain's first-spike maps, winners, decisions and
+    # updated weights, bit for bit
+    wl = synth.WORKLOADS[2](40)
+    inp = synth.make_inputs(wl)
+
+    def run(compact):
+        ch = chain_for(wl, inp["bank"], want_potentials=not compact, want_spikes=not compact)
+        ch.set_weights([torch.from_numpy(w) for w in inp["weights"]])
+        ch.set_input(image=torch.from_numpy(inp["image"]), labels=torch.from_numpy(inp["labels"]))
+        ch.step()
+        torch.cuda.synchronize()
+        out = [ch.bufs[i][k].cpu() for i in ch.conv_stages() for k in ("tf", "vf", "win", "nw")]
+        return out + [w.cpu() for w in ch.weights()] + [ch.decision.cpu(), ch.reward.cpu()]
+
+    for a, b in zip(run(True), run(False)):
+        assert torch.equal(a, b)
