@@ -624,9 +624,14 @@ constexpr int INF_MW = 2;   // position tiles per wave
 constexpr int INF_NW = 4;   // 16-feature tiles per workgroup
 constexpr int INF_KC = 8;   // K-steps per LDS chunk
 constexpr int INF_CHUNK_U4 = INF_KC * INF_NW * 2 * 64;  // uint4 per chunk buffer
+constexpr int INF_ZW = 4;   // zero waves (waves 8-11)
 
+// With VEC, INF_ZW more waves write the zero planes of steps 0..T-2 (potentials
+// and spikes of images blockIdx.x, blockIdx.x + gridDim.x, ...) while the MFMA
+// waves compute: they pass the same barriers, one slice of their stores between
+// two barriers.
 template <bool VEC>
-__global__ __launch_bounds__(INF_WAVES * 64, 1) void k_conv_fire_inf(
+__global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
     const int2 *__restrict__ koff2, ConvGeom g, int n_mb, int n_ng, const float *__restrict__ inv_scale,
     float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF) {
@@ -635,7 +640,7 @@ __global__ __launch_bounds__(INF_WAVES * 64, 1) void k_conv_fire_inf(
     uint4 *cbuf = lds + (g.ksteps * 4 * 8 + 15) / 16;  // 2 chunk buffers [ksl][n][hi/lo][64]
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int gq = lane >> 4, c = lane & 15;
-    for (int i = tid; i < g.ksteps * 4; i += INF_WAVES * 64) koff_l[i] = koff2[i];
+    for (int i = tid; i < g.ksteps * 4; i += (INF_WAVES + INF_ZW) * 64) koff_l[i] = koff2[i];
     const float inv_s = *inv_scale;
     const uint32_t ct = step_const(g.T - 1);
     const int nchunks = (g.ksteps + INF_KC - 1) / INF_KC;
@@ -643,6 +648,42 @@ __global__ __launch_bounds__(INF_WAVES * 64, 1) void k_conv_fire_inf(
     const int ntask = n_mb * n_ng, per_x = (ntask + 7) / 8;
     const int t_lo = x * per_x, t_hi = min(ntask, t_lo + per_x);
     const int64_t tstride = (int64_t)g.Cout * g.HoWo;
+
+    if (wv >= INF_WAVES) {
+        // zero waves: 16-byte units of potentials (4 per unit) and 4-byte units of spikes
+        // (4 per unit); images b = blockIdx.x + i * gridDim.x; one slice per barrier interval
+        const int zt = tid - INF_WAVES * 64;
+        const int64_t zp = VEC && P && g.T > 1 ? (g.T - 1) * tstride / 4 : 0;  // units per image
+        const int64_t zs = VEC && S && g.T > 1 ? (g.T - 1) * tstride / 4 : 0;
+        const int64_t nimg = g.B > (int)blockIdx.x ? (g.B - 1 - (int)blockIdx.x) / gridDim.x + 1 : 0;
+        const int64_t total = nimg * (zp + zs);
+        const int ntk = t_lo + j < t_hi ? (t_hi - 1 - (t_lo + j)) / per_xcd + 1 : 0;
+        const int nint = ntk * (1 + nchunks) + 1;  // barrier intervals (the last one after the loop)
+        const int64_t per = (total + nint - 1) / nint;
+        int64_t u0 = 0;
+        auto slice = [&]() {
+            const int64_t u1 = min(total, u0 + per);
+            for (int64_t u = u0 + zt; u < u1; u += INF_ZW * 64) {
+                const int64_t im = u / (zp + zs), r = u - im * (zp + zs);
+                const int64_t b = blockIdx.x + im * gridDim.x;
+                if (r < zp)
+                    *reinterpret_cast<f4 *>(P + b * g.T * tstride + 4 * r) = f4{0.f, 0.f, 0.f, 0.f};
+                else
+                    *reinterpret_cast<uint32_t *>(S + b * g.T * tstride + 4 * (r - zp)) = 0u;
+            }
+            u0 = u1;
+        };
+        for (int tk = 0; tk < ntk; ++tk) {
+            slice();
+            __syncthreads();  // the MFMA waves' "buffers free"
+            for (int ch = 0; ch < nchunks; ++ch) {
+                slice();
+                __syncthreads();  // the MFMA waves' chunk barrier
+            }
+        }
+        slice();
+        return;
+    }
 
     for (int task = t_lo + j; task < t_hi; task += per_xcd) {
         const int ng = task / n_mb, mb = task % n_mb;
@@ -911,13 +952,13 @@ void launch_inf(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const i
     const int n_mb = (int)spk::ceil_div(g.total_mtiles, INF_WAVES * INF_MW);
     const int n_ng = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), INF_NW);
     const size_t lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16) + 2 * (size_t)INF_CHUNK_U4 * 16;
-    if (g.T > 1 && (P || S)) {
+    if (!VEC && g.T > 1 && (P || S)) {  // (with VEC the conv kernel's zero waves write them)
         const int64_t n = (int64_t)(g.T - 1) * g.Cout * g.HoWo;
         const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>(64, spk::ceil_div(n, 256 * 16)));
         hipLaunchKernelGGL(k_zero_planes, dim3(gx, (unsigned)std::min(g.B, 65535)), dim3(256), 0, st, g, P, S);
     }
-    hipLaunchKernelGGL((k_conv_fire_inf<VEC>), dim3(256), dim3(INF_WAVES * 64), lds, st, tpad, whi, wlo, koff2, g, n_mb,
-                       n_ng, inv_scale, P, S, TF, VF);
+    hipLaunchKernelGGL((k_conv_fire_inf<VEC>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad, whi, wlo,
+                       koff2, g, n_mb, n_ng, inv_scale, P, S, TF, VF);
 }
 
 }  // namespace
