@@ -10,9 +10,12 @@
 //     bits 63..56  255 - t_first          (earlier spike wins)
 //     bits 55..24  v_first, order-mapped  (larger potential wins)
 //     bits 23..0   2^24 - 1 - index       (lower linear index wins ties)
-// Silent neurons get key 0.  Small maps use tiles of 16 consecutive positions
-// and one 256-thread workgroup per image (see "small maps" below); large maps cut each
-// feature map into tiles of RB rows:
+// Silent neurons get key 0.  Three paths, by size:
+//   * k <= 16 with per-position lists that fit in LDS: the k best keys of every
+//     position, then k rounds without global reads ("per-position top-k");
+//   * other small maps: tiles of 16 consecutive positions and one 256-thread
+//     workgroup per image ("small maps");
+//   * large maps cut each feature map into tiles of RB rows:
 //   1. k_kwta_tiles: the maximum key of every tile (a group of G lanes per
 //      tile, shuffle reduction), written to the workspace.
 //   2. k_kwta_select: one workgroup per image keeps its tile keys in LDS and
@@ -389,6 +392,230 @@ __global__ __launch_bounds__(SMALL_THREADS) void k_kwta_select_small(const uint8
     if (tid == 0) n_winners[b] = found;
 }
 
+// ------------------------------------------------------------ per-position top-k
+// When k <= 16 and each image's lists fit in LDS, one workgroup per image
+// first keeps, for every position, the k largest keys over all feature maps:
+// one pass over the image's neurons, with each position owned by one thread
+// (on maps of few positions, the feature maps are split among up to
+// TOPK_THREADS / HW threads per position, whose lists the owner then merges).
+// The rounds never read global memory again.  At round j at most j features
+// are retired, so a position's best live key is among its first j + 1 list
+// entries: the owner skips entries of retired features with a per-position
+// cursor, and marks its position inhibited when it falls in a winner's
+// window.  Only the per-round maximum crosses threads.
+constexpr int TOPK_THREADS = 256;       // most threads per workgroup
+constexpr int TOPK_MAX_K = 16;
+constexpr size_t TOPK_LDS = 40 * 1024;  // lists and cursors (the stash adds 16 KB)
+constexpr int TOPK_U = 8;               // feature maps loaded per block
+constexpr int TOPK_STASH_MIN = 64;      // features per split from which the stash pays
+
+struct KwtaTopk {
+    int B, T, C, HW, W, k, r;
+    int S, fps;  // feature splits per position (small maps) and features per split
+    int nt;      // threads per workgroup
+    unsigned mHW, mW;
+};
+
+// Inserts key into the descending list top (keys are unique; the caller has
+// checked key > top[KM - 1], so the last entry drops out).
+template <int KM>
+__device__ __forceinline__ void topk_insert(uint64_t (&top)[KM], uint64_t key) {
+#pragma unroll
+    for (int i = KM - 1; i > 0; --i) {
+        const bool above = key > top[i - 1];
+        const bool here = key > top[i];
+        top[i] = above ? top[i - 1] : (here ? key : top[i]);
+    }
+    top[0] = key > top[0] ? key : top[0];
+}
+
+template <int KM, int U, bool STASH>
+__global__ __launch_bounds__(TOPK_THREADS) void k_kwta_topk(const uint8_t *__restrict__ tf_all,
+                                                            const float *__restrict__ vf_all, KwtaTopk g,
+                                                            int32_t *__restrict__ winners,
+                                                            int32_t *__restrict__ n_winners) {
+    extern __shared__ uint64_t lists[];  // [S][HW][KM] keys, then [HW] cursors
+    uint8_t *cur = reinterpret_cast<uint8_t *>(lists + (size_t)g.S * g.HW * KM);
+    __shared__ uint64_t red[2][TOPK_THREADS / 64];
+    __shared__ uint64_t stash[STASH ? U : 1][TOPK_THREADS];  // a block's keys, read back by their own lane
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int NT = blockDim.x, NW = NT >> 6;
+    const int HW = g.HW, S = g.S;
+    const int64_t N = (int64_t)g.C * HW;
+    const uint8_t *tf = tf_all + (int64_t)b * N;
+    const float *vf = vf_all + (int64_t)b * N;
+    int32_t *win = winners + (int64_t)b * g.k * 4;
+    for (int i = tid; i < 4 * g.k; i += NT) win[i] = -1;
+
+    // pass over the image: the KM best keys of every (position, feature split)
+    for (int pp = tid; pp < HW * S; pp += NT) {
+        const int s = (int)qdiv((unsigned)pp, g.mHW), p = pp - s * HW;
+        uint64_t top[KM];
+#pragma unroll
+        for (int i = 0; i < KM; ++i) top[i] = 0;
+        const int fa = s * g.fps, fb = min(g.C, fa + g.fps);
+        for (int f0 = fa; f0 < fb; f0 += U) {
+            int tv[U];
+            float vv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const bool ok = f0 + u < fb;
+                const int o = (f0 + u) * HW + p;
+                tv[u] = ok ? (int)tf[o] : g.T;
+                vv[u] = ok ? vf[o] : 0.0f;
+            }
+            if constexpr (STASH) {
+                // the keys that beat the list's last entry are inserted after the
+                // block, each lane walking only its own: the wave then loops as
+                // often as its busiest lane rather than once per key any lane keeps
+                unsigned pass = 0;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const uint64_t key = tv[u] < g.T ? kwta_key(tv[u], vv[u], (uint32_t)((f0 + u) * HW + p)) : 0;
+                    stash[u][tid] = key;
+                    pass |= (key > top[KM - 1] ? 1u : 0u) << u;
+                }
+                while (pass) {
+                    const int j = __builtin_ctz(pass);
+                    pass &= pass - 1;
+                    const uint64_t key = stash[j][tid];
+                    if (key > top[KM - 1]) topk_insert(top, key);
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    if (tv[u] < g.T) {
+                        const uint64_t key = kwta_key(tv[u], vv[u], (uint32_t)((f0 + u) * HW + p));
+                        if (key > top[KM - 1]) topk_insert(top, key);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < KM; ++i) lists[(size_t)pp * KM + i] = top[i];
+    }
+    if (S > 1) {  // uniform
+        __syncthreads();
+        // owners fold the other splits' lists into their own
+        for (int p = tid; p < HW; p += NT) {
+            uint64_t top[KM];
+#pragma unroll
+            for (int i = 0; i < KM; ++i) top[i] = lists[(size_t)p * KM + i];
+            for (int s = 1; s < S; ++s)
+                for (int e = 0; e < KM; ++e) {
+                    const uint64_t key = lists[((size_t)s * HW + p) * KM + e];
+                    if (!(key > top[KM - 1])) break;  // the split's list is sorted
+                    topk_insert(top, key);
+                }
+#pragma unroll
+            for (int i = 0; i < KM; ++i) lists[(size_t)p * KM + i] = top[i];
+        }
+    }
+    for (int p = tid; p < HW; p += NT) cur[p] = 0;
+
+    int deadf[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) deadf[j] = -1;
+    int found = 0;
+    for (int round = 0; round < g.k; ++round) {
+        uint64_t m = 0;
+        for (int p = tid; p < HW; p += NT) {
+            int c = cur[p];
+            if (c == 0xFF) continue;  // laterally inhibited
+            const int c0 = c;
+            uint64_t key = 0;
+            for (; c < KM; ++c) {
+                key = lists[(size_t)p * KM + c];
+                if (key == 0) break;
+                const int f = (int)qdiv(0xFFFFFFu - (unsigned)(key & 0xFFFFFFu), g.mHW);
+                bool dead = false;
+#pragma unroll
+                for (int j = 0; j < KM; ++j) dead |= deadf[j] == f;
+                if (!dead) break;
+                key = 0;
+            }
+            if (c != c0) cur[p] = (uint8_t)c;
+            m = key > m ? key : m;
+        }
+        m = spk::wave_max_u64(m);
+        if (lane == 0) red[round & 1][wv] = m;
+        __syncthreads();
+        uint64_t best = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) best = red[round & 1][w] > best ? red[round & 1][w] : best;
+        if (best == 0) break;  // uniform
+        const int idx = (int)(0xFFFFFFu - (unsigned)(best & 0xFFFFFFu));
+        const int t = 255 - (int)(best >> 56);
+        const int fw = (int)qdiv((unsigned)idx, g.mHW);
+        const int pos = idx - fw * HW;
+        const int yw = (int)qdiv((unsigned)pos, g.mW);
+        const int xw = pos - yw * g.W;
+        if (tid == 0) {
+            win[4 * round + 0] = fw;
+            win[4 * round + 1] = t;
+            win[4 * round + 2] = yw;
+            win[4 * round + 3] = xw;
+        }
+#pragma unroll
+        for (int j = 0; j < KM; ++j)
+            if (j == found) deadf[j] = fw;
+        ++found;
+        for (int p = tid; p < HW; p += NT) {
+            const int y = (int)qdiv((unsigned)p, g.mW), x = p - y * g.W;
+            if (abs(y - yw) <= g.r && abs(x - xw) <= g.r) cur[p] = 0xFF;
+        }
+    }
+    if (tid == 0) n_winners[b] = found;
+}
+
+bool kwta_topk(int B, int T, int C, int H, int W, int k, int r, KwtaTopk &s) {
+    const int64_t HW = (int64_t)H * W;
+    if (k > TOPK_MAX_K || HW > 65536) return false;
+    // maps of few positions split the feature maps among up to TOPK_THREADS / HW threads per position
+    int S = HW <= TOPK_THREADS ? (int)std::min<int64_t>(C, TOPK_THREADS / HW) : 1;
+    const int fps = (C + S - 1) / S;
+    S = (C + fps - 1) / fps;
+    // threads: whole waves covering HW * S in as few passes as TOPK_THREADS allows
+    const int64_t work = HW * S, passes = (work + TOPK_THREADS - 1) / TOPK_THREADS;
+    const int nt = (int)(((work + passes - 1) / passes + 63) / 64 * 64);
+    if ((size_t)HW * (S * k * sizeof(uint64_t) + 1) > TOPK_LDS) return false;
+    auto magic = [](int64_t d) {  // 0 for d == 1 (see qdiv)
+        return d == 1 ? 0u : (unsigned)(((1ULL << 32) + (uint64_t)d - 1) / (uint64_t)d);
+    };
+    auto exact = [](int64_t d, int64_t n) {  // umulhi(x, ceil(2^32/d)) == x/d for all x < n
+        const uint64_t m = ((1ULL << 32) + (uint64_t)d - 1) / (uint64_t)d;
+        const uint64_t e = m * (uint64_t)d - (1ULL << 32);
+        return (uint64_t)n * e < (1ULL << 32);
+    };
+    if (!exact(HW, (int64_t)C * HW) || !exact(W, HW)) return false;
+    s = KwtaTopk{B, T, C, (int)HW, W, k, r, S, fps, nt, magic(HW), magic(W)};
+    return true;
+}
+
+template <int KM>
+void launch_topk(const KwtaTopk &s, const uint8_t *tf, const float *vf, int32_t *winners, int32_t *nw,
+                 hipStream_t st) {
+    const size_t lds = (size_t)s.HW * (s.S * KM * sizeof(uint64_t) + 1);
+    if (s.fps >= TOPK_STASH_MIN)
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_kwta_topk<KM, TOPK_U, true>), dim3(s.B), dim3(s.nt), lds, st, tf, vf, s,
+                           winners, nw);
+    else
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_kwta_topk<KM, TOPK_U, false>), dim3(s.B), dim3(s.nt), lds, st, tf, vf, s,
+                           winners, nw);
+}
+
+void dispatch_topk(const KwtaTopk &s, const uint8_t *tf, const float *vf, int32_t *winners, int32_t *nw,
+                   hipStream_t st) {
+    switch (s.k) {
+#define SPK_TOPK(K) \
+    case K: launch_topk<K>(s, tf, vf, winners, nw, st); break;
+        SPK_TOPK(1) SPK_TOPK(2) SPK_TOPK(3) SPK_TOPK(4) SPK_TOPK(5) SPK_TOPK(6) SPK_TOPK(7) SPK_TOPK(8)
+        SPK_TOPK(9) SPK_TOPK(10) SPK_TOPK(11) SPK_TOPK(12) SPK_TOPK(13) SPK_TOPK(14) SPK_TOPK(15) SPK_TOPK(16)
+#undef SPK_TOPK
+        default: break;
+    }
+}
+
 bool kwta_small(int B, int T, int C, int H, int W, int k, int r, KwtaSmall &s) {
     const int64_t HW = (int64_t)H * W;
     const int64_t tpm = (HW + 15) / 16;
@@ -457,6 +684,11 @@ extern "C" int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int
                 ws_bytes, need);
     hipStream_t st = spk::as_stream(stream);
     uint64_t *tilekey = static_cast<uint64_t *>(workspace);
+    KwtaTopk tk;
+    if (kwta_topk(B, T, C, H, W, k, radius, tk)) {
+        dispatch_topk(tk, t_first, v_first, winners, n_winners, st);
+        return spk::check_launch("spk_kwta");
+    }
     KwtaSmall sm;
     if (kwta_small(B, T, C, H, W, k, radius, sm)) {
         const int64_t threads = (int64_t)B * sm.ntiles * 4;

@@ -186,9 +186,14 @@ def test_pool_toy_t2(golden):
 
 
 # ---------------------------------------------------------------- kWTA
+# (B, T, C, H, W, k, radius).  Per-position top-k path: the first five, the
+# 1x1 and 1x9 maps, (300 maps of 10x10: feature split with the stash) and
+# (k = 16); 16-position tiles: (40x300 maps), (k = 20 > 16) and (k = 16 with
+# lists beyond LDS); row tiles: test_kwta_large_tiles.
 KWTA_CASES = [(4, 15, 30, 28, 28, 5, 3), (3, 15, 250, 14, 14, 8, 1), (6, 15, 200, 4, 4, 1, 0),
               (2, 30, 20, 10, 25, 1, 5), (3, 4, 3, 5, 7, 12, 1), (2, 15, 5, 40, 300, 6, 2),
-              (3, 15, 40, 1, 1, 4, 0), (2, 15, 7, 1, 9, 3, 1)]
+              (3, 15, 40, 1, 1, 4, 0), (2, 15, 7, 1, 9, 3, 1), (2, 15, 300, 10, 10, 8, 2),
+              (2, 15, 64, 6, 6, 16, 1), (2, 15, 30, 12, 12, 20, 1), (2, 15, 20, 30, 40, 16, 0)]
 
 
 def kwta_inputs(seed, B, T, C, H, W, ties=True):
