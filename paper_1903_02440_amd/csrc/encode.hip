@@ -8,7 +8,8 @@
 //   1. k_filter: same-size cross-correlation of each u8 image with the C
 //      filters (double accumulation over the non-zero taps, one rounding to
 //      float, then values below the threshold set to 0).  One workgroup per
-//      (image, band of 8 rows) stages the zero-padded band in LDS.
+//      (image, band of rows: the whole image when it fits) stages the
+//      zero-padded band in LDS and computes all channels.
 //   2. k_rank_select: one workgroup per image finds the T-1 bin boundaries of
 //      the rank-order code by an MSD radix select (8 passes of 8 bits) on the
 //      unique 64-bit keys  (float bits of I) << 32 | ~index  of the positive
@@ -27,7 +28,6 @@
 
 namespace {
 
-constexpr int ROWS = 8;          // filter rows per workgroup
 constexpr int MAX_KF = 31;
 constexpr int SEL_THREADS = 1024;
 constexpr int MAX_GROUPS = 32;   // bin boundaries resolved per select batch
@@ -40,72 +40,91 @@ constexpr int SORT_THREADS = 1024;
 // tap loop has no bounds checks; padded pixels contribute +0 terms, which
 // leave every partial sum unchanged (the sums are never -0), so the result
 // equals the sum over the in-image taps in the same ky-then-kx order.  A
-// thread makes 4 consecutive outputs of a row: along kx it keeps the 4 pixels
-// under the taps in registers and reads one new pixel per tap (3 zero columns
-// pad the band on the right for the last group).
+// workgroup covers a band of R rows (the whole image when it fits in LDS) and
+// all C channels: its work items are (channel, row, group of 4 columns), so
+// every thread has work however narrow the image.  An item makes 4
+// consecutive outputs of a row: along kx it keeps the 4 pixels under the taps
+// in registers and reads one new pixel per tap (3 zero columns pad the band on
+// the right for the last group).
+__device__ __forceinline__ int wave_min_i32(int v) {
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) v = min(v, __shfl_xor(v, s, 64));
+    return v;
+}
+__device__ __forceinline__ int wave_max_i32(int v) {
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) v = max(v, __shfl_xor(v, s, 64));
+    return v;
+}
+
 __global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img, int B, int H, int W,
-                                                const float *__restrict__ filt, int C, int KF, float thr,
+                                                const float *__restrict__ filt, int C, int KF, float thr, int R,
                                                 float *__restrict__ out) {
     extern __shared__ double smem_d[];
-    const int nb = (H + ROWS - 1) / ROWS;
+    const int nb = (H + R - 1) / R;
     const int b = blockIdx.x / nb, band = blockIdx.x % nb;
-    const int y0 = band * ROWS, p = (KF - 1) / 2;
-    const int rows = min(ROWS, H - y0);
+    const int y0 = band * R, p = (KF - 1) / 2;
+    const int rows = min(R, H - y0);
     const int srows = rows + KF - 1, Wp = W + 2 * p + 3;
+    const int KK = KF * KF;
     double *fd = smem_d;                                       // C*KF*KF taps
-    double *sim = fd + C * KF * KF;                            // srows x Wp pixels
+    double *sim = fd + C * KK;                                 // srows x Wp pixels
     int *bbox = reinterpret_cast<int *>(sim + srows * Wp);     // C x (y0,y1,x0,x1)
 
-    for (int i = threadIdx.x; i < C * KF * KF; i += blockDim.x) fd[i] = (double)filt[i];
+    for (int i = threadIdx.x; i < C * KK; i += blockDim.x) fd[i] = (double)filt[i];
     for (int i = threadIdx.x; i < srows * Wp; i += blockDim.x) {
         const int r = i / Wp, xp = i - r * Wp;
         const int y = y0 - p + r, x = xp - p;
         sim[i] = (y >= 0 && y < H && x >= 0 && x < W) ? (double)img[((int64_t)b * H + y) * W + x] : 0.0;
     }
     __syncthreads();
-    // bounding box of the non-zero taps of each channel (zero taps add nothing)
-    for (int c = threadIdx.x; c < C; c += blockDim.x) {
+    // bounding box of the non-zero taps of each channel (zero taps add nothing),
+    // one wave per channel
+    const int lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+    for (int c = threadIdx.x >> 6; c < C; c += nw) {
         int ya = KF, yb = -1, xa = KF, xb = -1;
-        for (int ky = 0; ky < KF; ++ky)
-            for (int kx = 0; kx < KF; ++kx)
-                if (fd[(c * KF + ky) * KF + kx] != 0.0) {
-                    ya = min(ya, ky); yb = max(yb, ky); xa = min(xa, kx); xb = max(xb, kx);
-                }
-        bbox[4 * c] = ya; bbox[4 * c + 1] = yb; bbox[4 * c + 2] = xa; bbox[4 * c + 3] = xb;
+        for (int i = lane; i < KK; i += 64)
+            if (fd[c * KK + i] != 0.0) {
+                const int ky = i / KF, kx = i - ky * KF;
+                ya = min(ya, ky); yb = max(yb, ky); xa = min(xa, kx); xb = max(xb, kx);
+            }
+        ya = wave_min_i32(ya); yb = wave_max_i32(yb); xa = wave_min_i32(xa); xb = wave_max_i32(xb);
+        if (lane == 0) {
+            bbox[4 * c] = ya; bbox[4 * c + 1] = yb; bbox[4 * c + 2] = xa; bbox[4 * c + 3] = xb;
+        }
     }
     __syncthreads();
-    const int xg = (W + 3) / 4, per = rows * xg;
-    for (int c = 0; c < C; ++c) {
+    const int xg = (W + 3) / 4, per = rows * xg, items = C * per;
+    for (int i = threadIdx.x; i < items; i += blockDim.x) {
+        const int c = i / per, rem = i - c * per;
+        const int r = rem / xg, x = (rem - r * xg) * 4;
         const int ya = bbox[4 * c], yb = bbox[4 * c + 1], xa = bbox[4 * c + 2], xb = bbox[4 * c + 3];
-        const double *fc = fd + c * KF * KF;
-        for (int i = threadIdx.x; i < per; i += blockDim.x) {
-            const int r = i / xg, x = (i - r * xg) * 4;
-            double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-            for (int ky = ya; ky <= yb; ++ky) {
-                const double *row = sim + (r + ky) * Wp + x;
-                const double *frow = fc + ky * KF;
-                double w0 = row[xa], w1 = row[xa + 1], w2 = row[xa + 2];
+        const double *fc = fd + c * KK;
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+        for (int ky = ya; ky <= yb; ++ky) {
+            const double *row = sim + (r + ky) * Wp + x;
+            const double *frow = fc + ky * KF;
+            double w0 = row[xa], w1 = row[xa + 1], w2 = row[xa + 2];
 #pragma unroll 4
-                for (int kx = xa; kx <= xb; ++kx) {
-                    const double w3 = row[kx + 3], f = frow[kx];
-                    s0 += f * w0;
-                    s1 += f * w1;
-                    s2 += f * w2;
-                    s3 += f * w3;
-                    w0 = w1;
-                    w1 = w2;
-                    w2 = w3;
-                }
+            for (int kx = xa; kx <= xb; ++kx) {
+                const double w3 = row[kx + 3], f = frow[kx];
+                s0 += f * w0;
+                s1 += f * w1;
+                s2 += f * w2;
+                s3 += f * w3;
+                w0 = w1;
+                w1 = w2;
+                w2 = w3;
             }
-            float *o = out + (((int64_t)b * C + c) * H + y0 + r) * W + x;
-            const double sv[4] = {s0, s1, s2, s3};
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (x + j < W) {
-                    const float v = (float)sv[j];
-                    o[j] = (v < thr) ? 0.0f : v;
-                }
         }
+        float *o = out + (((int64_t)b * C + c) * H + y0 + r) * W + x;
+        const double sv[4] = {s0, s1, s2, s3};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (x + j < W) {
+                const float v = (float)sv[j];
+                o[j] = (v < thr) ? 0.0f : v;
+            }
     }
 }
 
@@ -464,13 +483,20 @@ extern "C" int spk_encode_latency(const uint8_t *image, int B, int H, int W, con
     uint32_t *count = cv.take<uint32_t>(p.count_bytes / sizeof(uint32_t));
     float *I = intensities ? intensities : ws_int;
 
-    const int nb = (H + ROWS - 1) / ROWS;
-    const size_t lds = ((size_t)C * KF * KF + (size_t)(ROWS + KF - 1) * (W + KF - 1 + 3)) * sizeof(double) +
-                       4 * C * sizeof(int);
-    SPK_REQUIRE(lds <= 65536, SPK_E_RANGE, "spk_encode_latency: %d filters of %dx%d on width %d do not fit", C, KF,
-                KF, W);
-    hipLaunchKernelGGL(k_filter, dim3((unsigned)(B * nb)), dim3(256), lds, st, image, B, H, W, filters, C, KF,
-                       filter_threshold, I);
+    // rows per band: the whole image when it fits in LDS, else the most that
+    // fit, then evened out over the bands
+    auto filter_lds = [&](int rows) {
+        return ((size_t)C * KF * KF + (size_t)(rows + KF - 1) * (W + KF - 1 + 3)) * sizeof(double) +
+               4 * C * sizeof(int);
+    };
+    int R = H;
+    while (R > 1 && filter_lds(R) > 65536) --R;
+    SPK_REQUIRE(filter_lds(R) <= 65536, SPK_E_RANGE, "spk_encode_latency: %d filters of %dx%d on width %d do not fit",
+                C, KF, KF, W);
+    const int nb = (H + R - 1) / R;
+    R = (H + nb - 1) / nb;
+    hipLaunchKernelGGL(k_filter, dim3((unsigned)(B * nb)), dim3(256), filter_lds(R), st, image, B, H, W, filters, C,
+                       KF, filter_threshold, R, I);
     if (!t_first && !wave) return spk::check_launch("spk_encode_latency");
     if (p.N <= SORT_MAX) {
         hipLaunchKernelGGL(k_rank_sort, dim3(B), dim3(SORT_THREADS), 0, st, I, (int)p.N, T, t_first, wave);

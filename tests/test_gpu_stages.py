@@ -276,7 +276,8 @@ def test_encode_toy_t4(golden):
 
 ENC_CASES = [("dog", 3, 28, 28, 15, 0.0), ("gabor", 2, 160, 250, 30, 0.0), ("dog", 2, 28, 28, 1, 0.0),
              ("dog", 2, 28, 28, 64, 0.0), ("dog", 1, 28, 28, 255, 0.0), ("rand", 2, 19, 23, 15, 3.0),
-             ("pos", 2, 40, 50, 15, 0.0), ("pos", 1, 41, 50, 15, 0.0), ("pos", 3, 1, 1, 15, 0.0)]
+             ("pos", 2, 40, 50, 15, 0.0), ("pos", 1, 41, 50, 15, 0.0), ("pos", 3, 1, 1, 15, 0.0),
+             ("dog", 1, 100, 300, 15, 0.0)]  # 13x13 filters on a wide image: bands of rows
 
 
 @pytest.mark.parametrize("case", ENC_CASES)
