@@ -47,6 +47,18 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
     return v;
 }
 
+// Eq.1 for 4 neurons at once: byte j of the result is 1 when step t has
+// reached the first-spike time in byte j of t4 (times <= T, t < T).  With
+// T <= 127 every byte is below 128, so (t | 0x80) - b keeps bit 7 exactly
+// when t >= b and never borrows from the next byte.
+__device__ __forceinline__ uint32_t spikes4(uint32_t t4, int t, int T) {
+    if (T <= 127) return (((((uint32_t)t * 0x01010101u) | 0x80808080u) - t4) & 0x80808080u) >> 7;
+    uint32_t w = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w |= (uint32_t)(t >= (int)((t4 >> (8 * j)) & 255u)) << (8 * j);
+    return w;
+}
+
 __device__ __forceinline__ int wave_sum_i32(int v) {
 #pragma unroll
     for (int s = 32; s >= 1; s >>= 1) v += __shfl_xor(v, s, 64);

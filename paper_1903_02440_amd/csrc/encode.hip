@@ -295,12 +295,8 @@ __global__ __launch_bounds__(256) void k_expand_latency(const float *__restrict_
         if (vec) {
             if (tf_out) *reinterpret_cast<uint32_t *>(tf_out + (int64_t)b * N + q * 4) = tv;
             if (wave)
-                for (int t = 0; t < T; ++t) {
-                    uint32_t w = 0;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) w |= (uint32_t)(t >= t4[j]) << (8 * j);
-                    *reinterpret_cast<uint32_t *>(wave + ((int64_t)b * T + t) * N + q * 4) = w;
-                }
+                for (int t = 0; t < T; ++t)
+                    *reinterpret_cast<uint32_t *>(wave + ((int64_t)b * T + t) * N + q * 4) = spk::spikes4(tv, t, T);
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -325,10 +321,18 @@ __global__ __launch_bounds__(SORT_THREADS) void k_rank_sort(const float *__restr
     if (tid == 0) npos = 0;
     for (int i = tid; i < N; i += SORT_THREADS) tmap[i] = (uint8_t)T;
     __syncthreads();
-    // gather the positive entries' keys (their order in LDS does not matter: keys are unique)
-    for (int i0 = 0; i0 < N; i0 += SORT_THREADS) {
-        const int i = i0 + tid;
-        const float v = i < N ? I[i] : 0.0f;
+    // gather the positive entries' keys (their order in LDS does not matter: keys are
+    // unique); every load of the thread is issued before the first is used
+    float vin[SORT_MAX / SORT_THREADS];
+#pragma unroll
+    for (int r = 0; r < SORT_MAX / SORT_THREADS; ++r) {
+        const int i = r * SORT_THREADS + tid;
+        vin[r] = i < N ? I[i] : 0.0f;
+    }
+#pragma unroll
+    for (int r = 0; r < SORT_MAX / SORT_THREADS; ++r) {
+        const int i = r * SORT_THREADS + tid;
+        const float v = vin[r];
         const bool pos = v > 0.0f;
         const uint64_t m = __ballot(pos);
         int base = 0;
@@ -367,16 +371,9 @@ __global__ __launch_bounds__(SORT_THREADS) void k_rank_sort(const float *__restr
         for (int q = tid; q < nq; q += SORT_THREADS) {
             const uint32_t t4 = *reinterpret_cast<const uint32_t *>(tmap + 4 * q);
             if (tf) *reinterpret_cast<uint32_t *>(tf + 4 * q) = t4;
+            if (wv)
+                for (int t = 0; t < T; ++t) *reinterpret_cast<uint32_t *>(wv + (int64_t)t * N + 4 * q) = spk::spikes4(t4, t, T);
         }
-        if (wv)
-            for (int e = tid; e < T * nq; e += SORT_THREADS) {
-                const int t = e / nq, q = e - t * nq;
-                const uint32_t t4 = *reinterpret_cast<const uint32_t *>(tmap + 4 * q);
-                uint32_t w = 0;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) w |= (uint32_t)(t >= (int)((t4 >> (8 * j)) & 255u)) << (8 * j);
-                *reinterpret_cast<uint32_t *>(wv + (int64_t)t * N + 4 * q) = w;
-            }
     } else {
         for (int i = tid; i < N; i += SORT_THREADS)
             if (tf) tf[i] = tmap[i];
@@ -397,12 +394,7 @@ __global__ __launch_bounds__(256) void k_expand_wave(const uint8_t *__restrict__
     const int64_t b = q / groups_per_img, g = q % groups_per_img;
     if ((N % 4) == 0) {
         const uint32_t t4 = *reinterpret_cast<const uint32_t *>(tf + b * N + g * 4);
-        for (int t = 0; t < T; ++t) {
-            uint32_t w = 0;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) w |= (uint32_t)(t >= (int)((t4 >> (8 * j)) & 255u)) << (8 * j);
-            *reinterpret_cast<uint32_t *>(wave + (b * T + t) * N + g * 4) = w;
-        }
+        for (int t = 0; t < T; ++t) *reinterpret_cast<uint32_t *>(wave + (b * T + t) * N + g * 4) = spk::spikes4(t4, t, T);
     } else {
         for (int j = 0; j < 4; ++j) {
             const int64_t i = g * 4 + j;

@@ -89,12 +89,8 @@ __global__ __launch_bounds__(256) void k_pool_first_spike(const uint8_t *__restr
         if (out_tf) *reinterpret_cast<uint32_t *>(out_tf + b * per_img + i0) = m4;
         if (out) {
             uint8_t *dst = out + b * T * (int64_t)per_img + i0;
-            for (int t = 0; t < T; ++t) {
-                uint32_t w = 0;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) w |= (uint32_t)(t >= (int)((m4 >> (8 * q)) & 255u)) << (8 * q);
-                *reinterpret_cast<uint32_t *>(dst + (int64_t)t * per_img) = w;
-            }
+            for (int t = 0; t < T; ++t)
+                *reinterpret_cast<uint32_t *>(dst + (int64_t)t * per_img) = spk::spikes4(m4, t, T);
         }
     } else {
         const int m = (int)m4;
