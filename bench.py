@@ -14,6 +14,7 @@ Only one GPU is measured; --gpus above 1 exits with a message.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import math
@@ -136,6 +137,32 @@ def copy_probe(nbytes):
     print(json.dumps({"copy_probe_bytes": nbytes, "launches": 5}), flush=True)
 
 
+def online_bench(wl, inp, dev, group):
+    """Online plasticity: every image its own step (forward with the weights
+    the previous images left, then plasticity), graph-replayed in groups."""
+    import torch
+    from paper_1903_02440_amd.pipeline import online_for
+    assert wl.source == "image", "online plasticity runs on an image workload"
+    tr = online_for(wl, inp["bank"], device=dev, steps_per_graph=group)
+    tr.set_weights([torch.from_numpy(w) for w in inp["weights"]])
+    imgs = torch.from_numpy(inp["image"]).to(dev)
+    labs = torch.from_numpy(inp["labels"]).to(dev)
+    n = (wl.B // group) * group
+    tr.run(imgs[:group], labs[:group])  # capture and warm up
+    tr.set_weights([torch.from_numpy(w) for w in inp["weights"]])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    tr.run(imgs[:n], labs[:n])
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    print(json.dumps({"metric": "online images/s (one image per step: forward with the weights the previous "
+                                "images left, then plasticity)", "value": round(n / dt, 1), "unit": "images/s",
+                      "n_gpus": 1, "images": n, "ms_per_image": round(dt * 1e3 / n, 4), "higher_is_better": True,
+                      "dtype": "f32", "data": "synthetic",
+                      "config": {"workload": wl.name, "T": wl.T, "steps_per_graph": group,
+                                 "form": "compact (no per-step potentials)"}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,6 +174,10 @@ def main():
     ap.add_argument("--compact", action="store_true",
                     help="the compact inter-layer form: no per-step potentials and no unread per-step spikes "
                          "(a separate figure, not the contract number)")
+    ap.add_argument("--online", type=int, default=0, metavar="N",
+                    help="only time online plasticity (one image per step, graph-replayed groups of "
+                         "--online-group steps) over N images of the workload and exit (a separate figure)")
+    ap.add_argument("--online-group", type=int, default=32, help="steps per captured graph with --online")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 5 times (the reference "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -168,9 +199,14 @@ def main():
     from paper_1903_02440_amd.pipeline import chain_for
 
     wl = synth.WORKLOADS[args.workload]() if args.batch is None else synth.WORKLOADS[args.workload](args.batch)
+    if args.online:
+        wl = dataclasses.replace(wl, B=args.online)
     inp = synth.make_inputs(wl)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.online:
+        online_bench(wl, inp, dev, args.online_group)
+        return
     ch = chain_for(wl, inp.get("bank"), device=dev, want_potentials=not args.compact,
                    want_spikes=not args.compact)
     ch.set_weights([torch.from_numpy(w) for w in inp["weights"]])

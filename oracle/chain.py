@@ -115,6 +115,25 @@ def step(wl, inputs, weights, workers=1):
     return learn(wl, res, weights, dec), res, dec
 
 
+def online(wl, inputs, weights, images=None):
+    """Online plasticity, one image at a time (section "Tutorial", "Training
+    and Testing": each sample's forward runs with the weights the previous
+    samples left): `step` on each selected image alone, in order.  Returns
+    the weights after every image."""
+    import dataclasses
+    wl1 = dataclasses.replace(wl, B=1)
+    sel = np.arange(wl.B) if images is None else np.asarray(images)
+    W = [w.copy() for w in weights]
+    after = []
+    for i in sel:
+        one = dict(inputs)
+        one["image"] = inputs["image"][i:i + 1]
+        one["labels"] = inputs["labels"][i:i + 1]
+        W, _, _ = step(wl1, one, W)
+        after.append([w.copy() for w in W])
+    return after
+
+
 def default_workers():
     try:
         n = len(os.sched_getaffinity(0))

@@ -279,3 +279,87 @@ def chain_for(workload, filter_bank=None, device="cuda", **kw):
 
 
 INF = math.inf
+
+
+class OnlineTrainer:
+    """Online plasticity: one image per step, each image's forward run with the
+    weights left by the images before it (the tutorial's training loop,
+    section "Tutorial", "Training and Testing": each sample goes through the
+    network in train mode and its layer's STDP object updates the weights
+    before the next sample).  Equal to a sequence of one-image Chain steps.
+
+    A one-image Chain (one stream, compact inter-layer form: no per-step
+    potentials) does the work.  With use_graph, `steps_per_graph` consecutive
+    steps -- each copying its image and label from a staging slot into the
+    chain's inputs, then the chain's forward and plasticity -- are captured
+    once in a HIP graph, so steps_per_graph images cost one staging copy and
+    one graph launch, with no host work in between.  A trailing partial group
+    runs eagerly.  Weights change in place (chain.weights())."""
+
+    def __init__(self, stages, T, H, W, cin, filter_bank, filter_threshold=0.0, n_classes=10, device="cuda",
+                 use_graph=True, steps_per_graph=16):
+        self.chain = Chain(stages, 1, T, H, W, cin, source="image", filter_bank=filter_bank,
+                           filter_threshold=filter_threshold, n_classes=n_classes, device=device,
+                           want_potentials=False, want_spikes=False, concurrent_learn=False)
+        dev = self.chain.image.device
+        self.use_graph = use_graph
+        self.K = max(1, int(steps_per_graph))
+        self.img_stage = torch.zeros((self.K, H, W), dtype=torch.uint8, device=dev)
+        self.lab_stage = torch.zeros((self.K,), dtype=torch.int32, device=dev)
+        self.graph = None
+
+    def set_weights(self, weights):
+        self.chain.set_weights(weights)
+
+    def weights(self):
+        return self.chain.weights()
+
+    def _step_from(self, j):
+        self.chain.image.copy_(self.img_stage[j:j + 1])
+        self.chain.labels.copy_(self.lab_stage[j:j + 1])
+        self.chain.step()
+
+    def _capture(self):
+        # one eager step on a side stream first (first launches load the kernels),
+        # with the weights it changes restored afterwards
+        saved = [w.clone() for w in self.chain.weights()]
+        side = torch.cuda.Stream(device=self.chain.image.device)
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self._step_from(0)
+        torch.cuda.current_stream().wait_stream(side)
+        for w, v in zip(self.chain.weights(), saved):
+            w.copy_(v)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for j in range(self.K):
+                self._step_from(j)
+        self.graph = g
+
+    def run(self, images, labels=None):
+        """Learn from images (u8 [N, H, W] on the device) in order; labels
+        (i32 [N]) feed the decision of a reward-modulated last layer."""
+        N = images.shape[0]
+        i = 0
+        while i < N:
+            n = min(self.K, N - i)
+            self.img_stage[:n].copy_(images[i:i + n])
+            if labels is not None:
+                self.lab_stage[:n].copy_(labels[i:i + n])
+            if self.use_graph and n == self.K:
+                if self.graph is None:
+                    self._capture()
+                self.graph.replay()
+            else:
+                for j in range(n):
+                    self._step_from(j)
+            i += n
+
+
+def online_for(workload, filter_bank, device="cuda", **kw):
+    """An OnlineTrainer for a workload description with an image source."""
+    bank = filter_bank
+    if bank is not None and not isinstance(bank, torch.Tensor):
+        bank = torch.from_numpy(bank)
+    return OnlineTrainer(workload.stages, workload.T, workload.H, workload.W, workload.cin, bank,
+                         n_classes=workload.n_classes, device=device, **kw)

@@ -348,3 +348,25 @@ def test_filter_asymmetric_kernel_orientation():
     ref = F.conv2d(torch.from_numpy(img[:, None].astype(np.float64)),
                    torch.from_numpy(bank[:, None].astype(np.float64)), padding=2)
     assert np.array_equal(I, ref.numpy().astype(np.float32))
+
+
+# ---------------------------------------------------------------- online plasticity
+def test_online_composes_one_image_steps():
+    """online() is `step` on each image alone, in order: one image equals a
+    one-image batch; zero rates leave the weights as they were; the weights
+    after image k do not depend on later images; and order matters."""
+    import dataclasses
+    import oracle.chain as ochain
+    wl = synth.mnist_single(3)
+    inp = synth.make_inputs(wl)
+    after = ochain.online(wl, inp, inp["weights"])
+    one = dict(inp, image=inp["image"][:1], labels=inp["labels"][:1])
+    W1, _, _ = ochain.step(dataclasses.replace(wl, B=1), one, inp["weights"])
+    assert np.array_equal(after[0][0], W1[0])
+    first2 = ochain.online(wl, inp, inp["weights"], images=[0, 1])
+    assert np.array_equal(first2[1][0], after[1][0])
+    rev = ochain.online(wl, inp, inp["weights"], images=[2, 1, 0])
+    assert not np.array_equal(rev[2][0], after[2][0])
+    still = dataclasses.replace(wl, stages=[dataclasses.replace(wl.stages[0], a_plus=0.0, a_minus=0.0)])
+    frozen = ochain.online(still, inp, inp["weights"])
+    assert np.array_equal(frozen[-1][0], inp["weights"][0])
