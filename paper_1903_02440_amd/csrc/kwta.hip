@@ -397,13 +397,17 @@ __global__ __launch_bounds__(SMALL_THREADS) void k_kwta_select_small(const uint8
 // first keeps, for every position, the k largest keys over all feature maps:
 // one pass over the image's neurons, with each position owned by one thread
 // (on maps of few positions, the feature maps are split among up to
-// TOPK_THREADS / HW threads per position, whose lists the owner then merges).
+// TOPK_THREADS / HW threads per position, whose lists the owner then merges;
+// small batches, which leave most CUs idle, take up to TOPK_THREADS_SMALL_B
+// threads per workgroup so that each thread scans fewer feature maps).
 // The rounds never read global memory again.  At round j at most j features
 // are retired, so a position's best live key is among its first j + 1 list
 // entries: the owner skips entries of retired features with a per-position
 // cursor, and marks its position inhibited when it falls in a winner's
 // window.  Only the per-round maximum crosses threads.
 constexpr int TOPK_THREADS = 256;       // most threads per workgroup
+constexpr int TOPK_THREADS_SMALL_B = 1024;  // most threads per workgroup for batches below TOPK_SMALL_B
+constexpr int TOPK_SMALL_B = 256;
 constexpr int TOPK_MAX_K = 16;
 constexpr size_t TOPK_LDS = 40 * 1024;  // lists and cursors (the stash adds 16 KB)
 constexpr int TOPK_U = 8;               // feature maps loaded per block
@@ -430,14 +434,15 @@ __device__ __forceinline__ void topk_insert(uint64_t (&top)[KM], uint64_t key) {
 }
 
 template <int KM, int U, bool STASH>
-__global__ __launch_bounds__(TOPK_THREADS) void k_kwta_topk(const uint8_t *__restrict__ tf_all,
+__global__ __launch_bounds__(TOPK_THREADS_SMALL_B) void k_kwta_topk(const uint8_t *__restrict__ tf_all,
                                                             const float *__restrict__ vf_all, KwtaTopk g,
                                                             int32_t *__restrict__ winners,
                                                             int32_t *__restrict__ n_winners) {
     extern __shared__ uint64_t lists[];  // [S][HW][KM] keys, then [HW] cursors
     uint8_t *cur = reinterpret_cast<uint8_t *>(lists + (size_t)g.S * g.HW * KM);
-    __shared__ uint64_t red[2][TOPK_THREADS / 64];
-    __shared__ uint64_t stash[STASH ? U : 1][TOPK_THREADS];  // a block's keys, read back by their own lane
+    __shared__ uint64_t red[2][TOPK_THREADS_SMALL_B / 64];
+    // a block's keys, read back by their own lane (STASH launches have at most TOPK_THREADS threads)
+    __shared__ uint64_t stash[STASH ? U : 1][TOPK_THREADS];
     const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int NT = blockDim.x, NW = NT >> 6;
     const int HW = g.HW, S = g.S;
@@ -571,12 +576,14 @@ __global__ __launch_bounds__(TOPK_THREADS) void k_kwta_topk(const uint8_t *__res
 bool kwta_topk(int B, int T, int C, int H, int W, int k, int r, KwtaTopk &s) {
     const int64_t HW = (int64_t)H * W;
     if (k > TOPK_MAX_K || HW > 65536) return false;
-    // maps of few positions split the feature maps among up to TOPK_THREADS / HW threads per position
-    int S = HW <= TOPK_THREADS ? (int)std::min<int64_t>(C, TOPK_THREADS / HW) : 1;
+    // maps of few positions split the feature maps among up to NT / HW threads per position
+    const int NT = B < TOPK_SMALL_B ? TOPK_THREADS_SMALL_B : TOPK_THREADS;
+    int S = HW <= NT ? (int)std::min<int64_t>(C, NT / HW) : 1;
+    while (S > 1 && (size_t)HW * (S * k * sizeof(uint64_t) + 1) > TOPK_LDS) --S;  // the splits' lists fit
     const int fps = (C + S - 1) / S;
     S = (C + fps - 1) / fps;
-    // threads: whole waves covering HW * S in as few passes as TOPK_THREADS allows
-    const int64_t work = HW * S, passes = (work + TOPK_THREADS - 1) / TOPK_THREADS;
+    // threads: whole waves covering HW * S in as few passes as NT allows
+    const int64_t work = HW * S, passes = (work + NT - 1) / NT;
     const int nt = (int)(((work + passes - 1) / passes + 63) / 64 * 64);
     if ((size_t)HW * (S * k * sizeof(uint64_t) + 1) > TOPK_LDS) return false;
     auto magic = [](int64_t d) {  // 0 for d == 1 (see qdiv)
@@ -596,7 +603,7 @@ template <int KM>
 void launch_topk(const KwtaTopk &s, const uint8_t *tf, const float *vf, int32_t *winners, int32_t *nw,
                  hipStream_t st) {
     const size_t lds = (size_t)s.HW * (s.S * KM * sizeof(uint64_t) + 1);
-    if (s.fps >= TOPK_STASH_MIN)
+    if (s.fps >= TOPK_STASH_MIN && s.nt <= TOPK_THREADS)
         hipLaunchKernelGGL(HIP_KERNEL_NAME(k_kwta_topk<KM, TOPK_U, true>), dim3(s.B), dim3(s.nt), lds, st, tf, vf, s,
                            winners, nw);
     else
