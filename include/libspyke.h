@@ -154,6 +154,30 @@ SPK_API int spk_pool_first_spike(const uint8_t *t_first, int B, int T, int C, in
                                  int kernel, int stride, int pad,
                                  uint8_t *out_wave, uint8_t *out_t_first, void *stream);
 
+/* Max-pooling of potentials (section "snn Module": pooling a potentials
+ * tensor keeps the largest potential of each window).  potentials f32
+ * [B][T][C][H][W] -> out f32 [B][T][C][Ho][Wo], Ho = (H + 2*pad - kernel) /
+ * stride + 1.  Zero padding: a padded element is a potential of +0 and takes
+ * part in the maximum; of equal values the first in row-major window order
+ * is kept.  out must not overlap potentials.                               */
+SPK_API int spk_pool_potentials(const float *potentials, int B, int T, int C, int H, int W,
+                                int kernel, int stride, int pad, float *out, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Pointwise inhibition (section "functional Module": at each location only
+ * the neuron of the most salient feature may spike -- the earliest spike,
+ * then the highest potential; ties go to the lower feature index, as in
+ * spk_kwta).  In: t_first u8 and v_first f32 [B][C][H][W] (t_first >= T:
+ * silent).  Out: out_t_first / out_v_first [B][C][H][W] keep the winner of
+ * each location and make every other feature silent (T, 0); a location
+ * where nothing spikes stays silent.  They may alias the inputs.  Optional
+ * (NULL to skip): out_wave u8 [B][T][C][H][W], the Eq.1 wave of out_t_first;
+ * potentials f32 [B][T][C][H][W], masked in place: every value of a feature
+ * that is not its location's winner becomes 0.  Limits: T <= 255.          */
+SPK_API int spk_pointwise_inhibition(const uint8_t *t_first, const float *v_first, int B, int T, int C,
+                                     int H, int W, uint8_t *out_t_first, float *out_v_first,
+                                     uint8_t *out_wave, float *potentials, void *stream);
+
 /* ------------------------------------------------------------------------
  * k winners-take-all with feature-wise and lateral inhibition (sections
  * "snn Module" and "functional Module": get_k_winners).  Eligible neurons

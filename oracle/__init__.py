@@ -79,6 +79,7 @@ def _load():
         "orc_kwta": (None, [_u8p, _f32p, _i64, _int, _int, _int, _int, _int, _int, _i32p, _i32p]),
         "orc_decide": (None, [_i32p, _i32p, _i64, _int, _i32p, _int, _i32p, _i8p]),
         "orc_count_events": (_i64, [_u8p, _i64, _int, _int, _int, _int, _int, _int, _int]),
+        "orc_pool_potentials": (None, [_f32p, _i64, _int, _int, _int, _int, _int, _int, _int, _f32p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -88,6 +89,9 @@ def _load():
     lib.orc_stdp.restype = None
     lib.orc_stdp.argtypes = [_f32p, _int, _int, _int, _int, _u8p, _i64, _int, _int, _int,
                              _i32p, _i32p, _int, ctypes.c_void_p, _flt, _flt, _flt, _flt, _int]
+    # orc_pointwise_inhibition takes nullable potentials
+    lib.orc_pointwise_inhibition.restype = None
+    lib.orc_pointwise_inhibition.argtypes = [_u8p, _f32p, _i64, _int, _int, _i64, _u8p, _f32p, ctypes.c_void_p]
     _lib = lib
     return lib
 
@@ -233,6 +237,31 @@ def pool(wave: np.ndarray, P: int, R: int | None = None, D: int = 0) -> np.ndarr
     out = np.empty((B, T, C, pool_size(H, P, R, D), pool_size(W, P, R, D)), np.uint8)
     _load().orc_pool(w, B, T, C, H, W, P, R, D, out)
     return out
+
+
+def pool_potentials(pot: np.ndarray, P: int, R: int | None = None, D: int = 0) -> np.ndarray:
+    """Max-pooling of potentials [B,T,C,H,W] (largest potential per window; zero padding)."""
+    R = P if R is None else R
+    x = _c(pot, np.float32)
+    B, T, C, H, W = x.shape
+    out = np.empty((B, T, C, pool_size(H, P, R, D), pool_size(W, P, R, D)), np.float32)
+    _load().orc_pool_potentials(x, B, T, C, H, W, P, R, D, out)
+    return out
+
+
+def pointwise_inhibition(t_first: np.ndarray, v_first: np.ndarray, T: int, potentials: np.ndarray | None = None):
+    """Per location only the most salient feature keeps its spike (earliest,
+    then highest potential, then lowest feature index): (t_first, v_first)
+    [B,C,H,W] of the survivors, and the masked potentials [B,T,C,H,W] if given."""
+    tf = _c(t_first, np.uint8)
+    vf = _c(v_first, np.float32)
+    B, C, H, W = tf.shape
+    ot = np.empty_like(tf)
+    ov = np.empty_like(vf)
+    pot = None if potentials is None else np.array(potentials, dtype=np.float32, order="C", copy=True)
+    _load().orc_pointwise_inhibition(tf, vf, B, T, C, H * W, ot, ov,
+                                     None if pot is None else pot.ctypes.data_as(ctypes.c_void_p))
+    return (ot, ov) if pot is None else (ot, ov, pot)
 
 
 # ---------------------------------------------------------------- kWTA

@@ -268,6 +268,67 @@ ORC_API void orc_pool(const uint8_t *wave, int64_t B, int T, int C, int H, int W
 }
 
 /* ------------------------------------------------------------------ */
+/* Max-pooling of a potentials tensor (section "snn Module": on potentials the
+ * pooling keeps the largest potential of each window).  Window P, stride R,
+ * zero padding D: a padded element is a potential of +0 and takes part in the
+ * maximum.  Within a window the first of equal values (row-major order) is
+ * kept, so -0 and +0 keep the one met first. */
+ORC_API void orc_pool_potentials(const float *pot, int64_t B, int T, int C, int H, int W,
+                                 int P, int R, int D, float *out) {
+    int Ho = (H + 2 * D - P) / R + 1, Wo = (W + 2 * D - P) / R + 1;
+    for (int64_t b = 0; b < B; ++b)
+        for (int t = 0; t < T; ++t)
+            for (int c = 0; c < C; ++c)
+                for (int yo = 0; yo < Ho; ++yo)
+                    for (int xo = 0; xo < Wo; ++xo) {
+                        int first = 1;
+                        float m = 0.0f;
+                        for (int dy = 0; dy < P; ++dy)
+                            for (int dx = 0; dx < P; ++dx) {
+                                int iy = yo * R + dy - D, ix = xo * R + dx - D;
+                                float v = 0.0f;
+                                if (iy >= 0 && iy < H && ix >= 0 && ix < W)
+                                    v = pot[(((b * T + t) * C + c) * (int64_t)H + iy) * W + ix];
+                                if (first || v > m) m = v;
+                                first = 0;
+                            }
+                        out[(((b * T + t) * C + c) * (int64_t)Ho + yo) * Wo + xo] = m;
+                    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Pointwise inhibition (section "functional Module": at each location only
+ * the neuron of the most salient feature may spike -- the earliest spike,
+ * then the highest potential; ties go to the lower feature index, a
+ * reading).  In the first-spike form: every other feature at that location
+ * becomes silent (time T, potential 0); a location where nothing spikes is
+ * left silent.  Optional potentials [B][T][C][HW] are masked the same way:
+ * every plane value of a feature that is not its location's winner becomes
+ * 0 (all of them where nothing spikes). */
+ORC_API void orc_pointwise_inhibition(const uint8_t *t_first, const float *v_first, int64_t B, int T, int C,
+                                      int64_t HW, uint8_t *out_t, float *out_v, float *pot) {
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t p = 0; p < HW; ++p) {
+            int best = -1;
+            for (int c = 0; c < C; ++c) {
+                int64_t i = (b * C + c) * HW + p;
+                if (t_first[i] >= T) continue;
+                if (best < 0) { best = c; continue; }
+                int64_t j = (b * C + best) * HW + p;
+                if (t_first[i] < t_first[j] || (t_first[i] == t_first[j] && v_first[i] > v_first[j])) best = c;
+            }
+            for (int c = 0; c < C; ++c) {
+                int64_t i = (b * C + c) * HW + p;
+                int keep = c == best;
+                out_t[i] = keep ? t_first[i] : (uint8_t)T;
+                out_v[i] = keep ? v_first[i] : 0.0f;
+                if (pot && !keep)
+                    for (int t = 0; t < T; ++t) pot[((b * T + t) * C + c) * HW + p] = 0.0f;
+            }
+        }
+}
+
+/* ------------------------------------------------------------------ */
 /* k winners-take-all (sections "snn Module" and "functional Module":
  * get_k_winners).  Eligible neurons are the ones that spiked.  Up to k
  * times: take the eligible, uninhibited neuron with the earliest spike,

@@ -45,6 +45,8 @@ _SIGS = {
     "spk_conv_fire_first_spike": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z, _P]),
     "spk_pool": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
     "spk_pool_first_spike": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
+    "spk_pool_potentials": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
+    "spk_pointwise_inhibition": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "spk_kwta_workspace_size": (_Z, [_I, _I, _I, _I]),
     "spk_kwta": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _Z, _P]),
     "spk_stdp_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
@@ -250,6 +252,36 @@ def spk_pool_first_spike(t_first, T, kernel, stride=None, pad=0, out_wave=None, 
     _check(_lib.spk_pool_first_spike(_ptr(t_first), B, T, C, H, W, kernel, stride, pad, _ptr(out_wave),
                                      _ptr(out_t_first), _stream(stream)))
     return out_wave, out_t_first
+
+
+def spk_pool_potentials(potentials, kernel, stride=None, pad=0, out=None, stream=None):
+    """Max-pooling of potentials f32 [B,T,C,H,W] -> f32 [B,T,C,Ho,Wo] (zero padding)."""
+    stride = kernel if stride is None else stride
+    B, T, C, H, W = potentials.shape
+    _need(potentials, torch.float32, (B, T, C, H, W), "potentials")
+    Ho, Wo = pool_out_size(H, kernel, stride, pad), pool_out_size(W, kernel, stride, pad)
+    out = _out(out, (B, T, C, Ho, Wo), torch.float32, potentials.device, "out")
+    _check(_lib.spk_pool_potentials(_ptr(potentials), B, T, C, H, W, kernel, stride, pad, _ptr(out), _stream(stream)))
+    return out
+
+
+def spk_pointwise_inhibition(t_first, v_first, T, out_t_first=None, out_v_first=None, out_wave=False,
+                             potentials=None, stream=None):
+    """Per location only the most salient feature keeps its spike: (t_first u8, v_first f32)
+    [B,C,H,W] -> (out_t_first, out_v_first, out_wave u8 [B,T,C,H,W] or None); potentials
+    f32 [B,T,C,H,W], if given, are masked in place.  out_wave=None allocates the wave."""
+    B, C, H, W = t_first.shape
+    _need(t_first, torch.uint8, (B, C, H, W), "t_first")
+    _need(v_first, torch.float32, (B, C, H, W), "v_first")
+    dev = t_first.device
+    out_t_first = _out(out_t_first, (B, C, H, W), torch.uint8, dev, "out_t_first")
+    out_v_first = _out(out_v_first, (B, C, H, W), torch.float32, dev, "out_v_first")
+    out_wave = _out(out_wave, (B, T, C, H, W), torch.uint8, dev, "out_wave")
+    if potentials is not None:
+        _need(potentials, torch.float32, (B, T, C, H, W), "potentials")
+    _check(_lib.spk_pointwise_inhibition(_ptr(t_first), _ptr(v_first), B, T, C, H, W, _ptr(out_t_first),
+                                         _ptr(out_v_first), _ptr(out_wave), _ptr(potentials), _stream(stream)))
+    return out_t_first, out_v_first, (out_wave if out_wave is not False else None)
 
 
 # ---------------------------------------------------------------- kWTA

@@ -185,6 +185,45 @@ def test_pool_toy_t2(golden):
     assert_equal(host(otf), g["t_first_out"].astype(np.uint8), "T2")
 
 
+# ---------------------------------------------------------------- pointwise inhibition, potentials pooling
+@pytest.mark.parametrize("case", [(3, 15, 30, 28, 28), (2, 15, 250, 14, 14), (2, 9, 7, 5, 3), (1, 4, 1, 2, 2),
+                                  (2, 15, 200, 4, 4)])
+def test_pointwise_inhibition_parity(case):
+    B, T, C, H, W = case
+    g = synth.rng(700 + C + H, 0)
+    tf = synth.times_uniform_or_silent(g, (B, C, H, W), T, 0.5)
+    vf = (g.integers(0, 6, (B, C, H, W)) * 0.5).astype(np.float32)  # ties decided by the feature index
+    vf[tf >= T] = 0
+    pot = g.normal(0, 3, (B, T, C, H, W)).astype(np.float32)
+    rt, rv, rp = orc.pointwise_inhibition(tf, vf, T, pot)
+    gp = dev(pot)
+    ot, ov, ow = spk.spk_pointwise_inhibition(dev(tf), dev(vf), T, out_wave=None, potentials=gp)
+    sync()
+    assert_equal(host(ot), rt, "t_first")
+    assert_equal(host(ov), rv, "v_first")
+    assert_equal(host(ow), orc.expand_wave(rt, T), "wave")
+    assert_equal(host(gp), rp, "masked potentials")
+    # in place, without the optional outputs
+    it, iv = dev(tf), dev(vf)
+    spk.spk_pointwise_inhibition(it, iv, T, out_t_first=it, out_v_first=iv)
+    sync()
+    assert_equal(host(it), rt, "t_first in place")
+    assert_equal(host(iv), rv, "v_first in place")
+
+
+@pytest.mark.parametrize("case", [(2, 15, 30, 28, 28, 2, 2, 0), (2, 15, 250, 14, 14, 3, 3, 0),
+                                  (1, 5, 4, 9, 11, 3, 2, 1), (1, 3, 2, 7, 7, 4, 3, 2), (2, 4, 3, 5, 6, 1, 1, 0)])
+def test_pool_potentials_parity(case):
+    B, T, C, H, W, P, R, D = case
+    g = synth.rng(800 + P + C, 0)
+    pot = (g.integers(-8, 9, (B, T, C, H, W)) * 0.25).astype(np.float32)  # ties, zeros and negatives
+    pot[..., 0, 0] = -0.0
+    out = spk.spk_pool_potentials(dev(pot), P, R, D)
+    sync()
+    ref = orc.pool_potentials(pot, P, R, D)
+    assert_equal(host(out).view(np.uint32), ref.view(np.uint32), "pooled potentials (bit patterns)")
+
+
 # ---------------------------------------------------------------- kWTA
 # (B, T, C, H, W, k, radius).  Per-position top-k path: the first five, the
 # 1x1 and 1x9 maps, (300 maps of 10x10: feature split with the stash) and

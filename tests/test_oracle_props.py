@@ -370,3 +370,37 @@ def test_online_composes_one_image_steps():
     still = dataclasses.replace(wl, stages=[dataclasses.replace(wl.stages[0], a_plus=0.0, a_minus=0.0)])
     frozen = ochain.online(still, inp, inp["weights"])
     assert np.array_equal(frozen[-1][0], inp["weights"][0])
+
+
+# ---------------------------------------------------------------- potentials pooling, pointwise inhibition
+@pytest.mark.parametrize("P,R,D", [(2, 2, 0), (3, 3, 0), (3, 2, 1), (4, 3, 2), (1, 1, 0)])
+def test_pool_potentials_is_max_pool_of_the_zero_padded_map(P, R, D):
+    g = np.random.default_rng(31 + P + R + D)
+    x = g.normal(0, 2, (2, 3, 4, 9, 11)).astype(np.float32)
+    got = orc.pool_potentials(x, P, R, D)
+    xt = F.pad(torch.from_numpy(x).reshape(-1, 1, 9, 11), (D, D, D, D), value=0.0)
+    ref = F.max_pool2d(xt, P, R).reshape(got.shape).numpy()
+    assert np.array_equal(got, ref)
+
+
+def test_pointwise_inhibition_second_formulation():
+    """Against a lexicographic sort per location: the survivor is the first of
+    (t_first, -v_first, feature) among spiking features; everything else is
+    silenced, and the masked potentials keep only the survivor's planes."""
+    g = np.random.default_rng(5)
+    B, T, C, H, W = 3, 9, 7, 4, 5
+    tf = np.where(g.random((B, C, H, W)) < 0.4, T, g.integers(0, T, (B, C, H, W))).astype(np.uint8)
+    vf = (g.integers(0, 4, (B, C, H, W)) * 0.5).astype(np.float32)  # many ties
+    vf[tf >= T] = 0
+    pot = g.normal(0, 1, (B, T, C, H, W)).astype(np.float32)
+    ot, ov, op = orc.pointwise_inhibition(tf, vf, T, pot)
+    for b in range(B):
+        for y in range(H):
+            for x in range(W):
+                spiking = [c for c in range(C) if tf[b, c, y, x] < T]
+                win = min(spiking, key=lambda c: (tf[b, c, y, x], -vf[b, c, y, x], c)) if spiking else None
+                for c in range(C):
+                    keep = c == win
+                    assert ot[b, c, y, x] == (tf[b, c, y, x] if keep else T)
+                    assert ov[b, c, y, x] == (vf[b, c, y, x] if keep else 0.0)
+                    assert np.array_equal(op[b, :, c, y, x], pot[b, :, c, y, x] if keep else np.zeros(T, np.float32))
