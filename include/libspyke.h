@@ -82,6 +82,29 @@ SPK_API int spk_encode_latency(const uint8_t *image, int B, int H, int W,
                        uint8_t *wave, uint8_t *t_first, float *intensities,
                        void *workspace, size_t ws_bytes, void *stream);
 
+/* Rank-order code of a given intensity map (the second half of
+ * spk_encode_latency, for maps prepared otherwise -- e.g. locally normalised):
+ * intensities f32 [B][C][H][W] -> wave u8 [B][T][C][H][W] and/or t_first u8
+ * [B][C][H][W] (either may be NULL), with the ranking of spk_encode_latency.
+ * Workspace: spk_rank_latency_workspace_size(B, C, H, W, T) bytes.         */
+SPK_API size_t spk_rank_latency_workspace_size(int B, int C, int H, int W, int T);
+SPK_API int spk_rank_latency(const float *intensities, int B, int C, int H, int W, int T,
+                             uint8_t *wave, uint8_t *t_first, void *workspace, size_t ws_bytes,
+                             void *stream);
+
+/* Local normalisation (section "functional Module": intensities normalised by
+ * their regional mean; in the tutorial it sits between the filter and the
+ * latency code).  A reading -- the paper gives no formula: per channel,
+ *     out = in / (mean + eps),
+ * mean over the (2*radius+1)^2 window centred on the entry with zero padding
+ * (padding counts in the window size).  Operation order, fixed so that the
+ * result is reproducible: row sums in double (dx ascending), their sum in
+ * double (dy ascending), mean = float(sum / (2r+1)^2), then float mean + eps
+ * and a correctly rounded float division.  intensities, out f32
+ * [B][C][H][W], not overlapping.  Limits: 0 <= radius <= 1024.              */
+SPK_API int spk_local_normalization(const float *intensities, int B, int C, int H, int W, int radius,
+                                    float eps, float *out, void *stream);
+
 /* Eq.1: wave u8 [B][T][C][H][W] from first-spike times u8 [B][C][H][W]
  * (values >= T never spike).  1 <= T <= 255.                               */
 SPK_API int spk_expand_wave(const uint8_t *t_first, int B, int T, int C, int H, int W,

@@ -80,6 +80,7 @@ def _load():
         "orc_decide": (None, [_i32p, _i32p, _i64, _int, _i32p, _int, _i32p, _i8p]),
         "orc_count_events": (_i64, [_u8p, _i64, _int, _int, _int, _int, _int, _int, _int]),
         "orc_pool_potentials": (None, [_f32p, _i64, _int, _int, _int, _int, _int, _int, _int, _f32p]),
+        "orc_local_normalize": (None, [_f32p, _i64, _int, _int, _int, _int, _flt, _f32p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -138,6 +139,16 @@ def filter_images(img: np.ndarray, filt: np.ndarray, thr: float = 0.0) -> np.nda
     C, KF, _ = fl.shape
     out = np.empty((B, C, H, W), np.float32)
     _load().orc_filter(im, B, H, W, fl, C, KF, float(thr), out)
+    return out
+
+
+def local_normalize(inten: np.ndarray, radius: int, eps: float = 1e-12) -> np.ndarray:
+    """Intensities [B,C,H,W] divided by their per-channel regional mean (window
+    2r+1, zero padding) plus eps, in a fixed operation order (see orc.c)."""
+    x = _c(inten, np.float32)
+    B, C, H, W = x.shape
+    out = np.empty_like(x)
+    _load().orc_local_normalize(x, B, C, H, W, radius, eps, out)
     return out
 
 

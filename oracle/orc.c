@@ -93,6 +93,43 @@ ORC_API void orc_filter(const uint8_t *img, int64_t B, int H, int W,
 }
 
 /* ------------------------------------------------------------------ */
+/* Local normalisation (section "functional Module": intensities normalised
+ * by their regional mean; the tutorial applies it between filtering and the
+ * latency code).  A reading, the paper gives no formula: per channel, the
+ * mean over the (2r+1)x(2r+1) window centred on the entry, the image
+ * zero-padded (padding counts in the window size), then
+ *     out = in / (mean + eps).
+ * Operation order, fixed: row sums R(y', x) = sum over dx of in(y', x+dx)
+ * (double, dx ascending), window sum S = sum over dy of R(y+dy, x) (double,
+ * dy ascending), mean = float(S / (2r+1)^2), then float mean + eps and a
+ * float division. */
+ORC_API void orc_local_normalize(const float *in, int64_t B, int C, int H, int W, int r, float eps,
+                                 float *out) {
+    double n = (double)(2 * r + 1) * (double)(2 * r + 1);
+    for (int64_t b = 0; b < B; ++b)
+        for (int c = 0; c < C; ++c) {
+            const float *src = in + (b * C + c) * (int64_t)H * W;
+            float *dst = out + (b * C + c) * (int64_t)H * W;
+            for (int y = 0; y < H; ++y)
+                for (int x = 0; x < W; ++x) {
+                    double S = 0.0;
+                    for (int dy = -r; dy <= r; ++dy) {
+                        double R = 0.0;
+                        for (int dx = -r; dx <= r; ++dx) {
+                            int yy = y + dy, xx = x + dx;
+                            if (yy >= 0 && yy < H && xx >= 0 && xx < W) R += (double)src[(int64_t)yy * W + xx];
+                            else R += 0.0;
+                        }
+                        S += R;
+                    }
+                    float mean = (float)(S / n);
+                    float d = mean + eps;
+                    dst[(int64_t)y * W + x] = src[(int64_t)y * W + x] / d;
+                }
+        }
+}
+
+/* ------------------------------------------------------------------ */
 /* Intensity-to-latency, rank-order coding (sections "utils Module" and the
  * abstract: rank-order encoding).  Per image, all channels together: the n
  * positive intensities are ranked from largest to smallest (equal values by

@@ -39,6 +39,9 @@ _SIGS = {
     "spk_encode_latency_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
     "spk_encode_latency": (_I, [_P, _I, _I, _I, _P, _I, _I, _F, _I, _P, _P, _P, _P, _Z, _P]),
     "spk_expand_wave": (_I, [_P, _I, _I, _I, _I, _I, _P, _P]),
+    "spk_rank_latency_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
+    "spk_rank_latency": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _Z, _P]),
+    "spk_local_normalization": (_I, [_P, _I, _I, _I, _I, _I, _F, _P, _P]),
     "spk_validate_wave": (_I, [_P, _I, _I, _I, _I, _I, _P, _P]),
     "spk_conv_fire_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I]),
     "spk_conv_fire": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z, _P]),
@@ -150,6 +153,34 @@ def spk_encode_latency(image, filters, T, filter_threshold=0.0, wave=None, t_fir
     _check(_lib.spk_encode_latency(_ptr(image), B, H, W, _ptr(filters), C, KF, float(filter_threshold), T,
                                    _ptr(wave), _ptr(t_first), _ptr(intensities), _ptr(ws), n, _stream(stream)))
     return wave, t_first, intensities
+
+
+def spk_rank_latency_workspace_size(B, C, H, W, T) -> int:
+    return int(_lib.spk_rank_latency_workspace_size(B, C, H, W, T))
+
+
+def spk_rank_latency(intensities, T, wave=None, t_first=None, workspace=None, stream=None):
+    """Rank-order code of an intensity map f32 [B,C,H,W] -> (wave u8 [B,T,C,H,W], t_first u8 [B,C,H,W])."""
+    B, C, H, W = intensities.shape
+    _need(intensities, torch.float32, (B, C, H, W), "intensities")
+    dev = intensities.device
+    wave = _out(wave, (B, T, C, H, W), torch.uint8, dev, "wave")
+    t_first = _out(t_first, (B, C, H, W), torch.uint8, dev, "t_first")
+    n = spk_rank_latency_workspace_size(B, C, H, W, T)
+    ws = _ws(workspace, n, dev)
+    _check(_lib.spk_rank_latency(_ptr(intensities), B, C, H, W, T, _ptr(wave), _ptr(t_first), _ptr(ws), n,
+                                 _stream(stream)))
+    return (wave if wave is not False else None), (t_first if t_first is not False else None)
+
+
+def spk_local_normalization(intensities, radius, eps=1e-12, out=None, stream=None):
+    """Intensities f32 [B,C,H,W] divided by their per-channel regional mean plus eps."""
+    B, C, H, W = intensities.shape
+    _need(intensities, torch.float32, (B, C, H, W), "intensities")
+    out = _out(out, (B, C, H, W), torch.float32, intensities.device, "out")
+    _check(_lib.spk_local_normalization(_ptr(intensities), B, C, H, W, radius, float(eps), _ptr(out),
+                                        _stream(stream)))
+    return out
 
 
 def spk_expand_wave(t_first, T, wave=None, stream=None):

@@ -385,6 +385,36 @@ __global__ __launch_bounds__(SORT_THREADS) void k_rank_sort(const float *__restr
     }
 }
 
+// ------------------------------------------------------------------ local normalisation
+// One thread per entry: out = in / (float(S / (2r+1)^2) + eps), where S sums
+// the zero-padded window of the entry's channel as row sums (double, dx
+// ascending) added over the rows (dy ascending) -- the operation order the
+// definition fixes, so the result is reproducible bit for bit.
+__global__ __launch_bounds__(256) void k_local_norm(const float *__restrict__ in, int64_t total, int H, int W, int r,
+                                                    float eps, float *__restrict__ out) {
+#pragma clang fp contract(off)
+    const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (o >= total) return;
+    const int64_t pl = o / ((int64_t)H * W);
+    const int rem = (int)(o - pl * H * W), y = rem / W, x = rem - y * W;
+    const float *src = in + pl * H * W;
+    double S = 0.0;
+    for (int dy = -r; dy <= r; ++dy) {
+        const int yy = y + dy;
+        double R = 0.0;
+        if (yy >= 0 && yy < H)
+            for (int dx = -r; dx <= r; ++dx) {
+                const int xx = x + dx;
+                R += (xx >= 0 && xx < W) ? (double)src[(int64_t)yy * W + xx] : 0.0;
+            }
+        S += R;
+    }
+    const double n = (double)(2 * r + 1) * (double)(2 * r + 1);
+    const float mean = (float)(S / n);
+    const float d = mean + eps;
+    out[o] = src[(int64_t)y * W + x] / d;
+}
+
 // ------------------------------------------------------------------ Eq.1 utilities
 __global__ __launch_bounds__(256) void k_expand_wave(const uint8_t *__restrict__ tf, int64_t N, int T,
                                                      uint8_t *__restrict__ wave, int64_t total_groups,
@@ -441,6 +471,21 @@ int enc_plan(int B, int C, int H, int W, int T, EncPlan &p) {
     return SPK_OK;
 }
 
+// The rank-order code of an intensity map: one sorting kernel per image when it
+// fits in LDS, else the bin boundaries by radix select and a separate expansion.
+void launch_rank(const float *I, int B, int64_t N, int T, uint8_t *t_first, uint8_t *wave, uint64_t *bounds,
+                 uint32_t *count, hipStream_t st) {
+    if (N <= SORT_MAX) {
+        hipLaunchKernelGGL(k_rank_sort, dim3(B), dim3(SORT_THREADS), 0, st, I, (int)N, T, t_first, wave);
+        return;
+    }
+    if (T > 1) hipLaunchKernelGGL(k_rank_select, dim3(B), dim3(SEL_THREADS), 0, st, I, N, T, bounds, count);
+    const int64_t groups = (N + 3) / 4;
+    const int chunks = (int)std::max<int64_t>(1, std::min<int64_t>(64, spk::ceil_div(groups, 256)));
+    hipLaunchKernelGGL(k_expand_latency, dim3((unsigned)(B * chunks)), dim3(256), 0, st, I, N, T, bounds, t_first,
+                       wave, chunks);
+}
+
 }  // namespace
 
 extern "C" size_t spk_encode_latency_workspace_size(int B, int C, int H, int W, int T) {
@@ -490,17 +535,50 @@ extern "C" int spk_encode_latency(const uint8_t *image, int B, int H, int W, con
     hipLaunchKernelGGL(k_filter, dim3((unsigned)(B * nb)), dim3(256), filter_lds(R), st, image, B, H, W, filters, C,
                        KF, filter_threshold, R, I);
     if (!t_first && !wave) return spk::check_launch("spk_encode_latency");
-    if (p.N <= SORT_MAX) {
-        hipLaunchKernelGGL(k_rank_sort, dim3(B), dim3(SORT_THREADS), 0, st, I, (int)p.N, T, t_first, wave);
-        return spk::check_launch("spk_encode_latency");
-    }
-    if (T > 1)
-        hipLaunchKernelGGL(k_rank_select, dim3(B), dim3(SEL_THREADS), 0, st, I, p.N, T, bounds, count);
-    const int64_t groups = (p.N + 3) / 4;
-    const int chunks = (int)std::max<int64_t>(1, std::min<int64_t>(64, spk::ceil_div(groups, 256)));
-    hipLaunchKernelGGL(k_expand_latency, dim3((unsigned)(B * chunks)), dim3(256), 0, st, I, p.N, T, bounds,
-                       t_first, wave, chunks);
+    launch_rank(I, B, p.N, T, t_first, wave, bounds, count, st);
     return spk::check_launch("spk_encode_latency");
+}
+
+extern "C" size_t spk_rank_latency_workspace_size(int B, int C, int H, int W, int T) {
+    EncPlan p;
+    if (enc_plan(B, C, H, W, T, p) != SPK_OK) return 0;
+    spk::Carver c(nullptr);
+    c.take<uint64_t>(p.bound_bytes / sizeof(uint64_t));
+    c.take<uint32_t>(p.count_bytes / sizeof(uint32_t));
+    return spk::align_up(c.off, 256);
+}
+
+extern "C" int spk_rank_latency(const float *intensities, int B, int C, int H, int W, int T, uint8_t *wave,
+                                uint8_t *t_first, void *workspace, size_t ws_bytes, void *stream) {
+    EncPlan p;
+    int rc = enc_plan(B, C, H, W, T, p);
+    if (rc != SPK_OK) return rc;
+    if (B == 0) return spk::ok();
+    SPK_REQUIRE(intensities && (wave || t_first), SPK_E_ARG,
+                "spk_rank_latency: intensities and wave or t_first are required");
+    const size_t need = spk_rank_latency_workspace_size(B, C, H, W, T);
+    SPK_REQUIRE(workspace && ws_bytes >= need, SPK_E_WORKSPACE, "spk_rank_latency: workspace of %zu bytes < %zu required",
+                ws_bytes, need);
+    spk::Carver cv(workspace);
+    uint64_t *bounds = cv.take<uint64_t>(p.bound_bytes / sizeof(uint64_t));
+    uint32_t *count = cv.take<uint32_t>(p.count_bytes / sizeof(uint32_t));
+    launch_rank(intensities, B, p.N, T, t_first, wave, bounds, count, spk::as_stream(stream));
+    return spk::check_launch("spk_rank_latency");
+}
+
+extern "C" int spk_local_normalization(const float *intensities, int B, int C, int H, int W, int radius, float eps,
+                                       float *out, void *stream) {
+    SPK_REQUIRE(B >= 0 && C >= 1 && H >= 1 && W >= 1, SPK_E_SHAPE, "spk_local_normalization: bad sizes");
+    SPK_REQUIRE(radius >= 0 && radius <= 1024, SPK_E_RANGE, "spk_local_normalization: radius %d", radius);
+    SPK_REQUIRE(!std::isnan(eps), SPK_E_ARG, "spk_local_normalization: eps is NaN");
+    if (B == 0) return spk::ok();
+    SPK_REQUIRE(intensities && out && intensities != out, SPK_E_ARG,
+                "spk_local_normalization: intensities and a separate out are required");
+    const int64_t total = (int64_t)B * C * H * W;
+    SPK_REQUIRE(spk::ceil_div(total, 256) < (1LL << 31), SPK_E_RANGE, "spk_local_normalization: too large");
+    hipLaunchKernelGGL(k_local_norm, dim3((unsigned)spk::ceil_div(total, 256)), dim3(256), 0, spk::as_stream(stream),
+                       intensities, total, H, W, radius, eps, out);
+    return spk::check_launch("spk_local_normalization");
 }
 
 extern "C" int spk_expand_wave(const uint8_t *t_first, int B, int T, int C, int H, int W, uint8_t *wave,

@@ -6,6 +6,8 @@ calls on one stream, with no host synchronisation and no allocation inside
 :meth:`Chain.forward` / :meth:`Chain.learn`:
 
 * source: ``spk_encode_latency`` (images + filter bank) or a given wave;
+  with ``local_norm=(radius, eps)`` the filter map is locally normalised
+  (``spk_local_normalization``) before ``spk_rank_latency`` codes it;
 * each conv stage: ``spk_conv_fire`` then ``spk_kwta`` (the winners feed
   plasticity and, for the last layer, the decision); when its input is the
   encoder's or a pool's output, whose wave is Eq.1 of its first-spike map by
@@ -36,7 +38,8 @@ import torch
 from . import (pool_out_size, conv_out_size, spk_conv_fire, spk_conv_fire_first_spike, spk_conv_fire_workspace_size,
                spk_decide,
                spk_encode_latency, spk_encode_latency_workspace_size, spk_kwta, spk_kwta_workspace_size,
-               spk_pool, spk_pool_first_spike, spk_rstdp, spk_stdp, spk_stdp_workspace_size)
+               spk_local_normalization, spk_pool, spk_pool_first_spike, spk_rank_latency, spk_rstdp, spk_stdp,
+               spk_stdp_workspace_size)
 
 
 def _is_conv(st):
@@ -46,7 +49,7 @@ def _is_conv(st):
 class Chain:
     def __init__(self, stages, B, T, H, W, cin, source="image", filter_bank=None, filter_threshold=0.0,
                  n_classes=10, device="cuda", want_potentials=True, pool_from_first_spike=True,
-                 concurrent_learn=True, want_spikes=True):
+                 concurrent_learn=True, want_spikes=True, local_norm=None):
         self.stages = list(stages)
         self.pool_from_first_spike = pool_from_first_spike
         self.B, self.T, self.source = B, T, source
@@ -60,9 +63,15 @@ class Chain:
             C = self.bank.shape[0]
             self.image = torch.zeros((B, H, W), dtype=u8, device=dev)
             ws_bytes = max(ws_bytes, spk_encode_latency_workspace_size(B, C, H, W, T))
+            # local_norm = (radius, eps): filter, spk_local_normalization, then the rank-order code
+            self.local_norm = local_norm
+            if local_norm is not None:
+                self.inten = torch.empty((B, C, H, W), dtype=f32, device=dev)
+                self.inten_norm = torch.empty((B, C, H, W), dtype=f32, device=dev)
         else:
             C = cin
             self.image = None
+            self.local_norm = None
         self.input_wave = torch.zeros((B, T, C, H, W), dtype=u8, device=dev)
         self.input_tf = torch.zeros((B, C, H, W), dtype=u8, device=dev) if source == "image" else None
         self.bufs = []
@@ -148,8 +157,16 @@ class Chain:
         self._wait_pending(-1, main)
         if self.source == "image":
             mark("encode", 0)
-            spk_encode_latency(self.image, self.bank, self.T, self.filter_threshold, wave=self.input_wave,
-                               t_first=self.input_tf, intensities=False, workspace=self.workspace, stream=stream)
+            if self.local_norm is None:
+                spk_encode_latency(self.image, self.bank, self.T, self.filter_threshold, wave=self.input_wave,
+                                   t_first=self.input_tf, intensities=False, workspace=self.workspace, stream=stream)
+            else:
+                spk_encode_latency(self.image, self.bank, self.T, self.filter_threshold, wave=False, t_first=False,
+                                   intensities=self.inten, workspace=self.workspace, stream=stream)
+                spk_local_normalization(self.inten, self.local_norm[0], self.local_norm[1], out=self.inten_norm,
+                                        stream=stream)
+                spk_rank_latency(self.inten_norm, self.T, wave=self.input_wave, t_first=self.input_tf,
+                                 workspace=self.workspace, stream=stream)
             mark("encode", 1)
         x, x_tf = self.input_wave, self.input_tf
         x_exact = x_tf is not None  # x is Eq.1 of x_tf

@@ -341,6 +341,43 @@ def test_encode_parity(case):
     assert_equal(host(wave), rwave, "wave")
 
 
+@pytest.mark.parametrize("r", [0, 2, 8, 30])
+def test_local_normalization_parity(r):
+    g = synth.rng(900 + r, 0)
+    x = np.abs(g.normal(0, 40, (3, 6, 28, 28))).astype(np.float32)  # general floats: the fixed order decides
+    x[:, :, :4] = 0.0
+    out = spk.spk_local_normalization(dev(x), r, 1e-6)
+    sync()
+    assert_equal(host(out).view(np.uint32), orc.local_normalize(x, r, 1e-6).view(np.uint32), "normalised (bits)")
+
+
+@pytest.mark.parametrize("shape,T", [((3, 6, 28, 28), 15), ((2, 4, 41, 50), 15), ((2, 2, 5, 7), 30)])
+def test_rank_latency_parity(shape, T):
+    g = synth.rng(950 + T + shape[1], 0)
+    x = (g.integers(-20, 60, shape) * 0.5).astype(np.float32)  # ties and non-positive entries
+    wave, tf = spk.spk_rank_latency(dev(x), T)
+    sync()
+    rtf = orc.rank_latency(x, T)
+    assert_equal(host(tf), rtf, "t_first")
+    assert_equal(host(wave), orc.expand_wave(rtf, T), "wave")
+
+
+def test_chain_encode_with_local_normalization():
+    # filter -> local normalisation (radius 8, the tutorial's) -> rank-order code, against the oracle's steps
+    from paper_1903_02440_amd.pipeline import chain_for
+    wl = synth.mnist_single(4)
+    inp = synth.make_inputs(wl)
+    ch = chain_for(wl, inp["bank"], local_norm=(8, 1e-12))
+    ch.set_weights([torch.from_numpy(w) for w in inp["weights"]])
+    ch.set_input(image=torch.from_numpy(inp["image"]))
+    ch.forward()
+    sync()
+    I = orc.filter_images(inp["image"], inp["bank"], 0.0)
+    rtf = orc.rank_latency(orc.local_normalize(I, 8, 1e-12), wl.T)
+    assert_equal(host(ch.input_tf), rtf, "t_first")
+    assert_equal(host(ch.input_wave), orc.expand_wave(rtf, wl.T), "wave")
+
+
 def test_encode_blank_image_never_spikes():
     img = np.zeros((2, 28, 28), np.uint8)
     wave, tf, _ = spk.spk_encode_latency(dev(img), dev(synth.dog_bank()), 15)

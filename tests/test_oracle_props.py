@@ -404,3 +404,25 @@ def test_pointwise_inhibition_second_formulation():
                     assert ot[b, c, y, x] == (tf[b, c, y, x] if keep else T)
                     assert ov[b, c, y, x] == (vf[b, c, y, x] if keep else 0.0)
                     assert np.array_equal(op[b, :, c, y, x], pot[b, :, c, y, x] if keep else np.zeros(T, np.float32))
+
+
+@pytest.mark.parametrize("r", [0, 1, 3, 8, 40])
+def test_local_normalize_against_box_sums(r):
+    """Exactly summable intensities (multiples of 1/16 below 2^12): every
+    window sum is exact in double whatever the order, so a box sum from a
+    padded array and float32 arithmetic reproduce the oracle bit for bit; r = 0
+    gives in / (in + eps), and a window beyond the image sees the zero padding."""
+    g = np.random.default_rng(40 + r)
+    x = (g.integers(0, 1 << 16, (2, 3, 9, 13)) / 16.0).astype(np.float32)
+    eps = np.float32(1e-3)
+    got = orc.local_normalize(x, r, float(eps))
+    xp = np.pad(x.astype(np.float64), ((0, 0), (0, 0), (r, r), (r, r)))
+    S = np.zeros(x.shape, np.float64)
+    for dy in range(2 * r + 1):
+        for dx in range(2 * r + 1):
+            S += xp[:, :, dy:dy + 9, dx:dx + 13]
+    mean = (S / float((2 * r + 1) ** 2)).astype(np.float32)
+    ref = x / (mean + eps)
+    assert np.array_equal(got, ref)
+    if r == 0:
+        assert np.array_equal(got, x / (x + eps))
