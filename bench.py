@@ -163,6 +163,59 @@ def online_bench(wl, inp, dev, group):
                                  "form": "compact (no per-step potentials)"}}), flush=True)
 
 
+def ops_bench(wl, inp, dev, reps=10):
+    """Per-op device time (HIP events on the current stream, median of `reps`) and
+    algorithmic bytes of the variant ops, on tensors of the workload's first two
+    conv stages: local normalisation (radius 8) and the rank-order code of the
+    filter map, pointwise inhibition of the second conv's first-spike map (with
+    its wave), and 2x2 pooling of the first conv's potentials."""
+    import torch
+    import paper_1903_02440_amd as spk
+    from paper_1903_02440_amd.pipeline import chain_for
+    ch = chain_for(wl, inp["bank"], device=dev)
+    ch.set_weights([torch.from_numpy(w) for w in inp["weights"]])
+    ch.set_input(image=torch.from_numpy(inp["image"]), labels=torch.from_numpy(inp["labels"]))
+    ch.forward()
+    _, _, I = spk.spk_encode_latency(ch.image, ch.bank, wl.T, wave=False, t_first=False, intensities=None)
+    convs = ch.conv_stages()
+    b1, b2 = ch.bufs[convs[0]], ch.bufs[convs[1]]
+    In = torch.empty_like(I)
+    wave, tfl = spk.spk_rank_latency(In, wl.T)
+    ws = torch.empty(spk.spk_rank_latency_workspace_size(*I.shape, wl.T), dtype=torch.uint8, device=dev)
+    otf, ovf = torch.empty_like(b2["tf"]), torch.empty_like(b2["vf"])
+    B, C2, H2, W2 = b2["tf"].shape
+    owave = torch.empty((B, wl.T, C2, H2, W2), dtype=torch.uint8, device=dev)
+    pp = spk.spk_pool_potentials(b1["P"], 2)
+    NI, N2 = I.numel(), b2["tf"].numel()
+    ops = {
+        "local_normalization_r8": (lambda: spk.spk_local_normalization(I, 8, 1e-12, out=In), 8 * NI),
+        "rank_latency": (lambda: spk.spk_rank_latency(In, wl.T, wave=wave, t_first=tfl, workspace=ws),
+                         4 * NI + (wl.T + 1) * NI),
+        "pointwise_inhibition_conv2_with_wave": (
+            lambda: spk.spk_pointwise_inhibition(b2["tf"], b2["vf"], wl.T, out_t_first=otf, out_v_first=ovf,
+                                                 out_wave=owave), 10 * N2 + wl.T * N2),
+        "pool_potentials_conv1_2x2": (lambda: spk.spk_pool_potentials(b1["P"], 2, out=pp),
+                                      4 * b1["P"].numel() + 4 * pp.numel()),
+    }
+    res = {}
+    for name, (fn, nbytes) in ops.items():
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ms = sorted(ts)[len(ts) // 2]
+        res[name] = {"ms": round(ms, 4), "algorithmic_bytes": int(nbytes), "GB_per_s": round(nbytes / ms / 1e6, 1),
+                     "frac_of_8TBps": round(nbytes / ms / 1e6 / 8000.0, 3)}
+    print(json.dumps({"metric": "variant ops: device time and achieved bandwidth", "workload": wl.name,
+                      "global_batch": wl.B, "ops": res}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -178,6 +231,9 @@ def main():
                     help="only time online plasticity (one image per step, graph-replayed groups of "
                          "--online-group steps) over N images of the workload and exit (a separate figure)")
     ap.add_argument("--online-group", type=int, default=32, help="steps per captured graph with --online")
+    ap.add_argument("--ops", action="store_true",
+                    help="only time the variant ops (local normalisation, rank-order code, pointwise inhibition, "
+                         "pooling of potentials) at the workload's shapes and exit (a separate figure)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes 5 times (the reference "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -206,6 +262,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.online:
         online_bench(wl, inp, dev, args.online_group)
+        return
+    if args.ops:
+        ops_bench(wl, inp, dev)
         return
     ch = chain_for(wl, inp.get("bank"), device=dev, want_potentials=not args.compact,
                    want_spikes=not args.compact)

@@ -101,7 +101,8 @@ SPK_API int spk_rank_latency(const float *intensities, int B, int C, int H, int 
  * result is reproducible: row sums in double (dx ascending), their sum in
  * double (dy ascending), mean = float(sum / (2r+1)^2), then float mean + eps
  * and a correctly rounded float division.  intensities, out f32
- * [B][C][H][W], not overlapping.  Limits: 0 <= radius <= 1024.              */
+ * [B][C][H][W], not overlapping.  Limits: radius >= 0 and
+ * (2*radius + 1) * (12*W + 8*radius) <= 61440 (the rows of one window in LDS). */
 SPK_API int spk_local_normalization(const float *intensities, int B, int C, int H, int W, int radius,
                                     float eps, float *out, void *stream);
 

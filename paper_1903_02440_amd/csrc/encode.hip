@@ -386,33 +386,56 @@ __global__ __launch_bounds__(SORT_THREADS) void k_rank_sort(const float *__restr
 }
 
 // ------------------------------------------------------------------ local normalisation
-// One thread per entry: out = in / (float(S / (2r+1)^2) + eps), where S sums
-// the zero-padded window of the entry's channel as row sums (double, dx
-// ascending) added over the rows (dy ascending) -- the operation order the
-// definition fixes, so the result is reproducible bit for bit.
-__global__ __launch_bounds__(256) void k_local_norm(const float *__restrict__ in, int64_t total, int H, int W, int r,
+// out = in / (float(S / (2r+1)^2) + eps), S the sum of the zero-padded window
+// of the entry's channel taken as row sums R(y', x) (double, dx ascending)
+// added over the rows (dy ascending) -- the order the definition fixes, so
+// the result is reproducible bit for bit.  A row sum is the same value for
+// every entry that uses it, so a workgroup computes each once: it takes a
+// tile of TR output rows of one plane, stages the TR + 2r input rows with
+// their zero margins in LDS, computes their row sums into LDS, then adds
+// 2r + 1 of them per entry.
+__global__ __launch_bounds__(256) void k_local_norm(const float *__restrict__ in, int H, int W, int r, int TR,
                                                     float eps, float *__restrict__ out) {
 #pragma clang fp contract(off)
-    const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (o >= total) return;
-    const int64_t pl = o / ((int64_t)H * W);
-    const int rem = (int)(o - pl * H * W), y = rem / W, x = rem - y * W;
+    extern __shared__ double lnsm[];
+    const int ntile = (H + TR - 1) / TR;
+    const int64_t pl = blockIdx.x / ntile;
+    const int y0 = (int)(blockIdx.x % ntile) * TR;
+    const int rows = min(TR, H - y0), srows = rows + 2 * r, Wp = W + 2 * r;
+    double *R = lnsm;                                          // srows x W row sums
+    float *xs = reinterpret_cast<float *>(R + (size_t)srows * W);  // srows x Wp padded input
     const float *src = in + pl * H * W;
-    double S = 0.0;
-    for (int dy = -r; dy <= r; ++dy) {
-        const int yy = y + dy;
-        double R = 0.0;
-        if (yy >= 0 && yy < H)
-            for (int dx = -r; dx <= r; ++dx) {
-                const int xx = x + dx;
-                R += (xx >= 0 && xx < W) ? (double)src[(int64_t)yy * W + xx] : 0.0;
-            }
-        S += R;
+    for (int i = threadIdx.x; i < srows * Wp; i += blockDim.x) {
+        const int rr = i / Wp, cc = i - rr * Wp;
+        const int y = y0 - r + rr, x = cc - r;
+        xs[i] = (y >= 0 && y < H && x >= 0 && x < W) ? src[(int64_t)y * W + x] : 0.0f;
     }
+    __syncthreads();
+    for (int i = threadIdx.x; i < srows * W; i += blockDim.x) {
+        const int rr = i / W, x = i - rr * W;
+        const float *row = xs + rr * Wp + x;
+        double acc = 0.0;
+        for (int dx = 0; dx <= 2 * r; ++dx) acc += (double)row[dx];
+        R[i] = acc;
+    }
+    __syncthreads();
     const double n = (double)(2 * r + 1) * (double)(2 * r + 1);
-    const float mean = (float)(S / n);
-    const float d = mean + eps;
-    out[o] = src[(int64_t)y * W + x] / d;
+    float *dst = out + pl * H * W;
+    for (int i = threadIdx.x; i < rows * W; i += blockDim.x) {
+        const int yy = i / W, x = i - yy * W;
+        double S = 0.0;
+        for (int dy = 0; dy <= 2 * r; ++dy) S += R[(yy + dy) * W + x];
+        const float mean = (float)(S / n);
+        const float d = mean + eps;
+        dst[(int64_t)(y0 + yy) * W + x] = xs[(yy + r) * Wp + x + r] / d;
+    }
+}
+
+// Output rows per workgroup of the local normalisation: as many as LDS holds.
+int local_norm_rows(int H, int W, int r) {
+    const size_t per_row = (size_t)W * sizeof(double) + (size_t)(W + 2 * r) * sizeof(float);
+    const size_t cap = 60 * 1024 / per_row;
+    return cap > (size_t)(2 * r) ? (int)std::min<size_t>(H, cap - 2 * r) : 0;
 }
 
 // ------------------------------------------------------------------ Eq.1 utilities
@@ -574,10 +597,14 @@ extern "C" int spk_local_normalization(const float *intensities, int B, int C, i
     if (B == 0) return spk::ok();
     SPK_REQUIRE(intensities && out && intensities != out, SPK_E_ARG,
                 "spk_local_normalization: intensities and a separate out are required");
-    const int64_t total = (int64_t)B * C * H * W;
-    SPK_REQUIRE(spk::ceil_div(total, 256) < (1LL << 31), SPK_E_RANGE, "spk_local_normalization: too large");
-    hipLaunchKernelGGL(k_local_norm, dim3((unsigned)spk::ceil_div(total, 256)), dim3(256), 0, spk::as_stream(stream),
-                       intensities, total, H, W, radius, eps, out);
+    const int TR = local_norm_rows(H, W, radius);
+    SPK_REQUIRE(TR >= 1, SPK_E_RANGE, "spk_local_normalization: radius %d on width %d does not fit", radius, W);
+    const int64_t blocks = (int64_t)B * C * ((H + TR - 1) / TR);
+    SPK_REQUIRE(blocks < (1LL << 31), SPK_E_RANGE, "spk_local_normalization: too large");
+    const int srows = std::min(TR, H) + 2 * radius;
+    const size_t lds = (size_t)srows * W * sizeof(double) + (size_t)srows * (W + 2 * radius) * sizeof(float);
+    hipLaunchKernelGGL(k_local_norm, dim3((unsigned)blocks), dim3(256), lds, spk::as_stream(stream), intensities, H,
+                       W, radius, TR, eps, out);
     return spk::check_launch("spk_local_normalization");
 }
 

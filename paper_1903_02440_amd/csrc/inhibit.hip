@@ -8,48 +8,100 @@
 
 namespace {
 
-// One thread per location of one image: the winner over the C features (the
-// kWTA order: earlier spike, then larger potential, then lower feature index),
-// then every feature's surviving first-spike time and potential, and, when
-// asked, the survivors' Eq.1 wave and the masked potentials.  All C features
-// of the location are read before any is written, so the first-spike outputs
-// may alias the inputs.  Consecutive threads take consecutive locations, so
-// every per-feature access of a wave is contiguous.
+// One thread per location of one image (VEC: per 4 consecutive locations,
+// with 4-byte / 16-byte accesses; the map size is then a multiple of 4): the
+// winner over the C features (the kWTA order: earlier spike, then larger
+// potential, then lower feature index), then every feature's surviving
+// first-spike time and potential, and, when asked, the survivors' Eq.1 wave
+// and the masked potentials.  All C features of the locations are read before
+// any is written, so the first-spike outputs may alias the inputs.
+// Consecutive threads take consecutive locations, so every per-feature
+// access of a wave is contiguous.
+template <bool VEC>
 __global__ __launch_bounds__(256) void k_pointwise(const uint8_t *tf, const float *vf, int64_t B, int T, int C,
                                                    int64_t HW, uint8_t *out_t, float *out_v, uint8_t *wave,
                                                    float *pot) {
+    constexpr int L = VEC ? 4 : 1;
+    const int64_t per_img = HW / L;
     const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (q >= B * HW) return;
-    const int64_t b = q / HW, p = q - b * HW;
+    if (q >= B * per_img) return;
+    const int64_t b = q / per_img, p = (q - b * per_img) * L;
     const int64_t base = b * C * HW + p;
-    int best = -1, bt = T;
-    float bv = 0.0f;
-    for (int c = 0; c < C; ++c) {
-        const int t = tf[base + c * HW];
-        if (t >= T) continue;
-        const float v = vf[base + c * HW];
-        if (best < 0 || t < bt || (t == bt && v > bv)) {
-            best = c;
-            bt = t;
-            bv = v;
-        }
+    int best[L], bt[L];
+    float bv[L];
+#pragma unroll
+    for (int j = 0; j < L; ++j) {
+        best[j] = -1;
+        bt[j] = T;
+        bv[j] = 0.0f;
     }
     for (int c = 0; c < C; ++c) {
-        const bool keep = c == best;
-        out_t[base + c * HW] = keep ? (uint8_t)bt : (uint8_t)T;
-        out_v[base + c * HW] = keep ? bv : 0.0f;
+        int t[L];
+        float v[L];
+        if (VEC) {
+            const uint32_t t4 = *reinterpret_cast<const uint32_t *>(tf + base + c * HW);
+            const float4 v4 = *reinterpret_cast<const float4 *>(vf + base + c * HW);
+            t[0] = t4 & 255u; t[L > 1 ? 1 : 0] = (t4 >> 8) & 255u;
+            t[L > 2 ? 2 : 0] = (t4 >> 16) & 255u; t[L > 3 ? 3 : 0] = t4 >> 24;
+            v[0] = v4.x; v[L > 1 ? 1 : 0] = v4.y; v[L > 2 ? 2 : 0] = v4.z; v[L > 3 ? 3 : 0] = v4.w;
+        } else {
+            t[0] = tf[base + c * HW];
+            v[0] = vf[base + c * HW];
+        }
+#pragma unroll
+        for (int j = 0; j < L; ++j)
+            if (t[j] < T && (best[j] < 0 || t[j] < bt[j] || (t[j] == bt[j] && v[j] > bv[j]))) {
+                best[j] = c;
+                bt[j] = t[j];
+                bv[j] = v[j];
+            }
+    }
+    // the surviving first-spike times of feature c, 4 to a word
+    auto word = [&](int c) {
+        uint32_t w = 0;
+#pragma unroll
+        for (int j = 0; j < L; ++j) w |= (uint32_t)(c == best[j] ? bt[j] : T) << (8 * j);
+        return w;
+    };
+    for (int c = 0; c < C; ++c) {
+        if (VEC) {
+            *reinterpret_cast<uint32_t *>(out_t + base + c * HW) = word(c);
+            *reinterpret_cast<float4 *>(out_v + base + c * HW) =
+                float4{c == best[0] ? bv[0] : 0.0f, c == best[L > 1 ? 1 : 0] ? bv[L > 1 ? 1 : 0] : 0.0f,
+                       c == best[L > 2 ? 2 : 0] ? bv[L > 2 ? 2 : 0] : 0.0f,
+                       c == best[L > 3 ? 3 : 0] ? bv[L > 3 ? 3 : 0] : 0.0f};
+        } else {
+            out_t[base + c * HW] = (uint8_t)(c == best[0] ? bt[0] : T);
+            out_v[base + c * HW] = c == best[0] ? bv[0] : 0.0f;
+        }
     }
     const int64_t plane = (int64_t)C * HW;
     if (wave)
         for (int t = 0; t < T; ++t) {
             uint8_t *w = wave + (b * T + t) * plane + p;
-            for (int c = 0; c < C; ++c) w[c * HW] = (uint8_t)(c == best && t >= bt);
+            for (int c = 0; c < C; ++c) {
+                if (VEC) *reinterpret_cast<uint32_t *>(w + c * HW) = spk::spikes4(word(c), t, T);
+                else w[c * HW] = (uint8_t)(c == best[0] && t >= bt[0]);
+            }
         }
     if (pot)
         for (int t = 0; t < T; ++t) {
             float *pp = pot + (b * T + t) * plane + p;
-            for (int c = 0; c < C; ++c)
-                if (c != best) pp[c * HW] = 0.0f;
+            for (int c = 0; c < C; ++c) {
+                if (VEC) {
+                    if (c == best[0] && c == best[L > 1 ? 1 : 0] && c == best[L > 2 ? 2 : 0] &&
+                        c == best[L > 3 ? 3 : 0])
+                        continue;  // the feature survives at all four locations
+                    float4 x = *reinterpret_cast<const float4 *>(pp + c * HW);
+                    if (c != best[0]) x.x = 0.0f;
+                    if (c != best[L > 1 ? 1 : 0]) x.y = 0.0f;
+                    if (c != best[L > 2 ? 2 : 0]) x.z = 0.0f;
+                    if (c != best[L > 3 ? 3 : 0]) x.w = 0.0f;
+                    *reinterpret_cast<float4 *>(pp + c * HW) = x;
+                } else if (c != best[0]) {
+                    pp[c * HW] = 0.0f;
+                }
+            }
         }
 }
 
@@ -87,8 +139,16 @@ extern "C" int spk_pointwise_inhibition(const uint8_t *t_first, const float *v_f
                 "spk_pointwise_inhibition: t_first, v_first, out_t_first and out_v_first are required");
     const int64_t HW = (int64_t)H * W, total = (int64_t)B * HW;
     SPK_REQUIRE(spk::ceil_div(total, 256) < (1LL << 31), SPK_E_RANGE, "spk_pointwise_inhibition: too large");
-    hipLaunchKernelGGL(k_pointwise, dim3((unsigned)spk::ceil_div(total, 256)), dim3(256), 0, spk::as_stream(stream),
-                       t_first, v_first, (int64_t)B, T, C, HW, out_t_first, out_v_first, out_wave, potentials);
+    auto al = [](const void *q, uintptr_t a) { return ((uintptr_t)q & (a - 1)) == 0; };
+    const bool vec = HW % 4 == 0 && al(t_first, 4) && al(out_t_first, 4) && al(out_wave, 4) && al(v_first, 16) &&
+                     al(out_v_first, 16) && al(potentials, 16);
+    hipStream_t st = spk::as_stream(stream);
+    if (vec)
+        hipLaunchKernelGGL(k_pointwise<true>, dim3((unsigned)spk::ceil_div(total / 4, 256)), dim3(256), 0, st, t_first,
+                           v_first, (int64_t)B, T, C, HW, out_t_first, out_v_first, out_wave, potentials);
+    else
+        hipLaunchKernelGGL(k_pointwise<false>, dim3((unsigned)spk::ceil_div(total, 256)), dim3(256), 0, st, t_first,
+                           v_first, (int64_t)B, T, C, HW, out_t_first, out_v_first, out_wave, potentials);
     return spk::check_launch("spk_pointwise_inhibition");
 }
 

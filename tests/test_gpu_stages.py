@@ -341,10 +341,12 @@ def test_encode_parity(case):
     assert_equal(host(wave), rwave, "wave")
 
 
-@pytest.mark.parametrize("r", [0, 2, 8, 30])
-def test_local_normalization_parity(r):
-    g = synth.rng(900 + r, 0)
-    x = np.abs(g.normal(0, 40, (3, 6, 28, 28))).astype(np.float32)  # general floats: the fixed order decides
+@pytest.mark.parametrize("r,shape", [(0, (3, 6, 28, 28)), (2, (3, 6, 28, 28)), (8, (3, 6, 28, 28)),
+                                     (30, (3, 6, 28, 28)), (8, (1, 2, 100, 250)), (3, (2, 1, 37, 5))])
+def test_local_normalization_parity(r, shape):
+    # (8, 100x250): rows split over several workgroups; general floats, so the fixed order decides
+    g = synth.rng(900 + r + shape[2], 0)
+    x = np.abs(g.normal(0, 40, shape)).astype(np.float32)
     x[:, :, :4] = 0.0
     out = spk.spk_local_normalization(dev(x), r, 1e-6)
     sync()
