@@ -13,6 +13,7 @@ HEADER = os.path.join(ROOT, "include", "libspyke.h")
 spk = pytest.importorskip("paper_1903_02440_amd")
 
 DUMMY = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
+DUMMY2 = ctypes.c_void_p(0x2000)
 
 
 def declared():
@@ -104,3 +105,28 @@ def test_zero_batch_is_a_no_op():
                              None) == spk.SPK_OK
     assert lib.spk_pool(None, 0, 15, 6, 28, 28, 2, 2, 0, None, None, None) == spk.SPK_OK
     assert lib.spk_kwta(None, None, 0, 15, 6, 28, 28, 5, 3, None, None, None, 0, None) == spk.SPK_OK
+
+
+def test_variant_op_validation_errors():
+    lib = spk.lib()
+    # pooling of potentials: window larger than the padded input, NULL buffers
+    assert lib.spk_pool_potentials(DUMMY, 1, 4, 1, 4, 4, 9, 2, 0, DUMMY, None) == spk.SPK_E_SHAPE
+    assert lib.spk_pool_potentials(DUMMY, 1, 4, 1, 4, 4, 2, 0, 0, DUMMY, None) == spk.SPK_E_SHAPE
+    assert lib.spk_pool_potentials(None, 1, 4, 1, 4, 4, 2, 2, 0, DUMMY, None) == spk.SPK_E_ARG
+    assert lib.spk_pool_potentials(None, 0, 4, 1, 4, 4, 2, 2, 0, None, None) == spk.SPK_OK
+    # pointwise inhibition: T range, required outputs (the optional ones may be NULL)
+    assert lib.spk_pointwise_inhibition(DUMMY, DUMMY, 1, 256, 2, 4, 4, DUMMY, DUMMY, None, None, None) == spk.SPK_E_RANGE
+    assert lib.spk_pointwise_inhibition(DUMMY, DUMMY, 1, 15, 2, 4, 4, None, DUMMY, None, None, None) == spk.SPK_E_ARG
+    assert lib.spk_pointwise_inhibition(None, None, 0, 15, 2, 4, 4, None, None, None, None, None) == spk.SPK_OK
+    # local normalisation: NaN eps, in-place call, a window that does not fit in LDS
+    assert lib.spk_local_normalization(DUMMY, 1, 2, 8, 8, 2, float("nan"), DUMMY2, None) == spk.SPK_E_ARG
+    assert lib.spk_local_normalization(DUMMY, 1, 2, 8, 8, 2, 1e-6, DUMMY, None) == spk.SPK_E_ARG
+    assert b"separate" in lib.spk_last_error()
+    assert lib.spk_local_normalization(DUMMY, 1, 2, 8, 2000, 64, 1e-6, DUMMY2, None) == spk.SPK_E_RANGE
+    assert lib.spk_local_normalization(DUMMY, 1, 2, 8, 8, -1, 1e-6, DUMMY2, None) == spk.SPK_E_RANGE
+    # rank-order code: workspace too small, no output
+    n = spk.spk_rank_latency_workspace_size(2, 6, 28, 28, 15)
+    assert n > 0
+    assert lib.spk_rank_latency(DUMMY, 2, 6, 28, 28, 15, DUMMY, DUMMY, DUMMY, n - 1, None) == spk.SPK_E_WORKSPACE
+    assert lib.spk_rank_latency(DUMMY, 2, 6, 28, 28, 15, None, None, DUMMY, n, None) == spk.SPK_E_ARG
+    assert lib.spk_rank_latency(DUMMY, 2, 6, 28, 28, 256, DUMMY, None, DUMMY, n, None) == spk.SPK_E_RANGE
