@@ -61,11 +61,17 @@ __global__ __launch_bounds__(256) void k_pool_first_spike(const uint8_t *__restr
     const int64_t b = blockIdx.x;
     const int hw = Ho * Wo;
     uint32_t m4 = 0;
+    // (c, yo, xo) of the first output, then stepped along x for the others
+    int c = i0 / hw, yo = (i0 - c * hw) / Wo, xo = i0 - c * hw - yo * Wo;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-        const int i = i0 + q;
-        const int c = i / hw, pix = i - c * hw;
-        const int yo = pix / Wo, xo = pix - yo * Wo;
+        if (q > 0 && ++xo == Wo) {
+            xo = 0;
+            if (++yo == Ho) {
+                yo = 0;
+                ++c;
+            }
+        }
         const int y0 = yo * R - D, x0 = xo * R - D;
         const int ya = max(y0, 0), yb = min(y0 + P, H), xa = max(x0, 0), xb = min(x0 + P, W);
         const uint8_t *src = tf + (b * C + c) * (int64_t)H * W;
@@ -102,6 +108,74 @@ __global__ __launch_bounds__(256) void k_pool_first_spike(const uint8_t *__restr
     }
 }
 
+// The same pooling with the input staged in LDS: a workgroup takes CB whole
+// input planes of one image (contiguous in memory), copies them with
+// coalesced loads, and makes their outputs 4 consecutive ones per thread, so
+// the window reads hit LDS instead of scattering bytes over many cache lines.
+// Needs CB * Ho * Wo % 4 == 0 (quads never straddle blocks) and 4-byte
+// aligned outputs.
+template <int PW>
+__global__ __launch_bounds__(256) void k_pool_first_spike_lds(const uint8_t *__restrict__ tf, int T, int C, int H,
+                                                              int W, int P, int R, int D, int Ho, int Wo, int CB,
+                                                              uint8_t *__restrict__ out, uint8_t *__restrict__ out_tf) {
+    extern __shared__ uint32_t plsm[];
+    uint8_t *lt = reinterpret_cast<uint8_t *>(plsm);
+    const int64_t b = blockIdx.x;
+    const int c0 = blockIdx.y * CB, cb = min(CB, C - c0);
+    const int HW = H * W, hw = Ho * Wo;
+    const uint8_t *src = tf + (b * C + c0) * (int64_t)HW;
+    const int nbytes = cb * HW;
+    if ((((uintptr_t)src) & 3) == 0) {
+        const int nw = nbytes >> 2;
+        for (int i = threadIdx.x; i < nw; i += 256) plsm[i] = reinterpret_cast<const uint32_t *>(src)[i];
+        for (int i = (nw << 2) + threadIdx.x; i < nbytes; i += 256) lt[i] = src[i];
+    } else {
+        for (int i = threadIdx.x; i < nbytes; i += 256) lt[i] = src[i];
+    }
+    __syncthreads();
+    const int per_img = C * hw, nq = cb * hw / 4;
+    for (int qd = threadIdx.x; qd < nq; qd += 256) {
+        const int j0 = qd * 4;  // first output of the quad within the block
+        int c = j0 / hw, yo = (j0 - c * hw) / Wo, xo = j0 - c * hw - yo * Wo;
+        uint32_t m4 = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (q > 0 && ++xo == Wo) {
+                xo = 0;
+                if (++yo == Ho) {
+                    yo = 0;
+                    ++c;
+                }
+            }
+            const int y0 = yo * R - D, x0 = xo * R - D;
+            const uint8_t *pl = lt + c * HW;
+            int m = T;
+            if (PW > 0) {
+#pragma unroll
+                for (int dy = 0; dy < PW; ++dy)
+#pragma unroll
+                    for (int dx = 0; dx < PW; ++dx) {
+                        const int y = y0 + dy, x = x0 + dx;
+                        const bool in = y >= 0 && y < H && x >= 0 && x < W;
+                        m = min(m, in ? (int)pl[y * W + x] : T);
+                    }
+            } else {
+                const int ya = max(y0, 0), yb = min(y0 + P, H), xa = max(x0, 0), xb = min(x0 + P, W);
+                for (int y = ya; y < yb; ++y)
+                    for (int x = xa; x < xb; ++x) m = min(m, (int)pl[y * W + x]);
+            }
+            m4 |= (uint32_t)m << (8 * q);
+        }
+        const int64_t i0 = (int64_t)c0 * hw + j0;
+        if (out_tf) *reinterpret_cast<uint32_t *>(out_tf + b * per_img + i0) = m4;
+        if (out) {
+            uint8_t *dst = out + b * T * (int64_t)per_img + i0;
+            for (int t = 0; t < T; ++t)
+                *reinterpret_cast<uint32_t *>(dst + (int64_t)t * per_img) = spk::spikes4(m4, t, T);
+        }
+    }
+}
+
 }  // namespace
 
 extern "C" int spk_pool_first_spike(const uint8_t *t_first, int B, int T, int C, int H, int W, int kernel,
@@ -120,8 +194,27 @@ extern "C" int spk_pool_first_spike(const uint8_t *t_first, int B, int T, int C,
     SPK_REQUIRE(per_img <= 65535LL * 256 && (int64_t)C * H * W < (1LL << 31), SPK_E_RANGE,
                 "spk_pool_first_spike: image too large");
     const bool vec = per_img % 4 == 0 && ((uintptr_t)out_wave & 3) == 0 && ((uintptr_t)out_t_first & 3) == 0;
-    const dim3 grid((unsigned)B, (unsigned)spk::ceil_div(per_img, vec ? 1024 : 256));
     hipStream_t st = spk::as_stream(stream);
+    // LDS-staged form: blocks of whole input planes (up to 16 KB), quads within a block
+    const int64_t HW = (int64_t)H * W, hw = (int64_t)Ho * Wo;
+    if (vec && HW <= 16384) {
+        // about 1024 outputs (4 per thread) per workgroup, at most 16 KB of planes
+        int CB = (int)std::min<int64_t>(std::min<int64_t>(C, 16384 / HW), std::max<int64_t>(1, (1024 + hw - 1) / hw));
+        while (CB > 1 && (CB * hw) % 4 != 0) --CB;
+        if ((CB * hw) % 4 == 0 && (C % CB == 0 || ((int64_t)(C % CB) * hw) % 4 == 0)) {
+            const dim3 g2((unsigned)B, (unsigned)spk::ceil_div(C, CB));
+            const size_t lds = spk::align_up((size_t)CB * HW, 4);
+#define SPK_POOL_LDS(PW)                                                                                          \
+    hipLaunchKernelGGL((k_pool_first_spike_lds<PW>), g2, dim3(256), lds, st, t_first, T, C, H, W, kernel, stride, pad, \
+                       Ho, Wo, CB, out_wave, out_t_first)
+            if (kernel == 2) SPK_POOL_LDS(2);
+            else if (kernel == 3) SPK_POOL_LDS(3);
+            else SPK_POOL_LDS(0);
+#undef SPK_POOL_LDS
+            return spk::check_launch("spk_pool_first_spike");
+        }
+    }
+    const dim3 grid((unsigned)B, (unsigned)spk::ceil_div(per_img, vec ? 1024 : 256));
 #define SPK_POOL(V, PW)                                                                                            \
     hipLaunchKernelGGL((k_pool_first_spike<V, PW>), grid, dim3(256), 0, st, t_first, T, C, H, W, kernel, stride, pad, \
                        Ho, Wo, out_wave, out_t_first)

@@ -148,8 +148,14 @@ def test_conv_fire_unaligned_wave():
 
 
 # ---------------------------------------------------------------- pool
+# (B, T, C, H, W, P, R, D).  First-spike pooling stages whole planes in LDS
+# (blocks of channels) when C*Ho*Wo is a multiple of 4 and a plane holds at
+# most 16 KB: the first two (a partial last block), (4x4 window with padding)
+# and (odd 5x5 output planes); the 160x250 planes and the rest take the
+# direct paths.
 POOL_CASES = [(3, 15, 30, 28, 28, 2, 2, 0), (2, 15, 250, 14, 14, 3, 3, 0), (2, 30, 4, 160, 250, 7, 6, 0),
-              (2, 7, 3, 9, 10, 3, 2, 1), (1, 5, 2, 5, 5, 5, 1, 2), (2, 3, 1, 1, 1, 1, 1, 0)]
+              (2, 7, 3, 9, 10, 3, 2, 1), (1, 5, 2, 5, 5, 5, 1, 2), (2, 3, 1, 1, 1, 1, 1, 0),
+              (2, 9, 8, 12, 12, 4, 2, 1), (2, 5, 12, 10, 10, 2, 2, 0)]
 
 
 @pytest.mark.parametrize("case", POOL_CASES)
