@@ -31,6 +31,7 @@
 #include <algorithm>
 #include <cmath>
 #include <numeric>
+#include <type_traits>
 
 #include "common.hpp"
 
@@ -277,6 +278,14 @@ __host__ __device__ constexpr int chunk_tiles_max(int G) { return G == 4 ? 16 : 
 // epilogue 16-byte write fall in distinct LDS bank groups.
 __host__ __device__ constexpr int stage_stride(int np) { return (((np + 3) / 4) | 1) * 4; }
 
+// Work of an MFMA wave on (tile slot i, 16-feature half n) in second-slot mode M
+// (0 both halves, 1 the first, 2 the second, 3 none): the first slot always has both.
+template <int M>
+__device__ constexpr bool fin_unit(int i, int n) {
+    return i == 0 || M == 0 || (M == 1 && n == 0) || (M == 2 && n == 1);
+}
+static_assert(FIN_MT == 2, "the tile slots of an MFMA wave are wv and wv + FIN_CW");
+
 template <int G, bool BLDS, bool ALDS>
 __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
@@ -374,9 +383,10 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 
     if (wv < FIN_CW) {
         // ------------------------------------------------ MFMA waves
-        // Every wave computes 4 tiles (local tiles wv, wv+4, wv+8, wv+12); tiles
-        // past the chunk repeat its last position and are never stored, which
-        // keeps the MFMA stream free of branches.
+        // Every wave computes up to two tiles of 16 positions for the 32 features;
+        // positions of a tile past the chunk repeat its last position and are
+        // never stored, which keeps the MFMA stream free of branches.  The K-step
+        // loop is compiled once per second-slot mode (below).
         const half8 *gh = whi + (int64_t)(pair * 2) * g.ksteps * 64 + lane;
         const half8 *gl = wlo + (int64_t)(pair * 2) * g.ksteps * 64 + lane;
         int abuf_sel = 0;
@@ -388,9 +398,32 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             int row0_t, w0_t, nw_t;
             region(task, row0_t, w0_t, nw_t);
             const uint8_t *abuf_t = reinterpret_cast<const uint8_t *>(abuf + abuf_sel * a_words);
+            // Local tiles: wv, and wv + 8 when the task has it.  The task's tiles are
+            // spread over the four SIMDs as waves (s, s + 4) for SIMD s; when their
+            // count is 1 mod 4 (and at least 9), the SIMD holding the last tile would
+            // carry a whole tile more than the others, so its two 16-feature halves
+            // go to two SIMDs: the owner wave computes features 0-15 of it and the
+            // next wave, whose second slot is empty, features 16-31.  A second slot
+            // past the task is skipped.
+            const int ntl = (np + 15) / 16;
+            int tile1 = wv + FIN_CW;
+            int mode1 = tile1 < ntl ? 0 : 3;  // 0 both halves, 1 first half, 2 second half, 3 none
+            if ((ntl & 3) == 1 && ntl > FIN_CW) {
+                if (wv == ntl - 1 - FIN_CW) {
+                    mode1 = 1;
+                } else if (wv == ntl - FIN_CW) {
+                    tile1 = ntl - 1;
+                    mode1 = 2;
+                }
+            }
+            if (!BLDS) {  // weight fragments from L2: one code path, the old assignment
+                tile1 = wv + FIN_CW;
+                mode1 = 0;
+            }
+            const int tl[FIN_MT] = {wv, tile1};
 #pragma unroll
             for (int i = 0; i < FIN_MT; ++i) {
-                const int gp = min(pos0 + (wv + FIN_CW * i) * 16 + c, pos0 + np - 1);
+                const int gp = min(pos0 + tl[i] * 16 + c, pos0 + np - 1);
                 const int b = gp / g.HoWo, pos = gp - b * g.HoWo;
                 const int y = pos / g.Wo, xx = pos - y * g.Wo;
                 const int row = b * g.Hp + y;
@@ -399,6 +432,9 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             }
             const bool has_next = ALDS && task + R < t_hi;
             if (has_next) fill_region(task + R, abuf + (abuf_sel ^ 1) * a_words);  // read from the next task on
+            auto blocks = [&](auto mode_c) {
+            constexpr int M = decltype(mode_c)::value;
+            constexpr int MT = M == 3 ? 1 : FIN_MT;  // slots with work
             for (int tb0 = (g.T - 1) / FIN_TB * FIN_TB; tb0 >= 0; tb0 -= FIN_TB) {  // latest steps first
                 const bool last_block = tb0 == 0;
                 f4 acc[FIN_MT][2][FIN_TB];
@@ -414,7 +450,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 auto koff_at = [&](int ks) { return koff_l[min(ks, g.ksteps - 1) * 4 + gq]; };
                 auto load_a = [&](uint32_t (&an)[FIN_MT][2], int2 o) {
 #pragma unroll
-                    for (int i = 0; i < FIN_MT; ++i) {
+                    for (int i = 0; i < MT; ++i) {
                         if (ALDS) {  // CP >= 8: the lane's 8 taps are 8 contiguous bytes (o.y == o.x + 4)
                             const uint2 w2 = *reinterpret_cast<const uint2 *>(abuf_t + alds[i] + (uint32_t)o.x);
                             an[i][0] = w2.x;
@@ -443,7 +479,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 auto kstep = [&](const uint32_t (&an)[FIN_MT][2], const half8 (&bc)[4]) {
                     uint32_t xn[FIN_MT][4];
 #pragma unroll
-                    for (int i = 0; i < FIN_MT; ++i) {
+                    for (int i = 0; i < MT; ++i) {
                         neg_times(an[i][0], xn[i][0], xn[i][1]);
                         neg_times(an[i][1], xn[i][2], xn[i][3]);
                     }
@@ -452,16 +488,18 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                         const uint32_t ct = step_const(tb0 + t);
                         half8 a[FIN_MT];
 #pragma unroll
-                        for (int i = 0; i < FIN_MT; ++i) a[i] = spike_operand(xn[i], ct);
+                        for (int i = 0; i < MT; ++i) a[i] = spike_operand(xn[i], ct);
                         // all hi products first, then the lo ones: dependent MFMAs are 8 apart
 #pragma unroll
-                        for (int i = 0; i < FIN_MT; ++i)
+                        for (int i = 0; i < MT; ++i)
 #pragma unroll
-                            for (int n = 0; n < 2; ++n) acc[i][n][t] = mfma(a[i], bc[2 * n], acc[i][n][t]);
+                            for (int n = 0; n < 2; ++n)
+                                if (fin_unit<M>(i, n)) acc[i][n][t] = mfma(a[i], bc[2 * n], acc[i][n][t]);
 #pragma unroll
-                        for (int i = 0; i < FIN_MT; ++i)
+                        for (int i = 0; i < MT; ++i)
 #pragma unroll
-                            for (int n = 0; n < 2; ++n) acc[i][n][t] = mfma(a[i], bc[2 * n + 1], acc[i][n][t]);
+                            for (int n = 0; n < 2; ++n)
+                                if (fin_unit<M>(i, n)) acc[i][n][t] = mfma(a[i], bc[2 * n + 1], acc[i][n][t]);
                     }
                 };
                 uint32_t a0[FIN_MT][2], a1[FIN_MT][2];
@@ -488,30 +526,45 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 }
                 if (ks < g.ksteps) kstep(a0, b0);
                 __syncthreads();  // staging free: the store waves are done with the previous block
+                // Staging offset = the lane's part (feature c, positions 4*gq..) plus a
+                // wave-uniform part; the lane part is made opaque here so that the
+                // compiler forms the addresses at the writes instead of keeping one
+                // register per (step, tile, half) alive through the K-step loop.
+                const int sp = stage_stride(np);
+                int lofs = c * sp + gq * 4;
+                asm volatile("" : "+v"(lofs));
 #pragma unroll
                 for (int t = 0; t < FIN_TB; ++t) {
                     if (tb0 + t >= g.T) break;
-                    float *st = stage + t * stage_t;
-                    const int sp = stage_stride(np);
+                    float *st = stage + t * stage_t + lofs;
 #pragma unroll
-                    for (int i = 0; i < FIN_MT; ++i) {
-                        const int pl = (wv + FIN_CW * i) * 16 + gq * 4;  // first of this lane's 4 positions
+                    for (int i = 0; i < MT; ++i) {
+                        const int pl = tl[i] * 16 + gq * 4;  // first of this lane's 4 positions
 #pragma unroll
                         for (int n = 0; n < 2; ++n) {
-                            const int fl = n * 16 + c;
+                            if (!fin_unit<M>(i, n)) continue;
+                            const int uo = n * 16 * sp + tl[i] * 16;  // wave-uniform part
                             const f4 v = acc[i][n][t] * inv_s;  // undo the weight scaling (a power of two)
                             if (G == 4) {
-                                if (pl < np) *reinterpret_cast<f4 *>(st + fl * sp + pl) = v;
+                                if (pl < np) *reinterpret_cast<f4 *>(st + uo) = v;
                             } else {
 #pragma unroll
                                 for (int q = 0; q < 4; ++q)
-                                    if (pl + q < np) st[fl * sp + pl + q] = v[q];
+                                    if (pl + q < np) st[uo + q] = v[q];
                             }
                         }
                     }
                 }
                 if (has_next && last_block) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                 __syncthreads();  // staging full
+            }
+            };
+            if (!BLDS) mode1 = 0;
+            switch (mode1) {
+                case 0: blocks(std::integral_constant<int, 0>{}); break;
+                case 1: blocks(std::integral_constant<int, 1>{}); break;
+                case 2: blocks(std::integral_constant<int, 2>{}); break;
+                default: blocks(std::integral_constant<int, 3>{}); break;
             }
             abuf_sel ^= 1;
         }

@@ -82,6 +82,9 @@ CONV_CASES = [
     ("tiny", 1, 1, 1, 1, 1, 1, 1, 0, 0.5, 0.3),
     ("inf-small", 3, 4, 2, 6, 6, 5, 3, 1, math.inf, 0.5),
     ("K1", 2, 5, 7, 3, 5, 33, 1, 0, 2.0, 0.3),
+    # 9 and 13 position tiles per image: the last tile's feature halves go to two waves
+    ("tiles9-split", 3, 9, 12, 12, 12, 24, 3, 1, 4.0, 0.4),
+    ("tiles13-split", 3, 15, 16, 14, 14, 20, 3, 1, 6.0, 0.5),
 ]
 
 
