@@ -24,8 +24,10 @@
 //      or to a multiple of 8; padding and padded channels hold T = never).
 //      Taps are ordered k = (ky*K + kx)*CP + ci, so the 8 taps a lane feeds to
 //      one MFMA are two 4-byte words of tpad.
-//   2. k_weight_absmax + k_split_weights: W -> scaled hi/lo fp16 B-operand
-//      fragments and the per-lane word offsets of every 8-tap group.
+//      The same launch reduces |W| to per-block maxima (extra workgroups).
+//   2. W -> scaled hi/lo fp16 B-operand fragments and the per-lane word offsets
+//      of every 8-tap group: built by the finite-threshold kernel itself when
+//      its fragments fit in LDS, else by k_split_weights into the workspace.
 //   3. finite threshold: k_conv_fire_fin (below); threshold = +inf (Eq.5):
 //      k_conv_fire_inf, which computes only the last step.
 #include <algorithm>
@@ -64,14 +66,41 @@ struct ConvGeom {
 // 16-byte boundaries coincide.
 constexpr int PAD_LDS = 32768;
 
+// Workgroups past the nchunk * ny padding ones each write the largest |w| bit
+// pattern of one run of wper weights to wmax[part] (the weights' scale, below).
+constexpr int WMAX_PARTS = 2048;  // weight-maximum partials at most
+
 // TIMES: the input is the first-spike map t_first [B][Cin][H][W] itself (T = never).
+// 1D grid: workgroup (chunk, yb) = (id % nchunk, id / nchunk) pads images yb, yb + ny, ...
 template <bool TIMES>
 __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restrict__ wave, ConvGeom g,
-                                                         int rows_per_chunk, uint8_t *__restrict__ tpad) {
+                                                         int rows_per_chunk, int nchunk, int ny,
+                                                         uint8_t *__restrict__ tpad, const float *__restrict__ w,
+                                                         int64_t nw, int wper, unsigned *__restrict__ wmax) {
     __shared__ __attribute__((aligned(16))) uint8_t buf[PAD_LDS + 16];
     const int tid = threadIdx.x;
+    if ((int)blockIdx.x >= nchunk * ny) {
+        const int part = (int)blockIdx.x - nchunk * ny;
+        const int64_t i1 = min(nw, (int64_t)(part + 1) * wper);
+        unsigned m = 0;
+        // four independent loads per thread and pass
+        for (int64_t i0 = (int64_t)part * wper + tid; i0 < i1; i0 += 1024) {
+            float v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = i0 + 256 * j < i1 ? w[i0 + 256 * j] : 0.0f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) m = max(m, __float_as_uint(fabsf(v[j])));
+        }
+#pragma unroll
+        for (int s = 32; s >= 1; s >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, s, 64));
+        unsigned *red = reinterpret_cast<unsigned *>(buf);
+        if ((tid & 63) == 0) red[tid >> 6] = m;
+        __syncthreads();
+        if (tid == 0) wmax[part] = max(max(red[0], red[1]), max(red[2], red[3]));
+        return;
+    }
     const int row_bytes = g.Wp * g.CP;
-    const int r0 = blockIdx.x * rows_per_chunk;
+    const int r0 = ((int)blockIdx.x % nchunk) * rows_per_chunk;
     const int nr = min(rows_per_chunk, g.Hp - r0);
     const int nbytes = nr * row_bytes;
     const int hw = g.H * g.W;
@@ -79,7 +108,7 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
     const int y_lo = max(r0 - g.pad, 0), y_hi = min(r0 + nr - g.pad, g.H);
     const int ncell = y_hi > y_lo ? g.Cin * (y_hi - y_lo) * g.W : 0;
     const uint32_t tfill = (uint32_t)g.T * 0x01010101u;
-    for (int64_t b = blockIdx.y; b < g.B; b += gridDim.y) {
+    for (int64_t b = (int)blockIdx.x / nchunk; b < g.B; b += ny) {
         uint8_t *out = tpad + (b * g.Hp + r0) * (int64_t)row_bytes;
         const int shift = (int)((uintptr_t)out & 15);
         for (int i = tid * 4; i < shift + nbytes; i += 1024) *reinterpret_cast<uint32_t *>(buf + i) = tfill;
@@ -119,31 +148,24 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
 // w*s = hi + lo + err with |err| <= 2^-22 |w*s|.  The GEMM result is
 // multiplied back by 1/s (exact).  Fragment (nt, ks, lane) holds, for feature
 // n = nt*16 + lane%16, the 8 taps k = ks*32 + 8*(lane/16) + j, j = 0..7.
-__global__ __launch_bounds__(256) void k_weight_absmax(const float *__restrict__ w, int64_t n,
-                                                       unsigned *__restrict__ maxbits) {
-    __shared__ unsigned red[4];
+__device__ __forceinline__ int weight_scale_exp(unsigned maxbits) {
+    const int E = maxbits ? (int)((maxbits >> 23) & 255u) - 127 : 0;  // subnormal maxima count as 2^-127
+    return 12 - max(-100, min(100, E));
+}
+
+// Largest of the n weight-maximum partials, returned to every thread of the
+// workgroup (blockDim.x a multiple of 64; red: blockDim.x / 64 words of LDS).
+__device__ unsigned reduce_wmax(const unsigned *__restrict__ parts, int n, unsigned *red) {
     unsigned m = 0;
-    // four independent loads per thread and pass, then one atomic per workgroup
-    for (int64_t i0 = (int64_t)blockIdx.x * 1024 + threadIdx.x; i0 < n; i0 += (int64_t)gridDim.x * 1024) {
-        float v[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = i0 + 256 * j < n ? w[i0 + 256 * j] : 0.0f;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) m = max(m, __float_as_uint(fabsf(v[j])));
-    }
+    for (int i = threadIdx.x; i < n; i += blockDim.x) m = max(m, parts[i]);
 #pragma unroll
     for (int s = 32; s >= 1; s >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, s, 64));
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        m = max(max(red[0], red[1]), max(red[2], red[3]));
-        if (m) atomicMax(maxbits, m);
-    }
-}
-
-__device__ __forceinline__ int weight_scale_exp(unsigned maxbits) {
-    const int E = maxbits ? (int)((maxbits >> 23) & 255u) - 127 : 0;  // subnormal maxima count as 2^-127
-    return 12 - max(-100, min(100, E));
+    m = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) m = max(m, red[i]);
+    __syncthreads();
+    return m;
 }
 
 // Tap (K-step ks, lane group gq, j) of the padded receptive field -> (cell kyx,
@@ -169,51 +191,60 @@ __device__ __forceinline__ void tap_of(const ConvGeom &g, int ks, int gq, int j,
 // to the output position's top-left input cell) of its two 4-byte words; with
 // CP >= 8 they are adjacent, with CP == 4 they are the cells 2q and 2q+1.
 // Groups past the receptive field point at offset 0 (their weights are 0).
+// hi / lo fp16 halves of fragment (nt, ks, lane), weights scaled by 2^e; w holds
+// the weights of features n0, n0 + 1, ... ([Cout - n0][Cin][K][K]).
+__device__ __forceinline__ void split_fragment(const float *w, int n0, const ConvGeom &g, int nt, int ks, int lane,
+                                               int e, half8 &h, half8 &l) {
+    const int KK = g.K * g.K;
+    const int n = nt * 16 + (lane & 15);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        int kyx, ci;
+        tap_of(g, ks, lane >> 4, j, kyx, ci);
+        float v = 0.0f;
+        if (n < g.Cout && kyx < KK && ci < g.Cin) v = ldexpf(w[((int64_t)(n - n0) * g.Cin + ci) * KK + kyx], e);
+        const _Float16 hv = (_Float16)v;
+        const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
+        h[j] = hv;
+        l[j] = (_Float16)rest;
+    }
+}
+
+// Word offsets of the 8-tap group q (koff2 below).
+__device__ __forceinline__ int2 koff_of(const ConvGeom &g, int q) {
+    const int KK = g.K * g.K;
+    int2 o{0, 0};
+    auto cell = [&](int kyx) { return kyx < KK ? ((kyx / g.K) * g.Wp + kyx % g.K) * g.CP : 0; };
+    if (g.CP >= 8) {
+        int kyx, ci0;
+        tap_of(g, q / 4, q % 4, 0, kyx, ci0);
+        o.x = kyx < KK ? cell(kyx) + ci0 : 0;
+        o.y = kyx < KK ? o.x + 4 : 0;
+    } else {
+        o.x = cell(2 * q);
+        o.y = cell(2 * q + 1);
+    }
+    return o;
+}
+
 __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__ w, ConvGeom g,
-                                                       const unsigned *__restrict__ maxbits,
+                                                       const unsigned *__restrict__ wmax, int n_wmax,
                                                        half8 *__restrict__ whi, half8 *__restrict__ wlo,
                                                        int2 *__restrict__ koff2, float *__restrict__ inv_scale) {
+    __shared__ unsigned red[4];
+    const int e = weight_scale_exp(reduce_wmax(wmax, n_wmax, red));
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t total = (int64_t)g.ntiles * g.ksteps * 64;
-    const int e = weight_scale_exp(*maxbits);
-    const int KK = g.K * g.K;
     if (i == 0) *inv_scale = ldexpf(1.0f, -e);
     if (i < total) {
         const int lane = (int)(i & 63);
         const int64_t r = i >> 6;
-        const int ks = (int)(r % g.ksteps);
-        const int nt = (int)(r / g.ksteps);
-        const int n = nt * 16 + (lane & 15);
         half8 h, l;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            int kyx, ci;
-            tap_of(g, ks, lane >> 4, j, kyx, ci);
-            float v = 0.0f;
-            if (n < g.Cout && kyx < KK && ci < g.Cin) v = ldexpf(w[((int64_t)n * g.Cin + ci) * KK + kyx], e);
-            const _Float16 hv = (_Float16)v;
-            const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
-            h[j] = hv;
-            l[j] = (_Float16)rest;
-        }
+        split_fragment(w, 0, g, (int)(r / g.ksteps), (int)(r % g.ksteps), lane, e, h, l);
         whi[i] = h;
         wlo[i] = l;
     }
-    if (i < (int64_t)g.ksteps * 4) {
-        const int q = (int)i;
-        int2 o{0, 0};
-        auto cell = [&](int kyx) { return kyx < KK ? ((kyx / g.K) * g.Wp + kyx % g.K) * g.CP : 0; };
-        if (g.CP >= 8) {
-            int kyx, ci0;
-            tap_of(g, q / 4, q % 4, 0, kyx, ci0);
-            o.x = kyx < KK ? cell(kyx) + ci0 : 0;
-            o.y = kyx < KK ? o.x + 4 : 0;
-        } else {
-            o.x = cell(2 * q);
-            o.y = cell(2 * q + 1);
-        }
-        koff2[q] = o;
-    }
+    if (i < (int64_t)g.ksteps * 4) koff2[i] = koff_of(g, (int)i);
 }
 
 // ------------------------------------------------------------------ shared MFMA helpers
@@ -290,7 +321,8 @@ template <int G, bool BLDS, bool ALDS>
 __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
     const int2 *__restrict__ koff2, ConvGeom g, int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max,
-    int a_words, const float *__restrict__ inv_scale, float *__restrict__ P, uint8_t *__restrict__ S,
+    int a_words, const float *__restrict__ inv_scale, const float *__restrict__ wts,
+    const unsigned *__restrict__ wmax, int n_wmax, float *__restrict__ P, uint8_t *__restrict__ S,
     uint8_t *__restrict__ TF, float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
@@ -366,19 +398,34 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             koff_l[i] = int2{ox, ox + 4};
         }
     } else {
-        for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) koff_l[i] = koff2[i];
+        for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) koff_l[i] = koff_of(g, i);
     }
-    if (BLDS) {
-        for (int i = tid; i < g.ksteps * 4 * 64; i += FIN_THREADS) {
-            const int ln = i & 63, rr = i >> 6;  // rr = (ks*2 + n)*2 + h
-            const int h = rr & 1, n = (rr >> 1) & 1, ks = rr >> 2;
-            const half8 *src = h ? wlo : whi;
-            frag_l[i] = __builtin_bit_cast(uint4, src[((int64_t)(pair * 2 + n) * g.ksteps + ks) * 64 + ln]);
+    float inv_s;
+    if (BLDS) {  // the pair's fragments, split here from the weights: [ks][n][hi/lo][64]
+        // (the staging area, unused until the main loop, holds the reduction's words)
+        const int e = weight_scale_exp(reduce_wmax(wmax, n_wmax, reinterpret_cast<unsigned *>(stage)));
+        inv_s = ldexpf(1.0f, -e);
+        // the pair's weights, contiguous in W, go through the staging area when
+        // they fit (coalesced loads instead of one load per tap)
+        const int per_f = g.Cin * g.K * g.K, nwp = nf * per_f;
+        const bool wl = nwp <= FIN_TB * stage_t;
+        if (wl) {
+            for (int i = tid; i < nwp; i += FIN_THREADS) stage[i] = wts[(int64_t)f0 * per_f + i];
+            __syncthreads();
         }
+        const float *wsrc = wl ? stage : wts + (int64_t)f0 * per_f;
+        for (int i = tid; i < g.ksteps * 2 * 64; i += FIN_THREADS) {
+            const int ln = i & 63, rr = i >> 6;  // rr = ks*2 + n
+            half8 h, l;
+            split_fragment(wsrc, f0, g, pair * 2 + (rr & 1), rr >> 1, ln, e, h, l);
+            frag_l[(rr * 2) * 64 + ln] = __builtin_bit_cast(uint4, h);
+            frag_l[(rr * 2 + 1) * 64 + ln] = __builtin_bit_cast(uint4, l);
+        }
+    } else {
+        inv_s = *inv_scale;
     }
     if (ALDS) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    const float inv_s = *inv_scale;
     const int64_t tplane = (int64_t)g.Cout * g.HoWo;
 
     if (wv < FIN_CW) {
@@ -559,12 +606,18 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 __syncthreads();  // staging full
             }
             };
-            if (!BLDS) mode1 = 0;
-            switch (mode1) {
-                case 0: blocks(std::integral_constant<int, 0>{}); break;
-                case 1: blocks(std::integral_constant<int, 1>{}); break;
-                case 2: blocks(std::integral_constant<int, 2>{}); break;
-                default: blocks(std::integral_constant<int, 3>{}); break;
+            if (!BLDS) {
+                blocks(std::integral_constant<int, 0>{});
+            } else if (G == 1) {  // at most 8 tiles per task: never split
+                if (mode1 == 0) blocks(std::integral_constant<int, 0>{});
+                else blocks(std::integral_constant<int, 3>{});
+            } else {
+                switch (mode1) {
+                    case 0: blocks(std::integral_constant<int, 0>{}); break;
+                    case 1: blocks(std::integral_constant<int, 1>{}); break;
+                    case 2: blocks(std::integral_constant<int, 2>{}); break;
+                    default: blocks(std::integral_constant<int, 3>{}); break;
+                }
             }
             abuf_sel ^= 1;
         }
@@ -919,10 +972,6 @@ __global__ __launch_bounds__(256) void k_zero_planes(ConvGeom g, float *__restri
     }
 }
 
-__global__ void k_zero_u32(unsigned *p, int n) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = 0u;
-}
 
 
 struct ConvPlan {
@@ -975,7 +1024,8 @@ size_t plan_workspace(const ConvPlan &pl) {
     c.take<half8>(pl.frag_count);
     c.take<half8>(pl.frag_count);
     c.take<int2>(pl.koff_count);
-    c.take<unsigned>(2);  // max|w| bits, 1/scale
+    c.take<float>(1);                // 1/scale
+    c.take<unsigned>(WMAX_PARTS);    // weight-maximum partials
     return spk::align_up(c.off, 256);
 }
 
@@ -988,15 +1038,14 @@ int max_lds_per_block() {
 
 template <int G, bool BLDS, bool ALDS>
 void launch_fin(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, const float *inv_scale,
-                const ConvGeom &g, int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words,
-                size_t lds,
-                float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
+                const float *wts, const unsigned *wmax, int n_wmax, const ConvGeom &g, int n_pairs, int n_chunks,
+                int cpi, int chunk_tiles, int np_max, int a_words, size_t lds, float *P, uint8_t *S, uint8_t *TF,
+                float *VF, hipStream_t st) {
     // one workgroup per CU: a multiple of the feature pairs on every XCD
     const int per_xcd = (int)spk::ceil_div(std::max(32, n_pairs), n_pairs) * n_pairs;
     hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
-                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, P, S,
-                       TF,
-                       VF);
+                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, wts,
+                       wmax, n_wmax, P, S, TF, VF);
 }
 
 template <bool VEC>
@@ -1047,8 +1096,8 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     half8 *whi = cv.take<half8>(pl.frag_count);
     half8 *wlo = cv.take<half8>(pl.frag_count);
     int2 *koff2 = cv.take<int2>(pl.koff_count);
-    unsigned *maxbits = cv.take<unsigned>(2);
-    float *inv_scale = reinterpret_cast<float *>(maxbits + 1);
+    float *inv_scale = cv.take<float>(1);
+    unsigned *wmax = cv.take<unsigned>(WMAX_PARTS);
     hipStream_t st = spk::as_stream(stream);
 
     // finite-threshold launch configuration (validated before anything is enqueued)
@@ -1113,18 +1162,22 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
 
     const int row_bytes = g.Wp * g.CP;
     const int rows_per_chunk = std::min(g.Hp, PAD_LDS / row_bytes);
-    const dim3 pad_grid((unsigned)spk::ceil_div(g.Hp, rows_per_chunk), (unsigned)std::min(B, 65535));
-    if (times)
-        hipLaunchKernelGGL(k_pad_first_spike<true>, pad_grid, dim3(256), 0, st, wave, g, rows_per_chunk, tpad);
-    else
-        hipLaunchKernelGGL(k_pad_first_spike<false>, pad_grid, dim3(256), 0, st, wave, g, rows_per_chunk, tpad);
-    hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(64), 0, st, maxbits, 1);
+    const int nchunk = (int)spk::ceil_div(g.Hp, rows_per_chunk), ny = std::min(B, 65535);
     const int64_t nw = (int64_t)Cout * Cin * K * K;
-    hipLaunchKernelGGL(k_weight_absmax, dim3((unsigned)std::min<int64_t>(2048, spk::ceil_div(nw, 1024))), dim3(256),
-                       0, st, weight, nw, maxbits);
-    const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
-    hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, maxbits,
-                       whi, wlo, koff2, inv_scale);
+    const int wper = (int)spk::align_up((size_t)std::max<int64_t>(1024, spk::ceil_div(nw, WMAX_PARTS)), 1024);
+    const int n_wmax = (int)spk::ceil_div(nw, wper);
+    const dim3 pad_grid((unsigned)((int64_t)nchunk * ny + n_wmax));
+    if (times)
+        hipLaunchKernelGGL(k_pad_first_spike<true>, pad_grid, dim3(256), 0, st, wave, g, rows_per_chunk, nchunk, ny,
+                           tpad, weight, nw, wper, wmax);
+    else
+        hipLaunchKernelGGL(k_pad_first_spike<false>, pad_grid, dim3(256), 0, st, wave, g, rows_per_chunk, nchunk, ny,
+                           tpad, weight, nw, wper, wmax);
+    if (inf_mode || !blds) {  // fragments in the workspace (the finite-threshold kernel with LDS room builds its own)
+        const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
+        hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, wmax,
+                           n_wmax, whi, wlo, koff2, inv_scale);
+    }
     if (inf_mode) {
         if (vec)
             launch_inf<true>(tpad, whi, wlo, koff2, inv_scale, g, potentials, spikes, t_first, v_first, st);
@@ -1132,8 +1185,8 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
             launch_inf<false>(tpad, whi, wlo, koff2, inv_scale, g, potentials, spikes, t_first, v_first, st);
     } else {
 #define SPK_FIN(G, BL, AL)                                                                                    \
-    launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, \
-                          fin_lds, potentials, spikes, t_first, v_first, st)
+    launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, weight, wmax, n_wmax, g, n_pairs, n_chunks, cpi, \
+                          chunk_tiles, np_max, a_words, fin_lds, potentials, spikes, t_first, v_first, st)
         const int sel = (vec ? 4 : 0) + (blds ? 2 : 0) + (alds ? 1 : 0);
         switch (sel) {
             case 0: SPK_FIN(1, false, false); break;
