@@ -65,6 +65,7 @@ struct ConvGeom {
 // LDS copy is shifted by the chunk's address mod 16 so that LDS and global
 // 16-byte boundaries coincide.
 constexpr int PAD_LDS = 32768;
+constexpr int PAD_RAW = 8192;   // input bytes of one image staged in LDS at most
 
 // Workgroups past the nchunk * ny padding ones each write the largest |w| bit
 // pattern of one run of wper weights to wmax[part] (the weights' scale, below).
@@ -78,6 +79,7 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
                                                          uint8_t *__restrict__ tpad, const float *__restrict__ w,
                                                          int64_t nw, int wper, unsigned *__restrict__ wmax) {
     __shared__ __attribute__((aligned(16))) uint8_t buf[PAD_LDS + 16];
+    __shared__ __attribute__((aligned(16))) uint8_t raw[TIMES ? PAD_RAW : 16];
     const int tid = threadIdx.x;
     if ((int)blockIdx.x >= nchunk * ny) {
         const int part = (int)blockIdx.x - nchunk * ny;
@@ -114,7 +116,39 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
         for (int i = tid * 4; i < shift + nbytes; i += 1024) *reinterpret_cast<uint32_t *>(buf + i) = tfill;
         __syncthreads();
         const uint8_t *src = wave + b * (TIMES ? 1 : g.T) * (int64_t)g.Cin * hw;
-        for (int i = tid; i < ncell; i += 256) {
+        // A whole image's first-spike map is one contiguous block: it is read
+        // with word loads, all issued before any is used, into LDS first.
+        const bool staged = TIMES && nchunk == 1 && ((uintptr_t)src & 3) == 0 && (g.Cin * hw) % 4 == 0 &&
+                            g.Cin * hw <= PAD_RAW;
+        if (staged) {
+            const int nwd = g.Cin * hw / 4;
+            const uint32_t *s4 = reinterpret_cast<const uint32_t *>(src);
+            uint32_t *r4 = reinterpret_cast<uint32_t *>(raw);
+            for (int i0 = tid; i0 < nwd; i0 += 8 * 256) {
+                uint32_t v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) v[u] = i0 + 256 * u < nwd ? s4[i0 + 256 * u] : 0u;
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (i0 + 256 * u < nwd) r4[i0 + 256 * u] = v[u];
+            }
+            __syncthreads();
+            // one 4-channel word of the padded map per item: (cell, channel quad)
+            const int nq = g.CP / 4;
+            for (int wi = tid; wi < hw * nq; wi += 256) {
+                const int yx = wi / nq, cq = wi - yx * nq;
+                const int y = yx / g.W, x = yx - y * g.W;
+                uint32_t word = 0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int ci = cq * 4 + j;
+                    const int tp = ci < g.Cin ? min((int)raw[ci * hw + yx], g.T) : g.T;
+                    word |= (uint32_t)tp << (8 * j);
+                }
+                *reinterpret_cast<uint32_t *>(buf + shift + ((y + g.pad) * g.Wp + x + g.pad) * g.CP + cq * 4) = word;
+            }
+        }
+        for (int i = tid; i < (staged ? 0 : ncell); i += 256) {
             const int x = i % g.W, rest = i / g.W;
             const int yy = rest % (y_hi - y_lo), ci = rest / (y_hi - y_lo);
             const int y = y_lo + yy;
