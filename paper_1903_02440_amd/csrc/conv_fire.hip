@@ -765,6 +765,7 @@ constexpr int INF_NW = 4;   // 16-feature tiles per workgroup
 constexpr int INF_KC = 8;   // K-steps per LDS chunk
 constexpr int INF_CHUNK_U4 = INF_KC * INF_NW * 2 * 64;  // uint4 per chunk buffer
 constexpr int INF_ZW = 4;   // zero waves (waves 8-11)
+constexpr int64_t INF_PART_MAX = 1 << 21;  // floats of split partial sums at most
 
 // With VEC, INF_ZW more waves write the zero planes of steps 0..T-2 (potentials
 // and spikes of images blockIdx.x, blockIdx.x + gridDim.x, ...) while the MFMA
@@ -773,8 +774,9 @@ constexpr int INF_ZW = 4;   // zero waves (waves 8-11)
 template <bool VEC>
 __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
-    const int2 *__restrict__ koff2, ConvGeom g, int n_mb, int n_ng, const float *__restrict__ inv_scale,
-    float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF) {
+    const int2 *__restrict__ koff2, ConvGeom g, int n_mb, int n_ng, int ksplit, float *__restrict__ part,
+    const float *__restrict__ inv_scale, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
+    float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     int2 *koff_l = reinterpret_cast<int2 *>(lds);
     uint4 *cbuf = lds + (g.ksteps * 4 * 8 + 15) / 16;  // 2 chunk buffers [ksl][n][hi/lo][64]
@@ -785,9 +787,17 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     const uint32_t ct = step_const(g.T - 1);
     const int nchunks = (g.ksteps + INF_KC - 1) / INF_KC;
     const int x = blockIdx.x % 8, j = blockIdx.x / 8, per_xcd = (int)gridDim.x / 8;
-    const int ntask = n_mb * n_ng, per_x = (ntask + 7) / 8;
+    const int ntask = n_mb * n_ng * ksplit, per_x = (ntask + 7) / 8;
     const int t_lo = x * per_x, t_hi = min(ntask, t_lo + per_x);
     const int64_t tstride = (int64_t)g.Cout * g.HoWo;
+    // With ksplit > 1 a task is (feature group, position block, part of the K
+    // chunks): its raw sums go to part[kp][B][Cout][HoWo], added up in part
+    // order by k_inf_reduce.
+    const int cpp = (nchunks + ksplit - 1) / ksplit;
+    auto chunk_range = [&](int task, int &c_lo, int &c_hi) {
+        c_lo = (task % ksplit) * cpp;
+        c_hi = min(nchunks, c_lo + cpp);
+    };
 
     if (wv >= INF_WAVES) {
         // zero waves: 16-byte units of potentials (4 per unit) and 4-byte units of spikes
@@ -797,8 +807,12 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         const int64_t zs = VEC && S && g.T > 1 ? (g.T - 1) * tstride / 4 : 0;
         const int64_t nimg = g.B > (int)blockIdx.x ? (g.B - 1 - (int)blockIdx.x) / gridDim.x + 1 : 0;
         const int64_t total = nimg * (zp + zs);
-        const int ntk = t_lo + j < t_hi ? (t_hi - 1 - (t_lo + j)) / per_xcd + 1 : 0;
-        const int nint = ntk * (1 + nchunks) + 1;  // barrier intervals (the last one after the loop)
+        int nint = 1;  // barrier intervals (the last one after the loop)
+        for (int task = t_lo + j; task < t_hi; task += per_xcd) {
+            int c_lo, c_hi;
+            chunk_range(task, c_lo, c_hi);
+            nint += 1 + max(0, c_hi - c_lo);
+        }
         const int64_t per = (total + nint - 1) / nint;
         int64_t u0 = 0;
         auto slice = [&]() {
@@ -813,10 +827,12 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             }
             u0 = u1;
         };
-        for (int tk = 0; tk < ntk; ++tk) {
+        for (int task = t_lo + j; task < t_hi; task += per_xcd) {
+            int c_lo, c_hi;
+            chunk_range(task, c_lo, c_hi);
             slice();
             __syncthreads();  // the MFMA waves' "buffers free"
-            for (int ch = 0; ch < nchunks; ++ch) {
+            for (int ch = c_lo; ch < c_hi; ++ch) {
                 slice();
                 __syncthreads();  // the MFMA waves' chunk barrier
             }
@@ -826,7 +842,10 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     }
 
     for (int task = t_lo + j; task < t_hi; task += per_xcd) {
-        const int ng = task / n_mb, mb = task % n_mb;
+        const int tq = task / ksplit, kp = task % ksplit;
+        const int ng = tq / n_mb, mb = tq % n_mb;
+        int c_lo, c_hi;
+        chunk_range(task, c_lo, c_hi);
         const half8 *fh = whi + (int64_t)ng * INF_NW * g.ksteps * 64;
         const half8 *fl = wlo + (int64_t)ng * INF_NW * g.ksteps * 64;
         // chunk ch -> buffer: wave w issues the 64-lane groups w, w+8, ... (16 bytes per lane)
@@ -902,7 +921,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             const int nk = min(INF_KC, g.ksteps - ch * INF_KC);
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's words and fill of chunk ch landed
             __syncthreads();  // every wave's part of chunk ch is in LDS; chunk ch-1's buffer is free
-            if (ch + 1 < nchunks) {
+            if (ch + 1 < c_hi) {
                 load_aw(ch + 1, awn);
                 fill(ch + 1);
             }
@@ -935,11 +954,13 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             }
         };
         __syncthreads();  // the buffers are free (previous task done), koff is visible
-        load_aw(0, aw0);
-        fill(0);
-        for (int ch = 0; ch < nchunks; ch += 2) {
+        if (c_lo < c_hi) {
+            load_aw(c_lo, aw0);
+            fill(c_lo);
+        }
+        for (int ch = c_lo; ch < c_hi; ch += 2) {
             chunk(ch, aw0, aw1);
-            if (ch + 1 < nchunks) chunk(ch + 1, aw1, aw0);
+            if (ch + 1 < c_hi) chunk(ch + 1, aw1, aw0);
         }
         // the last step's potentials and spikes, the first-spike time and potential
 #pragma unroll
@@ -948,8 +969,15 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             for (int n = 0; n < INF_NW; ++n) {
                 const int f = (ng * INF_NW + n) * 16 + c;
                 if (img[i] < 0 || f >= g.Cout || mpos0[i] >= g.HoWo) continue;
-                const f4 v = acc[i][n] * inv_s;
                 const int lim = g.HoWo - mpos0[i];
+                if (ksplit > 1) {  // this part's raw sums
+                    const int64_t op = (((int64_t)kp * g.B + img[i]) * g.Cout + f) * g.HoWo + mpos0[i];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        if (q < lim) part[op + q] = acc[i][n][q];
+                    continue;
+                }
+                const f4 v = acc[i][n] * inv_s;
                 const int64_t o = (img[i] * g.T + g.T - 1) * tstride + (int64_t)f * g.HoWo + mpos0[i];
                 const int64_t of = (img[i] * (int64_t)g.Cout + f) * g.HoWo + mpos0[i];
                 uint32_t sp = 0, tv = 0;
@@ -1008,9 +1036,31 @@ __global__ __launch_bounds__(256) void k_zero_planes(ConvGeom g, float *__restri
 
 
 
+// The Eq.5 outputs from split sums: P[T-1] = (sum of the parts, in part order)
+// / scale; one thread per (image, feature, position).
+__global__ __launch_bounds__(256) void k_inf_reduce(const float *__restrict__ part, int ksplit, ConvGeom g,
+                                                    const float *__restrict__ inv_scale, float *__restrict__ P,
+                                                    uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
+                                                    float *__restrict__ VF) {
+    const int64_t plane = (int64_t)g.Cout * g.HoWo, n = g.B * plane;
+    const int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (o >= n) return;
+    float sum = part[o];
+    for (int k = 1; k < ksplit; ++k) sum += part[k * n + o];
+    const float v = sum * *inv_scale;
+    const int64_t b = o / plane, r = o - b * plane;
+    const int64_t ot = (b * g.T + g.T - 1) * plane + r;
+    if (P) P[ot] = v;
+    if (S) S[ot] = (uint8_t)(v > 0.0f);
+    TF[o] = (uint8_t)(v > 0.0f ? g.T - 1 : g.T);
+    VF[o] = v;
+}
+
 struct ConvPlan {
     ConvGeom g;
     size_t tpad_bytes, frag_count, koff_count;
+    int ksplit;         // K parts of the Eq.5 kernel (1: not split)
+    size_t part_count;  // floats of its partial sums
 };
 
 int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, ConvPlan &pl) {
@@ -1049,6 +1099,17 @@ int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, Con
     pl.tpad_bytes = (size_t)B * g.Hp * g.Wp * g.CP;
     pl.frag_count = (size_t)g.ntiles * g.ksteps * 64;
     pl.koff_count = (size_t)g.ksteps * 4;
+    // Eq.5 mode on few tasks (a small batch): the K chunks are split into parts
+    // run by separate workgroups, so that more than a handful of CUs work; the
+    // partial sums take at most INF_PART_MAX floats.
+    const int64_t n_mb = spk::ceil_div(g.total_mtiles, INF_WAVES * INF_MW);
+    const int64_t n_ng = spk::ceil_div(spk::ceil_div(Cout, 16), INF_NW);
+    const int64_t nch = spk::ceil_div(g.ksteps, INF_KC), outs = (int64_t)B * Cout * g.HoWo;
+    int64_t ks = n_mb * n_ng > 0 && n_mb * n_ng < 128 ? std::min<int64_t>(nch, spk::ceil_div(256, n_mb * n_ng)) : 1;
+    if (outs > 0) ks = std::min<int64_t>(ks, INF_PART_MAX / outs);
+    if (ks >= 2) ks = spk::ceil_div(nch, spk::ceil_div(nch, ks));  // no part without chunks
+    pl.ksplit = ks >= 2 ? (int)ks : 1;
+    pl.part_count = pl.ksplit > 1 ? (size_t)(pl.ksplit * outs) : 0;
     return SPK_OK;
 }
 
@@ -1060,6 +1121,7 @@ size_t plan_workspace(const ConvPlan &pl) {
     c.take<int2>(pl.koff_count);
     c.take<float>(1);                // 1/scale
     c.take<unsigned>(WMAX_PARTS);    // weight-maximum partials
+    c.take<float>(pl.part_count);    // Eq.5 split sums
     return spk::align_up(c.off, 256);
 }
 
@@ -1084,7 +1146,8 @@ void launch_fin(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const i
 
 template <bool VEC>
 void launch_inf(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, const float *inv_scale,
-                const ConvGeom &g, float *P, uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
+                const ConvGeom &g, int ksplit, float *part, float *P, uint8_t *S, uint8_t *TF, float *VF,
+                hipStream_t st) {
     const int n_mb = (int)spk::ceil_div(g.total_mtiles, INF_WAVES * INF_MW);
     const int n_ng = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), INF_NW);
     const size_t lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16) + 2 * (size_t)INF_CHUNK_U4 * 16;
@@ -1094,7 +1157,12 @@ void launch_inf(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const i
         hipLaunchKernelGGL(k_zero_planes, dim3(gx, (unsigned)std::min(g.B, 65535)), dim3(256), 0, st, g, P, S);
     }
     hipLaunchKernelGGL((k_conv_fire_inf<VEC>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad, whi, wlo,
-                       koff2, g, n_mb, n_ng, inv_scale, P, S, TF, VF);
+                       koff2, g, n_mb, n_ng, ksplit, part, inv_scale, P, S, TF, VF);
+    if (ksplit > 1) {
+        const int64_t n = (int64_t)g.B * g.Cout * g.HoWo;
+        hipLaunchKernelGGL(k_inf_reduce, dim3((unsigned)spk::ceil_div(n, 256)), dim3(256), 0, st, part, ksplit, g,
+                           inv_scale, P, S, TF, VF);
+    }
 }
 
 }  // namespace
@@ -1132,6 +1200,7 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     int2 *koff2 = cv.take<int2>(pl.koff_count);
     float *inv_scale = cv.take<float>(1);
     unsigned *wmax = cv.take<unsigned>(WMAX_PARTS);
+    float *part = cv.take<float>(pl.part_count);
     hipStream_t st = spk::as_stream(stream);
 
     // finite-threshold launch configuration (validated before anything is enqueued)
@@ -1214,9 +1283,11 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     }
     if (inf_mode) {
         if (vec)
-            launch_inf<true>(tpad, whi, wlo, koff2, inv_scale, g, potentials, spikes, t_first, v_first, st);
+            launch_inf<true>(tpad, whi, wlo, koff2, inv_scale, g, pl.ksplit, part, potentials, spikes, t_first,
+                             v_first, st);
         else
-            launch_inf<false>(tpad, whi, wlo, koff2, inv_scale, g, potentials, spikes, t_first, v_first, st);
+            launch_inf<false>(tpad, whi, wlo, koff2, inv_scale, g, pl.ksplit, part, potentials, spikes, t_first,
+                              v_first, st);
     } else {
 #define SPK_FIN(G, BL, AL)                                                                                    \
     launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, weight, wmax, n_wmax, g, n_pairs, n_chunks, cpi, \

@@ -85,6 +85,8 @@ CONV_CASES = [
     # 9 and 13 position tiles per image: the last tile's feature halves go to two waves
     ("tiles9-split", 3, 9, 12, 12, 12, 24, 3, 1, 4.0, 0.4),
     ("tiles13-split", 3, 15, 16, 14, 14, 20, 3, 1, 6.0, 0.5),
+    # Eq.5 on few tasks: the K chunks split over workgroups, two chunks per part
+    ("inf-ksplit", 112, 15, 64, 12, 12, 8, 5, 2, math.inf, 0.6),
 ]
 
 
