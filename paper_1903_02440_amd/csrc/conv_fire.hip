@@ -1211,7 +1211,11 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     // contiguous region); larger images are cut into chunks of the flattened
     // (image, position) space, which may span two images, so that no tile slot
     // is padding (store offsets relative to the chunk's first image fit 32 bits).
-    const int ct_max = chunk_tiles_max(vec ? 4 : 1);
+    const int n_pairs = (int)spk::ceil_div(spk::ceil_div(Cout, 16), 2);
+    // Few tiles in all (small batches, online steps): smaller chunks, so that
+    // more workgroups share the call (at least 4 tiles per task).
+    int ct_max = chunk_tiles_max(vec ? 4 : 1);
+    while (ct_max > 4 && (int64_t)n_pairs * B * g.mt_per_img / ct_max < 256) ct_max /= 2;
     const int64_t npos = (int64_t)B * g.HoWo;
     const bool flat = g.mt_per_img > ct_max && ((int64_t)T * Cout + 32) * g.HoWo < (1LL << 31);
     int cpi, chunk_tiles, n_chunks;
@@ -1225,7 +1229,6 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
         n_chunks = B * cpi;
     }
     const int np_max = chunk_tiles * 16;
-    const int n_pairs = (int)spk::ceil_div(spk::ceil_div(Cout, 16), 2);
     const size_t koff_lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16);
     const size_t stage_lds = (size_t)FIN_TB * 32 * stage_stride(np_max) * sizeof(float);
     const size_t frag_lds = (size_t)g.ksteps * 4 * 64 * 16;

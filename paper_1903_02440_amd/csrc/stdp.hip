@@ -231,6 +231,38 @@ __global__ __launch_bounds__(256) void k_stdp_apply(float *__restrict__ weight, 
     if (own) *wp = wf;
 }
 
+// B == 1 (online steps): grid (chunk of 256 weights, winner slot).  Each
+// winner updates its feature's weights directly -- the replay's chain of one
+// update, with the record rules of k_stdp_list (the first record of a feature
+// whose step lies in [0, T); nothing for reward 0) -- without the list,
+// offset and bit passes.
+template <bool FAST>
+__global__ __launch_bounds__(256) void k_stdp_single(float *__restrict__ weight, const uint8_t *__restrict__ pre,
+                                                     const int32_t *__restrict__ winners,
+                                                     const int32_t *__restrict__ n_win,
+                                                     const int8_t *__restrict__ reward, StdpArgs a) {
+#pragma clang fp contract(off)
+    const int j = blockIdx.y;
+    if (j >= min(n_win[0], a.k) || (reward && reward[0] == 0)) return;  // uniform
+    auto valid = [&](int q) { return winners[4 * q + 1] >= 0 && winners[4 * q + 1] < a.T; };
+    const int f = winners[4 * j], t = winners[4 * j + 1];
+    if (f < 0 || f >= a.Cout || !valid(j)) return;
+    for (int q = 0; q < j; ++q)
+        if (winners[4 * q] == f && valid(q)) return;  // an earlier record of the feature is the one used
+    const int KK = a.K * a.K, Kc = a.Cin * KK;
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e >= Kc) return;
+    const int ci = e / KK, ky = (e % KK) / a.K, kx = e % a.K;
+    const int iy = winners[4 * j + 2] + ky - a.pad, ix = winners[4 * j + 3] + kx - a.pad;
+    uint8_t v = 0;
+    if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
+        v = pre[((int64_t)t * a.Cin + ci) * a.H * a.W + (int64_t)iy * a.W + ix];
+    double r = v != 0 ? (double)a.a_plus : (double)a.a_minus;
+    if (reward && reward[0] < 0) r = -r;
+    float *wp = weight + (int64_t)f * Kc + e;
+    *wp = stdp_one<FAST>(*wp, r, a.lb, a.ub, FAST || a.stabilizer, true);
+}
+
 __global__ __launch_bounds__(256) void k_decide(const int32_t *__restrict__ winners, const int32_t *__restrict__ n_win,
                                                 int B, int k, const int32_t *__restrict__ labels, int n_classes,
                                                 int32_t *__restrict__ decision, int8_t *__restrict__ reward) {
@@ -271,12 +303,22 @@ int stdp_common(float *weight, int Cout, int Cin, int K, int pad, const uint8_t 
     StdpArgs a{Cout, Cin, K, pad, B, T, H, W, k, stabilizer, a_plus, a_minus, lb, ub};
     hipStream_t st = spk::as_stream(stream);
     const unsigned wchunks = (unsigned)spk::ceil_div((int64_t)Cin * K * K, 256);
+    // the clamp can be dropped after the first update (see k_stdp_apply)
+    const double rmax = std::max(std::fabs((double)a_plus), std::fabs((double)a_minus));
+    const bool fast = stabilizer && rmax * ((double)ub - (double)lb) <= 0.5;
+    if (B == 1 && k <= 65535) {
+        if (fast)
+            hipLaunchKernelGGL(k_stdp_single<true>, dim3(wchunks, (unsigned)k), dim3(256), 0, st, weight, pre_wave,
+                               winners, n_winners, reward, a);
+        else
+            hipLaunchKernelGGL(k_stdp_single<false>, dim3(wchunks, (unsigned)k), dim3(256), 0, st, weight, pre_wave,
+                               winners, n_winners, reward, a);
+        return spk::check_launch(name);
+    }
     hipLaunchKernelGGL(k_stdp_list, dim3(Cout), dim3(LIST_THREADS), 0, st, winners, n_winners, reward, a, wk);
     hipLaunchKernelGGL(k_stdp_offsets, dim3(1), dim3(1024), 0, st, Cout, wk);
     hipLaunchKernelGGL(k_stdp_bits, dim3(wchunks, (unsigned)wk.rows), dim3(256), 0, st, pre_wave, a, wk);
-    // the clamp can be dropped after the first update (see k_stdp_apply)
-    const double rmax = std::max(std::fabs((double)a_plus), std::fabs((double)a_minus));
-    if (stabilizer && rmax * ((double)ub - (double)lb) <= 0.5)
+    if (fast)
         hipLaunchKernelGGL(k_stdp_apply<true>, dim3(wchunks, Cout), dim3(256), 0, st, weight, a, wk);
     else
         hipLaunchKernelGGL(k_stdp_apply<false>, dim3(wchunks, Cout), dim3(256), 0, st, weight, a, wk);

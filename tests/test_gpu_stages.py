@@ -438,6 +438,49 @@ def test_stdp_parity(case):
     assert_equal(host(Wg), orc.stdp(Wt, wave, pad, win, nw, 0.004, -0.003), "weights")
 
 
+@pytest.mark.parametrize("case", STDP_CASES)
+@pytest.mark.parametrize("rew", [None, 1, -1, 0])
+def test_stdp_single_image(case, rew):
+    # one image (the online step's direct update): oracle parity for STDP and R-STDP
+    wave, Wt, win, nw = layer_case(*case)
+    wave, win, nw = wave[:1], win[:1], nw[:1]
+    pad = case[8]
+    Wg = dev(Wt)
+    if rew is None:
+        spk.spk_stdp(Wg, pad, dev(wave), dev(win), dev(nw), 0.004, -0.003)
+        ref = orc.stdp(Wt, wave, pad, win, nw, 0.004, -0.003)
+    else:
+        reward = np.array([rew], np.int8)
+        spk.spk_rstdp(Wg, pad, dev(wave), dev(win), dev(nw), dev(reward), 0.004, -0.003)
+        ref = orc.stdp(Wt, wave, pad, win, nw, 0.004, -0.003, reward=reward)
+    sync()
+    assert_equal(host(Wg), ref, "weights")
+
+
+def test_stdp_single_image_odd_records_match_replay():
+    # records the replay skips (a repeated feature, a step outside [0, T), a feature
+    # out of range): the one-image path applies the same updates as the batched
+    # replay of a two-image batch whose second image has no winners
+    wave, Wt, win, nw = layer_case(*STDP_CASES[0])
+    T, pad, k = wave.shape[1], 2, win.shape[1]
+    w1 = win[:1].copy()
+    w1[0, 1] = w1[0, 0]                    # the first record's feature again, other step and place
+    w1[0, 1, 1] = (w1[0, 0, 1] + 3) % T
+    w1[0, 1, 2:] = (5, 7)
+    w1[0, 2, 1] = T                        # a step outside [0, T)
+    w1[0, 3, 0] = 999                      # a feature out of range
+    n1 = np.array([k], np.int32)
+    wave2 = np.concatenate([wave[:1], wave[1:2]])
+    win2 = np.concatenate([w1, np.full_like(w1, -1)])
+    n2 = np.array([k, 0], np.int32)
+    for rates in [(0.004, -0.003), (0.6, -0.5)]:
+        Wa, Wb = dev(Wt), dev(Wt)
+        spk.spk_stdp(Wa, pad, dev(wave[:1]), dev(w1), dev(n1), *rates)
+        spk.spk_stdp(Wb, pad, dev(wave2), dev(win2), dev(n2), *rates)
+        sync()
+        assert_equal(host(Wa), host(Wb), f"one image vs replay, rates {rates}")
+
+
 def test_rstdp_and_bounds_variant():
     wave, Wt, win, nw = layer_case(*STDP_CASES[2])
     B = wave.shape[0]
