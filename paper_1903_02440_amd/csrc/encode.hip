@@ -553,7 +553,9 @@ extern "C" int spk_encode_latency(const uint8_t *image, int B, int H, int W, con
     while (R > 1 && filter_lds(R) > 65536) --R;
     SPK_REQUIRE(filter_lds(R) <= 65536, SPK_E_RANGE, "spk_encode_latency: %d filters of %dx%d on width %d do not fit",
                 C, KF, KF, W);
-    const int nb = (H + R - 1) / R;
+    int nb = (H + R - 1) / R;
+    // few images (online steps): more, thinner bands, so that more workgroups share them
+    while ((int64_t)B * nb < 128 && nb < H) nb = std::min(H, 2 * nb);
     R = (H + nb - 1) / nb;
     hipLaunchKernelGGL(k_filter, dim3((unsigned)(B * nb)), dim3(256), filter_lds(R), st, image, B, H, W, filters, C,
                        KF, filter_threshold, R, I);

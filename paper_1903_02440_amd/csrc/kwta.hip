@@ -412,12 +412,20 @@ constexpr int TOPK_MAX_K = 16;
 constexpr size_t TOPK_LDS = 40 * 1024;  // lists and cursors (the stash adds 16 KB)
 constexpr int TOPK_U = 8;               // feature maps loaded per block
 constexpr int TOPK_STASH_MIN = 64;      // features per split from which the stash pays
+// Batches below TOPK_PRE_B images (online steps) leave most CUs idle: the
+// lists are then built by a grid of (image, split of the feature maps)
+// workgroups into the workspace, and the rounds' workgroup merges them.
+constexpr int TOPK_PRE_B = 8;
+constexpr int TOPK_PRE_NS = 16;         // feature splits at most
+constexpr int TOPK_PRE_HW = 4096;       // positions at most
 
 struct KwtaTopk {
     int B, T, C, HW, W, k, r;
     int S, fps;  // feature splits per position (small maps) and features per split
     int nt;      // threads per workgroup
     unsigned mHW, mW;
+    int ns, fps2;  // workgroup feature splits and their features (ns > 1: lists built by k_kwta_lists)
+    uint64_t *lg;  // their lists, [B][ns][HW][KM]
 };
 
 // Inserts key into the descending list top (keys are unique; the caller has
@@ -431,6 +439,44 @@ __device__ __forceinline__ void topk_insert(uint64_t (&top)[KM], uint64_t key) {
         top[i] = above ? top[i - 1] : (here ? key : top[i]);
     }
     top[0] = key > top[0] ? key : top[0];
+}
+
+// Grid (image, split): the KM best keys of every position over the split's
+// feature maps, into g.lg.
+template <int KM, int U>
+__global__ __launch_bounds__(TOPK_THREADS_SMALL_B) void k_kwta_lists(const uint8_t *__restrict__ tf_all,
+                                                             const float *__restrict__ vf_all, KwtaTopk g) {
+    const int b = blockIdx.x, sp = blockIdx.y, HW = g.HW;
+    const int64_t N = (int64_t)g.C * HW;
+    const uint8_t *tf = tf_all + (int64_t)b * N;
+    const float *vf = vf_all + (int64_t)b * N;
+    const int fa = sp * g.fps2, fb = min(g.C, fa + g.fps2);
+    for (int p = threadIdx.x; p < HW; p += blockDim.x) {
+        uint64_t top[KM];
+#pragma unroll
+        for (int i = 0; i < KM; ++i) top[i] = 0;
+        for (int f0 = fa; f0 < fb; f0 += U) {
+            int tv[U];
+            float vv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const bool ok = f0 + u < fb;
+                const int o = (f0 + u) * HW + p;
+                tv[u] = ok ? (int)tf[o] : g.T;
+                vv[u] = ok ? vf[o] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (tv[u] < g.T) {
+                    const uint64_t key = kwta_key(tv[u], vv[u], (uint32_t)((f0 + u) * HW + p));
+                    if (key > top[KM - 1]) topk_insert(top, key);
+                }
+            }
+        }
+        uint64_t *dst = g.lg + (((int64_t)b * g.ns + sp) * HW + p) * KM;
+#pragma unroll
+        for (int i = 0; i < KM; ++i) dst[i] = top[i];
+    }
 }
 
 template <int KM, int U, bool STASH>
@@ -452,8 +498,25 @@ __global__ __launch_bounds__(TOPK_THREADS_SMALL_B) void k_kwta_topk(const uint8_
     int32_t *win = winners + (int64_t)b * g.k * 4;
     for (int i = tid; i < 4 * g.k; i += NT) win[i] = -1;
 
+    if (g.ns > 1) {  // the lists of the workgroup splits, merged (each is sorted)
+        for (int p = tid; p < HW; p += NT) {
+            uint64_t top[KM];
+#pragma unroll
+            for (int i = 0; i < KM; ++i) top[i] = 0;
+            for (int sp = 0; sp < g.ns; ++sp) {
+                const uint64_t *src = g.lg + (((int64_t)b * g.ns + sp) * HW + p) * KM;
+                for (int e = 0; e < KM; ++e) {
+                    const uint64_t key = src[e];
+                    if (!(key > top[KM - 1])) break;
+                    topk_insert(top, key);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < KM; ++i) lists[(size_t)p * KM + i] = top[i];
+        }
+    }
     // pass over the image: the KM best keys of every (position, feature split)
-    for (int pp = tid; pp < HW * S; pp += NT) {
+    for (int pp = tid; pp < (g.ns > 1 ? 0 : HW * S); pp += NT) {
         const int s = (int)qdiv((unsigned)pp, g.mHW), p = pp - s * HW;
         uint64_t top[KM];
 #pragma unroll
@@ -499,7 +562,7 @@ __global__ __launch_bounds__(TOPK_THREADS_SMALL_B) void k_kwta_topk(const uint8_
 #pragma unroll
         for (int i = 0; i < KM; ++i) lists[(size_t)pp * KM + i] = top[i];
     }
-    if (S > 1) {  // uniform
+    if (S > 1 && g.ns <= 1) {  // uniform
         __syncthreads();
         // owners fold the other splits' lists into their own
         for (int p = tid; p < HW; p += NT) {
@@ -595,7 +658,19 @@ bool kwta_topk(int B, int T, int C, int H, int W, int k, int r, KwtaTopk &s) {
         return (uint64_t)n * e < (1ULL << 32);
     };
     if (!exact(HW, (int64_t)C * HW) || !exact(W, HW)) return false;
-    s = KwtaTopk{B, T, C, (int)HW, W, k, r, S, fps, nt, magic(HW), magic(W)};
+    s = KwtaTopk{B, T, C, (int)HW, W, k, r, S, fps, nt, magic(HW), magic(W), 1, C, nullptr};
+    if (B < TOPK_PRE_B && HW <= TOPK_PRE_HW) {  // lists by a grid of workgroups (the rounds' workgroup: S = 1)
+        const int ns = (int)std::min<int64_t>(TOPK_PRE_NS, (C + 15) / 16);
+        if (ns > 1) {
+            s.ns = ns;
+            s.fps2 = (C + ns - 1) / ns;
+            s.ns = (C + s.fps2 - 1) / s.fps2;
+            s.S = 1;
+            s.fps = C;
+            const int64_t passes = (HW + NT - 1) / NT;
+            s.nt = (int)(((HW + passes - 1) / passes + 63) / 64 * 64);
+        }
+    }
     return true;
 }
 
@@ -603,6 +678,13 @@ template <int KM>
 void launch_topk(const KwtaTopk &s, const uint8_t *tf, const float *vf, int32_t *winners, int32_t *nw,
                  hipStream_t st) {
     const size_t lds = (size_t)s.HW * (s.S * KM * sizeof(uint64_t) + 1);
+    if (s.ns > 1) {
+        const int nt = (int)std::min<int64_t>(TOPK_THREADS_SMALL_B, ((int64_t)s.HW + 63) / 64 * 64);
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_kwta_lists<KM, TOPK_U>), dim3(s.B, s.ns), dim3(nt), 0, st, tf, vf, s);
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_kwta_topk<KM, TOPK_U, false>), dim3(s.B), dim3(s.nt), lds, st, tf, vf,
+                           s, winners, nw);
+        return;
+    }
     if (s.fps >= TOPK_STASH_MIN && s.nt <= TOPK_THREADS)
         hipLaunchKernelGGL(HIP_KERNEL_NAME(k_kwta_topk<KM, TOPK_U, true>), dim3(s.B), dim3(s.nt), lds, st, tf, vf, s,
                            winners, nw);
@@ -674,7 +756,10 @@ extern "C" size_t spk_kwta_workspace_size(int B, int C, int H, int W) {
     if (kwta_geom(B, 1, C, H, W, 1, 0, g) != SPK_OK) return 0;
     KwtaSmall sm;
     const int ntiles = kwta_small(B, 1, C, H, W, 1, 0, sm) ? sm.ntiles : g.ntiles;
-    return spk::align_up((size_t)B * ntiles * sizeof(uint64_t), 256);
+    size_t need = (size_t)B * ntiles * sizeof(uint64_t);
+    if (B < TOPK_PRE_B && (int64_t)H * W <= TOPK_PRE_HW)  // the workgroup splits' lists (any k up to TOPK_MAX_K)
+        need = std::max(need, (size_t)B * TOPK_PRE_NS * H * W * TOPK_MAX_K * sizeof(uint64_t));
+    return spk::align_up(need, 256);
 }
 
 extern "C" int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int T, int C, int H, int W, int k,
@@ -693,6 +778,7 @@ extern "C" int spk_kwta(const uint8_t *t_first, const float *v_first, int B, int
     uint64_t *tilekey = static_cast<uint64_t *>(workspace);
     KwtaTopk tk;
     if (kwta_topk(B, T, C, H, W, k, radius, tk)) {
+        tk.lg = static_cast<uint64_t *>(workspace);
         dispatch_topk(tk, t_first, v_first, winners, n_winners, st);
         return spk::check_launch("spk_kwta");
     }

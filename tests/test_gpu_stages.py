@@ -243,7 +243,10 @@ def test_pool_potentials_parity(case):
 KWTA_CASES = [(4, 15, 30, 28, 28, 5, 3), (3, 15, 250, 14, 14, 8, 1), (6, 15, 200, 4, 4, 1, 0),
               (2, 30, 20, 10, 25, 1, 5), (3, 4, 3, 5, 7, 12, 1), (2, 15, 5, 40, 300, 6, 2),
               (3, 15, 40, 1, 1, 4, 0), (2, 15, 7, 1, 9, 3, 1), (2, 15, 300, 10, 10, 8, 2),
-              (2, 15, 64, 6, 6, 16, 1), (2, 15, 30, 12, 12, 20, 1), (2, 15, 20, 30, 40, 16, 0)]
+              (2, 15, 64, 6, 6, 16, 1), (2, 15, 30, 12, 12, 20, 1), (2, 15, 20, 30, 40, 16, 0),
+              # below 8 images the lists come from a grid of (image, feature split) workgroups;
+              # from 8 on from the rounds' own workgroup
+              (1, 15, 250, 14, 14, 8, 1), (8, 15, 250, 14, 14, 8, 1), (9, 15, 30, 28, 28, 5, 3)]
 
 
 def kwta_inputs(seed, B, T, C, H, W, ties=True):
