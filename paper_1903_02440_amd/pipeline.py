@@ -9,7 +9,9 @@ calls on one stream, with no host synchronisation and no allocation inside
   with ``local_norm=(radius, eps)`` the filter map is locally normalised
   (``spk_local_normalization``) before ``spk_rank_latency`` codes it;
 * each conv stage: ``spk_conv_fire`` then ``spk_kwta`` (the winners feed
-  plasticity and, for the last layer, the decision); when its input is the
+  plasticity and, for the last layer, the decision; in :meth:`Chain.step`
+  the kWTA of a layer whose plasticity starts early runs on that layer's
+  side stream, ahead of its plasticity); when its input is the
   encoder's or a pool's output, whose wave is Eq.1 of its first-spike map by
   construction, ``spk_conv_fire_first_spike`` reads that map instead of the
   T planes of the wave;
@@ -96,6 +98,8 @@ class Chain:
                 # each learning layer has its own plasticity workspace (the layers update concurrently)
                 b["ws_learn"] = (torch.empty(max(256, spk_stdp_workspace_size(st.cout, st.cin, st.K, B, st.k)),
                                              dtype=u8, device=dev) if st.learn is not None else None)
+                b["ws_kwta"] = (torch.empty(max(256, spk_kwta_workspace_size(B, st.cout, ho, wo)), dtype=u8,
+                                            device=dev) if st.learn is not None else None)
                 ws_bytes = max(ws_bytes, spk_conv_fire_workspace_size(B, T, st.cin, h, w, st.cout, st.K, st.pad),
                                spk_kwta_workspace_size(B, st.cout, ho, wo))
                 c, h, w = st.cout, ho, wo
@@ -123,6 +127,11 @@ class Chain:
         # overlaps the rest of the forward; the last conv stage's follows it.
         convs = [i for i, st in enumerate(self.stages) if _is_conv(st)]
         self._early_at = convs[-2] if self.concurrent_learn and len(convs) >= 2 else None
+        # ... and in a step the kWTA of those layers runs on their side stream too, ahead of
+        # their plasticity (its winners feed nothing else), overlapping the next stages
+        self._side_kwta = {i: j for j, (i, st, b) in enumerate(self._learners())
+                           if self._early_at is not None and i <= self._early_at}
+        self._conv_done = {i: torch.cuda.Event() for i in self._side_kwta}
         self._launched = set()
         # step(defer_learn=True): learner stage -> its join event, waited for by the next
         # forward right before the stage that rewrites the learner's input
@@ -184,10 +193,20 @@ class Chain:
                     spk_conv_fire(x, b["weight"], st.pad, st.thr, potentials=b["P"], spikes=b["S"], t_first=b["tf"],
                                   v_first=b["vf"], workspace=self.workspace, stream=stream)
                 mark(f"conv{i}", 1)
-                mark(f"kwta{i}", 0)
-                spk_kwta(b["tf"], b["vf"], self.T, st.k, st.r, winners=b["win"], n_winners=b["nw"],
-                         workspace=self.workspace, stream=stream)
-                mark(f"kwta{i}", 1)
+                if early_learn and i in self._side_kwta:
+                    side = self._side[self._side_kwta[i]]
+                    self._conv_done[i].record(main)
+                    side.wait_event(self._conv_done[i])
+                    with torch.cuda.stream(side):  # (a hook's events go on the side stream)
+                        mark(f"kwta{i}", 0)
+                        spk_kwta(b["tf"], b["vf"], self.T, st.k, st.r, winners=b["win"], n_winners=b["nw"],
+                                 workspace=b["ws_kwta"], stream=side)
+                        mark(f"kwta{i}", 1)
+                else:
+                    mark(f"kwta{i}", 0)
+                    spk_kwta(b["tf"], b["vf"], self.T, st.k, st.r, winners=b["win"], n_winners=b["nw"],
+                             workspace=self.workspace, stream=stream)
+                    mark(f"kwta{i}", 1)
                 if early_learn and i == self._early_at:
                     self._launch_learners(lambda ii: ii <= i, self._forks[0], stream)
                 x, x_tf, x_exact = b["S"], b["tf"], False
