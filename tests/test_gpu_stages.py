@@ -160,7 +160,9 @@ def test_conv_fire_unaligned_wave():
 # direct paths.
 POOL_CASES = [(3, 15, 30, 28, 28, 2, 2, 0), (2, 15, 250, 14, 14, 3, 3, 0), (2, 30, 4, 160, 250, 7, 6, 0),
               (2, 7, 3, 9, 10, 3, 2, 1), (1, 5, 2, 5, 5, 5, 1, 2), (2, 3, 1, 1, 1, 1, 1, 0),
-              (2, 9, 8, 12, 12, 4, 2, 1), (2, 5, 12, 10, 10, 2, 2, 0)]
+              (2, 9, 8, 12, 12, 4, 2, 1), (2, 5, 12, 10, 10, 2, 2, 0),
+              # batches of a few hundred images
+              (256, 15, 30, 8, 8, 2, 2, 0), (260, 15, 25, 9, 9, 3, 3, 0)]
 
 
 @pytest.mark.parametrize("case", POOL_CASES)
