@@ -347,8 +347,8 @@ def main():
                             else "contract: every call writes its full outputs")},
         "synaptic_events_per_s": round(ev * args.steps / elapsed, 1),
         "synaptic_events_per_step": ev,
-        "roofline": {"bound": "hbm", "kernel": f"spk_conv_fire ({dominant}: pad-first-spike + weight split + "
-                                               "MFMA conv-fire launches)",
+        "roofline": {"bound": "hbm", "kernel": f"spk_conv_fire ({dominant}: padding launch + MFMA conv-fire "
+                                               "launch, which splits the weights itself)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes": nbytes[dominant], "avg_ms": round(dom_avg_ms, 4)},
