@@ -42,6 +42,11 @@ def test_workspace_sizes_are_host_only_and_consistent():
     assert spk.spk_encode_latency_workspace_size(1000, 6, 28, 28, 15) >= 1000 * 6 * 28 * 28 * 4
     assert spk.spk_kwta_workspace_size(16, 256, 256, 256) == 16 * 4096 * 8
     assert spk.spk_kwta_workspace_size(1, 1, 512, 512) == 0  # H*W above the limit
+    # below 8 images the workgroup splits' lists (16 splits of up to 16 keys per position) fit
+    assert spk.spk_kwta_workspace_size(1, 250, 14, 14) >= 16 * 196 * 16 * 8
+    assert spk.spk_kwta_workspace_size(7, 30, 28, 28) >= 7 * 16 * 784 * 16 * 8
+    # the Eq.5 kernel's split partial sums of a small batch are part of the conv workspace
+    assert spk.spk_conv_fire_workspace_size(1, 15, 250, 4, 4, 200, 5, 2) >= 25 * 200 * 16 * 4
 
 
 def _status(fn, *args):
