@@ -133,7 +133,11 @@ SPK_API int spk_validate_wave(const uint8_t *wave, int B, int T, int C, int H, i
  *              of two fixed by the layer's largest |w|, is split into two
  *              fp16 terms (relative weight error <= 2^-22 for every weight
  *              down to 2^-17 times the largest); float accumulation; the
- *              scaling is undone exactly.
+ *              scaling is undone exactly.  Repeated calls give the same
+ *              bits; the accumulation order depends on the call's size (in
+ *              Eq.5 mode a small batch's sum is split into parts added in
+ *              order), so one image's potentials may differ in the last bits
+ *              between batch sizes.
  *   spikes     u8  [B][T][Cout][Ho][Wo] or NULL: 1 where the neuron fires.
  *   t_first    u8  [B][Cout][Ho][Wo]: first firing step, T if silent.
  *   v_first    f32 [B][Cout][Ho][Wo]: potential at t_first, 0 if silent.
