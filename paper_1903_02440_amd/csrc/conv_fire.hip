@@ -67,6 +67,15 @@ struct ConvGeom {
 constexpr int PAD_LDS = 32768;
 constexpr int PAD_RAW = 8192;   // input bytes of one image staged in LDS at most
 
+// LDS of the padding kernel: the padded rows of a chunk, then the raw map of a
+// whole image when staged (a whole-image chunk of 4-byte words, at most PAD_RAW).
+__host__ __device__ inline int pad_raw_offset(const ConvGeom &g, int rows_per_chunk) {
+    return (rows_per_chunk * g.Wp * g.CP + 16 + 15) / 16 * 16;
+}
+__host__ __device__ inline bool pad_raw_fits(const ConvGeom &g, int nchunk) {
+    return nchunk == 1 && (g.Cin * g.H * g.W) % 4 == 0 && g.Cin * g.H * g.W <= PAD_RAW;
+}
+
 // Workgroups past the nchunk * ny padding ones each write the largest |w| bit
 // pattern of one run of wper weights to wmax[part] (the weights' scale, below).
 constexpr int WMAX_PARTS = 2048;  // weight-maximum partials at most
@@ -78,8 +87,11 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
                                                          int rows_per_chunk, int nchunk, int ny,
                                                          uint8_t *__restrict__ tpad, const float *__restrict__ w,
                                                          int64_t nw, int wper, unsigned *__restrict__ wmax) {
-    __shared__ __attribute__((aligned(16))) uint8_t buf[PAD_LDS + 16];
-    __shared__ __attribute__((aligned(16))) uint8_t raw[TIMES ? PAD_RAW : 16];
+    // dynamic LDS: the chunk's padded rows (+16 for the alignment shift), then,
+    // for a whole-image first-spike map that fits, the raw map (pad_lds_split)
+    extern __shared__ uint4 pad_lds[];
+    uint8_t *buf = reinterpret_cast<uint8_t *>(pad_lds);
+    uint8_t *raw = buf + pad_raw_offset(g, rows_per_chunk);
     const int tid = threadIdx.x;
     if ((int)blockIdx.x >= nchunk * ny) {
         const int part = (int)blockIdx.x - nchunk * ny;
@@ -118,8 +130,7 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
         const uint8_t *src = wave + b * (TIMES ? 1 : g.T) * (int64_t)g.Cin * hw;
         // A whole image's first-spike map is one contiguous block: it is read
         // with word loads, all issued before any is used, into LDS first.
-        const bool staged = TIMES && nchunk == 1 && ((uintptr_t)src & 3) == 0 && (g.Cin * hw) % 4 == 0 &&
-                            g.Cin * hw <= PAD_RAW;
+        const bool staged = TIMES && pad_raw_fits(g, nchunk) && ((uintptr_t)src & 3) == 0;
         if (staged) {
             const int nwd = g.Cin * hw / 4;
             const uint32_t *s4 = reinterpret_cast<const uint32_t *>(src);
@@ -1270,14 +1281,16 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     const int rows_per_chunk = std::min(g.Hp, PAD_LDS / row_bytes);
     const int nchunk = (int)spk::ceil_div(g.Hp, rows_per_chunk), ny = std::min(B, 65535);
     const int64_t nw = (int64_t)Cout * Cin * K * K;
-    const int wper = (int)spk::align_up((size_t)std::max<int64_t>(1024, spk::ceil_div(nw, WMAX_PARTS)), 1024);
+    const int wper = (int)spk::align_up((size_t)std::max<int64_t>(4096, spk::ceil_div(nw, WMAX_PARTS)), 1024);
+    const size_t pad_lds =
+        (size_t)pad_raw_offset(g, rows_per_chunk) + (pad_raw_fits(g, nchunk) ? (size_t)Cin * H * W : 0);
     const int n_wmax = (int)spk::ceil_div(nw, wper);
     const dim3 pad_grid((unsigned)((int64_t)nchunk * ny + n_wmax));
     if (times)
-        hipLaunchKernelGGL(k_pad_first_spike<true>, pad_grid, dim3(256), 0, st, wave, g, rows_per_chunk, nchunk, ny,
+        hipLaunchKernelGGL(k_pad_first_spike<true>, pad_grid, dim3(256), pad_lds, st, wave, g, rows_per_chunk, nchunk, ny,
                            tpad, weight, nw, wper, wmax);
     else
-        hipLaunchKernelGGL(k_pad_first_spike<false>, pad_grid, dim3(256), 0, st, wave, g, rows_per_chunk, nchunk, ny,
+        hipLaunchKernelGGL(k_pad_first_spike<false>, pad_grid, dim3(256), pad_lds, st, wave, g, rows_per_chunk, nchunk, ny,
                            tpad, weight, nw, wper, wmax);
     if (inf_mode || !blds) {  // fragments in the workspace (the finite-threshold kernel with LDS room builds its own)
         const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
