@@ -25,6 +25,10 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+# The arithmetic of the conv contraction (the rest of the path is u8 spike
+# logic and f32/f64 scalar updates)
+DTYPE = ("f32 weights as 16-bit MFMA terms (fp16 x2, or bf16 x3 when the layer's weight range needs it), "
+         "f32 accumulate")
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 
 
@@ -158,7 +162,7 @@ def online_bench(wl, inp, dev, group):
     print(json.dumps({"metric": "online images/s (one image per step: forward with the weights the previous "
                                 "images left, then plasticity)", "value": round(n / dt, 1), "unit": "images/s",
                       "n_gpus": 1, "images": n, "ms_per_image": round(dt * 1e3 / n, 4), "higher_is_better": True,
-                      "dtype": "f32", "data": "synthetic",
+                      "dtype": DTYPE, "data": "synthetic",
                       "config": {"workload": wl.name, "T": wl.T, "steps_per_graph": group,
                                  "form": "compact (no per-step potentials)"}}), flush=True)
 
@@ -336,7 +340,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": DTYPE,
         "data": "synthetic",
         "config": {"workload": wl.name, "global_batch": wl.B, "T": wl.T,
                    "layers": [f"conv {s.cin}->{s.cout} k{s.K} p{s.pad} thr {s.thr} kwta {s.k}/{s.r} {s.learn}"

@@ -9,14 +9,25 @@
 // where k runs over the receptive field and tp_k is the first-spike step of
 // that input neuron (Eq.1 makes S[t] = [tp <= t]).  Per image this is a GEMM
 // P_t[pos, f] = A_t[pos, k] * W^T[k, f] for every t, with a binary A_t made on
-// the fly from the u8 first-spike map.  It runs on the fp16 matrix cores
-// (v_mfma_f32_16x16x32_f16): a spike is fp16 1.0, produced for two taps at
-// once by one packed add with clamping, clamp((1025 + t) - (1024 + tp)), which
-// is 1 exactly when tp <= t and 0 otherwise; every fp32 weight, scaled by a
-// power of two so that the layer's largest |w| lies in [2^12, 2^13), is split
-// into hi = fp16(v), lo = fp16(v - hi), so each product pair carries 22
-// significant bits of w for every weight down to 2^-17 times the largest;
-// accumulation is fp32 and the scale is undone exactly.
+// the fly from the u8 first-spike map.  It runs on the 16-bit matrix cores: a
+// spike is produced for two taps at once by one packed fp16 add with clamping,
+// clamp((1025 + t) - (1024 + tp)), which is 1.0 exactly when tp <= t and 0
+// otherwise.  The same bits (0x3C00) read as bf16 are 2^-7, so one spike
+// operand serves both MFMA types.  The fp32 weights, scaled by a power of two,
+// become sums of 16-bit terms, chosen per call from the layer's largest and
+// smallest non-zero |w| (both reduced on the device):
+//   * two fp16 terms hi = fp16(v), lo = fp16(v - hi)
+//     (v_mfma_f32_16x16x32_f16) when every non-zero |w| is at least 2^-15
+//     times the largest one's power of two: each weight is then carried to
+//     within 2^-22 of itself;
+//   * otherwise three bf16 terms hi = bf16(v), mid = bf16(v - hi),
+//     lo = v - hi - mid (v_mfma_f32_16x16x32_bf16), which represent the
+//     weights exactly: bf16 has float's exponent range, and the three 8-bit
+//     significands cover float's 24 bits (every float weight when the
+//     largest |w| is below 2^8; else every |w| >= 2^-156 times the largest
+//     one's power of two).
+// Products with a spike are exact either way; accumulation is fp32, and the
+// scale is undone exactly.
 //
 // Pipeline of one call (all on the caller's stream):
 //   1. k_pad_first_spike: wave [B,T,Cin,H,W] -> zero-padded first-spike map in
@@ -24,10 +35,12 @@
 //      or to a multiple of 8; padding and padded channels hold T = never).
 //      Taps are ordered k = (ky*K + kx)*CP + ci, so the 8 taps a lane feeds to
 //      one MFMA are two 4-byte words of tpad.
-//      The same launch reduces |W| to per-block maxima (extra workgroups).
-//   2. W -> scaled hi/lo fp16 B-operand fragments and the per-lane word offsets
-//      of every 8-tap group: built by the finite-threshold kernel itself when
-//      its fragments fit in LDS, else by k_split_weights into the workspace.
+//      The same launch reduces |W| to per-block maxima and non-zero minima
+//      (extra workgroups).
+//   2. W -> scaled 16-bit B-operand fragments (two or three terms) and the
+//      per-lane word offsets of every 8-tap group: built by the
+//      finite-threshold kernel itself when its fragments fit in LDS, else by
+//      k_split_weights into the workspace.
 //   3. finite threshold: k_conv_fire_fin (below); threshold = +inf (Eq.5):
 //      k_conv_fire_inf, which computes only the last step.
 #include <algorithm>
@@ -40,6 +53,7 @@
 namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
@@ -76,9 +90,11 @@ __host__ __device__ inline bool pad_raw_fits(const ConvGeom &g, int nchunk) {
     return nchunk == 1 && (g.Cin * g.H * g.W) % 4 == 0 && g.Cin * g.H * g.W <= PAD_RAW;
 }
 
-// Workgroups past the nchunk * ny padding ones each write the largest |w| bit
-// pattern of one run of wper weights to wmax[part] (the weights' scale, below).
-constexpr int WMAX_PARTS = 2048;  // weight-maximum partials at most
+// Workgroups past the nchunk * ny padding ones each write, for one run of wper
+// weights, the bit patterns of the largest |w| to wmax[part] and of the
+// smallest non-zero |w| to wmin[part] (0xFFFFFFFF if the run is all zeros):
+// they fix the weights' scale and split (below).
+constexpr int WMAX_PARTS = 2048;  // weight-range partials at most
 
 // TIMES: the input is the first-spike map t_first [B][Cin][H][W] itself (T = never).
 // 1D grid: workgroup (chunk, yb) = (id % nchunk, id / nchunk) pads images yb, yb + ny, ...
@@ -86,7 +102,8 @@ template <bool TIMES>
 __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restrict__ wave, ConvGeom g,
                                                          int rows_per_chunk, int nchunk, int ny,
                                                          uint8_t *__restrict__ tpad, const float *__restrict__ w,
-                                                         int64_t nw, int wper, unsigned *__restrict__ wmax) {
+                                                         int64_t nw, int wper, unsigned *__restrict__ wmax,
+                                                         unsigned *__restrict__ wmin) {
     // dynamic LDS: the chunk's padded rows (+16 for the alignment shift), then,
     // for a whole-image first-spike map that fits, the raw map (pad_lds_split)
     extern __shared__ uint4 pad_lds[];
@@ -96,21 +113,34 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
     if ((int)blockIdx.x >= nchunk * ny) {
         const int part = (int)blockIdx.x - nchunk * ny;
         const int64_t i1 = min(nw, (int64_t)(part + 1) * wper);
-        unsigned m = 0;
+        unsigned m = 0, mn = 0xFFFFFFFFu;
         // four independent loads per thread and pass
         for (int64_t i0 = (int64_t)part * wper + tid; i0 < i1; i0 += 1024) {
             float v[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) v[j] = i0 + 256 * j < i1 ? w[i0 + 256 * j] : 0.0f;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) m = max(m, __float_as_uint(fabsf(v[j])));
+            for (int j = 0; j < 4; ++j) {
+                const unsigned b = __float_as_uint(fabsf(v[j]));
+                m = max(m, b);
+                mn = b ? min(mn, b) : mn;
+            }
         }
 #pragma unroll
-        for (int s = 32; s >= 1; s >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, s, 64));
+        for (int s = 32; s >= 1; s >>= 1) {
+            m = max(m, (unsigned)__shfl_xor((int)m, s, 64));
+            mn = min(mn, (unsigned)__shfl_xor((int)mn, s, 64));
+        }
         unsigned *red = reinterpret_cast<unsigned *>(buf);
-        if ((tid & 63) == 0) red[tid >> 6] = m;
+        if ((tid & 63) == 0) {
+            red[tid >> 6] = m;
+            red[4 + (tid >> 6)] = mn;
+        }
         __syncthreads();
-        if (tid == 0) wmax[part] = max(max(red[0], red[1]), max(red[2], red[3]));
+        if (tid == 0) {
+            wmax[part] = max(max(red[0], red[1]), max(red[2], red[3]));
+            wmin[part] = min(min(red[4], red[5]), min(red[6], red[7]));
+        }
         return;
     }
     const int row_bytes = g.Wp * g.CP;
@@ -187,30 +217,69 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
 }
 
 // ------------------------------------------------------------------ 2. weight fragments
-// Every weight is scaled by s = 2^e, e = 12 - E with E the exponent of max|w|,
-// so the largest scaled weight lies in [2^12, 2^13): both terms of the split
-// are then normal fp16 for every weight down to max|w| * 2^-17, i.e.
-// w*s = hi + lo + err with |err| <= 2^-22 |w*s|.  The GEMM result is
-// multiplied back by 1/s (exact).  Fragment (nt, ks, lane) holds, for feature
-// n = nt*16 + lane%16, the 8 taps k = ks*32 + 8*(lane/16) + j, j = 0..7.
-__device__ __forceinline__ int weight_scale_exp(unsigned maxbits) {
+// Weight split of a call, from the bit patterns of the largest |w| (maxbits)
+// and the smallest non-zero |w| (minbits; 0xFFFFFFFF when all are zero).
+// With E the exponent of max|w|:
+//   * nt = 2 (fp16 hi/lo): v = w * 2^e with e = 12 - E, so the largest |v|
+//     lies in [2^12, 2^13).  For |v| >= 2^-3 both terms keep 11 significant
+//     bits (lo, if subnormal, is still within 2^-25 <= 2^-22 |v|), so
+//     |v - hi - lo| <= 2^-22 |v|.  Taken when every non-zero |w| >= 2^(E-15)
+//     and |E| <= 100.
+//   * nt = 3 (bf16 hi/mid/lo) otherwise: v = w * 2^e with e = 60 - max(E, -60),
+//     so |v| < 2^61, and for |w| >= 2^(E-156) (every float when E <= 7) every
+//     non-zero term is at least 2^-119, normal even times a spike's 2^-7;
+//     hi + mid + lo == v exactly (v - hi and v - hi - mid are exact in float
+//     and carry at most 16 and 8 significant bits).  A spike is 2^-7 as
+//     bf16, so the sums are scaled by 2^(e - 7).
+// inv_s undoes the scale (a power of two, exact).
+struct WSplit {
+    int nt;
+    int e;
+    float inv_s;
+};
+
+__device__ __forceinline__ WSplit weight_split(unsigned maxbits, unsigned minbits) {
     const int E = maxbits ? (int)((maxbits >> 23) & 255u) - 127 : 0;  // subnormal maxima count as 2^-127
-    return 12 - max(-100, min(100, E));
+    if (E >= -100 && E <= 100 && minbits >= ((unsigned)(E - 15 + 127) << 23)) return {2, 12 - E, ldexpf(1.0f, E - 12)};
+    const int e = 60 - max(E, -60);
+    return {3, e, ldexpf(1.0f, 7 - e)};
 }
 
-// Largest of the n weight-maximum partials, returned to every thread of the
-// workgroup (blockDim.x a multiple of 64; red: blockDim.x / 64 words of LDS).
-__device__ unsigned reduce_wmax(const unsigned *__restrict__ parts, int n, unsigned *red) {
-    unsigned m = 0;
-    for (int i = threadIdx.x; i < n; i += blockDim.x) m = max(m, parts[i]);
+// Largest of the n maximum partials and smallest of the n minimum partials,
+// returned to every thread of the workgroup (blockDim.x a multiple of 64;
+// red: 2 * blockDim.x / 64 words of LDS).
+__device__ uint2 reduce_wrange(const unsigned *__restrict__ pmax, const unsigned *__restrict__ pmin, int n,
+                               unsigned *red) {
+    unsigned m = 0, mn = 0xFFFFFFFFu;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+        m = max(m, pmax[i]);
+        mn = min(mn, pmin[i]);
+    }
 #pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) m = max(m, (unsigned)__shfl_xor((int)m, s, 64));
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    for (int s = 32; s >= 1; s >>= 1) {
+        m = max(m, (unsigned)__shfl_xor((int)m, s, 64));
+        mn = min(mn, (unsigned)__shfl_xor((int)mn, s, 64));
+    }
+    const int nw = (int)(blockDim.x >> 6);
+    if ((threadIdx.x & 63) == 0) {
+        red[threadIdx.x >> 6] = m;
+        red[nw + (threadIdx.x >> 6)] = mn;
+    }
     __syncthreads();
     m = 0;
-    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) m = max(m, red[i]);
+    mn = 0xFFFFFFFFu;
+    for (int i = 0; i < nw; ++i) {
+        m = max(m, red[i]);
+        mn = min(mn, red[nw + i]);
+    }
     __syncthreads();
-    return m;
+    return uint2{m, mn};
+}
+
+// bf16 bits of v rounded to nearest even (v finite, |v| < 2^127).
+__device__ __forceinline__ uint32_t bf16_bits(float v) {
+    const uint32_t u = __float_as_uint(v);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
 // Tap (K-step ks, lane group gq, j) of the padded receptive field -> (cell kyx,
@@ -236,23 +305,42 @@ __device__ __forceinline__ void tap_of(const ConvGeom &g, int ks, int gq, int j,
 // to the output position's top-left input cell) of its two 4-byte words; with
 // CP >= 8 they are adjacent, with CP == 4 they are the cells 2q and 2q+1.
 // Groups past the receptive field point at offset 0 (their weights are 0).
-// hi / lo fp16 halves of fragment (nt, ks, lane), weights scaled by 2^e; w holds
-// the weights of features n0, n0 + 1, ... ([Cout - n0][Cin][K][K]).
+//
+// Fragment (nt, ks, lane) holds, for feature n = nt*16 + lane%16, the 8 taps
+// k = ks*32 + 8*(lane/16) + j, j = 0..7, as s.nt 16-bit terms (each a uint4 of
+// 8 fp16 or bf16 values).  w holds the weights of features n0, n0 + 1, ...
+// ([Cout - n0][Cin][K][K]).
+constexpr int NT_MAX = 3;  // fragment terms at most (storage stride)
+
 __device__ __forceinline__ void split_fragment(const float *w, int n0, const ConvGeom &g, int nt, int ks, int lane,
-                                               int e, half8 &h, half8 &l) {
+                                               const WSplit &s, uint4 (&out)[NT_MAX]) {
     const int KK = g.K * g.K;
     const int n = nt * 16 + (lane & 15);
+    uint32_t t[NT_MAX][4] = {};
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         int kyx, ci;
         tap_of(g, ks, lane >> 4, j, kyx, ci);
         float v = 0.0f;
-        if (n < g.Cout && kyx < KK && ci < g.Cin) v = ldexpf(w[((int64_t)(n - n0) * g.Cin + ci) * KK + kyx], e);
-        const _Float16 hv = (_Float16)v;
-        const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
-        h[j] = hv;
-        l[j] = (_Float16)rest;
+        if (n < g.Cout && kyx < KK && ci < g.Cin) v = ldexpf(w[((int64_t)(n - n0) * g.Cin + ci) * KK + kyx], s.e);
+        uint32_t h[NT_MAX];
+        if (s.nt == 2) {
+            const _Float16 hv = (_Float16)v;
+            const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
+            h[0] = __builtin_bit_cast(uint16_t, hv);
+            h[1] = __builtin_bit_cast(uint16_t, (_Float16)rest);
+            h[2] = 0;
+        } else {
+            h[0] = bf16_bits(v);
+            const float r1 = v - __uint_as_float(h[0] << 16);  // exact, at most 16 significant bits
+            h[1] = bf16_bits(r1);
+            h[2] = bf16_bits(r1 - __uint_as_float(h[1] << 16));  // exact, at most 8 significant bits
+        }
+#pragma unroll
+        for (int q = 0; q < NT_MAX; ++q) t[q][j >> 1] |= h[q] << (16 * (j & 1));
     }
+#pragma unroll
+    for (int q = 0; q < NT_MAX; ++q) out[q] = uint4{t[q][0], t[q][1], t[q][2], t[q][3]};
 }
 
 // Word offsets of the 8-tap group q (koff2 below).
@@ -272,22 +360,30 @@ __device__ __forceinline__ int2 koff_of(const ConvGeom &g, int q) {
     return o;
 }
 
+// Fragments of every 16-feature tile into the workspace, frag[nt][ks][term][64]
+// (NT_MAX terms of stride; the unused third is zero when nt == 2), the tap
+// offsets, and the split's term count and inverse scale.
 __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__ w, ConvGeom g,
-                                                       const unsigned *__restrict__ wmax, int n_wmax,
-                                                       half8 *__restrict__ whi, half8 *__restrict__ wlo,
-                                                       int2 *__restrict__ koff2, float *__restrict__ inv_scale) {
-    __shared__ unsigned red[4];
-    const int e = weight_scale_exp(reduce_wmax(wmax, n_wmax, red));
+                                                       const unsigned *__restrict__ wmax,
+                                                       const unsigned *__restrict__ wmin, int n_wmax,
+                                                       uint4 *__restrict__ frag, int2 *__restrict__ koff2,
+                                                       float *__restrict__ inv_scale, int *__restrict__ nterms) {
+    __shared__ unsigned red[8];
+    const uint2 mm = reduce_wrange(wmax, wmin, n_wmax, red);
+    const WSplit ws = weight_split(mm.x, mm.y);
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t total = (int64_t)g.ntiles * g.ksteps * 64;
-    if (i == 0) *inv_scale = ldexpf(1.0f, -e);
+    if (i == 0) {
+        *inv_scale = ws.inv_s;
+        *nterms = ws.nt;
+    }
     if (i < total) {
         const int lane = (int)(i & 63);
         const int64_t r = i >> 6;
-        half8 h, l;
-        split_fragment(w, 0, g, (int)(r / g.ksteps), (int)(r % g.ksteps), lane, e, h, l);
-        whi[i] = h;
-        wlo[i] = l;
+        uint4 t[NT_MAX];
+        split_fragment(w, 0, g, (int)(r / g.ksteps), (int)(r % g.ksteps), lane, ws, t);
+#pragma unroll
+        for (int q = 0; q < NT_MAX; ++q) frag[(r * NT_MAX + q) * 64 + lane] = t[q];
     }
     if (i < (int64_t)g.ksteps * 4) koff2[i] = koff_of(g, (int)i);
 }
@@ -299,21 +395,30 @@ __device__ __forceinline__ void neg_times(uint32_t w, uint32_t &lo, uint32_t &hi
     hi = __builtin_amdgcn_perm(0xE4E4E4E4u, w, 0x05030402u);
 }
 
-// Spike operand of 8 taps at step t: clamp((1025 + t) - (1024 + tp)) per tap.
-__device__ __forceinline__ half8 spike_operand(const uint32_t (&xn)[4], uint32_t ct) {
+// Spike operand of 8 taps at step t: clamp((1025 + t) - (1024 + tp)) per tap,
+// fp16 1.0 / 0 (as bf16: 2^-7 / 0).
+__device__ __forceinline__ u4 spike_operand(const uint32_t (&xn)[4], uint32_t ct) {
     u4 a;
     asm("v_pk_add_f16 %0, %1, %2 clamp" : "=v"(a.x) : "v"(ct), "v"(xn[0]));
     asm("v_pk_add_f16 %0, %1, %2 clamp" : "=v"(a.y) : "v"(ct), "v"(xn[1]));
     asm("v_pk_add_f16 %0, %1, %2 clamp" : "=v"(a.z) : "v"(ct), "v"(xn[2]));
     asm("v_pk_add_f16 %0, %1, %2 clamp" : "=v"(a.w) : "v"(ct), "v"(xn[3]));
-    return __builtin_bit_cast(half8, a);
+    return a;
 }
 
 // fp16 (1025 + t) in both halves (t <= 1022)
 __device__ __forceinline__ uint32_t step_const(int t) { return (0x6401u + (uint32_t)t) * 0x10001u; }
 
-__device__ __forceinline__ f4 mfma(half8 a, half8 b, f4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+// One 16x16x32 product of a spike operand with one weight term: fp16 terms for
+// the two-term split, bf16 for the three-term one.
+template <int NT>
+__device__ __forceinline__ f4 mfma(u4 a, uint4 b, f4 c) {
+    if constexpr (NT == 2)
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a), __builtin_bit_cast(half8, b), c, 0,
+                                                      0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, a), __builtin_bit_cast(bf8, b), c, 0, 0,
+                                                       0);
 }
 
 // ------------------------------------------------------------------ 3a. finite threshold
@@ -342,7 +447,7 @@ __device__ __forceinline__ f4 mfma(half8 a, half8 b, f4 c) {
 // rows are stored channel-group major (see k_conv_fire_fin's ALDS buffers).
 // Two waves per SIMD do the firing and storing: their VALU work and LDS
 // waits overlap each other's.
-constexpr int FIN_TB = 3;
+constexpr int FIN_TB = 3;          // time steps per block (staging depth)
 constexpr int FIN_CW = 8;          // MFMA waves (waves 0-7)
 constexpr int FIN_MT = 2;          // position tiles per MFMA wave
 constexpr int FIN_SW = 8;          // store waves (waves 8-15)
@@ -364,17 +469,17 @@ static_assert(FIN_MT == 2, "the tile slots of an MFMA wave are wv and wv + FIN_C
 
 template <int G, bool BLDS, bool ALDS>
 __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
-    const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
-    const int2 *__restrict__ koff2, ConvGeom g, int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max,
-    int a_words, const float *__restrict__ inv_scale, const float *__restrict__ wts,
-    const unsigned *__restrict__ wmax, int n_wmax, float *__restrict__ P, uint8_t *__restrict__ S,
-    uint8_t *__restrict__ TF, float *__restrict__ VF) {
+    const uint8_t *__restrict__ tpad, const uint4 *__restrict__ frag, const int2 *__restrict__ koff2, ConvGeom g,
+    int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words,
+    const float *__restrict__ inv_scale, const int *__restrict__ nterms, const float *__restrict__ wts,
+    const unsigned *__restrict__ wmax, const unsigned *__restrict__ wmin, int n_wmax, float *__restrict__ P,
+    uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
     const int gq = lane >> 4, c = lane & 15;
     int2 *koff_l = reinterpret_cast<int2 *>(lds);
-    uint4 *frag_l = lds + (g.ksteps * 4 * 8 + 15) / 16;                  // [ks][n(2)][hi/lo][64] (BLDS)
-    float *stage = reinterpret_cast<float *>(frag_l + (BLDS ? g.ksteps * 4 * 64 : 0));  // [TB][32*np_max]
+    uint4 *frag_l = lds + (g.ksteps * 4 * 8 + 15) / 16;  // [ks][n(2)][term(NT_MAX)][64] (BLDS)
+    float *stage = reinterpret_cast<float *>(frag_l + (BLDS ? g.ksteps * 2 * NT_MAX * 64 : 0));  // [TB][32*np_max]
     const int stage_t = 32 * stage_stride(np_max);
     // ALDS: 2 buffers of a_words words (a multiple of 64) holding a task's
     // padded rows channel-group major, [row][CP/8][Wp][8 bytes], so that the 16
@@ -446,10 +551,13 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) koff_l[i] = koff_of(g, i);
     }
     float inv_s;
-    if (BLDS) {  // the pair's fragments, split here from the weights: [ks][n][hi/lo][64]
+    int n_terms;
+    if (BLDS) {  // the pair's fragments, split here from the weights: [ks][n][term][64]
         // (the staging area, unused until the main loop, holds the reduction's words)
-        const int e = weight_scale_exp(reduce_wmax(wmax, n_wmax, reinterpret_cast<unsigned *>(stage)));
-        inv_s = ldexpf(1.0f, -e);
+        const uint2 mm = reduce_wrange(wmax, wmin, n_wmax, reinterpret_cast<unsigned *>(stage));
+        const WSplit ws = weight_split(mm.x, mm.y);
+        inv_s = ws.inv_s;
+        n_terms = ws.nt;
         // the pair's weights, contiguous in W, go through the staging area when
         // they fit (coalesced loads instead of one load per tap)
         const int per_f = g.Cin * g.K * g.K, nwp = nf * per_f;
@@ -461,13 +569,14 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         const float *wsrc = wl ? stage : wts + (int64_t)f0 * per_f;
         for (int i = tid; i < g.ksteps * 2 * 64; i += FIN_THREADS) {
             const int ln = i & 63, rr = i >> 6;  // rr = ks*2 + n
-            half8 h, l;
-            split_fragment(wsrc, f0, g, pair * 2 + (rr & 1), rr >> 1, ln, e, h, l);
-            frag_l[(rr * 2) * 64 + ln] = __builtin_bit_cast(uint4, h);
-            frag_l[(rr * 2 + 1) * 64 + ln] = __builtin_bit_cast(uint4, l);
+            uint4 t[NT_MAX];
+            split_fragment(wsrc, f0, g, pair * 2 + (rr & 1), rr >> 1, ln, ws, t);
+#pragma unroll
+            for (int q = 0; q < NT_MAX; ++q) frag_l[(rr * NT_MAX + q) * 64 + ln] = t[q];
         }
     } else {
         inv_s = *inv_scale;
+        n_terms = *nterms;
     }
     if (ALDS) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -478,9 +587,11 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         // Every wave computes up to two tiles of 16 positions for the 32 features;
         // positions of a tile past the chunk repeat its last position and are
         // never stored, which keeps the MFMA stream free of branches.  The K-step
-        // loop is compiled once per second-slot mode (below).
-        const half8 *gh = whi + (int64_t)(pair * 2) * g.ksteps * 64 + lane;
-        const half8 *gl = wlo + (int64_t)(pair * 2) * g.ksteps * 64 + lane;
+        // loop is compiled once per weight split (NT terms) and second-slot mode
+        // (below).
+        const uint4 *gf = frag + (int64_t)(pair * 2) * g.ksteps * NT_MAX * 64 + lane;
+        auto mfma_waves = [&](auto nt_c) {
+        constexpr int NT = decltype(nt_c)::value;
         int abuf_sel = 0;
         for (int task = t_lo + r; task < t_hi; task += R) {
             int pos0, np;
@@ -527,15 +638,16 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             auto blocks = [&](auto mode_c) {
             constexpr int M = decltype(mode_c)::value;
             constexpr int MT = M == 3 ? 1 : FIN_MT;  // slots with work
-            for (int tb0 = (g.T - 1) / FIN_TB * FIN_TB; tb0 >= 0; tb0 -= FIN_TB) {  // latest steps first
+            constexpr int TB = FIN_TB;
+            for (int tb0 = (g.T - 1) / TB * TB; tb0 >= 0; tb0 -= TB) {  // latest steps first
                 const bool last_block = tb0 == 0;
-                f4 acc[FIN_MT][2][FIN_TB];
+                f4 acc[FIN_MT][2][TB];
 #pragma unroll
                 for (int i = 0; i < FIN_MT; ++i)
 #pragma unroll
                     for (int n = 0; n < 2; ++n)
 #pragma unroll
-                        for (int t = 0; t < FIN_TB; ++t) acc[i][n][t] = f4{0.f, 0.f, 0.f, 0.f};
+                        for (int t = 0; t < TB; ++t) acc[i][n][t] = f4{0.f, 0.f, 0.f, 0.f};
                 // Software pipeline, unrolled by two K-steps with two register sets:
                 // while K-step ks runs on the matrix cores, the spike words and weight
                 // fragments of ks+1 are in flight and the tap offsets of ks+2 are read.
@@ -553,22 +665,20 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                         }
                     }
                 };
-                auto load_b = [&](half8 (&bn)[4], int ks) {
-                    if (BLDS) {
-                        const uint4 *fr = frag_l + ks * 256 + lane;
-                        bn[0] = __builtin_bit_cast(half8, fr[0]);
-                        bn[1] = __builtin_bit_cast(half8, fr[64]);
-                        bn[2] = __builtin_bit_cast(half8, fr[128]);
-                        bn[3] = __builtin_bit_cast(half8, fr[192]);
-                    } else {
-                        bn[0] = gh[ks * 64];
-                        bn[1] = gl[ks * 64];
-                        bn[2] = gh[(g.ksteps + ks) * 64];
-                        bn[3] = gl[(g.ksteps + ks) * 64];
-                    }
+                // B fragments of a K-step: bn[n * NT + q] = term q of feature tile n
+                auto load_b = [&](uint4 (&bn)[2 * NT], int ks) {
+                    // (one base address per K-step and constant offsets: per-fragment
+                    // addresses would each hold a register through the loop)
+                    const uint4 *fr = frag_l + ks * (2 * NT_MAX * 64) + lane;
+#pragma unroll
+                    for (int n = 0; n < 2; ++n)
+#pragma unroll
+                        for (int q = 0; q < NT; ++q)
+                            bn[n * NT + q] = BLDS ? fr[(n * NT_MAX + q) * 64]
+                                                  : gf[((n * g.ksteps + ks) * NT_MAX + q) * 64];
                 };
-                // one K-step: spike operands from the words, then TB x 4 tiles x 2 features x hi/lo
-                auto kstep = [&](const uint32_t (&an)[FIN_MT][2], const half8 (&bc)[4]) {
+                // one K-step: spike operands from the words, then TB x 4 tiles x 2 features x NT terms
+                auto kstep = [&](const uint32_t (&an)[FIN_MT][2], const uint4 (&bc)[2 * NT]) {
                     uint32_t xn[FIN_MT][4];
 #pragma unroll
                     for (int i = 0; i < MT; ++i) {
@@ -576,26 +686,25 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                         neg_times(an[i][1], xn[i][2], xn[i][3]);
                     }
 #pragma unroll
-                    for (int t = 0; t < FIN_TB; ++t) {
+                    for (int t = 0; t < TB; ++t) {
                         const uint32_t ct = step_const(tb0 + t);
-                        half8 a[FIN_MT];
+                        u4 a[FIN_MT];
 #pragma unroll
                         for (int i = 0; i < MT; ++i) a[i] = spike_operand(xn[i], ct);
-                        // all hi products first, then the lo ones: dependent MFMAs are 8 apart
+                        // one term of every unit after the other: dependent MFMAs are 8 apart
 #pragma unroll
-                        for (int i = 0; i < MT; ++i)
+                        for (int q = 0; q < NT; ++q)
 #pragma unroll
-                            for (int n = 0; n < 2; ++n)
-                                if (fin_unit<M>(i, n)) acc[i][n][t] = mfma(a[i], bc[2 * n], acc[i][n][t]);
+                            for (int i = 0; i < MT; ++i)
 #pragma unroll
-                        for (int i = 0; i < MT; ++i)
-#pragma unroll
-                            for (int n = 0; n < 2; ++n)
-                                if (fin_unit<M>(i, n)) acc[i][n][t] = mfma(a[i], bc[2 * n + 1], acc[i][n][t]);
+                                for (int n = 0; n < 2; ++n)
+                                    if (fin_unit<M>(i, n))
+                                        acc[i][n][t] = mfma<NT>(a[i], bc[n * NT + q], acc[i][n][t]);
                     }
                 };
+                if constexpr (NT == 2) {
                 uint32_t a0[FIN_MT][2], a1[FIN_MT][2];
-                half8 b0[4], b1[4];
+                uint4 b0[2 * NT], b1[2 * NT];
                 int2 o2 = koff_at(0);
                 load_a(a0, o2);
                 load_b(b0, 0);
@@ -617,6 +726,71 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                     load_b(b1, min(ks + 3, g.ksteps - 1));
                 }
                 if (ks < g.ksteps) kstep(a0, b0);
+                } else {
+                // Three terms, term-major: a K-step's spike operands for all TB
+                // steps are formed once, then each term's 4*TB products run while
+                // the next term's two fragments are read (only one term of B is
+                // held in flight: the three-term fragments would not fit the
+                // registers double-buffered whole).  Unrolled by two K-steps so
+                // that the alternating register sets stay static.
+                auto load_bq = [&](uint4 (&bn)[2], int ks, int q) {
+                    const uint4 *fr = frag_l + ks * (2 * NT_MAX * 64) + lane;
+#pragma unroll
+                    for (int n = 0; n < 2; ++n)
+                        bn[n] = BLDS ? fr[(n * NT_MAX + q) * 64] : gf[((n * g.ksteps + ks) * NT_MAX + q) * 64];
+                };
+                auto spikes_of = [&](const uint32_t (&an)[FIN_MT][2], u4 (&a)[FIN_MT][TB]) {
+#pragma unroll
+                    for (int i = 0; i < MT; ++i) {
+                        uint32_t xn[4];
+                        neg_times(an[i][0], xn[0], xn[1]);
+                        neg_times(an[i][1], xn[2], xn[3]);
+#pragma unroll
+                        for (int t = 0; t < TB; ++t) a[i][t] = spike_operand(xn, step_const(tb0 + t));
+                    }
+                };
+                auto term = [&](const u4 (&a)[FIN_MT][TB], const uint4 (&bq)[2]) {
+#pragma unroll
+                    for (int t = 0; t < TB; ++t)
+#pragma unroll
+                        for (int i = 0; i < MT; ++i)
+#pragma unroll
+                            for (int n = 0; n < 2; ++n)
+                                if (fin_unit<M>(i, n)) acc[i][n][t] = mfma<3>(a[i][t], bq[n], acc[i][n][t]);
+                };
+                uint32_t aw0[FIN_MT][2], aw1[FIN_MT][2];
+                uint4 bq0[2], bq1[2];
+                u4 a[FIN_MT][TB];
+                load_a(aw0, koff_at(0));
+                load_bq(bq0, 0, 0);
+                int ks = 0;
+                for (; ks + 1 < g.ksteps; ks += 2) {
+                    spikes_of(aw0, a);
+                    load_a(aw1, koff_at(ks + 1));
+                    load_bq(bq1, ks, 1);
+                    term(a, bq0);
+                    load_bq(bq0, ks, 2);
+                    term(a, bq1);
+                    load_bq(bq1, ks + 1, 0);
+                    term(a, bq0);
+                    spikes_of(aw1, a);
+                    load_a(aw0, koff_at(ks + 2));
+                    load_bq(bq0, ks + 1, 1);
+                    term(a, bq1);
+                    load_bq(bq1, ks + 1, 2);
+                    term(a, bq0);
+                    load_bq(bq0, min(ks + 2, g.ksteps - 1), 0);
+                    term(a, bq1);
+                }
+                if (ks < g.ksteps) {  // an odd last K-step: its words are in aw0, its first term in bq0
+                    spikes_of(aw0, a);
+                    load_bq(bq1, ks, 1);
+                    term(a, bq0);
+                    load_bq(bq0, ks, 2);
+                    term(a, bq1);
+                    term(a, bq0);
+                }
+                }
                 __syncthreads();  // staging free: the store waves are done with the previous block
                 // Staging offset = the lane's part (feature c, positions 4*gq..) plus a
                 // wave-uniform part; the lane part is made opaque here so that the
@@ -626,7 +800,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 int lofs = c * sp + gq * 4;
                 asm volatile("" : "+v"(lofs));
 #pragma unroll
-                for (int t = 0; t < FIN_TB; ++t) {
+                for (int t = 0; t < TB; ++t) {
                     if (tb0 + t >= g.T) break;
                     float *st = stage + t * stage_t + lofs;
 #pragma unroll
@@ -666,6 +840,11 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             }
             abuf_sel ^= 1;
         }
+        };
+        if (n_terms == 3)
+            mfma_waves(std::integral_constant<int, 3>{});
+        else
+            mfma_waves(std::integral_constant<int, 2>{});
     } else {
         // ------------------------------------------------ store waves
         const int s = tid - FIN_CW * 64;
@@ -773,8 +952,14 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 constexpr int INF_WAVES = 8;
 constexpr int INF_MW = 2;   // position tiles per wave
 constexpr int INF_NW = 4;   // 16-feature tiles per workgroup
-constexpr int INF_KC = 8;   // K-steps per LDS chunk
-constexpr int INF_CHUNK_U4 = INF_KC * INF_NW * 2 * 64;  // uint4 per chunk buffer
+// K-steps per LDS chunk: 8 with two weight terms, 4 with three (so that a K
+// range made of whole 8-step chunks is whole chunks for both)
+template <int NT>
+constexpr int inf_kc() { return NT == 2 ? 8 : 4; }
+template <int NT>
+constexpr int inf_chunk_u4() { return inf_kc<NT>() * INF_NW * NT * 64; }  // uint4 per chunk buffer
+constexpr int INF_CHUNK_U4_MAX = inf_chunk_u4<2>() > inf_chunk_u4<3>() ? inf_chunk_u4<2>() : inf_chunk_u4<3>();
+constexpr int INF_KPART = 8;  // a K part is a multiple of this many K-steps
 constexpr int INF_ZW = 4;   // zero waves (waves 8-11)
 constexpr int64_t INF_PART_MAX = 1 << 21;  // floats of split partial sums at most
 
@@ -784,31 +969,32 @@ constexpr int64_t INF_PART_MAX = 1 << 21;  // floats of split partial sums at mo
 // two barriers.
 template <bool VEC>
 __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
-    const uint8_t *__restrict__ tpad, const half8 *__restrict__ whi, const half8 *__restrict__ wlo,
-    const int2 *__restrict__ koff2, ConvGeom g, int n_mb, int n_ng, int ksplit, float *__restrict__ part,
-    const float *__restrict__ inv_scale, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
+    const uint8_t *__restrict__ tpad, const uint4 *__restrict__ frag, const int2 *__restrict__ koff2, ConvGeom g,
+    int n_mb, int n_ng, int ksplit, int kpp, float *__restrict__ part, const float *__restrict__ inv_scale,
+    const int *__restrict__ nterms, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
     float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     int2 *koff_l = reinterpret_cast<int2 *>(lds);
-    uint4 *cbuf = lds + (g.ksteps * 4 * 8 + 15) / 16;  // 2 chunk buffers [ksl][n][hi/lo][64]
+    uint4 *cbuf = lds + (g.ksteps * 4 * 8 + 15) / 16;  // 2 chunk buffers [ksl][n][term][64]
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int gq = lane >> 4, c = lane & 15;
     for (int i = tid; i < g.ksteps * 4; i += (INF_WAVES + INF_ZW) * 64) koff_l[i] = koff2[i];
     const float inv_s = *inv_scale;
+    const int n_terms = *nterms;
     const uint32_t ct = step_const(g.T - 1);
-    const int nchunks = (g.ksteps + INF_KC - 1) / INF_KC;
     const int x = blockIdx.x % 8, j = blockIdx.x / 8, per_xcd = (int)gridDim.x / 8;
     const int ntask = n_mb * n_ng * ksplit, per_x = (ntask + 7) / 8;
     const int t_lo = x * per_x, t_hi = min(ntask, t_lo + per_x);
     const int64_t tstride = (int64_t)g.Cout * g.HoWo;
     // With ksplit > 1 a task is (feature group, position block, part of the K
-    // chunks): its raw sums go to part[kp][B][Cout][HoWo], added up in part
-    // order by k_inf_reduce.
-    const int cpp = (nchunks + ksplit - 1) / ksplit;
-    auto chunk_range = [&](int task, int &c_lo, int &c_hi) {
-        c_lo = (task % ksplit) * cpp;
-        c_hi = min(nchunks, c_lo + cpp);
+    // steps: kpp of them, a multiple of INF_KPART): its raw sums go to
+    // part[kp][B][Cout][HoWo], added up in part order by k_inf_reduce.
+    auto chunk_range = [&](int task, int kc, int &c_lo, int &c_hi) {
+        const int k_lo = (task % ksplit) * kpp, k_hi = min(g.ksteps, k_lo + kpp);
+        c_lo = k_lo / kc;
+        c_hi = k_hi > k_lo ? (k_hi + kc - 1) / kc : c_lo;
     };
+    const int kc_run = n_terms == 3 ? inf_kc<3>() : inf_kc<2>();
 
     if (wv >= INF_WAVES) {
         // zero waves: 16-byte units of potentials (4 per unit) and 4-byte units of spikes
@@ -821,12 +1007,13 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         int nint = 1;  // barrier intervals (the last one after the loop)
         for (int task = t_lo + j; task < t_hi; task += per_xcd) {
             int c_lo, c_hi;
-            chunk_range(task, c_lo, c_hi);
+            chunk_range(task, kc_run, c_lo, c_hi);
             nint += 1 + max(0, c_hi - c_lo);
         }
         const int64_t per = (total + nint - 1) / nint;
         int64_t u0 = 0;
         auto slice = [&]() {
+            if (!VEC) return;  // a separate fill kernel writes the zeros
             const int64_t u1 = min(total, u0 + per);
             for (int64_t u = u0 + zt; u < u1; u += INF_ZW * 64) {
                 const int64_t im = u / (zp + zs), r = u - im * (zp + zs);
@@ -840,7 +1027,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         };
         for (int task = t_lo + j; task < t_hi; task += per_xcd) {
             int c_lo, c_hi;
-            chunk_range(task, c_lo, c_hi);
+            chunk_range(task, kc_run, c_lo, c_hi);
             slice();
             __syncthreads();  // the MFMA waves' "buffers free"
             for (int ch = c_lo; ch < c_hi; ++ch) {
@@ -852,20 +1039,23 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         return;
     }
 
+    auto mfma_waves = [&](auto nt_c) {
+    constexpr int NT = decltype(nt_c)::value;
+    constexpr int KC = inf_kc<NT>();
+    constexpr int CHUNK_U4 = inf_chunk_u4<NT>();
     for (int task = t_lo + j; task < t_hi; task += per_xcd) {
         const int tq = task / ksplit, kp = task % ksplit;
         const int ng = tq / n_mb, mb = tq % n_mb;
         int c_lo, c_hi;
-        chunk_range(task, c_lo, c_hi);
-        const half8 *fh = whi + (int64_t)ng * INF_NW * g.ksteps * 64;
-        const half8 *fl = wlo + (int64_t)ng * INF_NW * g.ksteps * 64;
+        chunk_range(task, KC, c_lo, c_hi);
+        const uint4 *fg = frag + (int64_t)ng * INF_NW * g.ksteps * NT_MAX * 64;
         // chunk ch -> buffer: wave w issues the 64-lane groups w, w+8, ... (16 bytes per lane)
         auto fill = [&](int ch) {
-            uint4 *dst = cbuf + (ch & 1) * INF_CHUNK_U4;
-            const int k0 = ch * INF_KC, nk = min(INF_KC, g.ksteps - k0);
-            for (int grp = wv; grp < nk * INF_NW * 2; grp += INF_WAVES) {
-                const int h = grp & 1, n = (grp >> 1) % INF_NW, ksl = (grp >> 1) / INF_NW;
-                const half8 *src = (h ? fl : fh) + ((int64_t)n * g.ksteps + k0 + ksl) * 64 + lane;
+            uint4 *dst = cbuf + (ch & 1) * CHUNK_U4;
+            const int k0 = ch * KC, nk = min(KC, g.ksteps - k0);
+            for (int grp = wv; grp < nk * INF_NW * NT; grp += INF_WAVES) {
+                const int q = grp % NT, n = (grp / NT) % INF_NW, ksl = grp / (NT * INF_NW);
+                const uint4 *src = fg + (((int64_t)n * g.ksteps + k0 + ksl) * NT_MAX + q) * 64 + lane;
                 __builtin_amdgcn_global_load_lds(src, dst + grp * 64, 16, 0, 0);
             }
         };
@@ -891,16 +1081,16 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             for (int n = 0; n < INF_NW; ++n) acc[i][n] = f4{0.f, 0.f, 0.f, 0.f};
         // the spike words of a chunk are loaded with its fill, one chunk ahead; two
         // register sets, the loop unrolled by two chunks so that both are static
-        uint32_t aw0[INF_KC][INF_MW][2], aw1[INF_KC][INF_MW][2];
+        uint32_t aw0[KC][INF_MW][2], aw1[KC][INF_MW][2];
         // With CP a multiple of 64 a cell has an even number of K-steps and K-steps
         // 2m, 2m+1 of it are 16 consecutive, aligned bytes of a lane's run; with
         // CP >= 8 a K-step's two words are adjacent; with CP == 4 separate cells.
         const int wide = g.CP % 64 == 0 ? 2 : (g.CP >= 8 ? 1 : 0);
-        auto load_aw = [&](int ch, uint32_t (&dst)[INF_KC][INF_MW][2]) {
+        auto load_aw = [&](int ch, uint32_t (&dst)[KC][INF_MW][2]) {
             if (wide == 2) {
 #pragma unroll
-                for (int kl = 0; kl < INF_KC; kl += 2) {
-                    const int2 o = koff_l[min(ch * INF_KC + kl, g.ksteps - 2) * 4 + gq];
+                for (int kl = 0; kl < KC; kl += 2) {
+                    const int2 o = koff_l[min(ch * KC + kl, g.ksteps - 2) * 4 + gq];
 #pragma unroll
                     for (int i = 0; i < INF_MW; ++i) {
                         const uint4 v = *reinterpret_cast<const uint4 *>(abase[i] + (uint32_t)o.x);
@@ -912,8 +1102,8 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
                 }
             } else {
 #pragma unroll
-                for (int kl = 0; kl < INF_KC; ++kl) {
-                    const int2 o = koff_l[min(ch * INF_KC + kl, g.ksteps - 1) * 4 + gq];
+                for (int kl = 0; kl < KC; ++kl) {
+                    const int2 o = koff_l[min(ch * KC + kl, g.ksteps - 1) * 4 + gq];
 #pragma unroll
                     for (int i = 0; i < INF_MW; ++i) {
                         if (wide == 1) {
@@ -928,25 +1118,24 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
                 }
             }
         };
-        auto chunk = [&](int ch, const uint32_t (&awc)[INF_KC][INF_MW][2], uint32_t (&awn)[INF_KC][INF_MW][2]) {
-            const int nk = min(INF_KC, g.ksteps - ch * INF_KC);
+        auto chunk = [&](int ch, const uint32_t (&awc)[KC][INF_MW][2], uint32_t (&awn)[KC][INF_MW][2]) {
+            const int nk = min(KC, g.ksteps - ch * KC);
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's words and fill of chunk ch landed
             __syncthreads();  // every wave's part of chunk ch is in LDS; chunk ch-1's buffer is free
             if (ch + 1 < c_hi) {
                 load_aw(ch + 1, awn);
                 fill(ch + 1);
             }
-            const uint4 *fr = cbuf + (ch & 1) * INF_CHUNK_U4 + lane;
+            const uint4 *fr = cbuf + (ch & 1) * CHUNK_U4 + lane;
 #pragma unroll
-            for (int kl = 0; kl < INF_KC; ++kl) {
+            for (int kl = 0; kl < KC; ++kl) {
                 if (kl >= nk) break;  // uniform
-                half8 bh[INF_NW], bl[INF_NW];
+                uint4 bt[NT][INF_NW];
 #pragma unroll
-                for (int n = 0; n < INF_NW; ++n) {
-                    bh[n] = __builtin_bit_cast(half8, fr[((kl * INF_NW + n) * 2) * 64]);
-                    bl[n] = __builtin_bit_cast(half8, fr[((kl * INF_NW + n) * 2 + 1) * 64]);
-                }
-                half8 a[INF_MW];
+                for (int n = 0; n < INF_NW; ++n)
+#pragma unroll
+                    for (int q = 0; q < NT; ++q) bt[q][n] = fr[((kl * INF_NW + n) * NT + q) * 64];
+                u4 a[INF_MW];
 #pragma unroll
                 for (int i = 0; i < INF_MW; ++i) {
                     uint32_t xn[4];
@@ -955,13 +1144,11 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
                     a[i] = spike_operand(xn, ct);
                 }
 #pragma unroll
-                for (int i = 0; i < INF_MW; ++i)
+                for (int q = 0; q < NT; ++q)
 #pragma unroll
-                    for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma(a[i], bh[n], acc[i][n]);
+                    for (int i = 0; i < INF_MW; ++i)
 #pragma unroll
-                for (int i = 0; i < INF_MW; ++i)
-#pragma unroll
-                    for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma(a[i], bl[n], acc[i][n]);
+                        for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma<NT>(a[i], bt[q][n], acc[i][n]);
             }
         };
         __syncthreads();  // the buffers are free (previous task done), koff is visible
@@ -1014,6 +1201,11 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
                 }
             }
     }
+    };
+    if (n_terms == 3)
+        mfma_waves(std::integral_constant<int, 3>{});
+    else
+        mfma_waves(std::integral_constant<int, 2>{});
 }
 
 // Zero potentials (f32) and spikes (u8) of steps 0..T-2 of every image: per
@@ -1071,6 +1263,7 @@ struct ConvPlan {
     ConvGeom g;
     size_t tpad_bytes, frag_count, koff_count;
     int ksplit;         // K parts of the Eq.5 kernel (1: not split)
+    int kpp;            // K-steps per part (a multiple of INF_KPART when split)
     size_t part_count;  // floats of its partial sums
 };
 
@@ -1108,18 +1301,19 @@ int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, Con
     g.mt_per_img = (g.HoWo + 15) / 16;
     g.total_mtiles = (int64_t)B * g.mt_per_img;
     pl.tpad_bytes = (size_t)B * g.Hp * g.Wp * g.CP;
-    pl.frag_count = (size_t)g.ntiles * g.ksteps * 64;
+    pl.frag_count = (size_t)g.ntiles * g.ksteps * NT_MAX * 64;
     pl.koff_count = (size_t)g.ksteps * 4;
     // Eq.5 mode on few tasks (a small batch): the K chunks are split into parts
     // run by separate workgroups, so that more than a handful of CUs work; the
     // partial sums take at most INF_PART_MAX floats.
     const int64_t n_mb = spk::ceil_div(g.total_mtiles, INF_WAVES * INF_MW);
     const int64_t n_ng = spk::ceil_div(spk::ceil_div(Cout, 16), INF_NW);
-    const int64_t nch = spk::ceil_div(g.ksteps, INF_KC), outs = (int64_t)B * Cout * g.HoWo;
+    const int64_t nch = spk::ceil_div(g.ksteps, INF_KPART), outs = (int64_t)B * Cout * g.HoWo;
     int64_t ks = n_mb * n_ng > 0 && n_mb * n_ng < 128 ? std::min<int64_t>(nch, spk::ceil_div(256, n_mb * n_ng)) : 1;
     if (outs > 0) ks = std::min<int64_t>(ks, INF_PART_MAX / outs);
-    if (ks >= 2) ks = spk::ceil_div(nch, spk::ceil_div(nch, ks));  // no part without chunks
+    if (ks >= 2) ks = spk::ceil_div(nch, spk::ceil_div(nch, ks));  // no part without K-steps
     pl.ksplit = ks >= 2 ? (int)ks : 1;
+    pl.kpp = pl.ksplit > 1 ? (int)spk::ceil_div(nch, pl.ksplit) * INF_KPART : g.ksteps;
     pl.part_count = pl.ksplit > 1 ? (size_t)(pl.ksplit * outs) : 0;
     return SPK_OK;
 }
@@ -1127,11 +1321,12 @@ int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, Con
 size_t plan_workspace(const ConvPlan &pl) {
     spk::Carver c(nullptr);
     c.take<uint8_t>(pl.tpad_bytes);
-    c.take<half8>(pl.frag_count);
-    c.take<half8>(pl.frag_count);
+    c.take<uint4>(pl.frag_count);
     c.take<int2>(pl.koff_count);
     c.take<float>(1);                // 1/scale
-    c.take<unsigned>(WMAX_PARTS);    // weight-maximum partials
+    c.take<int>(1);                  // weight terms
+    c.take<unsigned>(WMAX_PARTS);    // weight-range partials: maxima
+    c.take<unsigned>(WMAX_PARTS);    //                        non-zero minima
     c.take<float>(pl.part_count);    // Eq.5 split sums
     return spk::align_up(c.off, 256);
 }
@@ -1144,31 +1339,31 @@ int max_lds_per_block() {
 }
 
 template <int G, bool BLDS, bool ALDS>
-void launch_fin(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, const float *inv_scale,
-                const float *wts, const unsigned *wmax, int n_wmax, const ConvGeom &g, int n_pairs, int n_chunks,
-                int cpi, int chunk_tiles, int np_max, int a_words, size_t lds, float *P, uint8_t *S, uint8_t *TF,
-                float *VF, hipStream_t st) {
+void launch_fin(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const float *inv_scale, const int *nterms,
+                const float *wts, const unsigned *wmax, const unsigned *wmin, int n_wmax, const ConvGeom &g,
+                int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words, size_t lds, float *P,
+                uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
     // one workgroup per CU: a multiple of the feature pairs on every XCD
     const int per_xcd = (int)spk::ceil_div(std::max(32, n_pairs), n_pairs) * n_pairs;
     hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
-                       tpad, whi, wlo, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, wts,
-                       wmax, n_wmax, P, S, TF, VF);
+                       tpad, frag, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, nterms,
+                       wts, wmax, wmin, n_wmax, P, S, TF, VF);
 }
 
 template <bool VEC>
-void launch_inf(const uint8_t *tpad, const half8 *whi, const half8 *wlo, const int2 *koff2, const float *inv_scale,
-                const ConvGeom &g, int ksplit, float *part, float *P, uint8_t *S, uint8_t *TF, float *VF,
+void launch_inf(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const float *inv_scale, const int *nterms,
+                const ConvGeom &g, int ksplit, int kpp, float *part, float *P, uint8_t *S, uint8_t *TF, float *VF,
                 hipStream_t st) {
     const int n_mb = (int)spk::ceil_div(g.total_mtiles, INF_WAVES * INF_MW);
     const int n_ng = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), INF_NW);
-    const size_t lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16) + 2 * (size_t)INF_CHUNK_U4 * 16;
+    const size_t lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16) + 2 * (size_t)INF_CHUNK_U4_MAX * 16;
     if (!VEC && g.T > 1 && (P || S)) {  // (with VEC the conv kernel's zero waves write them)
         const int64_t n = (int64_t)(g.T - 1) * g.Cout * g.HoWo;
         const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>(64, spk::ceil_div(n, 256 * 16)));
         hipLaunchKernelGGL(k_zero_planes, dim3(gx, (unsigned)std::min(g.B, 65535)), dim3(256), 0, st, g, P, S);
     }
-    hipLaunchKernelGGL((k_conv_fire_inf<VEC>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad, whi, wlo,
-                       koff2, g, n_mb, n_ng, ksplit, part, inv_scale, P, S, TF, VF);
+    hipLaunchKernelGGL((k_conv_fire_inf<VEC>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad, frag,
+                       koff2, g, n_mb, n_ng, ksplit, kpp, part, inv_scale, nterms, P, S, TF, VF);
     if (ksplit > 1) {
         const int64_t n = (int64_t)g.B * g.Cout * g.HoWo;
         hipLaunchKernelGGL(k_inf_reduce, dim3((unsigned)spk::ceil_div(n, 256)), dim3(256), 0, st, part, ksplit, g,
@@ -1206,11 +1401,12 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
 
     spk::Carver cv(workspace);
     uint8_t *tpad = cv.take<uint8_t>(pl.tpad_bytes);
-    half8 *whi = cv.take<half8>(pl.frag_count);
-    half8 *wlo = cv.take<half8>(pl.frag_count);
+    uint4 *frag = cv.take<uint4>(pl.frag_count);
     int2 *koff2 = cv.take<int2>(pl.koff_count);
     float *inv_scale = cv.take<float>(1);
+    int *nterms = cv.take<int>(1);
     unsigned *wmax = cv.take<unsigned>(WMAX_PARTS);
+    unsigned *wmin = cv.take<unsigned>(WMAX_PARTS);
     float *part = cv.take<float>(pl.part_count);
     hipStream_t st = spk::as_stream(stream);
 
@@ -1242,7 +1438,7 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     const int np_max = chunk_tiles * 16;
     const size_t koff_lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16);
     const size_t stage_lds = (size_t)FIN_TB * 32 * stage_stride(np_max) * sizeof(float);
-    const size_t frag_lds = (size_t)g.ksteps * 4 * 64 * 16;
+    const size_t frag_lds = (size_t)g.ksteps * 2 * NT_MAX * 64 * 16;
     const size_t lds_limit = (size_t)max_lds_per_block();
     // spike rows of the largest task, staged in LDS (double-buffered) when small enough
     // (the row count of a chunk depends on its first position modulo HoWo, which repeats
@@ -1271,7 +1467,7 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     const bool alds = g.CP >= 8 && koff_lds + stage_lds + a_lds <= lds_limit;
     const bool blds = koff_lds + frag_lds + stage_lds + (alds ? a_lds : 0) <= lds_limit;
     const size_t fin_lds = koff_lds + (blds ? frag_lds : 0) + stage_lds + (alds ? a_lds : 0);
-    const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4 * 16;
+    const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4_MAX * 16;
     SPK_REQUIRE(!inf_mode || inf_lds <= lds_limit, SPK_E_RANGE,
                 "spk_conv_fire: needs %zu bytes of LDS per workgroup, the device has %zu", inf_lds, lds_limit);
     SPK_REQUIRE(inf_mode || fin_lds <= lds_limit, SPK_E_RANGE,
@@ -1288,26 +1484,26 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     const dim3 pad_grid((unsigned)((int64_t)nchunk * ny + n_wmax));
     if (times)
         hipLaunchKernelGGL(k_pad_first_spike<true>, pad_grid, dim3(256), pad_lds, st, wave, g, rows_per_chunk, nchunk, ny,
-                           tpad, weight, nw, wper, wmax);
+                           tpad, weight, nw, wper, wmax, wmin);
     else
         hipLaunchKernelGGL(k_pad_first_spike<false>, pad_grid, dim3(256), pad_lds, st, wave, g, rows_per_chunk, nchunk, ny,
-                           tpad, weight, nw, wper, wmax);
+                           tpad, weight, nw, wper, wmax, wmin);
     if (inf_mode || !blds) {  // fragments in the workspace (the finite-threshold kernel with LDS room builds its own)
         const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
         hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, wmax,
-                           n_wmax, whi, wlo, koff2, inv_scale);
+                           wmin, n_wmax, frag, koff2, inv_scale, nterms);
     }
     if (inf_mode) {
         if (vec)
-            launch_inf<true>(tpad, whi, wlo, koff2, inv_scale, g, pl.ksplit, part, potentials, spikes, t_first,
-                             v_first, st);
+            launch_inf<true>(tpad, frag, koff2, inv_scale, nterms, g, pl.ksplit, pl.kpp, part, potentials, spikes,
+                             t_first, v_first, st);
         else
-            launch_inf<false>(tpad, whi, wlo, koff2, inv_scale, g, pl.ksplit, part, potentials, spikes, t_first,
-                              v_first, st);
+            launch_inf<false>(tpad, frag, koff2, inv_scale, nterms, g, pl.ksplit, pl.kpp, part, potentials, spikes,
+                              t_first, v_first, st);
     } else {
 #define SPK_FIN(G, BL, AL)                                                                                    \
-    launch_fin<G, BL, AL>(tpad, whi, wlo, koff2, inv_scale, weight, wmax, n_wmax, g, n_pairs, n_chunks, cpi, \
-                          chunk_tiles, np_max, a_words, fin_lds, potentials, spikes, t_first, v_first, st)
+    launch_fin<G, BL, AL>(tpad, frag, koff2, inv_scale, nterms, weight, wmax, wmin, n_wmax, g, n_pairs, n_chunks, \
+                          cpi, chunk_tiles, np_max, a_words, fin_lds, potentials, spikes, t_first, v_first, st)
         const int sel = (vec ? 4 : 0) + (blds ? 2 : 0) + (alds ? 1 : 0);
         switch (sel) {
             case 0: SPK_FIN(1, false, false); break;

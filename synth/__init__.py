@@ -134,6 +134,14 @@ def dyadic_weights(g: np.random.Generator, shape, taps: int) -> np.ndarray:
     return (m.astype(np.float64) / (1 << f)).astype(np.float32)
 
 
+def loguniform_weights(g: np.random.Generator, shape, decades: float, p_zero: float = 0.0) -> np.ndarray:
+    """Weights 10^U(-decades, 0), i.e. spread evenly over `decades` orders of
+    magnitude below 1, with a fraction p_zero of exact zeros."""
+    w = np.power(10.0, g.uniform(-decades, 0.0, size=shape))
+    w[g.random(size=shape) < p_zero] = 0.0
+    return w.astype(np.float32)
+
+
 def labels(g: np.random.Generator, B: int, n_classes: int = 10) -> np.ndarray:
     return g.integers(0, n_classes, size=B).astype(np.int32)
 

@@ -1,3 +1,4 @@
+import json
 import os
 import sys
 
@@ -29,3 +30,29 @@ def load_golden(name):
 @pytest.fixture
 def golden():
     return load_golden
+
+
+# Neurons and images the parity rules exclude (near-threshold neurons,
+# ambiguous chained images), gathered per test and written at the end of the
+# session to $SPK_PARITY_SUMMARY (default gpurun_out/parity_exclusions.json).
+_EXCLUSIONS = []
+
+
+@pytest.fixture
+def near_log(request):
+    def log(what, excluded, total):
+        _EXCLUSIONS.append({"test": request.node.nodeid, "what": what, "excluded": int(excluded),
+                            "total": int(total)})
+        print(f"{what}: {int(excluded)} of {int(total)} excluded", flush=True)
+    return log
+
+
+def pytest_sessionfinish(session, exitstatus):
+    if not _EXCLUSIONS:
+        return
+    path = os.environ.get("SPK_PARITY_SUMMARY", os.path.join(ROOT, "gpurun_out", "parity_exclusions.json"))
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    summary = {"cases": len(_EXCLUSIONS), "excluded": sum(e["excluded"] for e in _EXCLUSIONS),
+               "total": sum(e["total"] for e in _EXCLUSIONS), "records": _EXCLUSIONS}
+    with open(path, "w") as f:
+        json.dump(summary, f, indent=1)
