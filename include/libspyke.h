@@ -166,6 +166,20 @@ SPK_API int spk_conv_fire_first_spike(const uint8_t *in_t_first, int B, int T, i
              float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
              void *workspace, size_t ws_bytes, void *stream);
 
+/* The same call for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * no workspace argument, the scratch is a static device array of
+ * 64 MiB per GPU inside the library, held until the process ends, and the
+ * call allocates nothing.  A call whose spk_conv_fire_workspace_size()
+ * exceeds 64 MiB returns SPK_E_RANGE with nothing launched.  Every call on
+ * one GPU shares that GPU's scratch: calls that overlap in time on one GPU
+ * (concurrent streams, or threads) race and must be serialised by the
+ * caller.  Arguments, outputs and errors otherwise as
+ * spk_conv_fire_first_spike.                                                */
+SPK_API int spk_conv_fire_first_spike_noalloc(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+             const float *weight, int Cout, int K, int pad, float threshold,
+             float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first, void *stream);
+
 /* ------------------------------------------------------------------------
  * Spike max-pooling (section "snn Module", Eq.3): on a spike wave each
  * window yields its earliest spike.  Window `kernel`, stride `stride`,

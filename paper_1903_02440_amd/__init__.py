@@ -46,6 +46,7 @@ _SIGS = {
     "spk_conv_fire_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I]),
     "spk_conv_fire": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z, _P]),
     "spk_conv_fire_first_spike": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z, _P]),
+    "spk_conv_fire_first_spike_noalloc": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _F, _P, _P, _P, _P, _P]),
     "spk_pool": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
     "spk_pool_first_spike": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
     "spk_pool_potentials": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
@@ -251,6 +252,27 @@ def spk_conv_fire_first_spike(in_t_first, T, weight, pad, threshold, potentials=
     _check(_lib.spk_conv_fire_first_spike(_ptr(in_t_first), B, T, Cin, H, W, _ptr(weight), Cout, K, pad,
                                           float(threshold), _ptr(potentials), _ptr(spikes), _ptr(t_first),
                                           _ptr(v_first), _ptr(ws), n, _stream(stream)))
+    return potentials, spikes, t_first, v_first
+
+
+def spk_conv_fire_first_spike_noalloc(in_t_first, T, weight, pad, threshold, potentials=None, spikes=None,
+                                      t_first=None, v_first=None, stream=None):
+    """As spk_conv_fire_first_spike, with the library's static device scratch
+    instead of a workspace (the C call allocates nothing; calls on one GPU must
+    not overlap)."""
+    B, Cin, H, W = in_t_first.shape
+    Cout, Cin2, K, _ = weight.shape
+    _need(in_t_first, torch.uint8, (B, Cin, H, W), "in_t_first")
+    _need(weight, torch.float32, (Cout, Cin, K, K), "weight")
+    Ho, Wo = conv_out_size(H, K, pad), conv_out_size(W, K, pad)
+    dev = in_t_first.device
+    potentials = _out(potentials, (B, T, Cout, Ho, Wo), torch.float32, dev, "potentials")
+    spikes = _out(spikes, (B, T, Cout, Ho, Wo), torch.uint8, dev, "spikes")
+    t_first = _out(t_first, (B, Cout, Ho, Wo), torch.uint8, dev, "t_first")
+    v_first = _out(v_first, (B, Cout, Ho, Wo), torch.float32, dev, "v_first")
+    _check(_lib.spk_conv_fire_first_spike_noalloc(_ptr(in_t_first), B, T, Cin, H, W, _ptr(weight), Cout, K, pad,
+                                                  float(threshold), _ptr(potentials), _ptr(spikes), _ptr(t_first),
+                                                  _ptr(v_first), _stream(stream)))
     return potentials, spikes, t_first, v_first
 
 

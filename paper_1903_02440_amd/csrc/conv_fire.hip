@@ -45,6 +45,7 @@
 //      k_conv_fire_inf, which computes only the last step.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <numeric>
 #include <type_traits>
 
@@ -1534,4 +1535,59 @@ extern "C" int spk_conv_fire_first_spike(const uint8_t *in_t_first, int B, int T
                                          void *workspace, size_t ws_bytes, void *stream) {
     return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, pad, threshold, potentials, spikes,
                      t_first, v_first, workspace, ws_bytes, stream);
+}
+
+// ------------------------------------------------------------------ allocation-free variant
+// The workspace of spk_conv_fire_first_spike_noalloc: a static device array,
+// one copy per GPU, held until the process ends.  In host code `scratch` is
+// only a stand-in for the symbol: its device address, per device, comes from
+// hipGetSymbolAddress and is what the kernels receive.  Nothing in the conv
+// workspace needs to start at zero (every byte a kernel reads was written
+// earlier in the same call), so calls do not clear it.
+constexpr size_t SPK_NOALLOC_SCRATCH_BYTES = size_t(64) << 20;
+static __device__ __align__(256) uint8_t scratch[SPK_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int SPK_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[SPK_MAX_DEVICES] = {};
+
+// Device address of the current device's scratch (looked up once per device).
+int current_scratch(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SPK_MAX_DEVICES)
+        return spk::fail(SPK_E_HIP, "spk_conv_fire_first_spike_noalloc: no usable current device (%d)", dev);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return spk::fail(SPK_E_HIP, "spk_conv_fire_first_spike_noalloc: hipGetSymbolAddress failed on device %d: %s",
+                             dev, hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return SPK_OK;
+}
+}  // namespace
+
+extern "C" int spk_conv_fire_first_spike_noalloc(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+                                                 const float *weight, int Cout, int K, int pad, float threshold,
+                                                 float *potentials, uint8_t *spikes, uint8_t *t_first,
+                                                 float *v_first, void *stream) {
+    ConvPlan pl;
+    int rc = make_plan(B, T, Cin, H, W, Cout, K, pad, pl);
+    if (rc != SPK_OK) return rc;
+    const size_t need = plan_workspace(pl);
+    SPK_REQUIRE(need <= SPK_NOALLOC_SCRATCH_BYTES, SPK_E_RANGE,
+                "spk_conv_fire_first_spike_noalloc: the call needs %zu bytes of scratch, the static scratch holds %zu "
+                "(use spk_conv_fire_first_spike with a workspace)",
+                need, SPK_NOALLOC_SCRATCH_BYTES);
+    if (B == 0) return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, pad, threshold, potentials,
+                                 spikes, t_first, v_first, nullptr, 0, stream);
+    void *ws = nullptr;
+    rc = current_scratch(&ws);
+    if (rc != SPK_OK) return rc;
+    return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, pad, threshold, potentials, spikes, t_first,
+                     v_first, ws, SPK_NOALLOC_SCRATCH_BYTES, stream);
 }

@@ -22,7 +22,7 @@ def declared():
 
 def test_every_declared_symbol_is_exported():
     names = declared()
-    assert len(names) == 23
+    assert len(names) == 24
     lib = spk.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -135,3 +135,13 @@ def test_variant_op_validation_errors():
     assert lib.spk_rank_latency(DUMMY, 2, 6, 28, 28, 15, DUMMY, DUMMY, DUMMY, n - 1, None) == spk.SPK_E_WORKSPACE
     assert lib.spk_rank_latency(DUMMY, 2, 6, 28, 28, 15, None, None, DUMMY, n, None) == spk.SPK_E_ARG
     assert lib.spk_rank_latency(DUMMY, 2, 6, 28, 28, 256, DUMMY, None, DUMMY, n, None) == spk.SPK_E_RANGE
+
+
+def test_conv_noalloc_rejects_beyond_its_scratch():
+    # host-side size check before any HIP call: the large stress layer's padded input exceeds 64 MiB
+    lib = spk.lib()
+    rc = lib.spk_conv_fire_first_spike_noalloc(DUMMY, 16, 64, 64, 256, 256, DUMMY2, 256, 5, 2, ctypes.c_float(40.0),
+                                               None, None, DUMMY, DUMMY2, None)
+    assert rc == spk.SPK_E_RANGE and b"static scratch" in lib.spk_last_error()
+    assert spk.spk_conv_fire_workspace_size(16, 64, 64, 256, 256, 256, 5, 2) > (64 << 20)
+    assert spk.spk_conv_fire_workspace_size(1000, 15, 30, 14, 14, 250, 3, 1) <= (64 << 20)
