@@ -84,12 +84,34 @@ CONV_CASES = [
     ("tiny", 1, 1, 1, 1, 1, 1, 1, 0, 0.5, 0.3),
     ("inf-small", 3, 4, 2, 6, 6, 5, 3, 1, math.inf, 0.5),
     ("K1", 2, 5, 7, 3, 5, 33, 1, 0, 2.0, 0.3),
-    # 9 and 13 position tiles per image: the last tile's feature halves go to two waves
-    ("tiles9-split", 3, 9, 12, 12, 12, 24, 3, 1, 4.0, 0.4),
-    ("tiles13-split", 3, 15, 16, 14, 14, 20, 3, 1, 6.0, 0.5),
+    # 9 and 13 position tiles per image, enough of them for whole-image tasks (8
+    # feature pairs): the last tile's feature halves go to two waves
+    ("tiles9-split", 57, 9, 12, 12, 12, 256, 3, 1, 4.0, 0.4),
+    ("tiles13-split", 40, 15, 16, 14, 14, 256, 3, 1, 6.0, 0.5),
     # Eq.5 on few tasks: the K chunks split over workgroups, two chunks per part
     ("inf-ksplit", 112, 15, 64, 12, 12, 8, 5, 2, math.inf, 0.6),
 ]
+
+
+def fin_task_form(B, Cout, Ho, Wo):
+    """How the finite-threshold conv call cuts its work (a restatement of the
+    host plan): ("image", split) when each task is one whole image, split being
+    whether the last tile's feature halves go to two waves; ("chunks", False)
+    for chunks of the flattened position space."""
+    mt = -(-Ho * Wo // 16)
+    n_pairs = -(-(-(-Cout // 16)) // 2)
+    ct = 16 if (Ho * Wo) % 4 == 0 else 8
+    while ct > 4 and n_pairs * B * mt // ct < 256:
+        ct //= 2
+    if mt > ct:
+        return ("chunks", False)
+    return ("image", (mt & 3) == 1 and mt > 8 and ct == 16)
+
+
+def test_split_cases_take_the_whole_image_split():
+    for name in ("tiles9-split", "tiles13-split"):
+        _, B, T, Cin, H, W, Cout, K, pad, thr, ps = next(c for c in CONV_CASES if c[0] == name)
+        assert fin_task_form(B, Cout, H + 2 * pad - K + 1, W + 2 * pad - K + 1) == ("image", True), name
 
 
 @pytest.mark.parametrize("case", CONV_CASES, ids=[c[0] for c in CONV_CASES])
@@ -211,6 +233,20 @@ def test_conv_fire_unaligned_wave():
     ref = orc.conv_fire(wave, Wt, pad, 15.0)
     for x, r, name in zip(out, ref, ("P", "S", "t_first", "v_first")):
         assert_equal(host(x), r, name)
+
+
+# ---------------------------------------------------------------- synaptic events
+@pytest.mark.parametrize("case", [(3, 15, 6, 28, 28, 30, 5, 2), (5, 15, 30, 14, 14, 250, 3, 1),
+                                  (7, 15, 250, 4, 4, 200, 5, 2), (2, 30, 4, 26, 41, 20, 17, 0),
+                                  (3, 7, 3, 5, 9, 17, 3, 1), (1, 4, 2, 3, 3, 1, 3, 0), (13, 9, 5, 7, 7, 11, 3, 2)])
+def test_count_events_parity(case):
+    # batch * output positions not a multiple of 64 in the last cases (the reduction's tail), padding in most
+    B, T, Cin, H, W, Cout, K, pad = case
+    g = synth.rng(140 + H + Cin, 0)
+    tf = synth.times_uniform_or_silent(g, (B, Cin, H, W), T, 0.6)
+    count = spk.spk_count_events(dev(wave_of(tf, T)), Cout, K, pad)
+    sync()
+    assert int(count.item()) == orc.count_events(tf, T, Cout, K, pad)
 
 
 # ---------------------------------------------------------------- pool
