@@ -71,6 +71,14 @@ def step_bytes(wl, compact=False):
     return out
 
 
+# what each timed call launches (the roofline's kernel)
+CALL_KERNELS = {
+    "conv": "spk_conv_fire: padding launch + MFMA conv-fire launch",
+    "enco": "spk_encode_latency: filter, rank-order bins, Eq.1 wave",
+    "kwta": "spk_kwta",
+    "pool": "spk_pool_first_spike",
+}
+
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_fire_S2_mnist3layer_traffic.md")
 CONV_SRC = os.path.join(ROOT, "paper_1903_02440_amd", "csrc", "conv_fire.hip")
 
@@ -92,41 +100,89 @@ def read_traffic(workload, call):
     return int(kv["traffic_bytes_per_call"])
 
 
-def cpu_baseline(wl, inp, budget_s):
-    """The oracle, untuned, single-threaded, on the first images of the batch
-    until about budget_s seconds of work: forward of every layer, then the
-    plasticity replay of those images."""
+def _oracle_forward_images(args):
+    """Oracle forward of the images idx (a worker of the multi-process figure)."""
+    wl, inp, idx = args
+    from oracle import chain as ochain
+    r, _, dec = ochain.forward(wl, inp, inp["weights"], idx)
+    keep = [{k: v for k, v in d.items() if k in ("pre_wave", "win", "nw")} for d in r]
+    return keep, dec
+
+
+def _oracle_learn(wl, inp, parts, n):
+    """The ordered plasticity replay of the first n images from forward parts."""
+    import copy
     import numpy as np
     from oracle import chain as ochain
-    n, t_used = 0, 0.0
-    chunk = 8
-    res_parts = []
-    t0 = time.perf_counter()
-    while n < wl.B and (time.perf_counter() - t0) < budget_s * 0.8:
-        idx = np.arange(n, min(wl.B, n + chunk))
-        r, _, dec = ochain.forward(wl, inp, inp["weights"], idx)
-        res_parts.append((r, dec))
-        n += len(idx)
-    # plasticity of the sampled images, in order
-    import copy
     sub = copy.copy(wl)
     sub.B = n
     res = []
     for si in range(len(wl.stages)):
         d = {}
         for k in ("pre_wave", "win", "nw"):
-            vals = [p[0][si][k] for p in res_parts if k in p[0][si]]
+            vals = [p[0][si][k] for p in parts if k in p[0][si]]
             if vals:
                 d[k] = np.concatenate(vals)
         res.append(d)
     dec = None
-    if res_parts[0][1] is not None:
-        dec = (np.concatenate([p[1][0] for p in res_parts]), np.concatenate([p[1][1] for p in res_parts]))
+    if parts[0][1] is not None:
+        dec = (np.concatenate([p[1][0] for p in parts]), np.concatenate([p[1][1] for p in parts]))
     ochain.learn(sub, res, inp["weights"], dec)
-    t_used = time.perf_counter() - t0
-    return {"value": round(n / t_used, 3), "unit": "images/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {n} of the {wl.B} images of the batch: encode + all layers + plasticity, "
-                      f"single-threaded C oracle, {t_used:.1f} s"}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, inp, budget_s):
+    """The oracle, untuned and single-threaded, on the first images of the batch,
+    one image per call until about budget_s seconds of work (at least one
+    image): forward of every layer, then the plasticity replay of those images.
+    Beside it, the same oracle run as N forked processes over consecutive images
+    (forward), then the replay on one core."""
+    import numpy as np
+    n = 0
+    parts = []
+    t0 = time.perf_counter()
+    while n < wl.B and (n == 0 or (time.perf_counter() - t0) < budget_s * 0.8):
+        c = 1 if n == 0 else min(8, wl.B - n)  # one image first: a large one alone can fill the budget
+        parts.append(_oracle_forward_images((wl, inp, np.arange(n, n + c))))
+        n += c
+    _oracle_learn(wl, inp, parts, n)
+    t1 = time.perf_counter() - t0
+    rec = {"value": round(n / t1, 3), "unit": "images/s", "cores": 1, "kind": "oracle",
+           "cpu_model": cpu_model(),
+           "sample": f"first {n} of the {wl.B} images of the batch: encode + every layer + "
+                     f"plasticity replay, single-threaded C oracle, {t1:.1f} s"}
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    cores = max(1, min(16, cores))
+    # each process holds one image's per-step potentials and spikes of the largest layer: keep to ~64 GB
+    per_img = max(st.cout * wl.T * (wl.H + 2 * st.pad) * (wl.W + 2 * st.pad) * 5 for st in wl.stages
+                  if hasattr(st, "cout")) * 3 // 2 + wl.T * wl.cin * wl.H * wl.W
+    cores = max(1, min(cores, int(64e9 // max(1, per_img))))
+    if cores > 1 and wl.B > 1:
+        import multiprocessing as mp
+        per = max(1, int(round(n / t1 * budget_s * 0.8)))  # images per process for about budget_s
+        m = min(wl.B, per * cores)
+        chunks = [c for c in np.array_split(np.arange(m), cores) if len(c)]
+        t0 = time.perf_counter()
+        with mp.get_context("fork").Pool(len(chunks)) as pool:
+            pparts = pool.map(_oracle_forward_images, [(wl, inp, c) for c in chunks])
+        _oracle_learn(wl, inp, pparts, m)
+        t2 = time.perf_counter() - t0
+        rec["parallel"] = {"value": round(m / t2, 3), "unit": "images/s", "cores": len(chunks),
+                           "sample": f"first {m} of the {wl.B} images, forward split over {len(chunks)} forked "
+                                     f"oracle processes, then the plasticity replay on one core, {t2:.1f} s"}
+    return rec
 
 
 def copy_probe(nbytes):
@@ -281,8 +337,8 @@ def main():
     torch.cuda.synchronize()
 
     nbytes = step_bytes(wl, args.compact)
-    convs = [k for k in nbytes if k.startswith("conv")]
-    dominant = max(convs, key=lambda k: nbytes[k])
+    # the call with the most algorithmic bytes among those timed one by one
+    dominant = max((k for k in nbytes if not k.startswith("stdp")), key=lambda k: nbytes[k])
 
     for _ in range(args.warmup):
         ch.step()
@@ -351,8 +407,7 @@ def main():
                             else "contract: every call writes its full outputs")},
         "synaptic_events_per_s": round(ev * args.steps / elapsed, 1),
         "synaptic_events_per_step": ev,
-        "roofline": {"bound": "hbm", "kernel": f"spk_conv_fire ({dominant}: padding launch + MFMA conv-fire "
-                                               "launch, which splits the weights itself)",
+        "roofline": {"bound": "hbm", "kernel": CALL_KERNELS.get(dominant[:4], dominant) + f" ({dominant})",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes": nbytes[dominant], "avg_ms": round(dom_avg_ms, 4)},
