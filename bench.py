@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 
 # The arithmetic of the conv contraction (the rest of the path is u8 spike
 # logic and f32/f64 scalar updates)
-DTYPE = ("f32 weights as 16-bit MFMA terms (fp16 x2, or bf16 x3 when the layer's weight range needs it), "
+DTYPE = ("f32 weights as two 16-bit MFMA terms (fp16, or bf16 when the layer's weight range needs it), "
          "f32 accumulate")
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 

@@ -130,13 +130,14 @@ SPK_API int spk_validate_wave(const uint8_t *wave, int B, int T, int C, int H, i
  *   potentials f32 [B][T][Cout][Ho][Wo] or NULL:
  *              P[t,f,y,x] = sum over (ci,ky,kx) of W[f,ci,ky,kx] * S[t,ci,y+ky-pad,x+kx-pad].
  *              Computed on 16-bit matrix cores with float accumulation:
- *              each weight, scaled by a power of two, becomes a sum of
- *              16-bit terms chosen per call on the device from the layer's
- *              largest and smallest non-zero |w| -- two fp16 terms (each
- *              weight within 2^-22 of itself) when every non-zero |w| is at
- *              least 2^-15 times the largest one's power of two, else three
- *              bf16 terms that equal the weight exactly (every float weight
- *              when max|w| < 2^8).  Products with spikes are exact and the
+ *              each weight, scaled by a power of two, becomes the sum of
+ *              two 16-bit terms whose type is chosen per call on the device
+ *              from the layer's largest and smallest non-zero |w| -- fp16
+ *              (each weight within 2^-22 of itself) when every non-zero |w|
+ *              is at least 2^-15 times the largest one's power of two, else
+ *              bf16 (each weight within 2^-17 of itself, exactly when it has
+ *              at most 17 significant bits; every float weight when
+ *              max|w| < 2^8).  Products with spikes are exact and the
  *              scaling is undone exactly.  Repeated calls give the same
  *              bits; the accumulation order depends on the call's size (in
  *              Eq.5 mode a small batch's sum is split into parts added in

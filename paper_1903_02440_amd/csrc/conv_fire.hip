@@ -14,18 +14,17 @@
 // clamp((1025 + t) - (1024 + tp)), which is 1.0 exactly when tp <= t and 0
 // otherwise.  The same bits (0x3C00) read as bf16 are 2^-7, so one spike
 // operand serves both MFMA types.  The fp32 weights, scaled by a power of two,
-// become sums of 16-bit terms, chosen per call from the layer's largest and
+// become the sum of two 16-bit terms hi = r(v), lo = r(v - hi) (v - hi is
+// exact in float), the type chosen per call from the layer's largest and
 // smallest non-zero |w| (both reduced on the device):
-//   * two fp16 terms hi = fp16(v), lo = fp16(v - hi)
-//     (v_mfma_f32_16x16x32_f16) when every non-zero |w| is at least 2^-15
-//     times the largest one's power of two: each weight is then carried to
-//     within 2^-22 of itself;
-//   * otherwise three bf16 terms hi = bf16(v), mid = bf16(v - hi),
-//     lo = v - hi - mid (v_mfma_f32_16x16x32_bf16), which represent the
-//     weights exactly: bf16 has float's exponent range, and the three 8-bit
-//     significands cover float's 24 bits (every float weight when the
-//     largest |w| is below 2^8; else every |w| >= 2^-156 times the largest
-//     one's power of two).
+//   * fp16 terms (v_mfma_f32_16x16x32_f16) when every non-zero |w| is at
+//     least 2^-15 times the largest one's power of two: each weight is then
+//     carried to within 2^-22 of itself;
+//   * otherwise bf16 terms (v_mfma_f32_16x16x32_bf16): bf16 has float's
+//     exponent range, and two round-to-nearest 8-bit significands carry every
+//     weight to within 2^-17 of itself (exactly when it has at most 17
+//     significant bits), for every float weight when the largest |w| is below
+//     2^8, else every |w| >= 2^-156 times the largest one's power of two.
 // Products with a spike are exact either way; accumulation is fp32, and the
 // scale is undone exactly.
 //
@@ -37,7 +36,7 @@
 //      one MFMA are two 4-byte words of tpad.
 //      The same launch reduces |W| to per-block maxima and non-zero minima
 //      (extra workgroups).
-//   2. W -> scaled 16-bit B-operand fragments (two or three terms) and the
+//   2. W -> scaled 16-bit B-operand fragments (two terms) and the
 //      per-lane word offsets of every 8-tap group: built by the
 //      finite-threshold kernel itself when its fragments fit in LDS, else by
 //      k_split_weights into the workspace.
@@ -220,30 +219,33 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
 // ------------------------------------------------------------------ 2. weight fragments
 // Weight split of a call, from the bit patterns of the largest |w| (maxbits)
 // and the smallest non-zero |w| (minbits; 0xFFFFFFFF when all are zero).
-// With E the exponent of max|w|:
-//   * nt = 2 (fp16 hi/lo): v = w * 2^e with e = 12 - E, so the largest |v|
-//     lies in [2^12, 2^13).  For |v| >= 2^-3 both terms keep 11 significant
-//     bits (lo, if subnormal, is still within 2^-25 <= 2^-22 |v|), so
-//     |v - hi - lo| <= 2^-22 |v|.  Taken when every non-zero |w| >= 2^(E-15)
-//     and |E| <= 100.
-//   * nt = 3 (bf16 hi/mid/lo) otherwise: v = w * 2^e with e = 60 - max(E, -60),
-//     so |v| < 2^61, and for |w| >= 2^(E-156) (every float when E <= 7) every
-//     non-zero term is at least 2^-119, normal even times a spike's 2^-7;
-//     hi + mid + lo == v exactly (v - hi and v - hi - mid are exact in float
-//     and carry at most 16 and 8 significant bits).  A spike is 2^-7 as
-//     bf16, so the sums are scaled by 2^(e - 7).
+// With E the exponent of max|w|, each weight w becomes v = w * 2^e, split into
+// hi = r(v) and lo = r(v - hi), r rounding to nearest even (v - hi is exact in
+// float):
+//   * fp16 terms: e = 12 - E, so the largest |v| lies in [2^12, 2^13).  For
+//     |v| >= 2^-3 both terms keep 11 significant bits (lo, if subnormal, is
+//     still within 2^-25 <= 2^-22 |v|), so |v - hi - lo| <= 2^-22 |v|.  Taken
+//     when every non-zero |w| >= 2^(E-15) and |E| <= 100.
+//   * bf16 terms otherwise: e = 60 - max(E, -60), so |v| < 2^61.  With v in
+//     [2^m, 2^(m+1)), |v - hi| <= 2^(m-8); below 2^(m-8) v - hi has an ulp of
+//     at most 2^(m-16), so |v - hi - lo| <= 2^(m-17) <= 2^-17 |v| (and v - hi
+//     is exact at 2^(m-8)).  A v of at most 17 significant bits is carried
+//     exactly.  For |w| >= 2^(E-156) (every float when E <= 7) every non-zero
+//     term is at least 2^-119, normal even times a spike's 2^-7.  A spike is
+//     2^-7 as bf16, so the sums are scaled by 2^(e - 7).
 // inv_s undoes the scale (a power of two, exact).
 struct WSplit {
-    int nt;
+    bool bf;
     int e;
     float inv_s;
 };
 
 __device__ __forceinline__ WSplit weight_split(unsigned maxbits, unsigned minbits) {
     const int E = maxbits ? (int)((maxbits >> 23) & 255u) - 127 : 0;  // subnormal maxima count as 2^-127
-    if (E >= -100 && E <= 100 && minbits >= ((unsigned)(E - 15 + 127) << 23)) return {2, 12 - E, ldexpf(1.0f, E - 12)};
+    if (E >= -100 && E <= 100 && minbits >= ((unsigned)(E - 15 + 127) << 23))
+        return {false, 12 - E, ldexpf(1.0f, E - 12)};
     const int e = 60 - max(E, -60);
-    return {3, e, ldexpf(1.0f, 7 - e)};
+    return {true, e, ldexpf(1.0f, 7 - e)};
 }
 
 // Largest of the n maximum partials and smallest of the n minimum partials,
@@ -308,40 +310,37 @@ __device__ __forceinline__ void tap_of(const ConvGeom &g, int ks, int gq, int j,
 // Groups past the receptive field point at offset 0 (their weights are 0).
 //
 // Fragment (nt, ks, lane) holds, for feature n = nt*16 + lane%16, the 8 taps
-// k = ks*32 + 8*(lane/16) + j, j = 0..7, as s.nt 16-bit terms (each a uint4 of
+// k = ks*32 + 8*(lane/16) + j, j = 0..7, as two 16-bit terms (each a uint4 of
 // 8 fp16 or bf16 values).  w holds the weights of features n0, n0 + 1, ...
 // ([Cout - n0][Cin][K][K]).
-constexpr int NT_MAX = 3;  // fragment terms at most (storage stride)
+constexpr int NT = 2;  // 16-bit terms per weight
 
 __device__ __forceinline__ void split_fragment(const float *w, int n0, const ConvGeom &g, int nt, int ks, int lane,
-                                               const WSplit &s, uint4 (&out)[NT_MAX]) {
+                                               const WSplit &s, uint4 (&out)[NT]) {
     const int KK = g.K * g.K;
     const int n = nt * 16 + (lane & 15);
-    uint32_t t[NT_MAX][4] = {};
+    uint32_t t[NT][4] = {};
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         int kyx, ci;
         tap_of(g, ks, lane >> 4, j, kyx, ci);
         float v = 0.0f;
         if (n < g.Cout && kyx < KK && ci < g.Cin) v = ldexpf(w[((int64_t)(n - n0) * g.Cin + ci) * KK + kyx], s.e);
-        uint32_t h[NT_MAX];
-        if (s.nt == 2) {
+        uint32_t h[NT];
+        if (!s.bf) {
             const _Float16 hv = (_Float16)v;
             const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
             h[0] = __builtin_bit_cast(uint16_t, hv);
             h[1] = __builtin_bit_cast(uint16_t, (_Float16)rest);
-            h[2] = 0;
         } else {
             h[0] = bf16_bits(v);
-            const float r1 = v - __uint_as_float(h[0] << 16);  // exact, at most 16 significant bits
-            h[1] = bf16_bits(r1);
-            h[2] = bf16_bits(r1 - __uint_as_float(h[1] << 16));  // exact, at most 8 significant bits
+            h[1] = bf16_bits(v - __uint_as_float(h[0] << 16));  // v - hi exact, at most 16 significant bits
         }
 #pragma unroll
-        for (int q = 0; q < NT_MAX; ++q) t[q][j >> 1] |= h[q] << (16 * (j & 1));
+        for (int q = 0; q < NT; ++q) t[q][j >> 1] |= h[q] << (16 * (j & 1));
     }
 #pragma unroll
-    for (int q = 0; q < NT_MAX; ++q) out[q] = uint4{t[q][0], t[q][1], t[q][2], t[q][3]};
+    for (int q = 0; q < NT; ++q) out[q] = uint4{t[q][0], t[q][1], t[q][2], t[q][3]};
 }
 
 // Word offsets of the 8-tap group q (koff2 below).
@@ -361,14 +360,13 @@ __device__ __forceinline__ int2 koff_of(const ConvGeom &g, int q) {
     return o;
 }
 
-// Fragments of every 16-feature tile into the workspace, frag[nt][ks][term][64]
-// (NT_MAX terms of stride; the unused third is zero when nt == 2), the tap
-// offsets, and the split's term count and inverse scale.
+// Fragments of every 16-feature tile into the workspace, frag[nt][ks][term][64],
+// the tap offsets, and the split's term type (1: bf16) and inverse scale.
 __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__ w, ConvGeom g,
                                                        const unsigned *__restrict__ wmax,
                                                        const unsigned *__restrict__ wmin, int n_wmax,
                                                        uint4 *__restrict__ frag, int2 *__restrict__ koff2,
-                                                       float *__restrict__ inv_scale, int *__restrict__ nterms) {
+                                                       float *__restrict__ inv_scale, int *__restrict__ wbf16) {
     __shared__ unsigned red[8];
     const uint2 mm = reduce_wrange(wmax, wmin, n_wmax, red);
     const WSplit ws = weight_split(mm.x, mm.y);
@@ -376,15 +374,15 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
     const int64_t total = (int64_t)g.ntiles * g.ksteps * 64;
     if (i == 0) {
         *inv_scale = ws.inv_s;
-        *nterms = ws.nt;
+        *wbf16 = ws.bf ? 1 : 0;
     }
     if (i < total) {
         const int lane = (int)(i & 63);
         const int64_t r = i >> 6;
-        uint4 t[NT_MAX];
+        uint4 t[NT];
         split_fragment(w, 0, g, (int)(r / g.ksteps), (int)(r % g.ksteps), lane, ws, t);
 #pragma unroll
-        for (int q = 0; q < NT_MAX; ++q) frag[(r * NT_MAX + q) * 64 + lane] = t[q];
+        for (int q = 0; q < NT; ++q) frag[(r * NT + q) * 64 + lane] = t[q];
     }
     if (i < (int64_t)g.ksteps * 4) koff2[i] = koff_of(g, (int)i);
 }
@@ -410,11 +408,10 @@ __device__ __forceinline__ u4 spike_operand(const uint32_t (&xn)[4], uint32_t ct
 // fp16 (1025 + t) in both halves (t <= 1022)
 __device__ __forceinline__ uint32_t step_const(int t) { return (0x6401u + (uint32_t)t) * 0x10001u; }
 
-// One 16x16x32 product of a spike operand with one weight term: fp16 terms for
-// the two-term split, bf16 for the three-term one.
-template <int NT>
+// One 16x16x32 product of a spike operand with one weight term (fp16 or bf16).
+template <bool BF>
 __device__ __forceinline__ f4 mfma(u4 a, uint4 b, f4 c) {
-    if constexpr (NT == 2)
+    if constexpr (!BF)
         return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a), __builtin_bit_cast(half8, b), c, 0,
                                                       0, 0);
     else
@@ -472,15 +469,15 @@ template <int G, bool BLDS, bool ALDS>
 __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     const uint8_t *__restrict__ tpad, const uint4 *__restrict__ frag, const int2 *__restrict__ koff2, ConvGeom g,
     int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words,
-    const float *__restrict__ inv_scale, const int *__restrict__ nterms, const float *__restrict__ wts,
+    const float *__restrict__ inv_scale, const int *__restrict__ wbf16, const float *__restrict__ wts,
     const unsigned *__restrict__ wmax, const unsigned *__restrict__ wmin, int n_wmax, float *__restrict__ P,
     uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
     const int gq = lane >> 4, c = lane & 15;
     int2 *koff_l = reinterpret_cast<int2 *>(lds);
-    uint4 *frag_l = lds + (g.ksteps * 4 * 8 + 15) / 16;  // [ks][n(2)][term(NT_MAX)][64] (BLDS)
-    float *stage = reinterpret_cast<float *>(frag_l + (BLDS ? g.ksteps * 2 * NT_MAX * 64 : 0));  // [TB][32*np_max]
+    uint4 *frag_l = lds + (g.ksteps * 4 * 8 + 15) / 16;  // [ks][n(2)][term(NT)][64] (BLDS)
+    float *stage = reinterpret_cast<float *>(frag_l + (BLDS ? g.ksteps * 2 * NT * 64 : 0));  // [TB][32*np_max]
     const int stage_t = 32 * stage_stride(np_max);
     // ALDS: 2 buffers of a_words words (a multiple of 64) holding a task's
     // padded rows channel-group major, [row][CP/8][Wp][8 bytes], so that the 16
@@ -552,13 +549,13 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) koff_l[i] = koff_of(g, i);
     }
     float inv_s;
-    int n_terms;
+    bool use_bf;
     if (BLDS) {  // the pair's fragments, split here from the weights: [ks][n][term][64]
         // (the staging area, unused until the main loop, holds the reduction's words)
         const uint2 mm = reduce_wrange(wmax, wmin, n_wmax, reinterpret_cast<unsigned *>(stage));
         const WSplit ws = weight_split(mm.x, mm.y);
         inv_s = ws.inv_s;
-        n_terms = ws.nt;
+        use_bf = ws.bf;
         // the pair's weights, contiguous in W, go through the staging area when
         // they fit (coalesced loads instead of one load per tap)
         const int per_f = g.Cin * g.K * g.K, nwp = nf * per_f;
@@ -570,14 +567,14 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         const float *wsrc = wl ? stage : wts + (int64_t)f0 * per_f;
         for (int i = tid; i < g.ksteps * 2 * 64; i += FIN_THREADS) {
             const int ln = i & 63, rr = i >> 6;  // rr = ks*2 + n
-            uint4 t[NT_MAX];
+            uint4 t[NT];
             split_fragment(wsrc, f0, g, pair * 2 + (rr & 1), rr >> 1, ln, ws, t);
 #pragma unroll
-            for (int q = 0; q < NT_MAX; ++q) frag_l[(rr * NT_MAX + q) * 64 + ln] = t[q];
+            for (int q = 0; q < NT; ++q) frag_l[(rr * NT + q) * 64 + ln] = t[q];
         }
     } else {
         inv_s = *inv_scale;
-        n_terms = *nterms;
+        use_bf = *wbf16 != 0;
     }
     if (ALDS) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -588,11 +585,11 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         // Every wave computes up to two tiles of 16 positions for the 32 features;
         // positions of a tile past the chunk repeat its last position and are
         // never stored, which keeps the MFMA stream free of branches.  The K-step
-        // loop is compiled once per weight split (NT terms) and second-slot mode
+        // loop is compiled once per term type (fp16 / bf16) and second-slot mode
         // (below).
-        const uint4 *gf = frag + (int64_t)(pair * 2) * g.ksteps * NT_MAX * 64 + lane;
-        auto mfma_waves = [&](auto nt_c) {
-        constexpr int NT = decltype(nt_c)::value;
+        const uint4 *gf = frag + (int64_t)(pair * 2) * g.ksteps * NT * 64 + lane;
+        auto mfma_waves = [&](auto bf_c) {
+        constexpr bool BF = decltype(bf_c)::value;
         int abuf_sel = 0;
         for (int task = t_lo + r; task < t_hi; task += R) {
             int pos0, np;
@@ -670,13 +667,12 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 auto load_b = [&](uint4 (&bn)[2 * NT], int ks) {
                     // (one base address per K-step and constant offsets: per-fragment
                     // addresses would each hold a register through the loop)
-                    const uint4 *fr = frag_l + ks * (2 * NT_MAX * 64) + lane;
+                    const uint4 *fr = frag_l + ks * (2 * NT * 64) + lane;
 #pragma unroll
                     for (int n = 0; n < 2; ++n)
 #pragma unroll
                         for (int q = 0; q < NT; ++q)
-                            bn[n * NT + q] = BLDS ? fr[(n * NT_MAX + q) * 64]
-                                                  : gf[((n * g.ksteps + ks) * NT_MAX + q) * 64];
+                            bn[n * NT + q] = BLDS ? fr[(n * NT + q) * 64] : gf[((n * g.ksteps + ks) * NT + q) * 64];
                 };
                 // one K-step: spike operands from the words, then TB x 4 tiles x 2 features x NT terms
                 auto kstep = [&](const uint32_t (&an)[FIN_MT][2], const uint4 (&bc)[2 * NT]) {
@@ -700,10 +696,9 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 #pragma unroll
                                 for (int n = 0; n < 2; ++n)
                                     if (fin_unit<M>(i, n))
-                                        acc[i][n][t] = mfma<NT>(a[i], bc[n * NT + q], acc[i][n][t]);
+                                        acc[i][n][t] = mfma<BF>(a[i], bc[n * NT + q], acc[i][n][t]);
                     }
                 };
-                if constexpr (NT == 2) {
                 uint32_t a0[FIN_MT][2], a1[FIN_MT][2];
                 uint4 b0[2 * NT], b1[2 * NT];
                 int2 o2 = koff_at(0);
@@ -727,71 +722,6 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                     load_b(b1, min(ks + 3, g.ksteps - 1));
                 }
                 if (ks < g.ksteps) kstep(a0, b0);
-                } else {
-                // Three terms, term-major: a K-step's spike operands for all TB
-                // steps are formed once, then each term's 4*TB products run while
-                // the next term's two fragments are read (only one term of B is
-                // held in flight: the three-term fragments would not fit the
-                // registers double-buffered whole).  Unrolled by two K-steps so
-                // that the alternating register sets stay static.
-                auto load_bq = [&](uint4 (&bn)[2], int ks, int q) {
-                    const uint4 *fr = frag_l + ks * (2 * NT_MAX * 64) + lane;
-#pragma unroll
-                    for (int n = 0; n < 2; ++n)
-                        bn[n] = BLDS ? fr[(n * NT_MAX + q) * 64] : gf[((n * g.ksteps + ks) * NT_MAX + q) * 64];
-                };
-                auto spikes_of = [&](const uint32_t (&an)[FIN_MT][2], u4 (&a)[FIN_MT][TB]) {
-#pragma unroll
-                    for (int i = 0; i < MT; ++i) {
-                        uint32_t xn[4];
-                        neg_times(an[i][0], xn[0], xn[1]);
-                        neg_times(an[i][1], xn[2], xn[3]);
-#pragma unroll
-                        for (int t = 0; t < TB; ++t) a[i][t] = spike_operand(xn, step_const(tb0 + t));
-                    }
-                };
-                auto term = [&](const u4 (&a)[FIN_MT][TB], const uint4 (&bq)[2]) {
-#pragma unroll
-                    for (int t = 0; t < TB; ++t)
-#pragma unroll
-                        for (int i = 0; i < MT; ++i)
-#pragma unroll
-                            for (int n = 0; n < 2; ++n)
-                                if (fin_unit<M>(i, n)) acc[i][n][t] = mfma<3>(a[i][t], bq[n], acc[i][n][t]);
-                };
-                uint32_t aw0[FIN_MT][2], aw1[FIN_MT][2];
-                uint4 bq0[2], bq1[2];
-                u4 a[FIN_MT][TB];
-                load_a(aw0, koff_at(0));
-                load_bq(bq0, 0, 0);
-                int ks = 0;
-                for (; ks + 1 < g.ksteps; ks += 2) {
-                    spikes_of(aw0, a);
-                    load_a(aw1, koff_at(ks + 1));
-                    load_bq(bq1, ks, 1);
-                    term(a, bq0);
-                    load_bq(bq0, ks, 2);
-                    term(a, bq1);
-                    load_bq(bq1, ks + 1, 0);
-                    term(a, bq0);
-                    spikes_of(aw1, a);
-                    load_a(aw0, koff_at(ks + 2));
-                    load_bq(bq0, ks + 1, 1);
-                    term(a, bq1);
-                    load_bq(bq1, ks + 1, 2);
-                    term(a, bq0);
-                    load_bq(bq0, min(ks + 2, g.ksteps - 1), 0);
-                    term(a, bq1);
-                }
-                if (ks < g.ksteps) {  // an odd last K-step: its words are in aw0, its first term in bq0
-                    spikes_of(aw0, a);
-                    load_bq(bq1, ks, 1);
-                    term(a, bq0);
-                    load_bq(bq0, ks, 2);
-                    term(a, bq1);
-                    term(a, bq0);
-                }
-                }
                 __syncthreads();  // staging free: the store waves are done with the previous block
                 // Staging offset = the lane's part (feature c, positions 4*gq..) plus a
                 // wave-uniform part; the lane part is made opaque here so that the
@@ -842,10 +772,10 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             abuf_sel ^= 1;
         }
         };
-        if (n_terms == 3)
-            mfma_waves(std::integral_constant<int, 3>{});
+        if (use_bf)
+            mfma_waves(std::integral_constant<bool, true>{});
         else
-            mfma_waves(std::integral_constant<int, 2>{});
+            mfma_waves(std::integral_constant<bool, false>{});
     } else {
         // ------------------------------------------------ store waves
         const int s = tid - FIN_CW * 64;
@@ -953,14 +883,9 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 constexpr int INF_WAVES = 8;
 constexpr int INF_MW = 2;   // position tiles per wave
 constexpr int INF_NW = 4;   // 16-feature tiles per workgroup
-// K-steps per LDS chunk: 8 with two weight terms, 4 with three (so that a K
-// range made of whole 8-step chunks is whole chunks for both)
-template <int NT>
-constexpr int inf_kc() { return NT == 2 ? 8 : 4; }
-template <int NT>
-constexpr int inf_chunk_u4() { return inf_kc<NT>() * INF_NW * NT * 64; }  // uint4 per chunk buffer
-constexpr int INF_CHUNK_U4_MAX = inf_chunk_u4<2>() > inf_chunk_u4<3>() ? inf_chunk_u4<2>() : inf_chunk_u4<3>();
-constexpr int INF_KPART = 8;  // a K part is a multiple of this many K-steps
+constexpr int INF_KC = 8;     // K-steps per LDS chunk
+constexpr int INF_CHUNK_U4 = INF_KC * INF_NW * NT * 64;  // uint4 per chunk buffer
+constexpr int INF_KPART = INF_KC;  // a K part is a multiple of this many K-steps (whole chunks)
 constexpr int INF_ZW = 4;   // zero waves (waves 8-11)
 constexpr int64_t INF_PART_MAX = 1 << 21;  // floats of split partial sums at most
 
@@ -972,7 +897,7 @@ template <bool VEC>
 __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     const uint8_t *__restrict__ tpad, const uint4 *__restrict__ frag, const int2 *__restrict__ koff2, ConvGeom g,
     int n_mb, int n_ng, int ksplit, int kpp, float *__restrict__ part, const float *__restrict__ inv_scale,
-    const int *__restrict__ nterms, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
+    const int *__restrict__ wbf16, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
     float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     int2 *koff_l = reinterpret_cast<int2 *>(lds);
@@ -981,7 +906,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     const int gq = lane >> 4, c = lane & 15;
     for (int i = tid; i < g.ksteps * 4; i += (INF_WAVES + INF_ZW) * 64) koff_l[i] = koff2[i];
     const float inv_s = *inv_scale;
-    const int n_terms = *nterms;
+    const bool use_bf = *wbf16 != 0;
     const uint32_t ct = step_const(g.T - 1);
     const int x = blockIdx.x % 8, j = blockIdx.x / 8, per_xcd = (int)gridDim.x / 8;
     const int ntask = n_mb * n_ng * ksplit, per_x = (ntask + 7) / 8;
@@ -995,7 +920,6 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         c_lo = k_lo / kc;
         c_hi = k_hi > k_lo ? (k_hi + kc - 1) / kc : c_lo;
     };
-    const int kc_run = n_terms == 3 ? inf_kc<3>() : inf_kc<2>();
 
     if (wv >= INF_WAVES) {
         // zero waves: 16-byte units of potentials (4 per unit) and 4-byte units of spikes
@@ -1008,7 +932,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         int nint = 1;  // barrier intervals (the last one after the loop)
         for (int task = t_lo + j; task < t_hi; task += per_xcd) {
             int c_lo, c_hi;
-            chunk_range(task, kc_run, c_lo, c_hi);
+            chunk_range(task, INF_KC, c_lo, c_hi);
             nint += 1 + max(0, c_hi - c_lo);
         }
         const int64_t per = (total + nint - 1) / nint;
@@ -1028,7 +952,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         };
         for (int task = t_lo + j; task < t_hi; task += per_xcd) {
             int c_lo, c_hi;
-            chunk_range(task, kc_run, c_lo, c_hi);
+            chunk_range(task, INF_KC, c_lo, c_hi);
             slice();
             __syncthreads();  // the MFMA waves' "buffers free"
             for (int ch = c_lo; ch < c_hi; ++ch) {
@@ -1040,23 +964,23 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         return;
     }
 
-    auto mfma_waves = [&](auto nt_c) {
-    constexpr int NT = decltype(nt_c)::value;
-    constexpr int KC = inf_kc<NT>();
-    constexpr int CHUNK_U4 = inf_chunk_u4<NT>();
+    auto mfma_waves = [&](auto bf_c) {
+    constexpr bool BF = decltype(bf_c)::value;
+    constexpr int KC = INF_KC;
+    constexpr int CHUNK_U4 = INF_CHUNK_U4;
     for (int task = t_lo + j; task < t_hi; task += per_xcd) {
         const int tq = task / ksplit, kp = task % ksplit;
         const int ng = tq / n_mb, mb = tq % n_mb;
         int c_lo, c_hi;
         chunk_range(task, KC, c_lo, c_hi);
-        const uint4 *fg = frag + (int64_t)ng * INF_NW * g.ksteps * NT_MAX * 64;
+        const uint4 *fg = frag + (int64_t)ng * INF_NW * g.ksteps * NT * 64;
         // chunk ch -> buffer: wave w issues the 64-lane groups w, w+8, ... (16 bytes per lane)
         auto fill = [&](int ch) {
             uint4 *dst = cbuf + (ch & 1) * CHUNK_U4;
             const int k0 = ch * KC, nk = min(KC, g.ksteps - k0);
             for (int grp = wv; grp < nk * INF_NW * NT; grp += INF_WAVES) {
                 const int q = grp % NT, n = (grp / NT) % INF_NW, ksl = grp / (NT * INF_NW);
-                const uint4 *src = fg + (((int64_t)n * g.ksteps + k0 + ksl) * NT_MAX + q) * 64 + lane;
+                const uint4 *src = fg + (((int64_t)n * g.ksteps + k0 + ksl) * NT + q) * 64 + lane;
                 __builtin_amdgcn_global_load_lds(src, dst + grp * 64, 16, 0, 0);
             }
         };
@@ -1149,7 +1073,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
 #pragma unroll
                     for (int i = 0; i < INF_MW; ++i)
 #pragma unroll
-                        for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma<NT>(a[i], bt[q][n], acc[i][n]);
+                        for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma<BF>(a[i], bt[q][n], acc[i][n]);
             }
         };
         __syncthreads();  // the buffers are free (previous task done), koff is visible
@@ -1203,10 +1127,10 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             }
     }
     };
-    if (n_terms == 3)
-        mfma_waves(std::integral_constant<int, 3>{});
+    if (use_bf)
+        mfma_waves(std::integral_constant<bool, true>{});
     else
-        mfma_waves(std::integral_constant<int, 2>{});
+        mfma_waves(std::integral_constant<bool, false>{});
 }
 
 // Zero potentials (f32) and spikes (u8) of steps 0..T-2 of every image: per
@@ -1302,7 +1226,7 @@ int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, Con
     g.mt_per_img = (g.HoWo + 15) / 16;
     g.total_mtiles = (int64_t)B * g.mt_per_img;
     pl.tpad_bytes = (size_t)B * g.Hp * g.Wp * g.CP;
-    pl.frag_count = (size_t)g.ntiles * g.ksteps * NT_MAX * 64;
+    pl.frag_count = (size_t)g.ntiles * g.ksteps * NT * 64;
     pl.koff_count = (size_t)g.ksteps * 4;
     // Eq.5 mode on few tasks (a small batch): the K chunks are split into parts
     // run by separate workgroups, so that more than a handful of CUs work; the
@@ -1325,7 +1249,7 @@ size_t plan_workspace(const ConvPlan &pl) {
     c.take<uint4>(pl.frag_count);
     c.take<int2>(pl.koff_count);
     c.take<float>(1);                // 1/scale
-    c.take<int>(1);                  // weight terms
+    c.take<int>(1);                  // weight term type
     c.take<unsigned>(WMAX_PARTS);    // weight-range partials: maxima
     c.take<unsigned>(WMAX_PARTS);    //                        non-zero minima
     c.take<float>(pl.part_count);    // Eq.5 split sums
@@ -1340,31 +1264,31 @@ int max_lds_per_block() {
 }
 
 template <int G, bool BLDS, bool ALDS>
-void launch_fin(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const float *inv_scale, const int *nterms,
+void launch_fin(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const float *inv_scale, const int *wbf16,
                 const float *wts, const unsigned *wmax, const unsigned *wmin, int n_wmax, const ConvGeom &g,
                 int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words, size_t lds, float *P,
                 uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
     // one workgroup per CU: a multiple of the feature pairs on every XCD
     const int per_xcd = (int)spk::ceil_div(std::max(32, n_pairs), n_pairs) * n_pairs;
     hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
-                       tpad, frag, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, nterms,
+                       tpad, frag, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, wbf16,
                        wts, wmax, wmin, n_wmax, P, S, TF, VF);
 }
 
 template <bool VEC>
-void launch_inf(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const float *inv_scale, const int *nterms,
+void launch_inf(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const float *inv_scale, const int *wbf16,
                 const ConvGeom &g, int ksplit, int kpp, float *part, float *P, uint8_t *S, uint8_t *TF, float *VF,
                 hipStream_t st) {
     const int n_mb = (int)spk::ceil_div(g.total_mtiles, INF_WAVES * INF_MW);
     const int n_ng = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), INF_NW);
-    const size_t lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16) + 2 * (size_t)INF_CHUNK_U4_MAX * 16;
+    const size_t lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16) + 2 * (size_t)INF_CHUNK_U4 * 16;
     if (!VEC && g.T > 1 && (P || S)) {  // (with VEC the conv kernel's zero waves write them)
         const int64_t n = (int64_t)(g.T - 1) * g.Cout * g.HoWo;
         const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>(64, spk::ceil_div(n, 256 * 16)));
         hipLaunchKernelGGL(k_zero_planes, dim3(gx, (unsigned)std::min(g.B, 65535)), dim3(256), 0, st, g, P, S);
     }
     hipLaunchKernelGGL((k_conv_fire_inf<VEC>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad, frag,
-                       koff2, g, n_mb, n_ng, ksplit, kpp, part, inv_scale, nterms, P, S, TF, VF);
+                       koff2, g, n_mb, n_ng, ksplit, kpp, part, inv_scale, wbf16, P, S, TF, VF);
     if (ksplit > 1) {
         const int64_t n = (int64_t)g.B * g.Cout * g.HoWo;
         hipLaunchKernelGGL(k_inf_reduce, dim3((unsigned)spk::ceil_div(n, 256)), dim3(256), 0, st, part, ksplit, g,
@@ -1405,7 +1329,7 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     uint4 *frag = cv.take<uint4>(pl.frag_count);
     int2 *koff2 = cv.take<int2>(pl.koff_count);
     float *inv_scale = cv.take<float>(1);
-    int *nterms = cv.take<int>(1);
+    int *wbf16 = cv.take<int>(1);
     unsigned *wmax = cv.take<unsigned>(WMAX_PARTS);
     unsigned *wmin = cv.take<unsigned>(WMAX_PARTS);
     float *part = cv.take<float>(pl.part_count);
@@ -1439,7 +1363,7 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     const int np_max = chunk_tiles * 16;
     const size_t koff_lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16);
     const size_t stage_lds = (size_t)FIN_TB * 32 * stage_stride(np_max) * sizeof(float);
-    const size_t frag_lds = (size_t)g.ksteps * 2 * NT_MAX * 64 * 16;
+    const size_t frag_lds = (size_t)g.ksteps * 2 * NT * 64 * 16;
     const size_t lds_limit = (size_t)max_lds_per_block();
     // spike rows of the largest task, staged in LDS (double-buffered) when small enough
     // (the row count of a chunk depends on its first position modulo HoWo, which repeats
@@ -1468,7 +1392,7 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     const bool alds = g.CP >= 8 && koff_lds + stage_lds + a_lds <= lds_limit;
     const bool blds = koff_lds + frag_lds + stage_lds + (alds ? a_lds : 0) <= lds_limit;
     const size_t fin_lds = koff_lds + (blds ? frag_lds : 0) + stage_lds + (alds ? a_lds : 0);
-    const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4_MAX * 16;
+    const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4 * 16;
     SPK_REQUIRE(!inf_mode || inf_lds <= lds_limit, SPK_E_RANGE,
                 "spk_conv_fire: needs %zu bytes of LDS per workgroup, the device has %zu", inf_lds, lds_limit);
     SPK_REQUIRE(inf_mode || fin_lds <= lds_limit, SPK_E_RANGE,
@@ -1492,18 +1416,18 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     if (inf_mode || !blds) {  // fragments in the workspace (the finite-threshold kernel with LDS room builds its own)
         const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
         hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, wmax,
-                           wmin, n_wmax, frag, koff2, inv_scale, nterms);
+                           wmin, n_wmax, frag, koff2, inv_scale, wbf16);
     }
     if (inf_mode) {
         if (vec)
-            launch_inf<true>(tpad, frag, koff2, inv_scale, nterms, g, pl.ksplit, pl.kpp, part, potentials, spikes,
+            launch_inf<true>(tpad, frag, koff2, inv_scale, wbf16, g, pl.ksplit, pl.kpp, part, potentials, spikes,
                              t_first, v_first, st);
         else
-            launch_inf<false>(tpad, frag, koff2, inv_scale, nterms, g, pl.ksplit, pl.kpp, part, potentials, spikes,
+            launch_inf<false>(tpad, frag, koff2, inv_scale, wbf16, g, pl.ksplit, pl.kpp, part, potentials, spikes,
                               t_first, v_first, st);
     } else {
 #define SPK_FIN(G, BL, AL)                                                                                    \
-    launch_fin<G, BL, AL>(tpad, frag, koff2, inv_scale, nterms, weight, wmax, wmin, n_wmax, g, n_pairs, n_chunks, \
+    launch_fin<G, BL, AL>(tpad, frag, koff2, inv_scale, wbf16, weight, wmax, wmin, n_wmax, g, n_pairs, n_chunks, \
                           cpi, chunk_tiles, np_max, a_words, fin_lds, potentials, spikes, t_first, v_first, st)
         const int sel = (vec ? 4 : 0) + (blds ? 2 : 0) + (alds ? 1 : 0);
         switch (sel) {

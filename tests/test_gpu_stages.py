@@ -195,13 +195,14 @@ def test_conv_fire_weight_range(case, kind, near_log):
 
 
 @pytest.mark.parametrize("case", RANGE_SHAPES, ids=[c[0] for c in RANGE_SHAPES])
-def test_conv_fire_three_term_exact(case):
-    # exactly summable weights whose range takes the three-term split: bit-exact
+def test_conv_fire_bf16_split_exact(case):
+    # exactly summable weights of at most 17 significant bits whose range takes
+    # the bf16 split: bit-exact
     name, B, T, Cin, H, W, Cout, K, pad, thr = case
     g = synth.rng(180 + len(name), 1)
     tf = synth.times_uniform_or_silent(g, (B, Cin, H, W), T, 0.5)
     wave = wave_of(tf, T)
-    Wt = weights.three_term_dyadic(g, (Cout, Cin, K, K), Cin * K * K)
+    Wt = weights.wide_range_dyadic(g, (Cout, Cin, K, K), Cin * K * K)
     thr = math.inf if math.isinf(thr) else float(np.float32(0.37 * Cin * K * K))
     gpu = gpu_conv(wave, Wt, pad, thr)
     ref = orc.conv_fire(wave, Wt, pad, thr)

@@ -69,12 +69,14 @@ def range_weights(kind, shape, seed, T=15, H=8, W=8, pad=1):
     raise ValueError(kind)
 
 
-def three_term_dyadic(g, shape, taps):
-    """Exactly summable weights (multiples of 2^-f, every partial sum exact in
-    float32) whose range needs the three-term split: one weight is 2^(16-f)
-    and one is 2^-f, which is below 2^-15 of the largest weight's power of two."""
-    Wt = synth.dyadic_weights(g, shape, taps)
-    f = min(24 - int(np.ceil(np.log2(taps + 1))), 20)
+def wide_range_dyadic(g, shape, taps):
+    """Exactly summable weights (multiples of 2^-f with f <= 17, every partial
+    sum exact in float32) whose range takes the bf16 split: one weight is
+    2^(16-f) and one is 2^-f, below 2^-15 of the largest weight's power of
+    two.  With at most 17 significant bits each is carried exactly."""
+    f = min(24 - int(np.ceil(np.log2(taps + 1))), 17)
+    m = g.integers(0, (1 << f) + 1, size=shape)
+    Wt = (m.astype(np.float64) / (1 << f)).astype(np.float32)
     flat = Wt.reshape(-1)
     flat[0] = np.float32(2.0 ** (16 - f))
     flat[flat.size // 2] = np.float32(2.0 ** -f)
