@@ -70,15 +70,15 @@ def _load():
         "orc_count_invalid": (_i64, [_u8p, _i64, _int, _i64]),
         "orc_filter": (None, [_u8p, _i64, _int, _int, _f32p, _int, _int, _flt, _f32p]),
         "orc_rank_latency": (None, [_f32p, _i64, _i64, _int, _u8p]),
-        "orc_conv_wave": (None, [_u8p, _i64, _int, _int, _int, _int, _f32p, _int, _int, _int, _f32p]),
-        "orc_conv_times": (None, [_u8p, _i64, _int, _int, _int, _int, _f32p, _int, _int, _int, _f32p]),
-        "orc_conv_points": (None, [_u8p, _i64, _int, _int, _int, _int, _f32p, _int, _int, _int,
+        "orc_conv_wave": (None, [_u8p, _i64, _int, _int, _int, _int, _f32p, _int, _int, _int, _int, _f32p]),
+        "orc_conv_times": (None, [_u8p, _i64, _int, _int, _int, _int, _f32p, _int, _int, _int, _int, _f32p]),
+        "orc_conv_points": (None, [_u8p, _i64, _int, _int, _int, _int, _f32p, _int, _int, _int, _int,
                                    _i32p, _i64, _f32p]),
         "orc_fire": (None, [_f32p, _i64, _int, _i64, _flt, _int, _u8p, _u8p, _f32p]),
         "orc_pool": (None, [_u8p, _i64, _int, _int, _int, _int, _int, _int, _int, _u8p]),
         "orc_kwta": (None, [_u8p, _f32p, _i64, _int, _int, _int, _int, _int, _int, _i32p, _i32p]),
         "orc_decide": (None, [_i32p, _i32p, _i64, _int, _i32p, _int, _i32p, _i8p]),
-        "orc_count_events": (_i64, [_u8p, _i64, _int, _int, _int, _int, _int, _int, _int]),
+        "orc_count_events": (_i64, [_u8p, _i64, _int, _int, _int, _int, _int, _int, _int, _int]),
         "orc_pool_potentials": (None, [_f32p, _i64, _int, _int, _int, _int, _int, _int, _int, _f32p]),
         "orc_local_normalize": (None, [_f32p, _i64, _int, _int, _int, _int, _flt, _f32p]),
     }
@@ -88,7 +88,7 @@ def _load():
         fn.argtypes = args
     # orc_stdp takes a nullable reward pointer: declare it with c_void_p.
     lib.orc_stdp.restype = None
-    lib.orc_stdp.argtypes = [_f32p, _int, _int, _int, _int, _u8p, _i64, _int, _int, _int,
+    lib.orc_stdp.argtypes = [_f32p, _int, _int, _int, _int, _int, _u8p, _i64, _int, _int, _int,
                              _i32p, _i32p, _int, ctypes.c_void_p, _flt, _flt, _flt, _flt, _int]
     # orc_pointwise_inhibition takes nullable potentials
     lib.orc_pointwise_inhibition.restype = None
@@ -170,38 +170,39 @@ def encode(img: np.ndarray, filt: np.ndarray, T: int, thr: float = 0.0):
 
 
 # ---------------------------------------------------------------- conv / fire
-def out_size(n: int, pad: int, K: int) -> int:
-    """Eq.2 applied to the zero-padded input."""
-    return n + 2 * pad - K + 1
+def out_size(n: int, pad: int, K: int, stride: int = 1) -> int:
+    """Eq.2 applied to the zero-padded input, floor((n + 2 pad - K) / stride) + 1."""
+    return (n + 2 * pad - K) // stride + 1
 
 
-def conv_wave(wave: np.ndarray, weight: np.ndarray, pad: int) -> np.ndarray:
-    """Potentials [B,T,Cout,Ho,Wo]: per-step cross-correlation of the wave."""
+def conv_wave(wave: np.ndarray, weight: np.ndarray, pad: int, stride: int = 1) -> np.ndarray:
+    """Potentials [B,T,Cout,Ho,Wo]: per-step cross-correlation of the wave
+    (output (y, x) reads the padded window at (y*stride, x*stride))."""
     w = _c(wave, np.uint8)
     wt = _c(weight, np.float32)
     B, T, Cin, H, W = w.shape
     Cout, Cin2, K, _ = wt.shape
     assert Cin2 == Cin
-    Ho, Wo = out_size(H, pad, K), out_size(W, pad, K)
+    Ho, Wo = out_size(H, pad, K, stride), out_size(W, pad, K, stride)
     out = np.empty((B, T, Cout, Ho, Wo), np.float32)
-    _load().orc_conv_wave(w, B, T, Cin, H, W, wt, Cout, K, pad, out)
+    _load().orc_conv_wave(w, B, T, Cin, H, W, wt, Cout, K, pad, stride, out)
     return out
 
 
-def conv_times(t_first: np.ndarray, T: int, weight: np.ndarray, pad: int) -> np.ndarray:
+def conv_times(t_first: np.ndarray, T: int, weight: np.ndarray, pad: int, stride: int = 1) -> np.ndarray:
     """Same potentials from first-spike times (running sum over t)."""
     tf = _c(t_first, np.uint8)
     wt = _c(weight, np.float32)
     B, Cin, H, W = tf.shape
     Cout, Cin2, K, _ = wt.shape
     assert Cin2 == Cin
-    Ho, Wo = out_size(H, pad, K), out_size(W, pad, K)
+    Ho, Wo = out_size(H, pad, K, stride), out_size(W, pad, K, stride)
     out = np.empty((B, T, Cout, Ho, Wo), np.float32)
-    _load().orc_conv_times(tf, B, T, Cin, H, W, wt, Cout, K, pad, out)
+    _load().orc_conv_times(tf, B, T, Cin, H, W, wt, Cout, K, pad, stride, out)
     return out
 
 
-def conv_points(wave: np.ndarray, weight: np.ndarray, pad: int, pts: np.ndarray) -> np.ndarray:
+def conv_points(wave: np.ndarray, weight: np.ndarray, pad: int, pts: np.ndarray, stride: int = 1) -> np.ndarray:
     """Potentials P[b, :, f, y, x] for each row (b, f, y, x) of pts -> [n, T]."""
     w = _c(wave, np.uint8)
     wt = _c(weight, np.float32)
@@ -209,7 +210,7 @@ def conv_points(wave: np.ndarray, weight: np.ndarray, pad: int, pts: np.ndarray)
     B, T, Cin, H, W = w.shape
     Cout, _, K, _ = wt.shape
     out = np.empty((p.shape[0], T), np.float32)
-    _load().orc_conv_points(w, B, T, Cin, H, W, wt, Cout, K, pad, p, p.shape[0], out)
+    _load().orc_conv_points(w, B, T, Cin, H, W, wt, Cout, K, pad, stride, p, p.shape[0], out)
     return out
 
 
@@ -229,9 +230,9 @@ def fire(pot: np.ndarray, thr: float):
     return P, spk, tf, vf
 
 
-def conv_fire(wave: np.ndarray, weight: np.ndarray, pad: int, thr: float):
+def conv_fire(wave: np.ndarray, weight: np.ndarray, pad: int, thr: float, stride: int = 1):
     """conv_wave followed by fire: (potentials, spikes, t_first, v_first)."""
-    return fire(conv_wave(wave, weight, pad), thr)
+    return fire(conv_wave(wave, weight, pad, stride), thr)
 
 
 # ---------------------------------------------------------------- pool
@@ -290,10 +291,11 @@ def kwta(t_first: np.ndarray, v_first: np.ndarray, T: int, k: int, r: int):
 # ---------------------------------------------------------------- plasticity
 def stdp(weight: np.ndarray, pre_wave: np.ndarray, pad: int, winners: np.ndarray,
          n_win: np.ndarray, a_plus: float, a_minus: float, lb: float = 0.0, ub: float = 1.0,
-         stabilizer: bool = True, reward: np.ndarray | None = None) -> np.ndarray:
+         stabilizer: bool = True, reward: np.ndarray | None = None, stride: int = 1) -> np.ndarray:
     """Eq.4 on the winners (ordered replay over images); returns new weights.
 
-    reward (int8 [B] in {+1,-1,0}) turns it into R-STDP."""
+    reward (int8 [B] in {+1,-1,0}) turns it into R-STDP; stride is the
+    layer's (the winner (y, x) sees the input window at (y*stride, x*stride))."""
     wt = np.array(weight, dtype=np.float32, order="C", copy=True)
     pw = _c(pre_wave, np.uint8)
     wn = _c(winners, np.int32)
@@ -308,7 +310,7 @@ def stdp(weight: np.ndarray, pre_wave: np.ndarray, pad: int, winners: np.ndarray
         rptr = rw.ctypes.data_as(ctypes.c_void_p)
     else:
         rptr = None
-    _load().orc_stdp(wt, Cout, Cin, K, pad, pw, B, T, H, W, wn, nw, k, rptr,
+    _load().orc_stdp(wt, Cout, Cin, K, pad, stride, pw, B, T, H, W, wn, nw, k, rptr,
                      float(a_plus), float(a_minus), float(lb), float(ub), int(bool(stabilizer)))
     return wt
 
@@ -325,8 +327,8 @@ def decide(winners: np.ndarray, n_win: np.ndarray, labels: np.ndarray, n_classes
     return dec, rew
 
 
-def count_events(t_first: np.ndarray, T: int, Cout: int, K: int, pad: int) -> int:
+def count_events(t_first: np.ndarray, T: int, Cout: int, K: int, pad: int, stride: int = 1) -> int:
     """Synaptic events: (spiking pre, post) pairs, each counted once."""
     tf = _c(t_first, np.uint8)
     B, Cin, H, W = tf.shape
-    return int(_load().orc_count_events(tf, B, T, Cin, H, W, Cout, K, pad))
+    return int(_load().orc_count_events(tf, B, T, Cin, H, W, Cout, K, pad, stride))

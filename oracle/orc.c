@@ -164,14 +164,18 @@ ORC_API void orc_rank_latency(const float *inten, int64_t B, int64_t N, int T,
 
 /* ------------------------------------------------------------------ */
 /* Convolution of a spike wave (section "snn Module", Eq.2): for every
- * time-step independently, a stride-1 valid cross-correlation of the
- * (zero-padded, as in the tutorial's forward pass) input wave with the
- * weights.  Literal form: the sum over all taps of W * S[t] at each t. */
-static inline int orc_out_size(int n, int pad, int K) { return n + 2 * pad - K + 1; }
+ * time-step independently, a valid cross-correlation of the (zero-padded,
+ * as in the tutorial's forward pass) input wave with the weights.  Literal
+ * form: the sum over all taps of W * S[t] at each t.  The paper's layers
+ * have stride 1 and name larger strides as the next version's feature; with
+ * stride s the output neuron (y, x) sees the input window whose top-left
+ * padded position is (y*s, x*s), and Eq.2 becomes
+ * H_out = floor((H_in + 2*pad - K) / s) + 1 (stride 1: H_in + 2*pad - K + 1). */
+static inline int orc_out_size(int n, int pad, int K, int stride) { return (n + 2 * pad - K) / stride + 1; }
 
 ORC_API void orc_conv_wave(const uint8_t *wave, int64_t B, int T, int Cin, int H, int W,
-                           const float *wt, int Cout, int K, int pad, float *pot) {
-    int Ho = orc_out_size(H, pad, K), Wo = orc_out_size(W, pad, K);
+                           const float *wt, int Cout, int K, int pad, int stride, float *pot) {
+    int Ho = orc_out_size(H, pad, K, stride), Wo = orc_out_size(W, pad, K, stride);
     for (int64_t b = 0; b < B; ++b)
         for (int t = 0; t < T; ++t) {
             const uint8_t *S = wave + (b * T + t) * (int64_t)Cin * H * W;
@@ -182,7 +186,7 @@ ORC_API void orc_conv_wave(const uint8_t *wave, int64_t B, int T, int Cin, int H
                         for (int ci = 0; ci < Cin; ++ci)
                             for (int ky = 0; ky < K; ++ky)
                                 for (int kx = 0; kx < K; ++kx) {
-                                    int iy = y + ky - pad, ix = x + kx - pad;
+                                    int iy = y * stride + ky - pad, ix = x * stride + kx - pad;
                                     if (iy < 0 || iy >= H || ix < 0 || ix >= W) continue;
                                     if (S[((int64_t)ci * H + iy) * W + ix])
                                         s += (double)wt[((f * Cin + ci) * K + ky) * K + kx];
@@ -198,8 +202,8 @@ ORC_API void orc_conv_wave(const uint8_t *wave, int64_t B, int T, int Cin, int H
  * spiked exactly at t.  Used to cross-check the literal form; it is also
  * the form that stays fast at large T. */
 ORC_API void orc_conv_times(const uint8_t *tin, int64_t B, int T, int Cin, int H, int W,
-                            const float *wt, int Cout, int K, int pad, float *pot) {
-    int Ho = orc_out_size(H, pad, K), Wo = orc_out_size(W, pad, K);
+                            const float *wt, int Cout, int K, int pad, int stride, float *pot) {
+    int Ho = orc_out_size(H, pad, K, stride), Wo = orc_out_size(W, pad, K, stride);
     double *hist = (double *)malloc((size_t)(T + 1) * sizeof(double));
     for (int64_t b = 0; b < B; ++b)
         for (int f = 0; f < Cout; ++f)
@@ -209,7 +213,7 @@ ORC_API void orc_conv_times(const uint8_t *tin, int64_t B, int T, int Cin, int H
                     for (int ci = 0; ci < Cin; ++ci)
                         for (int ky = 0; ky < K; ++ky)
                             for (int kx = 0; kx < K; ++kx) {
-                                int iy = y + ky - pad, ix = x + kx - pad;
+                                int iy = y * stride + ky - pad, ix = x * stride + kx - pad;
                                 if (iy < 0 || iy >= H || ix < 0 || ix >= W) continue;
                                 int tj = tin[((b * Cin + ci) * (int64_t)H + iy) * W + ix];
                                 if (tj < T)
@@ -227,7 +231,7 @@ ORC_API void orc_conv_times(const uint8_t *tin, int64_t B, int T, int Cin, int H
 /* Potentials of selected neurons only (full-size checks sample outputs):
  * for each of the n requested (b, f, y, x) it writes P[0..T-1], literal form. */
 ORC_API void orc_conv_points(const uint8_t *wave, int64_t B, int T, int Cin, int H, int W,
-                             const float *wt, int Cout, int K, int pad,
+                             const float *wt, int Cout, int K, int pad, int stride,
                              const int32_t *pts, int64_t n, float *out) {
     (void)B; (void)Cout;
     for (int64_t q = 0; q < n; ++q) {
@@ -238,7 +242,7 @@ ORC_API void orc_conv_points(const uint8_t *wave, int64_t B, int T, int Cin, int
             for (int ci = 0; ci < Cin; ++ci)
                 for (int ky = 0; ky < K; ++ky)
                     for (int kx = 0; kx < K; ++kx) {
-                        int iy = y + ky - pad, ix = x + kx - pad;
+                        int iy = y * stride + ky - pad, ix = x * stride + kx - pad;
                         if (iy < 0 || iy >= H || ix < 0 || ix >= W) continue;
                         if (S[((int64_t)ci * H + iy) * W + ix])
                             s += (double)wt[((f * Cin + ci) * K + ky) * K + kx];
@@ -413,7 +417,8 @@ ORC_API void orc_kwta(const uint8_t *t_first, const float *v_first, int64_t B, i
 /* STDP (Eq.4) applied to the winners' weights, and R-STDP (section
  * "snn Module": two STDP objects; tutorial: anti-STDP negates the learning
  * rates).  For winner i = (f, t_i, y, x) and each synapse (ci, ky, kx) the
- * pre-synaptic neuron j sits at (ci, y+ky-pad, x+kx-pad) of the layer input;
+ * pre-synaptic neuron j sits at (ci, y*s+ky-pad, x*s+kx-pad) of the layer
+ * input (s the layer's stride);
  * T_j <= T_i holds exactly when the cumulative input wave is 1 there at
  * step t_i (a padded position never spikes).  Then
  *     dW = A * (W - LB) * (UB - W),  A = A+ if T_j <= T_i else A-,
@@ -424,7 +429,7 @@ ORC_API void orc_kwta(const uint8_t *t_first, const float *v_first, int64_t B, i
  * negated) or 0 (no update) per image.
  * Evaluation order, in double precision, rounded to float once per update:
  *     d = (w - lb) * (ub - w);  u = a * d;  w = w + u;  clamp to [lb, ub]. */
-ORC_API void orc_stdp(float *wt, int Cout, int Cin, int K, int pad,
+ORC_API void orc_stdp(float *wt, int Cout, int Cin, int K, int pad, int stride,
                       const uint8_t *pre_wave, int64_t B, int T, int H, int W,
                       const int32_t *winners, const int32_t *n_win, int k,
                       const int8_t *reward, float a_plus, float a_minus,
@@ -443,7 +448,7 @@ ORC_API void orc_stdp(float *wt, int Cout, int Cin, int K, int pad,
             for (int ci = 0; ci < Cin; ++ci)
                 for (int ky = 0; ky < K; ++ky)
                     for (int kx = 0; kx < K; ++kx) {
-                        int iy = y + ky - pad, ix = x + kx - pad;
+                        int iy = y * stride + ky - pad, ix = x * stride + kx - pad;
                         int pre = 0;
                         if (iy >= 0 && iy < H && ix >= 0 && ix < W)
                             pre = S[((int64_t)ci * H + iy) * W + ix] != 0;
@@ -483,8 +488,8 @@ ORC_API void orc_decide(const int32_t *winners, const int32_t *n_win, int64_t B,
  * simulation, i.e. for every output neuron the number of its input taps
  * whose neuron spikes at some step.  Returns the total over the batch. */
 ORC_API int64_t orc_count_events(const uint8_t *tin, int64_t B, int T, int Cin, int H, int W,
-                                 int Cout, int K, int pad) {
-    int Ho = orc_out_size(H, pad, K), Wo = orc_out_size(W, pad, K);
+                                 int Cout, int K, int pad, int stride) {
+    int Ho = orc_out_size(H, pad, K, stride), Wo = orc_out_size(W, pad, K, stride);
     int64_t e = 0;
     for (int64_t b = 0; b < B; ++b)
         for (int y = 0; y < Ho; ++y)
@@ -493,7 +498,7 @@ ORC_API int64_t orc_count_events(const uint8_t *tin, int64_t B, int T, int Cin, 
                 for (int ci = 0; ci < Cin; ++ci)
                     for (int ky = 0; ky < K; ++ky)
                         for (int kx = 0; kx < K; ++kx) {
-                            int iy = y + ky - pad, ix = x + kx - pad;
+                            int iy = y * stride + ky - pad, ix = x * stride + kx - pad;
                             if (iy < 0 || iy >= H || ix < 0 || ix >= W) continue;
                             c += tin[((b * Cin + ci) * (int64_t)H + iy) * W + ix] < T;
                         }

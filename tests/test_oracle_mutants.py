@@ -22,9 +22,21 @@ MUTANTS = {
         "s += (double)wt[((f * Cin + ci) * K + (K - 1 - ky)) * K + (K - 1 - kx)];"),
     "conv: padding dropped": (
         "for (int ky = 0; ky < K; ++ky)\n                                for (int kx = 0; kx < K; ++kx) {\n"
-        "                                    int iy = y + ky - pad, ix = x + kx - pad;",
+        "                                    int iy = y * stride + ky - pad, ix = x * stride + kx - pad;",
         "for (int ky = 0; ky < K; ++ky)\n                                for (int kx = 0; kx < K; ++kx) {\n"
-        "                                    int iy = y + ky, ix = x + kx;"),
+        "                                    int iy = y * stride + ky, ix = x * stride + kx;"),
+    "conv: stride ignored": ("int iy = y * stride + ky - pad, ix = x * stride + kx - pad;\n"
+                             "                                    if (iy < 0",
+                             "int iy = y + ky - pad, ix = x + kx - pad;\n"
+                             "                                    if (iy < 0"),
+    "conv: stride on one axis only": ("int iy = y * stride + ky - pad, ix = x * stride + kx - pad;",
+                                      "int iy = y * stride + ky - pad, ix = x + kx - pad;"),
+    "conv: output size rounded up": ("return (n + 2 * pad - K) / stride + 1;",
+                                     "return (n + 2 * pad - K + stride - 1) / stride + 1;"),
+    "stdp: stride ignored": ("int iy = y * stride + ky - pad, ix = x * stride + kx - pad;\n"
+                             "                        int pre = 0;",
+                             "int iy = y + ky - pad, ix = x + kx - pad;\n"
+                             "                        int pre = 0;"),
     "conv_times: prefix off by one step": (
         "run += hist[t];\n                        pot[", "pot["),
     "wave: strict > in Eq.1": ("(uint8_t)(t >= t_first[b * N + i])", "(uint8_t)(t > t_first[b * N + i])"),

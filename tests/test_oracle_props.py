@@ -53,6 +53,73 @@ def test_conv_matches_torch_float64_per_step(pad, K, Cin, Cout, H, W, T):
     assert np.array_equal(P, ref)
 
 
+# Stride > 1 (the paper names it as the next version's feature): torch's
+# float64 conv2d with the same stride, and the stride-1 map subsampled.
+@pytest.mark.parametrize("pad,K,Cin,Cout,H,W,T,s", [(0, 3, 2, 3, 9, 8, 4, 2), (2, 5, 3, 4, 11, 9, 6, 2),
+                                                    (1, 3, 2, 2, 10, 7, 5, 3), (0, 2, 1, 2, 9, 10, 3, 3),
+                                                    (3, 7, 2, 3, 13, 12, 4, 4)])
+def test_conv_stride_matches_torch_float64_per_step(pad, K, Cin, Cout, H, W, T, s):
+    g = np.random.default_rng(17)
+    tf = _rand_times(K * 10 + pad + s, (2, Cin, H, W), T)
+    wave = orc.expand_wave(tf, T)
+    Wt = g.uniform(0, 1, (Cout, Cin, K, K)).astype(np.float32)
+    P = orc.conv_wave(wave, Wt, pad, s)
+    ref = F.conv2d(torch.from_numpy(wave.reshape(-1, Cin, H, W).astype(np.float64)),
+                   torch.from_numpy(Wt.astype(np.float64)), padding=pad, stride=s)
+    assert P.shape[-2:] == (orc.out_size(H, pad, K, s), orc.out_size(W, pad, K, s)) == tuple(ref.shape[-2:])
+    assert np.array_equal(P, ref.numpy().astype(np.float32).reshape(P.shape))
+    # the same sums as the stride-1 potentials at every s-th position
+    P1 = orc.conv_wave(wave, Wt, pad)
+    assert np.array_equal(P, P1[..., ::s, ::s][..., :P.shape[-2], :P.shape[-1]])
+    assert np.array_equal(P, orc.conv_times(tf, T, Wt, pad, s)) or \
+        np.max(np.abs(P.astype(np.float64) - orc.conv_times(tf, T, Wt, pad, s))) <= np.max(np.spacing(np.abs(P)))
+    pts = np.array([[0, 0, 0, 0], [1, Cout - 1, P.shape[-2] - 1, P.shape[-1] - 1]], np.int32)
+    c = orc.conv_points(wave, Wt, pad, pts, s)
+    for q, (bb, f, y, x) in enumerate(pts):
+        assert np.array_equal(c[q], P[bb, :, f, y, x])
+
+
+def test_stdp_stride_reduces_to_stride_1():
+    # a winner (y, x) of a stride-s layer sees the window of the stride-1
+    # neuron (y*s, x*s): the updates are identical
+    g = np.random.default_rng(21)
+    T, Cin, Cout, K, pad, H, W, s, B, k = 8, 3, 5, 3, 1, 11, 10, 2, 3, 3
+    wave = orc.expand_wave(_rand_times(12, (B, Cin, H, W), T, 0.5), T)
+    Wt = g.uniform(0.05, 0.95, (Cout, Cin, K, K)).astype(np.float32)
+    Ho, Wo = orc.out_size(H, pad, K, s), orc.out_size(W, pad, K, s)
+    win = np.full((B, k, 4), -1, np.int32)
+    nw = np.array([3, 0, 2], np.int32)
+    for b in range(B):
+        fs = g.permutation(Cout)[:nw[b]]
+        for j in range(nw[b]):
+            win[b, j] = (fs[j], g.integers(0, T), g.integers(0, Ho), g.integers(0, Wo))
+    win[0, 2, 2:] = (Ho - 1, Wo - 1)  # the last window, partly in the padding
+    w1 = win.copy()
+    w1[..., 2:] = np.where(win[..., 2:] >= 0, win[..., 2:] * s, -1)
+    a = orc.stdp(Wt, wave, pad, win, nw, 0.004, -0.003, stride=s)
+    assert np.array_equal(a, orc.stdp(Wt, wave, pad, w1, nw, 0.004, -0.003))
+    assert not np.array_equal(a, orc.stdp(Wt, wave, pad, win, nw, 0.004, -0.003))
+    rw = np.array([-1, 1, 0], np.int8)
+    assert np.array_equal(orc.stdp(Wt, wave, pad, win, nw, 0.004, -0.003, reward=rw, stride=s),
+                          orc.stdp(Wt, wave, pad, w1, nw, 0.004, -0.003, reward=rw))
+
+
+def test_count_events_stride_brute_force():
+    T, Cin, Cout, K, pad, H, W, s = 6, 3, 4, 3, 1, 9, 8, 2
+    tf = _rand_times(9, (2, Cin, H, W), T, 0.5)
+    e = 0
+    for b in range(2):
+        for y in range((H + 2 * pad - K) // s + 1):
+            for x in range((W + 2 * pad - K) // s + 1):
+                for ci in range(Cin):
+                    for ky in range(K):
+                        for kx in range(K):
+                            iy, ix = y * s + ky - pad, x * s + kx - pad
+                            if 0 <= iy < H and 0 <= ix < W and tf[b, ci, iy, ix] < T:
+                                e += Cout
+    assert orc.count_events(tf, T, Cout, K, pad, s) == e
+
+
 def test_fig2_shapes():
     # Fig.2 caption: one 5x5 input map, 3 steps, a 3x3 valid kernel -> [3,1,3,3] potentials.
     tf = _rand_times(3, (1, 1, 5, 5), 3)
