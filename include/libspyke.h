@@ -181,6 +181,27 @@ SPK_API int spk_conv_fire_first_spike_noalloc(const uint8_t *in_t_first, int B, 
              const float *weight, int Cout, int K, int pad, float threshold,
              float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first, void *stream);
 
+/* Convolution + firing with stride > 1 (section "snn Module" names strides
+ * above 1 as the next version's feature): output neuron (y, x) reads the
+ * zero-padded input window whose top-left corner is (y*stride, x*stride),
+ *   P[t,f,y,x] = sum over (ci,ky,kx) of W[f,ci,ky,kx] * S[t,ci,y*stride+ky-pad,x*stride+kx-pad],
+ * and Eq.2 becomes Ho = floor((H + 2*pad - K) / stride) + 1 (likewise Wo).
+ *   stride  1..64 (1 is spk_conv_fire / spk_conv_fire_first_spike).
+ * Everything else -- arguments, firing, Eq.5 mode, the weight terms, limits,
+ * errors -- as spk_conv_fire (the wave form) and spk_conv_fire_first_spike
+ * (the first-spike form).  Workspace:
+ * spk_conv_fire_strided_workspace_size(...) bytes.                          */
+SPK_API size_t spk_conv_fire_strided_workspace_size(int B, int T, int Cin, int H, int W, int Cout, int K,
+             int stride, int pad);
+SPK_API int spk_conv_fire_strided(const uint8_t *wave, int B, int T, int Cin, int H, int W,
+             const float *weight, int Cout, int K, int stride, int pad, float threshold,
+             float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
+             void *workspace, size_t ws_bytes, void *stream);
+SPK_API int spk_conv_fire_first_spike_strided(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+             const float *weight, int Cout, int K, int stride, int pad, float threshold,
+             float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
+             void *workspace, size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------------------
  * Spike max-pooling (section "snn Module", Eq.3): on a spike wave each
  * window yields its earliest spike.  Window `kernel`, stride `stride`,
@@ -279,6 +300,22 @@ SPK_API int spk_rstdp(float *weight, int Cout, int Cin, int K, int pad,
               float a_plus, float a_minus, float lb, float ub, int stabilizer,
               void *workspace, size_t ws_bytes, void *stream);
 
+/* STDP / R-STDP of a layer with stride > 1 (Eq.4; stride as in
+ * spk_conv_fire_strided): the pre-synaptic neuron of winner (f, t_i, y, x)
+ * and synapse (ci, ky, kx) is (ci, y*stride+ky-pad, x*stride+kx-pad) of the
+ * layer input.  stride 1..64; all else as spk_stdp / spk_rstdp (same
+ * workspace).                                                               */
+SPK_API int spk_stdp_strided(float *weight, int Cout, int Cin, int K, int stride, int pad,
+             const uint8_t *pre_wave, int B, int T, int H, int W,
+             const int32_t *winners, const int32_t *n_winners, int k,
+             float a_plus, float a_minus, float lb, float ub, int stabilizer,
+             void *workspace, size_t ws_bytes, void *stream);
+SPK_API int spk_rstdp_strided(float *weight, int Cout, int Cin, int K, int stride, int pad,
+             const uint8_t *pre_wave, int B, int T, int H, int W,
+             const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward,
+             float a_plus, float a_minus, float lb, float ub, int stabilizer,
+             void *workspace, size_t ws_bytes, void *stream);
+
 /* Decision and reward (tutorial: the first winner's feature maps to a
  * class; reward when it equals the label, punish otherwise, nothing for a
  * silent sample).  decision i32 [B] = winners[b][0].feature % n_classes or
@@ -295,6 +332,10 @@ SPK_API int spk_decide(const int32_t *winners, const int32_t *n_winners, int B, 
  * *count is a device u64, overwritten.  Same size rules as spk_conv_fire.  */
 SPK_API int spk_count_events(const uint8_t *wave, int B, int T, int Cin, int H, int W,
                              int Cout, int K, int pad, uint64_t *count, void *stream);
+/* The same count for a layer with stride > 1 (receptive fields as in
+ * spk_conv_fire_strided; stride 1..64).                                    */
+SPK_API int spk_count_events_strided(const uint8_t *wave, int B, int T, int Cin, int H, int W,
+                             int Cout, int K, int stride, int pad, uint64_t *count, void *stream);
 
 #ifdef __cplusplus
 }

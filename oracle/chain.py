@@ -17,6 +17,10 @@ def _is_conv(st):
     return hasattr(st, "cout")
 
 
+def _stride(st):
+    return getattr(st, "stride", 1)
+
+
 def forward(wl, inputs, weights, images=None):
     """Per-stage oracle results for the selected images (default: all).
 
@@ -37,7 +41,7 @@ def forward(wl, inputs, weights, images=None):
     wi = 0
     for st in wl.stages:
         if _is_conv(st):
-            P, S, tf1, vf1 = fire(conv_times(tf, T, weights[wi], st.pad), st.thr)
+            P, S, tf1, vf1 = fire(conv_times(tf, T, weights[wi], st.pad, _stride(st)), st.thr)
             win, nw = kwta(tf1, vf1, T, st.k, st.r)
             out.append({"pre_wave": wave, "P": P, "S": S, "tf": tf1, "vf": vf1, "win": win, "nw": nw})
             wave, tf = S, tf1
@@ -102,10 +106,10 @@ def learn(wl, res, weights, dec):
             new.append(W.copy())
         elif st.learn == "rstdp":
             new.append(stdp(W, r["pre_wave"], st.pad, r["win"], r["nw"], st.a_plus, st.a_minus, st.lb, st.ub,
-                            st.stabilizer, reward=dec[1]))
+                            st.stabilizer, reward=dec[1], stride=_stride(st)))
         else:
             new.append(stdp(W, r["pre_wave"], st.pad, r["win"], r["nw"], st.a_plus, st.a_minus, st.lb, st.ub,
-                            st.stabilizer))
+                            st.stabilizer, stride=_stride(st)))
     return new
 
 

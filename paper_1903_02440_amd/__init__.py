@@ -58,6 +58,15 @@ _SIGS = {
     "spk_rstdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _P, _F, _F, _F, _F, _I, _P, _Z, _P]),
     "spk_decide": (_I, [_P, _P, _I, _I, _P, _I, _P, _P, _P]),
     "spk_count_events": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
+    "spk_conv_fire_strided_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
+    "spk_conv_fire_strided": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z, _P]),
+    "spk_conv_fire_first_spike_strided": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P,
+                                               _Z, _P]),
+    "spk_stdp_strided": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _F, _F, _F, _F, _I, _P, _Z,
+                              _P]),
+    "spk_rstdp_strided": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _P, _F, _F, _F, _F, _I, _P,
+                               _Z, _P]),
+    "spk_count_events_strided": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -203,56 +212,82 @@ def spk_validate_wave(wave, bad_count=None, stream=None):
 
 
 # ---------------------------------------------------------------- conv + fire
-def conv_out_size(n, K, pad):
-    return n + 2 * pad - K + 1
+def conv_out_size(n, K, pad, stride=1):
+    """Eq.2 on the zero-padded input: floor((n + 2 pad - K) / stride) + 1."""
+    return (n + 2 * pad - K) // stride + 1
 
 
 def spk_conv_fire_workspace_size(B, T, Cin, H, W, Cout, K, pad) -> int:
     return int(_lib.spk_conv_fire_workspace_size(B, T, Cin, H, W, Cout, K, pad))
 
 
-def spk_conv_fire(wave, weight, pad, threshold, potentials=None, spikes=None, t_first=None, v_first=None,
-                  workspace=None, stream=None):
-    """wave u8 [B,T,Cin,H,W], weight f32 [Cout,Cin,K,K] ->
-    (potentials f32 [B,T,Cout,Ho,Wo], spikes u8 [B,T,Cout,Ho,Wo], t_first u8 [B,Cout,Ho,Wo], v_first f32)."""
-    B, T, Cin, H, W = wave.shape
+def spk_conv_fire_strided_workspace_size(B, T, Cin, H, W, Cout, K, stride, pad) -> int:
+    return int(_lib.spk_conv_fire_strided_workspace_size(B, T, Cin, H, W, Cout, K, stride, pad))
+
+
+def _conv_call(x, times, T, weight, stride, pad, threshold, potentials, spikes, t_first, v_first, workspace,
+               stream):
+    """Marshal one conv call; x is the wave u8 [B,T,Cin,H,W] or (times) the
+    first-spike map u8 [B,Cin,H,W].  stride None calls the stride-1 entry points."""
+    if times:
+        B, Cin, H, W = x.shape
+        _need(x, torch.uint8, (B, Cin, H, W), "in_t_first")
+    else:
+        B, T, Cin, H, W = x.shape
+        _need(x, torch.uint8, (B, T, Cin, H, W), "wave")
     Cout, Cin2, K, _ = weight.shape
-    _need(wave, torch.uint8, (B, T, Cin, H, W), "wave")
     _need(weight, torch.float32, (Cout, Cin, K, K), "weight")
-    Ho, Wo = conv_out_size(H, K, pad), conv_out_size(W, K, pad)
-    dev = wave.device
+    s = 1 if stride is None else stride
+    Ho, Wo = conv_out_size(H, K, pad, s), conv_out_size(W, K, pad, s)
+    dev = x.device
     potentials = _out(potentials, (B, T, Cout, Ho, Wo), torch.float32, dev, "potentials")
     spikes = _out(spikes, (B, T, Cout, Ho, Wo), torch.uint8, dev, "spikes")
     t_first = _out(t_first, (B, Cout, Ho, Wo), torch.uint8, dev, "t_first")
     v_first = _out(v_first, (B, Cout, Ho, Wo), torch.float32, dev, "v_first")
-    n = spk_conv_fire_workspace_size(B, T, Cin, H, W, Cout, K, pad)
-    ws = _ws(workspace, n, dev)
-    _check(_lib.spk_conv_fire(_ptr(wave), B, T, Cin, H, W, _ptr(weight), Cout, K, pad, float(threshold),
-                              _ptr(potentials), _ptr(spikes), _ptr(t_first), _ptr(v_first), _ptr(ws), n,
-                              _stream(stream)))
+    outs = (_ptr(potentials), _ptr(spikes), _ptr(t_first), _ptr(v_first))
+    if stride is None:
+        n = spk_conv_fire_workspace_size(B, T, Cin, H, W, Cout, K, pad)
+        ws = _ws(workspace, n, dev)
+        fn = _lib.spk_conv_fire_first_spike if times else _lib.spk_conv_fire
+        _check(fn(_ptr(x), B, T, Cin, H, W, _ptr(weight), Cout, K, pad, float(threshold), *outs, _ptr(ws), n,
+                  _stream(stream)))
+    else:
+        n = spk_conv_fire_strided_workspace_size(B, T, Cin, H, W, Cout, K, stride, pad)
+        ws = _ws(workspace, n, dev)
+        fn = _lib.spk_conv_fire_first_spike_strided if times else _lib.spk_conv_fire_strided
+        _check(fn(_ptr(x), B, T, Cin, H, W, _ptr(weight), Cout, K, stride, pad, float(threshold), *outs, _ptr(ws),
+                  n, _stream(stream)))
     return potentials, spikes, t_first, v_first
+
+
+def spk_conv_fire(wave, weight, pad, threshold, potentials=None, spikes=None, t_first=None, v_first=None,
+                  workspace=None, stream=None):
+    """wave u8 [B,T,Cin,H,W], weight f32 [Cout,Cin,K,K] ->
+    (potentials f32 [B,T,Cout,Ho,Wo], spikes u8 [B,T,Cout,Ho,Wo], t_first u8 [B,Cout,Ho,Wo], v_first f32)."""
+    return _conv_call(wave, False, None, weight, None, pad, threshold, potentials, spikes, t_first, v_first,
+                      workspace, stream)
 
 
 def spk_conv_fire_first_spike(in_t_first, T, weight, pad, threshold, potentials=None, spikes=None, t_first=None,
                               v_first=None, workspace=None, stream=None):
     """As spk_conv_fire, with the input given by its first-spike map in_t_first u8 [B,Cin,H,W]
     (T = never; the wave it stands for is Eq.1 of it)."""
-    B, Cin, H, W = in_t_first.shape
-    Cout, Cin2, K, _ = weight.shape
-    _need(in_t_first, torch.uint8, (B, Cin, H, W), "in_t_first")
-    _need(weight, torch.float32, (Cout, Cin, K, K), "weight")
-    Ho, Wo = conv_out_size(H, K, pad), conv_out_size(W, K, pad)
-    dev = in_t_first.device
-    potentials = _out(potentials, (B, T, Cout, Ho, Wo), torch.float32, dev, "potentials")
-    spikes = _out(spikes, (B, T, Cout, Ho, Wo), torch.uint8, dev, "spikes")
-    t_first = _out(t_first, (B, Cout, Ho, Wo), torch.uint8, dev, "t_first")
-    v_first = _out(v_first, (B, Cout, Ho, Wo), torch.float32, dev, "v_first")
-    n = spk_conv_fire_workspace_size(B, T, Cin, H, W, Cout, K, pad)
-    ws = _ws(workspace, n, dev)
-    _check(_lib.spk_conv_fire_first_spike(_ptr(in_t_first), B, T, Cin, H, W, _ptr(weight), Cout, K, pad,
-                                          float(threshold), _ptr(potentials), _ptr(spikes), _ptr(t_first),
-                                          _ptr(v_first), _ptr(ws), n, _stream(stream)))
-    return potentials, spikes, t_first, v_first
+    return _conv_call(in_t_first, True, T, weight, None, pad, threshold, potentials, spikes, t_first, v_first,
+                      workspace, stream)
+
+
+def spk_conv_fire_strided(wave, weight, stride, pad, threshold, potentials=None, spikes=None, t_first=None,
+                          v_first=None, workspace=None, stream=None):
+    """spk_conv_fire with stride: output (y, x) reads the padded window at (y*stride, x*stride)."""
+    return _conv_call(wave, False, None, weight, int(stride), pad, threshold, potentials, spikes, t_first, v_first,
+                      workspace, stream)
+
+
+def spk_conv_fire_first_spike_strided(in_t_first, T, weight, stride, pad, threshold, potentials=None, spikes=None,
+                                      t_first=None, v_first=None, workspace=None, stream=None):
+    """spk_conv_fire_first_spike with stride."""
+    return _conv_call(in_t_first, True, T, weight, int(stride), pad, threshold, potentials, spikes, t_first, v_first,
+                      workspace, stream)
 
 
 def spk_conv_fire_first_spike_noalloc(in_t_first, T, weight, pad, threshold, potentials=None, spikes=None,
@@ -373,29 +408,48 @@ def spk_stdp_workspace_size(Cout, Cin, K, B, k) -> int:
     return int(_lib.spk_stdp_workspace_size(Cout, Cin, K, B, k))
 
 
+def _stdp_call(weight, stride, pad, pre_wave, winners, n_winners, reward, a_plus, a_minus, lb, ub, stabilizer,
+               workspace, stream):
+    Cout, Cin, K, B, T, H, W, k = _stdp_args(weight, pre_wave, winners, n_winners)
+    if reward is not None:
+        _need(reward, torch.int8, (B,), "reward")
+    n = spk_stdp_workspace_size(Cout, Cin, K, B, k)
+    ws = _ws(workspace, n, weight.device)
+    head = (_ptr(weight), Cout, Cin, K) + ((pad,) if stride is None else (stride, pad))
+    mid = (_ptr(pre_wave), B, T, H, W, _ptr(winners), _ptr(n_winners), k) + (() if reward is None else (_ptr(reward),))
+    tail = (float(a_plus), float(a_minus), float(lb), float(ub), int(bool(stabilizer)), _ptr(ws), n, _stream(stream))
+    fn = {(False, False): _lib.spk_stdp, (True, False): _lib.spk_rstdp, (False, True): _lib.spk_stdp_strided,
+          (True, True): _lib.spk_rstdp_strided}[(reward is not None, stride is not None)]
+    _check(fn(*head, *mid, *tail))
+    return weight
+
+
 def spk_stdp(weight, pad, pre_wave, winners, n_winners, a_plus, a_minus, lb=0.0, ub=1.0, stabilizer=True,
              workspace=None, stream=None):
     """Eq.4 on the winners' weights (in place on `weight`), ordered replay over images."""
-    Cout, Cin, K, B, T, H, W, k = _stdp_args(weight, pre_wave, winners, n_winners)
-    n = spk_stdp_workspace_size(Cout, Cin, K, B, k)
-    ws = _ws(workspace, n, weight.device)
-    _check(_lib.spk_stdp(_ptr(weight), Cout, Cin, K, pad, _ptr(pre_wave), B, T, H, W, _ptr(winners),
-                         _ptr(n_winners), k, float(a_plus), float(a_minus), float(lb), float(ub), int(bool(stabilizer)),
-                         _ptr(ws), n, _stream(stream)))
-    return weight
+    return _stdp_call(weight, None, pad, pre_wave, winners, n_winners, None, a_plus, a_minus, lb, ub, stabilizer,
+                      workspace, stream)
 
 
 def spk_rstdp(weight, pad, pre_wave, winners, n_winners, reward, a_plus, a_minus, lb=0.0, ub=1.0, stabilizer=True,
               workspace=None, stream=None):
     """R-STDP: reward i8 [B] in {+1,-1,0} selects STDP, anti-STDP or nothing per image."""
-    Cout, Cin, K, B, T, H, W, k = _stdp_args(weight, pre_wave, winners, n_winners)
-    _need(reward, torch.int8, (B,), "reward")
-    n = spk_stdp_workspace_size(Cout, Cin, K, B, k)
-    ws = _ws(workspace, n, weight.device)
-    _check(_lib.spk_rstdp(_ptr(weight), Cout, Cin, K, pad, _ptr(pre_wave), B, T, H, W, _ptr(winners),
-                          _ptr(n_winners), k, _ptr(reward), float(a_plus), float(a_minus), float(lb), float(ub),
-                          int(bool(stabilizer)), _ptr(ws), n, _stream(stream)))
-    return weight
+    return _stdp_call(weight, None, pad, pre_wave, winners, n_winners, reward, a_plus, a_minus, lb, ub, stabilizer,
+                      workspace, stream)
+
+
+def spk_stdp_strided(weight, stride, pad, pre_wave, winners, n_winners, a_plus, a_minus, lb=0.0, ub=1.0,
+                     stabilizer=True, workspace=None, stream=None):
+    """spk_stdp of a layer with stride (winner (y, x) sees the input window at (y*stride, x*stride))."""
+    return _stdp_call(weight, int(stride), pad, pre_wave, winners, n_winners, None, a_plus, a_minus, lb, ub,
+                      stabilizer, workspace, stream)
+
+
+def spk_rstdp_strided(weight, stride, pad, pre_wave, winners, n_winners, reward, a_plus, a_minus, lb=0.0, ub=1.0,
+                      stabilizer=True, workspace=None, stream=None):
+    """spk_rstdp of a layer with stride."""
+    return _stdp_call(weight, int(stride), pad, pre_wave, winners, n_winners, reward, a_plus, a_minus, lb, ub,
+                      stabilizer, workspace, stream)
 
 
 def spk_decide(winners, n_winners, labels, n_classes=10, decision=None, reward=None, stream=None):
@@ -417,6 +471,16 @@ def spk_count_events(wave, Cout, K, pad, count=None, stream=None):
     _need(wave, torch.uint8, (B, T, Cin, H, W), "wave")
     count = _out(count, (1,), torch.int64, wave.device, "count")
     _check(_lib.spk_count_events(_ptr(wave), B, T, Cin, H, W, Cout, K, pad, _ptr(count), _stream(stream)))
+    return count
+
+
+def spk_count_events_strided(wave, Cout, K, stride, pad, count=None, stream=None):
+    """spk_count_events of a conv with stride."""
+    B, T, Cin, H, W = wave.shape
+    _need(wave, torch.uint8, (B, T, Cin, H, W), "wave")
+    count = _out(count, (1,), torch.int64, wave.device, "count")
+    _check(_lib.spk_count_events_strided(_ptr(wave), B, T, Cin, H, W, Cout, K, int(stride), pad, _ptr(count),
+                                         _stream(stream)))
     return count
 
 

@@ -61,6 +61,7 @@ constexpr int NTILE_ALIGN = 4;  // the N tiles (16 features) are padded to a mul
 
 struct ConvGeom {
     int B, T, Cin, H, W, Cout, K, pad;
+    int S;           // stride: output (y, x) reads the padded window at (y*S, x*S)
     int CP;          // channels per tpad cell (Cin rounded up)
     int Hp, Wp, Ho, Wo, HoWo;
     int ksteps;      // ceil(K*K*CP / 32)
@@ -515,8 +516,8 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         task_range(task, p0, np);
         const int pa = p0, pb = p0 + np - 1;
         const int ba = pa / g.HoWo, bb = pb / g.HoWo;
-        row0 = ba * g.Hp + (pa - ba * g.HoWo) / g.Wo;
-        const int row1 = bb * g.Hp + (pb - bb * g.HoWo) / g.Wo + g.K - 1;
+        row0 = ba * g.Hp + (pa - ba * g.HoWo) / g.Wo * g.S;
+        const int row1 = bb * g.Hp + (pb - bb * g.HoWo) / g.Wo * g.S + g.K - 1;
         w0 = (int)(((int64_t)row0 * row_bytes) >> 2);
         nw = (row1 - row0 + 1) * row_bytes / 4;
     };
@@ -626,8 +627,8 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             for (int i = 0; i < FIN_MT; ++i) {
                 const int gp = min(pos0 + tl[i] * 16 + c, pos0 + np - 1);
                 const int b = gp / g.HoWo, pos = gp - b * g.HoWo;
-                const int y = pos / g.Wo, xx = pos - y * g.Wo;
-                const int row = b * g.Hp + y;
+                const int y = pos / g.Wo, xx = (pos - y * g.Wo) * g.S;  // the window's padded column
+                const int row = b * g.Hp + y * g.S;
                 abase[i] = tpad + (uint32_t)(((int64_t)row * g.Wp + xx) * g.CP);
                 alds[i] = (uint32_t)((row - row0_t) * row_bytes + xx * 8);
             }
@@ -995,7 +996,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             const int mt = v ? (int)(gm % g.mt_per_img) : 0;
             const int pos = min(mt * 16 + c, g.HoWo - 1);  // rows past the image are computed, not stored
             const int y = pos / g.Wo, xx = pos % g.Wo;
-            abase[i] = tpad + (uint32_t)(((b * g.Hp + y) * g.Wp + xx) * g.CP);
+            abase[i] = tpad + (uint32_t)(((b * g.Hp + y * g.S) * g.Wp + xx * g.S) * g.CP);
             img[i] = v ? b : -1;
             mpos0[i] = mt * 16 + gq * 4;
         }
@@ -1192,22 +1193,23 @@ struct ConvPlan {
     size_t part_count;  // floats of its partial sums
 };
 
-int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int pad, ConvPlan &pl) {
-    SPK_REQUIRE(B >= 0 && T >= 1 && Cin >= 1 && H >= 1 && W >= 1 && Cout >= 1 && K >= 1 && pad >= 0,
-                SPK_E_SHAPE, "spk_conv_fire: bad sizes B=%d T=%d Cin=%d H=%d W=%d Cout=%d K=%d pad=%d",
-                B, T, Cin, H, W, Cout, K, pad);
+int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int stride, int pad, ConvPlan &pl) {
+    SPK_REQUIRE(B >= 0 && T >= 1 && Cin >= 1 && H >= 1 && W >= 1 && Cout >= 1 && K >= 1 && pad >= 0 && stride >= 1,
+                SPK_E_SHAPE, "spk_conv_fire: bad sizes B=%d T=%d Cin=%d H=%d W=%d Cout=%d K=%d stride=%d pad=%d",
+                B, T, Cin, H, W, Cout, K, stride, pad);
+    SPK_REQUIRE(stride <= 64, SPK_E_RANGE, "spk_conv_fire: stride=%d > 64", stride);
     SPK_REQUIRE(T <= 255, SPK_E_RANGE, "spk_conv_fire: T=%d > 255", T);
     SPK_REQUIRE(Cin <= 4096 && K <= 64 && pad <= 64 && H <= 65536 && W <= 65536, SPK_E_RANGE,
                 "spk_conv_fire: Cin, K, pad or the image too large");
     ConvGeom &g = pl.g;
-    g.B = B; g.T = T; g.Cin = Cin; g.H = H; g.W = W; g.Cout = Cout; g.K = K; g.pad = pad;
+    g.B = B; g.T = T; g.Cin = Cin; g.H = H; g.W = W; g.Cout = Cout; g.K = K; g.pad = pad; g.S = stride;
     g.CP = Cin <= 4 ? 4 : (Cin + 7) / 8 * 8;
     g.Hp = H + 2 * pad;
     g.Wp = W + 2 * pad;
-    g.Ho = g.Hp - K + 1;
-    g.Wo = g.Wp - K + 1;
-    SPK_REQUIRE(g.Ho >= 1 && g.Wo >= 1, SPK_E_SHAPE, "spk_conv_fire: kernel %d larger than padded input %dx%d",
+    SPK_REQUIRE(g.Hp >= K && g.Wp >= K, SPK_E_SHAPE, "spk_conv_fire: kernel %d larger than padded input %dx%d",
                 K, g.Hp, g.Wp);
+    g.Ho = (g.Hp - K) / stride + 1;  // Eq.2 with stride: floor((H + 2 pad - K) / stride) + 1
+    g.Wo = (g.Wp - K) / stride + 1;
     SPK_REQUIRE((int64_t)K * K * g.CP <= 16384, SPK_E_RANGE,
                 "spk_conv_fire: K*K*Cin (Cin rounded up to %d) = %lld > 16384", g.CP, (long long)K * K * g.CP);
     SPK_REQUIRE(Cout <= 4096, SPK_E_RANGE, "spk_conv_fire: Cout=%d > 4096", Cout);
@@ -1300,17 +1302,24 @@ void launch_inf(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const
 
 extern "C" size_t spk_conv_fire_workspace_size(int B, int T, int Cin, int H, int W, int Cout, int K, int pad) {
     ConvPlan pl;
-    if (make_plan(B, T, Cin, H, W, Cout, K, pad, pl) != SPK_OK) return 0;
+    if (make_plan(B, T, Cin, H, W, Cout, K, 1, pad, pl) != SPK_OK) return 0;
+    return plan_workspace(pl);
+}
+
+extern "C" size_t spk_conv_fire_strided_workspace_size(int B, int T, int Cin, int H, int W, int Cout, int K,
+                                                       int stride, int pad) {
+    ConvPlan pl;
+    if (make_plan(B, T, Cin, H, W, Cout, K, stride, pad, pl) != SPK_OK) return 0;
     return plan_workspace(pl);
 }
 
 namespace {
 // The conv call on either input form (times: in = first-spike map, else the wave).
 int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int W, const float *weight, int Cout,
-              int K, int pad, float threshold, float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
-              void *workspace, size_t ws_bytes, void *stream) {
+              int K, int stride, int pad, float threshold, float *potentials, uint8_t *spikes, uint8_t *t_first,
+              float *v_first, void *workspace, size_t ws_bytes, void *stream) {
     ConvPlan pl;
-    int rc = make_plan(B, T, Cin, H, W, Cout, K, pad, pl);
+    int rc = make_plan(B, T, Cin, H, W, Cout, K, stride, pad, pl);
     if (rc != SPK_OK) return rc;
     SPK_REQUIRE(!std::isnan(threshold) && !(std::isinf(threshold) && threshold < 0), SPK_E_ARG,
                 "spk_conv_fire: threshold must be a number or +INFINITY");
@@ -1371,20 +1380,21 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     auto chunk_rows = [&](int64_t p0) {
         const int64_t pb = std::min(p0 + np_max, npos) - 1;
         const int64_t ba = p0 / g.HoWo, bb = pb / g.HoWo;
-        return (int)((bb * g.Hp + (pb - bb * g.HoWo) / g.Wo + K) - (ba * g.Hp + (p0 - ba * g.HoWo) / g.Wo));
+        return (int)((bb * g.Hp + (pb - bb * g.HoWo) / g.Wo * stride + K) -
+                     (ba * g.Hp + (p0 - ba * g.HoWo) / g.Wo * stride));
     };
     const int64_t period = g.HoWo / std::gcd((int64_t)g.HoWo, (int64_t)np_max);
     int a_rows = 0;
     if (!flat) {
         for (int ch = 0; ch < cpi; ++ch) {
             const int p0 = ch * np_max, np = std::min(np_max, g.HoWo - p0);
-            a_rows = std::max(a_rows, (p0 + np - 1) / g.Wo + K - p0 / g.Wo);
+            a_rows = std::max(a_rows, ((p0 + np - 1) / g.Wo - p0 / g.Wo) * stride + K);
         }
     } else if (period <= 65536) {
         for (int64_t ch = 0; ch < std::min<int64_t>(n_chunks, period); ++ch)
             a_rows = std::max(a_rows, chunk_rows(ch * np_max));
     } else {  // HoWo > 65536 > np_max: a chunk touches at most two images
-        a_rows = (np_max + g.Wo - 1) / g.Wo + 2 * g.Hp;
+        a_rows = (np_max + g.Wo - 1) / g.Wo * stride + 2 * g.Hp + K;
     }
     // staged spike rows: CP >= 8 (8-byte reads of one channel group), buffers rounded to 64 words
     const int a_words = (int)spk::align_up((size_t)a_rows * g.Wp * g.CP / 4, 64);
@@ -1449,7 +1459,7 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
 extern "C" int spk_conv_fire(const uint8_t *wave, int B, int T, int Cin, int H, int W, const float *weight,
                              int Cout, int K, int pad, float threshold, float *potentials, uint8_t *spikes,
                              uint8_t *t_first, float *v_first, void *workspace, size_t ws_bytes, void *stream) {
-    return conv_fire(wave, false, B, T, Cin, H, W, weight, Cout, K, pad, threshold, potentials, spikes, t_first,
+    return conv_fire(wave, false, B, T, Cin, H, W, weight, Cout, K, 1, pad, threshold, potentials, spikes, t_first,
                      v_first, workspace, ws_bytes, stream);
 }
 
@@ -1457,7 +1467,24 @@ extern "C" int spk_conv_fire_first_spike(const uint8_t *in_t_first, int B, int T
                                          const float *weight, int Cout, int K, int pad, float threshold,
                                          float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
                                          void *workspace, size_t ws_bytes, void *stream) {
-    return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, pad, threshold, potentials, spikes,
+    return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, 1, pad, threshold, potentials, spikes,
+                     t_first, v_first, workspace, ws_bytes, stream);
+}
+
+extern "C" int spk_conv_fire_strided(const uint8_t *wave, int B, int T, int Cin, int H, int W, const float *weight,
+                                     int Cout, int K, int stride, int pad, float threshold, float *potentials,
+                                     uint8_t *spikes, uint8_t *t_first, float *v_first, void *workspace,
+                                     size_t ws_bytes, void *stream) {
+    return conv_fire(wave, false, B, T, Cin, H, W, weight, Cout, K, stride, pad, threshold, potentials, spikes,
+                     t_first, v_first, workspace, ws_bytes, stream);
+}
+
+extern "C" int spk_conv_fire_first_spike_strided(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+                                                 const float *weight, int Cout, int K, int stride, int pad,
+                                                 float threshold, float *potentials, uint8_t *spikes,
+                                                 uint8_t *t_first, float *v_first, void *workspace, size_t ws_bytes,
+                                                 void *stream) {
+    return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, stride, pad, threshold, potentials, spikes,
                      t_first, v_first, workspace, ws_bytes, stream);
 }
 
@@ -1500,18 +1527,18 @@ extern "C" int spk_conv_fire_first_spike_noalloc(const uint8_t *in_t_first, int 
                                                  float *potentials, uint8_t *spikes, uint8_t *t_first,
                                                  float *v_first, void *stream) {
     ConvPlan pl;
-    int rc = make_plan(B, T, Cin, H, W, Cout, K, pad, pl);
+    int rc = make_plan(B, T, Cin, H, W, Cout, K, 1, pad, pl);
     if (rc != SPK_OK) return rc;
     const size_t need = plan_workspace(pl);
     SPK_REQUIRE(need <= SPK_NOALLOC_SCRATCH_BYTES, SPK_E_RANGE,
                 "spk_conv_fire_first_spike_noalloc: the call needs %zu bytes of scratch, the static scratch holds %zu "
                 "(use spk_conv_fire_first_spike with a workspace)",
                 need, SPK_NOALLOC_SCRATCH_BYTES);
-    if (B == 0) return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, pad, threshold, potentials,
+    if (B == 0) return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, 1, pad, threshold, potentials,
                                  spikes, t_first, v_first, nullptr, 0, stream);
     void *ws = nullptr;
     rc = current_scratch(&ws);
     if (rc != SPK_OK) return rc;
-    return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, pad, threshold, potentials, spikes, t_first,
-                     v_first, ws, SPK_NOALLOC_SCRATCH_BYTES, stream);
+    return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, 1, pad, threshold, potentials, spikes,
+                     t_first, v_first, ws, SPK_NOALLOC_SCRATCH_BYTES, stream);
 }

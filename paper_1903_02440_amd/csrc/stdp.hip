@@ -28,7 +28,7 @@ namespace {
 constexpr int LIST_THREADS = 1024;  // images scanned per pass of the list kernel
 
 struct StdpArgs {
-    int Cout, Cin, K, pad, B, T, H, W, k, stabilizer;
+    int Cout, Cin, K, pad, stride, B, T, H, W, k, stabilizer;
     float a_plus, a_minus, lb, ub;
 };
 
@@ -130,8 +130,9 @@ __global__ __launch_bounds__(1024) void k_stdp_offsets(int Cout, StdpWork w) {
 // 3. Grid (chunk of 256 weights, bit row).  Row r belongs to the feature f
 // with woff[f] <= r < woff[f+1] (binary search); its thread for weight
 // e = (ci, ky, kx) loads the pre-synaptic byte of each of the row's up to 32
-// updates -- the layer input at (image, winner step, ci, y+ky-pad, x+kx-pad),
-// 0 in the padding -- with independent loads and packs the 32 bits.
+// updates -- the layer input at (image, winner step, ci, y*s+ky-pad,
+// x*s+kx-pad) for the layer's stride s, 0 in the padding -- with independent
+// loads and packs the 32 bits.
 __global__ __launch_bounds__(256) void k_stdp_bits(const uint8_t *__restrict__ pre, StdpArgs a, StdpWork w) {
     const int r = blockIdx.y;
     if (r >= w.woff[a.Cout]) return;  // uniform
@@ -159,7 +160,7 @@ __global__ __launch_bounds__(256) void k_stdp_bits(const uint8_t *__restrict__ p
         v[q] = 0;
         if (q < cnt) {
             const int4 u = lst[q];
-            const int iy = u.z + ky - a.pad, ix = u.w + kx - a.pad;
+            const int iy = u.z * a.stride + ky - a.pad, ix = u.w * a.stride + kx - a.pad;
             if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
                 v[q] = pre[((int64_t)u.x * a.T + u.y) * plane + cioff + (int64_t)iy * a.W + ix];
         }
@@ -253,7 +254,7 @@ __global__ __launch_bounds__(256) void k_stdp_single(float *__restrict__ weight,
     const int e = blockIdx.x * 256 + threadIdx.x;
     if (e >= Kc) return;
     const int ci = e / KK, ky = (e % KK) / a.K, kx = e % a.K;
-    const int iy = winners[4 * j + 2] + ky - a.pad, ix = winners[4 * j + 3] + kx - a.pad;
+    const int iy = winners[4 * j + 2] * a.stride + ky - a.pad, ix = winners[4 * j + 3] * a.stride + kx - a.pad;
     uint8_t v = 0;
     if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
         v = pre[((int64_t)t * a.Cin + ci) * a.H * a.W + (int64_t)iy * a.W + ix];
@@ -278,12 +279,14 @@ __global__ __launch_bounds__(256) void k_decide(const int32_t *__restrict__ winn
     reward[b] = (int8_t)(d == labels[b] ? 1 : -1);
 }
 
-int stdp_common(float *weight, int Cout, int Cin, int K, int pad, const uint8_t *pre_wave, int B, int T, int H,
-                int W, const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward, float a_plus,
-                float a_minus, float lb, float ub, int stabilizer, void *workspace, size_t ws_bytes, void *stream,
-                const char *name) {
-    SPK_REQUIRE(Cout >= 1 && Cin >= 1 && K >= 1 && pad >= 0 && B >= 0 && T >= 1 && H >= 1 && W >= 1 && k >= 1,
+int stdp_common(float *weight, int Cout, int Cin, int K, int stride, int pad, const uint8_t *pre_wave, int B, int T,
+                int H, int W, const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward,
+                float a_plus, float a_minus, float lb, float ub, int stabilizer, void *workspace, size_t ws_bytes,
+                void *stream, const char *name) {
+    SPK_REQUIRE(Cout >= 1 && Cin >= 1 && K >= 1 && pad >= 0 && stride >= 1 && B >= 0 && T >= 1 && H >= 1 &&
+                    W >= 1 && k >= 1,
                 SPK_E_SHAPE, "%s: bad sizes", name);
+    SPK_REQUIRE(stride <= 64, SPK_E_RANGE, "%s: stride=%d > 64", name, stride);
     SPK_REQUIRE(T <= 255, SPK_E_RANGE, "%s: T=%d > 255", name, T);
     SPK_REQUIRE(Cout <= 65535 && (int64_t)Cout * B < (1LL << 31), SPK_E_RANGE, "%s: Cout*B too large", name);
     SPK_REQUIRE((int64_t)Cin * K * K <= 65535LL * 256 && bit_rows(Cout, B, k) <= 65535 &&
@@ -300,7 +303,7 @@ int stdp_common(float *weight, int Cout, int Cin, int K, int pad, const uint8_t 
     SPK_REQUIRE(workspace && ws_bytes >= need, SPK_E_WORKSPACE, "%s: workspace of %zu bytes < %zu required", name,
                 ws_bytes, need);
     StdpWork wk = carve(workspace, Cout, Cin, K, B, k, nullptr);
-    StdpArgs a{Cout, Cin, K, pad, B, T, H, W, k, stabilizer, a_plus, a_minus, lb, ub};
+    StdpArgs a{Cout, Cin, K, pad, stride, B, T, H, W, k, stabilizer, a_plus, a_minus, lb, ub};
     hipStream_t st = spk::as_stream(stream);
     const unsigned wchunks = (unsigned)spk::ceil_div((int64_t)Cin * K * K, 256);
     // the clamp can be dropped after the first update (see k_stdp_apply)
@@ -338,7 +341,7 @@ extern "C" int spk_stdp(float *weight, int Cout, int Cin, int K, int pad, const 
                         int H, int W, const int32_t *winners, const int32_t *n_winners, int k, float a_plus,
                         float a_minus, float lb, float ub, int stabilizer, void *workspace, size_t ws_bytes,
                         void *stream) {
-    return stdp_common(weight, Cout, Cin, K, pad, pre_wave, B, T, H, W, winners, n_winners, k, nullptr, a_plus,
+    return stdp_common(weight, Cout, Cin, K, 1, pad, pre_wave, B, T, H, W, winners, n_winners, k, nullptr, a_plus,
                        a_minus, lb, ub, stabilizer, workspace, ws_bytes, stream, "spk_stdp");
 }
 
@@ -347,8 +350,25 @@ extern "C" int spk_rstdp(float *weight, int Cout, int Cin, int K, int pad, const
                          float a_plus, float a_minus, float lb, float ub, int stabilizer, void *workspace,
                          size_t ws_bytes, void *stream) {
     SPK_REQUIRE(reward || B == 0, SPK_E_ARG, "spk_rstdp: reward is required");
-    return stdp_common(weight, Cout, Cin, K, pad, pre_wave, B, T, H, W, winners, n_winners, k, reward, a_plus,
+    return stdp_common(weight, Cout, Cin, K, 1, pad, pre_wave, B, T, H, W, winners, n_winners, k, reward, a_plus,
                        a_minus, lb, ub, stabilizer, workspace, ws_bytes, stream, "spk_rstdp");
+}
+
+extern "C" int spk_stdp_strided(float *weight, int Cout, int Cin, int K, int stride, int pad, const uint8_t *pre_wave,
+                                int B, int T, int H, int W, const int32_t *winners, const int32_t *n_winners, int k,
+                                float a_plus, float a_minus, float lb, float ub, int stabilizer, void *workspace,
+                                size_t ws_bytes, void *stream) {
+    return stdp_common(weight, Cout, Cin, K, stride, pad, pre_wave, B, T, H, W, winners, n_winners, k, nullptr,
+                       a_plus, a_minus, lb, ub, stabilizer, workspace, ws_bytes, stream, "spk_stdp_strided");
+}
+
+extern "C" int spk_rstdp_strided(float *weight, int Cout, int Cin, int K, int stride, int pad,
+                                 const uint8_t *pre_wave, int B, int T, int H, int W, const int32_t *winners,
+                                 const int32_t *n_winners, int k, const int8_t *reward, float a_plus, float a_minus,
+                                 float lb, float ub, int stabilizer, void *workspace, size_t ws_bytes, void *stream) {
+    SPK_REQUIRE(reward || B == 0, SPK_E_ARG, "spk_rstdp_strided: reward is required");
+    return stdp_common(weight, Cout, Cin, K, stride, pad, pre_wave, B, T, H, W, winners, n_winners, k, reward,
+                       a_plus, a_minus, lb, ub, stabilizer, workspace, ws_bytes, stream, "spk_rstdp_strided");
 }
 
 extern "C" int spk_decide(const int32_t *winners, const int32_t *n_winners, int B, int k, const int32_t *labels,

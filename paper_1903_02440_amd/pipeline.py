@@ -29,16 +29,19 @@ calls on one stream, with no host synchronisation and no allocation inside
 
 A stage list is any sequence of objects with the attributes of
 ``Conv(cin, cout, K, pad, thr, k, r, learn, a_plus, a_minus, lb, ub,
-stabilizer)`` and ``Pool(P, R, D)``.
+stabilizer)`` (and optionally ``stride``, default 1: a strided stage calls
+the ``*_strided`` entry points) and ``Pool(P, R, D)``.
 """
 from __future__ import annotations
 
+import copy
 import math
 
 import torch
 
 from . import (pool_out_size, conv_out_size, spk_conv_fire, spk_conv_fire_first_spike, spk_conv_fire_workspace_size,
-               spk_decide,
+               spk_conv_fire_strided, spk_conv_fire_first_spike_strided, spk_conv_fire_strided_workspace_size,
+               spk_rstdp_strided, spk_stdp_strided, spk_decide,
                spk_encode_latency, spk_encode_latency_workspace_size, spk_kwta, spk_kwta_workspace_size,
                spk_local_normalization, spk_pool, spk_pool_first_spike, spk_rank_latency, spk_rstdp, spk_stdp,
                spk_stdp_workspace_size)
@@ -48,11 +51,15 @@ def _is_conv(st):
     return hasattr(st, "cout")
 
 
+def _stride(st):
+    return getattr(st, "stride", 1)
+
+
 class Chain:
     def __init__(self, stages, B, T, H, W, cin, source="image", filter_bank=None, filter_threshold=0.0,
                  n_classes=10, device="cuda", want_potentials=True, pool_from_first_spike=True,
                  concurrent_learn=True, want_spikes=True, local_norm=None):
-        self.stages = list(stages)
+        self.stages = [copy.copy(st) for st in stages]  # own copies: set_rates changes them
         self.pool_from_first_spike = pool_from_first_spike
         self.B, self.T, self.source = B, T, source
         self.n_classes = n_classes
@@ -82,7 +89,7 @@ class Chain:
             b = {}
             if _is_conv(st):
                 assert st.cin == c, "stage input channels do not match"
-                ho, wo = conv_out_size(h, st.K, st.pad), conv_out_size(w, st.K, st.pad)
+                ho, wo = conv_out_size(h, st.K, st.pad, _stride(st)), conv_out_size(w, st.K, st.pad, _stride(st))
                 b["P"] = torch.empty((B, T, st.cout, ho, wo), dtype=f32, device=dev) if want_potentials else False
                 # without want_spikes a conv stage's per-step spikes are written only when the next
                 # stage reads them (a conv, or a pool on waves); the first-spike map always is
@@ -100,7 +107,9 @@ class Chain:
                                              dtype=u8, device=dev) if st.learn is not None else None)
                 b["ws_kwta"] = (torch.empty(max(256, spk_kwta_workspace_size(B, st.cout, ho, wo)), dtype=u8,
                                             device=dev) if st.learn is not None else None)
-                ws_bytes = max(ws_bytes, spk_conv_fire_workspace_size(B, T, st.cin, h, w, st.cout, st.K, st.pad),
+                ws_bytes = max(ws_bytes,
+                               spk_conv_fire_strided_workspace_size(B, T, st.cin, h, w, st.cout, st.K, _stride(st),
+                                                                    st.pad),
                                spk_kwta_workspace_size(B, st.cout, ho, wo))
                 c, h, w = st.cout, ho, wo
             else:
@@ -148,6 +157,17 @@ class Chain:
     def weights(self):
         return [self.bufs[i]["weight"] for i in self.conv_stages()]
 
+    def set_rates(self, layer, a_plus, a_minus):
+        """Learning rates of conv layer `layer` (0-based among the conv stages)
+        for the steps enqueued from now on: a schedule (the tutorial's adaptive
+        or multiplied rates) is a sequence of such calls between steps."""
+        st = self.stages[self.conv_stages()[layer]]
+        st.a_plus, st.a_minus = float(a_plus), float(a_minus)
+
+    def rates(self, layer):
+        st = self.stages[self.conv_stages()[layer]]
+        return st.a_plus, st.a_minus
+
     def set_input(self, image=None, wave=None, labels=None):
         if image is not None:
             self.image.copy_(image)
@@ -185,13 +205,17 @@ class Chain:
             self.pre_waves[i] = x
             if _is_conv(st):
                 mark(f"conv{i}", 0)
-                if x_exact:
-                    spk_conv_fire_first_spike(x_tf, self.T, b["weight"], st.pad, st.thr, potentials=b["P"],
-                                              spikes=b["S"], t_first=b["tf"], v_first=b["vf"],
-                                              workspace=self.workspace, stream=stream)
+                outs = dict(potentials=b["P"], spikes=b["S"], t_first=b["tf"], v_first=b["vf"],
+                            workspace=self.workspace, stream=stream)
+                s = _stride(st)
+                if x_exact and s == 1:
+                    spk_conv_fire_first_spike(x_tf, self.T, b["weight"], st.pad, st.thr, **outs)
+                elif x_exact:
+                    spk_conv_fire_first_spike_strided(x_tf, self.T, b["weight"], s, st.pad, st.thr, **outs)
+                elif s == 1:
+                    spk_conv_fire(x, b["weight"], st.pad, st.thr, **outs)
                 else:
-                    spk_conv_fire(x, b["weight"], st.pad, st.thr, potentials=b["P"], spikes=b["S"], t_first=b["tf"],
-                                  v_first=b["vf"], workspace=self.workspace, stream=stream)
+                    spk_conv_fire_strided(x, b["weight"], s, st.pad, st.thr, **outs)
                 mark(f"conv{i}", 1)
                 if early_learn and i in self._side_kwta:
                     side = self._side[self._side_kwta[i]]
@@ -234,12 +258,18 @@ class Chain:
                 if _is_conv(st) and st.learn is not None]
 
     def _apply(self, i, st, b, s):
-        if st.learn == "rstdp":
-            spk_rstdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], self.reward, st.a_plus,
-                      st.a_minus, st.lb, st.ub, st.stabilizer, workspace=b["ws_learn"], stream=s)
+        common = (self.pre_waves[i], b["win"], b["nw"])
+        rates = (st.a_plus, st.a_minus, st.lb, st.ub, st.stabilizer)
+        kw = dict(workspace=b["ws_learn"], stream=s)
+        stride = _stride(st)
+        if st.learn == "rstdp" and stride == 1:
+            spk_rstdp(b["weight"], st.pad, *common, self.reward, *rates, **kw)
+        elif st.learn == "rstdp":
+            spk_rstdp_strided(b["weight"], stride, st.pad, *common, self.reward, *rates, **kw)
+        elif stride == 1:
+            spk_stdp(b["weight"], st.pad, *common, *rates, **kw)
         else:
-            spk_stdp(b["weight"], st.pad, self.pre_waves[i], b["win"], b["nw"], st.a_plus, st.a_minus, st.lb,
-                     st.ub, st.stabilizer, workspace=b["ws_learn"], stream=s)
+            spk_stdp_strided(b["weight"], stride, st.pad, *common, *rates, **kw)
 
     def _launch_learners(self, which, fork, stream):
         """Enqueue, each on its side stream forked from the caller's stream at
@@ -346,6 +376,12 @@ class OnlineTrainer:
 
     def set_weights(self, weights):
         self.chain.set_weights(weights)
+
+    def set_rates(self, layer, a_plus, a_minus):
+        """Rates of conv layer `layer` for the images run from now on; a captured
+        graph holds the old rates as kernel arguments, so it is captured again."""
+        self.chain.set_rates(layer, a_plus, a_minus)
+        self.graph = None
 
     def weights(self):
         return self.chain.weights()

@@ -177,6 +177,7 @@ class Conv:
     lb: float = 0.0
     ub: float = 1.0
     stabilizer: bool = True
+    stride: int = 1
 
 
 @dataclass

@@ -22,7 +22,7 @@ def declared():
 
 def test_every_declared_symbol_is_exported():
     names = declared()
-    assert len(names) == 24
+    assert len(names) == 30
     lib = spk.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -145,3 +145,29 @@ def test_conv_noalloc_rejects_beyond_its_scratch():
     assert rc == spk.SPK_E_RANGE and b"static scratch" in lib.spk_last_error()
     assert spk.spk_conv_fire_workspace_size(16, 64, 64, 256, 256, 256, 5, 2) > (64 << 20)
     assert spk.spk_conv_fire_workspace_size(1000, 15, 30, 14, 14, 250, 3, 1) <= (64 << 20)
+
+
+def test_strided_entry_points_validate_and_size():
+    lib = spk.lib()
+    f = lib.spk_conv_fire_strided
+    # stride 0, stride above 64, a kernel larger than the padded input: rejected before any HIP call
+    assert f(DUMMY, 1, 15, 6, 28, 28, DUMMY, 30, 5, 0, 2, 15.0, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, 1 << 30,
+             None) == spk.SPK_E_SHAPE
+    assert f(DUMMY, 1, 15, 6, 28, 28, DUMMY, 30, 5, 65, 2, 15.0, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, 1 << 30,
+             None) == spk.SPK_E_RANGE
+    assert lib.spk_conv_fire_first_spike_strided(DUMMY, 1, 15, 6, 3, 3, DUMMY, 30, 9, 2, 2, 15.0, DUMMY, DUMMY,
+                                                 DUMMY, DUMMY, DUMMY, 1 << 30, None) == spk.SPK_E_SHAPE
+    assert f(None, 0, 15, 6, 28, 28, None, 30, 5, 2, 2, 15.0, None, None, None, None, None, 0, None) == spk.SPK_OK
+    # the workspace of a strided call; stride 1 is the plain call's
+    assert spk.spk_conv_fire_strided_workspace_size(8, 15, 6, 28, 28, 30, 5, 1, 2) == \
+        spk.spk_conv_fire_workspace_size(8, 15, 6, 28, 28, 30, 5, 2)
+    assert spk.spk_conv_fire_strided_workspace_size(8, 15, 6, 28, 28, 30, 5, 2, 2) > 0
+    assert spk.spk_conv_fire_strided_workspace_size(8, 15, 6, 28, 28, 30, 5, 0, 2) == 0
+    assert spk.conv_out_size(28, 5, 2, 2) == 14 and spk.conv_out_size(13, 7, 3, 4) == 4
+    ws = spk.spk_stdp_workspace_size(4, 2, 3, 1, 1)
+    assert lib.spk_stdp_strided(DUMMY, 4, 2, 3, 0, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, 0.004, -0.003, 0.0, 1.0,
+                                1, DUMMY, ws, None) == spk.SPK_E_SHAPE
+    assert lib.spk_rstdp_strided(DUMMY, 4, 2, 3, 2, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, None, 0.004, -0.003,
+                                 0.0, 1.0, 1, DUMMY, ws, None) == spk.SPK_E_ARG
+    assert lib.spk_count_events_strided(DUMMY, 1, 15, 2, 8, 8, 4, 3, 0, 1, DUMMY, None) == spk.SPK_E_SHAPE
+
