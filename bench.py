@@ -42,14 +42,17 @@ def conv_call_bytes(B, T, cin, h, w, st, from_times, write_p=True, write_s=True)
             + B * T * st.cout * ho * wo * (4 * write_p + write_s) + B * st.cout * ho * wo * 5), ho, wo
 
 
-def step_bytes(wl, compact=False):
+def step_bytes(wl, compact=False, fused=()):
     """Algorithmic bytes of every call of one step, by call name (compact: the
-    chain writes no potentials, and per-step spikes only where a stage reads them)."""
+    chain writes no potentials, per-step spikes only where a stage reads them,
+    and no Eq.1 wave of the encoder or a pool, only their first-spike maps;
+    fused: the conv stages whose pooling runs in their own launch, which then
+    also writes the pooled wave and first-spike map, with no pooling call)."""
     B, T = wl.B, wl.T
     out = {}
     c, h, w = (6 if wl.bank == "dog" else 4) if wl.source == "image" else wl.cin, wl.H, wl.W
     if wl.source == "image":
-        out["encode"] = B * h * w + B * T * c * h * w + B * c * h * w
+        out["encode"] = B * h * w + (0 if compact else B * T * c * h * w) + B * c * h * w
     exact = wl.source == "image"  # the chain feeds a conv the first-spike map of an Eq.1 wave
     for i, st in enumerate(wl.stages):
         if hasattr(st, "cout"):
@@ -57,6 +60,9 @@ def step_bytes(wl, compact=False):
             spikes_read = nxt is not None and hasattr(nxt, "cout")
             nb, ho, wo = conv_call_bytes(B, T, c, h, w, st, exact, not compact, not compact or spikes_read)
             exact = False
+            if i in fused:
+                P = nxt.P
+                nb += (0 if compact else B * T * st.cout * (ho // P) * (wo // P)) + B * st.cout * (ho // P) * (wo // P)
             out[f"conv{i}"] = nb
             out[f"kwta{i}"] = B * st.cout * ho * wo * 5 + B * st.k * 16
             if st.learn:
@@ -65,7 +71,8 @@ def step_bytes(wl, compact=False):
         else:
             ho, wo = (h + 2 * st.D - st.P) // st.R + 1, (w + 2 * st.D - st.P) // st.R + 1
             # first-spike pooling: one byte per input neuron in, the wave and first-spike map out
-            out[f"pool{i}"] = B * c * h * w + B * T * c * ho * wo + B * c * ho * wo
+            if i - 1 not in fused:
+                out[f"pool{i}"] = B * c * h * w + (0 if compact else B * T * c * ho * wo) + B * c * ho * wo
             h, w = ho, wo
             exact = True
     return out
@@ -74,6 +81,7 @@ def step_bytes(wl, compact=False):
 # what each timed call launches (the roofline's kernel)
 CALL_KERNELS = {
     "conv": "spk_conv_fire: padding launch + MFMA conv-fire launch",
+    "convpool": "spk_conv_fire_pool: padding launch + MFMA conv-fire launch with first-spike pooling",
     "enco": "spk_encode_latency: filter, rank-order bins, Eq.1 wave",
     "kwta": "spk_kwta",
     "pool": "spk_pool_first_spike",
@@ -284,6 +292,8 @@ def main():
     ap.add_argument("--workload", type=int, default=2, help="1..5 (2 = the 3-layer network, the headline)")
     ap.add_argument("--batch", type=int, default=None, help="override the workload's batch")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle baseline budget (0 = skip)")
+    ap.add_argument("--fused", action="store_true",
+                    help="compact form with each conv -> pool pair as one fused launch (a separate figure)")
     ap.add_argument("--compact", action="store_true",
                     help="the compact inter-layer form: no per-step potentials and no unread per-step spikes "
                          "(a separate figure, not the contract number)")
@@ -326,8 +336,10 @@ def main():
     if args.ops:
         ops_bench(wl, inp, dev)
         return
+    if args.fused:
+        args.compact = True
     ch = chain_for(wl, inp.get("bank"), device=dev, want_potentials=not args.compact,
-                   want_spikes=not args.compact)
+                   want_spikes=not args.compact, fused=args.fused, want_waves=not args.compact)
     ch.set_weights([torch.from_numpy(w) for w in inp["weights"]])
     labels = torch.from_numpy(inp["labels"])
     if wl.source == "image":
@@ -336,7 +348,10 @@ def main():
         ch.set_input(wave=spk.spk_expand_wave(torch.from_numpy(inp["t_first"]).to(dev), wl.T), labels=labels)
     torch.cuda.synchronize()
 
-    nbytes = step_bytes(wl, args.compact)
+    first_spike_in = [(i == 0 and wl.source == "image") or (i > 0 and not hasattr(wl.stages[i - 1], "cout"))
+                      for i in range(len(wl.stages))]
+    fused = tuple(i for i in range(len(wl.stages)) if ch._fusable(i, first_spike_in[i]))
+    nbytes = step_bytes(wl, args.compact, fused)
     # the call with the most algorithmic bytes among those timed one by one
     dominant = max((k for k in nbytes if not k.startswith("stdp")), key=lambda k: nbytes[k])
 
@@ -367,7 +382,8 @@ def main():
     ev = 0
     for i, st in enumerate(wl.stages):
         if hasattr(st, "cout"):
-            ev += int(spk.spk_count_events(ch.pre_waves[i], st.cout, st.K, st.pad).item())
+            pre = ch.pre_waves[i] if ch.pre_tf[i] is None or ch.want_waves else spk.spk_expand_wave(ch.pre_tf[i], wl.T)
+            ev += int(spk.spk_count_events(pre, st.cout, st.K, st.pad).item())
 
     # per-call breakdown from one extra, untimed step
     marks = {}
@@ -402,12 +418,16 @@ def main():
                    "layers": [f"conv {s.cin}->{s.cout} k{s.K} p{s.pad} thr {s.thr} kwta {s.k}/{s.r} {s.learn}"
                               if hasattr(s, "cout") else f"pool {s.P}/{s.R}" for s in wl.stages],
                    "source": wl.source + (f" ({wl.bank})" if wl.bank else ""), "parallelism": "none (1 GPU)",
-                   "form": ("compact: conv layers write first-spike maps only (no per-step potentials; "
-                            "per-step spikes only where a stage reads them)" if args.compact
-                            else "contract: every call writes its full outputs")},
+                   "form": (("fused: each conv -> pool pair is one launch (conv, fire, first-spike pooling); "
+                             if args.fused else "") +
+                            ("compact: layers pass first-spike maps (no per-step potentials, no Eq.1 waves of the "
+                             "encoder or the pools, per-step spikes only where a conv reads them)" if args.compact
+                             else "contract: every call writes its full outputs"))},
         "synaptic_events_per_s": round(ev * args.steps / elapsed, 1),
         "synaptic_events_per_step": ev,
-        "roofline": {"bound": "hbm", "kernel": CALL_KERNELS.get(dominant[:4], dominant) + f" ({dominant})",
+        "roofline": {"bound": "hbm", "kernel": CALL_KERNELS.get("convpool" if dominant.startswith("conv") and
+                                                                int(dominant[4:]) in fused else dominant[:4],
+                                                                dominant) + f" ({dominant})",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes": nbytes[dominant], "avg_ms": round(dom_avg_ms, 4)},

@@ -181,6 +181,35 @@ SPK_API int spk_conv_fire_first_spike_noalloc(const uint8_t *in_t_first, int B, 
              const float *weight, int Cout, int K, int pad, float threshold,
              float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first, void *stream);
 
+/* One layer in one launch: convolution + firing (as
+ * spk_conv_fire_first_spike) with the first-spike max-pooling of its output
+ * (section "snn Module", Pooling, Eq.3, with window = stride = pool and no
+ * padding) fused into it, so that the layer's first-spike map is pooled
+ * while it is still on chip (the batching and fewer-round-trips direction of
+ * the paper's conclusions).
+ *   in_t_first      u8 [B][Cin][H][W], the layer input's first-spike map.
+ *   pool            pooling window and stride, >= 1, with pool <= Ho, Wo and
+ *                   pool * Wo <= 256 (128 when Ho*Wo is not a multiple of 4
+ *                   or an output is not 16-byte aligned).
+ *   threshold       finite (Eq.5 mode has no fused form).
+ *   potentials, spikes   as spk_conv_fire, or NULL (the compact form).
+ *   t_first, v_first     required, as spk_conv_fire.
+ *   pooled_t_first  u8 [B][Cout][Ho/pool][Wo/pool] (floor): the earliest
+ *                   first spike of each window, T if none -- spk_pool_first_spike
+ *                   of t_first with (pool, pool, 0).
+ *   pooled_wave     u8 [B][T][Cout][Ho/pool][Wo/pool] or NULL: its Eq.1 wave.
+ * Work is cut into bands of whole pooling rows of one image; every output
+ * neuron's sum runs in the same order as in spk_conv_fire_first_spike, so
+ * all outputs equal that call's (and spk_pool_first_spike's).  Workspace:
+ * spk_conv_fire_workspace_size(...) bytes.  Errors as spk_conv_fire, plus
+ * SPK_E_ARG for an infinite threshold or a NULL pooled_t_first, SPK_E_SHAPE
+ * for a window larger than the map and SPK_E_RANGE for a band that exceeds
+ * the limit above.                                                          */
+SPK_API int spk_conv_fire_pool(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+             const float *weight, int Cout, int K, int pad, float threshold, int pool,
+             float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
+             uint8_t *pooled_t_first, uint8_t *pooled_wave, void *workspace, size_t ws_bytes, void *stream);
+
 /* Convolution + firing with stride > 1 (section "snn Module" names strides
  * above 1 as the next version's feature): output neuron (y, x) reads the
  * zero-padded input window whose top-left corner is (y*stride, x*stride),
@@ -299,6 +328,23 @@ SPK_API int spk_rstdp(float *weight, int Cout, int Cin, int K, int pad,
               const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward,
               float a_plus, float a_minus, float lb, float ub, int stabilizer,
               void *workspace, size_t ws_bytes, void *stream);
+
+/* STDP / R-STDP with the layer input given by its first-spike map
+ * pre_t_first u8 [B][Cin][H][W] (values in [0, T], T = never) instead of its
+ * wave: T_j <= T_i is read as pre_t_first <= t_i, which is the wave's entry
+ * at step t_i by Eq.1.  All else as spk_stdp / spk_rstdp (same workspace);
+ * the updates are identical to theirs on the map's Eq.1 wave.  For callers
+ * that keep first-spike maps only (the compact inter-layer form).            */
+SPK_API int spk_stdp_first_spike(float *weight, int Cout, int Cin, int K, int pad,
+             const uint8_t *pre_t_first, int B, int T, int H, int W,
+             const int32_t *winners, const int32_t *n_winners, int k,
+             float a_plus, float a_minus, float lb, float ub, int stabilizer,
+             void *workspace, size_t ws_bytes, void *stream);
+SPK_API int spk_rstdp_first_spike(float *weight, int Cout, int Cin, int K, int pad,
+             const uint8_t *pre_t_first, int B, int T, int H, int W,
+             const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward,
+             float a_plus, float a_minus, float lb, float ub, int stabilizer,
+             void *workspace, size_t ws_bytes, void *stream);
 
 /* STDP / R-STDP of a layer with stride > 1 (Eq.4; stride as in
  * spk_conv_fire_strided): the pre-synaptic neuron of winner (f, t_i, y, x)

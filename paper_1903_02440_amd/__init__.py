@@ -58,10 +58,16 @@ _SIGS = {
     "spk_rstdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _P, _F, _F, _F, _F, _I, _P, _Z, _P]),
     "spk_decide": (_I, [_P, _P, _I, _I, _P, _I, _P, _P, _P]),
     "spk_count_events": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
+    "spk_conv_fire_pool": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _F, _I, _P, _P, _P, _P, _P, _P, _P, _Z,
+                                _P]),
     "spk_conv_fire_strided_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
     "spk_conv_fire_strided": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z, _P]),
     "spk_conv_fire_first_spike_strided": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _P,
                                                _Z, _P]),
+    "spk_stdp_first_spike": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _F, _F, _F, _F, _I, _P, _Z,
+                                  _P]),
+    "spk_rstdp_first_spike": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _P, _F, _F, _F, _F, _I, _P,
+                                   _Z, _P]),
     "spk_stdp_strided": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _F, _F, _F, _F, _I, _P, _Z,
                               _P]),
     "spk_rstdp_strided": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _P, _F, _F, _F, _F, _I, _P,
@@ -276,6 +282,33 @@ def spk_conv_fire_first_spike(in_t_first, T, weight, pad, threshold, potentials=
                       workspace, stream)
 
 
+def spk_conv_fire_pool(in_t_first, T, weight, pad, threshold, pool, potentials=False, spikes=False, t_first=None,
+                       v_first=None, pooled_t_first=None, pooled_wave=None, workspace=None, stream=None):
+    """Conv + fire + first-spike pooling (window = stride = pool) in one launch:
+    -> (potentials or None, spikes or None, t_first, v_first, pooled_t_first u8 [B,Cout,Ho/pool,Wo/pool],
+    pooled_wave u8 [B,T,Cout,Ho/pool,Wo/pool] or None).  Per-step outputs default to skipped (False)."""
+    B, Cin, H, W = in_t_first.shape
+    Cout, Cin2, K, _ = weight.shape
+    _need(in_t_first, torch.uint8, (B, Cin, H, W), "in_t_first")
+    _need(weight, torch.float32, (Cout, Cin, K, K), "weight")
+    Ho, Wo = conv_out_size(H, K, pad), conv_out_size(W, K, pad)
+    Hp, Wp = Ho // pool, Wo // pool
+    dev = in_t_first.device
+    potentials = _out(potentials, (B, T, Cout, Ho, Wo), torch.float32, dev, "potentials")
+    spikes = _out(spikes, (B, T, Cout, Ho, Wo), torch.uint8, dev, "spikes")
+    t_first = _out(t_first, (B, Cout, Ho, Wo), torch.uint8, dev, "t_first")
+    v_first = _out(v_first, (B, Cout, Ho, Wo), torch.float32, dev, "v_first")
+    pooled_t_first = _out(pooled_t_first, (B, Cout, Hp, Wp), torch.uint8, dev, "pooled_t_first")
+    pooled_wave = _out(pooled_wave, (B, T, Cout, Hp, Wp), torch.uint8, dev, "pooled_wave")
+    n = spk_conv_fire_workspace_size(B, T, Cin, H, W, Cout, K, pad)
+    ws = _ws(workspace, n, dev)
+    _check(_lib.spk_conv_fire_pool(_ptr(in_t_first), B, T, Cin, H, W, _ptr(weight), Cout, K, pad, float(threshold),
+                                   int(pool), _ptr(potentials), _ptr(spikes), _ptr(t_first), _ptr(v_first),
+                                   _ptr(pooled_t_first), _ptr(pooled_wave), _ptr(ws), n, _stream(stream)))
+    none = lambda x: None if x is False else x  # noqa: E731
+    return none(potentials), none(spikes), t_first, v_first, pooled_t_first, none(pooled_wave)
+
+
 def spk_conv_fire_strided(wave, weight, stride, pad, threshold, potentials=None, spikes=None, t_first=None,
                           v_first=None, workspace=None, stream=None):
     """spk_conv_fire with stride: output (y, x) reads the padded window at (y*stride, x*stride)."""
@@ -393,12 +426,17 @@ def spk_kwta(t_first, v_first, T, k, radius, winners=None, n_winners=None, works
 
 
 # ---------------------------------------------------------------- plasticity
-def _stdp_args(weight, pre_wave, winners, n_winners):
+def _stdp_args(weight, pre_wave, winners, n_winners, T=None):
+    """Sizes of a plasticity call; with T given, pre_wave is the first-spike map [B,Cin,H,W]."""
     Cout, Cin, K, _ = weight.shape
-    B, T, Cin2, H, W = pre_wave.shape
+    if T is None:
+        B, T, Cin2, H, W = pre_wave.shape
+        _need(pre_wave, torch.uint8, (B, T, Cin, H, W), "pre_wave")
+    else:
+        B, Cin2, H, W = pre_wave.shape
+        _need(pre_wave, torch.uint8, (B, Cin, H, W), "pre_t_first")
     k = winners.shape[1]
     _need(weight, torch.float32, (Cout, Cin, K, K), "weight")
-    _need(pre_wave, torch.uint8, (B, T, Cin, H, W), "pre_wave")
     _need(winners, torch.int32, (B, k, 4), "winners")
     _need(n_winners, torch.int32, (B,), "n_winners")
     return Cout, Cin, K, B, T, H, W, k
@@ -409,17 +447,21 @@ def spk_stdp_workspace_size(Cout, Cin, K, B, k) -> int:
 
 
 def _stdp_call(weight, stride, pad, pre_wave, winners, n_winners, reward, a_plus, a_minus, lb, ub, stabilizer,
-               workspace, stream):
-    Cout, Cin, K, B, T, H, W, k = _stdp_args(weight, pre_wave, winners, n_winners)
+               workspace, stream, T=None):
+    Cout, Cin, K, B, T, H, W, k = _stdp_args(weight, pre_wave, winners, n_winners, T)
     if reward is not None:
         _need(reward, torch.int8, (B,), "reward")
     n = spk_stdp_workspace_size(Cout, Cin, K, B, k)
     ws = _ws(workspace, n, weight.device)
-    head = (_ptr(weight), Cout, Cin, K) + ((pad,) if stride is None else (stride, pad))
     mid = (_ptr(pre_wave), B, T, H, W, _ptr(winners), _ptr(n_winners), k) + (() if reward is None else (_ptr(reward),))
     tail = (float(a_plus), float(a_minus), float(lb), float(ub), int(bool(stabilizer)), _ptr(ws), n, _stream(stream))
-    fn = {(False, False): _lib.spk_stdp, (True, False): _lib.spk_rstdp, (False, True): _lib.spk_stdp_strided,
-          (True, True): _lib.spk_rstdp_strided}[(reward is not None, stride is not None)]
+    if stride == "times":  # first-spike map input (stride 1)
+        head = (_ptr(weight), Cout, Cin, K, pad)
+        fn = _lib.spk_rstdp_first_spike if reward is not None else _lib.spk_stdp_first_spike
+    else:
+        head = (_ptr(weight), Cout, Cin, K) + ((pad,) if stride is None else (stride, pad))
+        fn = {(False, False): _lib.spk_stdp, (True, False): _lib.spk_rstdp, (False, True): _lib.spk_stdp_strided,
+              (True, True): _lib.spk_rstdp_strided}[(reward is not None, stride is not None)]
     _check(fn(*head, *mid, *tail))
     return weight
 
@@ -436,6 +478,20 @@ def spk_rstdp(weight, pad, pre_wave, winners, n_winners, reward, a_plus, a_minus
     """R-STDP: reward i8 [B] in {+1,-1,0} selects STDP, anti-STDP or nothing per image."""
     return _stdp_call(weight, None, pad, pre_wave, winners, n_winners, reward, a_plus, a_minus, lb, ub, stabilizer,
                       workspace, stream)
+
+
+def spk_stdp_first_spike(weight, pad, pre_t_first, T, winners, n_winners, a_plus, a_minus, lb=0.0, ub=1.0,
+                         stabilizer=True, workspace=None, stream=None):
+    """spk_stdp with the layer input given by its first-spike map u8 [B,Cin,H,W] (T = never)."""
+    return _stdp_call(weight, "times", pad, pre_t_first, winners, n_winners, None, a_plus, a_minus, lb, ub,
+                      stabilizer, workspace, stream, T=T)
+
+
+def spk_rstdp_first_spike(weight, pad, pre_t_first, T, winners, n_winners, reward, a_plus, a_minus, lb=0.0, ub=1.0,
+                          stabilizer=True, workspace=None, stream=None):
+    """spk_rstdp with the layer input given by its first-spike map."""
+    return _stdp_call(weight, "times", pad, pre_t_first, winners, n_winners, reward, a_plus, a_minus, lb, ub,
+                      stabilizer, workspace, stream, T=T)
 
 
 def spk_stdp_strided(weight, stride, pad, pre_wave, winners, n_winners, a_plus, a_minus, lb=0.0, ub=1.0,

@@ -466,13 +466,29 @@ __device__ constexpr bool fin_unit(int i, int n) {
 }
 static_assert(FIN_MT == 2, "the tile slots of an MFMA wave are wv and wv + FIN_CW");
 
+// First-spike pooling fused into the finite-threshold call (window P = stride,
+// no padding; P == 0: none).  Tasks are then bands of whole pooling rows of one
+// image, so every window lies in one task: the store waves put a task's
+// first-spike times into an LDS map [32 features][np_max] and pool them after
+// the next barrier of the workgroup (the last task's after one more barrier).
+// With vec, each thread pools 4 consecutive positions of a feature's run of
+// the band (the band's pooled rows, contiguous in the map) and writes them,
+// and each step's Eq.1 word of them, as 4-byte stores.
+struct PoolOut {
+    int P;          // window and stride (0: no pooling)
+    int Hpo, Wpo;   // pooled map size, floor(Ho / P) x floor(Wo / P)
+    int vec;        // 4 pooled positions per thread (aligned maps, runs of a multiple of 4 at 4-byte offsets)
+    uint8_t *tf;    // pooled first-spike times [B][Cout][Hpo][Wpo]
+    uint8_t *wave;  // pooled Eq.1 wave [B][T][Cout][Hpo][Wpo], or null
+};
+
 template <int G, bool BLDS, bool ALDS>
 __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     const uint8_t *__restrict__ tpad, const uint4 *__restrict__ frag, const int2 *__restrict__ koff2, ConvGeom g,
-    int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words,
+    int n_pairs, int n_chunks, int cpi, int chunk_tiles, int band_pos, int np_max, int a_words,
     const float *__restrict__ inv_scale, const int *__restrict__ wbf16, const float *__restrict__ wts,
     const unsigned *__restrict__ wmax, const unsigned *__restrict__ wmin, int n_wmax, float *__restrict__ P,
-    uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF) {
+    uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF, PoolOut po) {
     extern __shared__ uint4 lds[];
     const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
     const int gq = lane >> 4, c = lane & 15;
@@ -484,6 +500,8 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     // padded rows channel-group major, [row][CP/8][Wp][8 bytes], so that the 16
     // consecutive positions of an 8-byte A read are 128 contiguous bytes.
     uint32_t *abuf = reinterpret_cast<uint32_t *>(stage + FIN_TB * stage_t);
+    // pooling: a task's first-spike times, [32 features][np_max]
+    uint8_t *pool_l = reinterpret_cast<uint8_t *>(abuf + (ALDS ? 2 * a_words : 0));
     const int row_bytes = g.Wp * g.CP;
 
     const int x = blockIdx.x % 8, j = blockIdx.x / 8;
@@ -497,15 +515,21 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 
     // A task is the flattened positions [p0, p0 + np): with cpi > 0, chunk
     // task % cpi of image task / cpi; with cpi == 0, chunk `task` of the
-    // flattened space, which may span two images.
+    // flattened space, which may span two images.  Chunks are band_pos
+    // positions (whole rows) when band_pos > 0, else chunk_tiles tiles.
     auto task_range = [&](int task, int &p0, int &np) {
-        if (cpi > 0) {
+        if (cpi > 0 && band_pos > 0) {
+            const int b = task / cpi, q0 = (task - b * cpi) * band_pos;
+            p0 = b * g.HoWo + q0;
+            np = min(band_pos, g.HoWo - q0);
+        } else if (cpi > 0) {
             const int b = task / cpi, q0 = (task - b * cpi) * chunk_tiles * 16;
             p0 = b * g.HoWo + q0;
             np = min(chunk_tiles * 16, g.HoWo - q0);
         } else {
-            p0 = task * chunk_tiles * 16;
-            np = min(chunk_tiles * 16, npos - p0);
+            const int cp = band_pos > 0 ? band_pos : chunk_tiles * 16;
+            p0 = task * cp;
+            np = min(cp, npos - p0);
         }
     };
     // The padded first-spike rows it reads: from row y_first of its first image
@@ -601,20 +625,31 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             region(task, row0_t, w0_t, nw_t);
             const uint8_t *abuf_t = reinterpret_cast<const uint8_t *>(abuf + abuf_sel * a_words);
             // Local tiles: wv, and wv + 8 when the task has it.  The task's tiles are
-            // spread over the four SIMDs as waves (s, s + 4) for SIMD s; when their
-            // count is 1 mod 4 (and at least 9), the SIMD holding the last tile would
-            // carry a whole tile more than the others, so its two 16-feature halves
-            // go to two SIMDs: the owner wave computes features 0-15 of it and the
-            // next wave, whose second slot is empty, features 16-31.  A second slot
-            // past the task is skipped.
+            // spread over the four SIMDs as waves (s, s + 4) for SIMD s.  With m = ntl - 8
+            // second slots in use (0 < m < 8), SIMD s carries 2 + [s < m] + [s + 4 < m]
+            // tiles.  When m is 1 or 5 the SIMD holding the last tile carries a whole
+            // tile more than the others, so its two 16-feature halves go to two SIMDs:
+            // the owner wave computes features 0-15 of it and the next wave, whose
+            // second slot is empty, features 16-31.  When m is 2 or 6 two SIMDs carry a
+            // tile more than the other two: the last two tiles are split the same way,
+            // their second halves going to the two waves after them (SIMDs then carry
+            // 5 or 7 halves each).  A second slot past the task is skipped.
             const int ntl = (np + 15) / 16;
             int tile1 = wv + FIN_CW;
             int mode1 = tile1 < ntl ? 0 : 3;  // 0 both halves, 1 first half, 2 second half, 3 none
-            if ((ntl & 3) == 1 && ntl > FIN_CW) {
-                if (wv == ntl - 1 - FIN_CW) {
+            const int m2 = ntl - FIN_CW;
+            if (ntl > FIN_CW && (ntl & 3) == 1) {
+                if (wv == m2 - 1) {
                     mode1 = 1;
-                } else if (wv == ntl - FIN_CW) {
+                } else if (wv == m2) {
                     tile1 = ntl - 1;
+                    mode1 = 2;
+                }
+            } else if (ntl > FIN_CW && (ntl & 3) == 2) {
+                if (wv == m2 - 2 || wv == m2 - 1) {
+                    mode1 = 1;
+                } else if (wv == m2 || wv == m2 + 1) {
+                    tile1 = ntl - 2 + (wv - m2);
                     mode1 = 2;
                 }
             }
@@ -777,9 +812,71 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             mfma_waves(std::integral_constant<bool, true>{});
         else
             mfma_waves(std::integral_constant<bool, false>{});
+        if (po.P > 0) __syncthreads();  // the store waves' last pooled map is complete in LDS
     } else {
         // ------------------------------------------------ store waves
         const int s = tid - FIN_CW * 64;
+        // Pooling of the task whose first-spike times are in pool_l (after a
+        // barrier): window (yo, xo) of feature fl is the min over its P x P
+        // positions; outputs of consecutive threads are consecutive in xo.
+        int pend_pos0 = -1, pend_np = 0;
+        auto pool_pending = [&]() {
+            if (pend_pos0 < 0) return;
+            const int64_t pplane = (int64_t)po.Hpo * po.Wpo, wplane = (int64_t)g.Cout * pplane;
+            // one segment per image the task covers (whole rows; a segment starts at
+            // a row that is a multiple of P)
+            for (int p = pend_pos0; p < pend_pos0 + pend_np;) {
+                const int b = p / g.HoWo, q0 = p - b * g.HoWo;
+                const int seg = min(pend_pos0 + pend_np, (b + 1) * g.HoWo) - p;
+                const uint8_t *map = pool_l + (p - pend_pos0);  // + fl * np_max
+                const int y0 = q0 / g.Wo, y1 = (q0 + seg) / g.Wo;  // the segment's output rows [y0, y1)
+                const int yo0 = y0 / po.P, nyo = min(po.Hpo, y1 / po.P) - yo0;
+                const int per_f = max(nyo, 0) * po.Wpo;
+                if (po.vec) {
+                    // per_f is a multiple of 4: groups of 4 consecutive pooled positions of one feature
+                    const int gpf = per_f >> 2;
+                    for (int i = s; i < nf * gpf; i += FIN_SW * 64) {
+                        const int fl = i / gpf, q = (i - fl * gpf) * 4;
+                        uint32_t t4 = 0;
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            const int yo = yo0 + (q + u) / po.Wpo, xo = (q + u) - ((q + u) / po.Wpo) * po.Wpo;
+                            const uint8_t *src = map + fl * np_max + (yo * po.P - y0) * g.Wo + xo * po.P;
+                            int tmin = g.T;
+                            for (int dy = 0; dy < po.P; ++dy)
+                                for (int dx = 0; dx < po.P; ++dx) tmin = min(tmin, (int)src[dy * g.Wo + dx]);
+                            t4 |= (uint32_t)tmin << (8 * u);
+                        }
+                        const int64_t o = ((int64_t)b * g.Cout + f0 + fl) * pplane + (int64_t)yo0 * po.Wpo + q;
+                        *reinterpret_cast<uint32_t *>(po.tf + o) = t4;
+                        if (po.wave) {
+                            uint8_t *wv0 = po.wave + (int64_t)b * g.T * wplane + (int64_t)(f0 + fl) * pplane +
+                                           (int64_t)yo0 * po.Wpo + q;
+                            for (int tt = 0; tt < g.T; ++tt)
+                                *reinterpret_cast<uint32_t *>(wv0 + tt * wplane) = spk::spikes4(t4, tt, g.T);
+                        }
+                    }
+                } else {
+                    for (int i = s; i < nf * per_f; i += FIN_SW * 64) {
+                        const int fl = i / per_f, rr = i - fl * per_f;
+                        const int yo = yo0 + rr / po.Wpo, xo = rr - (rr / po.Wpo) * po.Wpo;
+                        const uint8_t *src = map + fl * np_max + (yo * po.P - y0) * g.Wo + xo * po.P;
+                        int tmin = g.T;
+                        for (int dy = 0; dy < po.P; ++dy)
+                            for (int dx = 0; dx < po.P; ++dx) tmin = min(tmin, (int)src[dy * g.Wo + dx]);
+                        const int64_t o = ((int64_t)b * g.Cout + f0 + fl) * pplane + (int64_t)yo * po.Wpo + xo;
+                        po.tf[o] = (uint8_t)tmin;
+                        if (po.wave) {
+                            uint8_t *wv0 = po.wave + (int64_t)b * g.T * wplane + (int64_t)(f0 + fl) * pplane +
+                                           (int64_t)yo * po.Wpo + xo;
+                            for (int tt = 0; tt < g.T; ++tt) wv0[tt * wplane] = (uint8_t)(tt >= tmin);
+                        }
+                    }
+                }
+                p += seg;
+            }
+            pend_pos0 = -1;
+        };
         for (int task = t_lo + r; task < t_hi; task += R) {
             int pos0, np;
             task_range(task, pos0, np);
@@ -809,8 +906,15 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 #pragma unroll
                 for (int q = 0; q < G; ++q) vfirst[m][q] = 0.0f;
             }
+            // The previous task's map is complete in LDS after this task's first
+            // barrier.  It is pooled after the first block's firing, so that the
+            // MFMA waves compute the second block meanwhile; with a single block,
+            // between that block's two barriers (the map is rewritten right after
+            // the block).  A no-op without pooling, and after its first call.
+            const bool one_block = g.T <= FIN_TB;
             for (int tb0 = (g.T - 1) / FIN_TB * FIN_TB; tb0 >= 0; tb0 -= FIN_TB) {
                 __syncthreads();  // staging free
+                if (one_block) pool_pending();
                 __syncthreads();  // staging full
                 for (int t = min(FIN_TB, g.T - tb0) - 1; t >= 0; --t) {
                     const int tt = tb0 + t;
@@ -847,6 +951,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                         }
                     }
                 }
+                if (!one_block) pool_pending();
             }
             // first-spike time and the potential there
 #pragma unroll
@@ -865,7 +970,21 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                     TFt[o] = (uint8_t)tf4[m];
                     VFt[o] = vfirst[m][0];
                 }
+                if (po.P > 0) {  // this task's map for pooling (read after the next barrier)
+                    if (G == 4)
+                        *reinterpret_cast<uint32_t *>(pool_l + fl * np_max + pl) = tf4[m];
+                    else
+                        pool_l[fl * np_max + pl] = (uint8_t)tf4[m];
+                }
             }
+            if (po.P > 0) {
+                pend_pos0 = pos0;
+                pend_np = np;
+            }
+        }
+        if (po.P > 0) {
+            __syncthreads();  // matches the MFMA waves' last barrier
+            pool_pending();
         }
     }
 }
@@ -1268,13 +1387,13 @@ int max_lds_per_block() {
 template <int G, bool BLDS, bool ALDS>
 void launch_fin(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const float *inv_scale, const int *wbf16,
                 const float *wts, const unsigned *wmax, const unsigned *wmin, int n_wmax, const ConvGeom &g,
-                int n_pairs, int n_chunks, int cpi, int chunk_tiles, int np_max, int a_words, size_t lds, float *P,
-                uint8_t *S, uint8_t *TF, float *VF, hipStream_t st) {
+                int n_pairs, int n_chunks, int cpi, int chunk_tiles, int band_pos, int np_max, int a_words, size_t lds,
+                float *P, uint8_t *S, uint8_t *TF, float *VF, const PoolOut &po, hipStream_t st) {
     // one workgroup per CU: a multiple of the feature pairs on every XCD
     const int per_xcd = (int)spk::ceil_div(std::max(32, n_pairs), n_pairs) * n_pairs;
     hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
-                       tpad, frag, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, np_max, a_words, inv_scale, wbf16,
-                       wts, wmax, wmin, n_wmax, P, S, TF, VF);
+                       tpad, frag, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, band_pos, np_max, a_words, inv_scale,
+                       wbf16, wts, wmax, wmin, n_wmax, P, S, TF, VF, po);
 }
 
 template <bool VEC>
@@ -1314,15 +1433,66 @@ extern "C" size_t spk_conv_fire_strided_workspace_size(int B, int T, int Cin, in
 }
 
 namespace {
-// The conv call on either input form (times: in = first-spike map, else the wave).
+// The conv call on either input form (times: in = first-spike map, else the
+// wave); pool.P > 0 fuses first-spike pooling (window = stride = pool.P).
 int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int W, const float *weight, int Cout,
               int K, int stride, int pad, float threshold, float *potentials, uint8_t *spikes, uint8_t *t_first,
-              float *v_first, void *workspace, size_t ws_bytes, void *stream) {
+              float *v_first, void *workspace, size_t ws_bytes, void *stream,
+              PoolOut pool = PoolOut{0, 0, 0, 0, nullptr, nullptr}) {
     ConvPlan pl;
     int rc = make_plan(B, T, Cin, H, W, Cout, K, stride, pad, pl);
     if (rc != SPK_OK) return rc;
     SPK_REQUIRE(!std::isnan(threshold) && !(std::isinf(threshold) && threshold < 0), SPK_E_ARG,
                 "spk_conv_fire: threshold must be a number or +INFINITY");
+    const bool inf_mode = std::isinf(threshold);
+    // 4-element store groups need aligned outputs and groups that never straddle a task
+    bool vec = (pl.g.HoWo % 4) == 0 && ((uintptr_t)potentials & 15) == 0 && ((uintptr_t)v_first & 15) == 0 &&
+               ((uintptr_t)spikes & 3) == 0 && ((uintptr_t)t_first & 3) == 0;
+    const bool pooled = pool.P > 0;
+    int band_pos = 0, band_rows = 0;
+    bool flat_band = false;
+    if (pooled) {  // tasks: bands of whole pooling rows, at most as many positions as a task holds
+        SPK_REQUIRE(!inf_mode, SPK_E_ARG, "spk_conv_fire_pool: the threshold must be finite");
+        SPK_REQUIRE(pl.g.Ho >= pool.P && pl.g.Wo >= pool.P, SPK_E_SHAPE,
+                    "spk_conv_fire_pool: pooling window %d larger than the %dx%d map", pool.P, pl.g.Ho, pl.g.Wo);
+        auto band = [&](bool v) {
+            const int limit = 16 * chunk_tiles_max(v ? 4 : 1);
+            band_rows = pool.P * std::max(1, limit / (pool.P * pl.g.Wo));
+            band_pos = band_rows * pl.g.Wo;
+            return limit;
+        };
+        band(vec);
+        if (vec && band_pos % 4 != 0) vec = false;
+        const int limit = band(vec);
+        SPK_REQUIRE(pool.P * pl.g.Wo <= limit, SPK_E_RANGE,
+                    "spk_conv_fire_pool: a band of %d rows of %d positions exceeds %d positions", pool.P, pl.g.Wo,
+                    limit);
+        pool.Hpo = pl.g.Ho / pool.P;
+        pool.Wpo = pl.g.Wo / pool.P;
+        // Bands run over the flattened (image, row) space -- every task full, a task
+        // may end in the next image -- when every image starts on a window row
+        // (Ho a multiple of P) and an image is more than one band; else per image.
+        flat_band = pl.g.Ho % pool.P == 0 && pl.g.HoWo > band_pos &&
+                    ((int64_t)T * Cout + 32) * pl.g.HoWo < (1LL << 31);
+        // word stores of the pooled maps: every segment's run (its pooled rows of one
+        // feature in one image) starts at a multiple of 4 bytes and has a multiple of
+        // 4 positions; the segments repeat every lcm(band rows, Ho) flattened rows
+        const int64_t pplane = (int64_t)pool.Hpo * pool.Wpo;
+        bool runs4 = pplane % 4 == 0;
+        const int64_t Ho = pl.g.Ho;
+        const int64_t period_rows = flat_band ? band_rows / std::gcd((int64_t)band_rows, Ho) * Ho : Ho;
+        for (int64_t r0 = 0; runs4 && r0 < period_rows; r0 += band_rows) {
+            const int64_t r1 = flat_band ? r0 + band_rows : std::min(r0 + band_rows, Ho);
+            for (int64_t r = r0; r < r1;) {  // segments of [r0, r1) by image
+                const int64_t y0 = r % Ho, y1 = std::min(Ho, y0 + (r1 - r));
+                const int64_t yo0 = y0 / pool.P, nyo = std::max<int64_t>(0, std::min<int64_t>(pool.Hpo, y1 / pool.P) - yo0);
+                runs4 = runs4 && (yo0 * pool.Wpo) % 4 == 0 && (nyo * pool.Wpo) % 4 == 0;
+                r += y1 - y0;
+            }
+        }
+        pool.vec = runs4 && ((uintptr_t)pool.tf & 3) == 0 && ((uintptr_t)pool.wave & 3) == 0;
+    }
+
     if (B == 0) return spk::ok();
     SPK_REQUIRE(wave && weight && t_first && v_first, SPK_E_ARG,
                 "spk_conv_fire: the input, weight, t_first and v_first are required");
@@ -1330,9 +1500,7 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     SPK_REQUIRE(workspace && ws_bytes >= need, SPK_E_WORKSPACE,
                 "spk_conv_fire: workspace of %zu bytes < %zu required", ws_bytes, need);
     ConvGeom g = pl.g;
-    const bool inf_mode = std::isinf(threshold);
     g.thr = inf_mode ? 0.0f : threshold;
-
     spk::Carver cv(workspace);
     uint8_t *tpad = cv.take<uint8_t>(pl.tpad_bytes);
     uint4 *frag = cv.take<uint4>(pl.frag_count);
@@ -1345,8 +1513,6 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     hipStream_t st = spk::as_stream(stream);
 
     // finite-threshold launch configuration (validated before anything is enqueued)
-    const bool vec = (g.HoWo % 4) == 0 && ((uintptr_t)potentials & 15) == 0 && ((uintptr_t)v_first & 15) == 0 &&
-                     ((uintptr_t)spikes & 3) == 0 && ((uintptr_t)t_first & 3) == 0;
     // Tasks: chunks of up to ct_max position tiles.  An image of at most ct_max
     // tiles is one task (each step's outputs of a feature pair are then one
     // contiguous region); larger images are cut into chunks of the flattened
@@ -1358,9 +1524,17 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     int ct_max = chunk_tiles_max(vec ? 4 : 1);
     while (ct_max > 4 && (int64_t)n_pairs * B * g.mt_per_img / ct_max < 256) ct_max /= 2;
     const int64_t npos = (int64_t)B * g.HoWo;
-    const bool flat = g.mt_per_img > ct_max && ((int64_t)T * Cout + 32) * g.HoWo < (1LL << 31);
+    const bool flat = pooled ? flat_band : g.mt_per_img > ct_max && ((int64_t)T * Cout + 32) * g.HoWo < (1LL << 31);
     int cpi, chunk_tiles, n_chunks;
-    if (flat) {
+    if (pooled && flat) {
+        cpi = 0;
+        chunk_tiles = (band_pos + 15) / 16;
+        n_chunks = (int)spk::ceil_div(npos, band_pos);
+    } else if (pooled) {
+        cpi = (g.Ho + band_rows - 1) / band_rows;
+        chunk_tiles = (std::min(band_pos, g.HoWo) + 15) / 16;
+        n_chunks = B * cpi;
+    } else if (flat) {
         cpi = 0;
         chunk_tiles = ct_max;
         n_chunks = (int)spk::ceil_div(npos, ct_max * 16);
@@ -1377,31 +1551,33 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     // spike rows of the largest task, staged in LDS (double-buffered) when small enough
     // (the row count of a chunk depends on its first position modulo HoWo, which repeats
     // every HoWo / gcd(HoWo, np_max) chunks; past 65536 of them a bound is used)
+    const int cpos = pooled ? band_pos : np_max;  // positions per chunk
     auto chunk_rows = [&](int64_t p0) {
-        const int64_t pb = std::min(p0 + np_max, npos) - 1;
+        const int64_t pb = std::min(p0 + cpos, npos) - 1;
         const int64_t ba = p0 / g.HoWo, bb = pb / g.HoWo;
         return (int)((bb * g.Hp + (pb - bb * g.HoWo) / g.Wo * stride + K) -
                      (ba * g.Hp + (p0 - ba * g.HoWo) / g.Wo * stride));
     };
-    const int64_t period = g.HoWo / std::gcd((int64_t)g.HoWo, (int64_t)np_max);
+    const int64_t period = g.HoWo / std::gcd((int64_t)g.HoWo, (int64_t)cpos);
     int a_rows = 0;
     if (!flat) {
         for (int ch = 0; ch < cpi; ++ch) {
-            const int p0 = ch * np_max, np = std::min(np_max, g.HoWo - p0);
+            const int p0 = ch * cpos, np = std::min(cpos, g.HoWo - p0);
             a_rows = std::max(a_rows, ((p0 + np - 1) / g.Wo - p0 / g.Wo) * stride + K);
         }
     } else if (period <= 65536) {
         for (int64_t ch = 0; ch < std::min<int64_t>(n_chunks, period); ++ch)
-            a_rows = std::max(a_rows, chunk_rows(ch * np_max));
-    } else {  // HoWo > 65536 > np_max: a chunk touches at most two images
-        a_rows = (np_max + g.Wo - 1) / g.Wo * stride + 2 * g.Hp + K;
+            a_rows = std::max(a_rows, chunk_rows(ch * cpos));
+    } else {  // HoWo > 65536 > cpos: a chunk touches at most two images
+        a_rows = (cpos + g.Wo - 1) / g.Wo * stride + 2 * g.Hp + K;
     }
     // staged spike rows: CP >= 8 (8-byte reads of one channel group), buffers rounded to 64 words
     const int a_words = (int)spk::align_up((size_t)a_rows * g.Wp * g.CP / 4, 64);
     const size_t a_lds = 2 * (size_t)a_words * 4;
-    const bool alds = g.CP >= 8 && koff_lds + stage_lds + a_lds <= lds_limit;
-    const bool blds = koff_lds + frag_lds + stage_lds + (alds ? a_lds : 0) <= lds_limit;
-    const size_t fin_lds = koff_lds + (blds ? frag_lds : 0) + stage_lds + (alds ? a_lds : 0);
+    const size_t pool_lds = pooled ? (size_t)32 * np_max : 0;
+    const bool alds = g.CP >= 8 && koff_lds + stage_lds + a_lds + pool_lds <= lds_limit;
+    const bool blds = koff_lds + frag_lds + stage_lds + (alds ? a_lds : 0) + pool_lds <= lds_limit;
+    const size_t fin_lds = koff_lds + (blds ? frag_lds : 0) + stage_lds + (alds ? a_lds : 0) + pool_lds;
     const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4 * 16;
     SPK_REQUIRE(!inf_mode || inf_lds <= lds_limit, SPK_E_RANGE,
                 "spk_conv_fire: needs %zu bytes of LDS per workgroup, the device has %zu", inf_lds, lds_limit);
@@ -1438,7 +1614,8 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     } else {
 #define SPK_FIN(G, BL, AL)                                                                                    \
     launch_fin<G, BL, AL>(tpad, frag, koff2, inv_scale, wbf16, weight, wmax, wmin, n_wmax, g, n_pairs, n_chunks, \
-                          cpi, chunk_tiles, np_max, a_words, fin_lds, potentials, spikes, t_first, v_first, st)
+                          cpi, chunk_tiles, band_pos, np_max, a_words, fin_lds, potentials, spikes, t_first, v_first, \
+                          pool, st)
         const int sel = (vec ? 4 : 0) + (blds ? 2 : 0) + (alds ? 1 : 0);
         switch (sel) {
             case 0: SPK_FIN(1, false, false); break;
@@ -1469,6 +1646,17 @@ extern "C" int spk_conv_fire_first_spike(const uint8_t *in_t_first, int B, int T
                                          void *workspace, size_t ws_bytes, void *stream) {
     return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, 1, pad, threshold, potentials, spikes,
                      t_first, v_first, workspace, ws_bytes, stream);
+}
+
+extern "C" int spk_conv_fire_pool(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+                                  const float *weight, int Cout, int K, int pad, float threshold, int pool,
+                                  float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
+                                  uint8_t *pooled_t_first, uint8_t *pooled_wave, void *workspace, size_t ws_bytes,
+                                  void *stream) {
+    SPK_REQUIRE(pool >= 1, SPK_E_SHAPE, "spk_conv_fire_pool: pooling window %d < 1", pool);
+    SPK_REQUIRE(pooled_t_first || B == 0, SPK_E_ARG, "spk_conv_fire_pool: pooled_t_first is required");
+    return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, 1, pad, threshold, potentials, spikes,
+                     t_first, v_first, workspace, ws_bytes, stream, PoolOut{pool, 0, 0, 0, pooled_t_first, pooled_wave});
 }
 
 extern "C" int spk_conv_fire_strided(const uint8_t *wave, int B, int T, int Cin, int H, int W, const float *weight,

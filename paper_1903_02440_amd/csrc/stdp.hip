@@ -29,6 +29,7 @@ constexpr int LIST_THREADS = 1024;  // images scanned per pass of the list kerne
 
 struct StdpArgs {
     int Cout, Cin, K, pad, stride, B, T, H, W, k, stabilizer;
+    int times;  // pre is the layer input's first-spike map [B][Cin][H][W] instead of its wave
     float a_plus, a_minus, lb, ub;
 };
 
@@ -161,8 +162,12 @@ __global__ __launch_bounds__(256) void k_stdp_bits(const uint8_t *__restrict__ p
         if (q < cnt) {
             const int4 u = lst[q];
             const int iy = u.z * a.stride + ky - a.pad, ix = u.w * a.stride + kx - a.pad;
-            if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
-                v[q] = pre[((int64_t)u.x * a.T + u.y) * plane + cioff + (int64_t)iy * a.W + ix];
+            if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W) {
+                if (a.times)  // Eq.1: the wave is 1 at step t_i exactly where t_first <= t_i
+                    v[q] = pre[(int64_t)u.x * plane + cioff + (int64_t)iy * a.W + ix] <= u.y;
+                else
+                    v[q] = pre[((int64_t)u.x * a.T + u.y) * plane + cioff + (int64_t)iy * a.W + ix];
+            }
         }
     }
     uint32_t word = 0;
@@ -256,8 +261,12 @@ __global__ __launch_bounds__(256) void k_stdp_single(float *__restrict__ weight,
     const int ci = e / KK, ky = (e % KK) / a.K, kx = e % a.K;
     const int iy = winners[4 * j + 2] * a.stride + ky - a.pad, ix = winners[4 * j + 3] * a.stride + kx - a.pad;
     uint8_t v = 0;
-    if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W)
-        v = pre[((int64_t)t * a.Cin + ci) * a.H * a.W + (int64_t)iy * a.W + ix];
+    if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W) {
+        if (a.times)
+            v = pre[(int64_t)ci * a.H * a.W + (int64_t)iy * a.W + ix] <= t;
+        else
+            v = pre[((int64_t)t * a.Cin + ci) * a.H * a.W + (int64_t)iy * a.W + ix];
+    }
     double r = v != 0 ? (double)a.a_plus : (double)a.a_minus;
     if (reward && reward[0] < 0) r = -r;
     float *wp = weight + (int64_t)f * Kc + e;
@@ -282,7 +291,7 @@ __global__ __launch_bounds__(256) void k_decide(const int32_t *__restrict__ winn
 int stdp_common(float *weight, int Cout, int Cin, int K, int stride, int pad, const uint8_t *pre_wave, int B, int T,
                 int H, int W, const int32_t *winners, const int32_t *n_winners, int k, const int8_t *reward,
                 float a_plus, float a_minus, float lb, float ub, int stabilizer, void *workspace, size_t ws_bytes,
-                void *stream, const char *name) {
+                void *stream, const char *name, bool times = false) {
     SPK_REQUIRE(Cout >= 1 && Cin >= 1 && K >= 1 && pad >= 0 && stride >= 1 && B >= 0 && T >= 1 && H >= 1 &&
                     W >= 1 && k >= 1,
                 SPK_E_SHAPE, "%s: bad sizes", name);
@@ -303,7 +312,7 @@ int stdp_common(float *weight, int Cout, int Cin, int K, int stride, int pad, co
     SPK_REQUIRE(workspace && ws_bytes >= need, SPK_E_WORKSPACE, "%s: workspace of %zu bytes < %zu required", name,
                 ws_bytes, need);
     StdpWork wk = carve(workspace, Cout, Cin, K, B, k, nullptr);
-    StdpArgs a{Cout, Cin, K, pad, stride, B, T, H, W, k, stabilizer, a_plus, a_minus, lb, ub};
+    StdpArgs a{Cout, Cin, K, pad, stride, B, T, H, W, k, stabilizer, times ? 1 : 0, a_plus, a_minus, lb, ub};
     hipStream_t st = spk::as_stream(stream);
     const unsigned wchunks = (unsigned)spk::ceil_div((int64_t)Cin * K * K, 256);
     // the clamp can be dropped after the first update (see k_stdp_apply)
@@ -352,6 +361,23 @@ extern "C" int spk_rstdp(float *weight, int Cout, int Cin, int K, int pad, const
     SPK_REQUIRE(reward || B == 0, SPK_E_ARG, "spk_rstdp: reward is required");
     return stdp_common(weight, Cout, Cin, K, 1, pad, pre_wave, B, T, H, W, winners, n_winners, k, reward, a_plus,
                        a_minus, lb, ub, stabilizer, workspace, ws_bytes, stream, "spk_rstdp");
+}
+
+extern "C" int spk_stdp_first_spike(float *weight, int Cout, int Cin, int K, int pad, const uint8_t *pre_t_first,
+                                    int B, int T, int H, int W, const int32_t *winners, const int32_t *n_winners,
+                                    int k, float a_plus, float a_minus, float lb, float ub, int stabilizer,
+                                    void *workspace, size_t ws_bytes, void *stream) {
+    return stdp_common(weight, Cout, Cin, K, 1, pad, pre_t_first, B, T, H, W, winners, n_winners, k, nullptr, a_plus,
+                       a_minus, lb, ub, stabilizer, workspace, ws_bytes, stream, "spk_stdp_first_spike", true);
+}
+
+extern "C" int spk_rstdp_first_spike(float *weight, int Cout, int Cin, int K, int pad, const uint8_t *pre_t_first,
+                                     int B, int T, int H, int W, const int32_t *winners, const int32_t *n_winners,
+                                     int k, const int8_t *reward, float a_plus, float a_minus, float lb, float ub,
+                                     int stabilizer, void *workspace, size_t ws_bytes, void *stream) {
+    SPK_REQUIRE(reward || B == 0, SPK_E_ARG, "spk_rstdp_first_spike: reward is required");
+    return stdp_common(weight, Cout, Cin, K, 1, pad, pre_t_first, B, T, H, W, winners, n_winners, k, reward, a_plus,
+                       a_minus, lb, ub, stabilizer, workspace, ws_bytes, stream, "spk_rstdp_first_spike", true);
 }
 
 extern "C" int spk_stdp_strided(float *weight, int Cout, int Cin, int K, int stride, int pad, const uint8_t *pre_wave,

@@ -15,10 +15,19 @@ calls on one stream, with no host synchronisation and no allocation inside
   encoder's or a pool's output, whose wave is Eq.1 of its first-spike map by
   construction, ``spk_conv_fire_first_spike`` reads that map instead of the
   T planes of the wave;
+* with ``fused=True``, a conv stage with a finite threshold and stride 1 whose
+  input is a first-spike map, followed by a pool stage with window = stride
+  and no padding, runs as one ``spk_conv_fire_pool`` launch (conv, fire and
+  the first-spike pooling fused) that fills both stages' buffers;
 * each pool stage: ``spk_pool_first_spike`` on the first-spike map of the
   stage below (which equals ``spk_pool`` on its wave whenever that wave is
   cumulative -- always the case for non-negative weights), or ``spk_pool``
   on the wave when constructed with ``pool_from_first_spike=False``;
+* with ``want_waves=False`` no Eq.1 wave is written where a first-spike map
+  carries the same information: the encoder and the pools write first-spike
+  maps only, and a layer whose input is such a map learns from it
+  (``spk_stdp_first_spike`` / ``spk_rstdp_first_spike``); only a conv stage
+  fed by another conv still writes per-step spikes;
 * after a reward-modulated last layer: ``spk_decide``;
 * learning: ``spk_stdp`` / ``spk_rstdp`` per conv stage (frozen forward,
   ordered replay within the batch).  The layers' updates touch disjoint
@@ -41,7 +50,8 @@ import torch
 
 from . import (pool_out_size, conv_out_size, spk_conv_fire, spk_conv_fire_first_spike, spk_conv_fire_workspace_size,
                spk_conv_fire_strided, spk_conv_fire_first_spike_strided, spk_conv_fire_strided_workspace_size,
-               spk_rstdp_strided, spk_stdp_strided, spk_decide,
+               spk_conv_fire_pool,
+               spk_rstdp_strided, spk_stdp_strided, spk_stdp_first_spike, spk_rstdp_first_spike, spk_decide,
                spk_encode_latency, spk_encode_latency_workspace_size, spk_kwta, spk_kwta_workspace_size,
                spk_local_normalization, spk_pool, spk_pool_first_spike, spk_rank_latency, spk_rstdp, spk_stdp,
                spk_stdp_workspace_size)
@@ -58,8 +68,11 @@ def _stride(st):
 class Chain:
     def __init__(self, stages, B, T, H, W, cin, source="image", filter_bank=None, filter_threshold=0.0,
                  n_classes=10, device="cuda", want_potentials=True, pool_from_first_spike=True,
-                 concurrent_learn=True, want_spikes=True, local_norm=None):
+                 concurrent_learn=True, want_spikes=True, local_norm=None, fused=False, want_waves=True):
         self.stages = [copy.copy(st) for st in stages]  # own copies: set_rates changes them
+        self.fused = fused
+        # without waves, the encoder's and the pools' outputs are first-spike maps only
+        self.want_waves = want_waves or source != "image"
         self.pool_from_first_spike = pool_from_first_spike
         self.B, self.T, self.source = B, T, source
         self.n_classes = n_classes
@@ -81,7 +94,7 @@ class Chain:
             C = cin
             self.image = None
             self.local_norm = None
-        self.input_wave = torch.zeros((B, T, C, H, W), dtype=u8, device=dev)
+        self.input_wave = torch.zeros((B, T, C, H, W), dtype=u8, device=dev) if self.want_waves else None
         self.input_tf = torch.zeros((B, C, H, W), dtype=u8, device=dev) if source == "image" else None
         self.bufs = []
         c, h, w = C, H, W
@@ -114,7 +127,7 @@ class Chain:
                 c, h, w = st.cout, ho, wo
             else:
                 ho, wo = pool_out_size(h, st.P, st.R, st.D), pool_out_size(w, st.P, st.R, st.D)
-                b["out"] = torch.empty((B, T, c, ho, wo), dtype=u8, device=dev)
+                b["out"] = torch.empty((B, T, c, ho, wo), dtype=u8, device=dev) if self.want_waves else False
                 b["out_tf"] = torch.empty((B, c, ho, wo), dtype=u8, device=dev)
                 h, w = ho, wo
             b["shape_in"] = None
@@ -124,6 +137,7 @@ class Chain:
         self.decision = torch.empty((B,), dtype=i32, device=dev)
         self.reward = torch.zeros((B,), dtype=torch.int8, device=dev)
         self.pre_waves = [None] * len(self.stages)
+        self.pre_tf = [None] * len(self.stages)  # a conv stage's input first-spike map, when it has one
         n_learn = sum(1 for st in self.stages if _is_conv(st) and st.learn is not None)
         self.concurrent_learn = concurrent_learn and n_learn > 1
         if self.concurrent_learn:
@@ -186,29 +200,41 @@ class Chain:
         self._wait_pending(-1, main)
         if self.source == "image":
             mark("encode", 0)
+            wave_out = self.input_wave if self.want_waves else False
             if self.local_norm is None:
-                spk_encode_latency(self.image, self.bank, self.T, self.filter_threshold, wave=self.input_wave,
+                spk_encode_latency(self.image, self.bank, self.T, self.filter_threshold, wave=wave_out,
                                    t_first=self.input_tf, intensities=False, workspace=self.workspace, stream=stream)
             else:
                 spk_encode_latency(self.image, self.bank, self.T, self.filter_threshold, wave=False, t_first=False,
                                    intensities=self.inten, workspace=self.workspace, stream=stream)
                 spk_local_normalization(self.inten, self.local_norm[0], self.local_norm[1], out=self.inten_norm,
                                         stream=stream)
-                spk_rank_latency(self.inten_norm, self.T, wave=self.input_wave, t_first=self.input_tf,
+                spk_rank_latency(self.inten_norm, self.T, wave=wave_out, t_first=self.input_tf,
                                  workspace=self.workspace, stream=stream)
             mark("encode", 1)
         x, x_tf = self.input_wave, self.input_tf
         x_exact = x_tf is not None  # x is Eq.1 of x_tf
         last_conv = None
+        pooled_by = None  # a pool stage already done by the fused launch of the conv stage before it
         for i, (st, b) in enumerate(zip(self.stages, self.bufs)):
             self._wait_pending(i, main)
             self.pre_waves[i] = x
+            self.pre_tf[i] = x_tf if x_exact else None
+            if pooled_by is not None:
+                x, x_tf, x_exact, pooled_by = b["out"], b["out_tf"], True, None
+                continue
             if _is_conv(st):
                 mark(f"conv{i}", 0)
                 outs = dict(potentials=b["P"], spikes=b["S"], t_first=b["tf"], v_first=b["vf"],
                             workspace=self.workspace, stream=stream)
                 s = _stride(st)
-                if x_exact and s == 1:
+                nxt = self.stages[i + 1] if i + 1 < len(self.stages) else None
+                if self._fusable(i, x_exact):
+                    nb = self.bufs[i + 1]
+                    spk_conv_fire_pool(x_tf, self.T, b["weight"], st.pad, st.thr, nxt.P, pooled_t_first=nb["out_tf"],
+                                       pooled_wave=nb["out"] if self.want_waves else False, **outs)
+                    pooled_by = i
+                elif x_exact and s == 1:
                     spk_conv_fire_first_spike(x_tf, self.T, b["weight"], st.pad, st.thr, **outs)
                 elif x_exact:
                     spk_conv_fire_first_spike_strided(x_tf, self.T, b["weight"], s, st.pad, st.thr, **outs)
@@ -238,8 +264,8 @@ class Chain:
             else:
                 mark(f"pool{i}", 0)
                 if self.pool_from_first_spike and x_tf is not None:
-                    spk_pool_first_spike(x_tf, self.T, st.P, st.R, st.D, out_wave=b["out"], out_t_first=b["out_tf"],
-                                         stream=stream)
+                    spk_pool_first_spike(x_tf, self.T, st.P, st.R, st.D, out_wave=b["out"] if self.want_waves else False,
+                                         out_t_first=b["out_tf"], stream=stream)
                     x_exact = True  # the pooled wave is written as Eq.1 of the pooled map
                 else:
                     spk_pool(x, st.P, st.R, st.D, out_wave=b["out"], out_t_first=b["out_tf"], stream=stream)
@@ -253,6 +279,16 @@ class Chain:
                        stream=stream)
             mark("decide", 1)
 
+    def _fusable(self, i, x_exact):
+        """Conv stage i and the pool stage after it run as one spk_conv_fire_pool launch."""
+        st = self.stages[i]
+        nxt = self.stages[i + 1] if i + 1 < len(self.stages) else None
+        if not (self.fused and x_exact and _is_conv(st) and nxt is not None and not _is_conv(nxt)):
+            return False
+        ho, wo = self.bufs[i]["tf"].shape[2:]
+        return (_stride(st) == 1 and not math.isinf(st.thr) and nxt.P == nxt.R and nxt.D == 0 and nxt.P <= min(ho, wo)
+                and nxt.P * wo <= 128)
+
     def _learners(self):
         return [(i, st, b) for i, (st, b) in enumerate(zip(self.stages, self.bufs))
                 if _is_conv(st) and st.learn is not None]
@@ -262,7 +298,14 @@ class Chain:
         rates = (st.a_plus, st.a_minus, st.lb, st.ub, st.stabilizer)
         kw = dict(workspace=b["ws_learn"], stream=s)
         stride = _stride(st)
-        if st.learn == "rstdp" and stride == 1:
+        if not self.want_waves and self.pre_tf[i] is not None and stride == 1:
+            # the layer input is kept as its first-spike map only
+            if st.learn == "rstdp":
+                spk_rstdp_first_spike(b["weight"], st.pad, self.pre_tf[i], self.T, b["win"], b["nw"], self.reward,
+                                      *rates, **kw)
+            else:
+                spk_stdp_first_spike(b["weight"], st.pad, self.pre_tf[i], self.T, b["win"], b["nw"], *rates, **kw)
+        elif st.learn == "rstdp" and stride == 1:
             spk_rstdp(b["weight"], st.pad, *common, self.reward, *rates, **kw)
         elif st.learn == "rstdp":
             spk_rstdp_strided(b["weight"], stride, st.pad, *common, self.reward, *rates, **kw)

@@ -22,7 +22,7 @@ def declared():
 
 def test_every_declared_symbol_is_exported():
     names = declared()
-    assert len(names) == 30
+    assert len(names) == 33
     lib = spk.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -170,4 +170,20 @@ def test_strided_entry_points_validate_and_size():
     assert lib.spk_rstdp_strided(DUMMY, 4, 2, 3, 2, 1, DUMMY, 1, 15, 8, 8, DUMMY, DUMMY, 1, None, 0.004, -0.003,
                                  0.0, 1.0, 1, DUMMY, ws, None) == spk.SPK_E_ARG
     assert lib.spk_count_events_strided(DUMMY, 1, 15, 2, 8, 8, 4, 3, 0, 1, DUMMY, None) == spk.SPK_E_SHAPE
+
+
+def test_fused_layer_validation():
+    lib = spk.lib()
+    f = lib.spk_conv_fire_pool
+
+    def call(H=28, W=28, K=5, pad=2, thr=15.0, pool=2, ptf=DUMMY, B=1):
+        return f(DUMMY if B else None, B, 15, 6, H, W, DUMMY, 30, K, pad, thr, pool, None, None, DUMMY, DUMMY2, ptf,
+                 None, DUMMY, 1 << 30, None)
+
+    assert call(thr=math.inf) == spk.SPK_E_ARG          # Eq.5 has no fused form
+    assert call(pool=0) == spk.SPK_E_SHAPE
+    assert call(pool=29) == spk.SPK_E_SHAPE             # window larger than the 28x28 map
+    assert call(W=300, pool=2) == spk.SPK_E_RANGE       # a 2-row band of 300 positions
+    assert call(ptf=None) == spk.SPK_E_ARG
+    assert call(B=0, ptf=None) == spk.SPK_OK
 

@@ -84,10 +84,13 @@ CONV_CASES = [
     ("tiny", 1, 1, 1, 1, 1, 1, 1, 0, 0.5, 0.3),
     ("inf-small", 3, 4, 2, 6, 6, 5, 3, 1, math.inf, 0.5),
     ("K1", 2, 5, 7, 3, 5, 33, 1, 0, 2.0, 0.3),
-    # 9 and 13 position tiles per image, enough of them for whole-image tasks (8
-    # feature pairs): the last tile's feature halves go to two waves
+    # 9, 10, 13 and 14 position tiles per image, enough of them for whole-image
+    # tasks (8 feature pairs): the feature halves of the last tile (9, 13) or of
+    # the last two tiles (10, 14) go to two waves each
     ("tiles9-split", 57, 9, 12, 12, 12, 256, 3, 1, 4.0, 0.4),
+    ("tiles10-split", 52, 9, 12, 12, 13, 256, 3, 1, 4.0, 0.4),
     ("tiles13-split", 40, 15, 16, 14, 14, 256, 3, 1, 6.0, 0.5),
+    ("tiles14-split", 37, 15, 16, 16, 14, 256, 3, 1, 6.0, 0.5),
     # Eq.5 on few tasks: the K chunks split over workgroups, two chunks per part
     ("inf-ksplit", 112, 15, 64, 12, 12, 8, 5, 2, math.inf, 0.6),
 ]
@@ -105,11 +108,11 @@ def fin_task_form(B, Cout, Ho, Wo):
         ct //= 2
     if mt > ct:
         return ("chunks", False)
-    return ("image", (mt & 3) == 1 and mt > 8 and ct == 16)
+    return ("image", (mt & 3) in (1, 2) and mt > 8 and ct == 16)
 
 
 def test_split_cases_take_the_whole_image_split():
-    for name in ("tiles9-split", "tiles13-split"):
+    for name in ("tiles9-split", "tiles10-split", "tiles13-split", "tiles14-split"):
         _, B, T, Cin, H, W, Cout, K, pad, thr, ps = next(c for c in CONV_CASES if c[0] == name)
         assert fin_task_form(B, Cout, H + 2 * pad - K + 1, W + 2 * pad - K + 1) == ("image", True), name
 
@@ -539,6 +542,26 @@ def test_stdp_parity(case):
     spk.spk_stdp(Wg, pad, dev(wave), dev(win), dev(nw), 0.004, -0.003)
     sync()
     assert_equal(host(Wg), orc.stdp(Wt, wave, pad, win, nw, 0.004, -0.003), "weights")
+
+
+@pytest.mark.parametrize("case", STDP_CASES)
+@pytest.mark.parametrize("images", ["batch", "one"])
+def test_stdp_first_spike_input(case, images):
+    # the layer input given by its first-spike map: the same updates as Eq.4 on its wave
+    wave, Wt, win, nw = layer_case(*case)
+    if images == "one":
+        wave, win, nw = wave[:1], win[:1], nw[:1]
+    T, pad = wave.shape[1], case[8]
+    tf = orc.first_spike(wave)
+    Wg = dev(Wt)
+    spk.spk_stdp_first_spike(Wg, pad, dev(tf), T, dev(win), dev(nw), 0.004, -0.003)
+    torch.cuda.synchronize()
+    assert_equal(host(Wg), orc.stdp(Wt, wave, pad, win, nw, 0.004, -0.003), "STDP weights")
+    reward = synth.rng(560, 0).choice(np.array([1, -1, 0], np.int8), wave.shape[0])
+    Wg = dev(Wt)
+    spk.spk_rstdp_first_spike(Wg, pad, dev(tf), T, dev(win), dev(nw), dev(reward), 0.004, -0.003)
+    torch.cuda.synchronize()
+    assert_equal(host(Wg), orc.stdp(Wt, wave, pad, win, nw, 0.004, -0.003, reward=reward), "R-STDP weights")
 
 
 @pytest.mark.parametrize("case", STDP_CASES)
