@@ -284,6 +284,62 @@ def ops_bench(wl, inp, dev, reps=10):
                       "global_batch": wl.B, "ops": res}), flush=True)
 
 
+def conv_variants_bench(wl, inp, dev, reps=10):
+    """The design choice of the contraction, measured: every finite-threshold conv
+    stage of the workload fed by a first-spike map, on the inputs one chain step
+    gives it, with the 16-bit weight split (the path the chain runs) and with the
+    dense fp32 form (spk_conv_fire_first_spike_f32mfma), full outputs.  Per form:
+    median device time of `reps` calls, its algorithmic bytes per second, the dense
+    contraction's rate (2 * T * positions * Cout * Cin * K^2 flops), and the two
+    forms' largest relative potential difference."""
+    import torch
+    import paper_1903_02440_amd as spk
+    from paper_1903_02440_amd.pipeline import chain_for
+    ch = chain_for(wl, inp["bank"], device=dev)
+    ch.set_weights([torch.from_numpy(w) for w in inp["weights"]])
+    ch.set_input(image=torch.from_numpy(inp["image"]), labels=torch.from_numpy(inp["labels"]))
+    ch.forward()
+    torch.cuda.synchronize()
+
+    def median_ms(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return sorted(ts)[len(ts) // 2]
+
+    res = {}
+    for i, st in enumerate(wl.stages):
+        if not hasattr(st, "cout") or math.isinf(st.thr) or ch.pre_tf[i] is None:
+            continue
+        x, b = ch.pre_tf[i], ch.bufs[i]
+        B, cin, h, w = x.shape
+        nb, ho, wo = conv_call_bytes(B, wl.T, cin, h, w, st, True)
+        flops = 2.0 * B * wl.T * ho * wo * st.cout * cin * st.K * st.K
+        outs = [tuple(torch.empty_like(b[k]) for k in ("P", "S", "tf", "vf")) for _ in range(2)]
+        forms = {"split16": spk.spk_conv_fire_first_spike, "f32mfma": spk.spk_conv_fire_first_spike_f32mfma}
+        r = {}
+        for (name, fn), o in zip(forms.items(), outs):
+            ms = median_ms(lambda: fn(x, wl.T, b["weight"], st.pad, st.thr, potentials=o[0], spikes=o[1],
+                                      t_first=o[2], v_first=o[3]))
+            r[name] = {"ms": round(ms, 4), "GB_per_s": round(nb / ms / 1e6, 1),
+                       "dense_TFLOP_per_s": round(flops / ms / 1e9, 1)}
+        Pa, Pb = outs[0][0].double(), outs[1][0].double()
+        rel = ((Pa - Pb).abs() / Pb.abs().clamp_min(1e-30)).max().item()
+        r["max_rel_potential_difference"] = rel
+        r["t_first_differences"] = int((outs[0][2] != outs[1][2]).sum().item())
+        res[f"conv{i}"] = r
+    print(json.dumps({"metric": "conv contraction forms: device time and rates", "workload": wl.name,
+                      "global_batch": wl.B, "algorithmic_bytes_per_call": "as the bench's roofline",
+                      "stages": res}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -301,6 +357,8 @@ def main():
                     help="only time online plasticity (one image per step, graph-replayed groups of "
                          "--online-group steps) over N images of the workload and exit (a separate figure)")
     ap.add_argument("--online-group", type=int, default=32, help="steps per captured graph with --online")
+    ap.add_argument("--conv-variants", action="store_true",
+                    help="time every finite-threshold conv stage with the 16-bit split and the dense fp32 form")
     ap.add_argument("--ops", action="store_true",
                     help="only time the variant ops (local normalisation, rank-order code, pointwise inhibition, "
                          "pooling of potentials) at the workload's shapes and exit (a separate figure)")
@@ -335,6 +393,9 @@ def main():
         return
     if args.ops:
         ops_bench(wl, inp, dev)
+        return
+    if args.conv_variants:
+        conv_variants_bench(wl, inp, dev)
         return
     if args.fused:
         args.compact = True

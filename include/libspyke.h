@@ -181,6 +181,17 @@ SPK_API int spk_conv_fire_first_spike_noalloc(const uint8_t *in_t_first, int B, 
              const float *weight, int Cout, int K, int pad, float threshold,
              float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first, void *stream);
 
+/* The same call as spk_conv_fire_first_spike with the contraction on fp32
+ * matrix cores (v_mfma_f32_16x16x4_f32): each fp32 weight is one term, each
+ * product with a spike exact, fp32 accumulation -- the dense fp32 form of the
+ * time-parallel convolution, kept as the alternative the 16-bit split is
+ * measured against.  threshold must be finite (SPK_E_ARG otherwise); all else
+ * as spk_conv_fire_first_spike.                                             */
+SPK_API int spk_conv_fire_first_spike_f32mfma(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+             const float *weight, int Cout, int K, int pad, float threshold,
+             float *potentials, uint8_t *spikes, uint8_t *t_first, float *v_first,
+             void *workspace, size_t ws_bytes, void *stream);
+
 /* One layer in one launch: convolution + firing (as
  * spk_conv_fire_first_spike) with the first-spike max-pooling of its output
  * (section "snn Module", Pooling, Eq.3, with window = stride = pool and no

@@ -58,6 +58,8 @@ _SIGS = {
     "spk_rstdp": (_I, [_P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _P, _P, _I, _P, _F, _F, _F, _F, _I, _P, _Z, _P]),
     "spk_decide": (_I, [_P, _P, _I, _I, _P, _I, _P, _P, _P]),
     "spk_count_events": (_I, [_P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
+    "spk_conv_fire_first_spike_f32mfma": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _F, _P, _P, _P, _P, _P, _Z,
+                                               _P]),
     "spk_conv_fire_pool": (_I, [_P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _F, _I, _P, _P, _P, _P, _P, _P, _P, _Z,
                                 _P]),
     "spk_conv_fire_strided_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
@@ -243,7 +245,7 @@ def _conv_call(x, times, T, weight, stride, pad, threshold, potentials, spikes, 
         _need(x, torch.uint8, (B, T, Cin, H, W), "wave")
     Cout, Cin2, K, _ = weight.shape
     _need(weight, torch.float32, (Cout, Cin, K, K), "weight")
-    s = 1 if stride is None else stride
+    s = 1 if stride in (None, "f32") else stride
     Ho, Wo = conv_out_size(H, K, pad, s), conv_out_size(W, K, pad, s)
     dev = x.device
     potentials = _out(potentials, (B, T, Cout, Ho, Wo), torch.float32, dev, "potentials")
@@ -251,7 +253,12 @@ def _conv_call(x, times, T, weight, stride, pad, threshold, potentials, spikes, 
     t_first = _out(t_first, (B, Cout, Ho, Wo), torch.uint8, dev, "t_first")
     v_first = _out(v_first, (B, Cout, Ho, Wo), torch.float32, dev, "v_first")
     outs = (_ptr(potentials), _ptr(spikes), _ptr(t_first), _ptr(v_first))
-    if stride is None:
+    if stride == "f32":
+        n = spk_conv_fire_workspace_size(B, T, Cin, H, W, Cout, K, pad)
+        ws = _ws(workspace, n, dev)
+        _check(_lib.spk_conv_fire_first_spike_f32mfma(_ptr(x), B, T, Cin, H, W, _ptr(weight), Cout, K, pad,
+                                                      float(threshold), *outs, _ptr(ws), n, _stream(stream)))
+    elif stride is None:
         n = spk_conv_fire_workspace_size(B, T, Cin, H, W, Cout, K, pad)
         ws = _ws(workspace, n, dev)
         fn = _lib.spk_conv_fire_first_spike if times else _lib.spk_conv_fire
@@ -307,6 +314,13 @@ def spk_conv_fire_pool(in_t_first, T, weight, pad, threshold, pool, potentials=F
                                    _ptr(pooled_t_first), _ptr(pooled_wave), _ptr(ws), n, _stream(stream)))
     none = lambda x: None if x is False else x  # noqa: E731
     return none(potentials), none(spikes), t_first, v_first, pooled_t_first, none(pooled_wave)
+
+
+def spk_conv_fire_first_spike_f32mfma(in_t_first, T, weight, pad, threshold, potentials=None, spikes=None,
+                                      t_first=None, v_first=None, workspace=None, stream=None):
+    """spk_conv_fire_first_spike with the contraction on fp32 matrix cores (one fp32 term per weight)."""
+    return _conv_call(in_t_first, True, T, weight, "f32", pad, threshold, potentials, spikes, t_first, v_first,
+                      workspace, stream)
 
 
 def spk_conv_fire_strided(wave, weight, stride, pad, threshold, potentials=None, spikes=None, t_first=None,

@@ -235,18 +235,23 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
 //     term is at least 2^-119, normal even times a spike's 2^-7.  A spike is
 //     2^-7 as bf16, so the sums are scaled by 2^(e - 7).
 // inv_s undoes the scale (a power of two, exact).
+// The fp32 form (arith == 1, finite threshold only: the dense fp32 contraction,
+// kept to compare with the split) takes the weights unscaled as one fp32 term
+// on v_mfma_f32_16x16x4_f32, eight products per 8-tap fragment.
+constexpr int WK_F16 = 0, WK_BF16 = 1, WK_F32 = 2;  // weight term kinds
 struct WSplit {
-    bool bf;
+    int kind;
     int e;
     float inv_s;
 };
 
-__device__ __forceinline__ WSplit weight_split(unsigned maxbits, unsigned minbits) {
+__device__ __forceinline__ WSplit weight_split(unsigned maxbits, unsigned minbits, int arith = 0) {
+    if (arith == 1) return {WK_F32, 0, 1.0f};
     const int E = maxbits ? (int)((maxbits >> 23) & 255u) - 127 : 0;  // subnormal maxima count as 2^-127
     if (E >= -100 && E <= 100 && minbits >= ((unsigned)(E - 15 + 127) << 23))
-        return {false, 12 - E, ldexpf(1.0f, E - 12)};
+        return {WK_F16, 12 - E, ldexpf(1.0f, E - 12)};
     const int e = 60 - max(E, -60);
-    return {true, e, ldexpf(1.0f, 7 - e)};
+    return {WK_BF16, e, ldexpf(1.0f, 7 - e)};
 }
 
 // Largest of the n maximum partials and smallest of the n minimum partials,
@@ -312,7 +317,7 @@ __device__ __forceinline__ void tap_of(const ConvGeom &g, int ks, int gq, int j,
 //
 // Fragment (nt, ks, lane) holds, for feature n = nt*16 + lane%16, the 8 taps
 // k = ks*32 + 8*(lane/16) + j, j = 0..7, as two 16-bit terms (each a uint4 of
-// 8 fp16 or bf16 values).  w holds the weights of features n0, n0 + 1, ...
+// 8 fp16 or bf16 values), or as 8 floats (taps 0-3, then 4-7) in the fp32 form.  w holds the weights of features n0, n0 + 1, ...
 // ([Cout - n0][Cin][K][K]).
 constexpr int NT = 2;  // 16-bit terms per weight
 
@@ -327,8 +332,12 @@ __device__ __forceinline__ void split_fragment(const float *w, int n0, const Con
         tap_of(g, ks, lane >> 4, j, kyx, ci);
         float v = 0.0f;
         if (n < g.Cout && kyx < KK && ci < g.Cin) v = ldexpf(w[((int64_t)(n - n0) * g.Cin + ci) * KK + kyx], s.e);
+        if (s.kind == WK_F32) {  // taps 0-3 in out[0], 4-7 in out[1], as floats
+            t[j >> 2][j & 3] = __float_as_uint(v);
+            continue;
+        }
         uint32_t h[NT];
-        if (!s.bf) {
+        if (s.kind == WK_F16) {
             const _Float16 hv = (_Float16)v;
             const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
             h[0] = __builtin_bit_cast(uint16_t, hv);
@@ -367,15 +376,16 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
                                                        const unsigned *__restrict__ wmax,
                                                        const unsigned *__restrict__ wmin, int n_wmax,
                                                        uint4 *__restrict__ frag, int2 *__restrict__ koff2,
-                                                       float *__restrict__ inv_scale, int *__restrict__ wbf16) {
+                                                       float *__restrict__ inv_scale, int *__restrict__ wbf16,
+                                                       int arith) {
     __shared__ unsigned red[8];
     const uint2 mm = reduce_wrange(wmax, wmin, n_wmax, red);
-    const WSplit ws = weight_split(mm.x, mm.y);
+    const WSplit ws = weight_split(mm.x, mm.y, arith);
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t total = (int64_t)g.ntiles * g.ksteps * 64;
     if (i == 0) {
         *inv_scale = ws.inv_s;
-        *wbf16 = ws.bf ? 1 : 0;
+        *wbf16 = ws.kind;
     }
     if (i < total) {
         const int lane = (int)(i & 63);
@@ -410,9 +420,9 @@ __device__ __forceinline__ u4 spike_operand(const uint32_t (&xn)[4], uint32_t ct
 __device__ __forceinline__ uint32_t step_const(int t) { return (0x6401u + (uint32_t)t) * 0x10001u; }
 
 // One 16x16x32 product of a spike operand with one weight term (fp16 or bf16).
-template <bool BF>
+template <int KIND>
 __device__ __forceinline__ f4 mfma(u4 a, uint4 b, f4 c) {
-    if constexpr (!BF)
+    if constexpr (KIND == WK_F16)
         return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a), __builtin_bit_cast(half8, b), c, 0,
                                                       0, 0);
     else
@@ -482,13 +492,18 @@ struct PoolOut {
     uint8_t *wave;  // pooled Eq.1 wave [B][T][Cout][Hpo][Wpo], or null
 };
 
-template <int G, bool BLDS, bool ALDS>
+// Kernel forms: the 16-bit split (FIN_SPLIT), the split with fused pooling
+// (FIN_POOL) and the fp32 form (FIN_F32), each compiled on its own so that the
+// code of the others costs the plain form no registers.
+constexpr int FIN_SPLIT = 0, FIN_POOL = 1, FIN_F32 = 2;
+
+template <int G, bool BLDS, bool ALDS, int MODE>
 __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
     const uint8_t *__restrict__ tpad, const uint4 *__restrict__ frag, const int2 *__restrict__ koff2, ConvGeom g,
     int n_pairs, int n_chunks, int cpi, int chunk_tiles, int band_pos, int np_max, int a_words,
     const float *__restrict__ inv_scale, const int *__restrict__ wbf16, const float *__restrict__ wts,
     const unsigned *__restrict__ wmax, const unsigned *__restrict__ wmin, int n_wmax, float *__restrict__ P,
-    uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF, PoolOut po) {
+    uint8_t *__restrict__ S, uint8_t *__restrict__ TF, float *__restrict__ VF, PoolOut po, int arith) {
     extern __shared__ uint4 lds[];
     const int tid = threadIdx.x, wv = tid >> 6, lane = tid & 63;
     const int gq = lane >> 4, c = lane & 15;
@@ -574,13 +589,13 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         for (int i = tid; i < g.ksteps * 4; i += FIN_THREADS) koff_l[i] = koff_of(g, i);
     }
     float inv_s;
-    bool use_bf;
+    int kind;
     if (BLDS) {  // the pair's fragments, split here from the weights: [ks][n][term][64]
         // (the staging area, unused until the main loop, holds the reduction's words)
         const uint2 mm = reduce_wrange(wmax, wmin, n_wmax, reinterpret_cast<unsigned *>(stage));
-        const WSplit ws = weight_split(mm.x, mm.y);
+        const WSplit ws = weight_split(mm.x, mm.y, arith);
         inv_s = ws.inv_s;
-        use_bf = ws.bf;
+        kind = ws.kind;
         // the pair's weights, contiguous in W, go through the staging area when
         // they fit (coalesced loads instead of one load per tap)
         const int per_f = g.Cin * g.K * g.K, nwp = nf * per_f;
@@ -599,7 +614,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         }
     } else {
         inv_s = *inv_scale;
-        use_bf = *wbf16 != 0;
+        kind = *wbf16;
     }
     if (ALDS) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -610,11 +625,11 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         // Every wave computes up to two tiles of 16 positions for the 32 features;
         // positions of a tile past the chunk repeat its last position and are
         // never stored, which keeps the MFMA stream free of branches.  The K-step
-        // loop is compiled once per term type (fp16 / bf16) and second-slot mode
-        // (below).
+        // loop is compiled once per term kind (fp16 / bf16 / fp32) and second-slot
+        // mode (below).
         const uint4 *gf = frag + (int64_t)(pair * 2) * g.ksteps * NT * 64 + lane;
-        auto mfma_waves = [&](auto bf_c) {
-        constexpr bool BF = decltype(bf_c)::value;
+        auto mfma_waves = [&](auto kind_c) {
+        constexpr int KIND = decltype(kind_c)::value;
         int abuf_sel = 0;
         for (int task = t_lo + r; task < t_hi; task += R) {
             int pos0, np;
@@ -712,6 +727,34 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                 };
                 // one K-step: spike operands from the words, then TB x 4 tiles x 2 features x NT terms
                 auto kstep = [&](const uint32_t (&an)[FIN_MT][2], const uint4 (&bc)[2 * NT]) {
+                    if constexpr (KIND == WK_F32) {
+                        // fp32 form: instruction j takes tap 8*(lane/16) + j of every lane
+                        // group, spike 1.0f / 0.0f against that tap's weight
+#pragma unroll
+                        for (int t = 0; t < TB; ++t) {
+                            const int tt = tb0 + t;
+                            float af[FIN_MT][8];
+#pragma unroll
+                            for (int i = 0; i < MT; ++i)
+#pragma unroll
+                                for (int j = 0; j < 8; ++j)
+                                    af[i][j] = (int)((an[i][j >> 2] >> (8 * (j & 3))) & 255u) <= tt ? 1.0f : 0.0f;
+#pragma unroll
+                            for (int j = 0; j < 8; ++j)
+#pragma unroll
+                                for (int i = 0; i < MT; ++i)
+#pragma unroll
+                                    for (int n = 0; n < 2; ++n)
+                                        if (fin_unit<M>(i, n)) {
+                                            const uint4 b4 = bc[n * NT + (j >> 2)];
+                                            const uint32_t bw = (j & 3) == 0 ? b4.x : (j & 3) == 1 ? b4.y
+                                                              : (j & 3) == 2 ? b4.z : b4.w;
+                                            acc[i][n][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                                af[i][j], __uint_as_float(bw), acc[i][n][t], 0, 0, 0);
+                                        }
+                        }
+                        return;
+                    }
                     uint32_t xn[FIN_MT][4];
 #pragma unroll
                     for (int i = 0; i < MT; ++i) {
@@ -732,7 +775,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 #pragma unroll
                                 for (int n = 0; n < 2; ++n)
                                     if (fin_unit<M>(i, n))
-                                        acc[i][n][t] = mfma<BF>(a[i], bc[n * NT + q], acc[i][n][t]);
+                                        acc[i][n][t] = mfma<KIND>(a[i], bc[n * NT + q], acc[i][n][t]);
                     }
                 };
                 uint32_t a0[FIN_MT][2], a1[FIN_MT][2];
@@ -808,11 +851,15 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             abuf_sel ^= 1;
         }
         };
-        if (use_bf)
-            mfma_waves(std::integral_constant<bool, true>{});
-        else
-            mfma_waves(std::integral_constant<bool, false>{});
-        if (po.P > 0) __syncthreads();  // the store waves' last pooled map is complete in LDS
+        if constexpr (MODE == FIN_F32) {
+            mfma_waves(std::integral_constant<int, WK_F32>{});
+        } else {
+            if (kind == WK_BF16)
+                mfma_waves(std::integral_constant<int, WK_BF16>{});
+            else
+                mfma_waves(std::integral_constant<int, WK_F16>{});
+        }
+        if (MODE == FIN_POOL) __syncthreads();  // the store waves' last pooled map is complete in LDS
     } else {
         // ------------------------------------------------ store waves
         const int s = tid - FIN_CW * 64;
@@ -821,7 +868,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
         // positions; outputs of consecutive threads are consecutive in xo.
         int pend_pos0 = -1, pend_np = 0;
         auto pool_pending = [&]() {
-            if (pend_pos0 < 0) return;
+            if (MODE != FIN_POOL || pend_pos0 < 0) return;
             const int64_t pplane = (int64_t)po.Hpo * po.Wpo, wplane = (int64_t)g.Cout * pplane;
             // one segment per image the task covers (whole rows; a segment starts at
             // a row that is a multiple of P)
@@ -970,19 +1017,19 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                     TFt[o] = (uint8_t)tf4[m];
                     VFt[o] = vfirst[m][0];
                 }
-                if (po.P > 0) {  // this task's map for pooling (read after the next barrier)
+                if (MODE == FIN_POOL) {  // this task's map for pooling (read after the next barrier)
                     if (G == 4)
                         *reinterpret_cast<uint32_t *>(pool_l + fl * np_max + pl) = tf4[m];
                     else
                         pool_l[fl * np_max + pl] = (uint8_t)tf4[m];
                 }
             }
-            if (po.P > 0) {
+            if (MODE == FIN_POOL) {
                 pend_pos0 = pos0;
                 pend_np = np;
             }
         }
-        if (po.P > 0) {
+        if (MODE == FIN_POOL) {
             __syncthreads();  // matches the MFMA waves' last barrier
             pool_pending();
         }
@@ -1026,7 +1073,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     const int gq = lane >> 4, c = lane & 15;
     for (int i = tid; i < g.ksteps * 4; i += (INF_WAVES + INF_ZW) * 64) koff_l[i] = koff2[i];
     const float inv_s = *inv_scale;
-    const bool use_bf = *wbf16 != 0;
+    const bool use_bf = *wbf16 == WK_BF16;
     const uint32_t ct = step_const(g.T - 1);
     const int x = blockIdx.x % 8, j = blockIdx.x / 8, per_xcd = (int)gridDim.x / 8;
     const int ntask = n_mb * n_ng * ksplit, per_x = (ntask + 7) / 8;
@@ -1085,7 +1132,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     }
 
     auto mfma_waves = [&](auto bf_c) {
-    constexpr bool BF = decltype(bf_c)::value;
+    constexpr int KIND = decltype(bf_c)::value ? WK_BF16 : WK_F16;
     constexpr int KC = INF_KC;
     constexpr int CHUNK_U4 = INF_CHUNK_U4;
     for (int task = t_lo + j; task < t_hi; task += per_xcd) {
@@ -1193,7 +1240,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
 #pragma unroll
                     for (int i = 0; i < INF_MW; ++i)
 #pragma unroll
-                        for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma<BF>(a[i], bt[q][n], acc[i][n]);
+                        for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma<KIND>(a[i], bt[q][n], acc[i][n]);
             }
         };
         __syncthreads();  // the buffers are free (previous task done), koff is visible
@@ -1384,16 +1431,16 @@ int max_lds_per_block() {
     return v;
 }
 
-template <int G, bool BLDS, bool ALDS>
+template <int G, bool BLDS, bool ALDS, int MODE>
 void launch_fin(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const float *inv_scale, const int *wbf16,
                 const float *wts, const unsigned *wmax, const unsigned *wmin, int n_wmax, const ConvGeom &g,
                 int n_pairs, int n_chunks, int cpi, int chunk_tiles, int band_pos, int np_max, int a_words, size_t lds,
-                float *P, uint8_t *S, uint8_t *TF, float *VF, const PoolOut &po, hipStream_t st) {
+                float *P, uint8_t *S, uint8_t *TF, float *VF, const PoolOut &po, int arith, hipStream_t st) {
     // one workgroup per CU: a multiple of the feature pairs on every XCD
     const int per_xcd = (int)spk::ceil_div(std::max(32, n_pairs), n_pairs) * n_pairs;
-    hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
+    hipLaunchKernelGGL((k_conv_fire_fin<G, BLDS, ALDS, MODE>), dim3((unsigned)(per_xcd * 8)), dim3(FIN_THREADS), lds, st,
                        tpad, frag, koff2, g, n_pairs, n_chunks, cpi, chunk_tiles, band_pos, np_max, a_words, inv_scale,
-                       wbf16, wts, wmax, wmin, n_wmax, P, S, TF, VF, po);
+                       wbf16, wts, wmax, wmin, n_wmax, P, S, TF, VF, po, arith);
 }
 
 template <bool VEC>
@@ -1438,13 +1485,14 @@ namespace {
 int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int W, const float *weight, int Cout,
               int K, int stride, int pad, float threshold, float *potentials, uint8_t *spikes, uint8_t *t_first,
               float *v_first, void *workspace, size_t ws_bytes, void *stream,
-              PoolOut pool = PoolOut{0, 0, 0, 0, nullptr, nullptr}) {
+              PoolOut pool = PoolOut{0, 0, 0, 0, nullptr, nullptr}, int arith = 0) {
     ConvPlan pl;
     int rc = make_plan(B, T, Cin, H, W, Cout, K, stride, pad, pl);
     if (rc != SPK_OK) return rc;
     SPK_REQUIRE(!std::isnan(threshold) && !(std::isinf(threshold) && threshold < 0), SPK_E_ARG,
                 "spk_conv_fire: threshold must be a number or +INFINITY");
     const bool inf_mode = std::isinf(threshold);
+    SPK_REQUIRE(arith == 0 || !inf_mode, SPK_E_ARG, "spk_conv_fire: the fp32 form needs a finite threshold");
     // 4-element store groups need aligned outputs and groups that never straddle a task
     bool vec = (pl.g.HoWo % 4) == 0 && ((uintptr_t)potentials & 15) == 0 && ((uintptr_t)v_first & 15) == 0 &&
                ((uintptr_t)spikes & 3) == 0 && ((uintptr_t)t_first & 3) == 0;
@@ -1602,7 +1650,7 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     if (inf_mode || !blds) {  // fragments in the workspace (the finite-threshold kernel with LDS room builds its own)
         const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
         hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, wmax,
-                           wmin, n_wmax, frag, koff2, inv_scale, wbf16);
+                           wmin, n_wmax, frag, koff2, inv_scale, wbf16, arith);
     }
     if (inf_mode) {
         if (vec)
@@ -1612,10 +1660,21 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
             launch_inf<false>(tpad, frag, koff2, inv_scale, wbf16, g, pl.ksplit, pl.kpp, part, potentials, spikes,
                               t_first, v_first, st);
     } else {
-#define SPK_FIN(G, BL, AL)                                                                                    \
-    launch_fin<G, BL, AL>(tpad, frag, koff2, inv_scale, wbf16, weight, wmax, wmin, n_wmax, g, n_pairs, n_chunks, \
-                          cpi, chunk_tiles, band_pos, np_max, a_words, fin_lds, potentials, spikes, t_first, v_first, \
-                          pool, st)
+#define SPK_FIN(G, BL, AL)                                                                                        \
+    do {                                                                                                          \
+        if (arith == 1)                                                                                           \
+            launch_fin<G, BL, AL, FIN_F32>(tpad, frag, koff2, inv_scale, wbf16, weight, wmax, wmin, n_wmax, g,      \
+                                           n_pairs, n_chunks, cpi, chunk_tiles, band_pos, np_max, a_words, fin_lds, \
+                                           potentials, spikes, t_first, v_first, pool, arith, st);                  \
+        else if (pooled)                                                                                          \
+            launch_fin<G, BL, AL, FIN_POOL>(tpad, frag, koff2, inv_scale, wbf16, weight, wmax, wmin, n_wmax, g,     \
+                                            n_pairs, n_chunks, cpi, chunk_tiles, band_pos, np_max, a_words,         \
+                                            fin_lds, potentials, spikes, t_first, v_first, pool, arith, st);        \
+        else                                                                                                      \
+            launch_fin<G, BL, AL, FIN_SPLIT>(tpad, frag, koff2, inv_scale, wbf16, weight, wmax, wmin, n_wmax, g,    \
+                                             n_pairs, n_chunks, cpi, chunk_tiles, band_pos, np_max, a_words,        \
+                                             fin_lds, potentials, spikes, t_first, v_first, pool, arith, st);       \
+    } while (0)
         const int sel = (vec ? 4 : 0) + (blds ? 2 : 0) + (alds ? 1 : 0);
         switch (sel) {
             case 0: SPK_FIN(1, false, false); break;
@@ -1646,6 +1705,14 @@ extern "C" int spk_conv_fire_first_spike(const uint8_t *in_t_first, int B, int T
                                          void *workspace, size_t ws_bytes, void *stream) {
     return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, 1, pad, threshold, potentials, spikes,
                      t_first, v_first, workspace, ws_bytes, stream);
+}
+
+extern "C" int spk_conv_fire_first_spike_f32mfma(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,
+                                                 const float *weight, int Cout, int K, int pad, float threshold,
+                                                 float *potentials, uint8_t *spikes, uint8_t *t_first,
+                                                 float *v_first, void *workspace, size_t ws_bytes, void *stream) {
+    return conv_fire(in_t_first, true, B, T, Cin, H, W, weight, Cout, K, 1, pad, threshold, potentials, spikes,
+                     t_first, v_first, workspace, ws_bytes, stream, PoolOut{0, 0, 0, 0, nullptr, nullptr}, 1);
 }
 
 extern "C" int spk_conv_fire_pool(const uint8_t *in_t_first, int B, int T, int Cin, int H, int W,

@@ -22,7 +22,7 @@ def declared():
 
 def test_every_declared_symbol_is_exported():
     names = declared()
-    assert len(names) == 33
+    assert len(names) == 34
     lib = spk.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -186,4 +186,11 @@ def test_fused_layer_validation():
     assert call(W=300, pool=2) == spk.SPK_E_RANGE       # a 2-row band of 300 positions
     assert call(ptf=None) == spk.SPK_E_ARG
     assert call(B=0, ptf=None) == spk.SPK_OK
+
+
+def test_f32mfma_form_needs_a_finite_threshold():
+    lib = spk.lib()
+    rc = lib.spk_conv_fire_first_spike_f32mfma(DUMMY, 1, 15, 6, 28, 28, DUMMY2, 30, 5, 2, ctypes.c_float(math.inf),
+                                               None, None, DUMMY, DUMMY2, DUMMY, 1 << 30, None)
+    assert rc == spk.SPK_E_ARG and b"fp32" in lib.spk_last_error()
 

@@ -155,6 +155,29 @@ def test_conv_fire_first_spike_input(case, near_log):
     near_log(f"conv first-spike input {name}", compare_conv_fire(tuple(host(x) for x in got), ref, thr), ref[2].size)
 
 
+@pytest.mark.parametrize("case", [c for c in CONV_CASES if not math.isinf(c[9])], ids=lambda c: c[0])
+@pytest.mark.parametrize("kind", ["normal", "dyadic", "loguniform"])
+def test_conv_fire_f32mfma_parity(case, kind, near_log):
+    # the dense fp32 form of the contraction: the oracle's potentials within 1e-5 (exactly
+    # summable weights: bit-exact), spikes and first-spike times under the parity rules
+    name, B, T, Cin, H, W, Cout, K, pad, thr, ps = case
+    g = synth.rng(160 + len(name), 1)
+    tf = synth.times_uniform_or_silent(g, (B, Cin, H, W), T, ps)
+    if kind == "dyadic":
+        Wt = synth.dyadic_weights(g, (Cout, Cin, K, K), Cin * K * K)
+    elif kind == "loguniform":
+        Wt = synth.loguniform_weights(g, (Cout, Cin, K, K), 12.0, 0.1)
+        thr = 0.37
+    else:
+        Wt = synth.normal_weights(g, (Cout, Cin, K, K), 0.8, 0.05)
+    got = spk.spk_conv_fire_first_spike_f32mfma(dev(tf), T, dev(Wt), pad, thr)
+    sync()
+    ref = orc.conv_fire(wave_of(tf, T), Wt, pad, thr)
+    near_log(f"conv f32mfma {name}/{kind}",
+             compare_conv_fire(tuple(host(x) for x in got), ref, thr, exact_potentials=(kind == "dyadic")),
+             ref[2].size)
+
+
 # Weight ranges that the 16-bit terms of the contraction must carry: the
 # layer shapes of the workloads (finite threshold and Eq.5), the natural
 # layer whose fragments are read from the workspace, and a ragged small case.
