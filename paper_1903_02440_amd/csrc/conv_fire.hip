@@ -1103,17 +1103,19 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             nint += 1 + max(0, c_hi - c_lo);
         }
         const int64_t per = (total + nint - 1) / nint;
-        int64_t u0 = 0;
+        // lane zt writes units zt, zt + 256, ... in order, as (image im, unit r of it)
+        const int64_t zpz = zp + zs;
+        int64_t u0 = 0, cu = zt, cim = zpz > 0 ? cu / zpz : 0, cr = cu - cim * zpz;
         auto slice = [&]() {
             if (!VEC) return;  // a separate fill kernel writes the zeros
             const int64_t u1 = min(total, u0 + per);
-            for (int64_t u = u0 + zt; u < u1; u += INF_ZW * 64) {
-                const int64_t im = u / (zp + zs), r = u - im * (zp + zs);
-                const int64_t b = blockIdx.x + im * gridDim.x;
-                if (r < zp)
-                    *reinterpret_cast<f4 *>(P + b * g.T * tstride + 4 * r) = f4{0.f, 0.f, 0.f, 0.f};
+            for (; cu < u1; cu += INF_ZW * 64) {
+                const int64_t b = blockIdx.x + cim * gridDim.x;
+                if (cr < zp)
+                    *reinterpret_cast<f4 *>(P + b * g.T * tstride + 4 * cr) = f4{0.f, 0.f, 0.f, 0.f};
                 else
-                    *reinterpret_cast<uint32_t *>(S + b * g.T * tstride + 4 * (r - zp)) = 0u;
+                    *reinterpret_cast<uint32_t *>(S + b * g.T * tstride + 4 * (cr - zp)) = 0u;
+                for (cr += INF_ZW * 64; zpz > 0 && cr >= zpz; ++cim) cr -= zpz;
             }
             u0 = u1;
         };
