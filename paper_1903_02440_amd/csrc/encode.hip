@@ -4,24 +4,25 @@
 // image, Intensity2Latency = rank-order coding), the threshold semantics of
 // the "functional Module", and Eq.1 (cumulative spike wave).
 //
-// spk_encode_latency runs three kernels on the caller's stream:
+// spk_encode_latency, for maps of C*H*W <= SMALL_MAX entries whose padded
+// image fits in LDS (the MNIST-sized and other small inputs), is one kernel,
+// k_encode_small (one workgroup per image): filter, rank-order bins by radix
+// select, t_first and wave, with the intensity map never leaving LDS (it is
+// written out only when the caller asks for it).  Otherwise three kernels:
 //   1. k_filter: same-size cross-correlation of each u8 image with the C
 //      filters (double accumulation over the non-zero taps, one rounding to
 //      float, then values below the threshold set to 0).  One workgroup per
 //      (image, band of rows: the whole image when it fits) stages the
 //      zero-padded band in LDS and computes all channels.
-//   2. k_rank_select: one workgroup per image finds the T-1 bin boundaries of
-//      the rank-order code by an MSD radix select (8 passes of 8 bits) on the
-//      unique 64-bit keys  (float bits of I) << 32 | ~index  of the positive
-//      intensities; all boundaries share each pass's digit histograms.
+//   2. rank-order bins: k_encode_small without its filter step when the map
+//      has <= SMALL_MAX entries; else k_rank_select, one workgroup per image
+//      finding the T-1 bin boundaries by an MSD radix select (8 passes of 8
+//      bits) on the unique 64-bit keys  (float bits of I) << 32 | ~index  of
+//      the positive intensities, all boundaries sharing each pass's digit
+//      histograms, and
 //   3. k_expand_latency: every entry counts the boundaries its key does not
 //      exceed -- that count is its bin floor(rho*T/n) -- and writes t_first
 //      and the T planes of the wave (4 entries per thread, u32 stores).
-// When C*H*W <= SORT_MAX, steps 2 and 3 are one kernel instead,
-// k_rank_sort: one workgroup per image gathers the keys of the positive
-// intensities into LDS, sorts them (bitonic network over the next power of two
-// of their count), gives the entry at rank rho the bin floor(rho*T/n) in an
-// LDS map of t_first, and writes t_first and the wave from that map.
 #include <algorithm>
 
 #include "common.hpp"
@@ -32,8 +33,8 @@ constexpr int MAX_KF = 31;
 constexpr int SEL_THREADS = 1024;
 constexpr int MAX_GROUPS = 32;   // bin boundaries resolved per select batch
 constexpr int LDS_KEYS = 12288;  // intensities cached in LDS when N fits
-constexpr int SORT_MAX = 8192;   // entries per image sorted in LDS
-constexpr int SORT_THREADS = 1024;
+constexpr int SMALL_MAX = 8192;  // entries per image coded by one k_encode_small workgroup
+constexpr size_t SMALL_LDS = 60 * 1024;  // its dynamic LDS at most
 
 // ------------------------------------------------------------------ filter
 // LDS holds the taps and the zero-padded band of the image as doubles, so the
@@ -310,78 +311,511 @@ __global__ __launch_bounds__(256) void k_expand_latency(const float *__restrict_
     }
 }
 
-// ------------------------------------------------------------------ rank by sorting (small images)
-__global__ __launch_bounds__(SORT_THREADS) void k_rank_sort(const float *__restrict__ inten, int N, int T,
-                                                            uint8_t *__restrict__ tf_out, uint8_t *__restrict__ wave) {
-    __shared__ uint64_t key[SORT_MAX];
-    __shared__ uint8_t tmap[SORT_MAX];
-    __shared__ int npos;
-    const int b = blockIdx.x, tid = threadIdx.x;
-    const float *I = inten + (int64_t)b * N;
-    if (tid == 0) npos = 0;
-    for (int i = tid; i < N; i += SORT_THREADS) tmap[i] = (uint8_t)T;
-    __syncthreads();
-    // gather the positive entries' keys (their order in LDS does not matter: keys are
-    // unique); every load of the thread is issued before the first is used
-    float vin[SORT_MAX / SORT_THREADS];
+// ------------------------------------------------------------------ one workgroup per image (small maps)
+// k_encode_small: for C*H*W <= SMALL_MAX one workgroup of ENC_THREADS threads
+// per image keeps the intensity map in LDS and does the whole code there:
+//   1. (FILTER) the filter: the zero-padded image (float) and the taps (double)
+//      in LDS; a work item is (channel, row, group of 8 columns) with the
+//      lanes of a wave on consecutive rows, so their pixel reads fall in
+//      distinct banks (odd row stride), and the channels taken in decreasing
+//      order of their non-zero tap area.  Each output is accumulated in double
+//      in ky-then-kx order over the channel's non-zero taps and rounded once.
+//      A channel whose taps are exactly the negated taps of the channel before
+//      it (the on/off pairs of a DoG bank) is not computed: its sum is the
+//      exact negation, so its float is -v (+0 where v is 0).
+//      (!FILTER) the intensities are loaded instead.
+//   2. the T-1 bin boundaries: the keys at ranks ceil((j+1) n / T) of the
+//      positive entries in descending key order, key = float bits << 13 |
+//      (8191 - index) (unique; equal intensities rank in index order), found
+//      by an MSD radix select over the 44 key bits -- a 12-bit digit, then four
+//      8-bit digits -- resolving up to SEL_T boundaries at once, with 16-bit
+//      counters packed in pairs.  A boundary's digit is found by the thread
+//      that holds the digit's suffix count in registers.  The first 8-bit
+//      digit looks the entries' groups up in a table of the 12-bit prefixes;
+//      later digits revisit only the entries that matched (a candidate list,
+//      or all entries when it overflows).
+//   3. every entry's bin = the number of boundaries its key does not exceed,
+//      i.e. floor(rho T / n) for rank rho (T for entries <= 0); t_first and the
+//      T planes of the wave are written as 4-entry words.
+constexpr int ENC_THREADS = 256;
+constexpr int SEL_T = 16;        // boundaries resolved per select batch
+constexpr int HBINS = 4096;      // first digit: 12 bits
+constexpr int LCAP = 1024;       // candidate list capacity (entries)
+constexpr int KCAP = LCAP / 2;   // keys of the targets' first digits ranked directly (same LDS)
+constexpr int MAX_DERIV_C = 64;  // negated-channel detection and cost order for at most this many channels
+
+__device__ __forceinline__ uint64_t key44(float v, int i) {
+    return ((uint64_t)__float_as_uint(v) << 13) | (uint64_t)(8191 - i);
+}
+
+struct SmallFilter {
+    int H, W, C, KF, Wp, nxg;  // image, channels, filter size, staged row stride (odd), 8-column groups
+};
+
+__host__ __device__ inline size_t up16(size_t v) { return (v + 15) & ~(size_t)15; }
+__host__ __device__ inline int small_filter_wp(int W, int KF) {
+    const int nxg = (W + 7) / 8;
+    return (8 * nxg + KF + 6) | 1;
+}
+__host__ __device__ inline size_t small_filter_bytes(int H, int W, int C, int KF) {
+    const size_t taps = (size_t)C * KF * KF * sizeof(double);
+    const size_t img = (size_t)(H + KF - 1) * small_filter_wp(W, KF) * sizeof(float);
+    return taps + up16(img) + (size_t)6 * C * sizeof(int);
+}
+// packed counters (SEL_T groups x 256 digits, or the 4096 first digits, as
+// 16-bit halves), the 12-bit prefix table, two candidate lists
+constexpr size_t SEL_HIST = (size_t)SEL_T * 256 * 2;
+__host__ __device__ inline size_t small_select_bytes() { return SEL_HIST + HBINS + (size_t)2 * LCAP * 2; }
+
+__device__ __forceinline__ int tap_area(const int *bbox, int c) {
+    return max(0, bbox[4 * c + 1] - bbox[4 * c] + 1) * max(0, bbox[4 * c + 3] - bbox[4 * c + 2] + 1);
+}
+struct FiltCtx {
+    int H, W, C, KF, Wp;
+    float thr;
+    const double *fd;   // taps
+    const float *sim;   // zero-padded image, row stride Wp
+    const int *bbox, *deriv;
+    float *Ic, *gout;   // intensities in LDS, optionally in global memory
+};
+
+// 8 consecutive outputs of row y, columns 8*xg.., of channel c (and of the
+// negated channel after it): double sums in ky-then-kx order over the non-zero
+// taps, one rounding, the threshold.  Returns the number of positive outputs.
+__device__ __forceinline__ int filter_item(const FiltCtx &fx, int c, int xg, int y) {
+    constexpr int CW = 8;
+    const int KK = fx.KF * fx.KF;
+    const int ya = fx.bbox[4 * c], yb = fx.bbox[4 * c + 1], xa = fx.bbox[4 * c + 2], xb = fx.bbox[4 * c + 3];
+    const double *fc = fx.fd + c * KK;
+    double acc[CW];
 #pragma unroll
-    for (int r = 0; r < SORT_MAX / SORT_THREADS; ++r) {
-        const int i = r * SORT_THREADS + tid;
-        vin[r] = i < N ? I[i] : 0.0f;
-    }
+    for (int j = 0; j < CW; ++j) acc[j] = 0.0;
+    for (int ky = ya; ky <= yb; ++ky) {
+        const float *row = fx.sim + (y + ky) * fx.Wp + CW * xg;
+        for (int kx0 = xa; kx0 <= xb; kx0 += 8) {
+            double a[CW + 7];
 #pragma unroll
-    for (int r = 0; r < SORT_MAX / SORT_THREADS; ++r) {
-        const int i = r * SORT_THREADS + tid;
-        const float v = vin[r];
-        const bool pos = v > 0.0f;
-        const uint64_t m = __ballot(pos);
-        int base = 0;
-        if ((tid & 63) == 0 && m) base = atomicAdd(&npos, __popcll(m));
-        base = __shfl(base, 0, 64);
-        if (pos) key[base + __popcll(m & ((1ull << (tid & 63)) - 1ull))] = make_key(v, (uint32_t)i);
+            for (int q = 0; q < CW + 7; ++q) a[q] = (double)row[kx0 + q];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                if (kx0 + u > xb) break;
+                const double f = fc[ky * fx.KF + kx0 + u];
+#pragma unroll
+                for (int j = 0; j < CW; ++j) acc[j] = fma(f, a[u + j], acc[j]);
+            }
+        }
+    }
+    const bool dn = c + 1 < fx.C && fx.deriv[c + 1];
+    const int HW = fx.H * fx.W;
+    int npos = 0;
+#pragma unroll
+    for (int j = 0; j < CW; ++j) {
+        const int x = CW * xg + j;
+        if (x >= fx.W) break;
+        const float v = (float)acc[j];
+        const float o = v < fx.thr ? 0.0f : v;
+        const int e = (c * fx.H + y) * fx.W + x;
+        fx.Ic[e] = o;
+        npos += o > 0.0f;
+        if (fx.gout) fx.gout[e] = o;
+        if (dn) {
+            const float w = v == 0.0f ? 0.0f : -v;
+            const float o2 = w < fx.thr ? 0.0f : w;
+            fx.Ic[e + HW] = o2;
+            npos += o2 > 0.0f;
+            if (fx.gout) fx.gout[e + HW] = o2;
+        }
+    }
+    return npos;
+}
+
+template <bool FILTER>
+__global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__restrict__ img, SmallFilter fg,
+                                                             const float *__restrict__ filt, float thr,
+                                                             const float *__restrict__ inten_in, int N, int T,
+                                                             float *__restrict__ inten_out,
+                                                             uint8_t *__restrict__ tf_out, uint8_t *__restrict__ wave) {
+    static_assert(HBINS / 2 <= SEL_HIST / 4 && HBINS == 16 * ENC_THREADS, "first-digit counters");
+    extern __shared__ uint4 lds4[];
+    float *Ic = reinterpret_cast<float *>(lds4);  // N intensities
+    unsigned char *r2 = reinterpret_cast<unsigned char *>(lds4) + up16((size_t)N * 4);
+    __shared__ uint64_t kb[256];              // bin boundaries, zero past the last
+    __shared__ uint64_t tpre[2][SEL_T];       // per target: digits found so far (by pass parity)
+    __shared__ uint32_t trank[2][SEL_T];      // per target: rank among the keys with that prefix
+    __shared__ uint64_t gpre[SEL_T];          // distinct target prefixes, descending
+    __shared__ int tgrp[SEL_T];
+    __shared__ uint32_t tcnt[SEL_T];          // per target: entries with its first digit
+    __shared__ uint32_t gstart[SEL_T + 1], gcur[SEL_T];
+    __shared__ int s_n, s_m, s_ng, s_total, s_lc[2], s_wsum[ENC_THREADS / 64];
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    if (tid == 0) s_n = 0;
+    for (int j = tid; j < 256; j += ENC_THREADS) kb[j] = 0;
+    int npos = 0;
+
+    if constexpr (FILTER) {
+        const int H = fg.H, W = fg.W, C = fg.C, KF = fg.KF, Wp = fg.Wp, nxg = fg.nxg, KK = KF * KF;
+        const int p = (KF - 1) / 2, Hs = H + KF - 1;
+        double *fd = reinterpret_cast<double *>(r2);
+        float *sim = reinterpret_cast<float *>(r2 + (size_t)C * KK * sizeof(double));
+        int *bbox = reinterpret_cast<int *>(reinterpret_cast<unsigned char *>(sim) + up16((size_t)Hs * Wp * sizeof(float)));
+        int *deriv = bbox + 4 * C;  // 1: the exact negation of the channel before, not computed
+        int *order = deriv + C;     // computed channels, largest tap area first
+        __shared__ int s_ncomp;
+        for (int i = tid; i < C * KK; i += ENC_THREADS) fd[i] = (double)filt[i];
+        const uint8_t *im = img + (int64_t)b * H * W;
+        for (int i = tid; i < Hs * Wp; i += ENC_THREADS) {
+            const int r = i / Wp, xp = i - r * Wp;
+            const int y = r - p, x = xp - p;
+            sim[i] = (y >= 0 && y < H && x >= 0 && x < W) ? (float)im[y * W + x] : 0.0f;
+        }
+        __syncthreads();
+        // per channel (one wave each): bounding box of the non-zero taps, and
+        // whether the taps are the exact negation of the previous channel's
+        for (int c = wid; c < C; c += ENC_THREADS / 64) {
+            int ya = KF, yb = -1, xa = KF, xb = -1;
+            bool neg = c > 0 && C <= MAX_DERIV_C;
+            for (int i = lane; i < KK; i += 64) {
+                const double f = fd[c * KK + i];
+                if (f != 0.0) {
+                    const int ky = i / KF, kx = i - ky * KF;
+                    ya = min(ya, ky); yb = max(yb, ky); xa = min(xa, kx); xb = max(xb, kx);
+                }
+                if (c > 0) neg = neg && (f == -fd[(c - 1) * KK + i]);
+            }
+            ya = wave_min_i32(ya); yb = wave_max_i32(yb); xa = wave_min_i32(xa); xb = wave_max_i32(xb);
+            const bool all_neg = __ballot(!neg) == 0;
+            if (lane == 0) {
+                bbox[4 * c] = ya; bbox[4 * c + 1] = yb; bbox[4 * c + 2] = xa; bbox[4 * c + 3] = xb;
+                deriv[c] = all_neg ? 1 : 0;
+            }
+        }
+        __syncthreads();
+        if (tid == 0) {
+            // a negated channel is derived only from a computed one; the computed
+            // channels in decreasing order of tap area (stable), for balance
+            int nc = 0;
+            for (int c = 0; c < C; ++c) {
+                if (c > 0) deriv[c] = deriv[c] && !deriv[c - 1];
+                if (deriv[c]) continue;
+                const int area = tap_area(bbox, c);
+                int k = nc++;
+                if (C <= MAX_DERIV_C)
+                    for (; k > 0 && tap_area(bbox, order[k - 1]) < area; --k) order[k] = order[k - 1];
+                order[k] = c;
+            }
+            s_ncomp = nc;
+        }
+        __syncthreads();
+        float *gout = inten_out ? inten_out + (int64_t)b * N : nullptr;
+        const FiltCtx fx{H, W, C, KF, Wp, thr, fd, sim, bbox, deriv, Ic, gout};
+        const int per_c = H * nxg, items = s_ncomp * per_c;
+        for (int it = tid; it < items; it += ENC_THREADS) {
+            const int slot = it / per_c, rem = it - slot * per_c;
+            const int xg = rem / H, y = rem - xg * H;
+            npos += filter_item(fx, order[slot], xg, y);
+        }
+    } else {
+        const float *I = inten_in + (int64_t)b * N;
+        if ((N & 3) == 0) {
+            for (int q = tid; q < N / 4; q += ENC_THREADS) {
+                const float4 v = reinterpret_cast<const float4 *>(I)[q];
+                reinterpret_cast<float4 *>(Ic)[q] = v;
+                npos += (v.x > 0.0f) + (v.y > 0.0f) + (v.z > 0.0f) + (v.w > 0.0f);
+            }
+        } else {
+            for (int i = tid; i < N; i += ENC_THREADS) {
+                const float v = I[i];
+                Ic[i] = v;
+                npos += v > 0.0f;
+            }
+        }
+    }
+    npos = spk::wave_sum_i32(npos);
+    __syncthreads();  // the filter's LDS is free; s_n = 0 is seen by all
+    if (lane == 0) atomicAdd(&s_n, npos);
+    __syncthreads();
+    const int n = s_n, nb = T - 1;
+
+    uint32_t *hist = reinterpret_cast<uint32_t *>(r2);          // packed 16-bit counters
+    uint8_t *tab = r2 + SEL_HIST;  // first digit -> group of this batch's targets (0xFF: none)
+    uint16_t *list[2] = {reinterpret_cast<uint16_t *>(tab + HBINS), reinterpret_cast<uint16_t *>(tab + HBINS) + LCAP};
+    uint64_t *ckey = reinterpret_cast<uint64_t *>(tab + HBINS);  // (aliases the lists) keys of the targets' digits
+    // first digit (key bits 43..32) of the positive entries, counted once
+    for (int i = tid; i < HBINS / 2; i += ENC_THREADS) hist[i] = 0;
+    __syncthreads();
+    for (int i = tid; i < N; i += ENC_THREADS) {
+        const float v = Ic[i];
+        if (v > 0.0f) {
+            const uint32_t d = (uint32_t)(key44(v, i) >> 32);
+            atomicAdd(&hist[d >> 1], 1u << (16 * (d & 1)));
+        }
     }
     __syncthreads();
-    const int n = npos;
-    int m = 1;
-    while (m < n) m <<= 1;
-    for (int i = n + tid; i < m; i += SORT_THREADS) key[i] = 0;  // below every positive key
-    __syncthreads();
-    // bitonic network, descending overall
-    for (int k = 2; k <= m; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = tid; i < m / 2; i += SORT_THREADS) {
-                const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1)), hi = lo + j;
-                const uint64_t x = key[lo], y = key[hi];
-                const bool desc = (lo & k) == 0;
-                if ((x < y) == desc) {
-                    key[lo] = y;
-                    key[hi] = x;
+    // thread t holds digits 16t..16t+15: suffix counts S[q] = entries with digit >= 16t+q,
+    // and beyond = entries with digit >= 16t+16
+    uint32_t S[16], beyond;
+    {
+        uint32_t loc = 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const uint32_t w = hist[tid * 8 + q];
+            S[2 * q] = w & 0xFFFFu;
+            S[2 * q + 1] = w >> 16;
+            loc += S[2 * q] + S[2 * q + 1];
+        }
+        uint32_t suf = loc;  // over this wave's lanes >= lane
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t o = __shfl_down(suf, d, 64);
+            if (lane + d < 64) suf += o;
+        }
+        if (lane == 0) s_wsum[wid] = (int)suf;
+        __syncthreads();
+        uint32_t above = suf - loc;
+        for (int w = wid + 1; w < ENC_THREADS / 64; ++w) above += (uint32_t)s_wsum[w];
+        beyond = above;
+#pragma unroll
+        for (int q = 15; q >= 0; --q) {
+            above += S[q];
+            S[q] = above;
+        }
+    }
+    for (int j0 = 0; j0 < nb; j0 += SEL_T) {
+        const int jn = min(SEL_T, nb - j0);
+        if (tid < jn) {
+            const int64_t r = ((int64_t)(j0 + tid + 1) * n + T - 1) / T;  // ceil((j+1) n / T)
+            trank[0][tid] = (uint32_t)r;
+            tpre[0][tid] = 0;
+        }
+        if (tid == 0) {
+            int m = 0;
+            for (int j = 0; j < jn; ++j) m += ((int64_t)(j0 + j + 1) * n + T - 1) / T < n;
+            s_m = m;  // the targets with an entry at their rank are a prefix (ranks grow with j)
+        }
+        for (int i = tid; i < HBINS / 4; i += ENC_THREADS) reinterpret_cast<uint32_t *>(tab)[i] = 0xFFFFFFFFu;
+        __syncthreads();
+        const int m = s_m;
+        if (m == 0) continue;  // uniform
+        {
+            // the target whose rank r satisfies S[16t] > r >= S[16t+16] takes its digit here
+            uint32_t rr[SEL_T];
+#pragma unroll
+            for (int j = 0; j < SEL_T; ++j) rr[j] = trank[0][j];
+#pragma unroll
+            for (int j = 0; j < SEL_T; ++j) {
+                const uint32_t r = rr[j];
+                if (j < m && S[0] > r && r >= beyond) {
+                    int q = 0;
+#pragma unroll
+                    for (int k = 1; k < 16; ++k) q += S[k] > r;
+                    uint32_t sq = S[0], nxt = beyond;
+#pragma unroll
+                    for (int k = 1; k < 16; ++k) {
+                        sq = k == q ? S[k] : sq;
+                        nxt = k == q + 1 ? S[k] : nxt;
+                    }
+                    trank[1][j] = r - nxt;
+                    tpre[1][j] = (uint64_t)(16 * tid + q);
+                    tcnt[j] = sq - nxt;  // entries with this digit
+                }
+            }
+        }
+        __syncthreads();
+        // The targets' digits, distinct ones numbered g = 0, 1, ... (descending); each
+        // digit's entries get a segment [gstart, gend) of ckey, in that order.
+        if (tid < m) {
+            uint64_t pp[SEL_T];
+            uint32_t cc[SEL_T];
+#pragma unroll
+            for (int i = 0; i < SEL_T; ++i) {
+                pp[i] = tpre[1][i];
+                cc[i] = tcnt[i];
+            }
+            int g = 0;
+            uint32_t start = 0;
+#pragma unroll
+            for (int i = 1; i < SEL_T; ++i)
+                if (i <= tid && pp[i] != pp[i - 1]) {
+                    ++g;
+                    start += cc[i - 1];
+                }
+            tgrp[tid] = g;
+            if (tid == 0 || pp[tid] != pp[tid - 1]) {
+                gstart[g] = start;
+                gcur[g] = 0;
+                gpre[g] = pp[tid];
+                tab[pp[tid]] = (uint8_t)g;
+            }
+            if (tid == m - 1) {
+                s_ng = g + 1;
+                s_total = (int)(start + cc[tid]);
+                gstart[g + 1] = start + cc[tid];
+            }
+        }
+        __syncthreads();
+        if (s_total <= KCAP) {  // uniform: rank the targets' digits' entries directly
+            const int total = s_total, ng = s_ng;
+            for (int i = tid; i < N; i += ENC_THREADS) {
+                const float v = Ic[i];
+                if (!(v > 0.0f)) continue;
+                const uint64_t key = key44(v, i);
+                const int g = tab[key >> 32];
+                if (g == 0xFF) continue;
+                ckey[gstart[g] + atomicAdd(&gcur[g], 1u)] = key;
+            }
+            __syncthreads();
+            uint32_t rr[SEL_T];
+            int gg[SEL_T];
+#pragma unroll
+            for (int j = 0; j < SEL_T; ++j) {
+                rr[j] = trank[1][j];
+                gg[j] = j < m ? tgrp[j] : -1;
+            }
+            // the rank of a key within its digit is the number of larger keys there;
+            // the target with that rank takes the key as its boundary
+            for (int sl = tid; sl < total; sl += ENC_THREADS) {
+                const uint64_t key = ckey[sl];
+                int g = 0;
+                for (int k = 1; k < ng; ++k) g += sl >= (int)gstart[k];
+                const int e1 = (int)gstart[g + 1];
+                uint32_t rho = 0;
+                for (int u = (int)gstart[g]; u < e1; ++u) rho += ckey[u] > key;
+#pragma unroll
+                for (int j = 0; j < SEL_T; ++j)
+                    if (gg[j] == g && rr[j] == rho) kb[j0 + j] = key;
+            }
+            __syncthreads();
+            continue;
+        }
+        // Many entries share the targets' digits (ties): resolve the remaining
+        // digits 1..4 -- key bits 31..24, 23..16, 15..8, 7..0 -- per group of targets
+        // sharing a prefix
+        int src = -1;  // candidate list read by this digit (-1: all entries)
+        for (int pass = 1; pass <= 4; ++pass) {
+            const int shift = 32 - 8 * pass, cur = pass & 1, dst = src == 0 ? 1 : 0;
+            if (tid < m) {  // group of target tid: distinct prefixes among targets 0..tid
+                uint64_t pp[SEL_T];
+#pragma unroll
+                for (int i = 0; i < SEL_T; ++i) pp[i] = tpre[cur][i];
+                const uint64_t pj = tpre[cur][tid];
+                int g = 0;
+#pragma unroll
+                for (int i = 1; i < SEL_T; ++i) g += (i <= tid && pp[i] != pp[i - 1]) ? 1 : 0;
+                tgrp[tid] = g;
+                if (tid == 0 || pj != tpre[cur][tid - 1]) gpre[g] = pj;
+                if (tid == m - 1) s_ng = g + 1;
+            }
+            if (tid == 0) s_lc[dst] = 0;
+            for (int i = tid; i < SEL_T * 128; i += ENC_THREADS) hist[i] = 0;
+            __syncthreads();
+            const int ng = s_ng;
+            const int cnt = src < 0 ? N : s_lc[src];
+            for (int k = tid; k < cnt; k += ENC_THREADS) {
+                const int i = src < 0 ? k : (int)list[src][k];
+                const float v = Ic[i];
+                if (!(v > 0.0f)) continue;
+                const uint64_t key = key44(v, i), pre = key >> (shift + 8);
+                int g = -1, lo = 0, hi = ng - 1;  // gpre is descending
+                while (lo <= hi) {
+                    const int mid = (lo + hi) >> 1;
+                    const uint64_t gp = gpre[mid];
+                    if (gp == pre) { g = mid; break; }
+                    if (gp > pre) lo = mid + 1; else hi = mid - 1;
+                }
+                if (g < 0) continue;
+                const uint32_t d = (uint32_t)(key >> shift) & 255u;
+                atomicAdd(&hist[g * 128 + (d >> 1)], 1u << (16 * (d & 1)));
+                if (pass < 4) {  // a candidate of the next digit
+                    const int pos = atomicAdd(&s_lc[dst], 1);
+                    if (pos < LCAP) list[dst][pos] = (uint16_t)i;
                 }
             }
             __syncthreads();
+            // one wave per group; lane l holds digits 4l..4l+3; the targets' ranks and
+            // groups are read once, into registers
+            uint32_t rr[SEL_T];
+            int gg[SEL_T];
+#pragma unroll
+            for (int j = 0; j < SEL_T; ++j) {
+                rr[j] = trank[cur][j];
+                gg[j] = j < m ? tgrp[j] : -1;
+            }
+            for (int g = wid; g < ng; g += ENC_THREADS / 64) {
+                uint32_t S[4], loc = 0;
+                const uint32_t w0 = hist[g * 128 + 2 * lane], w1 = hist[g * 128 + 2 * lane + 1];
+                S[0] = w0 & 0xFFFFu; S[1] = w0 >> 16; S[2] = w1 & 0xFFFFu; S[3] = w1 >> 16;
+                loc = S[0] + S[1] + S[2] + S[3];
+                uint32_t suf = loc;
+#pragma unroll
+                for (int d = 1; d < 64; d <<= 1) {
+                    const uint32_t o = __shfl_down(suf, d, 64);
+                    if (lane + d < 64) suf += o;
+                }
+                const uint32_t beyond = suf - loc;
+                uint32_t above = beyond;
+#pragma unroll
+                for (int q = 3; q >= 0; --q) {
+                    above += S[q];
+                    S[q] = above;
+                }
+#pragma unroll
+                for (int j = 0; j < SEL_T; ++j) {
+                    const uint32_t r = rr[j];
+                    if (gg[j] == g && S[0] > r && r >= beyond) {
+                        const int q = (S[1] > r) + (S[2] > r) + (S[3] > r);
+                        const uint32_t nxt = q == 0 ? S[1] : q == 1 ? S[2] : q == 2 ? S[3] : beyond;
+                        trank[cur ^ 1][j] = r - nxt;
+                        tpre[cur ^ 1][j] = (tpre[cur][j] << 8) | (uint64_t)(4 * lane + q);
+                    }
+                }
+            }
+            __syncthreads();
+            src = s_lc[dst] <= LCAP ? dst : -1;
         }
+        if (tid < m) kb[j0 + tid] = tpre[1][tid];  // after 4 digits: pass 4 wrote parity 1
+        __syncthreads();
     }
-    for (int p = tid; p < n; p += SORT_THREADS)
-        tmap[0xFFFFFFFFu - (uint32_t)key[p]] = (uint8_t)(((int64_t)p * T) / n);
     __syncthreads();
+
+    // bins (a fixed-step search over the boundaries padded with zeros to a power of
+    // two, four entries interleaved), t_first and the wave
+    int nbp = 1;  // a power of two > nb: the search counts 0..nbp-1 boundaries
+    while (nbp <= nb) nbp <<= 1;
     uint8_t *tf = tf_out ? tf_out + (int64_t)b * N : nullptr;
     uint8_t *wv = wave ? wave + (int64_t)b * T * N : nullptr;
     if ((N & 3) == 0) {
-        const int nq = N / 4;
-        for (int q = tid; q < nq; q += SORT_THREADS) {
-            const uint32_t t4 = *reinterpret_cast<const uint32_t *>(tmap + 4 * q);
+        for (int q = tid; q < N / 4; q += ENC_THREADS) {
+            const float4 v4 = reinterpret_cast<const float4 *>(Ic)[q];
+            const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+            uint64_t key[4];
+            int pos[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                key[j] = key44(vv[j], 4 * q + j);
+                pos[j] = 0;
+            }
+            for (int step = nbp >> 1; step > 0; step >>= 1)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) pos[j] += kb[pos[j] + step - 1] >= key[j] ? step : 0;
+            uint32_t t4 = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) t4 |= (uint32_t)(vv[j] > 0.0f ? pos[j] : T) << (8 * j);
             if (tf) *reinterpret_cast<uint32_t *>(tf + 4 * q) = t4;
             if (wv)
-                for (int t = 0; t < T; ++t) *reinterpret_cast<uint32_t *>(wv + (int64_t)t * N + 4 * q) = spk::spikes4(t4, t, T);
+                for (int t = 0; t < T; ++t)
+                    *reinterpret_cast<uint32_t *>(wv + (int64_t)t * N + 4 * q) = spk::spikes4(t4, t, T);
         }
     } else {
-        for (int i = tid; i < N; i += SORT_THREADS)
-            if (tf) tf[i] = tmap[i];
-        if (wv)
-            for (int e = tid; e < T * N; e += SORT_THREADS) {
-                const int t = e / N, i = e - t * N;
-                wv[(int64_t)t * N + i] = (uint8_t)(t >= (int)tmap[i]);
-            }
+        for (int i = tid; i < N; i += ENC_THREADS) {
+            const float v = Ic[i];
+            const uint64_t key = key44(v, i);
+            int pos = 0;
+            for (int step = nbp >> 1; step > 0; step >>= 1) pos += kb[pos + step - 1] >= key ? step : 0;
+            const int t = v > 0.0f ? pos : T;
+            if (tf) tf[i] = (uint8_t)t;
+            if (wv)
+                for (int s2 = 0; s2 < T; ++s2) wv[(int64_t)s2 * N + i] = (uint8_t)(s2 >= t);
+        }
     }
 }
 
@@ -494,12 +928,16 @@ int enc_plan(int B, int C, int H, int W, int T, EncPlan &p) {
     return SPK_OK;
 }
 
-// The rank-order code of an intensity map: one sorting kernel per image when it
-// fits in LDS, else the bin boundaries by radix select and a separate expansion.
+size_t small_rank_lds(int64_t N) { return spk::align_up((size_t)N * 4, 16) + small_select_bytes(); }
+
+// The rank-order code of an intensity map: one workgroup per image when the
+// map has at most SMALL_MAX entries, else the bin boundaries by radix select
+// and a separate expansion.
 void launch_rank(const float *I, int B, int64_t N, int T, uint8_t *t_first, uint8_t *wave, uint64_t *bounds,
                  uint32_t *count, hipStream_t st) {
-    if (N <= SORT_MAX) {
-        hipLaunchKernelGGL(k_rank_sort, dim3(B), dim3(SORT_THREADS), 0, st, I, (int)N, T, t_first, wave);
+    if (N <= SMALL_MAX) {
+        hipLaunchKernelGGL(k_encode_small<false>, dim3(B), dim3(ENC_THREADS), small_rank_lds(N), st, nullptr,
+                           SmallFilter{}, nullptr, 0.0f, I, (int)N, T, nullptr, t_first, wave);
         return;
     }
     if (T > 1) hipLaunchKernelGGL(k_rank_select, dim3(B), dim3(SEL_THREADS), 0, st, I, N, T, bounds, count);
@@ -549,6 +987,15 @@ extern "C" int spk_encode_latency(const uint8_t *image, int B, int H, int W, con
         return ((size_t)C * KF * KF + (size_t)(rows + KF - 1) * (W + KF - 1 + 3)) * sizeof(double) +
                4 * C * sizeof(int);
     };
+    if ((t_first || wave) && p.N <= SMALL_MAX) {
+        const size_t lds = spk::align_up((size_t)p.N * 4, 16) + std::max(small_filter_bytes(H, W, C, KF), small_select_bytes());
+        if (lds <= SMALL_LDS) {  // the whole code in one kernel
+            const SmallFilter fg{H, W, C, KF, small_filter_wp(W, KF), (W + 7) / 8};
+            hipLaunchKernelGGL(k_encode_small<true>, dim3(B), dim3(ENC_THREADS), lds, st, image, fg, filters,
+                               filter_threshold, nullptr, (int)p.N, T, intensities, t_first, wave);
+            return spk::check_launch("spk_encode_latency");
+        }
+    }
     int R = H;
     while (R > 1 && filter_lds(R) > 65536) --R;
     SPK_REQUIRE(filter_lds(R) <= 65536, SPK_E_RANGE, "spk_encode_latency: %d filters of %dx%d on width %d do not fit",

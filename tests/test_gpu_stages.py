@@ -456,7 +456,10 @@ def test_encode_toy_t4(golden):
 ENC_CASES = [("dog", 3, 28, 28, 15, 0.0), ("gabor", 2, 160, 250, 30, 0.0), ("dog", 2, 28, 28, 1, 0.0),
              ("dog", 2, 28, 28, 64, 0.0), ("dog", 1, 28, 28, 255, 0.0), ("rand", 2, 19, 23, 15, 3.0),
              ("pos", 2, 40, 50, 15, 0.0), ("pos", 1, 41, 50, 15, 0.0), ("pos", 3, 1, 1, 15, 0.0),
-             ("dog", 1, 100, 300, 15, 0.0)]  # 13x13 filters on a wide image: bands of rows
+             ("dog", 1, 100, 300, 15, 0.0),  # 13x13 filters on a wide image: bands of rows
+             ("float", 3, 28, 28, 15, 0.0),  # general float taps: the sum order decides the bits
+             ("float", 2, 9, 13, 30, -0.5),  # ragged width, negative threshold
+             ("flat", 2, 40, 40, 15, 0.0)]  # all intensities equal: the index decides every rank
 
 
 @pytest.mark.parametrize("case", ENC_CASES)
@@ -470,6 +473,20 @@ def test_encode_parity(case):
     elif kind == "pos":  # 4 positive filters on a noise image: every entry is ranked
         img = g.integers(1, 256, (B, H, W)).astype(np.uint8)
         bank = (g.integers(1, 65, (4, 3, 3)) / 64.0).astype(np.float32)
+    elif kind == "float":
+        # channels 1 = -0 and 5 = -4 are exact negations (computed once on the GPU); 3 is
+        # -2 but for one tap; 4 = -3 although 3 is itself nearly a negation; taps spread
+        # over 2^-20..2^2, so partial sums round and only the defined order reproduces them
+        img = synth.stroke_images(g, B, H, W) if H >= 8 else g.integers(0, 256, (B, H, W)).astype(np.uint8)
+        base = (g.normal(0, 1, (3, 5, 5)) * np.exp2(g.integers(-20, 3, (3, 5, 5)))).astype(np.float32)
+        bank = np.stack([base[0], -base[0], base[1], -base[1], base[2], -base[2]])
+        bank[3, 2, 2] += np.float32(0.25)
+        bank[4] = -bank[3]
+        bank[5] = -bank[4]
+    elif kind == "flat":  # a constant image through a 1x1 filter
+        img = np.full((B, H, W), 200, np.uint8)
+        img[1, :3, :5] = 0
+        bank = np.ones((1, 1, 1), np.float32)
     else:
         img = g.integers(0, 256, (B, H, W)).astype(np.uint8)
         bank = (g.integers(-64, 65, (5, 7, 7)) / 64.0).astype(np.float32)
