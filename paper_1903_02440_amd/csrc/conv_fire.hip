@@ -59,6 +59,34 @@ typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
 constexpr int NTILE_ALIGN = 4;  // the N tiles (16 features) are padded to a multiple of this
 
+// 16 bytes per lane from global memory into LDS at byte offset m0 + 16*lane.
+// Issued as inline assembly so that the compiler, which cannot tell which LDS
+// bytes the transfer writes, does not wait for it before every later LDS read;
+// the caller waits for it explicitly (vmcnt) before the barrier that hands the
+// buffer to the other waves.
+__device__ __forceinline__ void lds_dma16(const uint4 *gsrc, uint32_t m0) {
+    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gsrc), "{m0}"(m0) : "memory");
+}
+
+// A workgroup barrier for LDS hand-offs only: this wave's LDS operations
+// complete, its global loads may stay in flight.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// s_waitcnt vmcnt(n) for a wave-uniform n (the immediate must be a constant)
+__device__ __forceinline__ void wait_vmcnt(int n) {
+    switch (n) {
+#define SPK_VMCNT(k) \
+    case k:          \
+        asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); \
+        break;
+        SPK_VMCNT(8) SPK_VMCNT(12) SPK_VMCNT(20)
+#undef SPK_VMCNT
+    default:
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+}
+
+
 struct ConvGeom {
     int B, T, Cin, H, W, Cout, K, pad;
     int S;           // stride: output (y, x) reads the padded window at (y*S, x*S)
@@ -801,7 +829,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                     load_b(b1, min(ks + 3, g.ksteps - 1));
                 }
                 if (ks < g.ksteps) kstep(a0, b0);
-                __syncthreads();  // staging free: the store waves are done with the previous block
+                lds_barrier();  // staging free: the store waves are done with the previous block
                 // Staging offset = the lane's part (feature c, positions 4*gq..) plus a
                 // wave-uniform part; the lane part is made opaque here so that the
                 // compiler forms the addresses at the writes instead of keeping one
@@ -832,7 +860,7 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
                     }
                 }
                 if (has_next && last_block) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-                __syncthreads();  // staging full
+                lds_barrier();  // staging full
             }
             };
             if (!BLDS) {
@@ -960,9 +988,9 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
             // the block).  A no-op without pooling, and after its first call.
             const bool one_block = g.T <= FIN_TB;
             for (int tb0 = (g.T - 1) / FIN_TB * FIN_TB; tb0 >= 0; tb0 -= FIN_TB) {
-                __syncthreads();  // staging free
+                lds_barrier();  // staging free
                 if (one_block) pool_pending();
-                __syncthreads();  // staging full
+                lds_barrier();  // staging full
                 for (int t = min(FIN_TB, g.T - tb0) - 1; t >= 0; --t) {
                     const int tt = tb0 + t;
                     const float *st = stage + t * stage_t;
@@ -1047,6 +1075,11 @@ __global__ __launch_bounds__(FIN_THREADS, 1) void k_conv_fire_fin(
 // K-steps, filled with direct global-to-LDS loads one chunk ahead; the spike
 // words of a chunk are fetched before the next chunk's fill is issued, so
 // the MFMA loop never waits behind it.
+// Position-major form (small maps whose receptive fields are mostly padding,
+// e.g. 4x4 maps under a 5x5 kernel): a 16-row tile is 16 images at one output
+// position, a task is (feature group, position, block of 256 images), and
+// the K loop runs only over the K-steps that touch the image at that
+// position (9, 12 or 16 of 25 taps on a 4x4 map), listed per task in LDS.
 constexpr int INF_WAVES = 8;
 constexpr int INF_MW = 2;   // position tiles per wave
 constexpr int INF_NW = 4;   // 16-feature tiles per workgroup
@@ -1055,20 +1088,55 @@ constexpr int INF_CHUNK_U4 = INF_KC * INF_NW * NT * 64;  // uint4 per chunk buff
 constexpr int INF_KPART = INF_KC;  // a K part is a multiple of this many K-steps (whole chunks)
 constexpr int INF_ZW = 4;   // zero waves (waves 8-11)
 constexpr int64_t INF_PART_MAX = 1 << 21;  // floats of split partial sums at most
+constexpr int INF_KLMAX = 512;  // K-steps at most (16384 / 32)
+constexpr int INF_PM_IMG = 16 * INF_WAVES * INF_MW;  // images per position-major task
+
+// Does K-step ks touch the image (not only padding) for output position (y, x)?
+__host__ __device__ inline bool kstep_valid(const ConvGeom &g, int y, int x, int ks) {
+    const int KK = g.K * g.K;
+    int c0, c1;
+    if (g.CP % 32 == 0) {
+        c0 = c1 = ks / (g.CP / 32);
+    } else {
+        c0 = ks * 32 / g.CP;
+        c1 = (ks * 32 + 31) / g.CP;
+        c1 = c1 < KK - 1 ? c1 : KK - 1;
+    }
+    for (int cell = c0; cell <= c1 && cell < KK; ++cell) {
+        const int iy = y * g.S + cell / g.K - g.pad, ix = x * g.S + cell % g.K - g.pad;
+        if (iy >= 0 && iy < g.H && ix >= 0 && ix < g.W) return true;
+    }
+    return false;
+}
+
+// K-steps of position pos that touch the image, counted by one wave
+__device__ __forceinline__ int count_valid_ksteps(const ConvGeom &g, int pos, int lane) {
+    const int y = pos / g.Wo, x = pos - y * g.Wo;
+    int n = 0;
+    for (int k0 = 0; k0 < g.ksteps; k0 += 64) n += __popcll(__ballot(k0 + lane < g.ksteps && kstep_valid(g, y, x, k0 + lane)));
+    return n;
+}
 
 // With VEC, INF_ZW more waves write the zero planes of steps 0..T-2 (potentials
 // and spikes of images blockIdx.x, blockIdx.x + gridDim.x, ...) while the MFMA
 // waves compute: they pass the same barriers, one slice of their stores between
 // two barriers.
-template <bool VEC>
+template <bool VEC, bool PM>
 __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     const uint8_t *__restrict__ tpad, const uint4 *__restrict__ frag, const int2 *__restrict__ koff2, ConvGeom g,
-    int n_mb, int n_ng, int ksplit, int kpp, float *__restrict__ part, const float *__restrict__ inv_scale,
+    int n_mb, int n_ng, int ksplit, int kpp, int pm_nib, float *__restrict__ part, const float *__restrict__ inv_scale,
     const int *__restrict__ wbf16, float *__restrict__ P, uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
     float *__restrict__ VF) {
     extern __shared__ uint4 lds[];
     int2 *koff_l = reinterpret_cast<int2 *>(lds);
     uint4 *cbuf = lds + (g.ksteps * 4 * 8 + 15) / 16;  // 2 chunk buffers [ksl][n][term][64]
+    uint16_t *klist = reinterpret_cast<uint16_t *>(cbuf + 2 * INF_CHUNK_U4);  // [2][INF_KLMAX] (position-major)
+    int2 *koffp = reinterpret_cast<int2 *>(klist + 2 * INF_KLMAX);            // [2][ksteps][4] (position-major)
+    // LDS byte address of the chunk buffers (for the position-major transfers)
+    const uint32_t cbuf_lds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)cbuf;
+    constexpr bool pm = PM;  // position-major tasks (pm_nib image blocks)
+    constexpr int KCH = PM ? INF_KC / 2 : INF_KC;  // K-steps per chunk (position-major: fewer, no spills)
+    constexpr int GPW_PM = KCH * INF_NW * NT / INF_WAVES;  // position-major fill loads per wave and chunk
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int gq = lane >> 4, c = lane & 15;
     for (int i = tid; i < g.ksteps * 4; i += (INF_WAVES + INF_ZW) * 64) koff_l[i] = koff2[i];
@@ -1082,7 +1150,15 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
     // With ksplit > 1 a task is (feature group, position block, part of the K
     // steps: kpp of them, a multiple of INF_KPART): its raw sums go to
     // part[kp][B][Cout][HoWo], added up in part order by k_inf_reduce.
-    auto chunk_range = [&](int task, int kc, int &c_lo, int &c_hi) {
+    // position-major: task -> (feature group, block of images, position); its
+    // K-steps are the valid ones of that position (nvalid of them)
+    auto pm_pos = [&](int task) { return (task % n_mb) % g.HoWo; };
+    auto chunk_range = [&](int task, int kc, int &c_lo, int &c_hi, int nvalid) {
+        if (pm) {
+            c_lo = 0;
+            c_hi = (nvalid + kc - 1) / kc;
+            return;
+        }
         const int k_lo = (task % ksplit) * kpp, k_hi = min(g.ksteps, k_lo + kpp);
         c_lo = k_lo / kc;
         c_hi = k_hi > k_lo ? (k_hi + kc - 1) / kc : c_lo;
@@ -1099,7 +1175,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         int nint = 1;  // barrier intervals (the last one after the loop)
         for (int task = t_lo + j; task < t_hi; task += per_xcd) {
             int c_lo, c_hi;
-            chunk_range(task, INF_KC, c_lo, c_hi);
+            chunk_range(task, KCH, c_lo, c_hi, pm ? count_valid_ksteps(g, pm_pos(task), lane) : 0);
             nint += 1 + max(0, c_hi - c_lo);
         }
         const int64_t per = (total + nint - 1) / nint;
@@ -1121,12 +1197,17 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         };
         for (int task = t_lo + j; task < t_hi; task += per_xcd) {
             int c_lo, c_hi;
-            chunk_range(task, INF_KC, c_lo, c_hi);
+            chunk_range(task, KCH, c_lo, c_hi, pm ? count_valid_ksteps(g, pm_pos(task), lane) : 0);
             slice();
             __syncthreads();  // the MFMA waves' "buffers free"
             for (int ch = c_lo; ch < c_hi; ++ch) {
                 slice();
-                __syncthreads();  // the MFMA waves' chunk barrier
+                // the MFMA waves' chunk barrier; in the position-major form it does
+                // not wait for this wave's stores
+                if constexpr (PM)
+                    lds_barrier();
+                else
+                    __syncthreads();
             }
         }
         slice();
@@ -1135,21 +1216,60 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
 
     auto mfma_waves = [&](auto bf_c) {
     constexpr int KIND = decltype(bf_c)::value ? WK_BF16 : WK_F16;
-    constexpr int KC = INF_KC;
+    constexpr int KC = KCH;
     constexpr int CHUNK_U4 = INF_CHUNK_U4;
-    for (int task = t_lo + j; task < t_hi; task += per_xcd) {
+    int tpar = 0;  // task parity: the K-step list buffer
+    for (int task = t_lo + j; task < t_hi; task += per_xcd, tpar ^= 1) {
         const int tq = task / ksplit, kp = task % ksplit;
         const int ng = tq / n_mb, mb = tq % n_mb;
+        const int ppos = pm ? pm_pos(task) : 0, pib = pm ? mb / g.HoWo : 0;
+        int nks = g.ksteps;
+        uint16_t *kl = klist + tpar * INF_KLMAX;
+        if constexpr (pm) {  // the valid K-steps of the position, in order (wave 0 lists them)
+            const int py = ppos / g.Wo, px = ppos - py * g.Wo;
+            nks = 0;
+            for (int k0 = 0; k0 < g.ksteps; k0 += 64) {
+                const bool v = k0 + lane < g.ksteps && kstep_valid(g, py, px, k0 + lane);
+                const uint64_t m = __ballot(v);
+                if (wv == 0 && v) {
+                    const int at = nks + __popcll(m & ((1ull << lane) - 1ull));
+                    kl[at] = (uint16_t)(k0 + lane);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) koffp[(tpar * g.ksteps + at) * 4 + q] = koff_l[(k0 + lane) * 4 + q];
+                }
+                nks += __popcll(m);
+            }
+        }
+        auto kidx = [&](int i) {
+            if constexpr (pm) return (int)kl[i];
+            else return i;
+        };
         int c_lo, c_hi;
-        chunk_range(task, KC, c_lo, c_hi);
+        chunk_range(task, KC, c_lo, c_hi, nks);
         const uint4 *fg = frag + (int64_t)ng * INF_NW * g.ksteps * NT * 64;
         // chunk ch -> buffer: wave w issues the 64-lane groups w, w+8, ... (16 bytes per lane)
         auto fill = [&](int ch) {
+            if constexpr (pm) {
+                // three chunk buffers; every wave issues the same number of loads per
+                // chunk (groups past the chunk's last K-step load a valid one that is
+                // never read), so the waits can count them
+                constexpr int GPW = KC * INF_NW * NT / INF_WAVES;
+                const uint32_t dst = cbuf_lds + (uint32_t)((ch % 3) * (KC * INF_NW * NT * 64)) * 16u;
+                const int k0 = ch * KC;
+#pragma unroll
+                for (int u = 0; u < GPW; ++u) {
+                    const int grp = wv + u * INF_WAVES;
+                    const int q = grp % NT, n = (grp / NT) % INF_NW, ksl = grp / (NT * INF_NW);
+                    const uint4 *src = fg + (((int64_t)n * g.ksteps + kidx(min(k0 + ksl, nks - 1))) * NT + q) * 64 + lane;
+                    lds_dma16(src, __builtin_amdgcn_readfirstlane(dst + (uint32_t)grp * 64u * 16u));
+                }
+                return;
+            }
             uint4 *dst = cbuf + (ch & 1) * CHUNK_U4;
-            const int k0 = ch * KC, nk = min(KC, g.ksteps - k0);
+            const int k0 = ch * KC, nk = min(KC, nks - k0);
             for (int grp = wv; grp < nk * INF_NW * NT; grp += INF_WAVES) {
                 const int q = grp % NT, n = (grp / NT) % INF_NW, ksl = grp / (NT * INF_NW);
-                const uint4 *src = fg + (((int64_t)n * g.ksteps + k0 + ksl) * NT + q) * 64 + lane;
+                const uint4 *src = fg + (((int64_t)n * g.ksteps + kidx(k0 + ksl)) * NT + q) * 64 + lane;
                 __builtin_amdgcn_global_load_lds(src, dst + grp * 64, 16, 0, 0);
             }
         };
@@ -1158,6 +1278,15 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
         int mpos0[INF_MW];
 #pragma unroll
         for (int i = 0; i < INF_MW; ++i) {
+            if constexpr (pm) {  // rows: images pib*INF_PM_IMG + (wv*MW + i)*16 + row, all at position ppos
+                const int64_t b0 = (int64_t)pib * INF_PM_IMG + (wv * INF_MW + i) * 16;
+                const int64_t b = min<int64_t>(b0 + c, g.B - 1);  // rows past the batch are computed, not stored
+                const int y = ppos / g.Wo, xx = ppos % g.Wo;
+                abase[i] = tpad + (uint32_t)(((b * g.Hp + y * g.S) * g.Wp + xx * g.S) * g.CP);
+                img[i] = b0 < g.B ? b0 : -1;
+                mpos0[i] = ppos;
+                continue;
+            }
             const int64_t gm = ((int64_t)mb * INF_WAVES + wv) * INF_MW + i;
             const bool v = gm < g.total_mtiles;
             const int64_t b = v ? gm / g.mt_per_img : 0;
@@ -1184,7 +1313,8 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             if (wide == 2) {
 #pragma unroll
                 for (int kl = 0; kl < KC; kl += 2) {
-                    const int2 o = koff_l[min(ch * KC + kl, g.ksteps - 2) * 4 + gq];
+                    const int2 o = pm ? koffp[(tpar * g.ksteps + max(0, min(ch * KC + kl, nks - 2))) * 4 + gq]
+                                      : koff_l[kidx(max(0, min(ch * KC + kl, nks - 2))) * 4 + gq];
 #pragma unroll
                     for (int i = 0; i < INF_MW; ++i) {
                         const uint4 v = *reinterpret_cast<const uint4 *>(abase[i] + (uint32_t)o.x);
@@ -1197,7 +1327,8 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
             } else {
 #pragma unroll
                 for (int kl = 0; kl < KC; ++kl) {
-                    const int2 o = koff_l[min(ch * KC + kl, g.ksteps - 1) * 4 + gq];
+                    const int2 o = pm ? koffp[(tpar * g.ksteps + max(0, min(ch * KC + kl, nks - 1))) * 4 + gq]
+                                      : koff_l[kidx(max(0, min(ch * KC + kl, nks - 1))) * 4 + gq];
 #pragma unroll
                     for (int i = 0; i < INF_MW; ++i) {
                         if (wide == 1) {
@@ -1212,15 +1343,7 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
                 }
             }
         };
-        auto chunk = [&](int ch, const uint32_t (&awc)[KC][INF_MW][2], uint32_t (&awn)[KC][INF_MW][2]) {
-            const int nk = min(KC, g.ksteps - ch * KC);
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's words and fill of chunk ch landed
-            __syncthreads();  // every wave's part of chunk ch is in LDS; chunk ch-1's buffer is free
-            if (ch + 1 < c_hi) {
-                load_aw(ch + 1, awn);
-                fill(ch + 1);
-            }
-            const uint4 *fr = cbuf + (ch & 1) * CHUNK_U4 + lane;
+        auto mma = [&](const uint4 *fr, int nk, const uint32_t (&awc)[KC][INF_MW][2]) {
 #pragma unroll
             for (int kl = 0; kl < KC; ++kl) {
                 if (kl >= nk) break;  // uniform
@@ -1245,16 +1368,76 @@ __global__ __launch_bounds__((INF_WAVES + INF_ZW) * 64, 1) void k_conv_fire_inf(
                         for (int n = 0; n < INF_NW; ++n) acc[i][n] = mfma<KIND>(a[i], bt[q][n], acc[i][n]);
             }
         };
-        __syncthreads();  // the buffers are free (previous task done), koff is visible
-        if (c_lo < c_hi) {
-            load_aw(c_lo, aw0);
-            fill(c_lo);
-        }
-        for (int ch = c_lo; ch < c_hi; ch += 2) {
-            chunk(ch, aw0, aw1);
-            if (ch + 1 < c_hi) chunk(ch + 1, aw1, aw0);
+        if constexpr (pm) {
+            // two chunks ahead: chunk ch's words and fill are waited for while chunk
+            // ch+1's loads (a fixed number per wave) stay in flight
+            uint32_t aw2[KC][INF_MW][2];
+            const int ahead = GPW_PM + (wide == 2 ? KC / 2 : wide == 1 ? KC : 2 * KC) * INF_MW;
+            auto chunk3 = [&](int ch, const uint32_t (&awc)[KC][INF_MW][2], uint32_t (&awn)[KC][INF_MW][2]) {
+                if (ch + 1 < c_hi)
+                    wait_vmcnt(ahead);
+                else
+                    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                lds_barrier();  // every wave's part of chunk ch is in LDS; chunk ch-1's buffer is free
+                if (ch + 2 < c_hi) {
+                    load_aw(ch + 2, awn);
+                    fill(ch + 2);
+                }
+                mma(cbuf + (ch % 3) * (KC * INF_NW * NT * 64) + lane, min(KC, nks - ch * KC), awc);
+            };
+            __syncthreads();  // the buffers are free (previous task done), the lists are visible
+            if (c_hi > 0) {
+                load_aw(0, aw0);
+                fill(0);
+            }
+            if (c_hi > 1) {
+                load_aw(1, aw1);
+                fill(1);
+            }
+            for (int ch = 0; ch < c_hi; ch += 3) {
+                chunk3(ch, aw0, aw2);
+                if (ch + 1 < c_hi) chunk3(ch + 1, aw1, aw0);
+                if (ch + 2 < c_hi) chunk3(ch + 2, aw2, aw1);
+            }
+        } else {
+            auto chunk = [&](int ch, const uint32_t (&awc)[KC][INF_MW][2], uint32_t (&awn)[KC][INF_MW][2]) {
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's words and fill of chunk ch landed
+                __syncthreads();  // every wave's part of chunk ch is in LDS; chunk ch-1's buffer is free
+                if (ch + 1 < c_hi) {
+                    load_aw(ch + 1, awn);
+                    fill(ch + 1);
+                }
+                mma(cbuf + (ch & 1) * CHUNK_U4 + lane, min(KC, nks - ch * KC), awc);
+            };
+            __syncthreads();  // the buffers are free (previous task done), koff is visible
+            if (c_lo < c_hi) {
+                load_aw(c_lo, aw0);
+                fill(c_lo);
+            }
+            for (int ch = c_lo; ch < c_hi; ch += 2) {
+                chunk(ch, aw0, aw1);
+                if (ch + 1 < c_hi) chunk(ch + 1, aw1, aw0);
+            }
         }
         // the last step's potentials and spikes, the first-spike time and potential
+        if constexpr (pm) {
+            // accumulator rows 4*gq + q are images img + 4*gq + q at position ppos: the
+            // raw sums go to part[ppos][b][f] (16 features contiguous), and
+            // k_inf_pm_finish writes them out per image
+#pragma unroll
+            for (int i = 0; i < INF_MW; ++i)
+#pragma unroll
+                for (int n = 0; n < INF_NW; ++n) {
+                    const int f = (ng * INF_NW + n) * 16 + c;
+                    if (img[i] < 0 || f >= g.Cout) continue;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int64_t b = img[i] + gq * 4 + q;
+                        if (b < g.B) part[((int64_t)ppos * g.B + b) * g.Cout + f] = acc[i][n][q];
+                    }
+                }
+            continue;
+        }
 #pragma unroll
         for (int i = 0; i < INF_MW; ++i)
 #pragma unroll
@@ -1353,6 +1536,36 @@ __global__ __launch_bounds__(256) void k_inf_reduce(const float *__restrict__ pa
     VF[o] = v;
 }
 
+// Position-major Eq.5 outputs: one workgroup per image reads the raw sums
+// part[pos][b][f] (contiguous in f), transposes them through LDS to the
+// image's [f][pos] order and writes P[T-1] = sum / scale, its spikes, the
+// first-spike time (T-1 where it fires, else T) and the potential there.
+constexpr int INF_PM_OUT = 16384;  // Cout * HoWo at most (the LDS transpose)
+__global__ __launch_bounds__(256) void k_inf_pm_finish(const float *__restrict__ part, ConvGeom g,
+                                                       const float *__restrict__ inv_scale, float *__restrict__ P,
+                                                       uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
+                                                       float *__restrict__ VF) {
+    extern __shared__ float buf[];  // Cout * HoWo (<= INF_PM_OUT)
+    const int64_t b = blockIdx.x, plane = (int64_t)g.Cout * g.HoWo;
+    const float inv_s = *inv_scale;
+    for (int i = threadIdx.x; i < plane; i += 256) {
+        const int pos = i / g.Cout, f = i - pos * g.Cout;
+        buf[f * g.HoWo + pos] = part[((int64_t)pos * g.B + b) * g.Cout + f];
+    }
+    __syncthreads();
+    const int64_t o0 = (b * g.T + g.T - 1) * plane, of0 = b * plane;
+    for (int i = threadIdx.x; i < plane; i += 256) {
+        const float v = buf[i] * inv_s;
+        const bool fire = v > 0.0f;
+        if (P) P[o0 + i] = v;
+        if (S) S[o0 + i] = (uint8_t)fire;
+        TF[of0 + i] = (uint8_t)(fire ? g.T - 1 : g.T);
+        VF[of0 + i] = v;
+    }
+}
+
+int inf_pm_nib(const ConvGeom &g, int ksplit);
+
 struct ConvPlan {
     ConvGeom g;
     size_t tpad_bytes, frag_count, koff_count;
@@ -1410,6 +1623,7 @@ int make_plan(int B, int T, int Cin, int H, int W, int Cout, int K, int stride, 
     pl.ksplit = ks >= 2 ? (int)ks : 1;
     pl.kpp = pl.ksplit > 1 ? (int)spk::ceil_div(nch, pl.ksplit) * INF_KPART : g.ksteps;
     pl.part_count = pl.ksplit > 1 ? (size_t)(pl.ksplit * outs) : 0;
+    if (inf_pm_nib(g, pl.ksplit)) pl.part_count = (size_t)outs;  // position-major sums of an Eq.5 call
     return SPK_OK;
 }
 
@@ -1445,20 +1659,42 @@ void launch_fin(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const
                        wbf16, wts, wmax, wmin, n_wmax, P, S, TF, VF, po, arith);
 }
 
+// Position-major Eq.5 tasks pay when most of the receptive fields' K-steps are
+// padding and there are enough (feature group, position, image block) tasks.
+int inf_pm_nib(const ConvGeom &g, int ksplit) {
+    if (ksplit > 1 || g.HoWo > 64 || (int64_t)g.Cout * g.HoWo > INF_PM_OUT || g.ksteps > 256) return 0;
+    int64_t valid = 0;
+    for (int pos = 0; pos < g.HoWo; ++pos)
+        for (int ks = 0; ks < g.ksteps; ++ks) valid += kstep_valid(g, pos / g.Wo, pos % g.Wo, ks);
+    const int nib = (int)spk::ceil_div(g.B, INF_PM_IMG);
+    const int64_t n_ng = spk::ceil_div(spk::ceil_div(g.Cout, 16), INF_NW);
+    const bool sparse = valid * 100 <= (int64_t)g.HoWo * g.ksteps * 85;
+    return sparse && n_ng * g.HoWo * nib >= 128 ? nib : 0;
+}
+
 template <bool VEC>
 void launch_inf(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const float *inv_scale, const int *wbf16,
                 const ConvGeom &g, int ksplit, int kpp, float *part, float *P, uint8_t *S, uint8_t *TF, float *VF,
                 hipStream_t st) {
-    const int n_mb = (int)spk::ceil_div(g.total_mtiles, INF_WAVES * INF_MW);
+    const int pm_nib = inf_pm_nib(g, ksplit);
+    const int n_mb = pm_nib ? g.HoWo * pm_nib : (int)spk::ceil_div(g.total_mtiles, INF_WAVES * INF_MW);
     const int n_ng = (int)spk::ceil_div(spk::ceil_div(g.Cout, 16), INF_NW);
-    const size_t lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16) + 2 * (size_t)INF_CHUNK_U4 * 16;
+    const size_t lds = spk::align_up((size_t)g.ksteps * 4 * sizeof(int2), 16) + 2 * (size_t)INF_CHUNK_U4 * 16 +
+                       2 * INF_KLMAX * sizeof(uint16_t) + (pm_nib ? 2 * (size_t)g.ksteps * 4 * sizeof(int2) : 0);
     if (!VEC && g.T > 1 && (P || S)) {  // (with VEC the conv kernel's zero waves write them)
         const int64_t n = (int64_t)(g.T - 1) * g.Cout * g.HoWo;
         const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>(64, spk::ceil_div(n, 256 * 16)));
         hipLaunchKernelGGL(k_zero_planes, dim3(gx, (unsigned)std::min(g.B, 65535)), dim3(256), 0, st, g, P, S);
     }
-    hipLaunchKernelGGL((k_conv_fire_inf<VEC>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad, frag,
-                       koff2, g, n_mb, n_ng, ksplit, kpp, part, inv_scale, wbf16, P, S, TF, VF);
+    if (pm_nib) {
+        hipLaunchKernelGGL((k_conv_fire_inf<VEC, true>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad,
+                           frag, koff2, g, n_mb, n_ng, ksplit, kpp, pm_nib, part, inv_scale, wbf16, P, S, TF, VF);
+        hipLaunchKernelGGL(k_inf_pm_finish, dim3((unsigned)g.B), dim3(256), (size_t)g.Cout * g.HoWo * sizeof(float), st,
+                           part, g, inv_scale, P, S, TF, VF);
+        return;
+    }
+        hipLaunchKernelGGL((k_conv_fire_inf<VEC, false>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad,
+                           frag, koff2, g, n_mb, n_ng, ksplit, kpp, pm_nib, part, inv_scale, wbf16, P, S, TF, VF);
     if (ksplit > 1) {
         const int64_t n = (int64_t)g.B * g.Cout * g.HoWo;
         hipLaunchKernelGGL(k_inf_reduce, dim3((unsigned)spk::ceil_div(n, 256)), dim3(256), 0, st, part, ksplit, g,
@@ -1628,7 +1864,8 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
     const bool alds = g.CP >= 8 && koff_lds + stage_lds + a_lds + pool_lds <= lds_limit;
     const bool blds = koff_lds + frag_lds + stage_lds + (alds ? a_lds : 0) + pool_lds <= lds_limit;
     const size_t fin_lds = koff_lds + (blds ? frag_lds : 0) + stage_lds + (alds ? a_lds : 0) + pool_lds;
-    const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4 * 16;
+    const size_t inf_lds = koff_lds + 2 * (size_t)INF_CHUNK_U4 * 16 + 2 * INF_KLMAX * sizeof(uint16_t) +
+                           (inf_pm_nib(g, pl.ksplit) ? 2 * (size_t)g.ksteps * 4 * sizeof(int2) : 0);
     SPK_REQUIRE(!inf_mode || inf_lds <= lds_limit, SPK_E_RANGE,
                 "spk_conv_fire: needs %zu bytes of LDS per workgroup, the device has %zu", inf_lds, lds_limit);
     SPK_REQUIRE(inf_mode || fin_lds <= lds_limit, SPK_E_RANGE,
