@@ -16,9 +16,11 @@ spk = pytest.importorskip("paper_1903_02440_amd")
 pytestmark = pytest.mark.gpu
 
 # (B, T, Cin, H, W, Cout, K, pad, thr): S2 of the 1000-image workload at 64
-# images, then a smaller S1-shaped call; then Eq.5 with a split K (few tasks)
+# images, then a smaller S1-shaped call; then Eq.5 with a split K (few tasks);
+# then Eq.5 in the position-major form (its sums go through the scratch)
 CALLS = [[(64, 15, 30, 14, 14, 250, 3, 1, 10.0), (3, 15, 6, 28, 28, 30, 5, 2, 15.0)],
-         [(40, 15, 250, 4, 4, 200, 5, 2, math.inf), (2, 15, 250, 4, 4, 200, 5, 2, math.inf)]]
+         [(40, 15, 250, 4, 4, 200, 5, 2, math.inf), (2, 15, 250, 4, 4, 200, 5, 2, math.inf)],
+         [(300, 15, 250, 4, 4, 200, 5, 2, math.inf), (260, 15, 250, 4, 4, 200, 5, 2, math.inf)]]
 
 
 def _inputs(seed, B, T, Cin, H, W, Cout, K):
@@ -37,7 +39,7 @@ def _outputs(B, T, Cout, Ho, Wo):
             torch.full((B, Cout, Ho, Wo), -7.0, device="cuda"))
 
 
-@pytest.mark.parametrize("calls", CALLS, ids=["finite", "eq5"])
+@pytest.mark.parametrize("calls", CALLS, ids=["finite", "eq5", "eq5-position-major"])
 def test_noalloc_matches_workspace_entry(calls):
     lib = spk.lib()
     st = torch.cuda.current_stream().cuda_stream
