@@ -57,6 +57,23 @@ __device__ __forceinline__ int wave_max_i32(int v) {
     for (int s = 32; s >= 1; s >>= 1) v = max(v, __shfl_xor(v, s, 64));
     return v;
 }
+// lane-wise min / max of two 16-bit halves over the wave
+__device__ __forceinline__ uint32_t wave_min_u16x2(uint32_t v) {
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+        const uint32_t o = __shfl_xor(v, s, 64);
+        v = min(v & 0xFFFFu, o & 0xFFFFu) | (min(v >> 16, o >> 16) << 16);
+    }
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_max_u16x2(uint32_t v) {
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+        const uint32_t o = __shfl_xor(v, s, 64);
+        v = max(v & 0xFFFFu, o & 0xFFFFu) | (max(v >> 16, o >> 16) << 16);
+    }
+    return v;
+}
 
 __global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img, int B, int H, int W,
                                                 const float *__restrict__ filt, int C, int KF, float thr, int R,
@@ -344,6 +361,27 @@ constexpr int LCAP = 1024;       // candidate list capacity (entries)
 constexpr int KCAP = LCAP / 2;   // keys of the targets' first digits ranked directly (same LDS)
 constexpr int MAX_DERIV_C = 64;  // negated-channel detection and cost order for at most this many channels
 
+// Global-to-LDS staging of n elements by one workgroup: a thread loads up to
+// STAGE_U elements into registers before it stores any, so their memory
+// latencies overlap (a load followed at once by its store waits each time).
+constexpr int STAGE_U = 8;
+template <typename Load, typename Store>
+__device__ __forceinline__ void stage_batched(int n, Load ld, Store stv) {
+    for (int i0 = threadIdx.x; i0 < n; i0 += STAGE_U * ENC_THREADS) {
+        float v[STAGE_U];
+#pragma unroll
+        for (int k = 0; k < STAGE_U; ++k) {
+            const int i = i0 + k * ENC_THREADS;
+            v[k] = i < n ? ld(i) : 0.0f;
+        }
+#pragma unroll
+        for (int k = 0; k < STAGE_U; ++k) {
+            const int i = i0 + k * ENC_THREADS;
+            if (i < n) stv(i, v[k]);
+        }
+    }
+}
+
 __device__ __forceinline__ uint64_t key44(float v, int i) {
     return ((uint64_t)__float_as_uint(v) << 13) | (uint64_t)(8191 - i);
 }
@@ -379,6 +417,22 @@ struct FiltCtx {
     float *Ic, *gout;   // intensities in LDS, optionally in global memory
 };
 
+// NU consecutive taps of one filter row applied to 8 consecutive outputs: the
+// 8 + NU - 1 pixels under them and the NU taps are all read before the first
+// product, then the products in kx order.
+template <int NU>
+__device__ __forceinline__ void filter_taps(const float *row, const double *fr, double (&acc)[8]) {
+    double a[8 + NU - 1], f[NU];
+#pragma unroll
+    for (int q = 0; q < 8 + NU - 1; ++q) a[q] = (double)row[q];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) f[u] = fr[u];
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = fma(f[u], a[u + j], acc[j]);
+}
+
 // 8 consecutive outputs of row y, columns 8*xg.., of channel c (and of the
 // negated channel after it): double sums in ky-then-kx order over the non-zero
 // taps, one rounding, the threshold.  Returns the number of positive outputs.
@@ -392,17 +446,18 @@ __device__ __forceinline__ int filter_item(const FiltCtx &fx, int c, int xg, int
     for (int j = 0; j < CW; ++j) acc[j] = 0.0;
     for (int ky = ya; ky <= yb; ++ky) {
         const float *row = fx.sim + (y + ky) * fx.Wp + CW * xg;
-        for (int kx0 = xa; kx0 <= xb; kx0 += 8) {
-            double a[CW + 7];
-#pragma unroll
-            for (int q = 0; q < CW + 7; ++q) a[q] = (double)row[kx0 + q];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                if (kx0 + u > xb) break;
-                const double f = fc[ky * fx.KF + kx0 + u];
-#pragma unroll
-                for (int j = 0; j < CW; ++j) acc[j] = fma(f, a[u + j], acc[j]);
-            }
+        const double *fr = fc + ky * fx.KF;
+        int kx0 = xa;
+        for (; kx0 + 8 <= xb + 1; kx0 += 8) filter_taps<8>(row + kx0, fr + kx0, acc);
+        switch (xb + 1 - kx0) {  // the row's last taps, without a branch per tap
+            case 1: filter_taps<1>(row + kx0, fr + kx0, acc); break;
+            case 2: filter_taps<2>(row + kx0, fr + kx0, acc); break;
+            case 3: filter_taps<3>(row + kx0, fr + kx0, acc); break;
+            case 4: filter_taps<4>(row + kx0, fr + kx0, acc); break;
+            case 5: filter_taps<5>(row + kx0, fr + kx0, acc); break;
+            case 6: filter_taps<6>(row + kx0, fr + kx0, acc); break;
+            case 7: filter_taps<7>(row + kx0, fr + kx0, acc); break;
+            default: break;
         }
     }
     const bool dn = c + 1 < fx.C && fx.deriv[c + 1];
@@ -430,7 +485,7 @@ __device__ __forceinline__ int filter_item(const FiltCtx &fx, int c, int xg, int
 }
 
 template <bool FILTER>
-__global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__restrict__ img, SmallFilter fg,
+__global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *__restrict__ img, SmallFilter fg,
                                                              const float *__restrict__ filt, float thr,
                                                              const float *__restrict__ inten_in, int N, int T,
                                                              float *__restrict__ inten_out,
@@ -461,19 +516,25 @@ __global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__r
         int *deriv = bbox + 4 * C;  // 1: the exact negation of the channel before, not computed
         int *order = deriv + C;     // computed channels, largest tap area first
         __shared__ int s_ncomp;
-        for (int i = tid; i < C * KK; i += ENC_THREADS) fd[i] = (double)filt[i];
+        // taps and the padded image: each thread issues a batch's global loads
+        // before its LDS stores, so a batch waits for memory once
+        stage_batched(C * KK, [&](int i) { return filt[i]; }, [&](int i, float v) { fd[i] = (double)v; });
         const uint8_t *im = img + (int64_t)b * H * W;
-        for (int i = tid; i < Hs * Wp; i += ENC_THREADS) {
-            const int r = i / Wp, xp = i - r * Wp;
-            const int y = r - p, x = xp - p;
-            sim[i] = (y >= 0 && y < H && x >= 0 && x < W) ? (float)im[y * W + x] : 0.0f;
-        }
+        stage_batched(
+            Hs * Wp,
+            [&](int i) {
+                const int r = i / Wp, xp = i - r * Wp;
+                const int y = r - p, x = xp - p;
+                return (y >= 0 && y < H && x >= 0 && x < W) ? (float)im[y * W + x] : 0.0f;
+            },
+            [&](int i, float v) { sim[i] = v; });
+        const bool order_c = C <= MAX_DERIV_C;  // negated channels and the cost order only then
         __syncthreads();
         // per channel (one wave each): bounding box of the non-zero taps, and
         // whether the taps are the exact negation of the previous channel's
         for (int c = wid; c < C; c += ENC_THREADS / 64) {
             int ya = KF, yb = -1, xa = KF, xb = -1;
-            bool neg = c > 0 && C <= MAX_DERIV_C;
+            bool neg = c > 0 && order_c;
             for (int i = lane; i < KK; i += 64) {
                 const double f = fd[c * KK + i];
                 if (f != 0.0) {
@@ -482,28 +543,43 @@ __global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__r
                 }
                 if (c > 0) neg = neg && (f == -fd[(c - 1) * KK + i]);
             }
-            ya = wave_min_i32(ya); yb = wave_max_i32(yb); xa = wave_min_i32(xa); xb = wave_max_i32(xb);
+            // two reductions of 16-bit pairs: (ya, xa) by min, (yb + 1, xb + 1) by max
+            const uint32_t lo = wave_min_u16x2((uint32_t)ya | ((uint32_t)xa << 16));
+            const uint32_t hi = wave_max_u16x2((uint32_t)(yb + 1) | ((uint32_t)(xb + 1) << 16));
             const bool all_neg = __ballot(!neg) == 0;
             if (lane == 0) {
-                bbox[4 * c] = ya; bbox[4 * c + 1] = yb; bbox[4 * c + 2] = xa; bbox[4 * c + 3] = xb;
+                bbox[4 * c] = (int)(lo & 0xFFFFu); bbox[4 * c + 1] = (int)(hi & 0xFFFFu) - 1;
+                bbox[4 * c + 2] = (int)(lo >> 16); bbox[4 * c + 3] = (int)(hi >> 16) - 1;
                 deriv[c] = all_neg ? 1 : 0;
             }
         }
         __syncthreads();
-        if (tid == 0) {
-            // a negated channel is derived only from a computed one; the computed
-            // channels in decreasing order of tap area (stable), for balance
-            int nc = 0;
-            for (int c = 0; c < C; ++c) {
-                if (c > 0) deriv[c] = deriv[c] && !deriv[c - 1];
-                if (deriv[c]) continue;
-                const int area = tap_area(bbox, c);
-                int k = nc++;
-                if (C <= MAX_DERIV_C)
-                    for (; k > 0 && tap_area(bbox, order[k - 1]) < area; --k) order[k] = order[k - 1];
-                order[k] = c;
+        if (order_c) {
+            if (wid == 0) {  // lane c: channel c
+                // A negated channel is derived only from a computed one: in a run of
+                // channels that each negate the one before, following a channel that
+                // does not, every second one is derived.
+                const bool neg = lane < C && deriv[lane] != 0;
+                const uint64_t upto = lane == 63 ? ~0ull : (2ull << lane) - 1;
+                const int c0 = 63 - __clzll(~__ballot(neg) & upto);  // channel 0 never negates
+                const bool der = neg && ((lane - c0) & 1);
+                // computed channels in decreasing order of tap area, equal areas by index
+                const int area = lane < C && !der ? tap_area(bbox, lane) : -1;
+                int rank = 0;
+                for (int k = 0; k < C; ++k) {
+                    const int ak = __shfl(area, k, 64);
+                    rank += ak > area || (ak == area && k < lane);
+                }
+                if (lane < C) {
+                    deriv[lane] = der ? 1 : 0;
+                    if (!der) order[rank] = lane;
+                }
+                const int nc = __popcll(__ballot(lane < C && !der));
+                if (lane == 0) s_ncomp = nc;
             }
-            s_ncomp = nc;
+        } else {
+            for (int c = tid; c < C; c += ENC_THREADS) order[c] = c;
+            if (tid == 0) s_ncomp = C;
         }
         __syncthreads();
         float *gout = inten_out ? inten_out + (int64_t)b * N : nullptr;
@@ -516,11 +592,21 @@ __global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__r
         }
     } else {
         const float *I = inten_in + (int64_t)b * N;
-        if ((N & 3) == 0) {
-            for (int q = tid; q < N / 4; q += ENC_THREADS) {
-                const float4 v = reinterpret_cast<const float4 *>(I)[q];
-                reinterpret_cast<float4 *>(Ic)[q] = v;
-                npos += (v.x > 0.0f) + (v.y > 0.0f) + (v.z > 0.0f) + (v.w > 0.0f);
+        if ((N & 3) == 0) {  // four float4 loads in flight per thread before its stores
+            const int n4 = N / 4;
+            for (int q0 = tid; q0 < n4; q0 += 4 * ENC_THREADS) {
+                float4 v[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int q = q0 + k * ENC_THREADS;
+                    v[k] = q < n4 ? reinterpret_cast<const float4 *>(I)[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int q = q0 + k * ENC_THREADS;
+                    if (q < n4) reinterpret_cast<float4 *>(Ic)[q] = v[k];
+                    npos += (v[k].x > 0.0f) + (v[k].y > 0.0f) + (v[k].z > 0.0f) + (v[k].w > 0.0f);
+                }
             }
         } else {
             for (int i = tid; i < N; i += ENC_THREADS) {
@@ -538,17 +624,21 @@ __global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__r
 
     uint32_t *hist = reinterpret_cast<uint32_t *>(r2);          // packed 16-bit counters
     uint8_t *tab = r2 + SEL_HIST;  // first digit -> group of this batch's targets (0xFF: none)
-    uint16_t *list[2] = {reinterpret_cast<uint16_t *>(tab + HBINS), reinterpret_cast<uint16_t *>(tab + HBINS) + LCAP};
+    uint16_t *lists = reinterpret_cast<uint16_t *>(tab + HBINS);  // two candidate lists of LCAP entries
     uint64_t *ckey = reinterpret_cast<uint64_t *>(tab + HBINS);  // (aliases the lists) keys of the targets' digits
     // first digit (key bits 43..32) of the positive entries, counted once
     for (int i = tid; i < HBINS / 2; i += ENC_THREADS) hist[i] = 0;
     __syncthreads();
-    for (int i = tid; i < N; i += ENC_THREADS) {
-        const float v = Ic[i];
-        if (v > 0.0f) {
-            const uint32_t d = (uint32_t)(key44(v, i) >> 32);
-            atomicAdd(&hist[d >> 1], 1u << (16 * (d & 1)));
-        }
+    for (int i0 = tid; i0 < N; i0 += 4 * ENC_THREADS) {  // four reads in flight per thread
+        float v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = i0 + k * ENC_THREADS < N ? Ic[i0 + k * ENC_THREADS] : 0.0f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (v[k] > 0.0f) {
+                const uint32_t d = (uint32_t)(key44(v[k], i0 + k * ENC_THREADS) >> 32);
+                atomicAdd(&hist[d >> 1], 1u << (16 * (d & 1)));
+            }
     }
     __syncthreads();
     // thread t holds digits 16t..16t+15: suffix counts S[q] = entries with digit >= 16t+q,
@@ -582,42 +672,46 @@ __global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__r
     }
     for (int j0 = 0; j0 < nb; j0 += SEL_T) {
         const int jn = min(SEL_T, nb - j0);
-        if (tid < jn) {
-            const int64_t r = ((int64_t)(j0 + tid + 1) * n + T - 1) / T;  // ceil((j+1) n / T)
-            trank[0][tid] = (uint32_t)r;
-            tpre[0][tid] = 0;
-        }
-        if (tid == 0) {
-            int m = 0;
-            for (int j = 0; j < jn; ++j) m += ((int64_t)(j0 + j + 1) * n + T - 1) / T < n;
-            s_m = m;  // the targets with an entry at their rank are a prefix (ranks grow with j)
+        if (wid == 0) {  // (j+1) n + T - 1 < 256 * 8192 + 256: 32-bit arithmetic is exact
+            const bool act = lane < jn;
+            const uint32_t r = act ? ((uint32_t)(j0 + lane + 1) * (uint32_t)n + (uint32_t)(T - 1)) / (uint32_t)T : 0u;
+            if (act) {
+                trank[0][lane] = r;  // ceil((j+1) n / T)
+                tpre[0][lane] = 0;
+            }
+            // the targets with an entry at their rank are a prefix (ranks grow with j)
+            const int m = __popcll(__ballot(act && r < (uint32_t)n));
+            if (lane == 0) s_m = m;
         }
         for (int i = tid; i < HBINS / 4; i += ENC_THREADS) reinterpret_cast<uint32_t *>(tab)[i] = 0xFFFFFFFFu;
         __syncthreads();
         const int m = s_m;
         if (m == 0) continue;  // uniform
         {
-            // the target whose rank r satisfies S[16t] > r >= S[16t+16] takes its digit here
-            uint32_t rr[SEL_T];
-#pragma unroll
-            for (int j = 0; j < SEL_T; ++j) rr[j] = trank[0][j];
+            // the target whose rank r satisfies S[16t] > r >= S[16t+16] takes its digit
+            // here; most threads hold none, and those skip the search
+            uint32_t own = 0;
 #pragma unroll
             for (int j = 0; j < SEL_T; ++j) {
-                const uint32_t r = rr[j];
-                if (j < m && S[0] > r && r >= beyond) {
-                    int q = 0;
+                const uint32_t r = trank[0][j];
+                own |= (j < m && S[0] > r && r >= beyond) ? (1u << j) : 0u;
+            }
+            while (own) {
+                const int j = __builtin_ctz(own);
+                own &= own - 1;
+                const uint32_t r = trank[0][j];
+                int q = 0;
 #pragma unroll
-                    for (int k = 1; k < 16; ++k) q += S[k] > r;
-                    uint32_t sq = S[0], nxt = beyond;
+                for (int k = 1; k < 16; ++k) q += S[k] > r;
+                uint32_t sq = S[0], nxt = beyond;
 #pragma unroll
-                    for (int k = 1; k < 16; ++k) {
-                        sq = k == q ? S[k] : sq;
-                        nxt = k == q + 1 ? S[k] : nxt;
-                    }
-                    trank[1][j] = r - nxt;
-                    tpre[1][j] = (uint64_t)(16 * tid + q);
-                    tcnt[j] = sq - nxt;  // entries with this digit
+                for (int k = 1; k < 16; ++k) {
+                    sq = k == q ? S[k] : sq;
+                    nxt = k == q + 1 ? S[k] : nxt;
                 }
+                trank[1][j] = r - nxt;
+                tpre[1][j] = (uint64_t)(16 * tid + q);
+                tcnt[j] = sq - nxt;  // entries with this digit
             }
         }
         __syncthreads();
@@ -640,49 +734,57 @@ __global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__r
                     start += cc[i - 1];
                 }
             tgrp[tid] = g;
-            if (tid == 0 || pp[tid] != pp[tid - 1]) {
+            const uint64_t pt = tpre[1][tid];  // (from LDS: an index into pp or cc by tid would go to scratch)
+            if (tid == 0 || pt != tpre[1][tid - 1]) {
                 gstart[g] = start;
                 gcur[g] = 0;
-                gpre[g] = pp[tid];
-                tab[pp[tid]] = (uint8_t)g;
+                gpre[g] = pt;
+                tab[pt] = (uint8_t)g;
             }
             if (tid == m - 1) {
                 s_ng = g + 1;
-                s_total = (int)(start + cc[tid]);
-                gstart[g + 1] = start + cc[tid];
+                s_total = (int)(start + tcnt[tid]);
+                gstart[g + 1] = start + tcnt[tid];
             }
         }
         __syncthreads();
         if (s_total <= KCAP) {  // uniform: rank the targets' digits' entries directly
             const int total = s_total, ng = s_ng;
-            for (int i = tid; i < N; i += ENC_THREADS) {
-                const float v = Ic[i];
-                if (!(v > 0.0f)) continue;
-                const uint64_t key = key44(v, i);
-                const int g = tab[key >> 32];
-                if (g == 0xFF) continue;
-                ckey[gstart[g] + atomicAdd(&gcur[g], 1u)] = key;
+            for (int i0 = tid; i0 < N; i0 += 4 * ENC_THREADS) {  // four entries in flight per thread
+                float v[4];
+                int g[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) v[k] = i0 + k * ENC_THREADS < N ? Ic[i0 + k * ENC_THREADS] : 0.0f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) g[k] = v[k] > 0.0f ? tab[key44(v[k], i0 + k * ENC_THREADS) >> 32] : 0xFF;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (g[k] != 0xFF)
+                        ckey[gstart[g[k]] + atomicAdd(&gcur[g[k]], 1u)] = key44(v[k], i0 + k * ENC_THREADS);
             }
             __syncthreads();
-            uint32_t rr[SEL_T];
-            int gg[SEL_T];
-#pragma unroll
-            for (int j = 0; j < SEL_T; ++j) {
-                rr[j] = trank[1][j];
-                gg[j] = j < m ? tgrp[j] : -1;
-            }
             // the rank of a key within its digit is the number of larger keys there;
             // the target with that rank takes the key as its boundary
             for (int sl = tid; sl < total; sl += ENC_THREADS) {
                 const uint64_t key = ckey[sl];
                 int g = 0;
-                for (int k = 1; k < ng; ++k) g += sl >= (int)gstart[k];
+#pragma unroll
+                for (int k = 1; k < SEL_T; ++k) g += (k < ng && sl >= (int)gstart[k]) ? 1 : 0;
                 const int e1 = (int)gstart[g + 1];
+                // eight independent reads per step, so that their latencies overlap
                 uint32_t rho = 0;
-                for (int u = (int)gstart[g]; u < e1; ++u) rho += ckey[u] > key;
+                int u = (int)gstart[g];
+                for (; u + 8 <= e1; u += 8) {
+                    uint64_t kk[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) kk[q] = ckey[u + q];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) rho += kk[q] > key;
+                }
+                for (; u < e1; ++u) rho += ckey[u] > key;
 #pragma unroll
                 for (int j = 0; j < SEL_T; ++j)
-                    if (gg[j] == g && rr[j] == rho) kb[j0 + j] = key;
+                    if (j < m && tgrp[j] == g && trank[1][j] == rho) kb[j0 + j] = key;
             }
             __syncthreads();
             continue;
@@ -711,7 +813,7 @@ __global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__r
             const int ng = s_ng;
             const int cnt = src < 0 ? N : s_lc[src];
             for (int k = tid; k < cnt; k += ENC_THREADS) {
-                const int i = src < 0 ? k : (int)list[src][k];
+                const int i = src < 0 ? k : (int)lists[src * LCAP + k];
                 const float v = Ic[i];
                 if (!(v > 0.0f)) continue;
                 const uint64_t key = key44(v, i), pre = key >> (shift + 8);
@@ -727,7 +829,7 @@ __global__ __launch_bounds__(ENC_THREADS) void k_encode_small(const uint8_t *__r
                 atomicAdd(&hist[g * 128 + (d >> 1)], 1u << (16 * (d & 1)));
                 if (pass < 4) {  // a candidate of the next digit
                     const int pos = atomicAdd(&s_lc[dst], 1);
-                    if (pos < LCAP) list[dst][pos] = (uint16_t)i;
+                    if (pos < LCAP) lists[dst * LCAP + pos] = (uint16_t)i;
                 }
             }
             __syncthreads();
