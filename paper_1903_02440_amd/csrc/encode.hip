@@ -57,23 +57,31 @@ __device__ __forceinline__ int wave_max_i32(int v) {
     for (int s = 32; s >= 1; s >>= 1) v = max(v, __shfl_xor(v, s, 64));
     return v;
 }
-// lane-wise min / max of two 16-bit halves over the wave
-__device__ __forceinline__ uint32_t wave_min_u16x2(uint32_t v) {
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) {
-        const uint32_t o = __shfl_xor(v, s, 64);
-        v = min(v & 0xFFFFu, o & 0xFFFFu) | (min(v >> 16, o >> 16) << 16);
-    }
-    return v;
+// Min / max of two 16-bit halves over the wave, by DPP lane moves (no LDS
+// round trips): within quads, eights, rows, then across rows to lane 63, whose
+// value is returned to every lane.  All 64 lanes must be active.
+template <bool MAX>
+__device__ __forceinline__ uint32_t pair_op(uint32_t a, uint32_t b) {
+    const uint32_t l = MAX ? max(a & 0xFFFFu, b & 0xFFFFu) : min(a & 0xFFFFu, b & 0xFFFFu);
+    const uint32_t h = MAX ? max(a >> 16, b >> 16) : min(a >> 16, b >> 16);
+    return l | h << 16;
 }
-__device__ __forceinline__ uint32_t wave_max_u16x2(uint32_t v) {
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) {
-        const uint32_t o = __shfl_xor(v, s, 64);
-        v = max(v & 0xFFFFu, o & 0xFFFFu) | (max(v >> 16, o >> 16) << 16);
-    }
-    return v;
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, CTRL, ROWS, 0xF, false);
 }
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_reduce_u16x2(uint32_t v) {
+    v = pair_op<MAX>(v, dpp_mov<0xB1, 0xF>(v));   // quad_perm [1,0,3,2]
+    v = pair_op<MAX>(v, dpp_mov<0x4E, 0xF>(v));   // quad_perm [2,3,0,1]
+    v = pair_op<MAX>(v, dpp_mov<0x141, 0xF>(v));  // row_half_mirror
+    v = pair_op<MAX>(v, dpp_mov<0x140, 0xF>(v));  // row_mirror
+    v = pair_op<MAX>(v, dpp_mov<0x142, 0xA>(v));  // row_bcast15 into rows 1, 3
+    v = pair_op<MAX>(v, dpp_mov<0x143, 0xC>(v));  // row_bcast31 into rows 2, 3
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+__device__ __forceinline__ uint32_t wave_min_u16x2(uint32_t v) { return wave_reduce_u16x2<false>(v); }
+__device__ __forceinline__ uint32_t wave_max_u16x2(uint32_t v) { return wave_reduce_u16x2<true>(v); }
 
 __global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img, int B, int H, int W,
                                                 const float *__restrict__ filt, int C, int KF, float thr, int R,
@@ -395,10 +403,26 @@ __host__ __device__ inline int small_filter_wp(int W, int KF) {
     const int nxg = (W + 7) / 8;
     return (8 * nxg + KF + 6) | 1;
 }
+// LDS of the filter step (offsets in bytes): the taps as staged (float), which
+// the double form's taps later replace; the zero-padded image as vertical
+// pixel pairs (row r, row r + 1, as int16); the integer form's packed taps;
+// per-channel integers.
+struct SmallFiltLayout {
+    size_t taps, pairs, itaps, ints, total;
+};
+constexpr int SF_INTS = 8;  // per channel: box (4), derived, order, tap offset, tap row stride
+__host__ __device__ inline SmallFiltLayout small_filter_layout(int H, int W, int C, int KF) {
+    const size_t KK = (size_t)KF * KF, img = (size_t)(H + KF - 1) * small_filter_wp(W, KF);
+    SmallFiltLayout L;
+    L.taps = 0;
+    L.pairs = up16(C * KK * sizeof(double));
+    L.itaps = L.pairs + up16(img * sizeof(uint32_t));
+    L.ints = L.itaps + up16((size_t)C * ((KF + 1) / 2) * KF * sizeof(uint32_t));
+    L.total = L.ints + (size_t)SF_INTS * C * sizeof(int);
+    return L;
+}
 __host__ __device__ inline size_t small_filter_bytes(int H, int W, int C, int KF) {
-    const size_t taps = (size_t)C * KF * KF * sizeof(double);
-    const size_t img = (size_t)(H + KF - 1) * small_filter_wp(W, KF) * sizeof(float);
-    return taps + up16(img) + (size_t)6 * C * sizeof(int);
+    return small_filter_layout(H, W, C, KF).total;
 }
 // packed counters (SEL_T groups x 256 digits, or the 4096 first digits, as
 // 16-bit halves), the 12-bit prefix table, two candidate lists
@@ -409,22 +433,23 @@ __device__ __forceinline__ int tap_area(const int *bbox, int c) {
     return max(0, bbox[4 * c + 1] - bbox[4 * c] + 1) * max(0, bbox[4 * c + 3] - bbox[4 * c + 2] + 1);
 }
 struct FiltCtx {
-    int H, W, C, KF, Wp;
+    int H, W, C, Wp;
     float thr;
-    const double *fd;   // taps
-    const float *sim;   // zero-padded image, row stride Wp
-    const int *bbox, *deriv;
-    float *Ic, *gout;   // intensities in LDS, optionally in global memory
+    const uint32_t *pairs;  // zero-padded image as (pixel row r, row r + 1) int16 pairs, row stride Wp
+    const void *taps;      // each computed channel's box of taps: packed pairs, or doubles in rows of stride tstr
+    const int *bbox, *deriv, *toff, *tstr;
+    double scale;          // integer form: 2^-s
+    float *Ic, *gout;      // intensities in LDS, optionally in global memory
 };
 
-// NU consecutive taps of one filter row applied to 8 consecutive outputs: the
-// 8 + NU - 1 pixels under them and the NU taps are all read before the first
-// product, then the products in kx order.
+// Double form: NU consecutive taps of one filter row applied to 8 consecutive
+// outputs; the 8 + NU - 1 pixels under them and the NU taps are all read
+// before the first product, then the products in kx order.
 template <int NU>
-__device__ __forceinline__ void filter_taps(const float *row, const double *fr, double (&acc)[8]) {
+__device__ __forceinline__ void filter_taps(const uint32_t *row, const double *fr, double (&acc)[8]) {
     double a[8 + NU - 1], f[NU];
 #pragma unroll
-    for (int q = 0; q < 8 + NU - 1; ++q) a[q] = (double)row[q];
+    for (int q = 0; q < 8 + NU - 1; ++q) a[q] = (double)(row[q] & 0xFFFFu);  // the pixel of row r
 #pragma unroll
     for (int u = 0; u < NU; ++u) f[u] = fr[u];
 #pragma unroll
@@ -432,32 +457,91 @@ __device__ __forceinline__ void filter_taps(const float *row, const double *fr, 
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[j] = fma(f[u], a[u + j], acc[j]);
 }
-
-// 8 consecutive outputs of row y, columns 8*xg.., of channel c (and of the
-// negated channel after it): double sums in ky-then-kx order over the non-zero
-// taps, one rounding, the threshold.  Returns the number of positive outputs.
-__device__ __forceinline__ int filter_item(const FiltCtx &fx, int c, int xg, int y) {
-    constexpr int CW = 8;
-    const int KK = fx.KF * fx.KF;
-    const int ya = fx.bbox[4 * c], yb = fx.bbox[4 * c + 1], xa = fx.bbox[4 * c + 2], xb = fx.bbox[4 * c + 3];
-    const double *fc = fx.fd + c * KK;
-    double acc[CW];
+// Integer form: NU tap pairs (rows ky, ky + 1 of NU consecutive columns)
+// against the vertical pixel pairs under them, one dot2 per pair and output.
+typedef short short2_t __attribute__((ext_vector_type(2)));
+template <int NU>
+__device__ __forceinline__ void int_taps(const uint32_t *row, const uint32_t *tr, int (&acc)[8]) {
+    uint32_t a[8 + NU - 1], f[NU];
 #pragma unroll
-    for (int j = 0; j < CW; ++j) acc[j] = 0.0;
-    for (int ky = ya; ky <= yb; ++ky) {
-        const float *row = fx.sim + (y + ky) * fx.Wp + CW * xg;
-        const double *fr = fc + ky * fx.KF;
-        int kx0 = xa;
-        for (; kx0 + 8 <= xb + 1; kx0 += 8) filter_taps<8>(row + kx0, fr + kx0, acc);
-        switch (xb + 1 - kx0) {  // the row's last taps, without a branch per tap
-            case 1: filter_taps<1>(row + kx0, fr + kx0, acc); break;
-            case 2: filter_taps<2>(row + kx0, fr + kx0, acc); break;
-            case 3: filter_taps<3>(row + kx0, fr + kx0, acc); break;
-            case 4: filter_taps<4>(row + kx0, fr + kx0, acc); break;
-            case 5: filter_taps<5>(row + kx0, fr + kx0, acc); break;
-            case 6: filter_taps<6>(row + kx0, fr + kx0, acc); break;
-            case 7: filter_taps<7>(row + kx0, fr + kx0, acc); break;
-            default: break;
+    for (int q = 0; q < 8 + NU - 1; ++q) a[q] = row[q];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) f[u] = tr[u];
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            acc[j] = __builtin_amdgcn_sdot2(__builtin_bit_cast(short2_t, a[u + j]), __builtin_bit_cast(short2_t, f[u]),
+                                            acc[j], false);
+}
+// a row of wx taps in chunks of 8 and a last chunk of wx % 8, without a
+// branch per tap
+template <typename P, typename T, typename A, typename F8, typename FR>
+__device__ __forceinline__ void tap_row(const P *row, const T *tr, int wx, A &acc, F8 &&full, FR &&rest) {
+    int u0 = 0;
+    for (; u0 + 8 <= wx; u0 += 8) full(row + u0, tr + u0, acc);
+    rest(wx - u0, row + u0, tr + u0, acc);
+}
+
+// 8 consecutive outputs of row y, columns 8*xg.., of computed channel slot k
+// (channel c, and the negated channel after it when that one is derived), the
+// threshold applied.  Returns the number of positive outputs.
+//  * double form: sums in ky-then-kx order over the channel's box of taps,
+//    one rounding to float;
+//  * integer form: int32 sums of tap 2^s times pixel, exact, times 2^-s and
+//    rounded once to float -- the same value, every partial sum of the
+//    double form being exact for such taps.
+template <bool INT>
+__device__ __forceinline__ int filter_item(const FiltCtx &fx, int k, int c, int xg, int y) {
+    constexpr int CW = 8;
+    const int ya = fx.bbox[4 * c], yb = fx.bbox[4 * c + 1], xa = fx.bbox[4 * c + 2], xb = fx.bbox[4 * c + 3];
+    const int wx = xb - xa + 1;
+    double val[CW];
+    if constexpr (INT) {
+        int acc[CW];
+#pragma unroll
+        for (int j = 0; j < CW; ++j) acc[j] = 0;
+        const uint32_t *tp = reinterpret_cast<const uint32_t *>(fx.taps) + fx.toff[k];
+        for (int ky = ya; ky <= yb; ky += 2) {
+            const uint32_t *row = fx.pairs + (y + ky) * fx.Wp + CW * xg + xa;
+            const uint32_t *tr = tp + ((ky - ya) >> 1) * wx;
+            tap_row(row, tr, wx, acc, [](const uint32_t *r, const uint32_t *t, int(&a)[8]) { int_taps<8>(r, t, a); },
+                    [](int n, const uint32_t *r, const uint32_t *t, int(&a)[8]) {
+                        switch (n) {
+                            case 1: int_taps<1>(r, t, a); break;
+                            case 2: int_taps<2>(r, t, a); break;
+                            case 3: int_taps<3>(r, t, a); break;
+                            case 4: int_taps<4>(r, t, a); break;
+                            case 5: int_taps<5>(r, t, a); break;
+                            case 6: int_taps<6>(r, t, a); break;
+                            case 7: int_taps<7>(r, t, a); break;
+                            default: break;
+                        }
+                    });
+        }
+#pragma unroll
+        for (int j = 0; j < CW; ++j) val[j] = (double)acc[j] * fx.scale;
+    } else {
+#pragma unroll
+        for (int j = 0; j < CW; ++j) val[j] = 0.0;
+        const double *fc = reinterpret_cast<const double *>(fx.taps) + fx.toff[k];
+        const int ts = fx.tstr[k];
+        for (int ky = ya; ky <= yb; ++ky) {
+            const uint32_t *row = fx.pairs + (y + ky) * fx.Wp + CW * xg + xa;
+            tap_row(row, fc + (ky - ya) * ts, wx, val,
+                    [](const uint32_t *r, const double *t, double(&a)[8]) { filter_taps<8>(r, t, a); },
+                    [](int n, const uint32_t *r, const double *t, double(&a)[8]) {
+                        switch (n) {
+                            case 1: filter_taps<1>(r, t, a); break;
+                            case 2: filter_taps<2>(r, t, a); break;
+                            case 3: filter_taps<3>(r, t, a); break;
+                            case 4: filter_taps<4>(r, t, a); break;
+                            case 5: filter_taps<5>(r, t, a); break;
+                            case 6: filter_taps<6>(r, t, a); break;
+                            case 7: filter_taps<7>(r, t, a); break;
+                            default: break;
+                        }
+                    });
         }
     }
     const bool dn = c + 1 < fx.C && fx.deriv[c + 1];
@@ -467,7 +551,7 @@ __device__ __forceinline__ int filter_item(const FiltCtx &fx, int c, int xg, int
     for (int j = 0; j < CW; ++j) {
         const int x = CW * xg + j;
         if (x >= fx.W) break;
-        const float v = (float)acc[j];
+        const float v = (float)val[j];
         const float o = v < fx.thr ? 0.0f : v;
         const int e = (c * fx.H + y) * fx.W + x;
         fx.Ic[e] = o;
@@ -510,52 +594,73 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
     if constexpr (FILTER) {
         const int H = fg.H, W = fg.W, C = fg.C, KF = fg.KF, Wp = fg.Wp, nxg = fg.nxg, KK = KF * KF;
         const int p = (KF - 1) / 2, Hs = H + KF - 1;
-        double *fd = reinterpret_cast<double *>(r2);
-        float *sim = reinterpret_cast<float *>(r2 + (size_t)C * KK * sizeof(double));
-        int *bbox = reinterpret_cast<int *>(reinterpret_cast<unsigned char *>(sim) + up16((size_t)Hs * Wp * sizeof(float)));
+        const SmallFiltLayout L = small_filter_layout(H, W, C, KF);
+        float *ft = reinterpret_cast<float *>(r2 + L.taps);
+        uint32_t *pairs = reinterpret_cast<uint32_t *>(r2 + L.pairs);
+        int *bbox = reinterpret_cast<int *>(r2 + L.ints);
         int *deriv = bbox + 4 * C;  // 1: the exact negation of the channel before, not computed
         int *order = deriv + C;     // computed channels, largest tap area first
-        __shared__ int s_ncomp;
-        // taps and the padded image: each thread issues a batch's global loads
-        // before its LDS stores, so a batch waits for memory once
-        stage_batched(C * KK, [&](int i) { return filt[i]; }, [&](int i, float v) { fd[i] = (double)v; });
+        int *toff = order + C;      // per computed slot: offset of its taps
+        int *tstr = toff + C;       // per computed slot: row stride of its taps (double form)
+        __shared__ int s_ncomp, s_s;
+        __shared__ uint32_t s_ex[MAX_DERIV_C];  // per channel: max fraction bits | (max exponent + 512) << 16
+        // taps and the padded image (as vertical pixel pairs, zero past the last
+        // row): each thread issues a batch's global loads before its LDS stores, so
+        // a batch waits for memory once
+        stage_batched(C * KK, [&](int i) { return filt[i]; }, [&](int i, float v) { ft[i] = v; });
         const uint8_t *im = img + (int64_t)b * H * W;
         stage_batched(
             Hs * Wp,
             [&](int i) {
                 const int r = i / Wp, xp = i - r * Wp;
                 const int y = r - p, x = xp - p;
-                return (y >= 0 && y < H && x >= 0 && x < W) ? (float)im[y * W + x] : 0.0f;
+                const bool in_x = x >= 0 && x < W;
+                const uint32_t lo = in_x && y >= 0 && y < H ? im[y * W + x] : 0u;
+                const uint32_t hi = in_x && y + 1 >= 0 && y + 1 < H ? im[(y + 1) * W + x] : 0u;
+                return __uint_as_float(lo | hi << 16);
             },
-            [&](int i, float v) { sim[i] = v; });
-        const bool order_c = C <= MAX_DERIV_C;  // negated channels and the cost order only then
+            [&](int i, float v) { pairs[i] = __float_as_uint(v); });
+        const bool order_c = C <= MAX_DERIV_C;  // negated channels, cost order and integer form only then
         __syncthreads();
-        // per channel (one wave each): bounding box of the non-zero taps, and
-        // whether the taps are the exact negation of the previous channel's
+        // per channel (one wave each): bounding box of the non-zero taps, whether the
+        // taps are the exact negation of the previous channel's, and the integer
+        // form's statistics (fraction bits and largest binary exponent of the taps)
         for (int c = wid; c < C; c += ENC_THREADS / 64) {
-            int ya = KF, yb = -1, xa = KF, xb = -1;
+            int ya = KF, yb = -1, xa = KF, xb = -1, fb = 0, em = -400;
             bool neg = c > 0 && order_c;
             for (int i = lane; i < KK; i += 64) {
-                const double f = fd[c * KK + i];
-                if (f != 0.0) {
+                const float f = ft[c * KK + i];
+                if (f != 0.0f) {
                     const int ky = i / KF, kx = i - ky * KF;
                     ya = min(ya, ky); yb = max(yb, ky); xa = min(xa, kx); xb = max(xb, kx);
+                    const uint32_t u = __float_as_uint(f), e = (u >> 23) & 255u, m = u & 0x7FFFFFu;
+                    if (e == 255u) {
+                        fb = 4095;  // not finite: the double form
+                    } else {
+                        const uint32_t mm = e ? (m | 0x800000u) : m;
+                        const int e0 = (int)(e ? e : 1u) - 150;  // value = mm * 2^e0
+                        fb = max(fb, -(e0 + (int)__builtin_ctz(mm)));
+                        em = max(em, e0 + 31 - (int)__builtin_clz(mm));
+                    }
                 }
-                if (c > 0) neg = neg && (f == -fd[(c - 1) * KK + i]);
+                if (c > 0) neg = neg && (f == -ft[(c - 1) * KK + i]);
             }
-            // two reductions of 16-bit pairs: (ya, xa) by min, (yb + 1, xb + 1) by max
+            // three reductions of 16-bit pairs: (ya, xa) by min, (yb + 1, xb + 1) and
+            // (fraction bits, exponent + 512) by max
             const uint32_t lo = wave_min_u16x2((uint32_t)ya | ((uint32_t)xa << 16));
             const uint32_t hi = wave_max_u16x2((uint32_t)(yb + 1) | ((uint32_t)(xb + 1) << 16));
+            const uint32_t ex = wave_max_u16x2((uint32_t)max(fb, 0) | ((uint32_t)(em + 512) << 16));
             const bool all_neg = __ballot(!neg) == 0;
             if (lane == 0) {
                 bbox[4 * c] = (int)(lo & 0xFFFFu); bbox[4 * c + 1] = (int)(hi & 0xFFFFu) - 1;
                 bbox[4 * c + 2] = (int)(lo >> 16); bbox[4 * c + 3] = (int)(hi >> 16) - 1;
                 deriv[c] = all_neg ? 1 : 0;
+                if (order_c) s_ex[c] = ex;
             }
         }
         __syncthreads();
-        if (order_c) {
-            if (wid == 0) {  // lane c: channel c
+        if (wid == 0) {
+            if (order_c) {  // lane c: channel c
                 // A negated channel is derived only from a computed one: in a run of
                 // channels that each negate the one before, following a channel that
                 // does not, every second one is derived.
@@ -563,32 +668,96 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
                 const uint64_t upto = lane == 63 ? ~0ull : (2ull << lane) - 1;
                 const int c0 = 63 - __clzll(~__ballot(neg) & upto);  // channel 0 never negates
                 const bool der = neg && ((lane - c0) & 1);
+                const bool comp = lane < C && !der;
                 // computed channels in decreasing order of tap area, equal areas by index
-                const int area = lane < C && !der ? tap_area(bbox, lane) : -1;
-                int rank = 0;
+                const int area = comp ? tap_area(bbox, lane) : -1;
+                // the integer form: every computed tap a multiple of 2^-s, |tap| 2^s <
+                // 2^15, and KK * 255 * 2^(exponent + s + 1) < 2^31 bounds every sum
+                const uint32_t ex = comp ? s_ex[lane] : 0u;
+                const uint32_t exm = wave_max_u16x2(comp ? ex : (uint32_t)(112u << 16));  // (-400 + 512) << 16
+                const int sfb = (int)(exm & 0xFFFFu), sem = (int)(exm >> 16) - 512;
+                const bool exact = sfb <= 126 && sem + sfb <= 14 &&
+                                   (sem + sfb + 1 < 0 || ((int64_t)KK * 255 << (sem + sfb + 1)) < (1LL << 31));
+                const int wy = comp ? bbox[4 * lane + 1] - bbox[4 * lane] + 1 : 0;
+                const int wxl = comp ? bbox[4 * lane + 3] - bbox[4 * lane + 2] + 1 : 0;
+                const int size = area <= 0 ? 0 : exact ? ((wy + 1) >> 1) * wxl : area;
+                int rank = 0, off = 0;
                 for (int k = 0; k < C; ++k) {
-                    const int ak = __shfl(area, k, 64);
-                    rank += ak > area || (ak == area && k < lane);
+                    const int ak = __builtin_amdgcn_readlane(area, k), sk = __builtin_amdgcn_readlane(size, k);
+                    const bool before = ak > area || (ak == area && k < lane);
+                    rank += before;
+                    off += before && ak >= 0 ? sk : 0;
                 }
                 if (lane < C) {
                     deriv[lane] = der ? 1 : 0;
-                    if (!der) order[rank] = lane;
+                    if (comp) {
+                        order[rank] = lane;
+                        toff[rank] = off;
+                        tstr[rank] = wxl;
+                    }
                 }
-                const int nc = __popcll(__ballot(lane < C && !der));
-                if (lane == 0) s_ncomp = nc;
+                const int nc = __popcll(__ballot(comp));
+                if (lane == 0) {
+                    s_ncomp = nc;
+                    s_s = exact ? sfb : -1;
+                }
+            } else {  // every channel computed, in index order, double form with full rows
+                for (int c = lane; c < C; c += 64) {
+                    order[c] = c;
+                    toff[c] = c * KK + max(bbox[4 * c], 0) * KF + max(bbox[4 * c + 2], 0);
+                    tstr[c] = KF;
+                }
+                if (lane == 0) {
+                    s_ncomp = C;
+                    s_s = -1;
+                }
+            }
+        }
+        __syncthreads();
+        const int ncomp = s_ncomp, sexp = s_s;
+        const bool int_form = sexp >= 0;
+        void *taps = r2 + (int_form ? L.itaps : L.taps);
+        if (int_form) {
+            // per computed channel: int16 pairs (tap row ky, ky + 1; zero past the box)
+            for (int k = 0; k < ncomp; ++k) {
+                const int c = order[k], ya = bbox[4 * c], yb = bbox[4 * c + 1], xa = bbox[4 * c + 2];
+                const int wxl = bbox[4 * c + 3] - xa + 1, n = ((yb - ya + 2) >> 1) * wxl;
+                uint32_t *tp = reinterpret_cast<uint32_t *>(taps) + toff[k];
+                for (int e = tid; e < n; e += ENC_THREADS) {
+                    const int kp = e / wxl, u = e - kp * wxl, ky = ya + 2 * kp;
+                    const int q0 = (int)ldexpf(ft[c * KK + ky * KF + xa + u], sexp);
+                    const int q1 = ky + 1 <= yb ? (int)ldexpf(ft[c * KK + (ky + 1) * KF + xa + u], sexp) : 0;
+                    tp[e] = ((uint32_t)q0 & 0xFFFFu) | ((uint32_t)q1 << 16);
+                }
             }
         } else {
-            for (int c = tid; c < C; c += ENC_THREADS) order[c] = c;
-            if (tid == 0) s_ncomp = C;
+            // per computed channel: its box of taps as doubles (whole rows when C is
+            // large), read from global memory since they replace the staged floats
+            double *tp = reinterpret_cast<double *>(taps);
+            for (int k = 0; k < ncomp; ++k) {
+                const int c = order[k];
+                if (order_c) {
+                    const int ya = bbox[4 * c], xa = bbox[4 * c + 2], wxl = tstr[k];
+                    const int n = max(0, (bbox[4 * c + 1] - ya + 1)) * wxl;
+                    for (int e = tid; e < n; e += ENC_THREADS) {
+                        const int r = e / wxl, u = e - r * wxl;
+                        tp[toff[k] + e] = (double)filt[c * KK + (ya + r) * KF + xa + u];
+                    }
+                } else {
+                    for (int e = tid; e < KK; e += ENC_THREADS) tp[c * KK + e] = (double)filt[c * KK + e];
+                }
+            }
         }
         __syncthreads();
         float *gout = inten_out ? inten_out + (int64_t)b * N : nullptr;
-        const FiltCtx fx{H, W, C, KF, Wp, thr, fd, sim, bbox, deriv, Ic, gout};
-        const int per_c = H * nxg, items = s_ncomp * per_c;
+        const FiltCtx fx{H, W, C, Wp, thr, pairs, taps, bbox, deriv, toff, tstr,
+                         int_form ? ldexp(1.0, -sexp) : 1.0, Ic, gout};
+        const int per_c = H * nxg, items = ncomp * per_c;
         for (int it = tid; it < items; it += ENC_THREADS) {
             const int slot = it / per_c, rem = it - slot * per_c;
             const int xg = rem / H, y = rem - xg * H;
-            npos += filter_item(fx, order[slot], xg, y);
+            const int c = order[slot];
+            npos += int_form ? filter_item<true>(fx, slot, c, xg, y) : filter_item<false>(fx, slot, c, xg, y);
         }
     } else {
         const float *I = inten_in + (int64_t)b * N;
