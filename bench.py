@@ -236,7 +236,8 @@ def ops_bench(wl, inp, dev, reps=10):
     algorithmic bytes of the variant ops, on tensors of the workload's first two
     conv stages: local normalisation (radius 8) and the rank-order code of the
     filter map, pointwise inhibition of the second conv's first-spike map (with
-    its wave), and 2x2 pooling of the first conv's potentials."""
+    its wave), and 2x2 pooling of the first conv's potentials; and the whole
+    encoder (filter, rank-order code, t_first and wave) on the workload's images."""
     import torch
     import paper_1903_02440_amd as spk
     from paper_1903_02440_amd.pipeline import chain_for
@@ -255,7 +256,13 @@ def ops_bench(wl, inp, dev, reps=10):
     owave = torch.empty((B, wl.T, C2, H2, W2), dtype=torch.uint8, device=dev)
     pp = spk.spk_pool_potentials(b1["P"], 2)
     NI, N2 = I.numel(), b2["tf"].numel()
+    ewave = torch.empty((I.shape[0], wl.T) + tuple(I.shape[1:]), dtype=torch.uint8, device=dev)
+    etf = torch.empty(I.shape, dtype=torch.uint8, device=dev)
+    ews = torch.empty(spk.spk_encode_latency_workspace_size(*I.shape, wl.T), dtype=torch.uint8, device=dev)
     ops = {
+        "encode_latency": (lambda: spk.spk_encode_latency(ch.image, ch.bank, wl.T, 0.0, wave=ewave, t_first=etf,
+                                                          intensities=False, workspace=ews),
+                           ch.image.numel() + 4 * ch.bank.numel() + (wl.T + 1) * NI),
         "local_normalization_r8": (lambda: spk.spk_local_normalization(I, 8, 1e-12, out=In), 8 * NI),
         "rank_latency": (lambda: spk.spk_rank_latency(In, wl.T, wave=wave, t_first=tfl, workspace=ws),
                          4 * NI + (wl.T + 1) * NI),

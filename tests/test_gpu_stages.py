@@ -459,7 +459,9 @@ ENC_CASES = [("dog", 3, 28, 28, 15, 0.0), ("gabor", 2, 160, 250, 30, 0.0), ("dog
              ("dog", 1, 100, 300, 15, 0.0),  # 13x13 filters on a wide image: bands of rows
              ("float", 3, 28, 28, 15, 0.0),  # general float taps: the sum order decides the bits
              ("float", 2, 9, 13, 30, -0.5),  # ragged width, negative threshold
-             ("flat", 2, 40, 40, 15, 0.0)]  # all intensities equal: the index decides every rank
+             ("flat", 2, 40, 40, 15, 0.0),  # all intensities equal: the index decides every rank
+             ("edge", 2, 28, 28, 15, 0.0),  # integer filter form near its int32 bound; a zero channel
+             ("bound", 2, 20, 24, 15, 0.0)]  # one bit past the integer form's bound: the double form
 
 
 @pytest.mark.parametrize("case", ENC_CASES)
@@ -483,6 +485,21 @@ def test_encode_parity(case):
         bank[3, 2, 2] += np.float32(0.25)
         bank[4] = -bank[3]
         bank[5] = -bank[4]
+    elif kind == "edge":
+        # taps k / 2^10, |k| < 2^14: exponent 3 + 10 fraction bits = 13 <= 14, and
+        # 169 * 255 * 2^14 < 2^31; sums reach ~2^29 on random pixels.  Channel 1 is
+        # all zeros, channel 2 the negation of channel 0 (derived)
+        img = g.integers(0, 256, (B, H, W)).astype(np.uint8)
+        k = g.integers(-16383, 16384, (13, 13))
+        k[6, 6] = 16383
+        bank = np.stack([k / 1024.0, np.zeros((13, 13)), -k / 1024.0]).astype(np.float32)
+    elif kind == "bound":
+        # taps k / 2^11, |k| < 2^15, and one tap k = 2^15 (16.0): one bit past the
+        # integer form's int16 limit, so the double form
+        img = g.integers(0, 256, (B, H, W)).astype(np.uint8)
+        k = g.integers(-32767, 32768, (2, 5, 5))
+        k[1, 2, 2] = 32768
+        bank = (k / 2048.0).astype(np.float32)
     elif kind == "flat":  # a constant image through a 1x1 filter
         img = np.full((B, H, W), 200, np.uint8)
         img[1, :3, :5] = 0
