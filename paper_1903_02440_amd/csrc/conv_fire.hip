@@ -349,6 +349,28 @@ __device__ __forceinline__ void tap_of(const ConvGeom &g, int ks, int gq, int j,
 // ([Cout - n0][Cin][K][K]).
 constexpr int NT = 2;  // 16-bit terms per weight
 
+// Tap j (0..7) of a fragment lane: the weight w (unscaled) into the terms'
+// words t[q][j / 2] (16-bit halves), or t[j / 4][j % 4] as a float (fp32 form).
+__device__ __forceinline__ void split_tap(float w, int j, const WSplit &s, uint32_t (&t)[NT][4]) {
+    const float v = ldexpf(w, s.e);
+    if (s.kind == WK_F32) {  // taps 0-3 in out[0], 4-7 in out[1], as floats
+        t[j >> 2][j & 3] = __float_as_uint(v);
+        return;
+    }
+    uint32_t h[NT];
+    if (s.kind == WK_F16) {
+        const _Float16 hv = (_Float16)v;
+        const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
+        h[0] = __builtin_bit_cast(uint16_t, hv);
+        h[1] = __builtin_bit_cast(uint16_t, (_Float16)rest);
+    } else {
+        h[0] = bf16_bits(v);
+        h[1] = bf16_bits(v - __uint_as_float(h[0] << 16));  // v - hi exact, at most 16 significant bits
+    }
+#pragma unroll
+    for (int q = 0; q < NT; ++q) t[q][j >> 1] |= h[q] << (16 * (j & 1));
+}
+
 __device__ __forceinline__ void split_fragment(const float *w, int n0, const ConvGeom &g, int nt, int ks, int lane,
                                                const WSplit &s, uint4 (&out)[NT]) {
     const int KK = g.K * g.K;
@@ -358,24 +380,8 @@ __device__ __forceinline__ void split_fragment(const float *w, int n0, const Con
     for (int j = 0; j < 8; ++j) {
         int kyx, ci;
         tap_of(g, ks, lane >> 4, j, kyx, ci);
-        float v = 0.0f;
-        if (n < g.Cout && kyx < KK && ci < g.Cin) v = ldexpf(w[((int64_t)(n - n0) * g.Cin + ci) * KK + kyx], s.e);
-        if (s.kind == WK_F32) {  // taps 0-3 in out[0], 4-7 in out[1], as floats
-            t[j >> 2][j & 3] = __float_as_uint(v);
-            continue;
-        }
-        uint32_t h[NT];
-        if (s.kind == WK_F16) {
-            const _Float16 hv = (_Float16)v;
-            const float rest = v - (float)hv;  // exact: hv is within half an fp16 ulp of v
-            h[0] = __builtin_bit_cast(uint16_t, hv);
-            h[1] = __builtin_bit_cast(uint16_t, (_Float16)rest);
-        } else {
-            h[0] = bf16_bits(v);
-            h[1] = bf16_bits(v - __uint_as_float(h[0] << 16));  // v - hi exact, at most 16 significant bits
-        }
-#pragma unroll
-        for (int q = 0; q < NT; ++q) t[q][j >> 1] |= h[q] << (16 * (j & 1));
+        const float v = n < g.Cout && kyx < KK && ci < g.Cin ? w[((int64_t)(n - n0) * g.Cin + ci) * KK + kyx] : 0.0f;
+        split_tap(v, j, s, t);
     }
 #pragma unroll
     for (int q = 0; q < NT; ++q) out[q] = uint4{t[q][0], t[q][1], t[q][2], t[q][3]};
@@ -424,6 +430,82 @@ __global__ __launch_bounds__(256) void k_split_weights(const float *__restrict__
         for (int q = 0; q < NT; ++q) frag[(r * NT + q) * 64 + lane] = t[q];
     }
     if (i < (int64_t)g.ksteps * 4) koff2[i] = koff_of(g, (int)i);
+}
+
+// The same fragments when CP is a multiple of 32 (the cell-contiguous tap
+// order of tap_of): there a fragment lane's 8 taps are 8 consecutive channels
+// of one cell, so the block of channels 8cb..8cb+7 gives, for every cell, the
+// 16 lanes (lane group cb / (CP/32)) of K-step cell * CP/32 + cb % (CP/32).
+// One workgroup per (16-feature tile, channel block): per feature the block's
+// weights (8 channels x KK cells) are contiguous, read coalesced into LDS;
+// each (cell, term) then leaves as 16 consecutive fragment lanes (256 bytes).
+constexpr int SPLIT_CELLS = 64;  // cells per LDS pass
+__global__ __launch_bounds__(256) void k_split_weights_cells(const float *__restrict__ w, ConvGeom g,
+                                                             const unsigned *__restrict__ wmax,
+                                                             const unsigned *__restrict__ wmin, int n_wmax,
+                                                             uint4 *__restrict__ frag, int2 *__restrict__ koff2,
+                                                             float *__restrict__ inv_scale, int *__restrict__ wbf16) {
+    __shared__ float wl[8 * SPLIT_CELLS * 17];  // [channel][cell][feature], rows of 17 (distinct banks)
+    __shared__ unsigned red[8];
+    const uint2 mm = reduce_wrange(wmax, wmin, n_wmax, red);
+    const WSplit ws = weight_split(mm.x, mm.y, 0);
+    const int tid = threadIdx.x, kpc = g.CP / 32, nb = g.CP / 8, KK = g.K * g.K;
+    const int nt = (int)blockIdx.x / nb, cb = (int)blockIdx.x % nb;
+    const int lane0 = (cb / kpc) * 16, m = cb % kpc;
+    if (blockIdx.x == 0) {
+        if (tid == 0) {
+            *inv_scale = ws.inv_s;
+            *wbf16 = ws.kind;
+        }
+        for (int i = tid; i < g.ksteps * 4; i += 256) koff2[i] = koff_of(g, i);
+    }
+    for (int c0 = 0; c0 < KK; c0 += SPLIT_CELLS) {
+        const int nc = min(SPLIT_CELLS, KK - c0), nv = 16 * 8 * nc;
+        // (feature, channel, cell) with the cell fastest: a feature's block is
+        // contiguous in w; eight loads in flight per thread before its stores.
+        // The index i = (f * 8 + j) * nc + cl is carried, not divided out.
+        const int dcl = 256 % nc, dj = (256 / nc) % 8, dfe = 256 / (8 * nc);
+        int cl = tid % nc, j = (tid / nc) % 8, f = tid / (8 * nc);
+        auto step = [&](int &a, int &b, int &c) {
+            a += dcl;
+            if (a >= nc) {
+                a -= nc;
+                ++b;
+            }
+            b += dj;
+            if (b >= 8) {
+                b -= 8;
+                ++c;
+            }
+            c += dfe;
+        };
+        for (int i0 = tid; i0 < nv; i0 += 8 * 256) {
+            float v[8];
+            int a = cl, bb = j, c = f;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int n = nt * 16 + c, ci = cb * 8 + bb;
+                v[u] = i0 + u * 256 < nv && n < g.Cout && ci < g.Cin ? w[((int64_t)n * g.Cin + ci) * KK + c0 + a] : 0.0f;
+                step(a, bb, c);
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                if (i0 + u * 256 < nv) wl[(j * SPLIT_CELLS + cl) * 17 + f] = v[u];
+                step(cl, j, f);
+            }
+        }
+        __syncthreads();
+        for (int i = tid; i < nc * 16; i += 256) {
+            const int cl = i >> 4, f = i & 15;
+            uint32_t t[NT][4] = {};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) split_tap(wl[(j * SPLIT_CELLS + cl) * 17 + f], j, ws, t);
+            const int64_t r = (int64_t)nt * g.ksteps + (c0 + cl) * kpc + m;
+#pragma unroll
+            for (int q = 0; q < NT; ++q) frag[(r * NT + q) * 64 + lane0 + f] = uint4{t[q][0], t[q][1], t[q][2], t[q][3]};
+        }
+        __syncthreads();
+    }
 }
 
 // ------------------------------------------------------------------ shared MFMA helpers
@@ -1544,18 +1626,71 @@ constexpr int INF_PM_OUT = 16384;  // Cout * HoWo at most (the LDS transpose)
 __global__ __launch_bounds__(256) void k_inf_pm_finish(const float *__restrict__ part, ConvGeom g,
                                                        const float *__restrict__ inv_scale, float *__restrict__ P,
                                                        uint8_t *__restrict__ S, uint8_t *__restrict__ TF,
-                                                       float *__restrict__ VF) {
-    extern __shared__ float buf[];  // Cout * HoWo (<= INF_PM_OUT)
+                                                       float *__restrict__ VF, int vec4) {
+    extern __shared__ float buf[];  // Cout rows of HoWo + 1 (odd stride: the transposing stores hit distinct banks)
     const int64_t b = blockIdx.x, plane = (int64_t)g.Cout * g.HoWo;
     const float inv_s = *inv_scale;
-    for (int i = threadIdx.x; i < plane; i += 256) {
-        const int pos = i / g.Cout, f = i - pos * g.Cout;
-        buf[f * g.HoWo + pos] = part[((int64_t)pos * g.B + b) * g.Cout + f];
+    // sixteen loads in flight per thread before its LDS stores (a load followed
+    // at once by its store waits for memory each time); element i = pos * Cout + f
+    // with (pos, f) carried, not divided out
+    constexpr int U = 16;
+    int pos = (int)threadIdx.x / g.Cout, f = (int)threadIdx.x - pos * g.Cout;
+    const int dpos = 256 / g.Cout, df = 256 - dpos * g.Cout;
+    auto step = [&](int &ps, int &ff) {
+        ps += dpos;
+        ff += df;
+        if (ff >= g.Cout) {
+            ff -= g.Cout;
+            ++ps;
+        }
+    };
+    for (int i0 = threadIdx.x; i0 < plane; i0 += U * 256) {
+        float v[U];
+        int ps = pos, ff = f;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            v[u] = i0 + u * 256 < plane ? part[((int64_t)ps * g.B + b) * g.Cout + ff] : 0.0f;
+            step(ps, ff);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (i0 + u * 256 < plane) buf[f * (g.HoWo + 1) + pos] = v[u];
+            step(pos, f);
+        }
     }
     __syncthreads();
     const int64_t o0 = (b * g.T + g.T - 1) * plane, of0 = b * plane;
+    if (vec4) {
+        // four positions of one feature per thread and pass: 16-byte potential and
+        // 4-byte spike / first-spike stores (HoWo a multiple of 4 and the buffers
+        // aligned: checked by the host)
+        const int q4 = g.HoWo / 4;
+        for (int i4 = threadIdx.x; i4 < plane / 4; i4 += 256) {
+            const int fo = i4 / q4, i = 4 * i4;
+            float4 v;
+            v.x = buf[i + fo] * inv_s;
+            v.y = buf[i + fo + 1] * inv_s;
+            v.z = buf[i + fo + 2] * inv_s;
+            v.w = buf[i + fo + 3] * inv_s;
+            const uint32_t fire = (v.x > 0.0f) | (v.y > 0.0f) << 8 | (v.z > 0.0f) << 16 | (uint32_t)(v.w > 0.0f) << 24;
+            if (P) *reinterpret_cast<float4 *>(P + o0 + i) = v;
+            if (S) *reinterpret_cast<uint32_t *>(S + o0 + i) = fire;
+            *reinterpret_cast<uint32_t *>(TF + of0 + i) = (uint32_t)g.T * 0x01010101u - fire;  // T - 1 where fired
+            *reinterpret_cast<float4 *>(VF + of0 + i) = v;
+        }
+        return;
+    }
+    // element i = f * HoWo + q: buf[i + f]
+    const int dq = 256 / g.HoWo, dr = 256 - dq * g.HoWo;
+    int fo = (int)threadIdx.x / g.HoWo, qo = (int)threadIdx.x - fo * g.HoWo;
     for (int i = threadIdx.x; i < plane; i += 256) {
-        const float v = buf[i] * inv_s;
+        const float v = buf[i + fo] * inv_s;
+        fo += dq;
+        qo += dr;
+        if (qo >= g.HoWo) {
+            qo -= g.HoWo;
+            ++fo;
+        }
         const bool fire = v > 0.0f;
         if (P) P[o0 + i] = v;
         if (S) S[o0 + i] = (uint8_t)fire;
@@ -1689,8 +1824,8 @@ void launch_inf(const uint8_t *tpad, const uint4 *frag, const int2 *koff2, const
     if (pm_nib) {
         hipLaunchKernelGGL((k_conv_fire_inf<VEC, true>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad,
                            frag, koff2, g, n_mb, n_ng, ksplit, kpp, pm_nib, part, inv_scale, wbf16, P, S, TF, VF);
-        hipLaunchKernelGGL(k_inf_pm_finish, dim3((unsigned)g.B), dim3(256), (size_t)g.Cout * g.HoWo * sizeof(float), st,
-                           part, g, inv_scale, P, S, TF, VF);
+        hipLaunchKernelGGL(k_inf_pm_finish, dim3((unsigned)g.B), dim3(256), (size_t)g.Cout * (g.HoWo + 1) * sizeof(float), st,
+                           part, g, inv_scale, P, S, TF, VF, VEC ? 1 : 0);
         return;
     }
         hipLaunchKernelGGL((k_conv_fire_inf<VEC, false>), dim3(256), dim3((INF_WAVES + INF_ZW) * 64), lds, st, tpad,
@@ -1887,9 +2022,14 @@ int conv_fire(const uint8_t *wave, bool times, int B, int T, int Cin, int H, int
         hipLaunchKernelGGL(k_pad_first_spike<false>, pad_grid, dim3(256), pad_lds, st, wave, g, rows_per_chunk, nchunk, ny,
                            tpad, weight, nw, wper, wmax, wmin);
     if (inf_mode || !blds) {  // fragments in the workspace (the finite-threshold kernel with LDS room builds its own)
-        const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
-        hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g, wmax,
-                           wmin, n_wmax, frag, koff2, inv_scale, wbf16, arith);
+        if (g.CP % 32 == 0 && arith != 1) {
+            hipLaunchKernelGGL(k_split_weights_cells, dim3((unsigned)(g.ntiles * (g.CP / 8))), dim3(256), 0, st, weight,
+                               g, wmax, wmin, n_wmax, frag, koff2, inv_scale, wbf16);
+        } else {
+            const int64_t n2 = std::max<int64_t>((int64_t)pl.frag_count, (int64_t)pl.koff_count);
+            hipLaunchKernelGGL(k_split_weights, dim3((unsigned)spk::ceil_div(n2, 256)), dim3(256), 0, st, weight, g,
+                               wmax, wmin, n_wmax, frag, koff2, inv_scale, wbf16, arith);
+        }
     }
     if (inf_mode) {
         if (vec)
