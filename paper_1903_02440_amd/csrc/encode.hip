@@ -701,6 +701,26 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
                     s_ncomp = nc;
                     s_s = exact ? sfb : -1;
                 }
+                if (exact) {
+                    // this wave packs the integer form's taps (int16 pairs of tap rows ky,
+                    // ky + 1; zero past the box), slot after slot, while the others wait
+                    uint32_t *itp = reinterpret_cast<uint32_t *>(r2 + L.itaps);
+                    const int bya = comp ? bbox[4 * lane] : 0, byb = comp ? bbox[4 * lane + 1] : 0;
+                    const int bxa = comp ? bbox[4 * lane + 2] : 0;
+                    for (int k = 0; k < nc; ++k) {
+                        const int c = (int)__builtin_ctzll(__ballot(comp && rank == k));  // slot k's channel
+                        const int ya = __builtin_amdgcn_readlane(bya, c), yb = __builtin_amdgcn_readlane(byb, c);
+                        const int xa = __builtin_amdgcn_readlane(bxa, c), wk = __builtin_amdgcn_readlane(wxl, c);
+                        const int n = ((yb - ya + 2) >> 1) * wk;
+                        uint32_t *tp = itp + __builtin_amdgcn_readlane(off, c);
+                        for (int e = lane; e < n; e += 64) {
+                            const int kp = e / wk, u = e - kp * wk, ky = ya + 2 * kp;
+                            const int q0 = (int)ldexpf(ft[c * KK + ky * KF + xa + u], sfb);
+                            const int q1 = ky + 1 <= yb ? (int)ldexpf(ft[c * KK + (ky + 1) * KF + xa + u], sfb) : 0;
+                            tp[e] = ((uint32_t)q0 & 0xFFFFu) | ((uint32_t)q1 << 16);
+                        }
+                    }
+                }
             } else {  // every channel computed, in index order, double form with full rows
                 for (int c = lane; c < C; c += 64) {
                     order[c] = c;
@@ -717,20 +737,7 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
         const int ncomp = s_ncomp, sexp = s_s;
         const bool int_form = sexp >= 0;
         void *taps = r2 + (int_form ? L.itaps : L.taps);
-        if (int_form) {
-            // per computed channel: int16 pairs (tap row ky, ky + 1; zero past the box)
-            for (int k = 0; k < ncomp; ++k) {
-                const int c = order[k], ya = bbox[4 * c], yb = bbox[4 * c + 1], xa = bbox[4 * c + 2];
-                const int wxl = bbox[4 * c + 3] - xa + 1, n = ((yb - ya + 2) >> 1) * wxl;
-                uint32_t *tp = reinterpret_cast<uint32_t *>(taps) + toff[k];
-                for (int e = tid; e < n; e += ENC_THREADS) {
-                    const int kp = e / wxl, u = e - kp * wxl, ky = ya + 2 * kp;
-                    const int q0 = (int)ldexpf(ft[c * KK + ky * KF + xa + u], sexp);
-                    const int q1 = ky + 1 <= yb ? (int)ldexpf(ft[c * KK + (ky + 1) * KF + xa + u], sexp) : 0;
-                    tp[e] = ((uint32_t)q0 & 0xFFFFu) | ((uint32_t)q1 << 16);
-                }
-            }
-        } else {
+        if (!int_form) {  // (the integer form's taps were packed with the order)
             // per computed channel: its box of taps as doubles (whole rows when C is
             // large), read from global memory since they replace the staged floats
             double *tp = reinterpret_cast<double *>(taps);
@@ -747,8 +754,8 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
                     for (int e = tid; e < KK; e += ENC_THREADS) tp[c * KK + e] = (double)filt[c * KK + e];
                 }
             }
+            __syncthreads();  // (uniform)
         }
-        __syncthreads();
         float *gout = inten_out ? inten_out + (int64_t)b * N : nullptr;
         const FiltCtx fx{H, W, C, Wp, thr, pairs, taps, bbox, deriv, toff, tstr,
                          int_form ? ldexp(1.0, -sexp) : 1.0, Ic, gout};
