@@ -82,6 +82,24 @@ __device__ __forceinline__ uint32_t wave_reduce_u16x2(uint32_t v) {
 }
 __device__ __forceinline__ uint32_t wave_min_u16x2(uint32_t v) { return wave_reduce_u16x2<false>(v); }
 __device__ __forceinline__ uint32_t wave_max_u16x2(uint32_t v) { return wave_reduce_u16x2<true>(v); }
+// v plus the DPP-moved value of v (0 where the source lane is outside the
+// row or the lane's row is not in ROWS)
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_add(uint32_t v) {
+    return v + (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, 0xF, false);
+}
+// Inclusive prefix sum over the lanes of the wave (lane 0 first): shifts by 1,
+// 2, 4, 8 within each row of 16, then the totals of earlier rows.  All 64
+// lanes must be active.
+__device__ __forceinline__ uint32_t wave_prefix_sum(uint32_t v) {
+    v = dpp_add<0x111, 0xF>(v);  // row_shr:1
+    v = dpp_add<0x112, 0xF>(v);  // row_shr:2
+    v = dpp_add<0x114, 0xF>(v);  // row_shr:4
+    v = dpp_add<0x118, 0xF>(v);  // row_shr:8
+    v = dpp_add<0x142, 0xA>(v);  // row_bcast15: rows 1, 3 add the row before
+    v = dpp_add<0x143, 0xC>(v);  // row_bcast31: rows 2, 3 add rows 0 and 1
+    return v;
+}
 
 __global__ __launch_bounds__(256) void k_filter(const uint8_t *__restrict__ img, int B, int H, int W,
                                                 const float *__restrict__ filt, int C, int KF, float thr, int R,
@@ -366,7 +384,7 @@ constexpr int ENC_THREADS = 256;
 constexpr int SEL_T = 16;        // boundaries resolved per select batch
 constexpr int HBINS = 4096;      // first digit: 12 bits
 constexpr int LCAP = 1024;       // candidate list capacity (entries)
-constexpr int KCAP = LCAP / 2;   // keys of the targets' first digits ranked directly (same LDS)
+constexpr int KCAP = LCAP;       // 32-bit keys of the targets' first digits ranked directly (same LDS)
 constexpr int MAX_DERIV_C = 64;  // negated-channel detection and cost order for at most this many channels
 
 // Global-to-LDS staging of n elements by one workgroup: a thread loads up to
@@ -792,19 +810,18 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
             }
         }
     }
-    npos = spk::wave_sum_i32(npos);
-    __syncthreads();  // the filter's LDS is free; s_n = 0 is seen by all
-    if (lane == 0) atomicAdd(&s_n, npos);
-    __syncthreads();
-    const int n = s_n, nb = T - 1;
-
     uint32_t *hist = reinterpret_cast<uint32_t *>(r2);          // packed 16-bit counters
     uint8_t *tab = r2 + SEL_HIST;  // first digit -> group of this batch's targets (0xFF: none)
     uint16_t *lists = reinterpret_cast<uint16_t *>(tab + HBINS);  // two candidate lists of LCAP entries
-    uint64_t *ckey = reinterpret_cast<uint64_t *>(tab + HBINS);  // (aliases the lists) keys of the targets' digits
+    // (aliases the lists) key bits 31..0 of the entries with the targets' first digits
+    uint32_t *ckey = reinterpret_cast<uint32_t *>(tab + HBINS);
+    npos = spk::wave_sum_i32(npos);
+    __syncthreads();  // the filter's LDS is free; s_n = 0 is seen by all
+    if (lane == 0) atomicAdd(&s_n, npos);
     // first digit (key bits 43..32) of the positive entries, counted once
     for (int i = tid; i < HBINS / 2; i += ENC_THREADS) hist[i] = 0;
     __syncthreads();
+    const int n = s_n, nb = T - 1;
     for (int i0 = tid; i0 < N; i0 += 4 * ENC_THREADS) {  // four reads in flight per thread
         float v[4];
 #pragma unroll
@@ -829,15 +846,11 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
             S[2 * q + 1] = w >> 16;
             loc += S[2 * q] + S[2 * q + 1];
         }
-        uint32_t suf = loc;  // over this wave's lanes >= lane
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const uint32_t o = __shfl_down(suf, d, 64);
-            if (lane + d < 64) suf += o;
-        }
-        if (lane == 0) s_wsum[wid] = (int)suf;
+        const uint32_t pre = wave_prefix_sum(loc);  // over this wave's lanes <= lane
+        const uint32_t wtot = (uint32_t)__builtin_amdgcn_readlane((int)pre, 63);
+        if (lane == 0) s_wsum[wid] = (int)wtot;
         __syncthreads();
-        uint32_t above = suf - loc;
+        uint32_t above = wtot - pre;  // this wave's lanes > lane
         for (int w = wid + 1; w < ENC_THREADS / 64; ++w) above += (uint32_t)s_wsum[w];
         beyond = above;
 #pragma unroll
@@ -860,6 +873,7 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
             if (lane == 0) s_m = m;
         }
         for (int i = tid; i < HBINS / 4; i += ENC_THREADS) reinterpret_cast<uint32_t *>(tab)[i] = 0xFFFFFFFFu;
+        for (int i = tid; i < KCAP / 4; i += ENC_THREADS) reinterpret_cast<uint4 *>(ckey)[i] = make_uint4(0, 0, 0, 0);
         __syncthreads();
         const int m = s_m;
         if (m == 0) continue;  // uniform
@@ -892,7 +906,8 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
         }
         __syncthreads();
         // The targets' digits, distinct ones numbered g = 0, 1, ... (descending); each
-        // digit's entries get a segment [gstart, gend) of ckey, in that order.
+        // digit's entries get a segment of ckey from gstart[g], in that order, its
+        // length rounded up to a multiple of 8 (the rest stays 0).
         if (tid < m) {
             uint64_t pp[SEL_T];
             uint32_t cc[SEL_T];
@@ -907,7 +922,7 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
             for (int i = 1; i < SEL_T; ++i)
                 if (i <= tid && pp[i] != pp[i - 1]) {
                     ++g;
-                    start += cc[i - 1];
+                    start += (cc[i - 1] + 7u) & ~7u;
                 }
             tgrp[tid] = g;
             const uint64_t pt = tpre[1][tid];  // (from LDS: an index into pp or cc by tid would go to scratch)
@@ -919,8 +934,8 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
             }
             if (tid == m - 1) {
                 s_ng = g + 1;
-                s_total = (int)(start + tcnt[tid]);
-                gstart[g + 1] = start + tcnt[tid];
+                s_total = (int)(start + ((tcnt[tid] + 7u) & ~7u));
+                gstart[g + 1] = (uint32_t)s_total;
             }
         }
         __syncthreads();
@@ -936,31 +951,41 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
 #pragma unroll
                 for (int k = 0; k < 4; ++k)
                     if (g[k] != 0xFF)
-                        ckey[gstart[g[k]] + atomicAdd(&gcur[g[k]], 1u)] = key44(v[k], i0 + k * ENC_THREADS);
+                        ckey[gstart[g[k]] + atomicAdd(&gcur[g[k]], 1u)] = (uint32_t)key44(v[k], i0 + k * ENC_THREADS);
             }
             __syncthreads();
-            // the rank of a key within its digit is the number of larger keys there;
-            // the target with that rank takes the key as its boundary
+            // Within a digit the keys differ in bits 31..0 only, so the rank of a key
+            // there is the number of larger low words; the target with that rank takes
+            // the key as its boundary.  The padding zeros exceed no key.
             for (int sl = tid; sl < total; sl += ENC_THREADS) {
-                const uint64_t key = ckey[sl];
                 int g = 0;
 #pragma unroll
                 for (int k = 1; k < SEL_T; ++k) g += (k < ng && sl >= (int)gstart[k]) ? 1 : 0;
-                const int e1 = (int)gstart[g + 1];
-                // eight independent reads per step, so that their latencies overlap
+                const int g0 = (int)gstart[g], e1 = (int)gstart[g + 1];
+                if (sl - g0 >= (int)gcur[g]) continue;  // padding
+                const uint32_t key = ckey[sl];
+                // eight keys per two 16-byte reads, two steps in flight
+                const uint4 *c4 = reinterpret_cast<const uint4 *>(ckey);
                 uint32_t rho = 0;
-                int u = (int)gstart[g];
-                for (; u + 8 <= e1; u += 8) {
-                    uint64_t kk[8];
+                int u = g0 / 4;
+                const int u1 = e1 / 4;
+                for (; u + 4 <= u1; u += 4) {
+                    uint4 kk[4];
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) kk[q] = ckey[u + q];
+                    for (int q = 0; q < 4; ++q) kk[q] = c4[u + q];
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) rho += kk[q] > key;
+                    for (int q = 0; q < 4; ++q)
+                        rho += (kk[q].x > key) + (kk[q].y > key) + (kk[q].z > key) + (kk[q].w > key);
                 }
-                for (; u < e1; ++u) rho += ckey[u] > key;
+                if (u < u1) {  // 8 keys left
+                    const uint4 ka = c4[u], kc = c4[u + 1];
+                    rho += (ka.x > key) + (ka.y > key) + (ka.z > key) + (ka.w > key);
+                    rho += (kc.x > key) + (kc.y > key) + (kc.z > key) + (kc.w > key);
+                }
+                const uint64_t full = gpre[g] << 32 | key;
 #pragma unroll
                 for (int j = 0; j < SEL_T; ++j)
-                    if (j < m && tgrp[j] == g && trank[1][j] == rho) kb[j0 + j] = key;
+                    if (j < m && tgrp[j] == g && trank[1][j] == rho) kb[j0 + j] = full;
             }
             __syncthreads();
             continue;
@@ -1023,13 +1048,8 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
                 const uint32_t w0 = hist[g * 128 + 2 * lane], w1 = hist[g * 128 + 2 * lane + 1];
                 S[0] = w0 & 0xFFFFu; S[1] = w0 >> 16; S[2] = w1 & 0xFFFFu; S[3] = w1 >> 16;
                 loc = S[0] + S[1] + S[2] + S[3];
-                uint32_t suf = loc;
-#pragma unroll
-                for (int d = 1; d < 64; d <<= 1) {
-                    const uint32_t o = __shfl_down(suf, d, 64);
-                    if (lane + d < 64) suf += o;
-                }
-                const uint32_t beyond = suf - loc;
+                const uint32_t pre = wave_prefix_sum(loc);
+                const uint32_t beyond = (uint32_t)__builtin_amdgcn_readlane((int)pre, 63) - pre;  // lanes > lane
                 uint32_t above = beyond;
 #pragma unroll
                 for (int q = 3; q >= 0; --q) {

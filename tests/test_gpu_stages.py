@@ -371,8 +371,9 @@ KWTA_CASES = [(4, 15, 30, 28, 28, 5, 3), (3, 15, 250, 14, 14, 8, 1), (6, 15, 200
               (3, 15, 40, 1, 1, 4, 0), (2, 15, 7, 1, 9, 3, 1), (2, 15, 300, 10, 10, 8, 2),
               (2, 15, 64, 6, 6, 16, 1), (2, 15, 30, 12, 12, 20, 1), (2, 15, 20, 30, 40, 16, 0),
               # below 8 images the lists come from a grid of (image, feature split) workgroups;
-              # from 8 on from the rounds' own workgroup
-              (1, 15, 250, 14, 14, 8, 1), (8, 15, 250, 14, 14, 8, 1), (9, 15, 30, 28, 28, 5, 3)]
+              # from 8 on from the rounds' own workgroup (1 to 13 feature splits per position)
+              (1, 15, 250, 14, 14, 8, 1), (8, 15, 250, 14, 14, 8, 1), (9, 15, 30, 28, 28, 5, 3),
+              (8, 15, 64, 6, 6, 10, 1), (8, 15, 7, 3, 5, 3, 1), (8, 15, 40, 8, 12, 11, 2)]
 
 
 def kwta_inputs(seed, B, T, C, H, W, ties=True):
@@ -398,7 +399,7 @@ def test_kwta_parity(case, ties):
     assert_equal(host(win), rw, "winners")
 
 
-@pytest.mark.parametrize("case", KWTA_CASES[:2])
+@pytest.mark.parametrize("case", KWTA_CASES[:2] + [(9, 15, 30, 28, 28, 5, 3)])
 def test_kwta_unaligned_inputs(case):
     B, T, C, H, W, k, r = case
     tf, vf = kwta_inputs(C + H + 1, B, T, C, H, W, False)
