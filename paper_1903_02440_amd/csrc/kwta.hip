@@ -41,9 +41,34 @@ struct KwtaGeom {
 };
 
 __device__ __forceinline__ uint64_t kwta_key(int t, float v, uint32_t idx) {
-    uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);  // -0 and +0 are equal potentials
-    u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-    return ((uint64_t)(255 - t) << 56) | ((uint64_t)u << 24) | (uint64_t)(0xFFFFFFu - idx);
+    uint32_t u = __float_as_uint(v);
+    u = u == 0x80000000u ? 0u : u;                        // -0 and +0 are equal potentials
+    u ^= (uint32_t)((int32_t)u >> 31) | 0x80000000u;     // order-preserving: ~u if negative, else u | sign
+    const uint32_t hi = ((uint32_t)(255 - t) << 24) | (u >> 8);
+    const uint32_t lo = (u << 24) | (0xFFFFFFu - idx);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Maximum over the wave by DPP lane moves (the value of lane 63 after moves
+// within quads, half-rows, rows, then across rows), returned to every lane.
+// All 64 lanes must be active.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint64_t max_dpp64(uint64_t v) {
+    const int lo = (int)(uint32_t)v, hi = (int)(uint32_t)(v >> 32);
+    const uint64_t o = ((uint64_t)(uint32_t)__builtin_amdgcn_update_dpp(hi, hi, CTRL, ROWS, 0xF, false) << 32) |
+                       (uint32_t)__builtin_amdgcn_update_dpp(lo, lo, CTRL, ROWS, 0xF, false);
+    return o > v ? o : v;
+}
+__device__ __forceinline__ uint64_t wave_max_u64_dpp(uint64_t v) {
+    v = max_dpp64<0xB1, 0xF>(v);   // quad_perm [1,0,3,2]
+    v = max_dpp64<0x4E, 0xF>(v);   // quad_perm [2,3,0,1]
+    v = max_dpp64<0x141, 0xF>(v);  // row_half_mirror
+    v = max_dpp64<0x140, 0xF>(v);  // row_mirror
+    v = max_dpp64<0x142, 0xA>(v);  // row_bcast15 into rows 1, 3
+    v = max_dpp64<0x143, 0xC>(v);  // row_bcast31 into rows 2, 3
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+    return ((uint64_t)hi << 32) | lo;
 }
 
 __device__ __forceinline__ uint64_t group_max(uint64_t v, int G) {
@@ -412,6 +437,7 @@ constexpr int TOPK_MAX_K = 16;
 constexpr size_t TOPK_LDS = 40 * 1024;  // lists and cursors (the stash adds 16 KB)
 constexpr int TOPK_U = 8;               // feature maps loaded per block
 constexpr int TOPK_STASH_MIN = 64;      // features per split from which the stash pays
+constexpr int TOPK_RP = 4;              // positions per thread up to which the rounds keep their keys in registers
 // Batches below TOPK_PRE_B images (online steps) leave most CUs idle: the
 // lists are then built by a grid of (image, split of the feature maps)
 // workgroups into the workspace, and the rounds' workgroup merges them.
@@ -432,13 +458,12 @@ struct KwtaTopk {
 // checked key > top[KM - 1], so the last entry drops out).
 template <int KM>
 __device__ __forceinline__ void topk_insert(uint64_t (&top)[KM], uint64_t key) {
+    bool gt[KM];  // every comparison first, then the moves
 #pragma unroll
-    for (int i = KM - 1; i > 0; --i) {
-        const bool above = key > top[i - 1];
-        const bool here = key > top[i];
-        top[i] = above ? top[i - 1] : (here ? key : top[i]);
-    }
-    top[0] = key > top[0] ? key : top[0];
+    for (int i = 0; i < KM; ++i) gt[i] = key > top[i];
+#pragma unroll
+    for (int i = KM - 1; i > 0; --i) top[i] = gt[i - 1] ? top[i - 1] : (gt[i] ? key : top[i]);
+    top[0] = gt[0] ? key : top[0];
 }
 
 // Grid (image, split): the KM best keys of every position over the split's
@@ -579,58 +604,127 @@ __global__ __launch_bounds__(TOPK_THREADS_SMALL_B) void k_kwta_topk(const uint8_
             for (int i = 0; i < KM; ++i) lists[(size_t)p * KM + i] = top[i];
         }
     }
-    for (int p = tid; p < HW; p += NT) cur[p] = 0;
-
     int deadf[KM];
 #pragma unroll
     for (int j = 0; j < KM; ++j) deadf[j] = -1;
     int found = 0;
-    for (int round = 0; round < g.k; ++round) {
-        uint64_t m = 0;
-        for (int p = tid; p < HW; p += NT) {
-            int c = cur[p];
-            if (c == 0xFF) continue;  // laterally inhibited
-            const int c0 = c;
-            uint64_t key = 0;
-            for (; c < KM; ++c) {
-                key = lists[(size_t)p * KM + c];
-                if (key == 0) break;
-                const int f = (int)qdiv(0xFFFFFFu - (unsigned)(key & 0xFFFFFFu), g.mHW);
-                bool dead = false;
+    auto feature = [&](uint64_t key) { return (int)qdiv(0xFFFFFFu - (unsigned)(key & 0xFFFFFFu), g.mHW); };
+    auto is_dead = [&](int f) {
+        bool dead = false;
 #pragma unroll
-                for (int j = 0; j < KM; ++j) dead |= deadf[j] == f;
-                if (!dead) break;
-                key = 0;
+        for (int j = 0; j < KM; ++j) dead |= deadf[j] == f;
+        return dead;
+    };
+    if (HW <= TOPK_RP * NT) {  // uniform
+        // Each thread holds the best live key of each of its positions in
+        // registers (0: none, or inhibited).  A round changes it only where the
+        // winner's window covers the position, or where the cached key belongs to
+        // the winner's feature: then the list is walked on to the next entry of a
+        // live feature (the cached key stays the best live one otherwise).
+        uint64_t bk[TOPK_RP];
+        int cc[TOPK_RP], py[TOPK_RP], px[TOPK_RP];
+#pragma unroll
+        for (int i = 0; i < TOPK_RP; ++i) {
+            const int p = tid + i * NT;
+            bk[i] = p < HW ? lists[(size_t)p * KM] : 0;
+            cc[i] = 0;
+            py[i] = (int)qdiv((unsigned)min(p, HW - 1), g.mW);
+            px[i] = min(p, HW - 1) - py[i] * g.W;
+        }
+        for (int round = 0; round < g.k; ++round) {
+            uint64_t m = 0;
+#pragma unroll
+            for (int i = 0; i < TOPK_RP; ++i) m = bk[i] > m ? bk[i] : m;
+            m = wave_max_u64_dpp(m);
+            if (lane == 0) red[round & 1][wv] = m;
+            __syncthreads();
+            uint64_t best = 0;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) best = red[round & 1][w] > best ? red[round & 1][w] : best;
+            if (best == 0) break;  // uniform
+            const int idx = (int)(0xFFFFFFu - (unsigned)(best & 0xFFFFFFu));
+            const int t = 255 - (int)(best >> 56);
+            const int fw = (int)qdiv((unsigned)idx, g.mHW);
+            const int pos = idx - fw * HW;
+            const int yw = (int)qdiv((unsigned)pos, g.mW);
+            const int xw = pos - yw * g.W;
+            if (tid == 0) {
+                win[4 * round + 0] = fw;
+                win[4 * round + 1] = t;
+                win[4 * round + 2] = yw;
+                win[4 * round + 3] = xw;
             }
-            if (c != c0) cur[p] = (uint8_t)c;
-            m = key > m ? key : m;
-        }
-        m = spk::wave_max_u64(m);
-        if (lane == 0) red[round & 1][wv] = m;
-        __syncthreads();
-        uint64_t best = 0;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) best = red[round & 1][w] > best ? red[round & 1][w] : best;
-        if (best == 0) break;  // uniform
-        const int idx = (int)(0xFFFFFFu - (unsigned)(best & 0xFFFFFFu));
-        const int t = 255 - (int)(best >> 56);
-        const int fw = (int)qdiv((unsigned)idx, g.mHW);
-        const int pos = idx - fw * HW;
-        const int yw = (int)qdiv((unsigned)pos, g.mW);
-        const int xw = pos - yw * g.W;
-        if (tid == 0) {
-            win[4 * round + 0] = fw;
-            win[4 * round + 1] = t;
-            win[4 * round + 2] = yw;
-            win[4 * round + 3] = xw;
-        }
+            for (int j = 0; j < KM; ++j)
+                if (j == found) deadf[j] = fw;
+            ++found;
 #pragma unroll
-        for (int j = 0; j < KM; ++j)
-            if (j == found) deadf[j] = fw;
-        ++found;
-        for (int p = tid; p < HW; p += NT) {
-            const int y = (int)qdiv((unsigned)p, g.mW), x = p - y * g.W;
-            if (abs(y - yw) <= g.r && abs(x - xw) <= g.r) cur[p] = 0xFF;
+            for (int i = 0; i < TOPK_RP; ++i) {
+                if (bk[i] == 0) continue;
+                if (abs(py[i] - yw) <= g.r && abs(px[i] - xw) <= g.r) {
+                    bk[i] = 0;
+                    continue;
+                }
+                if (feature(bk[i]) != fw) continue;
+                const int p = tid + i * NT;
+                uint64_t key = 0;
+                for (int c = cc[i] + 1; c < KM; ++c) {
+                    const uint64_t e = lists[(size_t)p * KM + c];
+                    if (e == 0) break;
+                    if (!is_dead(feature(e))) {
+                        key = e;
+                        cc[i] = c;
+                        break;
+                    }
+                }
+                bk[i] = key;
+            }
+        }
+    } else {
+        for (int p = tid; p < HW; p += NT) cur[p] = 0;
+        for (int round = 0; round < g.k; ++round) {
+            uint64_t m = 0;
+            for (int p = tid; p < HW; p += NT) {
+                int c = cur[p];
+                if (c == 0xFF) continue;  // laterally inhibited
+                const int c0 = c;
+                uint64_t key = 0;
+                for (; c < KM; ++c) {
+                    key = lists[(size_t)p * KM + c];
+                    if (key == 0) break;
+                    if (!is_dead(feature(key))) break;
+                    key = 0;
+                }
+                if (c != c0) cur[p] = (uint8_t)c;
+                m = key > m ? key : m;
+            }
+            m = wave_max_u64_dpp(m);
+            if (lane == 0) red[round & 1][wv] = m;
+            __syncthreads();
+            uint64_t best = 0;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) best = red[round & 1][w] > best ? red[round & 1][w] : best;
+            if (best == 0) break;  // uniform
+            const int idx = (int)(0xFFFFFFu - (unsigned)(best & 0xFFFFFFu));
+            const int t = 255 - (int)(best >> 56);
+            const int fw = (int)qdiv((unsigned)idx, g.mHW);
+            const int pos = idx - fw * HW;
+            const int yw = (int)qdiv((unsigned)pos, g.mW);
+            const int xw = pos - yw * g.W;
+            if (tid == 0) {
+                win[4 * round + 0] = fw;
+                win[4 * round + 1] = t;
+                win[4 * round + 2] = yw;
+                win[4 * round + 3] = xw;
+            }
+#pragma unroll
+            for (int j = 0; j < KM; ++j)
+                if (j == found) deadf[j] = fw;
+            ++found;
+            for (int p = tid; p < HW; p += NT) {
+                const int y = (int)qdiv((unsigned)p, g.mW), x = p - y * g.W;
+                if (abs(y - yw) <= g.r && abs(x - xw) <= g.r) cur[p] = 0xFF;
+            }
         }
     }
     if (tid == 0) n_winners[b] = found;
