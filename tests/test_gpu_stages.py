@@ -462,7 +462,10 @@ ENC_CASES = [("dog", 3, 28, 28, 15, 0.0), ("gabor", 2, 160, 250, 30, 0.0), ("dog
              ("float", 2, 9, 13, 30, -0.5),  # ragged width, negative threshold
              ("flat", 2, 40, 40, 15, 0.0),  # all intensities equal: the index decides every rank
              ("edge", 2, 28, 28, 15, 0.0),  # integer filter form near its int32 bound; a zero channel
-             ("bound", 2, 20, 24, 15, 0.0)]  # one bit past the integer form's bound: the double form
+             ("bound", 2, 20, 24, 15, 0.0),  # one bit past the integer form's bound: the double form
+             # the targets' first digits hold 936 and 968 (padded) keys, and 584 and 592: ranked
+             # directly, past the 512 of 64-bit keys the rank step once held
+             ("pos", 2, 16, 24, 15, 0.0), ("noise", 2, 40, 40, 15, 0.0)]
 
 
 @pytest.mark.parametrize("case", ENC_CASES)
@@ -473,6 +476,8 @@ def test_encode_parity(case):
         img, bank = synth.stroke_images(g, B, H, W), synth.dog_bank()
     elif kind == "gabor":
         img, bank = synth.pink_noise_images(g, B, H, W), synth.gabor_bank()
+    elif kind == "noise":
+        img, bank = synth.pink_noise_images(g, B, H, W), synth.dog_bank()
     elif kind == "pos":  # 4 positive filters on a noise image: every entry is ranked
         img = g.integers(1, 256, (B, H, W)).astype(np.uint8)
         bank = (g.integers(1, 65, (4, 3, 3)) / 64.0).astype(np.float32)
