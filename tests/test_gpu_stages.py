@@ -373,7 +373,11 @@ KWTA_CASES = [(4, 15, 30, 28, 28, 5, 3), (3, 15, 250, 14, 14, 8, 1), (6, 15, 200
               # below 8 images the lists come from a grid of (image, feature split) workgroups;
               # from 8 on from the rounds' own workgroup (1 to 13 feature splits per position)
               (1, 15, 250, 14, 14, 8, 1), (8, 15, 250, 14, 14, 8, 1), (9, 15, 30, 28, 28, 5, 3),
-              (8, 15, 64, 6, 6, 10, 1), (8, 15, 7, 3, 5, 3, 1), (8, 15, 40, 8, 12, 11, 2)]
+              (8, 15, 64, 6, 6, 10, 1), (8, 15, 7, 3, 5, 3, 1), (8, 15, 40, 8, 12, 11, 2),
+              # the rounds keep each position's best key in registers when a thread owns at most
+              # 4 positions (256 images: 256 threads, 3 or 4 positions each), else they walk the
+              # lists in LDS every round (65x65 maps: 896 threads, up to 5 positions each)
+              (256, 15, 30, 28, 28, 5, 3), (2, 15, 2, 65, 65, 1, 3)]
 
 
 def kwta_inputs(seed, B, T, C, H, W, ties=True):
