@@ -429,7 +429,8 @@ __global__ __launch_bounds__(SMALL_THREADS) void k_kwta_select_small(const uint8
 // are retired, so a position's best live key is among its first j + 1 list
 // entries: the owner skips entries of retired features with a per-position
 // cursor, and marks its position inhibited when it falls in a winner's
-// window.  Only the per-round maximum crosses threads.
+// window (with at most 4 positions per thread, the cursors and the current
+// best keys live in registers).  Only the per-round maximum crosses threads.
 constexpr int TOPK_THREADS = 256;       // most threads per workgroup
 constexpr int TOPK_THREADS_SMALL_B = 1024;  // most threads per workgroup for batches below TOPK_SMALL_B
 constexpr int TOPK_SMALL_B = 256;
