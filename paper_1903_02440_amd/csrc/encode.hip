@@ -357,26 +357,31 @@ __global__ __launch_bounds__(256) void k_expand_latency(const float *__restrict_
 // ------------------------------------------------------------------ one workgroup per image (small maps)
 // k_encode_small: for C*H*W <= SMALL_MAX one workgroup of ENC_THREADS threads
 // per image keeps the intensity map in LDS and does the whole code there:
-//   1. (FILTER) the filter: the zero-padded image (float) and the taps (double)
-//      in LDS; a work item is (channel, row, group of 8 columns) with the
-//      lanes of a wave on consecutive rows, so their pixel reads fall in
-//      distinct banks (odd row stride), and the channels taken in decreasing
-//      order of their non-zero tap area.  Each output is accumulated in double
-//      in ky-then-kx order over the channel's non-zero taps and rounded once.
+//   1. (FILTER) the filter: the zero-padded image (as vertical pixel pairs)
+//      and the taps in LDS; a work item is (channel, row, group of 8 columns)
+//      with the lanes of a wave on consecutive rows, so their pixel reads fall
+//      in distinct banks (odd row stride), and the channels taken in
+//      decreasing order of their non-zero tap area.  Each output is the sum
+//      over the channel's box of non-zero taps in ky-then-kx order, rounded
+//      once to float: as exact int32 sums of (tap 2^s) * pixel by dot2 when
+//      every tap allows it (the integer form), else accumulated in double.
 //      A channel whose taps are exactly the negated taps of the channel before
 //      it (the on/off pairs of a DoG bank) is not computed: its sum is the
 //      exact negation, so its float is -v (+0 where v is 0).
 //      (!FILTER) the intensities are loaded instead.
 //   2. the T-1 bin boundaries: the keys at ranks ceil((j+1) n / T) of the
 //      positive entries in descending key order, key = float bits << 13 |
-//      (8191 - index) (unique; equal intensities rank in index order), found
-//      by an MSD radix select over the 44 key bits -- a 12-bit digit, then four
-//      8-bit digits -- resolving up to SEL_T boundaries at once, with 16-bit
-//      counters packed in pairs.  A boundary's digit is found by the thread
-//      that holds the digit's suffix count in registers.  The first 8-bit
-//      digit looks the entries' groups up in a table of the 12-bit prefixes;
-//      later digits revisit only the entries that matched (a candidate list,
-//      or all entries when it overflows).
+//      (8191 - index) (unique; equal intensities rank in index order), up to
+//      SEL_T boundaries at once.  The first 12-bit digit (key bits 43..32) of
+//      every positive entry is counted (16-bit counters packed in pairs), and
+//      a boundary's digit is found by the thread that holds the digit's
+//      suffix count in registers.  When the entries with the boundaries'
+//      digits are few (at most KCAP after padding), their low 32 key bits are
+//      gathered per digit and a boundary is the key with the boundary's rank
+//      among them (the number of larger keys).  Otherwise (many ties) an MSD
+//      radix select resolves four more 8-bit digits, each revisiting only the
+//      entries that matched (a candidate list, or all entries when it
+//      overflows).
 //   3. every entry's bin = the number of boundaries its key does not exceed,
 //      i.e. floor(rho T / n) for rank rho (T for entries <= 0); t_first and the
 //      T planes of the wave are written as 4-entry words.
