@@ -126,8 +126,18 @@ __global__ __launch_bounds__(256) void k_pool_first_spike_lds(const uint8_t *__r
     const uint8_t *src = tf + (b * C + c0) * (int64_t)HW;
     const int nbytes = cb * HW;
     if ((((uintptr_t)src) & 3) == 0) {
+        // a thread issues up to 16 word loads before its first LDS store (clamped
+        // indices keep the loads unconditional, so none waits for the one before)
         const int nw = nbytes >> 2;
-        for (int i = threadIdx.x; i < nw; i += 256) plsm[i] = reinterpret_cast<const uint32_t *>(src)[i];
+        const uint32_t *s4 = reinterpret_cast<const uint32_t *>(src);
+        for (int i0 = threadIdx.x; i0 < nw; i0 += 16 * 256) {
+            uint32_t v[16];
+#pragma unroll
+            for (int k = 0; k < 16; ++k) v[k] = s4[min(i0 + k * 256, nw - 1)];
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+                if (i0 + k * 256 < nw) plsm[i0 + k * 256] = v[k];
+        }
         for (int i = (nw << 2) + threadIdx.x; i < nbytes; i += 256) lt[i] = src[i];
     } else {
         for (int i = threadIdx.x; i < nbytes; i += 256) lt[i] = src[i];
