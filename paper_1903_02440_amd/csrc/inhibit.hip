@@ -8,6 +8,8 @@
 
 namespace {
 
+constexpr int PW_U = 8;  // features per block of loads in the pointwise inhibition
+
 // One thread per location of one image (VEC: per 4 consecutive locations,
 // with 4-byte / 16-byte accesses; the map size is then a multiple of 4): the
 // winner over the C features (the kWTA order: earlier spike, then larger
@@ -35,26 +37,45 @@ __global__ __launch_bounds__(256) void k_pointwise(const uint8_t *tf, const floa
         bt[j] = T;
         bv[j] = 0.0f;
     }
-    for (int c = 0; c < C; ++c) {
-        int t[L];
-        float v[L];
-        if (VEC) {
-            const uint32_t t4 = *reinterpret_cast<const uint32_t *>(tf + base + c * HW);
-            const float4 v4 = *reinterpret_cast<const float4 *>(vf + base + c * HW);
-            t[0] = t4 & 255u; t[L > 1 ? 1 : 0] = (t4 >> 8) & 255u;
-            t[L > 2 ? 2 : 0] = (t4 >> 16) & 255u; t[L > 3 ? 3 : 0] = t4 >> 24;
-            v[0] = v4.x; v[L > 1 ? 1 : 0] = v4.y; v[L > 2 ? 2 : 0] = v4.z; v[L > 3 ? 3 : 0] = v4.w;
-        } else {
-            t[0] = tf[base + c * HW];
-            v[0] = vf[base + c * HW];
+    // features in blocks of PW_U, every load of a block issued before the
+    // first is used (clamped feature indices keep them unconditional), in
+    // increasing feature order so that strict comparisons keep the lower index
+    for (int c0 = 0; c0 < C; c0 += PW_U) {
+        uint32_t tw[PW_U];
+        float4 vw[PW_U];
+#pragma unroll
+        for (int u = 0; u < PW_U; ++u) {
+            const int64_t o = base + (int64_t)min(c0 + u, C - 1) * HW;
+            if (VEC) {
+                tw[u] = *reinterpret_cast<const uint32_t *>(tf + o);
+                vw[u] = *reinterpret_cast<const float4 *>(vf + o);
+            } else {
+                tw[u] = tf[o];
+                vw[u].x = vf[o];
+            }
         }
 #pragma unroll
-        for (int j = 0; j < L; ++j)
-            if (t[j] < T && (best[j] < 0 || t[j] < bt[j] || (t[j] == bt[j] && v[j] > bv[j]))) {
-                best[j] = c;
-                bt[j] = t[j];
-                bv[j] = v[j];
+        for (int u = 0; u < PW_U; ++u) {
+            const int c = c0 + u;
+            if (c >= C) break;
+            int t[L];
+            float v[L];
+            t[0] = tw[u] & 255u;
+            v[0] = vw[u].x;
+            if (VEC) {
+                t[L > 1 ? 1 : 0] = (tw[u] >> 8) & 255u;
+                t[L > 2 ? 2 : 0] = (tw[u] >> 16) & 255u;
+                t[L > 3 ? 3 : 0] = tw[u] >> 24;
+                v[L > 1 ? 1 : 0] = vw[u].y; v[L > 2 ? 2 : 0] = vw[u].z; v[L > 3 ? 3 : 0] = vw[u].w;
             }
+#pragma unroll
+            for (int j = 0; j < L; ++j)
+                if (t[j] < T && (best[j] < 0 || t[j] < bt[j] || (t[j] == bt[j] && v[j] > bv[j]))) {
+                    best[j] = c;
+                    bt[j] = t[j];
+                    bv[j] = v[j];
+                }
+        }
     }
     // the surviving first-spike times of feature c, 4 to a word
     auto word = [&](int c) {
@@ -76,31 +97,44 @@ __global__ __launch_bounds__(256) void k_pointwise(const uint8_t *tf, const floa
         }
     }
     const int64_t plane = (int64_t)C * HW;
-    if (wave)
-        for (int t = 0; t < T; ++t) {
-            uint8_t *w = wave + (b * T + t) * plane + p;
-            for (int c = 0; c < C; ++c) {
-                if (VEC) *reinterpret_cast<uint32_t *>(w + c * HW) = spk::spikes4(word(c), t, T);
-                else w[c * HW] = (uint8_t)(c == best[0] && t >= bt[0]);
+    if (wave)  // feature by feature: its surviving times once, then its T steps
+        for (int c = 0; c < C; ++c) {
+            uint8_t *w = wave + b * T * plane + (int64_t)c * HW + p;
+            if (VEC) {
+                const uint32_t wc = word(c);
+                for (int t = 0; t < T; ++t) *reinterpret_cast<uint32_t *>(w + t * plane) = spk::spikes4(wc, t, T);
+            } else {
+                const int tc = c == best[0] ? bt[0] : T;
+                for (int t = 0; t < T; ++t) w[t * plane] = (uint8_t)(t >= tc);
             }
         }
     if (pot)
         for (int t = 0; t < T; ++t) {
             float *pp = pot + (b * T + t) * plane + p;
-            for (int c = 0; c < C; ++c) {
-                if (VEC) {
-                    if (c == best[0] && c == best[L > 1 ? 1 : 0] && c == best[L > 2 ? 2 : 0] &&
-                        c == best[L > 3 ? 3 : 0])
-                        continue;  // the feature survives at all four locations
-                    float4 x = *reinterpret_cast<const float4 *>(pp + c * HW);
-                    if (c != best[0]) x.x = 0.0f;
-                    if (c != best[L > 1 ? 1 : 0]) x.y = 0.0f;
-                    if (c != best[L > 2 ? 2 : 0]) x.z = 0.0f;
-                    if (c != best[L > 3 ? 3 : 0]) x.w = 0.0f;
-                    *reinterpret_cast<float4 *>(pp + c * HW) = x;
-                } else if (c != best[0]) {
-                    pp[c * HW] = 0.0f;
+            if constexpr (VEC) {
+                // blocks of PW_U features: the loads first (clamped), then the masked stores
+                for (int c0 = 0; c0 < C; c0 += PW_U) {
+                    float4 xw[PW_U];
+#pragma unroll
+                    for (int u = 0; u < PW_U; ++u)
+                        xw[u] = *reinterpret_cast<const float4 *>(pp + (int64_t)min(c0 + u, C - 1) * HW);
+#pragma unroll
+                    for (int u = 0; u < PW_U; ++u) {
+                        const int c = c0 + u;
+                        if (c >= C) break;
+                        if (c == best[0] && c == best[1] && c == best[2] && c == best[3])
+                            continue;  // the feature survives at all four locations
+                        float4 x = xw[u];
+                        if (c != best[0]) x.x = 0.0f;
+                        if (c != best[1]) x.y = 0.0f;
+                        if (c != best[2]) x.z = 0.0f;
+                        if (c != best[3]) x.w = 0.0f;
+                        *reinterpret_cast<float4 *>(pp + (int64_t)c * HW) = x;
+                    }
                 }
+            } else {
+                for (int c = 0; c < C; ++c)
+                    if (c != best[0]) pp[c * HW] = 0.0f;
             }
         }
 }
