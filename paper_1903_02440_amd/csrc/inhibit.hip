@@ -161,6 +161,28 @@ __global__ __launch_bounds__(256) void k_pool_potentials(const float *__restrict
     out[o] = m;
 }
 
+// 2x2 windows, stride 2, no padding, W a multiple of 4, Wo even, aligned
+// tensors: one thread per two adjacent outputs, from one 16-byte load of each
+// of the two input rows; the same comparisons in the same window order.
+__global__ __launch_bounds__(256) void k_pool_potentials_2x2(const float *__restrict__ pot, uint32_t pairs, int H,
+                                                             int W, int Ho, int Wo, float *__restrict__ out) {
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= pairs) return;
+    const uint32_t hw2 = (uint32_t)(Ho * Wo) / 2, wo2 = (uint32_t)Wo / 2;
+    const uint32_t pl = i / hw2, r = i - pl * hw2, yo = r / wo2, x2 = r - yo * wo2;
+    const float *src = pot + (size_t)pl * H * W + (size_t)(2 * yo) * W + 4 * x2;
+    const float4 a = *reinterpret_cast<const float4 *>(src), c = *reinterpret_cast<const float4 *>(src + W);
+    auto win = [](float v00, float v01, float v10, float v11) {
+        float m = v00;
+        if (v01 > m) m = v01;
+        if (v10 > m) m = v10;
+        if (v11 > m) m = v11;
+        return m;
+    };
+    *reinterpret_cast<float2 *>(out + (size_t)pl * Ho * Wo + (size_t)yo * Wo + 2 * x2) =
+        float2{win(a.x, a.y, c.x, c.y), win(a.z, a.w, c.z, c.w)};
+}
+
 }  // namespace
 
 extern "C" int spk_pointwise_inhibition(const uint8_t *t_first, const float *v_first, int B, int T, int C, int H,
@@ -198,6 +220,14 @@ extern "C" int spk_pool_potentials(const float *potentials, int B, int T, int C,
     SPK_REQUIRE(potentials && out, SPK_E_ARG, "spk_pool_potentials: potentials and out are required");
     const int64_t total = (int64_t)B * T * C * Ho * Wo;
     SPK_REQUIRE(spk::ceil_div(total, 256) < (1LL << 31), SPK_E_RANGE, "spk_pool_potentials: too large");
+    const bool al16 = ((uintptr_t)potentials & 15) == 0 && ((uintptr_t)out & 7) == 0;
+    if (kernel == 2 && stride == 2 && pad == 0 && W % 4 == 0 && Wo % 2 == 0 && Ho == H / 2 && al16 &&
+        total / 2 < (1LL << 32) && (int64_t)B * T * C * H * W < (1LL << 32)) {
+        const int64_t pairs = total / 2;
+        hipLaunchKernelGGL(k_pool_potentials_2x2, dim3((unsigned)spk::ceil_div(pairs, 256)), dim3(256), 0,
+                           spk::as_stream(stream), potentials, (uint32_t)pairs, H, W, Ho, Wo, out);
+        return spk::check_launch("spk_pool_potentials");
+    }
     hipLaunchKernelGGL(k_pool_potentials, dim3((unsigned)spk::ceil_div(total, 256)), dim3(256), 0,
                        spk::as_stream(stream), potentials, total, H, W, kernel, stride, pad, Ho, Wo, out);
     return spk::check_launch("spk_pool_potentials");

@@ -348,8 +348,12 @@ def test_pointwise_inhibition_parity(case):
     assert_equal(host(iv), rv, "v_first in place")
 
 
+# 2x2 windows of stride 2 on widths that are multiples of 4 take 16-byte loads of
+# two rows (the 28x28 map; an odd height, whose last row no window covers); the
+# rest one output per thread
 @pytest.mark.parametrize("case", [(2, 15, 30, 28, 28, 2, 2, 0), (2, 15, 250, 14, 14, 3, 3, 0),
-                                  (1, 5, 4, 9, 11, 3, 2, 1), (1, 3, 2, 7, 7, 4, 3, 2), (2, 4, 3, 5, 6, 1, 1, 0)])
+                                  (1, 5, 4, 9, 11, 3, 2, 1), (1, 3, 2, 7, 7, 4, 3, 2), (2, 4, 3, 5, 6, 1, 1, 0),
+                                  (2, 3, 5, 9, 12, 2, 2, 0), (1, 2, 3, 6, 10, 2, 2, 0)])
 def test_pool_potentials_parity(case):
     B, T, C, H, W, P, R, D = case
     g = synth.rng(800 + P + C, 0)
