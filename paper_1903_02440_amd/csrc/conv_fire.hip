@@ -143,11 +143,14 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
         const int part = (int)blockIdx.x - nchunk * ny;
         const int64_t i1 = min(nw, (int64_t)(part + 1) * wper);
         unsigned m = 0, mn = 0xFFFFFFFFu;
-        // four independent loads per thread and pass
+        // four independent loads per thread and pass (at clamped indices, so that
+        // none sits behind a branch that waits for it; the clamped ones count 0)
         for (int64_t i0 = (int64_t)part * wper + tid; i0 < i1; i0 += 1024) {
             float v[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = i0 + 256 * j < i1 ? w[i0 + 256 * j] : 0.0f;
+            for (int j = 0; j < 4; ++j) v[j] = w[min(i0 + 256 * j, i1 - 1)];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = i0 + 256 * j < i1 ? v[j] : 0.0f;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const unsigned b = __float_as_uint(fabsf(v[j]));
@@ -197,7 +200,7 @@ __global__ __launch_bounds__(256) void k_pad_first_spike(const uint8_t *__restri
             for (int i0 = tid; i0 < nwd; i0 += 8 * 256) {
                 uint32_t v[8];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) v[u] = i0 + 256 * u < nwd ? s4[i0 + 256 * u] : 0u;
+                for (int u = 0; u < 8; ++u) v[u] = s4[min(i0 + 256 * u, nwd - 1)];  // (clamped: unconditional)
 #pragma unroll
                 for (int u = 0; u < 8; ++u)
                     if (i0 + 256 * u < nwd) r4[i0 + 256 * u] = v[u];
