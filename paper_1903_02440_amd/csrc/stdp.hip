@@ -149,30 +149,44 @@ __global__ __launch_bounds__(256) void k_stdp_bits(const uint8_t *__restrict__ p
         const uint64_t m = __ballot(neg);
         if (threadIdx.x == 0) w.sbits[r] = (uint32_t)m;
     }
+    // the row's updates, read once into LDS (entries past the row repeat its last)
+    __shared__ int4 s_lst[32];
+    if (threadIdx.x < 32) s_lst[threadIdx.x] = w.list[(int64_t)f * a.B + u0 + min((int)threadIdx.x, cnt - 1)];
+    __syncthreads();
     const int KK = a.K * a.K, Kc = a.Cin * KK;
     const int e = blockIdx.x * 256 + threadIdx.x;
     if (e >= Kc) return;
     const int ci = e / KK, ky = (e % KK) / a.K, kx = e % a.K;
     const int64_t plane = (int64_t)a.Cin * a.H * a.W, cioff = (int64_t)ci * a.H * a.W;
-    const int4 *lst = w.list + (int64_t)f * a.B + u0;
-    uint8_t v[32];
-#pragma unroll
-    for (int q = 0; q < 32; ++q) {
-        v[q] = 0;
-        if (q < cnt) {
-            const int4 u = lst[q];
-            const int iy = u.z * a.stride + ky - a.pad, ix = u.w * a.stride + kx - a.pad;
-            if (iy >= 0 && iy < a.H && ix >= 0 && ix < a.W) {
-                if (a.times)  // Eq.1: the wave is 1 at step t_i exactly where t_first <= t_i
-                    v[q] = pre[(int64_t)u.x * plane + cioff + (int64_t)iy * a.W + ix] <= u.y;
-                else
-                    v[q] = pre[((int64_t)u.x * a.T + u.y) * plane + cioff + (int64_t)iy * a.W + ix];
-            }
-        }
-    }
+    // two halves of 16 updates: every byte load of a half is issued before any
+    // is used (updates past the row or in the padding load byte 0 of the input
+    // and count 0), so that none waits behind a branch
     uint32_t word = 0;
 #pragma unroll
-    for (int q = 0; q < 32; ++q) word |= (uint32_t)(v[q] != 0) << q;
+    for (int h = 0; h < 2; ++h) {
+        int64_t off[16];
+        int lim[16];
+        bool ok[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int q = 16 * h + j;
+            const int4 u = s_lst[q];  // (cnt >= 1: the row holds an update)
+            const int iy = u.z * a.stride + ky - a.pad, ix = u.w * a.stride + kx - a.pad;
+            ok[j] = q < cnt && iy >= 0 && iy < a.H && ix >= 0 && ix < a.W;
+            const int64_t img = a.times ? (int64_t)u.x : (int64_t)u.x * a.T + u.y;
+            off[j] = ok[j] ? img * plane + cioff + (int64_t)iy * a.W + ix : 0;
+            lim[j] = u.y;
+        }
+        uint8_t v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = pre[off[j]];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            // Eq.1 for a first-spike input: the wave is 1 at step t_i exactly where t_first <= t_i
+            const bool bit = ok[j] && (a.times ? (int)v[j] <= lim[j] : v[j] != 0);
+            word |= (uint32_t)bit << (16 * h + j);
+        }
+    }
     w.bits[(int64_t)r * Kc + e] = word;
 }
 
