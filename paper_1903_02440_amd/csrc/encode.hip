@@ -398,12 +398,13 @@ constexpr int MAX_DERIV_C = 64;  // negated-channel detection and cost order for
 constexpr int STAGE_U = 8;
 template <typename Load, typename Store>
 __device__ __forceinline__ void stage_batched(int n, Load ld, Store stv) {
+    using V = decltype(ld(0));
     for (int i0 = threadIdx.x; i0 < n; i0 += STAGE_U * ENC_THREADS) {
-        float v[STAGE_U];
+        V v[STAGE_U];
 #pragma unroll
         for (int k = 0; k < STAGE_U; ++k) {
             const int i = i0 + k * ENC_THREADS;
-            v[k] = i < n ? ld(i) : 0.0f;
+            v[k] = i < n ? ld(i) : V{};
         }
 #pragma unroll
         for (int k = 0; k < STAGE_U; ++k) {
@@ -640,9 +641,13 @@ __global__ __launch_bounds__(ENC_THREADS, 4) void k_encode_small(const uint8_t *
                 const bool in_x = x >= 0 && x < W;
                 const uint32_t lo = in_x && y >= 0 && y < H ? im[y * W + x] : 0u;
                 const uint32_t hi = in_x && y + 1 >= 0 && y + 1 < H ? im[(y + 1) * W + x] : 0u;
-                return __uint_as_float(lo | hi << 16);
+                return uint2{lo, hi};  // (combined at the store: a use here would wait for the load)
             },
-            [&](int i, float v) { pairs[i] = __float_as_uint(v); });
+            [&](int i, uint2 v) {
+                uint32_t hi = v.y;
+                asm volatile("" : "+v"(hi));  // keeps the shift here, out of the load's branch
+                pairs[i] = v.x | hi << 16;
+            });
         const bool order_c = C <= MAX_DERIV_C;  // negated channels, cost order and integer form only then
         __syncthreads();
         // per channel (one wave each): bounding box of the non-zero taps, whether the
